@@ -1,0 +1,350 @@
+/*
+ * oracle.c -- plain, slow, obviously-correct CPU reference for block-quantized
+ * linear layers.  TEST INFRASTRUCTURE ONLY: nothing in the product library may
+ * link, load or call this file.  Only the test-suite, the smoke check and the
+ * CPU-baseline leg of the benchmark use it.  It shares no code, header, table
+ * or helper with the HIP implementation.
+ *
+ * What it computes (paper section 4, Table 3: the runtime is evaluated with
+ * 8-bit and 4-bit quantized C++ configurations; section 3.2, "latency-first
+ * fused execution", puts those quantized linear layers on the batch-1 path):
+ *
+ *   y[m][n] = sum_k x[m][k] * w_hat[n][k],   w_hat = dequant(quant(W))
+ *
+ * with the weights stored in the ggml-style Q8_0 / Q4_0 block formats:
+ * blocks of 32 consecutive weights along k (the input-feature axis of W[n][k]),
+ * each block carrying one IEEE binary16 scale.
+ *
+ *   Q8_0 block (34 bytes): d16 (little-endian binary16), then 32 int8 codes.
+ *     amax = max_j |x_j|;  d32 = fl32(amax / 127);  d16 = binary16_RNE(d32)
+ *     q_j  = clamp(round_half_away_from_zero(x_j / d16), -127, 127)
+ *            (0 for every j when d16 == 0)
+ *   Q4_0 block (18 bytes): d16, then 16 bytes of packed 4-bit codes.
+ *     m = the signed element of largest magnitude (first index on ties,
+ *         starting from +0.0);  d32 = fl32(m / -8);  d16 = binary16_RNE(d32)
+ *     c_j = clamp(floor(x_j / d16 + 1/2), -8, 7)   (0 when d16 == 0)
+ *     nibble_j = c_j + 8;  byte i (0..15) = nibble_i | nibble_{i+16} << 4
+ *   Dequant: w_hat = q * d16 (Q8_0) or (nibble - 8) * d16 (Q4_0), exact in
+ *   binary64.
+ *
+ * Readings taken where the format description is silent (each is listed with
+ * its reason in the design notes of the repository):
+ *   - codes are rounded against the *stored* binary16 scale d16, so that every
+ *     element satisfies |x - w_hat| <= |d16|/2 (saturated Q4_0 codes and
+ *     underflowed scales excepted);
+ *   - ties: Q8_0 rounds half away from zero, Q4_0 rounds half up;
+ *   - x / d16 is evaluated in binary64: x has 24 significant bits and d16 at
+ *     most 11, so the binary64 quotient can neither create nor destroy a tie
+ *     and every rounding decision equals the one on the exact quotient.
+ *
+ * Matmul: every product and sum in binary64, in plain k order, one output at
+ * a time.  Alongside y it returns bound[m][n] = sum_k |x[m][k]| * |w_hat[n][k]|,
+ * the scale against which an fp32-accumulating implementation's error is
+ * normalised.  Threads (pthreads) only split the set of outputs; each output
+ * is still one sequential binary64 loop.
+ *
+ * Build: gcc -O2 -fno-fast-math -ffp-contract=off -shared -fPIC -pthread
+ */
+#include <math.h>
+#include <pthread.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORACLE_OK 0
+#define ORACLE_EINVAL (-1)
+
+#define ORACLE_Q8_0 1
+#define ORACLE_Q4_0 2
+
+#define ORACLE_X_F16 1
+#define ORACLE_X_BF16 2
+
+#define QK 32
+
+/* ---------------------------------------------------------------------- */
+/* binary16 / bfloat16 encode and decode, written from the IEEE 754 formats */
+/* ---------------------------------------------------------------------- */
+
+/* binary16: 1 sign bit, 5 exponent bits (bias 15), 10 fraction bits. */
+double oracle_half_to_double(uint16_t h) {
+  int sign = (h >> 15) & 1;
+  int e = (h >> 10) & 0x1f;
+  int f = h & 0x3ff;
+  double v;
+  if (e == 0x1f) {
+    v = f ? NAN : INFINITY;
+  } else if (e == 0) {
+    v = ldexp((double)f, -24); /* subnormal: f * 2^-24 */
+  } else {
+    v = ldexp((double)(1024 + f), e - 25); /* (1 + f/1024) * 2^(e-15) */
+  }
+  return sign ? -v : v;
+}
+
+/* bfloat16: the upper 16 bits of an IEEE binary32. */
+double oracle_bf16_to_double(uint16_t b) {
+  int sign = (b >> 15) & 1;
+  int e = (b >> 7) & 0xff;
+  int f = b & 0x7f;
+  double v;
+  if (e == 0xff) {
+    v = f ? NAN : INFINITY;
+  } else if (e == 0) {
+    v = ldexp((double)f, -133); /* subnormal: f * 2^-126 * 2^-7 */
+  } else {
+    v = ldexp((double)(128 + f), e - 134); /* (1 + f/128) * 2^(e-127) */
+  }
+  return sign ? -v : v;
+}
+
+/* Round a binary32 value to the nearest binary16, ties to even (the IEEE 754
+ * default rounding), with gradual underflow and overflow to infinity. */
+uint16_t oracle_float_to_half_rne(float f) {
+  double a = fabs((double)f);
+  uint16_t sign = signbit(f) ? 0x8000u : 0u;
+  if (isnan(f)) return (uint16_t)(sign | 0x7e00u);
+  if (isinf(f)) return (uint16_t)(sign | 0x7c00u);
+  if (a == 0.0) return sign;
+  /* a lies in [2^E, 2^(E+1)); the binary16 spacing there is 2^(E-10), and
+   * below the normal range (E < -14) it stays 2^-24. */
+  int e2;
+  (void)frexp(a, &e2);
+  int E = e2 - 1;
+  if (E < -14) E = -14;
+  double spacing = ldexp(1.0, E - 10);
+  double r = rint(a / spacing); /* a/spacing is exact; rint = ties-to-even */
+  double v = r * spacing;       /* exact */
+  if (v > 65504.0) return (uint16_t)(sign | 0x7c00u);
+  uint16_t bits;
+  if (v < ldexp(1.0, -14)) {
+    bits = (uint16_t)(v * ldexp(1.0, 24)); /* subnormal fraction */
+  } else {
+    int ev;
+    double m = frexp(v, &ev); /* v = m * 2^ev, m in [0.5, 1) */
+    int biased = ev - 1 + 15;
+    int frac = (int)((2.0 * m - 1.0) * 1024.0);
+    bits = (uint16_t)((biased << 10) | frac);
+  }
+  return (uint16_t)(sign | bits);
+}
+
+/* ---------------------------------------------------------------------- */
+/* Quantization to the canonical (array-of-blocks) byte layout             */
+/* ---------------------------------------------------------------------- */
+
+static void put_d16(uint8_t *dst, uint16_t d16) {
+  dst[0] = (uint8_t)(d16 & 0xff);
+  dst[1] = (uint8_t)(d16 >> 8);
+}
+
+static uint16_t get_d16(const uint8_t *src) {
+  return (uint16_t)(src[0] | (src[1] << 8));
+}
+
+static void quantize_block_q8_0(const float *x, uint8_t *blk) {
+  float amax = 0.0f;
+  for (int j = 0; j < QK; ++j) {
+    float a = fabsf(x[j]);
+    if (a > amax) amax = a;
+  }
+  float d32 = amax / 127.0f;
+  uint16_t d16 = oracle_float_to_half_rne(d32);
+  double d = oracle_half_to_double(d16);
+  put_d16(blk, d16);
+  for (int j = 0; j < QK; ++j) {
+    int q = 0;
+    if (d != 0.0) {
+      double t = round((double)x[j] / d); /* round() = half away from zero */
+      if (t > 127.0) t = 127.0;
+      if (t < -127.0) t = -127.0;
+      q = (int)t;
+    }
+    blk[2 + j] = (uint8_t)(int8_t)q;
+  }
+}
+
+static void quantize_block_q4_0(const float *x, uint8_t *blk) {
+  float amax = 0.0f, m = 0.0f;
+  for (int j = 0; j < QK; ++j) {
+    float a = fabsf(x[j]);
+    if (a > amax) {
+      amax = a;
+      m = x[j];
+    }
+  }
+  float d32 = m / -8.0f;
+  uint16_t d16 = oracle_float_to_half_rne(d32);
+  double d = oracle_half_to_double(d16);
+  put_d16(blk, d16);
+  int nib[QK];
+  for (int j = 0; j < QK; ++j) {
+    int c = 0;
+    if (d != 0.0) {
+      double t = floor((double)x[j] / d + 0.5); /* round half up */
+      if (t > 7.0) t = 7.0;
+      if (t < -8.0) t = -8.0;
+      c = (int)t;
+    }
+    nib[j] = c + 8;
+  }
+  for (int i = 0; i < QK / 2; ++i) blk[2 + i] = (uint8_t)(nib[i] | (nib[i + QK / 2] << 4));
+}
+
+int64_t oracle_block_bytes(int qtype) {
+  if (qtype == ORACLE_Q8_0) return 2 + QK;
+  if (qtype == ORACLE_Q4_0) return 2 + QK / 2;
+  return -1;
+}
+
+/* w: fp32 [n][k] row-major; out: n * (k/32) canonical blocks, row by row. */
+int oracle_quantize(int qtype, const float *w, int64_t n, int64_t k, uint8_t *out) {
+  int64_t bb = oracle_block_bytes(qtype);
+  if (bb < 0 || n < 0 || k < 0 || k % QK != 0 || (!w && n * k) || (!out && n * k))
+    return ORACLE_EINVAL;
+  int64_t nb = k / QK;
+  for (int64_t r = 0; r < n; ++r)
+    for (int64_t b = 0; b < nb; ++b) {
+      const float *src = w + r * k + b * QK;
+      uint8_t *dst = out + (r * nb + b) * bb;
+      if (qtype == ORACLE_Q8_0)
+        quantize_block_q8_0(src, dst);
+      else
+        quantize_block_q4_0(src, dst);
+    }
+  return ORACLE_OK;
+}
+
+/* ---------------------------------------------------------------------- */
+/* Dequantization                                                          */
+/* ---------------------------------------------------------------------- */
+
+static double code_at(int qtype, const uint8_t *blk, int j) {
+  if (qtype == ORACLE_Q8_0) return (double)(int8_t)blk[2 + j];
+  int byte = blk[2 + (j % (QK / 2))];
+  int nibble = (j < QK / 2) ? (byte & 0x0f) : (byte >> 4);
+  return (double)(nibble - 8);
+}
+
+/* One row of w_hat (k values) from the row's nb = k/32 blocks. */
+static void dequant_row(int qtype, const uint8_t *row_blocks, int64_t k, double *dst) {
+  int64_t bb = oracle_block_bytes(qtype);
+  for (int64_t b = 0; b < k / QK; ++b) {
+    const uint8_t *blk = row_blocks + b * bb;
+    double d = oracle_half_to_double(get_d16(blk));
+    for (int j = 0; j < QK; ++j) dst[b * QK + j] = code_at(qtype, blk, j) * d;
+  }
+}
+
+int oracle_dequant(int qtype, const uint8_t *blocks, int64_t n, int64_t k, double *w_hat) {
+  int64_t bb = oracle_block_bytes(qtype);
+  if (bb < 0 || n < 0 || k < 0 || k % QK != 0) return ORACLE_EINVAL;
+  for (int64_t r = 0; r < n; ++r) dequant_row(qtype, blocks + r * (k / QK) * bb, k, w_hat + r * k);
+  return ORACLE_OK;
+}
+
+/* ---------------------------------------------------------------------- */
+/* Linear layer in binary64                                                */
+/* ---------------------------------------------------------------------- */
+
+typedef struct {
+  int qtype;
+  const uint8_t *blocks;
+  int64_t k;
+  const double *xd; /* [m][k] decoded activations */
+  int64_t m;
+  const int64_t *cols; /* output columns (rows of W) to compute */
+  int64_t ncols;
+  double *y, *bound; /* [m][ncols] */
+  int64_t begin, end; /* slice of cols for this worker */
+} job_t;
+
+static void *run_job(void *arg) {
+  job_t *J = (job_t *)arg;
+  int64_t bb = oracle_block_bytes(J->qtype);
+  double *wrow = (double *)malloc(sizeof(double) * (size_t)(J->k ? J->k : 1));
+  if (!wrow) return (void *)1;
+  for (int64_t c = J->begin; c < J->end; ++c) {
+    int64_t n = J->cols[c];
+    dequant_row(J->qtype, J->blocks + n * (J->k / QK) * bb, J->k, wrow);
+    for (int64_t i = 0; i < J->m; ++i) {
+      const double *xr = J->xd + i * J->k;
+      double s = 0.0, b = 0.0;
+      for (int64_t kk = 0; kk < J->k; ++kk) {
+        double p = xr[kk] * wrow[kk];
+        s += p;
+        b += fabs(p);
+      }
+      J->y[i * J->ncols + c] = s;
+      J->bound[i * J->ncols + c] = b;
+    }
+  }
+  free(wrow);
+  return NULL;
+}
+
+/*
+ * y[i][c], bound[i][c] for i < m and c < ncols, output column cols[c] (a row
+ * index of W in [0, n)).  x holds raw binary16 or bfloat16 words [m][k].
+ * nthreads <= 1 runs on the calling thread.
+ */
+int oracle_qlinear(int qtype, const uint8_t *blocks, int64_t n, int64_t k, const uint16_t *x,
+                   int xdtype, int64_t m, const int64_t *cols, int64_t ncols, double *y,
+                   double *bound, int nthreads) {
+  if (oracle_block_bytes(qtype) < 0 || k <= 0 || k % QK != 0 || n <= 0 || m < 0 || ncols < 0)
+    return ORACLE_EINVAL;
+  if (xdtype != ORACLE_X_F16 && xdtype != ORACLE_X_BF16) return ORACLE_EINVAL;
+  for (int64_t c = 0; c < ncols; ++c)
+    if (cols[c] < 0 || cols[c] >= n) return ORACLE_EINVAL;
+  if (m == 0 || ncols == 0) return ORACLE_OK;
+  double *xd = (double *)malloc(sizeof(double) * (size_t)(m * k));
+  if (!xd) return ORACLE_EINVAL;
+  for (int64_t i = 0; i < m * k; ++i)
+    xd[i] = (xdtype == ORACLE_X_F16) ? oracle_half_to_double(x[i]) : oracle_bf16_to_double(x[i]);
+
+  if (nthreads < 1) nthreads = 1;
+  if (nthreads > ncols) nthreads = (int)ncols;
+  job_t *jobs = (job_t *)calloc((size_t)nthreads, sizeof(job_t));
+  pthread_t *tids = (pthread_t *)calloc((size_t)nthreads, sizeof(pthread_t));
+  int rc = ORACLE_OK;
+  if (!jobs || !tids) {
+    rc = ORACLE_EINVAL;
+    goto done;
+  }
+  for (int t = 0; t < nthreads; ++t) {
+    job_t *J = &jobs[t];
+    J->qtype = qtype;
+    J->blocks = blocks;
+    J->k = k;
+    J->xd = xd;
+    J->m = m;
+    J->cols = cols;
+    J->ncols = ncols;
+    J->y = y;
+    J->bound = bound;
+    J->begin = ncols * t / nthreads;
+    J->end = ncols * (t + 1) / nthreads;
+  }
+  if (nthreads == 1) {
+    if (run_job(&jobs[0])) rc = ORACLE_EINVAL;
+  } else {
+    int started = 0;
+    for (int t = 0; t < nthreads; ++t) {
+      if (pthread_create(&tids[t], NULL, run_job, &jobs[t]) != 0) {
+        rc = ORACLE_EINVAL;
+        break;
+      }
+      ++started;
+    }
+    for (int t = 0; t < started; ++t) {
+      void *ret = NULL;
+      pthread_join(tids[t], &ret);
+      if (ret) rc = ORACLE_EINVAL;
+    }
+  }
+done:
+  free(jobs);
+  free(tids);
+  free(xd);
+  return rc;
+}
