@@ -1,0 +1,187 @@
+/*
+ * eb.h -- C ABI of libeb: linear layers on block-quantized weights for
+ * batch-1 embodied-model inference on AMD Instinct MI355X (gfx950).
+ *
+ * The operation is the quantized linear layer that the paper's runtime runs
+ * in its backbone and head plugins (paper section 3.2, "latency-first fused
+ * execution": operator fusion, backend-specific dispatch, buffer reuse and
+ * graph replay for batch-1 inference) at the 8-bit and 4-bit C++
+ * configurations it evaluates (section 4, Table 3):
+ *
+ *     y[m][n] = sum_k x[m][k] * w_hat[n][k],   w_hat = dequant(quant(W))
+ *
+ * Weight formats (ggml-style blocks of 32 consecutive weights along k, each
+ * with one IEEE binary16 scale d16):
+ *   EB_Q8_0: amax = max|w_j|, d16 = binary16_RNE(fl32(amax / 127)),
+ *            q_j = clamp(round_half_away(w_j / d16), -127, 127); w_hat = q * d16.
+ *   EB_Q4_0: m = signed element of largest |w_j| (first index wins),
+ *            d16 = binary16_RNE(fl32(m / -8)),
+ *            c_j = clamp(floor(w_j / d16 + 1/2), -8, 7); w_hat = c * d16.
+ *   When d16 == 0 every code is 0.  Codes are rounded against the stored
+ *   binary16 scale, exactly (the rounding decision equals the one on the exact
+ *   quotient).
+ *
+ * Canonical byte layout (array of blocks, row by row, k/32 blocks per row):
+ *   Q8_0 block, 34 bytes: d16 little-endian, then q_0..q_31 as int8.
+ *   Q4_0 block, 18 bytes: d16, then 16 bytes, byte i = (c_i + 8) | (c_{i+16} + 8) << 4.
+ *
+ * Device layout ("planar", what eb_quantize_* write and eb_qlinear reads),
+ * inside one buffer of eb_qweights_bytes(type, n, k) bytes:
+ *   qs plane at offset 0: row r, block b at byte (r * (k/32) + b) * QB, where
+ *     QB = 32 (Q8_0, the 32 int8 codes) or 16 (Q4_0, the 16 packed bytes in
+ *     the canonical order);
+ *   d plane at byte offset d_off = round_up(n * (k/32) * QB, 256): row r, block
+ *     b at binary16 index r * DS + b, DS = round_up(k/32, 8); entries b >= k/32
+ *     are zero.
+ *   It holds the canonical bytes, rearranged; eb_qweights_to_canonical /
+ *   eb_qweights_from_canonical convert in either direction.
+ *
+ * Conventions for every entry point:
+ *   - All pointers are DEVICE pointers unless stated otherwise; the caller owns
+ *     every buffer (weights, activations, outputs).  The library never
+ *     allocates device memory and never synchronises the stream.
+ *   - Work is enqueued on `stream` (0 = the null stream); EB_OK means the work
+ *     was enqueued, not that it finished.
+ *   - Arguments are validated on the host before anything is launched; on any
+ *     error nothing is launched and the output buffers are untouched.
+ *   - Inputs must be finite.  Quantization requires max|w| / 127 <= 65504 per
+ *     block (the binary16 scale must not overflow).
+ *   - Outputs must not overlap inputs.
+ *   - Sizes: 1 <= n <= 2^31 - 1, 32 <= k <= 2^24 with k % 32 == 0,
+ *     0 <= m <= 2^24 (m == 0 is a no-op).
+ *   - Thread-compatible: concurrent calls must use different output buffers.
+ */
+#ifndef EB_H
+#define EB_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t eb_status;
+#define EB_OK 0
+#define EB_ERR_INVALID (-1)     /* bad size, null pointer, bad enum value */
+#define EB_ERR_ALIGN (-2)       /* pointer not aligned as required */
+#define EB_ERR_UNSUPPORTED (-3) /* valid but unsupported combination (dtype pair, path) */
+#define EB_ERR_HIP (-4)         /* the HIP runtime reported an error (no device, launch failure) */
+
+/* quantization formats */
+#define EB_Q8_0 1
+#define EB_Q4_0 2
+
+/* element types */
+#define EB_F32 0
+#define EB_F16 1
+#define EB_BF16 2
+
+/* kernel paths for eb_qlinear_ex */
+#define EB_PATH_AUTO 0 /* pick by m, qtype and shape (measured crossover) */
+#define EB_PATH_GEMV 1 /* bandwidth-bound GEMV, requires m <= 4 and m * k <= 65536 */
+#define EB_PATH_MFMA 2 /* LDS-tiled dequantize-to-16-bit + MFMA, any m */
+
+/* A quantized weight matrix W[n][k] in the planar device layout above.
+ * `data` is a device pointer, 256-byte aligned, eb_qweights_bytes(type, n, k)
+ * bytes; it is owned by the caller. */
+typedef struct {
+  int32_t type; /* EB_Q8_0 or EB_Q4_0 */
+  int32_t reserved; /* must be 0 */
+  int64_t n;    /* output features (rows of W) */
+  int64_t k;    /* input features (columns of W), multiple of 32 */
+  void *data;
+} eb_qweights;
+
+/* Byte offsets of the planar layout (all values in bytes except d_stride). */
+typedef struct {
+  int64_t qs_offset;     /* always 0 */
+  int64_t qs_row_bytes;  /* (k/32) * QB */
+  int64_t d_offset;      /* start of the binary16 scale plane */
+  int64_t d_stride;      /* scale-plane row stride in binary16 elements (DS) */
+  int64_t total_bytes;   /* == eb_qweights_bytes */
+  int64_t canonical_bytes; /* n * (k/32) * (2 + QB), size of the canonical form */
+} eb_layout;
+
+/* One linear layer of a stack: y[m][n] = x[m][k] . w_hat^T. */
+typedef struct {
+  eb_qweights w;
+  const void *x; /* device, [m][k] of x_type, row-major, 16-byte aligned */
+  void *y;       /* device, [m][n] of y_type, row-major, 16-byte aligned */
+  int64_t m;
+  int32_t x_type; /* EB_F16 or EB_BF16 */
+  int32_t y_type; /* EB_F32 or EB_BF16 */
+} eb_qlinear_op;
+
+/* Library version string (static storage). */
+const char *eb_version(void);
+
+/* Human-readable name of a status code (static storage; never NULL). */
+const char *eb_status_str(eb_status s);
+
+/* Size in bytes of the planar device buffer for W[n][k] of format `type`
+ * (a multiple of 256), or 0 if the arguments are invalid. Host-only. */
+size_t eb_qweights_bytes(int32_t type, int64_t n, int64_t k);
+
+/* Fills *out with the planar layout of W[n][k]. Host-only.
+ * EB_ERR_INVALID on bad type/sizes or out == NULL. */
+eb_status eb_qweights_layout(int32_t type, int64_t n, int64_t k, eb_layout *out);
+
+/* Quantize fp32 W[n][k] (device, row-major, 16-byte aligned) into the planar
+ * Q8_0 layout at `out` (device, 256-byte aligned, eb_qweights_bytes bytes).
+ * Bit-exact with the definition above.  n == 0 is a no-op.
+ * EB_ERR_INVALID: null pointer with n > 0, n < 0, k % 32 != 0 or out-of-range size.
+ * EB_ERR_ALIGN: w not 16-byte aligned or out not 256-byte aligned. */
+eb_status eb_quantize_q8_0(const float *w, int64_t n, int64_t k, void *out, hipStream_t stream);
+
+/* Same as eb_quantize_q8_0 for the Q4_0 format. */
+eb_status eb_quantize_q4_0(const float *w, int64_t n, int64_t k, void *out, hipStream_t stream);
+
+/* Write the canonical array-of-blocks bytes of *w into `dst` (device,
+ * eb_layout.canonical_bytes bytes, no alignment requirement). */
+eb_status eb_qweights_to_canonical(const eb_qweights *w, void *dst, hipStream_t stream);
+
+/* Build the planar layout at `out` (device, 256-byte aligned,
+ * eb_qweights_bytes bytes) from canonical blocks at `src` (device). */
+eb_status eb_qweights_from_canonical(int32_t type, const void *src, int64_t n, int64_t k,
+                                     void *out, hipStream_t stream);
+
+/* y[m][n] = x[m][k] . w_hat[n][k]^T with fp32 accumulation, on the path chosen
+ * automatically.  x: device [m][k] of x_type (EB_F16 or EB_BF16); y: device
+ * [m][n] of y_type (EB_F32 or EB_BF16, bf16 rounded to nearest even).
+ * No bias.  Accuracy: |y - y_exact| <= 2e-3 * sum_k |x||w_hat| per output
+ * (plus the bf16 output rounding when y_type is EB_BF16).
+ * EB_ERR_INVALID: w or its data NULL, bad type/sizes, x/y NULL with m > 0.
+ * EB_ERR_ALIGN: x or y not 16-byte aligned, w->data not 256-byte aligned.
+ * EB_ERR_UNSUPPORTED: other dtypes. EB_ERR_HIP: launch failure. */
+eb_status eb_qlinear(const eb_qweights *w, const void *x, int32_t x_type, int64_t m, void *y,
+                     int32_t y_type, hipStream_t stream);
+
+/* eb_qlinear with an explicit kernel path (EB_PATH_*), for crossover
+ * measurement and tests.  EB_ERR_UNSUPPORTED if the forced path cannot run
+ * this shape (EB_PATH_GEMV with m > 4 or m * k > 65536). */
+eb_status eb_qlinear_ex(const eb_qweights *w, const void *x, int32_t x_type, int64_t m, void *y,
+                        int32_t y_type, int32_t path, hipStream_t stream);
+
+/* Which path EB_PATH_AUTO takes for this problem (host-only, no launch). */
+int32_t eb_qlinear_auto_path(int32_t type, int32_t x_type, int64_t m, int64_t n, int64_t k);
+
+/* Run ops[0..n_ops) in order on `stream`, each exactly as eb_qlinear would
+ * (paper section 3.2, graph replay and buffer reuse).  `ops` is a HOST array.
+ * The first call with a given op list records the launches into a HIP graph
+ * (captured on a library-owned stream); later calls with an identical list
+ * (same pointers, sizes and types) replay it with one graph launch.  All ops
+ * are validated before anything is enqueued.  n_ops == 0 is a no-op.
+ * Set the environment variable EB_STACK_GRAPH=0 to launch the ops directly. */
+eb_status eb_qlinear_stack(const eb_qlinear_op *ops, int32_t n_ops, hipStream_t stream);
+
+/* Drop every cached stack graph (frees their host/driver resources). */
+eb_status eb_stack_cache_clear(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EB_H */

@@ -197,22 +197,63 @@ int64_t oracle_block_bytes(int qtype) {
   return -1;
 }
 
-/* w: fp32 [n][k] row-major; out: n * (k/32) canonical blocks, row by row. */
-int oracle_quantize(int qtype, const float *w, int64_t n, int64_t k, uint8_t *out) {
-  int64_t bb = oracle_block_bytes(qtype);
-  if (bb < 0 || n < 0 || k < 0 || k % QK != 0 || (!w && n * k) || (!out && n * k))
-    return ORACLE_EINVAL;
-  int64_t nb = k / QK;
-  for (int64_t r = 0; r < n; ++r)
+typedef struct {
+  int qtype;
+  const float *w;
+  int64_t k;
+  uint8_t *out;
+  int64_t begin, end; /* rows for this worker */
+} qjob_t;
+
+static void *run_qjob(void *arg) {
+  qjob_t *J = (qjob_t *)arg;
+  int64_t bb = oracle_block_bytes(J->qtype);
+  int64_t nb = J->k / QK;
+  for (int64_t r = J->begin; r < J->end; ++r)
     for (int64_t b = 0; b < nb; ++b) {
-      const float *src = w + r * k + b * QK;
-      uint8_t *dst = out + (r * nb + b) * bb;
-      if (qtype == ORACLE_Q8_0)
+      const float *src = J->w + r * J->k + b * QK;
+      uint8_t *dst = J->out + (r * nb + b) * bb;
+      if (J->qtype == ORACLE_Q8_0)
         quantize_block_q8_0(src, dst);
       else
         quantize_block_q4_0(src, dst);
     }
-  return ORACLE_OK;
+  return NULL;
+}
+
+/* w: fp32 [n][k] row-major; out: n * (k/32) canonical blocks, row by row.
+ * Threads (nthreads <= 1: the calling thread) only split the rows. */
+int oracle_quantize(int qtype, const float *w, int64_t n, int64_t k, uint8_t *out, int nthreads) {
+  int64_t bb = oracle_block_bytes(qtype);
+  if (bb < 0 || n < 0 || k < 0 || k % QK != 0 || (!w && n * k) || (!out && n * k))
+    return ORACLE_EINVAL;
+  if (nthreads < 1) nthreads = 1;
+  if (nthreads > n) nthreads = n > 0 ? (int)n : 1;
+  qjob_t jobs[256];
+  pthread_t tids[256];
+  if (nthreads > 256) nthreads = 256;
+  for (int t = 0; t < nthreads; ++t) {
+    jobs[t].qtype = qtype;
+    jobs[t].w = w;
+    jobs[t].k = k;
+    jobs[t].out = out;
+    jobs[t].begin = n * t / nthreads;
+    jobs[t].end = n * (t + 1) / nthreads;
+  }
+  if (nthreads == 1) {
+    run_qjob(&jobs[0]);
+    return ORACLE_OK;
+  }
+  int started = 0, rc = ORACLE_OK;
+  for (int t = 0; t < nthreads; ++t) {
+    if (pthread_create(&tids[t], NULL, run_qjob, &jobs[t]) != 0) {
+      rc = ORACLE_EINVAL;
+      break;
+    }
+    ++started;
+  }
+  for (int t = 0; t < started; ++t) pthread_join(tids[t], NULL);
+  return rc;
 }
 
 /* ---------------------------------------------------------------------- */

@@ -56,7 +56,7 @@ class Oracle:
         L.oracle_block_bytes.argtypes = [ctypes.c_int]
         L.oracle_quantize.restype = ctypes.c_int
         L.oracle_quantize.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_int64,
-                                      ctypes.c_int64, ctypes.c_void_p]
+                                      ctypes.c_int64, ctypes.c_void_p, ctypes.c_int]
         L.oracle_dequant.restype = ctypes.c_int
         L.oracle_dequant.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_int64,
                                      ctypes.c_int64, ctypes.c_void_p]
@@ -80,13 +80,13 @@ class Oracle:
         return int(self.lib.oracle_block_bytes(qtype))
 
     # -- quantize / dequantize -----------------------------------------------
-    def quantize(self, qtype: int, w: np.ndarray) -> np.ndarray:
+    def quantize(self, qtype: int, w: np.ndarray, nthreads: int = 1) -> np.ndarray:
         """fp32 W[n, k] -> canonical blocks, uint8 [n, k/32, block_bytes]."""
         w = np.ascontiguousarray(w, dtype=np.float32)
         n, k = w.shape
         bb = self.block_bytes(qtype)
         out = np.zeros((n, k // QK, bb), dtype=np.uint8)
-        rc = self.lib.oracle_quantize(qtype, w.ctypes.data, n, k, out.ctypes.data)
+        rc = self.lib.oracle_quantize(qtype, w.ctypes.data, n, k, out.ctypes.data, int(nthreads))
         if rc != 0:
             raise ValueError("oracle_quantize rejected the arguments")
         return out

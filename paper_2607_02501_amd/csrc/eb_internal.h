@@ -1,0 +1,57 @@
+// eb_internal.h -- declarations shared by the library's translation units.
+// Host-side launchers live next to their kernels; eb_api.cpp validates
+// arguments and dispatches to them.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/eb.h"
+
+namespace eb {
+
+constexpr int kQK = 32;  // weights per block
+
+__host__ __device__ inline int64_t qs_bytes_per_block(int32_t type) { return type == EB_Q8_0 ? 32 : 16; }
+__host__ __device__ inline int64_t round_up(int64_t v, int64_t a) { return (v + a - 1) / a * a; }
+
+struct Layout {
+  int64_t nb;        // blocks per row
+  int64_t qs_row;    // bytes per qs row
+  int64_t d_off;     // byte offset of the scale plane
+  int64_t ds;        // scale-plane row stride (elements)
+  int64_t total;     // total bytes
+};
+
+inline Layout layout_of(int32_t type, int64_t n, int64_t k) {
+  Layout L;
+  L.nb = k / kQK;
+  L.qs_row = L.nb * qs_bytes_per_block(type);
+  L.d_off = round_up(n * L.qs_row, 256);
+  L.ds = round_up(L.nb, 8);
+  L.total = round_up(L.d_off + n * L.ds * 2, 256);
+  return L;
+}
+
+// ---- launchers (each returns hipSuccess or the launch error) ----
+hipError_t launch_quantize(int32_t type, const float *w, int64_t n, int64_t k, void *out,
+                           hipStream_t s);
+hipError_t launch_to_canonical(int32_t type, const void *planar, int64_t n, int64_t k, void *dst,
+                               hipStream_t s);
+hipError_t launch_from_canonical(int32_t type, const void *src, int64_t n, int64_t k, void *out,
+                                 hipStream_t s);
+
+// GEMV path: m <= 4, m * k <= kGemvMaxMK
+constexpr int64_t kGemvMaxM = 4;
+constexpr int64_t kGemvMaxMK = 65536;
+hipError_t launch_gemv(int32_t type, const void *wdata, int64_t n, int64_t k, const void *x,
+                       int32_t xt, int64_t m, void *y, int32_t yt, hipStream_t s);
+
+// MFMA path: any m
+hipError_t launch_mfma(int32_t type, const void *wdata, int64_t n, int64_t k, const void *x,
+                       int32_t xt, int64_t m, void *y, int32_t yt, hipStream_t s);
+
+// number of compute units of the current device (cached per device)
+int device_cu_count();
+
+}  // namespace eb

@@ -1,0 +1,602 @@
+// gemv.hip -- bandwidth-bound path of the quantized linear layer for m <= 4
+// activation rows (batch-1 decode: paper section 3.1, "latency-first
+// closed-loop control" runs effectively at batch 1; section 3.2 asks for
+// fused, backend-specific kernels for it).
+//
+// y[m][n] = sum_b d16[n][b] * sum_{j in block b} x[m][32b + j] * code[n][32b + j]
+//
+// Work decomposition (wave64):
+//   * a wave owns 4 weight rows at a time; 16 lanes per row, lane c of a row
+//     walks the row's 16-byte "units" u = c, c + 16, ... (a unit is one Q4_0
+//     block = 32 weights, or half a Q8_0 block = 16 weights), so each load
+//     instruction reads 4 contiguous 256-byte runs of packed codes;
+//   * RS such 4-row sets are in flight per wave;
+//   * the activations x[m][k] are staged once per workgroup into LDS, already
+//     permuted into the pair order the code decoder produces, together with a
+//     per-unit offset (see below);
+//   * the 16 partial sums of a row are added with four DPP steps.
+//
+// In-register dequantization never materialises the signed codes.  A 4-bit
+// code n (stored value c + 8) OR-ed into the mantissa of binary16 1024.0 reads
+// as 1024 + n; OR-ed one nibble higher it reads 1024 + 16 n.  For int8 codes q,
+// (q ^ 0x80) = q + 128 is placed the same way.  v_dot2_f32_f16 then multiplies
+// exact pairs, and the constant part (e.g. 1032 * sum x) is removed once per
+// unit with an offset precomputed from x in binary64 when x is staged.  For
+// bfloat16 activations the magic constant is bfloat16 128.0 (4-bit codes) or
+// the codes are converted to fp32 (8-bit codes).
+#include <hip/hip_runtime.h>
+
+#include <cstdio>
+#include <cstdlib>
+
+#include "eb_internal.h"
+
+namespace eb {
+namespace {
+
+typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf162_t __attribute__((ext_vector_type(2)));
+
+constexpr int kLanesPerRow = 16;
+constexpr int kRowsPerSet = 64 / kLanesPerRow;  // 4
+constexpr int kWaves = 4;                        // waves per workgroup
+constexpr int kM1MaxSlots = 8;                   // m == 1 kernel: up to 8 units per lane
+
+template <int QT>
+struct Unit {
+  static constexpr int kElems = (QT == EB_Q4_0) ? 32 : 16;  // weights per 16-byte unit
+  static constexpr int kChunks = kElems * 2 / 16;            // 16-byte x chunks per unit
+};
+
+__device__ inline float dpp_row_sum(float v) {
+  // quad_perm [1,0,3,2], quad_perm [2,3,0,1], row_ror:4, row_ror:8
+  v += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, true));
+  v += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x4E, 0xF, 0xF, true));
+  v += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x124, 0xF, 0xF, true));
+  v += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x128, 0xF, 0xF, true));
+  return v;
+}
+
+__device__ inline uint4 load_nt(const uint4 *p) {
+  typedef unsigned int u4 __attribute__((ext_vector_type(4)));
+  const u4 t = __builtin_nontemporal_load(reinterpret_cast<const u4 *>(p));
+  return make_uint4(t[0], t[1], t[2], t[3]);
+}
+
+__device__ inline float dot2h(uint32_t a, uint32_t b, float c) {
+  return __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, a), __builtin_bit_cast(half2_t, b), c,
+                                false);
+}
+__device__ inline float dot2bf(uint32_t a, uint32_t b, float c) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf162_t, a),
+                                         __builtin_bit_cast(bf162_t, b), c, false);
+}
+
+// (a & mask) | magic should be one v_and_or_b32, but gfx9 VOP3 encodings take
+// no literal and read at most one scalar operand, so with two constants the
+// compiler splits it into v_and + v_or.  vconst() hands the compiler the magic
+// constant as an opaque VGPR value (an identity DPP move), leaving the mask as
+// the single scalar operand; this halves the decode cost of 4-bit codes.
+__device__ inline uint32_t vconst(uint32_t c) {
+  return (uint32_t)__builtin_amdgcn_mov_dpp((int)c, 0xE4, 0xF, 0xF, false);  // quad_perm [0,1,2,3]
+}
+__device__ inline uint32_t and_or(uint32_t a, uint32_t mask, uint32_t magic) {
+  return (a & mask) | magic;
+}
+
+// Sum over one unit of (stored code value with the magic offset) * x, minus
+// the precomputed offset: returns sum_j code_j * x_j for the unit.
+template <int QT, int XT>
+__device__ inline float unit_dot(const uint4 q, const uint4 *xc, float off);
+
+// Q4_0, binary16 x.  x chunk i = pairs (x4i,x4i+2) (x4i+1,x4i+3) (x16+4i,x16+4i+2) (x16+4i+1,x16+4i+3)
+template <>
+__device__ inline float unit_dot<EB_Q4_0, EB_F16>(const uint4 q, const uint4 *xc, float off) {
+  const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+  const uint32_t mlo = 0x000F000Fu, mhi = 0x00F000F0u, magic = vconst(0x64006400u);
+  float lo = 0.f, hi = 0.f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t v = w[i], v8 = w[i] >> 8;
+    lo = dot2h(and_or(v, mlo, magic), xc[i].x, lo);
+    lo = dot2h(and_or(v8, mlo, magic), xc[i].y, lo);
+    hi = dot2h(and_or(v, mhi, magic), xc[i].z, hi);
+    hi = dot2h(and_or(v8, mhi, magic), xc[i].w, hi);
+  }
+  // lo terms are (c + 1032) x, hi terms (16 c + 1152) x
+  return __builtin_fmaf(hi, 0.0625f, lo) - off;
+}
+
+// Q4_0, bfloat16 x: bfloat16 128.0 | nibble = 128 + n = c + 136.
+template <>
+__device__ inline float unit_dot<EB_Q4_0, EB_BF16>(const uint4 q, const uint4 *xc, float off) {
+  const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+  const uint32_t mlo = 0x000F000Fu, magic = vconst(0x43004300u);
+  float a = 0.f, b = 0.f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t v = w[i];
+    a = dot2bf(and_or(v, mlo, magic), xc[i].x, a);
+    a = dot2bf(and_or(v >> 8, mlo, magic), xc[i].y, a);
+    b = dot2bf(and_or(v >> 4, mlo, magic), xc[i].z, b);
+    b = dot2bf(and_or(v >> 12, mlo, magic), xc[i].w, b);
+  }
+  return (a + b) - off;
+}
+
+// Q8_0 half block, binary16 x: (q ^ 0x80) placed under 0x64 reads 1024 + q + 128.
+template <>
+__device__ inline float unit_dot<EB_Q8_0, EB_F16>(const uint4 q, const uint4 *xc, float off) {
+  const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+  const uint32_t xs[8] = {xc[0].x, xc[0].y, xc[0].z, xc[0].w, xc[1].x, xc[1].y, xc[1].z, xc[1].w};
+  float a = 0.f, b = 0.f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t u = w[i] ^ 0x80808080u;
+    a = dot2h(__builtin_amdgcn_perm(0x64646464u, u, 0x04020400u), xs[2 * i], a);
+    b = dot2h(__builtin_amdgcn_perm(0x64646464u, u, 0x04030401u), xs[2 * i + 1], b);
+  }
+  return (a + b) - off;
+}
+
+// Q8_0 half block, bfloat16 x (natural order): codes via fp32 byte conversion.
+template <>
+__device__ inline float unit_dot<EB_Q8_0, EB_BF16>(const uint4 q, const uint4 *xc, float off) {
+  const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+  const uint32_t xs[8] = {xc[0].x, xc[0].y, xc[0].z, xc[0].w, xc[1].x, xc[1].y, xc[1].z, xc[1].w};
+  float a = 0.f, b = 0.f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t u = w[i] ^ 0x80808080u;
+    const uint32_t x01 = xs[2 * i], x23 = xs[2 * i + 1];
+    a = __builtin_fmaf((float)(u & 0xffu), __builtin_bit_cast(float, x01 << 16), a);
+    b = __builtin_fmaf((float)((u >> 8) & 0xffu), __builtin_bit_cast(float, x01 & 0xffff0000u), b);
+    a = __builtin_fmaf((float)((u >> 16) & 0xffu), __builtin_bit_cast(float, x23 << 16), a);
+    b = __builtin_fmaf((float)(u >> 24), __builtin_bit_cast(float, x23 & 0xffff0000u), b);
+  }
+  return (a + b) - off;
+}
+
+template <int XT>
+__device__ inline double x_to_f64(uint32_t h) {
+  if (XT == EB_F16) return (double)__builtin_bit_cast(_Float16, (uint16_t)h);
+  return (double)__builtin_bit_cast(float, h << 16);
+}
+
+// Stage x[m][k] (m <= MT rows; missing rows are zero) into LDS in the pair
+// order of unit_dot<QT, XT>, plus one offset per (row, unit).
+template <int QT, int XT, int MT>
+__device__ inline void stage_x(const uint16_t *__restrict__ x, int m, int64_t k, int64_t ku,
+                               uint4 *xs, float *xoff, int64_t pitch) {
+  constexpr int E = Unit<QT>::kElems;
+  constexpr int CH = Unit<QT>::kChunks;
+  for (int64_t idx = threadIdx.x; idx < (int64_t)MT * ku; idx += blockDim.x) {
+    const int mm = (int)(idx / ku);
+    const int64_t u = idx % ku;
+    uint32_t r[E / 2];  // raw dwords: r[j] = (h[2j], h[2j+1])
+    if (mm < m) {
+      const uint4 *src = reinterpret_cast<const uint4 *>(x + (int64_t)mm * k + u * E);
+#pragma unroll
+      for (int c = 0; c < E / 8; ++c) {
+        uint4 t = src[c];
+        r[4 * c] = t.x;
+        r[4 * c + 1] = t.y;
+        r[4 * c + 2] = t.z;
+        r[4 * c + 3] = t.w;
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < E / 2; ++j) r[j] = 0;
+    }
+    double s_lo = 0.0, s_hi = 0.0;
+#pragma unroll
+    for (int j = 0; j < E / 2; ++j) {
+      double v = x_to_f64<XT>(r[j] & 0xffffu) + x_to_f64<XT>(r[j] >> 16);
+      if (2 * j < 16)
+        s_lo += v;
+      else
+        s_hi += v;
+    }
+    uint4 out[CH];
+    double off;
+    if (QT == EB_Q4_0) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const uint32_t a = r[2 * i], b = r[2 * i + 1], c = r[8 + 2 * i], d = r[8 + 2 * i + 1];
+        out[i] = make_uint4((a & 0xffffu) | (b << 16), (a >> 16) | (b & 0xffff0000u),
+                            (c & 0xffffu) | (d << 16), (c >> 16) | (d & 0xffff0000u));
+      }
+      off = (XT == EB_F16) ? 1032.0 * s_lo + 72.0 * s_hi : 136.0 * (s_lo + s_hi);
+    } else {
+      if (XT == EB_F16) {
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+          const uint32_t a = r[4 * c], b = r[4 * c + 1], e = r[4 * c + 2], f = r[4 * c + 3];
+          out[c] = make_uint4((a & 0xffffu) | (b << 16), (a >> 16) | (b & 0xffff0000u),
+                              (e & 0xffffu) | (f << 16), (e >> 16) | (f & 0xffff0000u));
+        }
+        off = 1152.0 * s_lo;
+      } else {
+#pragma unroll
+        for (int c = 0; c < 2; ++c) out[c] = make_uint4(r[4 * c], r[4 * c + 1], r[4 * c + 2], r[4 * c + 3]);
+        off = 128.0 * s_lo;
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < CH; ++c) xs[((int64_t)mm * CH + c) * pitch + u] = out[c];
+    xoff[(int64_t)mm * pitch + u] = (float)off;
+  }
+}
+
+template <int QT, int XT, int MT, int RS>
+__global__ void __launch_bounds__(64 * kWaves)
+    gemv_kernel(const uint8_t *__restrict__ wdata, int64_t n, int64_t k, int64_t d_off, int64_t ds,
+                const uint16_t *__restrict__ x, int m, void *__restrict__ y, int yt) {
+  constexpr int CH = Unit<QT>::kChunks;
+  const int64_t ku = k / Unit<QT>::kElems;
+  extern __shared__ uint4 smem[];
+  uint4 *xs = smem;
+  float *xoff = reinterpret_cast<float *>(smem + (int64_t)MT * CH * ku);
+
+  stage_x<QT, XT, MT>(x, m, k, ku, xs, xoff, ku);
+  __syncthreads();
+
+  const uint4 *__restrict__ qs = reinterpret_cast<const uint4 *>(wdata);
+  const uint16_t *__restrict__ dplane = reinterpret_cast<const uint16_t *>(wdata + d_off);
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int rsub = lane / kLanesPerRow;
+  const int c = lane % kLanesPerRow;
+  constexpr int kRowsPerItem = kRowsPerSet * RS;
+  const int64_t items = (n + kRowsPerItem - 1) / kRowsPerItem;
+
+  for (int64_t it = (int64_t)blockIdx.x * kWaves + wave; it < items;
+       it += (int64_t)gridDim.x * kWaves) {
+    int64_t rows[RS];
+#pragma unroll
+    for (int s = 0; s < RS; ++s) {
+      const int64_t r = it * kRowsPerItem + s * kRowsPerSet + rsub;
+      rows[s] = r < n ? r : n - 1;  // clamp the tail; its results are not stored
+    }
+    float acc[RS][MT];
+#pragma unroll
+    for (int s = 0; s < RS; ++s)
+#pragma unroll
+      for (int mm = 0; mm < MT; ++mm) acc[s][mm] = 0.f;
+
+#pragma unroll 2
+    for (int64_t u = c; u < ku; u += kLanesPerRow) {
+      const int64_t b = (QT == EB_Q4_0) ? u : (u >> 1);
+      uint4 q[RS];
+      float d[RS];
+#pragma unroll
+      for (int s = 0; s < RS; ++s) {
+        q[s] = load_nt(qs + rows[s] * ku + u);
+        d[s] = (float)__builtin_bit_cast(_Float16, __builtin_nontemporal_load(dplane + rows[s] * ds + b));
+      }
+#pragma unroll
+      for (int mm = 0; mm < MT; ++mm) {
+        uint4 xc[CH];
+#pragma unroll
+        for (int ch = 0; ch < CH; ++ch) xc[ch] = xs[((int64_t)mm * CH + ch) * ku + u];
+        const float off = xoff[(int64_t)mm * ku + u];
+#pragma unroll
+        for (int s = 0; s < RS; ++s)
+          acc[s][mm] = __builtin_fmaf(d[s], unit_dot<QT, XT>(q[s], xc, off), acc[s][mm]);
+      }
+    }
+
+#pragma unroll
+    for (int s = 0; s < RS; ++s)
+#pragma unroll
+      for (int mm = 0; mm < MT; ++mm) acc[s][mm] = dpp_row_sum(acc[s][mm]);
+
+    if (c == 0) {
+#pragma unroll
+      for (int s = 0; s < RS; ++s) {
+        const int64_t r = it * kRowsPerItem + s * kRowsPerSet + rsub;
+        if (r >= n) continue;
+#pragma unroll
+        for (int mm = 0; mm < MT; ++mm) {
+          if (mm >= m) continue;
+          if (yt == EB_F32)
+            reinterpret_cast<float *>(y)[(int64_t)mm * n + r] = acc[s][mm];
+          else
+            reinterpret_cast<__bf16 *>(y)[(int64_t)mm * n + r] = (__bf16)acc[s][mm];
+        }
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// m == 1: one wave per weight row across the whole of k.  Lane l owns units
+// l, l + 64, ... of every row, so each load instruction reads 1 KiB of
+// contiguous packed codes; the lane's x fragments (already in pair order) stay
+// in VGPRs for the whole launch.  R rows are in flight per wave; their 64-lane
+// partial sums are reduced together by halving exchanges (v_permlane32_swap,
+// v_permlane16_swap, then DPP inside 16-lane rows), R values in O(R + log 64)
+// instructions.
+// ---------------------------------------------------------------------------
+
+template <int CTRL>
+__device__ inline float dpp(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL, 0xF, 0xF, true));
+}
+
+__device__ inline float red8(float v) {  // sum over aligned groups of 8 lanes
+  v += dpp<0xB1>(v);   // quad_perm [1,0,3,2]
+  v += dpp<0x4E>(v);   // quad_perm [2,3,0,1]
+  v += dpp<0x141>(v);  // row_half_mirror
+  return v;
+}
+__device__ inline float red16(float v) {  // sum over 16-lane rows
+  v = red8(v);
+  return v + dpp<0x140>(v);  // row_mirror
+}
+// lanes 0..31 get a[l] + a[l+32]; lanes 32..63 get b[l-32] + b[l]
+__device__ inline float swap32(float a, float b) {
+  auto p = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, a),
+                                            __builtin_bit_cast(unsigned, b), false, false);
+  return __builtin_bit_cast(float, (unsigned)p[0]) + __builtin_bit_cast(float, (unsigned)p[1]);
+}
+// even 16-lane rows get a + a(partner row); odd rows get b + b(partner row)
+__device__ inline float swap16(float a, float b) {
+  auto p = __builtin_amdgcn_permlane16_swap(__builtin_bit_cast(unsigned, a),
+                                            __builtin_bit_cast(unsigned, b), false, false);
+  return __builtin_bit_cast(float, (unsigned)p[0]) + __builtin_bit_cast(float, (unsigned)p[1]);
+}
+// lower 8 lanes of each row get a + a(l^8); upper 8 get b + b(l^8)
+__device__ inline float half8(float a, float b, int lane) {
+  const bool lo = (lane & 8) == 0;
+  const float keep = lo ? a : b, send = lo ? b : a;
+  return keep + dpp<0x128>(send);  // row_ror:8
+}
+
+// Reduce v[0..R) over the 64 lanes.  Returns the total of row `row` (a
+// function of the lane) in every lane; `writer` marks one lane per row.
+template <int R>
+__device__ inline float reduce_rows(const float (&v)[R], int lane, int &row, bool &writer) {
+  if constexpr (R == 8) {
+    float a0 = swap32(v[0], v[4]), a1 = swap32(v[1], v[5]), a2 = swap32(v[2], v[6]),
+          a3 = swap32(v[3], v[7]);
+    float b0 = swap16(a0, a2), b1 = swap16(a1, a3);
+    float c = red8(half8(b0, b1, lane));
+    row = ((lane >> 3) & 1) + 2 * ((lane >> 4) & 1) + 4 * (lane >> 5);
+    writer = (lane & 7) == 0;
+    return c;
+  } else if constexpr (R == 4) {
+    float a0 = swap32(v[0], v[2]), a1 = swap32(v[1], v[3]);
+    float b = red16(swap16(a0, a1));
+    row = ((lane >> 4) & 1) + 2 * (lane >> 5);
+    writer = (lane & 15) == 0;
+    return b;
+  } else if constexpr (R == 2) {
+    float a = red16(swap32(v[0], v[1]));
+    a = swap16(a, a);
+    row = lane >> 5;
+    writer = (lane & 31) == 0;
+    return a;
+  } else {
+    float a = red16(v[0]);
+    a = swap16(a, a);
+    a = swap32(a, a);
+    row = 0;
+    writer = lane == 0;
+    return a;
+  }
+}
+
+// Cache-policy bits of a buffer load: NT (non-temporal).  Weights are read
+// exactly once per call, so they are streamed past the caches; on MI355X this
+// raises the sustained HBM read rate by about 13% over ordinary loads.
+constexpr int kNT = 2;
+
+// Raw buffer descriptor over [base, base + bytes): the address of every load
+// is then a scalar base plus a per-lane constant offset, with no per-lane
+// 64-bit pointer arithmetic in the loop.  Word 3 (0x00020000) selects a raw
+// 32-bit buffer with no format conversion.
+__device__ inline __amdgpu_buffer_rsrc_t rsrc(const void *base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes,
+                                           0x00020000);
+}
+
+// WPE: minimum waves per SIMD the register allocation must allow; memory
+// latency is hidden by other waves rather than by deep per-wave prefetch.
+template <int QT, int XT, int NS, int R, int WPE>
+__global__ void __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(WPE)))
+    gemv_m1_kernel(const uint8_t *__restrict__ wdata, int64_t n, int64_t k, int64_t d_off,
+                   int64_t ds, const uint16_t *__restrict__ x, void *__restrict__ y, int yt) {
+  constexpr int CH = Unit<QT>::kChunks;
+  // LDS: CH chunk rows of P entries; entry 64 * NS of every row is zero and
+  // stands in for units past the end of the row.  P is a compile-time
+  // constant so every x read is one base register plus an immediate offset.
+  constexpr int P = 64 * NS + 1;
+  const int ku = (int)(k / Unit<QT>::kElems);  // 64 * (NS - 1) < ku <= 64 * NS
+  extern __shared__ uint4 smem[];
+  uint4 *xs = smem;
+  float *xoff = reinterpret_cast<float *>(smem + CH * P);
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
+  const int64_t groups = (n + R - 1) / R;
+  const int64_t gstride = (int64_t)gridDim.x * kWaves;
+  int64_t g = (int64_t)blockIdx.x * kWaves + wave;
+  const uint32_t qs_row = (uint32_t)ku * 16u, d_row = (uint32_t)(ds * 2);
+  const uint8_t *__restrict__ dbase = wdata + d_off;
+
+  // Per-lane byte offsets of the lane's units inside a row, fixed for the
+  // launch.  Units past the end of the row (last slot only) are clamped to the
+  // row's last unit; their x fragment is zero, so they add exactly 0.
+  uint32_t qoff[NS], doff[NS], xidx[NS];
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+    const int u = lane + 64 * s;
+    const int uc = min(u, ku - 1);
+    qoff[s] = (uint32_t)uc * 16u;
+    doff[s] = (uint32_t)((QT == EB_Q4_0) ? uc : (uc >> 1)) * 2u;
+    xidx[s] = u < ku ? (uint32_t)u : 64u * NS;
+  }
+
+  uint4 q[NS][R];
+  uint16_t dh[NS][R];
+  auto load_group = [&](int64_t grp) {
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      int64_t row = grp * R + r;
+      row = row < n ? row : n - 1;  // tail rows are computed but not stored
+      const auto rq = rsrc(wdata + row * qs_row, qs_row);
+      const auto rd = rsrc(dbase + row * d_row, d_row);
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+        const auto v = __builtin_amdgcn_raw_buffer_load_b128(rq, (int)qoff[s], 0, kNT);
+        q[s][r] = make_uint4(v[0], v[1], v[2], v[3]);
+        dh[s][r] = __builtin_amdgcn_raw_buffer_load_b16(rd, (int)doff[s], 0, kNT);
+      }
+    }
+  };
+  // weight loads of the first group are in flight while x is staged
+  if (g < groups) load_group(g);
+  stage_x<QT, XT, 1>(x, 1, k, ku, xs, xoff, P);
+  if (threadIdx.x < CH) xs[threadIdx.x * P + 64 * NS] = make_uint4(0, 0, 0, 0);
+  if (threadIdx.x == 0) xoff[64 * NS] = 0.f;
+  __syncthreads();
+
+  while (g < groups) {
+    float acc[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) acc[r] = 0.f;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      const uint4 *xp = xs + xidx[s];
+      uint4 xf[CH];
+#pragma unroll
+      for (int c = 0; c < CH; ++c) xf[c] = xp[c * P];
+      const float xo = xoff[xidx[s]];
+#pragma unroll
+      for (int r = 0; r < R; ++r)
+        acc[r] = __builtin_fmaf((float)__builtin_bit_cast(_Float16, dh[s][r]),
+                                unit_dot<QT, XT>(q[s][r], xf, xo), acc[r]);
+    }
+    int rr;
+    bool writer;
+    const float tot = reduce_rows<R>(acc, lane, rr, writer);
+    const int64_t row = g * R + rr;
+    if (writer && row < n) {
+      if (yt == EB_F32)
+        reinterpret_cast<float *>(y)[row] = tot;
+      else
+        reinterpret_cast<__bf16 *>(y)[row] = (__bf16)tot;
+    }
+    g += gstride;
+    // the weight registers are free again: load the next group into them
+    __builtin_amdgcn_sched_barrier(0);
+    if (g < groups) load_group(g);
+  }
+}
+
+template <int QT, int XT, int NS, int R, int WPE>
+hipError_t launch_m1_t(const void *wdata, int64_t n, int64_t k, const void *x, void *y, int32_t yt,
+                       hipStream_t s, int wg_per_cu) {
+  const Layout L = layout_of(QT, n, k);
+  const int64_t ku = k / Unit<QT>::kElems;
+  const size_t lds = (size_t)(64 * NS + 1) * (Unit<QT>::kChunks * 16 + 4);
+  (void)ku;
+  const int64_t groups = (n + R - 1) / R;
+  int64_t grid = (groups + kWaves - 1) / kWaves;
+  const int64_t cap = (int64_t)device_cu_count() * wg_per_cu;
+  if (grid > cap) grid = cap;
+  gemv_m1_kernel<QT, XT, NS, R, WPE><<<(unsigned)grid, 64 * kWaves, lds, s>>>(
+      (const uint8_t *)wdata, n, k, L.d_off, L.ds, (const uint16_t *)x, y, yt);
+  return hipGetLastError();
+}
+
+// Launch shape of the m == 1 kernel: rows per wave (R), minimum waves per
+// SIMD (WPE) and workgroups per CU.  The defaults are per slot count; the
+// environment variable EB_GEMV_M1="R,WPE,WGPERCU" overrides them (tuning).
+struct M1Shape {
+  int r, wpe, wg;
+};
+
+M1Shape m1_shape(int64_t ns) {
+  static const char *env = getenv("EB_GEMV_M1");
+  if (env) {
+    M1Shape v{0, 0, 0};
+    if (sscanf(env, "%d,%d,%d", &v.r, &v.wpe, &v.wg) == 3 && v.r > 0 && v.wpe > 0 && v.wg > 0) return v;
+  }
+  if (ns <= 1) return {4, 4, 4};
+  if (ns <= 2) return {2, 4, 4};
+  return {1, 4, 4};
+}
+
+template <int QT, int XT, int NS>
+hipError_t launch_m1_ns(const void *wdata, int64_t n, int64_t k, const void *x, void *y, int32_t yt,
+                        hipStream_t s) {
+  const M1Shape v = m1_shape(NS);
+#define EB_M1(R_, W_)                                                                      \
+  if (v.r == R_ && v.wpe == W_)                                                           \
+    return launch_m1_t<QT, XT, NS, R_, W_>(wdata, n, k, x, y, yt, s, v.wg);
+  EB_M1(1, 4) EB_M1(2, 4) EB_M1(4, 4) EB_M1(1, 2) EB_M1(2, 2) EB_M1(4, 2)
+#undef EB_M1
+  return hipErrorInvalidValue;
+}
+
+template <int QT, int XT>
+hipError_t launch_m1(const void *wdata, int64_t n, int64_t k, const void *x, void *y, int32_t yt,
+                     hipStream_t s) {
+  const int64_t ns = (k / Unit<QT>::kElems + 63) / 64;
+  switch (ns) {
+    case 1: return launch_m1_ns<QT, XT, 1>(wdata, n, k, x, y, yt, s);
+    case 2: return launch_m1_ns<QT, XT, 2>(wdata, n, k, x, y, yt, s);
+    case 3: return launch_m1_ns<QT, XT, 3>(wdata, n, k, x, y, yt, s);
+    case 4: return launch_m1_ns<QT, XT, 4>(wdata, n, k, x, y, yt, s);
+    case 5: return launch_m1_ns<QT, XT, 5>(wdata, n, k, x, y, yt, s);
+    case 6: return launch_m1_ns<QT, XT, 6>(wdata, n, k, x, y, yt, s);
+    case 7: return launch_m1_ns<QT, XT, 7>(wdata, n, k, x, y, yt, s);
+    default: return launch_m1_ns<QT, XT, 8>(wdata, n, k, x, y, yt, s);
+  }
+}
+
+template <int QT, int XT, int MT, int RS>
+hipError_t launch_t(const void *wdata, int64_t n, int64_t k, const void *x, int64_t m, void *y,
+                    int32_t yt, hipStream_t s) {
+  const Layout L = layout_of(QT, n, k);
+  const int64_t ku = k / Unit<QT>::kElems;
+  const size_t lds = (size_t)MT * ku * (Unit<QT>::kChunks * 16 + 4);
+  const int64_t items = (n + kRowsPerSet * RS - 1) / (kRowsPerSet * RS);
+  int64_t grid = (items + kWaves - 1) / kWaves;
+  const int64_t cap = (int64_t)device_cu_count() * 8;
+  if (grid > cap) grid = cap;
+  auto kern = gemv_kernel<QT, XT, MT, RS>;
+  if (lds > 64 * 1024) {
+    hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  kern<<<(unsigned)grid, 64 * kWaves, lds, s>>>((const uint8_t *)wdata, n, k, L.d_off, L.ds,
+                                                (const uint16_t *)x, (int)m, y, yt);
+  return hipGetLastError();
+}
+
+template <int QT, int XT>
+hipError_t launch_m(const void *wdata, int64_t n, int64_t k, const void *x, int64_t m, void *y,
+                    int32_t yt, hipStream_t s) {
+  if (m <= 1 && k / Unit<QT>::kElems <= 64 * kM1MaxSlots)
+    return launch_m1<QT, XT>(wdata, n, k, x, y, yt, s);
+  if (m <= 1) return launch_t<QT, XT, 1, 2>(wdata, n, k, x, m, y, yt, s);
+  if (m <= 2) return launch_t<QT, XT, 2, 2>(wdata, n, k, x, m, y, yt, s);
+  return launch_t<QT, XT, 4, 1>(wdata, n, k, x, m, y, yt, s);
+}
+
+}  // namespace
+
+hipError_t launch_gemv(int32_t type, const void *wdata, int64_t n, int64_t k, const void *x,
+                       int32_t xt, int64_t m, void *y, int32_t yt, hipStream_t s) {
+  if (type == EB_Q4_0) {
+    if (xt == EB_F16) return launch_m<EB_Q4_0, EB_F16>(wdata, n, k, x, m, y, yt, s);
+    return launch_m<EB_Q4_0, EB_BF16>(wdata, n, k, x, m, y, yt, s);
+  }
+  if (xt == EB_F16) return launch_m<EB_Q8_0, EB_F16>(wdata, n, k, x, m, y, yt, s);
+  return launch_m<EB_Q8_0, EB_BF16>(wdata, n, k, x, m, y, yt, s);
+}
+
+}  // namespace eb

@@ -1,0 +1,213 @@
+"""Python binding of libeb (argument marshalling only).
+
+Every computation runs in the HIP kernels of libeb.so; this module only
+allocates outputs with torch, passes raw device pointers and the current HIP
+stream, and turns status codes into exceptions.  It raises at import time if
+libeb.so has not been built (there is no fallback path).
+
+Names follow the C ABI in include/eb.h.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libeb.so")
+
+EB_OK = 0
+EB_ERR_INVALID = -1
+EB_ERR_ALIGN = -2
+EB_ERR_UNSUPPORTED = -3
+EB_ERR_HIP = -4
+
+EB_Q8_0 = 1
+EB_Q4_0 = 2
+EB_F32 = 0
+EB_F16 = 1
+EB_BF16 = 2
+EB_PATH_AUTO = 0
+EB_PATH_GEMV = 1
+EB_PATH_MFMA = 2
+
+QTYPES = {"q8_0": EB_Q8_0, "q4_0": EB_Q4_0}
+DTYPES = {torch.float32: EB_F32, torch.float16: EB_F16, torch.bfloat16: EB_BF16}
+PATHS = {"auto": EB_PATH_AUTO, "gemv": EB_PATH_GEMV, "mfma": EB_PATH_MFMA}
+
+
+class eb_qweights(ctypes.Structure):
+    _fields_ = [("type", ctypes.c_int32), ("reserved", ctypes.c_int32), ("n", ctypes.c_int64),
+                ("k", ctypes.c_int64), ("data", ctypes.c_void_p)]
+
+
+class eb_layout(ctypes.Structure):
+    _fields_ = [("qs_offset", ctypes.c_int64), ("qs_row_bytes", ctypes.c_int64),
+                ("d_offset", ctypes.c_int64), ("d_stride", ctypes.c_int64),
+                ("total_bytes", ctypes.c_int64), ("canonical_bytes", ctypes.c_int64)]
+
+
+class eb_qlinear_op(ctypes.Structure):
+    _fields_ = [("w", eb_qweights), ("x", ctypes.c_void_p), ("y", ctypes.c_void_p),
+                ("m", ctypes.c_int64), ("x_type", ctypes.c_int32), ("y_type", ctypes.c_int32)]
+
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"libeb.so not found at {LIB_PATH}: build it first "
+                      "(python -m paper_2607_02501_amd.build); there is no fallback path")
+
+lib = ctypes.CDLL(LIB_PATH)
+
+_vp, _i32, _i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+lib.eb_version.restype = ctypes.c_char_p
+lib.eb_version.argtypes = []
+lib.eb_status_str.restype = ctypes.c_char_p
+lib.eb_status_str.argtypes = [_i32]
+lib.eb_qweights_bytes.restype = ctypes.c_size_t
+lib.eb_qweights_bytes.argtypes = [_i32, _i64, _i64]
+lib.eb_qweights_layout.restype = _i32
+lib.eb_qweights_layout.argtypes = [_i32, _i64, _i64, ctypes.POINTER(eb_layout)]
+for _name in ("eb_quantize_q8_0", "eb_quantize_q4_0"):
+    getattr(lib, _name).restype = _i32
+    getattr(lib, _name).argtypes = [_vp, _i64, _i64, _vp, _vp]
+lib.eb_qweights_to_canonical.restype = _i32
+lib.eb_qweights_to_canonical.argtypes = [ctypes.POINTER(eb_qweights), _vp, _vp]
+lib.eb_qweights_from_canonical.restype = _i32
+lib.eb_qweights_from_canonical.argtypes = [_i32, _vp, _i64, _i64, _vp, _vp]
+lib.eb_qlinear.restype = _i32
+lib.eb_qlinear.argtypes = [ctypes.POINTER(eb_qweights), _vp, _i32, _i64, _vp, _i32, _vp]
+lib.eb_qlinear_ex.restype = _i32
+lib.eb_qlinear_ex.argtypes = [ctypes.POINTER(eb_qweights), _vp, _i32, _i64, _vp, _i32, _i32, _vp]
+lib.eb_qlinear_auto_path.restype = _i32
+lib.eb_qlinear_auto_path.argtypes = [_i32, _i32, _i64, _i64, _i64]
+lib.eb_qlinear_stack.restype = _i32
+lib.eb_qlinear_stack.argtypes = [ctypes.POINTER(eb_qlinear_op), _i32, _vp]
+lib.eb_stack_cache_clear.restype = _i32
+lib.eb_stack_cache_clear.argtypes = []
+
+
+class EBError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__(f"{what}: {lib.eb_status_str(status).decode()}")
+        self.status = status
+
+
+def _check(status: int, what: str) -> None:
+    if status != EB_OK:
+        raise EBError(status, what)
+
+
+def _stream(device) -> int:
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def version() -> str:
+    return lib.eb_version().decode()
+
+
+def qweights_bytes(qtype: str, n: int, k: int) -> int:
+    return int(lib.eb_qweights_bytes(QTYPES[qtype], n, k))
+
+
+def layout(qtype: str, n: int, k: int) -> eb_layout:
+    out = eb_layout()
+    _check(lib.eb_qweights_layout(QTYPES[qtype], n, k, ctypes.byref(out)), "eb_qweights_layout")
+    return out
+
+
+class QWeights:
+    """A quantized weight matrix W[n, k] held in a caller-owned device buffer."""
+
+    def __init__(self, qtype: str, n: int, k: int, buf: torch.Tensor):
+        assert buf.dtype == torch.uint8 and buf.is_cuda
+        self.qtype, self.n, self.k, self.buf = qtype, n, k, buf
+
+    @property
+    def c(self) -> eb_qweights:
+        return eb_qweights(QTYPES[self.qtype], 0, self.n, self.k, self.buf.data_ptr())
+
+    @property
+    def device(self):
+        return self.buf.device
+
+    def nbytes(self) -> int:
+        return qweights_bytes(self.qtype, self.n, self.k)
+
+
+def empty_qweights(qtype: str, n: int, k: int, device="cuda") -> QWeights:
+    nbytes = qweights_bytes(qtype, n, k)
+    if nbytes == 0:
+        raise EBError(EB_ERR_INVALID, "eb_qweights_bytes")
+    # torch's caching allocator returns 512-byte aligned blocks
+    buf = torch.empty(nbytes, dtype=torch.uint8, device=device)
+    return QWeights(qtype, n, k, buf)
+
+
+def quantize(w: torch.Tensor, qtype: str, out: QWeights | None = None) -> QWeights:
+    """fp32 W[n, k] (device) -> QWeights in the planar layout."""
+    assert w.dtype == torch.float32 and w.is_cuda and w.dim() == 2
+    w = w.contiguous()
+    n, k = w.shape
+    out = out or empty_qweights(qtype, n, k, w.device)
+    fn = lib.eb_quantize_q8_0 if qtype == "q8_0" else lib.eb_quantize_q4_0
+    _check(fn(w.data_ptr(), n, k, out.buf.data_ptr(), _stream(w.device)), fn.__name__)
+    return out
+
+
+def to_canonical(qw: QWeights) -> torch.Tensor:
+    """Canonical array-of-blocks bytes (device uint8 tensor [n, k/32, block_bytes])."""
+    bb = 34 if qw.qtype == "q8_0" else 18
+    dst = torch.empty((qw.n, qw.k // 32, bb), dtype=torch.uint8, device=qw.device)
+    c = qw.c
+    _check(lib.eb_qweights_to_canonical(ctypes.byref(c), dst.data_ptr(), _stream(qw.device)),
+           "eb_qweights_to_canonical")
+    return dst
+
+
+def from_canonical(blocks: torch.Tensor, qtype: str, n: int, k: int) -> QWeights:
+    assert blocks.dtype == torch.uint8 and blocks.is_cuda
+    blocks = blocks.contiguous()
+    out = empty_qweights(qtype, n, k, blocks.device)
+    _check(lib.eb_qweights_from_canonical(QTYPES[qtype], blocks.data_ptr(), n, k,
+                                          out.buf.data_ptr(), _stream(blocks.device)),
+           "eb_qweights_from_canonical")
+    return out
+
+
+def qlinear(qw: QWeights, x: torch.Tensor, out_dtype=torch.float32, path: str = "auto",
+            out: torch.Tensor | None = None) -> torch.Tensor:
+    """y[m, n] = x[m, k] . w_hat^T on the GPU (fp32 accumulation)."""
+    assert x.is_cuda and x.dim() == 2 and x.shape[1] == qw.k
+    x = x.contiguous()
+    m = x.shape[0]
+    if out is None:
+        out = torch.empty((m, qw.n), dtype=out_dtype, device=x.device)
+    c = qw.c
+    st = lib.eb_qlinear_ex(ctypes.byref(c), x.data_ptr(), DTYPES[x.dtype], m, out.data_ptr(),
+                           DTYPES[out.dtype], PATHS[path], _stream(x.device))
+    _check(st, "eb_qlinear_ex")
+    return out
+
+
+def auto_path(qtype: str, x_dtype, m: int, n: int, k: int) -> str:
+    p = lib.eb_qlinear_auto_path(QTYPES[qtype], DTYPES[x_dtype], m, n, k)
+    return {EB_PATH_GEMV: "gemv", EB_PATH_MFMA: "mfma"}.get(p, "invalid")
+
+
+def make_ops(entries) -> ctypes.Array:
+    """entries: iterable of (QWeights, x, y).  Returns a ctypes eb_qlinear_op array."""
+    entries = list(entries)
+    arr = (eb_qlinear_op * len(entries))()
+    for i, (qw, x, y) in enumerate(entries):
+        arr[i] = eb_qlinear_op(qw.c, x.data_ptr(), y.data_ptr(), x.shape[0], DTYPES[x.dtype],
+                               DTYPES[y.dtype])
+    return arr
+
+
+def qlinear_stack(ops: ctypes.Array, device=None) -> None:
+    _check(lib.eb_qlinear_stack(ops, len(ops), _stream(device)), "eb_qlinear_stack")
+
+
+def stack_cache_clear() -> None:
+    _check(lib.eb_stack_cache_clear(), "eb_stack_cache_clear")

@@ -1,0 +1,40 @@
+"""Shared helpers of the GPU parity tests (test infrastructure)."""
+import numpy as np
+import torch
+
+from oracle import oracle as O
+
+QT = {"q8_0": O.Q8_0, "q4_0": O.Q4_0}
+XT = {torch.float16: O.X_F16, torch.bfloat16: O.X_BF16}
+
+# Error bound of the method: fp32 accumulation of 16-bit inputs, normalised by
+# sum_k |x||w_hat| per output.  A bfloat16 output adds one rounding of |y| <= bound.
+TOL_F32 = 2e-3
+TOL_BF16 = 2e-3 + 2.0 ** -9 * (1 + 2e-3)
+
+
+def bits16(t: torch.Tensor) -> np.ndarray:
+    return t.detach().cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
+
+
+def oracle_reference(orc, qtype, w_rows_f32: np.ndarray, x: torch.Tensor):
+    """Oracle y and bound for all rows of x against the given fp32 weight rows."""
+    blocks = orc.quantize(QT[qtype], w_rows_f32, nthreads=O.available_cores())
+    n, k = w_rows_f32.shape
+    y, bound = orc.qlinear(QT[qtype], blocks, n, k, bits16(x), XT[x.dtype],
+                           nthreads=O.available_cores())
+    return blocks, y, bound
+
+
+def assert_parity(y_gpu, y_ref, bound, tol, what=""):
+    y = y_gpu.detach().double().cpu().numpy() if isinstance(y_gpu, torch.Tensor) else y_gpu
+    assert y.shape == y_ref.shape, (y.shape, y_ref.shape)
+    assert np.all(np.isfinite(y)), what
+    zero = bound == 0
+    assert np.all(y[zero] == 0), f"{what}: nonzero output where the bound is 0"
+    if (~zero).any():
+        rel = np.abs(y[~zero] - y_ref[~zero]) / bound[~zero]
+        worst = float(rel.max())
+        assert worst <= tol, f"{what}: max normalised error {worst:.3e} > {tol:.3e}"
+        return worst
+    return 0.0

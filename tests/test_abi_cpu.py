@@ -1,0 +1,168 @@
+"""The C ABI without a GPU: libeb.so loads, exports every symbol include/eb.h
+declares, its host-only layout functions are right, and argument validation
+rejects bad calls before anything reaches the HIP runtime."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "eb.h")
+
+
+@pytest.fixture(scope="module")
+def eb():
+    lib = os.path.join(ROOT, "paper_2607_02501_amd", "libeb.so")
+    if not os.path.exists(lib):
+        from paper_2607_02501_amd import build
+
+        build.build()
+    from paper_2607_02501_amd import eb as _eb
+
+    return _eb
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(eb_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for required in ("eb_quantize_q8_0", "eb_quantize_q4_0", "eb_qlinear", "eb_qlinear_stack"):
+        assert required in names
+
+
+def test_every_declared_symbol_is_exported(eb):
+    lib = ctypes.CDLL(eb.LIB_PATH)
+    missing = [n for n in declared_functions() if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+def test_status_strings(eb):
+    for s in (0, -1, -2, -3, -4, 17):
+        assert eb.lib.eb_status_str(s)
+    assert eb.version().startswith("eb ")
+
+
+@pytest.mark.parametrize("qtype,qb", [("q8_0", 32), ("q4_0", 16)])
+@pytest.mark.parametrize("n,k", [(1, 32), (7, 96), (4096, 4096), (4096, 11008), (3, 288)])
+def test_layout(eb, qtype, qb, n, k):
+    L = eb.layout(qtype, n, k)
+    nb = k // 32
+    assert L.qs_offset == 0 and L.qs_row_bytes == nb * qb
+    assert L.d_offset % 256 == 0 and L.d_offset >= n * nb * qb and L.d_offset - n * nb * qb < 256
+    assert L.d_stride % 8 == 0 and nb <= L.d_stride < nb + 8
+    assert L.total_bytes % 256 == 0 and L.total_bytes >= L.d_offset + 2 * n * L.d_stride
+    assert L.canonical_bytes == n * nb * (2 + qb)
+    assert eb.qweights_bytes(qtype, n, k) == L.total_bytes
+
+
+def test_bytes_rejects_bad_sizes(eb):
+    assert eb.lib.eb_qweights_bytes(eb.EB_Q8_0, 4, 33) == 0
+    assert eb.lib.eb_qweights_bytes(3, 4, 32) == 0
+    assert eb.lib.eb_qweights_bytes(eb.EB_Q4_0, -1, 32) == 0
+    assert eb.lib.eb_qweights_layout(eb.EB_Q4_0, 4, 32, None) == eb.EB_ERR_INVALID
+
+
+def _w(eb, qtype=None, n=64, k=64, data=0x100000, reserved=0):
+    return eb.eb_qweights(qtype or eb.EB_Q8_0, reserved, n, k, data)
+
+
+# Fake, never-dereferenced addresses: every call below must be rejected on the host.
+X, Y = 0x200000, 0x400000
+
+
+@pytest.mark.parametrize("case,expect", [
+    ("null_w", -1), ("null_data", -1), ("bad_type", -1), ("reserved", -1), ("k33", -1),
+    ("k0", -1), ("n0", -1), ("m_neg", -1), ("bad_xt", -1), ("bad_path", -1), ("x_null", -1),
+    ("w_misaligned", -2), ("x_misaligned", -2), ("y_misaligned", -2), ("x_f32", -3),
+    ("y_f16", -3), ("gemv_m8", -3), ("gemv_big_k", -3), ("overlap", -1),
+])
+def test_qlinear_validation(eb, case, expect):
+    w = _w(eb)
+    x, y, m, xt, yt, path = X, Y, 4, eb.EB_F16, eb.EB_F32, eb.EB_PATH_AUTO
+    wp = ctypes.byref(w)
+    if case == "null_w":
+        wp = None
+    elif case == "null_data":
+        w.data = None
+    elif case == "bad_type":
+        w.type = 7
+    elif case == "reserved":
+        w.reserved = 1
+    elif case == "k33":
+        w.k = 33
+    elif case == "k0":
+        w.k = 0
+    elif case == "n0":
+        w.n = 0
+    elif case == "m_neg":
+        m = -1
+    elif case == "bad_xt":
+        xt = 9
+    elif case == "bad_path":
+        path = 5
+    elif case == "x_null":
+        x = None
+    elif case == "w_misaligned":
+        w.data = 0x100010
+    elif case == "x_misaligned":
+        x = X + 8
+    elif case == "y_misaligned":
+        y = Y + 4
+    elif case == "x_f32":
+        xt = eb.EB_F32
+    elif case == "y_f16":
+        yt = eb.EB_F16
+    elif case == "gemv_m8":
+        m, path = 8, eb.EB_PATH_GEMV
+    elif case == "gemv_big_k":
+        w.k, m, path = 65536, 2, eb.EB_PATH_GEMV
+        y = 0x10000000  # clear of the (fake) 4.4 MB weight range
+    elif case == "overlap":
+        y = X + 64
+    assert eb.lib.eb_qlinear_ex(wp, x, xt, m, y, yt, path, None) == expect
+
+
+def test_qlinear_m0_is_noop(eb):
+    w = _w(eb)
+    assert eb.lib.eb_qlinear(ctypes.byref(w), None, eb.EB_F16, 0, None, eb.EB_F32, None) == 0
+
+
+def test_quantize_validation(eb):
+    L = eb.lib
+    assert L.eb_quantize_q8_0(None, 0, 64, None, None) == 0          # empty: no-op
+    assert L.eb_quantize_q8_0(None, 4, 64, 0x100000, None) == -1    # null w
+    assert L.eb_quantize_q4_0(0x200000, 4, 48, 0x100000, None) == -1  # k % 32
+    assert L.eb_quantize_q4_0(0x200004, 4, 64, 0x100000, None) == -2  # w misaligned
+    assert L.eb_quantize_q4_0(0x200000, 4, 64, 0x100080, None) == -2  # out misaligned
+    assert L.eb_quantize_q8_0(0x200000, -1, 64, 0x100000, None) == -1
+
+
+def test_canonical_validation(eb):
+    w = _w(eb)
+    assert eb.lib.eb_qweights_to_canonical(ctypes.byref(w), None, None) == -1
+    assert eb.lib.eb_qweights_from_canonical(eb.EB_Q4_0, 0x200000, 4, 40, 0x100000, None) == -1
+    assert eb.lib.eb_qweights_from_canonical(eb.EB_Q4_0, 0x200000, 4, 64, 0x100040, None) == -2
+
+
+def test_stack_validation(eb):
+    ops = (eb.eb_qlinear_op * 2)()
+    ops[0] = eb.eb_qlinear_op(_w(eb), X, Y, 1, eb.EB_F16, eb.EB_F32)
+    ops[1] = eb.eb_qlinear_op(_w(eb, k=33), X, Y, 1, eb.EB_F16, eb.EB_F32)
+    assert eb.lib.eb_qlinear_stack(ops, 2, None) == -1   # second op invalid -> nothing launched
+    assert eb.lib.eb_qlinear_stack(ops, 0, None) == 0
+    assert eb.lib.eb_qlinear_stack(ops, -1, None) == -1
+    assert eb.lib.eb_qlinear_stack(None, 3, None) == -1
+
+
+def test_auto_path(eb):
+    f = eb.lib.eb_qlinear_auto_path
+    assert f(eb.EB_Q4_0, eb.EB_F16, 1, 4096, 4096) == eb.EB_PATH_GEMV
+    assert f(eb.EB_Q8_0, eb.EB_BF16, 816, 2560, 2048) == eb.EB_PATH_MFMA
+    assert f(eb.EB_Q8_0, eb.EB_BF16, 50, 2048, 1024) == eb.EB_PATH_MFMA
+    assert f(eb.EB_Q8_0, eb.EB_F16, 1, 4096, 1 << 20) == eb.EB_PATH_MFMA  # x too large for LDS
+    assert f(eb.EB_Q8_0, eb.EB_F16, 0, 64, 64) == eb.EB_ERR_INVALID

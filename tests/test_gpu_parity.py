@@ -1,0 +1,254 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Bars: packed weights bit-exact; every output within 2e-3 of the binary64
+oracle, normalised by sum_k |x||w_hat| (plus one bf16 rounding for bf16
+outputs); outputs whose bound is 0 are exactly 0.
+"""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as O
+from paper_2607_02501_amd import workloads as W
+from tests.gpu_helpers import TOL_BF16, TOL_F32, assert_parity, bits16, oracle_reference
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+@pytest.fixture(scope="module")
+def eb():
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a GPU")
+    from paper_2607_02501_amd import eb as _eb
+
+    return _eb
+
+
+def _case(seed, n, k, m, xdtype, wscale=W.WEIGHT_STD):
+    w = W.normal((n, k), seed, "cpu", wscale)
+    x = W.normal((m, k), seed + 1, "cpu").to(xdtype)
+    return w, x
+
+
+# ---------------------------------------------------------------------------
+# Packing
+# ---------------------------------------------------------------------------
+
+def _special_blocks():
+    rng = np.random.default_rng(21)
+    rows = []
+    z = np.zeros(32, np.float32)
+    rows.append(z)
+    e = z.copy(); e[0] = 1.0; rows.append(e)
+    e = z.copy(); e[17] = 1.0; rows.append(e)
+    rows.append(-rows[1])
+    t = z.copy(); t[0] = 127 * 2.0 ** -7; t[1] = 2.5 * 2.0 ** -7; t[2] = -2.5 * 2.0 ** -7; rows.append(t)
+    t = z.copy(); t[0] = -1.0; t[1] = 0.3125; t[2] = -0.3125; t[3] = 0.99; rows.append(t)
+    t = z.copy(); t[0], t[5] = 1.0, -1.0; rows.append(t)
+    rows.append(rng.standard_normal(32).astype(np.float32) * np.float32(1e-6))
+    rows.append(rng.standard_normal(32).astype(np.float32) * np.float32(2e-5))
+    rows.append(rng.standard_normal(32).astype(np.float32) * np.float32(1000))
+    rows.append((np.arange(32, dtype=np.float32) - 16) * np.float32(0.0625))
+    return np.stack(rows).reshape(-1, 32)
+
+
+@pytest.mark.parametrize("qtype", ["q8_0", "q4_0"])
+def test_packing_special_blocks_bit_exact(eb, oracle, qtype):
+    w = _special_blocks()
+    qw = eb.quantize(torch.from_numpy(w).to(DEV), qtype)
+    got = eb.to_canonical(qw).cpu().numpy()
+    ref = oracle.quantize(O.Q8_0 if qtype == "q8_0" else O.Q4_0, w)
+    assert np.array_equal(got, ref)
+
+
+@pytest.mark.parametrize("qtype", ["q8_0", "q4_0"])
+@pytest.mark.parametrize("n,k", [(1, 32), (37, 96), (300, 1056), (64, 11008)])
+def test_packing_random_bit_exact(eb, oracle, qtype, n, k):
+    w = W.normal((n, k), 100 + n + k, "cpu", 0.02)
+    qw = eb.quantize(w.to(DEV), qtype)
+    got = eb.to_canonical(qw).cpu().numpy()
+    ref = oracle.quantize(O.Q8_0 if qtype == "q8_0" else O.Q4_0, w.numpy())
+    assert np.array_equal(got, ref)
+    # the planar scale-plane padding is zero
+    L = eb.layout(qtype, n, k)
+    raw = qw.buf.cpu().numpy()
+    d = raw[L.d_offset:L.d_offset + 2 * n * L.d_stride].view(np.uint16).reshape(n, L.d_stride)
+    assert np.all(d[:, k // 32:] == 0)
+
+
+@pytest.mark.parametrize("qtype", ["q8_0", "q4_0"])
+def test_from_canonical_round_trip(eb, oracle, qtype):
+    n, k = 129, 352
+    w = W.normal((n, k), 5, "cpu", 0.02).numpy()
+    ref = oracle.quantize(O.Q8_0 if qtype == "q8_0" else O.Q4_0, w)
+    qw = eb.from_canonical(torch.from_numpy(ref).to(DEV), qtype, n, k)
+    assert np.array_equal(eb.to_canonical(qw).cpu().numpy(), ref)
+    qw2 = eb.quantize(torch.from_numpy(w).to(DEV), qtype)
+    assert torch.equal(qw.buf, qw2.buf)
+
+
+# ---------------------------------------------------------------------------
+# qlinear on small ragged shapes, every path
+# ---------------------------------------------------------------------------
+
+SHAPES = [(37, 96), (515, 1056), (130, 2080)]
+MS_GEMV = [1, 2, 3, 4]
+MS_MFMA = [1, 5, 9, 50, 64, 65, 130]
+
+
+@pytest.mark.parametrize("qtype", ["q8_0", "q4_0"])
+@pytest.mark.parametrize("xdtype", [torch.float16, torch.bfloat16])
+@pytest.mark.parametrize("n,k", SHAPES)
+def test_qlinear_gemv_parity(eb, oracle, qtype, xdtype, n, k):
+    w, x = _case(1000 + n, n, k, max(MS_GEMV), xdtype)
+    qw = eb.quantize(w.to(DEV), qtype)
+    _, y_ref, bound = oracle_reference(oracle, qtype, w.numpy(), x)
+    for m in MS_GEMV:
+        y = eb.qlinear(qw, x[:m].to(DEV), path="gemv")
+        assert_parity(y, y_ref[:m], bound[:m], TOL_F32, f"gemv m={m}")
+    y = eb.qlinear(qw, x[:1].to(DEV), out_dtype=torch.bfloat16, path="gemv")
+    assert_parity(y, y_ref[:1], bound[:1], TOL_BF16, "gemv bf16 out")
+
+
+@pytest.mark.parametrize("qtype", ["q8_0", "q4_0"])
+@pytest.mark.parametrize("xdtype", [torch.float16, torch.bfloat16])
+@pytest.mark.parametrize("n,k", SHAPES)
+def test_qlinear_mfma_parity(eb, oracle, qtype, xdtype, n, k):
+    w, x = _case(2000 + n, n, k, max(MS_MFMA), xdtype)
+    qw = eb.quantize(w.to(DEV), qtype)
+    _, y_ref, bound = oracle_reference(oracle, qtype, w.numpy(), x)
+    for m in MS_MFMA:
+        y = eb.qlinear(qw, x[:m].to(DEV), path="mfma")
+        assert_parity(y, y_ref[:m], bound[:m], TOL_F32, f"mfma m={m}")
+    y = eb.qlinear(qw, x.to(DEV), out_dtype=torch.bfloat16, path="mfma")
+    assert_parity(y, y_ref, bound, TOL_BF16, "mfma bf16 out")
+
+
+@pytest.mark.parametrize("qtype", ["q8_0", "q4_0"])
+def test_qlinear_auto_matches_forced_path(eb, qtype):
+    n, k = 300, 1024
+    w, x = _case(7, n, k, 70, torch.bfloat16)
+    qw = eb.quantize(w.to(DEV), qtype)
+    xd = x.to(DEV)
+    for m in (1, 4, 5, 70):
+        want = eb.auto_path(qtype, torch.bfloat16, m, n, k)
+        assert torch.equal(eb.qlinear(qw, xd[:m]), eb.qlinear(qw, xd[:m], path=want))
+
+
+# ---------------------------------------------------------------------------
+# Closed forms and invariants
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("qtype", ["q8_0", "q4_0"])
+@pytest.mark.parametrize("xdtype", [torch.float16, torch.bfloat16])
+def test_onehot_reads_out_weights(eb, oracle, qtype, xdtype):
+    n, k = 96, 128
+    w = W.normal((n, k), 31, "cpu", 0.02)
+    qw = eb.quantize(w.to(DEV), qtype)
+    blocks = oracle.quantize(O.Q8_0 if qtype == "q8_0" else O.Q4_0, w.numpy())
+    what = oracle.dequant(O.Q8_0 if qtype == "q8_0" else O.Q4_0, blocks, n, k)  # [n, k] float64
+    eye = torch.eye(k, dtype=xdtype, device=DEV)
+    # GEMV path: exact w_hat (code * d16 is exact in fp32)
+    for j in range(0, k, 4):
+        y = eb.qlinear(qw, eye[j:j + 4], path="gemv").double().cpu().numpy()
+        assert np.array_equal(y, what[:, j:j + 4].T)
+    # MFMA path: w_hat rounded once to the activation type
+    y = eb.qlinear(qw, eye, path="mfma").cpu()
+    rounded = torch.from_numpy(what.T.copy()).to(xdtype).float()
+    assert torch.equal(y, rounded)
+
+
+def test_zero_weights_give_exact_zero(eb):
+    n, k = 70, 256
+    qw = eb.quantize(torch.zeros((n, k), device=DEV), "q4_0")
+    x = torch.randn(9, k, device=DEV).to(torch.float16)
+    for path, m in (("gemv", 3), ("mfma", 9)):
+        y = eb.qlinear(qw, x[:m], path=path)
+        assert torch.count_nonzero(y) == 0
+
+
+@pytest.mark.parametrize("path,m", [("gemv", 1), ("gemv", 4), ("mfma", 50), ("mfma", 200)])
+def test_deterministic(eb, path, m):
+    n, k = 1000, 2048
+    w, x = _case(41, n, k, m, torch.bfloat16)
+    qw = eb.quantize(w.to(DEV), "q8_0")
+    xd = x.to(DEV)
+    a = eb.qlinear(qw, xd, path=path)
+    b = eb.qlinear(qw, xd, path=path)
+    assert torch.equal(a, b)
+
+
+def test_minimum_and_empty_shapes(eb, oracle):
+    w, x = _case(3, 1, 32, 4, torch.float16)
+    for qtype in ("q8_0", "q4_0"):
+        qw = eb.quantize(w.to(DEV), qtype)
+        _, y_ref, bound = oracle_reference(oracle, qtype, w.numpy(), x)
+        for path, m in (("gemv", 1), ("gemv", 4), ("mfma", 4)):
+            assert_parity(eb.qlinear(qw, x[:m].to(DEV), path=path), y_ref[:m], bound[:m], TOL_F32)
+        y = eb.qlinear(qw, x[:0].to(DEV))
+        assert y.shape == (0, 1)
+
+
+# ---------------------------------------------------------------------------
+# Stack: graph replay and direct launches give the single-call results
+# ---------------------------------------------------------------------------
+
+def test_stack_matches_single_calls(eb, monkeypatch):
+    shapes = [("q4_0", torch.float16, 1, 300, 512), ("q8_0", torch.bfloat16, 50, 200, 1024),
+              ("q4_0", torch.bfloat16, 130, 260, 352), ("q8_0", torch.float16, 3, 96, 4096)]
+    entries, refs = [], []
+    for i, (qt, xdt, m, n, k) in enumerate(shapes):
+        w, x = _case(500 + i, n, k, m, xdt)
+        qw = eb.quantize(w.to(DEV), qt)
+        xd = x.to(DEV)
+        y = torch.full((m, n), float("nan"), device=DEV)
+        entries.append((qw, xd, y))
+        refs.append(eb.qlinear(qw, xd))
+    ops = eb.make_ops(entries)
+    for mode in ("1", "1", "0"):  # capture, replay, direct
+        monkeypatch.setenv("EB_STACK_GRAPH", mode)
+        for _, _, y in entries:
+            y.fill_(float("nan"))
+        eb.qlinear_stack(ops)
+        torch.cuda.synchronize()
+        for (_, _, y), r in zip(entries, refs):
+            assert torch.equal(y, r)
+    eb.stack_cache_clear()
+
+
+# ---------------------------------------------------------------------------
+# Full-size workloads (the shapes the benchmark times), sampled outputs
+# ---------------------------------------------------------------------------
+
+def _sample_idx(total, count, rng, extra=()):
+    base = {0, total - 1, *[e for e in extra if 0 <= e < total]}
+    pool = rng.choice(total, size=min(total, count), replace=False)
+    return np.array(sorted(base | set(int(v) for v in pool)), dtype=np.int64)
+
+
+@pytest.mark.parametrize("name", list(W.WORKLOADS))
+def test_workload_sampled_parity(eb, oracle, name):
+    wl = W.WORKLOADS[name]
+    rng = np.random.default_rng(77)
+    for layer in sorted({0, wl.layers - 1}):
+        for p, (pname, k, n) in enumerate(wl.projections):
+            print(f"[parity] {name} layer={layer} proj={pname} m={wl.m} n={n} k={k}", flush=True)
+            w = W.weights(wl, layer, p, DEV)
+            x = W.activations(wl, layer, p, DEV)
+            qw = eb.quantize(w, wl.qtype)
+            y = eb.qlinear(qw, x)                        # auto path, as timed by the benchmark
+            cols = _sample_idx(n, 48, rng, extra=(127, 128, 255, 256))
+            rows = _sample_idx(wl.m, 24, rng, extra=(63, 64, 127, 128))
+            wrows = w[torch.from_numpy(cols).to(DEV)].cpu().numpy()
+            blocks, y_ref, bound = oracle_reference(oracle, wl.qtype, wrows, x[torch.from_numpy(rows).to(DEV)])
+            # packing of the sampled rows is bit-exact
+            canon = eb.to_canonical(qw)[torch.from_numpy(cols).to(DEV)].cpu().numpy()
+            assert np.array_equal(canon, blocks), f"{name} {pname}: packed bytes differ"
+            got = y[torch.from_numpy(rows).to(DEV)][:, torch.from_numpy(cols).to(DEV)]
+            assert_parity(got, y_ref, bound, TOL_F32, f"{name} layer {layer} {pname}")
+            del w, qw, y
+    torch.cuda.empty_cache()
