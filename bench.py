@@ -143,10 +143,11 @@ def main():
     log(f"[bench] timed {args.steps} passes: {ms:.4f} ms/pass")
 
     # ---- per-kernel durations ------------------------------------------------
-    # Ops that run the same kernel instance (same path, formats, m and k) are
-    # graph-replayed back to back; HIP events on the launch stream bracket
-    # `reps` replays, so the average launch duration excludes host launch cost
-    # and agrees with rocprofv3's per-kernel average.
+    # Ops that run the same kernel instance (same path, formats, m and k) form
+    # one stack, graph-replayed back to back (independent m == 1 ops become one
+    # fused launch); HIP events on the launch stream bracket `reps` replays, so
+    # the average launch duration excludes host launch cost and agrees with
+    # rocprofv3's per-kernel average.
     groups = {}
     for ent, (pname, m, n, k) in zip(entries, meta):
         key = (eb.auto_path(wl.qtype, wl.x_dtype, m, n, k), m, k)
@@ -164,7 +165,8 @@ def main():
             eb.qlinear_stack(gops)
         b.record()
         torch.cuda.synchronize()
-        kinds[key] = {"ms": a.elapsed_time(b) / reps, "launches": len(items),
+        kinds[key] = {"ms": a.elapsed_time(b) / reps, "launches": eb.stack_launches(gops),
+                      "ops": len(items),
                       "bytes": sum(op_bytes(wl.qtype, m, n, k) for _, m, n, k in items),
                       "flops": sum(2 * m * n * k for _, m, n, k in items)}
     eb.stack_cache_clear()
@@ -174,7 +176,8 @@ def main():
     path = dom[0]
     kernel_name = f"{path}_{wl.qtype}_{'f16' if wl.x_dtype == torch.float16 else 'bf16'}_m{dom[1]}_k{dom[2]}"
     for p, d in kinds.items():
-        log(f"[bench] kernel {p}: {d['launches']} launches/pass, avg {1e3 * d['ms'] / d['launches']:.2f} us, "
+        log(f"[bench] kernel {p}: {d['ops']} ops in {d['launches']} launches/pass, "
+            f"avg {1e3 * d['ms'] / d['launches']:.2f} us, "
             f"{d['bytes'] / d['ms'] / 1e6:.1f} GB/s, {d['flops'] / d['ms'] / 1e9:.2f} TFLOP/s")
     if path == "mfma":
         achieved = dk["flops"] / dk["launches"] / (avg_ms * 1e-3) / 1e12
@@ -187,6 +190,7 @@ def main():
     roof["kernel"] = kernel_name
     roof["avg_launch_us"] = round(avg_ms * 1e3, 3)
     roof["launches_per_pass"] = dk["launches"]
+    roof["ops_per_launch"] = dk["ops"] / dk["launches"]
     roof["algorithmic_per_launch"] = (dk["flops"] if path == "mfma" else dk["bytes"]) // dk["launches"]
     roof["traffic"] = load_traffic(wl.name, kernel_name)
 

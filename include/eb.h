@@ -39,7 +39,8 @@
  * Conventions for every entry point:
  *   - All pointers are DEVICE pointers unless stated otherwise; the caller owns
  *     every buffer (weights, activations, outputs).  The library never
- *     allocates device memory and never synchronises the stream.
+ *     synchronises the stream, and allocates device memory only for cached
+ *     stack plans (eb_qlinear_stack).
  *   - Work is enqueued on `stream` (0 = the null stream); EB_OK means the work
  *     was enqueued, not that it finished.
  *   - Arguments are validated on the host before anything is launched; on any
@@ -168,14 +169,29 @@ eb_status eb_qlinear_ex(const eb_qweights *w, const void *x, int32_t x_type, int
 /* Which path EB_PATH_AUTO takes for this problem (host-only, no launch). */
 int32_t eb_qlinear_auto_path(int32_t type, int32_t x_type, int64_t m, int64_t n, int64_t k);
 
-/* Run ops[0..n_ops) in order on `stream`, each exactly as eb_qlinear would
- * (paper section 3.2, graph replay and buffer reuse).  `ops` is a HOST array.
- * The first call with a given op list records the launches into a HIP graph
- * (captured on a library-owned stream); later calls with an identical list
- * (same pointers, sizes and types) replay it with one graph launch.  All ops
- * are validated before anything is enqueued.  n_ops == 0 is a no-op.
- * Set the environment variable EB_STACK_GRAPH=0 to launch the ops directly. */
+/* Run ops[0..n_ops) on `stream` with the results of running them in order,
+ * each as eb_qlinear would (paper section 3.2: graph replay, operator fusion,
+ * buffer reuse).  `ops` is a HOST array.  All ops are validated before
+ * anything is enqueued; n_ops == 0 is a no-op.
+ *   Fusion: a run of consecutive m == 1 ops with the same formats in which no
+ *   op reads or writes memory that an earlier op of the run writes (decided by
+ *   address ranges of x, y and the weights) is executed by one persistent
+ *   launch per K size class instead of one launch per op.  Results are bitwise
+ *   identical to the unfused order.  EB_STACK_FUSE=0 disables fusion.
+ *   Graph replay: the first call with a given op list (same pointers, sizes,
+ *   types) builds a plan, records it into a HIP graph on a library-owned
+ *   stream and caches both; later calls replay the graph with one launch.
+ *   EB_STACK_GRAPH=0 launches the plan directly instead.  Called while
+ *   `stream` itself is being captured, the ops are launched plainly into it.
+ * Memory: a plan with fused runs owns a small device table (about 64 bytes
+ * per fused op), allocated once when the plan is built and freed by
+ * eb_stack_cache_clear (or when more than 64 plans are cached). */
 eb_status eb_qlinear_stack(const eb_qlinear_op *ops, int32_t n_ops, hipStream_t stream);
+
+/* Number of kernel launches eb_qlinear_stack makes for this op list (host
+ * only; nothing is allocated or launched), or a negative eb_status if an op is
+ * invalid. */
+int32_t eb_qlinear_stack_launches(const eb_qlinear_op *ops, int32_t n_ops);
 
 /* Drop every cached stack graph (frees their host/driver resources). */
 eb_status eb_stack_cache_clear(void);

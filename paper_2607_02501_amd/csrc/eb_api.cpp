@@ -6,6 +6,7 @@
 // path is testable without a GPU and nothing is launched on error.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <atomic>
 #include <cstdlib>
 #include <cstring>
@@ -114,16 +115,156 @@ eb_status quantize_common(int32_t type, const float *w, int64_t n, int64_t k, vo
 }
 
 // ---------------------------------------------------------------------------
-// Stack graph cache: op list bytes + device -> instantiated graph.
+// Stack plans.  A plan runs the ops in order; consecutive m == 1 GEMV ops with
+// the same formats that neither read nor write what an earlier op of the run
+// writes (checked by address ranges) are fused: the run is issued as one
+// persistent launch per slot count, which is equivalent to running them in
+// order because no op of the run observes another.  The plan and its device
+// op table are cached per op list, together with the HIP graph that replays it.
 // ---------------------------------------------------------------------------
-struct GraphEntry {
+struct Range {
+  uintptr_t a, b;  // [a, b)
+  bool hits(const Range &o) const { return a < o.b && o.a < b; }
+};
+
+struct OpSpan {
+  Range x, y, w;
+};
+
+OpSpan span_of(const eb_qlinear_op &o) {
+  OpSpan s;
+  const uintptr_t x = reinterpret_cast<uintptr_t>(o.x), y = reinterpret_cast<uintptr_t>(o.y),
+                  w = reinterpret_cast<uintptr_t>(o.w.data);
+  s.x = {x, x + (uintptr_t)(o.m * o.w.k * 2)};
+  s.y = {y, y + (uintptr_t)(o.m * o.w.n * (int64_t)dsize(o.y_type))};
+  s.w = {w, w + (uintptr_t)eb_qweights_bytes(o.w.type, o.w.n, o.w.k)};
+  return s;
+}
+
+// op b may join a run containing op a only if neither observes the other
+bool independent(const OpSpan &a, const OpSpan &b) {
+  return !(b.x.hits(a.y) || b.y.hits(a.y) || b.y.hits(a.x) || b.y.hits(a.w) || b.w.hits(a.y));
+}
+
+struct Step {
+  int op = -1;        // single op index, or -1 for a fused launch
+  int32_t type = 0, xt = 0;
+  int ns = 0;
+  size_t table = 0;   // first entry in the device table
+  int nops = 0;
+  int64_t units = 0, rows = 0;
+};
+
+struct Plan {
+  std::vector<Step> steps;
+  M1Op *table = nullptr;  // device copy of every fused launch's op table
   hipGraph_t graph = nullptr;
   hipGraphExec_t exec = nullptr;
 };
 
+bool env_off(const char *name) {
+  const char *v = std::getenv(name);
+  return v && v[0] == '0';
+}
+
+bool fusable(const eb_qlinear_op &o) {
+  return o.m == 1 && gemv_fits(1, o.w.k) && m1_fusable(o.w.type, o.m, o.w.k);
+}
+
+// Builds the plan; with `alloc`, also allocates and fills its device table
+// when any run is fused (without it the plan is only counted).
+eb_status build_plan(const eb_qlinear_op *ops, int32_t n_ops, bool alloc, Plan &P) {
+  const bool allow_fuse = true;
+  std::vector<M1Op> host;
+  const bool fuse = allow_fuse && !env_off("EB_STACK_FUSE");
+  int32_t i = 0;
+  while (i < n_ops) {
+    if (!fuse || !fusable(ops[i])) {
+      Step s;
+      s.op = i++;
+      P.steps.push_back(s);
+      continue;
+    }
+    std::vector<int32_t> run{i};
+    std::vector<OpSpan> spans{span_of(ops[i])};
+    int32_t j = i + 1;
+    for (; j < n_ops; ++j) {
+      const eb_qlinear_op &o = ops[j];
+      if (!fusable(o) || o.w.type != ops[i].w.type || o.x_type != ops[i].x_type) break;
+      const OpSpan sj = span_of(o);
+      bool ok = true;
+      for (const OpSpan &sp : spans) ok = ok && independent(sp, sj);
+      if (!ok) break;
+      run.push_back(j);
+      spans.push_back(sj);
+    }
+    if (run.size() == 1) {
+      Step s;
+      s.op = i;
+      P.steps.push_back(s);
+    } else {
+      // one fused launch per slot count, in order of first appearance
+      std::vector<int> classes;
+      for (int32_t r : run) {
+        const int ns = m1_slots(ops[r].w.type, ops[r].w.k);
+        if (std::find(classes.begin(), classes.end(), ns) == classes.end()) classes.push_back(ns);
+      }
+      for (int ns : classes) {
+        Step s;
+        s.type = ops[i].w.type;
+        s.xt = ops[i].x_type;
+        s.ns = ns;
+        s.table = host.size();
+        for (int32_t r : run) {
+          const eb_qlinear_op &o = ops[r];
+          if (m1_slots(o.w.type, o.w.k) != ns) continue;
+          M1Op e;
+          s.units += m1_fill(o.w.type, o.w.data, o.w.n, o.w.k, o.x, o.y, o.y_type, s.units, &e);
+          s.rows += o.w.n;
+          host.push_back(e);
+          ++s.nops;
+        }
+        P.steps.push_back(s);
+      }
+    }
+    i = j;
+  }
+  if (alloc && !host.empty()) {
+    if (hipMalloc((void **)&P.table, host.size() * sizeof(M1Op)) != hipSuccess) {
+      P.table = nullptr;
+      return EB_ERR_HIP;
+    }
+    if (hipMemcpy(P.table, host.data(), host.size() * sizeof(M1Op), hipMemcpyHostToDevice) !=
+        hipSuccess)
+      return EB_ERR_HIP;
+  }
+  return EB_OK;
+}
+
+eb_status run_plan(const eb_qlinear_op *ops, const Plan &P, hipStream_t s) {
+  for (const Step &st : P.steps) {
+    if (st.op >= 0) {
+      const eb_qlinear_op &o = ops[st.op];
+      eb_status r = launch_linear(&o.w, o.x, o.x_type, o.m, o.y, o.y_type, EB_PATH_AUTO, s);
+      if (r != EB_OK) return r;
+    } else if (launch_gemv_m1_multi(st.type, st.xt, st.ns, P.table + st.table, st.nops, st.units,
+                                    st.rows, s) != hipSuccess) {
+      return EB_ERR_HIP;
+    }
+  }
+  return EB_OK;
+}
+
+void destroy_plan(Plan &p) {
+  if (p.exec) (void)hipGraphExecDestroy(p.exec);
+  if (p.graph) (void)hipGraphDestroy(p.graph);
+  if (p.table) (void)hipFree(p.table);
+  p = Plan();
+}
+
 struct StackCache {
   std::mutex mu;
-  std::unordered_map<std::string, GraphEntry> map;
+  std::unordered_map<std::string, Plan> map;
   hipStream_t capture_stream[64] = {};
 };
 
@@ -132,18 +273,12 @@ StackCache &cache() {
   return *c;
 }
 
-constexpr size_t kMaxCachedGraphs = 64;
+constexpr size_t kMaxCachedPlans = 64;
 
-void destroy_entry(GraphEntry &g) {
-  if (g.exec) (void)hipGraphExecDestroy(g.exec);
-  if (g.graph) (void)hipGraphDestroy(g.graph);
-  g.exec = nullptr;
-  g.graph = nullptr;
-}
-
-bool graphs_enabled() {
-  const char *v = std::getenv("EB_STACK_GRAPH");
-  return !(v && v[0] == '0');
+void clear_cache_locked(StackCache &C) {
+  if (!C.map.empty()) (void)hipDeviceSynchronize();  // tables may still be in use
+  for (auto &kv : C.map) destroy_plan(kv.second);
+  C.map.clear();
 }
 
 eb_status run_ops_direct(const eb_qlinear_op *ops, int32_t n_ops, hipStream_t s) {
@@ -246,52 +381,76 @@ eb_status eb_qlinear_stack(const eb_qlinear_op *ops, int32_t n_ops, hipStream_t 
     eb_status st = check_linear(&o.w, o.x, o.x_type, o.m, o.y, o.y_type, EB_PATH_AUTO);
     if (st != EB_OK) return st;
   }
+  // Inside a caller's own stream capture, record plain launches into it.
   hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
-  if (!graphs_enabled() || hipStreamIsCapturing(stream, &cs) != hipSuccess ||
-      cs != hipStreamCaptureStatusNone)
+  if (hipStreamIsCapturing(stream, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone)
     return run_ops_direct(ops, n_ops, stream);
 
   int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return run_ops_direct(ops, n_ops, stream);
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return EB_ERR_HIP;
+  const bool use_graph = !env_off("EB_STACK_GRAPH");
   std::string key(reinterpret_cast<const char *>(&dev), sizeof(dev));
+  key.push_back(use_graph ? 'g' : 'd');
+  key.push_back(env_off("EB_STACK_FUSE") ? 'u' : 'f');
   key.append(reinterpret_cast<const char *>(ops), sizeof(eb_qlinear_op) * (size_t)n_ops);
 
   StackCache &C = cache();
   std::lock_guard<std::mutex> lock(C.mu);
   auto it = C.map.find(key);
   if (it == C.map.end()) {
-    if (!C.capture_stream[dev] &&
-        hipStreamCreateWithFlags(&C.capture_stream[dev], hipStreamNonBlocking) != hipSuccess) {
-      C.capture_stream[dev] = nullptr;
-      return EB_ERR_HIP;
+    if (C.map.size() >= kMaxCachedPlans) clear_cache_locked(C);
+    Plan P;
+    eb_status st = build_plan(ops, n_ops, true, P);
+    if (st != EB_OK) {
+      destroy_plan(P);
+      return st;
     }
-    hipStream_t cap = C.capture_stream[dev];
-    if (hipStreamBeginCapture(cap, hipStreamCaptureModeRelaxed) != hipSuccess) return EB_ERR_HIP;
-    eb_status st = run_ops_direct(ops, n_ops, cap);
-    GraphEntry g;
-    hipError_t e = hipStreamEndCapture(cap, &g.graph);
-    if (st != EB_OK || e != hipSuccess || !g.graph) {
-      destroy_entry(g);
-      return EB_ERR_HIP;
+    if (use_graph) {
+      if (!C.capture_stream[dev] &&
+          hipStreamCreateWithFlags(&C.capture_stream[dev], hipStreamNonBlocking) != hipSuccess) {
+        C.capture_stream[dev] = nullptr;
+        destroy_plan(P);
+        return EB_ERR_HIP;
+      }
+      hipStream_t cap = C.capture_stream[dev];
+      if (hipStreamBeginCapture(cap, hipStreamCaptureModeRelaxed) != hipSuccess) {
+        destroy_plan(P);
+        return EB_ERR_HIP;
+      }
+      st = run_plan(ops, P, cap);
+      hipError_t e = hipStreamEndCapture(cap, &P.graph);
+      if (st != EB_OK || e != hipSuccess || !P.graph ||
+          hipGraphInstantiate(&P.exec, P.graph, nullptr, nullptr, 0) != hipSuccess) {
+        destroy_plan(P);
+        return EB_ERR_HIP;
+      }
     }
-    if (hipGraphInstantiate(&g.exec, g.graph, nullptr, nullptr, 0) != hipSuccess) {
-      destroy_entry(g);
-      return EB_ERR_HIP;
-    }
-    if (C.map.size() >= kMaxCachedGraphs) {
-      for (auto &kv : C.map) destroy_entry(kv.second);
-      C.map.clear();
-    }
-    it = C.map.emplace(std::move(key), g).first;
+    it = C.map.emplace(std::move(key), P).first;
   }
-  return hipGraphLaunch(it->second.exec, stream) == hipSuccess ? EB_OK : EB_ERR_HIP;
+  const Plan &P = it->second;
+  if (P.exec) return hipGraphLaunch(P.exec, stream) == hipSuccess ? EB_OK : EB_ERR_HIP;
+  return run_plan(ops, P, stream);
+}
+
+int32_t eb_qlinear_stack_launches(const eb_qlinear_op *ops, int32_t n_ops) {
+  if (n_ops < 0 || (n_ops > 0 && !ops)) return EB_ERR_INVALID;
+  for (int32_t i = 0; i < n_ops; ++i) {
+    const eb_qlinear_op &o = ops[i];
+    eb_status st = check_linear(&o.w, o.x, o.x_type, o.m, o.y, o.y_type, EB_PATH_AUTO);
+    if (st != EB_OK) return st;
+  }
+  Plan P;
+  build_plan(ops, n_ops, false, P);
+  int32_t launches = 0;
+  for (const Step &st : P.steps)
+    if (st.op < 0 || ops[st.op].m > 0) ++launches;
+  return launches;
 }
 
 eb_status eb_stack_cache_clear(void) {
   StackCache &C = cache();
   std::lock_guard<std::mutex> lock(C.mu);
-  for (auto &kv : C.map) destroy_entry(kv.second);
-  C.map.clear();
+  clear_cache_locked(C);
   return EB_OK;
 }
 

@@ -47,6 +47,31 @@ constexpr int64_t kGemvMaxMK = 65536;
 hipError_t launch_gemv(int32_t type, const void *wdata, int64_t n, int64_t k, const void *x,
                        int32_t xt, int64_t m, void *y, int32_t yt, hipStream_t s);
 
+// Fused m == 1 GEMV over several independent matrices (one launch).  The
+// table lives in device memory; unit_begin (prefix sum of n * ku) ascends.
+struct M1Op {
+  const uint8_t *w;   // planar weights
+  const uint16_t *x;  // activations [k]
+  void *y;            // outputs [n]
+  int64_t n;
+  int64_t d_off;      // scale-plane offset
+  int64_t ds;         // scale-plane row stride (elements)
+  int64_t unit_begin; // work units (16-byte code units) before this matrix
+  int32_t k;
+  int32_t ku;         // 16-byte code units per row
+  int32_t yt;
+  int32_t pad;
+};
+bool m1_fusable(int32_t type, int64_t m, int64_t k);
+int m1_slots(int32_t type, int64_t k);
+// Fills *o for one matrix; returns its number of work units (n * ku).
+int64_t m1_fill(int32_t type, const void *wdata, int64_t n, int64_t k, const void *x, void *y,
+                int32_t yt, int64_t unit_begin, M1Op *o);
+// All matrices of one launch have the same slot count ns (m1_slots); units
+// and rows are the totals over the table.
+hipError_t launch_gemv_m1_multi(int32_t type, int32_t xt, int ns, const M1Op *dev_ops, int nops,
+                                int64_t units, int64_t rows, hipStream_t s);
+
 // MFMA path: any m
 hipError_t launch_mfma(int32_t type, const void *wdata, int64_t n, int64_t k, const void *x,
                        int32_t xt, int64_t m, void *y, int32_t yt, hipStream_t s);

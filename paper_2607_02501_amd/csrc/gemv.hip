@@ -401,31 +401,29 @@ __device__ inline __amdgpu_buffer_rsrc_t rsrc(const void *base, uint32_t bytes) 
                                            0x00020000);
 }
 
-// WPE: minimum waves per SIMD the register allocation must allow; memory
-// latency is hidden by other waves rather than by deep per-wave prefetch.
-template <int QT, int XT, int NS, int R, int WPE>
-__global__ void __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(WPE)))
-    gemv_m1_kernel(const uint8_t *__restrict__ wdata, int64_t n, int64_t k, int64_t d_off,
-                   int64_t ds, const uint16_t *__restrict__ x, void *__restrict__ y, int yt) {
+// Rows g*R .. g*R+R-1 for groups g = g0, g0 + gstride, ... < g_end of one
+// matrix, m == 1.  Called by every thread of the workgroup (it stages x into
+// LDS and synchronises once); waves whose first group is past g_end only help
+// with the staging.
+template <int QT, int XT, int NS, int R>
+__device__ __attribute__((always_inline)) inline void m1_rows(const uint8_t *__restrict__ wdata, int64_t n, int64_t k,
+                               int64_t d_off, int64_t ds, const uint16_t *__restrict__ x,
+                               void *__restrict__ y, int yt, int64_t g, int64_t g_end,
+                               int64_t gstride, uint4 *smem) {
   constexpr int CH = Unit<QT>::kChunks;
   // LDS: CH chunk rows of P entries; entry 64 * NS of every row is zero and
   // stands in for units past the end of the row.  P is a compile-time
   // constant so every x read is one base register plus an immediate offset.
   constexpr int P = 64 * NS + 1;
   const int ku = (int)(k / Unit<QT>::kElems);  // 64 * (NS - 1) < ku <= 64 * NS
-  extern __shared__ uint4 smem[];
   uint4 *xs = smem;
   float *xoff = reinterpret_cast<float *>(smem + CH * P);
   const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
-  const int64_t groups = (n + R - 1) / R;
-  const int64_t gstride = (int64_t)gridDim.x * kWaves;
-  int64_t g = (int64_t)blockIdx.x * kWaves + wave;
   const uint32_t qs_row = (uint32_t)ku * 16u, d_row = (uint32_t)(ds * 2);
   const uint8_t *__restrict__ dbase = wdata + d_off;
 
   // Per-lane byte offsets of the lane's units inside a row, fixed for the
-  // launch.  Units past the end of the row (last slot only) are clamped to the
+  // call.  Units past the end of the row (last slot only) are clamped to the
   // row's last unit; their x fragment is zero, so they add exactly 0.
   uint32_t qoff[NS], doff[NS], xidx[NS];
 #pragma unroll
@@ -439,7 +437,7 @@ __global__ void __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_e
 
   uint4 q[NS][R];
   uint16_t dh[NS][R];
-  auto load_group = [&](int64_t grp) {
+  auto load_group = [&](int64_t grp) __attribute__((always_inline)) {
 #pragma unroll
     for (int r = 0; r < R; ++r) {
       int64_t row = grp * R + r;
@@ -455,13 +453,13 @@ __global__ void __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_e
     }
   };
   // weight loads of the first group are in flight while x is staged
-  if (g < groups) load_group(g);
+  if (g < g_end) load_group(g);
   stage_x<QT, XT, 1>(x, 1, k, ku, xs, xoff, P);
   if (threadIdx.x < CH) xs[threadIdx.x * P + 64 * NS] = make_uint4(0, 0, 0, 0);
   if (threadIdx.x == 0) xoff[64 * NS] = 0.f;
   __syncthreads();
 
-  while (g < groups) {
+  while (g < g_end) {
     float acc[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) acc[r] = 0.f;
@@ -490,10 +488,68 @@ __global__ void __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_e
     g += gstride;
     // the weight registers are free again: load the next group into them
     __builtin_amdgcn_sched_barrier(0);
-    if (g < groups) load_group(g);
+    if (g < g_end) load_group(g);
   }
 }
 
+// One matrix per launch.  WPE: minimum waves per SIMD the register allocation
+// must allow; memory latency is hidden by other waves rather than by deep
+// per-wave prefetch.
+template <int QT, int XT, int NS, int R, int WPE>
+__global__ void __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(WPE)))
+    gemv_m1_kernel(const uint8_t *__restrict__ wdata, int64_t n, int64_t k, int64_t d_off,
+                   int64_t ds, const uint16_t *__restrict__ x, void *__restrict__ y, int yt) {
+  extern __shared__ uint4 smem[];
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
+  m1_rows<QT, XT, NS, R>(wdata, n, k, d_off, ds, x, y, yt, (int64_t)blockIdx.x * kWaves + wave,
+                         (n + R - 1) / R, (int64_t)gridDim.x * kWaves, smem);
+}
+
+// Rows per wave for the fused multi-matrix kernel, by slot count (no spills
+// at 4 waves per SIMD).
+// (The one-matrix kernel uses the same rows per wave by default, so a fused
+// stack and single calls add in the same order and agree bitwise.)
+__host__ __device__ constexpr int m1_multi_rows(int ns) { return ns <= 4 ? 2 : 1; }
+
+// Several independent matrices (m == 1, same formats, same slot count NS) in
+// one persistent launch, so the matrices of a stack overlap instead of each
+// paying a launch, an x staging and a ramp-up.  The launch's work, rows
+// weighted by their length (units), is cut into gridDim.x equal shares:
+// workgroup b takes units [b U / G, (b+1) U / G) of the concatenated matrices,
+// converted to row boundaries rounded down to whole R-row groups (both
+// neighbours round the same boundary the same way, so every row is computed
+// exactly once), and stages each matrix's x once for the part it covers.
+template <int QT, int XT, int NS>
+__global__ void __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(NS <= 2 ? 4 : 3)))
+    gemv_m1_multi_kernel(const M1Op *__restrict__ ops, int nops, int64_t units) {
+  constexpr int R = m1_multi_rows(NS);
+  extern __shared__ uint4 smem[];
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int64_t G = gridDim.x;
+  const int64_t u0 = units * (int64_t)blockIdx.x / G, u1 = units * ((int64_t)blockIdx.x + 1) / G;
+  // first matrix whose units reach past u0 (binary search; unit_begin ascends)
+  int lo = 0, hi = nops - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) / 2;
+    if (ops[mid].unit_begin <= u0) lo = mid; else hi = mid - 1;
+  }
+  for (int op = lo; op < nops && ops[op].unit_begin < u1; ++op) {
+    const M1Op o = ops[op];
+    // row boundary of unit u inside this matrix, rounded down to a whole group
+    auto row_at = [&](int64_t u) {
+      int64_t r = (u - o.unit_begin) / o.ku;
+      r = r < 0 ? 0 : (r > o.n ? o.n : r);
+      return r == o.n ? r : r / R * R;
+    };
+    const int64_t r0 = row_at(u0), r1 = row_at(u1);
+    if (r0 >= r1) continue;  // uniform across the workgroup
+    m1_rows<QT, XT, NS, R>(o.w, o.n, o.k, o.d_off, o.ds, o.x, o.y, o.yt, r0 / R + wave,
+                           (r1 + R - 1) / R, kWaves, smem);
+    __syncthreads();  // the next matrix restages LDS
+  }
+}
+
+// ---------------------------------------------------------------------------
 template <int QT, int XT, int NS, int R, int WPE>
 hipError_t launch_m1_t(const void *wdata, int64_t n, int64_t k, const void *x, void *y, int32_t yt,
                        hipStream_t s, int wg_per_cu) {
@@ -523,9 +579,7 @@ M1Shape m1_shape(int64_t ns) {
     M1Shape v{0, 0, 0};
     if (sscanf(env, "%d,%d,%d", &v.r, &v.wpe, &v.wg) == 3 && v.r > 0 && v.wpe > 0 && v.wg > 0) return v;
   }
-  if (ns <= 1) return {4, 4, 4};
-  if (ns <= 2) return {2, 4, 4};
-  return {1, 4, 4};
+  return {m1_multi_rows((int)ns), 4, 4};
 }
 
 template <int QT, int XT, int NS>
@@ -587,7 +641,71 @@ hipError_t launch_m(const void *wdata, int64_t n, int64_t k, const void *x, int6
   return launch_t<QT, XT, 4, 1>(wdata, n, k, x, m, y, yt, s);
 }
 
+template <int QT, int XT, int NS>
+hipError_t launch_multi_t(const M1Op *ops, int nops, int64_t units, int64_t rows,
+                          hipStream_t s) {
+  const size_t lds = (size_t)(64 * NS + 1) * (Unit<QT>::kChunks * 16 + 4);
+  int64_t grid = (int64_t)device_cu_count() * 4;
+  const int64_t groups = rows / (kWaves * m1_multi_rows(NS));  // keep every wave busy
+  if (grid > groups) grid = groups > 0 ? groups : 1;
+  gemv_m1_multi_kernel<QT, XT, NS><<<(unsigned)grid, 64 * kWaves, lds, s>>>(ops, nops, units);
+  return hipGetLastError();
+}
+
+template <int QT, int XT>
+hipError_t launch_multi_q(const M1Op *ops, int nops, int64_t items, int64_t rows, int ns,
+                          hipStream_t s) {
+  switch (ns) {
+    case 1: return launch_multi_t<QT, XT, 1>(ops, nops, items, rows, s);
+    case 2: return launch_multi_t<QT, XT, 2>(ops, nops, items, rows, s);
+    case 3: return launch_multi_t<QT, XT, 3>(ops, nops, items, rows, s);
+    case 4: return launch_multi_t<QT, XT, 4>(ops, nops, items, rows, s);
+    case 5: return launch_multi_t<QT, XT, 5>(ops, nops, items, rows, s);
+    case 6: return launch_multi_t<QT, XT, 6>(ops, nops, items, rows, s);
+    case 7: return launch_multi_t<QT, XT, 7>(ops, nops, items, rows, s);
+    case 8: return launch_multi_t<QT, XT, 8>(ops, nops, items, rows, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
 }  // namespace
+
+bool m1_fusable(int32_t type, int64_t m, int64_t k) {
+  const int64_t e = (type == EB_Q4_0) ? Unit<EB_Q4_0>::kElems : Unit<EB_Q8_0>::kElems;
+  return m == 1 && (k / e + 63) / 64 <= kM1MaxSlots;
+}
+
+int m1_slots(int32_t type, int64_t k) {
+  const int64_t e = (type == EB_Q4_0) ? Unit<EB_Q4_0>::kElems : Unit<EB_Q8_0>::kElems;
+  return (int)((k / e + 63) / 64);
+}
+
+int64_t m1_fill(int32_t type, const void *wdata, int64_t n, int64_t k, const void *x, void *y,
+                int32_t yt, int64_t unit_begin, M1Op *o) {
+  const int64_t e = (type == EB_Q4_0) ? Unit<EB_Q4_0>::kElems : Unit<EB_Q8_0>::kElems;
+  const Layout L = layout_of(type, n, k);
+  o->w = (const uint8_t *)wdata;
+  o->x = (const uint16_t *)x;
+  o->y = y;
+  o->n = n;
+  o->d_off = L.d_off;
+  o->ds = L.ds;
+  o->unit_begin = unit_begin;
+  o->k = (int32_t)k;
+  o->ku = (int32_t)(k / e);
+  o->yt = yt;
+  return n * (k / e);
+}
+
+hipError_t launch_gemv_m1_multi(int32_t type, int32_t xt, int ns, const M1Op *dev_ops, int nops,
+                                int64_t units, int64_t rows, hipStream_t s) {
+  if (type == EB_Q4_0) {
+    if (xt == EB_F16) return launch_multi_q<EB_Q4_0, EB_F16>(dev_ops, nops, units, rows, ns, s);
+    return launch_multi_q<EB_Q4_0, EB_BF16>(dev_ops, nops, units, rows, ns, s);
+  }
+  if (xt == EB_F16) return launch_multi_q<EB_Q8_0, EB_F16>(dev_ops, nops, units, rows, ns, s);
+  return launch_multi_q<EB_Q8_0, EB_BF16>(dev_ops, nops, units, rows, ns, s);
+}
 
 hipError_t launch_gemv(int32_t type, const void *wdata, int64_t n, int64_t k, const void *x,
                        int32_t xt, int64_t m, void *y, int32_t yt, hipStream_t s) {

@@ -83,6 +83,8 @@ lib.eb_qlinear_auto_path.restype = _i32
 lib.eb_qlinear_auto_path.argtypes = [_i32, _i32, _i64, _i64, _i64]
 lib.eb_qlinear_stack.restype = _i32
 lib.eb_qlinear_stack.argtypes = [ctypes.POINTER(eb_qlinear_op), _i32, _vp]
+lib.eb_qlinear_stack_launches.restype = _i32
+lib.eb_qlinear_stack_launches.argtypes = [ctypes.POINTER(eb_qlinear_op), _i32]
 lib.eb_stack_cache_clear.restype = _i32
 lib.eb_stack_cache_clear.argtypes = []
 
@@ -207,6 +209,14 @@ def make_ops(entries) -> ctypes.Array:
 
 def qlinear_stack(ops: ctypes.Array, device=None) -> None:
     _check(lib.eb_qlinear_stack(ops, len(ops), _stream(device)), "eb_qlinear_stack")
+
+
+def stack_launches(ops: ctypes.Array) -> int:
+    """Kernel launches eb_qlinear_stack makes for this op list (host-only)."""
+    n = lib.eb_qlinear_stack_launches(ops, len(ops))
+    if n < 0:
+        raise EBError(n, "eb_qlinear_stack_launches")
+    return n
 
 
 def stack_cache_clear() -> None:

@@ -166,3 +166,67 @@ def test_auto_path(eb):
     assert f(eb.EB_Q8_0, eb.EB_BF16, 50, 2048, 1024) == eb.EB_PATH_MFMA
     assert f(eb.EB_Q8_0, eb.EB_F16, 1, 4096, 1 << 20) == eb.EB_PATH_MFMA  # x too large for LDS
     assert f(eb.EB_Q8_0, eb.EB_F16, 0, 64, 64) == eb.EB_ERR_INVALID
+
+
+# ---------------------------------------------------------------------------
+# Stack plans: which runs of ops are fused (host-only; addresses are fake)
+# ---------------------------------------------------------------------------
+
+def _op(eb, data, x, y, k=4096, n=4096, m=1, qtype=None, xt=None, yt=None):
+    return eb.eb_qlinear_op(eb.eb_qweights(qtype or eb.EB_Q4_0, 0, n, k, data), x, y, m,
+                            xt or eb.EB_F16, yt or eb.EB_F32)
+
+
+def _launches(eb, ops):
+    arr = (eb.eb_qlinear_op * len(ops))(*ops)
+    return eb.lib.eb_qlinear_stack_launches(arr, len(ops))
+
+
+GB = 1 << 30
+
+
+def test_stack_fuses_independent_decode_ops(eb, monkeypatch):
+    monkeypatch.delenv("EB_STACK_FUSE", raising=False)
+    ops = [_op(eb, 1 * GB + i * (64 << 20), 8 * GB + i * 65536, 9 * GB + i * 65536) for i in range(12)]
+    assert _launches(eb, ops) == 1
+    # two K size classes (4096: 2 slots, 11008: 6 slots) -> one launch each
+    ops += [_op(eb, 3 * GB + i * (64 << 20), 10 * GB + i * 65536, 11 * GB + i * 65536, k=11008)
+            for i in range(4)]
+    assert _launches(eb, ops) == 2
+    monkeypatch.setenv("EB_STACK_FUSE", "0")
+    assert _launches(eb, ops) == len(ops)
+
+
+def test_stack_respects_dependencies(eb, monkeypatch):
+    monkeypatch.delenv("EB_STACK_FUSE", raising=False)
+    W0, W1, W2 = 1 * GB, 2 * GB, 3 * GB
+    X, Y0, Y1 = 8 * GB, 9 * GB, 10 * GB
+    # read-after-write: op1 reads op0's output (bf16 y feeding the next x)
+    raw = [_op(eb, W0, X, Y0, yt=eb.EB_BF16), _op(eb, W1, Y0, Y1, xt=eb.EB_BF16)]
+    assert _launches(eb, raw) == 2
+    # write-after-read: op1 overwrites op0's input
+    war = [_op(eb, W0, X, Y0), _op(eb, W1, 20 * GB, X, xt=eb.EB_BF16, yt=eb.EB_BF16)]
+    assert _launches(eb, war) == 2
+    # write-after-write on the same output
+    waw = [_op(eb, W0, X, Y0), _op(eb, W1, X + 65536, Y0)]
+    assert _launches(eb, waw) == 2
+    # independent again after the dependency: [a, b | c, d] -> 2 launches
+    bf = eb.EB_BF16
+    chain = [_op(eb, W0, X, Y0, xt=bf, yt=bf), _op(eb, W1, X + 65536, Y1, xt=bf),
+             _op(eb, W2, Y0, 11 * GB, xt=bf), _op(eb, 4 * GB, X + 2 * 65536, 12 * GB, xt=bf)]
+    assert _launches(eb, chain) == 2
+
+
+def test_stack_breaks_runs_on_format_and_m(eb, monkeypatch):
+    monkeypatch.delenv("EB_STACK_FUSE", raising=False)
+    a = [_op(eb, 1 * GB + i * (64 << 20), 8 * GB + i * 65536, 9 * GB + i * 65536) for i in range(3)]
+    q8 = _op(eb, 5 * GB, 10 * GB, 11 * GB, qtype=eb.EB_Q8_0)
+    b = [_op(eb, 6 * GB + i * (64 << 20), 12 * GB + i * 65536, 13 * GB + i * 65536) for i in range(3)]
+    assert _launches(eb, a + [q8] + b) == 3
+    m4 = _op(eb, 5 * GB, 10 * GB, 11 * GB, m=4)
+    assert _launches(eb, a + [m4] + b) == 3
+    m0 = _op(eb, 5 * GB, 10 * GB, 11 * GB, m=0)
+    assert _launches(eb, a + [m0] + b) == 2  # an empty op launches nothing
+    assert _launches(eb, [a[0]]) == 1
+    bad = a + [_op(eb, 5 * GB, 10 * GB, 11 * GB, k=33)]
+    assert _launches(eb, bad) == eb.EB_ERR_INVALID

@@ -220,6 +220,56 @@ def test_stack_matches_single_calls(eb, monkeypatch):
     eb.stack_cache_clear()
 
 
+@pytest.mark.parametrize("qtype", ["q4_0", "q8_0"])
+@pytest.mark.parametrize("xdtype", [torch.float16, torch.bfloat16])
+def test_fused_decode_stack_matches_single_calls(eb, qtype, xdtype, monkeypatch):
+    """Independent m == 1 ops of several K classes run as fused launches and
+    give bitwise the same outputs as one call per op."""
+    monkeypatch.delenv("EB_STACK_FUSE", raising=False)
+    shapes = [(512, 300), (4096, 1000), (1024, 64), (11008 if qtype == "q4_0" else 6144, 257),
+              (4096, 4097), (32, 5), (2048, 2048), (1024, 640)]
+    entries, refs = [], []
+    for i, (k, n) in enumerate(shapes):
+        w, x = _case(800 + i, n, k, 1, xdtype)
+        qw = eb.quantize(w.to(DEV), qtype)
+        xd = x.to(DEV)
+        y = torch.full((1, n), float("nan"), device=DEV, dtype=torch.bfloat16 if i % 3 == 2 else torch.float32)
+        entries.append((qw, xd, y))
+        refs.append(eb.qlinear(qw, xd, out_dtype=y.dtype))
+    ops = eb.make_ops(entries)
+    assert eb.stack_launches(ops) < len(shapes)
+    for mode in ("1", "1", "0"):
+        monkeypatch.setenv("EB_STACK_GRAPH", mode)
+        for _, _, y in entries:
+            y.fill_(float("nan"))
+        eb.qlinear_stack(ops)
+        torch.cuda.synchronize()
+        for (_, _, y), r in zip(entries, refs):
+            assert torch.equal(y, r)
+    eb.stack_cache_clear()
+
+
+def test_stack_dependent_chain(eb, oracle, monkeypatch):
+    """op 1 reads op 0's bf16 output: the plan must not fuse them."""
+    monkeypatch.delenv("EB_STACK_FUSE", raising=False)
+    k0, n0, n1 = 1024, 512, 384
+    w0, x0 = _case(900, n0, k0, 1, torch.bfloat16)
+    w1, _ = _case(901, n1, n0, 1, torch.bfloat16)
+    q0, q1 = eb.quantize(w0.to(DEV), "q4_0"), eb.quantize(w1.to(DEV), "q4_0")
+    xd = x0.to(DEV)
+    y0 = torch.empty((1, n0), dtype=torch.bfloat16, device=DEV)
+    y1 = torch.empty((1, n1), dtype=torch.float32, device=DEV)
+    ops = eb.make_ops([(q0, xd, y0), (q1, y0, y1)])
+    assert eb.stack_launches(ops) == 2
+    eb.qlinear_stack(ops)
+    torch.cuda.synchronize()
+    ref0 = eb.qlinear(q0, xd, out_dtype=torch.bfloat16)
+    assert torch.equal(y0, ref0)
+    _, y_ref, bound = oracle_reference(oracle, "q4_0", w1.numpy(), ref0)
+    assert_parity(y1, y_ref, bound, TOL_F32, "chained op")
+    eb.stack_cache_clear()
+
+
 # ---------------------------------------------------------------------------
 # Full-size workloads (the shapes the benchmark times), sampled outputs
 # ---------------------------------------------------------------------------
