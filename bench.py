@@ -22,7 +22,6 @@ Prints ONE JSON line:
 from __future__ import annotations
 
 import argparse
-import hashlib
 import json
 import os
 import sys
@@ -51,6 +50,9 @@ def parse():
     ap.add_argument("--cpu-layers", type=int, default=None, help="layers in the oracle sample")
     ap.add_argument("--cpu-rows", type=int, default=None, help="activation rows in the oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
+                    help="first run a plain device-to-device copy of BYTES (for scaling "
+                         "rocprofv3 FETCH_SIZE / WRITE_SIZE counters)")
     return ap.parse_args()
 
 
@@ -62,24 +64,19 @@ def op_bytes(qtype, m, n, k):
     return weight_bytes(qtype, n, k) + 2 * m * k + 4 * m * n
 
 
-def kernel_sources_sha():
-    h = hashlib.sha256()
-    for f in ("gemv.hip", "mfma.hip", "eb_api.cpp", "eb_internal.h"):
-        with open(os.path.join(ROOT, "paper_2607_02501_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
-    return h.hexdigest()[:16]
-
-
 def load_traffic(workload, kernel):
-    """HBM bytes per launch from committed rocprofv3 counter runs, if they were
-    taken on the current kernel sources; otherwise None."""
+    """HBM bytes per launch from committed rocprofv3 counter runs
+    (profiles/traffic.json, written by paper_2607_02501_amd.traffic), if they
+    were taken on the current kernel sources; otherwise None."""
+    from paper_2607_02501_amd.srchash import kernel_sources_sha
+
     path = os.path.join(ROOT, "profiles", "traffic.json")
     try:
         with open(path) as fh:
             rec = json.load(fh).get(workload, {}).get(kernel)
     except (OSError, ValueError):
         return None
-    if not rec or rec.get("kernel_sources_sha") != kernel_sources_sha():
+    if not rec or rec.get("kernel_sources_sha") != kernel_sources_sha(kernel.split("_")[0]):
         return None
     return rec.get("hbm_bytes_per_launch")
 
@@ -103,6 +100,14 @@ def main():
     wl = W.WORKLOADS[args.workload]
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.calibrate_copy:
+        src = torch.ones(args.calibrate_copy // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] calibration copy of {args.calibrate_copy} bytes done")
+        del src, dst
 
     # ---- resident inputs: quantized weights, activations, outputs ----------
     t_setup = time.time()
