@@ -39,8 +39,8 @@
  * Conventions for every entry point:
  *   - All pointers are DEVICE pointers unless stated otherwise; the caller owns
  *     every buffer (weights, activations, outputs).  The library never
- *     synchronises the stream, and allocates device memory only for cached
- *     stack plans (eb_qlinear_stack).
+ *     synchronises the stream.  It allocates device memory only for cached
+ *     stack plans (eb_qlinear_stack) and for split-K workspaces (below).
  *   - Work is enqueued on `stream` (0 = the null stream); EB_OK means the work
  *     was enqueued, not that it finished.
  *   - Arguments are validated on the host before anything is launched; on any
@@ -150,7 +150,17 @@ eb_status eb_qweights_from_canonical(int32_t type, const void *src, int64_t n, i
                                      void *out, hipStream_t stream);
 
 /* y[m][n] = x[m][k] . w_hat[n][k]^T with fp32 accumulation, on the path chosen
- * automatically.  x: device [m][k] of x_type (EB_F16 or EB_BF16); y: device
+ * automatically.
+ * On the MFMA path, a problem with too few output tiles to fill the GPU (few
+ * rows and columns, long k) may be split along k: each split writes fp32
+ * partial sums to a workspace and a second kernel adds them in a fixed order,
+ * so results stay deterministic.  Direct calls use a workspace owned by the
+ * library per (device, stream), at most 64 MiB per call, grown on demand and
+ * never freed before process exit (a graph captured from the stream may refer
+ * to it).  While the stream is being captured nothing is allocated: if the
+ * stream's workspace is too small the call runs unsplit.  A graph captured
+ * from stream S uses S's workspace: do not replay it concurrently with other
+ * calls made on S.  x: device [m][k] of x_type (EB_F16 or EB_BF16); y: device
  * [m][n] of y_type (EB_F32 or EB_BF16, bf16 rounded to nearest even).
  * No bias.  Accuracy: |y - y_exact| <= 2e-3 * sum_k |x||w_hat| per output
  * (plus the bf16 output rounding when y_type is EB_BF16).
@@ -195,6 +205,18 @@ int32_t eb_qlinear_stack_launches(const eb_qlinear_op *ops, int32_t n_ops);
 
 /* Drop every cached stack graph (frees their host/driver resources). */
 eb_status eb_stack_cache_clear(void);
+
+/* Number of tile configurations of the MFMA path (host-only). */
+int32_t eb_mfma_tile_count(void);
+
+/* Tuning and test hook: force the MFMA path's tile configuration `tile`
+ * (0 .. eb_mfma_tile_count() - 1, or -1 for the automatic choice) and its
+ * split of k (1 .. 16 splits, or 0 for automatic).  A forced split that a
+ * shape cannot take (fewer than 4 K-tiles of 64 per split) leaves that shape
+ * unsplit.  Process-wide; applies to launches made after the call (cached
+ * stack plans are keyed on it).  EB_ERR_INVALID for values out of range.  The
+ * environment variable EB_MFMA_CFG=<tile> sets the initial forced tile. */
+eb_status eb_mfma_force(int32_t tile, int32_t splits);
 
 #ifdef __cplusplus
 }

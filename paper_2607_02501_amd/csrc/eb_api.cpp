@@ -10,6 +10,7 @@
 #include <atomic>
 #include <cstdlib>
 #include <cstring>
+#include <map>
 #include <mutex>
 #include <string>
 #include <unordered_map>
@@ -94,13 +95,57 @@ int32_t pick_path(int32_t type, int32_t xt, int64_t m, int64_t n, int64_t k) {
   return gemv_fits(m, k) ? EB_PATH_GEMV : EB_PATH_MFMA;
 }
 
+// Split-K workspaces of direct calls, one per (device, stream) so calls on
+// different streams never share one.  A buffer that is outgrown is retired,
+// not freed: a graph the caller captured from that stream may still use it.
+struct WsCache {
+  std::mutex mu;
+  std::map<std::pair<int, hipStream_t>, std::pair<void *, size_t>> live;
+  std::vector<void *> retired;
+};
+
+WsCache &ws_cache() {
+  static WsCache *c = new WsCache();  // leaked on purpose: no teardown-order issues
+  return *c;
+}
+
+// Workspace of at least `bytes` for stream s, or nullptr (then the caller runs
+// unsplit): allocation failed, or s is being captured and the buffer it has is
+// too small (no allocation inside a capture).
+float *stream_workspace(hipStream_t s, size_t bytes) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return nullptr;
+  WsCache &C = ws_cache();
+  std::lock_guard<std::mutex> lock(C.mu);
+  auto &slot = C.live[{dev, s}];
+  if (slot.first && slot.second >= bytes) return static_cast<float *>(slot.first);
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(s, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone)
+    return nullptr;
+  const size_t want = std::max(bytes, std::max(slot.second * 2, (size_t)4 << 20));
+  void *p = nullptr;
+  if (hipMalloc(&p, want) != hipSuccess) {
+    (void)hipGetLastError();
+    return nullptr;
+  }
+  if (slot.first) C.retired.push_back(slot.first);
+  slot = {p, want};
+  return static_cast<float *>(p);
+}
+
 eb_status launch_linear(const eb_qweights *w, const void *x, int32_t xt, int64_t m, void *y,
                         int32_t yt, int32_t path, hipStream_t s) {
   if (m == 0) return EB_OK;
   if (path == EB_PATH_AUTO) path = pick_path(w->type, xt, m, w->n, w->k);
-  hipError_t e = (path == EB_PATH_GEMV)
-                     ? launch_gemv(w->type, w->data, w->n, w->k, x, xt, m, y, yt, s)
-                     : launch_mfma(w->type, w->data, w->n, w->k, x, xt, m, y, yt, s);
+  hipError_t e;
+  if (path == EB_PATH_GEMV) {
+    e = launch_gemv(w->type, w->data, w->n, w->k, x, xt, m, y, yt, s);
+  } else {
+    MfmaPlan P = plan_mfma(w->type, m, w->n, w->k, true);
+    float *ws = P.splits > 1 ? stream_workspace(s, P.ws_bytes) : nullptr;
+    if (P.splits > 1 && !ws) P = plan_mfma(w->type, m, w->n, w->k, false);
+    e = launch_mfma(w->type, w->data, w->n, w->k, x, xt, m, y, yt, P, ws, s);
+  }
   return e == hipSuccess ? EB_OK : EB_ERR_HIP;
 }
 
@@ -148,6 +193,8 @@ bool independent(const OpSpan &a, const OpSpan &b) {
 
 struct Step {
   int op = -1;        // single op index, or -1 for a fused launch
+  bool mfma = false;  // single op on the MFMA path, run with plan `mp`
+  MfmaPlan mp;
   int32_t type = 0, xt = 0;
   int ns = 0;
   size_t table = 0;   // first entry in the device table
@@ -158,6 +205,8 @@ struct Step {
 struct Plan {
   std::vector<Step> steps;
   M1Op *table = nullptr;  // device copy of every fused launch's op table
+  float *ws = nullptr;    // split-K workspace shared by the plan's MFMA steps (run in order)
+  size_t ws_bytes = 0;
   hipGraph_t graph = nullptr;
   hipGraphExec_t exec = nullptr;
 };
@@ -229,6 +278,18 @@ eb_status build_plan(const eb_qlinear_op *ops, int32_t n_ops, bool alloc, Plan &
     }
     i = j;
   }
+  for (Step &s : P.steps) {
+    if (s.op < 0) continue;
+    const eb_qlinear_op &o = ops[s.op];
+    if (o.m == 0 || pick_path(o.w.type, o.x_type, o.m, o.w.n, o.w.k) != EB_PATH_MFMA) continue;
+    s.mfma = true;
+    s.mp = plan_mfma(o.w.type, o.m, o.w.n, o.w.k, true);
+    P.ws_bytes = std::max(P.ws_bytes, s.mp.ws_bytes);
+  }
+  if (alloc && P.ws_bytes > 0 && hipMalloc((void **)&P.ws, P.ws_bytes) != hipSuccess) {
+    P.ws = nullptr;
+    return EB_ERR_HIP;
+  }
   if (alloc && !host.empty()) {
     if (hipMalloc((void **)&P.table, host.size() * sizeof(M1Op)) != hipSuccess) {
       P.table = nullptr;
@@ -243,7 +304,12 @@ eb_status build_plan(const eb_qlinear_op *ops, int32_t n_ops, bool alloc, Plan &
 
 eb_status run_plan(const eb_qlinear_op *ops, const Plan &P, hipStream_t s) {
   for (const Step &st : P.steps) {
-    if (st.op >= 0) {
+    if (st.mfma) {
+      const eb_qlinear_op &o = ops[st.op];
+      if (launch_mfma(o.w.type, o.w.data, o.w.n, o.w.k, o.x, o.x_type, o.m, o.y, o.y_type, st.mp,
+                      st.mp.splits > 1 ? P.ws : nullptr, s) != hipSuccess)
+        return EB_ERR_HIP;
+    } else if (st.op >= 0) {
       const eb_qlinear_op &o = ops[st.op];
       eb_status r = launch_linear(&o.w, o.x, o.x_type, o.m, o.y, o.y_type, EB_PATH_AUTO, s);
       if (r != EB_OK) return r;
@@ -259,6 +325,7 @@ void destroy_plan(Plan &p) {
   if (p.exec) (void)hipGraphExecDestroy(p.exec);
   if (p.graph) (void)hipGraphDestroy(p.graph);
   if (p.table) (void)hipFree(p.table);
+  if (p.ws) (void)hipFree(p.ws);
   p = Plan();
 }
 
@@ -392,6 +459,8 @@ eb_status eb_qlinear_stack(const eb_qlinear_op *ops, int32_t n_ops, hipStream_t 
   std::string key(reinterpret_cast<const char *>(&dev), sizeof(dev));
   key.push_back(use_graph ? 'g' : 'd');
   key.push_back(env_off("EB_STACK_FUSE") ? 'u' : 'f');
+  const int fk = mfma_force_key();
+  key.append(reinterpret_cast<const char *>(&fk), sizeof(fk));
   key.append(reinterpret_cast<const char *>(ops), sizeof(eb_qlinear_op) * (size_t)n_ops);
 
   StackCache &C = cache();
@@ -443,8 +512,16 @@ int32_t eb_qlinear_stack_launches(const eb_qlinear_op *ops, int32_t n_ops) {
   build_plan(ops, n_ops, false, P);
   int32_t launches = 0;
   for (const Step &st : P.steps)
-    if (st.op < 0 || ops[st.op].m > 0) ++launches;
+    if (st.op < 0 || ops[st.op].m > 0) launches += (st.mfma && st.mp.splits > 1) ? 2 : 1;
   return launches;
+}
+
+int32_t eb_mfma_tile_count(void) { return mfma_tile_count(); }
+
+eb_status eb_mfma_force(int32_t tile, int32_t splits) {
+  if (tile < -1 || tile >= mfma_tile_count() || splits < 0 || splits > 16) return EB_ERR_INVALID;
+  mfma_force(tile, splits);
+  return EB_OK;
 }
 
 eb_status eb_stack_cache_clear(void) {

@@ -72,9 +72,24 @@ int64_t m1_fill(int32_t type, const void *wdata, int64_t n, int64_t k, const voi
 hipError_t launch_gemv_m1_multi(int32_t type, int32_t xt, int ns, const M1Op *dev_ops, int nops,
                                 int64_t units, int64_t rows, hipStream_t s);
 
-// MFMA path: any m
+// MFMA path: any m.  A plan fixes the tile configuration and the split of K
+// over workgroups; with splits > 1 the launch needs ws_bytes of fp32 workspace
+// (partial sums, summed in order by a second kernel).
+struct MfmaPlan {
+  int cfg = 0;
+  int splits = 1;
+  int kts = 0;            // K-tiles of 64 per split
+  int64_t ws_stride = 0;  // floats between the partial outputs of two splits
+  size_t ws_bytes = 0;
+};
+MfmaPlan plan_mfma(int32_t type, int64_t m, int64_t n, int64_t k, bool allow_split);
+// ws == nullptr runs the plan's configuration unsplit.
 hipError_t launch_mfma(int32_t type, const void *wdata, int64_t n, int64_t k, const void *x,
-                       int32_t xt, int64_t m, void *y, int32_t yt, hipStream_t s);
+                       int32_t xt, int64_t m, void *y, int32_t yt, const MfmaPlan &plan, float *ws,
+                       hipStream_t s);
+int mfma_tile_count();
+void mfma_force(int cfg, int splits);  // cfg -1 / splits 0: automatic
+int mfma_force_key();                  // changes whenever the forced state does
 
 // number of compute units of the current device (cached per device)
 int device_cu_count();

@@ -7,16 +7,22 @@
 // the activation type (bfloat16 or binary16), fp32 accumulation.
 //
 // A workgroup of WM x WN waves computes a BM x BN tile of y; each wave owns a
-// (BM/WM) x (BN/WN) sub-tile held in fp32 accumulators (AGPRs).  Per K-tile of 64:
-//   * global -> registers: the x tile (16-byte loads) and the packed weight
-//     tile (16-byte loads of codes + binary16 scales), one K-tile ahead;
-//   * registers -> LDS: x copied, weights dequantized (code * d16 exact in
-//     fp32, one round-to-nearest-even to 16 bits) -- fused into the tile load,
-//     no dequantized weight ever reaches HBM;
+// (BM/WM) x (BN/WN) sub-tile of fp32 accumulators.  Per K-tile of 64:
+//   * global -> LDS: the x tile is copied by buffer loads that write LDS
+//     directly (no register staging), into one of three buffers;
+//   * global -> registers: the packed weight tile (16-byte code loads plus
+//     binary16 scales) into one of three register sets;
+//   * registers -> LDS: weights dequantized (code * d16 exact in fp32, one
+//     round-to-nearest-even to 16 bits) into one of two buffers -- fused into
+//     the tile load, no dequantized weight ever reaches HBM;
 //   * LDS -> MFMA: v_mfma_f32_32x32x16_{bf16,f16}, A = x rows, B = w_hat rows.
-// LDS is double-buffered, so one barrier per K-tile separates the MFMAs on
-// buffer i from the dequantizing stores into buffer i+1; the stores are
-// interleaved with the MFMA chain so VALU work overlaps the matrix cores.
+// Each K-tile step issues the x copy of tile t+2 and the weight loads of tile
+// t+3, runs the MFMAs of tile t with the dequantization of tile t+1
+// interleaved, and waits only for x tile t+1 before its barrier, so every load
+// has about two steps of MFMA work to land.
+//
+// Problems with too few tiles to fill the GPU split k over workgroups; each
+// split writes an fp32 partial tile and a second kernel sums them in order.
 //
 // Tiles are ordered for the 8 XCDs of MI355X (workgroups are dispatched to
 // XCDs round-robin, each XCD has its own L2): each XCD gets a contiguous range
@@ -24,6 +30,9 @@
 // block of x rows.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+#include <atomic>
+#include <cmath>
 #include <cstdlib>
 
 #include "eb_internal.h"
@@ -36,8 +45,6 @@ typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 constexpr int kBK = 64;        // K elements per tile (2 blocks)
-constexpr int kPad = 8;        // LDS row padding in 16-bit elements
-constexpr int kLds = kBK + kPad;
 constexpr int kXcds = 8;
 
 template <int XT>
@@ -67,134 +74,237 @@ struct WTile {
   static constexpr int kElemsPerChunk = (QT == EB_Q8_0) ? 16 : 32;
 };
 
-// Dequantize one 16-byte chunk into LDS row `dst` (16-bit elements).
-// Q8_0: 16 int8 codes.  u = q + 128 converts exactly with v_cvt_f32_ubyte and
-// fma(u, d, -128 d) = q d exactly (all terms fit in fp32), then one RNE.
-// Q4_0: 16 bytes, low nibbles = elements 0..15, high nibbles = 16..31, value
-// (n - 8) d = fma(n, d, -8 d) exactly.
+// Dequantize one 16-byte chunk of codes into 16-byte vectors of 16-bit
+// weights, in k order: Q8_0 16 codes -> 2 vectors, Q4_0 one block -> 4.
+// Each code c in 0..255 (Q8_0: q + 128) or 0..15 (Q4_0 nibble) is placed
+// under the binary16 exponent of 1024 by one byte permute per two codes,
+// giving the binary16 value 1024 + c exactly; then
+//   fma(1024 + c, d, -(1024 + z) d) = (c - z) d,   z = 128 (Q8_0) or 8 (Q4_0),
+// is exact (1152 d and 1032 d need at most 19 significant bits), and the one
+// rounding to the 16-bit activation type is round-to-nearest-even.
+template <int QT>
+struct Deq {
+  static constexpr int kVecs = (QT == EB_Q8_0) ? 2 : 4;
+};
+
+// two codes in bytes b0, b1 of v -> 16-bit halves 0x64bb of the result
+__device__ inline uint32_t under_1024(uint32_t v, uint32_t sel) {
+  return __builtin_amdgcn_perm(0x64646464u, v, sel);
+}
+
+template <int XT>
+__device__ inline uint32_t deq_pair(uint32_t h2, float d, float c) {
+  const _Float16 a = __builtin_bit_cast(_Float16, (uint16_t)(h2 & 0xffffu));
+  const _Float16 b = __builtin_bit_cast(_Float16, (uint16_t)(h2 >> 16));
+  return pack2<XT>(__builtin_fmaf((float)a, d, c), __builtin_fmaf((float)b, d, c));
+}
+
 template <int QT, int XT>
-__device__ inline void dequant_chunk(const uint4 q, float d, uint16_t *dst) {
+__device__ inline void dequant_chunk(const uint4 q, float d, uint4 (&v)[Deq<QT>::kVecs]) {
   const uint32_t w[4] = {q.x, q.y, q.z, q.w};
-  if (QT == EB_Q8_0) {
-    const float off = -128.0f * d;
+  // byte selectors: {S1.b0, 0x64, S1.b1, 0x64} and {S1.b2, 0x64, S1.b3, 0x64}
+  constexpr uint32_t kSelLo = 0x04010400u, kSelHi = 0x04030402u;
+  if constexpr (QT == EB_Q8_0) {
+    const float c = -1152.0f * d;
     uint32_t o[8];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const uint32_t u = w[j] ^ 0x80808080u;
-      const float f0 = __builtin_fmaf((float)(u & 0xffu), d, off);
-      const float f1 = __builtin_fmaf((float)((u >> 8) & 0xffu), d, off);
-      const float f2 = __builtin_fmaf((float)((u >> 16) & 0xffu), d, off);
-      const float f3 = __builtin_fmaf((float)(u >> 24), d, off);
-      o[2 * j] = pack2<XT>(f0, f1);
-      o[2 * j + 1] = pack2<XT>(f2, f3);
+      o[2 * j] = deq_pair<XT>(under_1024(u, kSelLo), d, c);
+      o[2 * j + 1] = deq_pair<XT>(under_1024(u, kSelHi), d, c);
     }
-    uint4 *p = reinterpret_cast<uint4 *>(dst);
-    p[0] = make_uint4(o[0], o[1], o[2], o[3]);
-    p[1] = make_uint4(o[4], o[5], o[6], o[7]);
+    v[0] = make_uint4(o[0], o[1], o[2], o[3]);
+    v[1] = make_uint4(o[4], o[5], o[6], o[7]);
   } else {
-    const float off = -8.0f * d;
+    const float c = -1032.0f * d;
     uint32_t lo[8], hi[8];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const uint32_t l = w[j] & 0x0f0f0f0fu, h = (w[j] >> 4) & 0x0f0f0f0fu;
-      lo[2 * j] = pack2<XT>(__builtin_fmaf((float)(l & 0xffu), d, off),
-                            __builtin_fmaf((float)((l >> 8) & 0xffu), d, off));
-      lo[2 * j + 1] = pack2<XT>(__builtin_fmaf((float)((l >> 16) & 0xffu), d, off),
-                                __builtin_fmaf((float)(l >> 24), d, off));
-      hi[2 * j] = pack2<XT>(__builtin_fmaf((float)(h & 0xffu), d, off),
-                            __builtin_fmaf((float)((h >> 8) & 0xffu), d, off));
-      hi[2 * j + 1] = pack2<XT>(__builtin_fmaf((float)((h >> 16) & 0xffu), d, off),
-                                __builtin_fmaf((float)(h >> 24), d, off));
+      lo[2 * j] = deq_pair<XT>(under_1024(l, kSelLo), d, c);
+      lo[2 * j + 1] = deq_pair<XT>(under_1024(l, kSelHi), d, c);
+      hi[2 * j] = deq_pair<XT>(under_1024(h, kSelLo), d, c);
+      hi[2 * j + 1] = deq_pair<XT>(under_1024(h, kSelHi), d, c);
     }
-    uint4 *p = reinterpret_cast<uint4 *>(dst);
-    p[0] = make_uint4(lo[0], lo[1], lo[2], lo[3]);
-    p[1] = make_uint4(lo[4], lo[5], lo[6], lo[7]);
-    p[2] = make_uint4(hi[0], hi[1], hi[2], hi[3]);
-    p[3] = make_uint4(hi[4], hi[5], hi[6], hi[7]);
+    v[0] = make_uint4(lo[0], lo[1], lo[2], lo[3]);
+    v[1] = make_uint4(lo[4], lo[5], lo[6], lo[7]);
+    v[2] = make_uint4(hi[0], hi[1], hi[2], hi[3]);
+    v[3] = make_uint4(hi[4], hi[5], hi[6], hi[7]);
   }
+}
+
+// Raw buffer descriptor over [base, base + bytes): every lane whose offset is
+// at or past `bytes` reads zeros, which is how the kernel handles rows past m
+// or n without branches.  The descriptor is rebuilt per K-tile (scalar work),
+// so the hardware range check always covers the whole access.
+__device__ inline __amdgpu_buffer_rsrc_t rsrc(const void *base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes,
+                                           0x00020000);
+}
+
+__device__ inline uint4 bload(__amdgpu_buffer_rsrc_t r, uint32_t voff) {
+  const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, 0, 0);
+  return make_uint4(v[0], v[1], v[2], v[3]);
+}
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+// Position of 16-byte chunk c of row r in the unpadded x tile (128-byte rows):
+// c ^ swz(r).  Any 16 consecutive rows read at one chunk index hit 16 distinct
+// 16-byte bank groups, and any 8 consecutive rows 8 distinct ones.
+__device__ inline uint32_t swz(uint32_t r) { return (r ^ (r >> 3)) & 7; }
+
+// Wait until at most N vector-memory operations of this wave are outstanding
+// and its LDS writes are done, then barrier.  Unlike __syncthreads this does
+// not drain every load, so loads issued for later K-tiles stay in flight.  The
+// "memory" clobber keeps IR passes, and the scheduling barriers the machine
+// scheduler, from moving memory accesses across it.
+template <int N>
+__device__ inline void wait_vm_barrier() {
+  // sched_barrier(0): the machine scheduler moves nothing across this point
+  __builtin_amdgcn_sched_barrier(0);
+  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
+  __builtin_amdgcn_sched_barrier(0);
 }
 
 template <int QT, int XT, int BM, int BN, int WM, int WN>
 __global__ void __launch_bounds__(WM *WN * 64)
     mfma_kernel(const uint8_t *__restrict__ wdata, int64_t n, int64_t k, int64_t d_off, int64_t ds,
-                const uint16_t *__restrict__ x, int64_t m, void *__restrict__ y, int yt) {
+                const uint16_t *__restrict__ x, int64_t m, void *__restrict__ y, int yt, int kts,
+                float *__restrict__ ws, int64_t ws_stride) {
   constexpr int T = WM * WN * 64;
+  constexpr int WAVES = WM * WN;
   constexpr int TM = BM / WM, TN = BN / WN;        // wave sub-tile
   constexpr int FM = TM / 32, FN = TN / 32;        // 32x32 fragments per wave
-  constexpr int ACH = BM * (kBK / 8) / T;          // x chunks per thread
+  constexpr int ADMA = BM / (8 * WAVES);           // x copies per wave per K-tile (8 rows each)
   constexpr int WCPR = WTile<QT>::kChunksPerRow;
-  constexpr int BCH = BN * WCPR / T;               // weight chunks per thread
+  constexpr int WCH = BN * WCPR;                   // weight chunks per K-tile
+  constexpr int BCH = (WCH + T - 1) / T;           // per thread (the last may be partial)
   constexpr int KSTEPS = kBK / 16;
-  static_assert(ACH * T == BM * (kBK / 8), "x tile must split evenly");
-  static_assert(BCH * T == BN * WCPR, "weight tile must split evenly");
-  static_assert(BCH % KSTEPS == 0 || KSTEPS % BCH == 0, "dequant interleave");
+  constexpr int QSB = (QT == EB_Q8_0) ? 32 : 16;   // code bytes per block
+  constexpr int NV = Deq<QT>::kVecs;               // 16-byte vectors per dequantized chunk
+  constexpr int ABYTES = BM * kBK * 2, BBYTES = BN * kBK * 2;
+  // vector-memory operations one thread issues per K-tile
+  constexpr int NX = ADMA, NW = 2 * BCH;
+  static_assert(ADMA >= 1 && ADMA * 8 * WAVES == BM, "x tile must split into 8-row copies");
+  static_assert(TM % 32 == 0 && TN % 32 == 0, "wave sub-tile must be whole fragments");
+  static_assert(2 * NW + NX <= 63, "vmcnt range");
 
-  extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
-  // buffer b: A tile at lds + b * (BM + BN) * kLds, B tile right after it
-  auto Abuf = [&](int b) { return lds + b * (BM + BN) * kLds; };
-  auto Bbuf = [&](int b) { return lds + b * (BM + BN) * kLds + BM * kLds; };
+  // Three x buffers (tile kt in use, kt+1 landing, kt+2 being copied) and two
+  // weight buffers.  Separate objects, so the compiler can tell the
+  // asynchronous copies into one x buffer from the reads of another.  Both
+  // tiles use unpadded 128-byte rows with 16-byte chunk c of row r stored at
+  // position c ^ swz(r).
+  __shared__ __attribute__((aligned(1024))) uint8_t sA0[ABYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t sA1[ABYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t sA2[ABYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t sB0[BBYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t sB1[BBYTES];
 
-  // XCD-aware tile order
+  // Workgroup -> (K split, output tile).  Split s covers K-tiles
+  // [s kts, (s + 1) kts) and, when there are several splits (ws != null),
+  // writes its fp32 partial tile to ws + s ws_stride; a second kernel sums them.
   const int64_t tiles_m = (m + BM - 1) / BM, tiles_n = (n + BN - 1) / BN;
   const int64_t tiles = tiles_m * tiles_n;
-  const int64_t bid = blockIdx.x;
+  const int split = (int)(blockIdx.x / tiles);
+  const int64_t bid = blockIdx.x % tiles;
+  // XCD-aware tile order
   int64_t t = bid;
   if (tiles % kXcds == 0) t = (bid % kXcds) * (tiles / kXcds) + bid / kXcds;
   const int64_t tm = t / tiles_n, tn = t % tiles_n;
   const int64_t m0 = tm * BM, n0 = tn * BN;
   const int64_t nb = k / kQK;
-  const int64_t qsb = (QT == EB_Q8_0) ? 32 : 16;
-  const uint16_t *__restrict__ dplane = reinterpret_cast<const uint16_t *>(wdata + d_off);
+  const int rows_m = (int)min((int64_t)BM, m - m0), rows_n = (int)min((int64_t)BN, n - n0);
 
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WN, wn = wave % WN;
 
-  uint4 areg[ACH];
-  uint4 breg[BCH];
-  uint16_t dreg[BCH];
+  // Per-workgroup bases, starting at this split's first K-tile; the byte
+  // counts shrink with them, so every range check still ends at the end of the
+  // tile's rows.  The host guarantees that they fit in 32 bits.
+  const int kt0 = split * kts;
+  const int nk = (int)min((int64_t)kts, (k + kBK - 1) / kBK - kt0);
+  const uint8_t *const xbase = reinterpret_cast<const uint8_t *>(x) + m0 * k * 2 + kt0 * (kBK * 2);
+  const uint8_t *const qbase = wdata + n0 * nb * QSB + kt0 * (2 * QSB);
+  const uint8_t *const dbase = wdata + d_off + n0 * ds * 2 + kt0 * 4;
+  const uint32_t xrec = (uint32_t)(rows_m * k * 2 - kt0 * (kBK * 2));
+  const uint32_t qrec = (uint32_t)(rows_n * nb * QSB - kt0 * (2 * QSB));
+  const uint32_t drec = (uint32_t)(rows_n * ds * 2 - kt0 * 4);
 
-  auto load_tile = [&](int64_t kt) {
+  // x copy: wave `wave`, copy i moves tile rows 8 (i WAVES + wave) .. +7; lane
+  // j fills LDS chunk position j % 8 of row j / 8, i.e. logical chunk
+  // (j % 8) ^ swz(row).  Rows past m fall past xrec and read zeros.
+  uint32_t xv[ADMA];
 #pragma unroll
-    for (int i = 0; i < ACH; ++i) {
-      const int idx = tid + i * T;
-      const int r = idx / (kBK / 8), c8 = idx % (kBK / 8);
-      const int64_t gm = m0 + r, gk = kt * kBK + c8 * 8;
-      areg[i] = (gm < m && gk < k) ? *reinterpret_cast<const uint4 *>(x + gm * k + gk)
-                                   : make_uint4(0, 0, 0, 0);
-    }
+  for (int i = 0; i < ADMA; ++i) {
+    const uint32_t r = 8 * (i * WAVES + wave) + (lane >> 3);
+    xv[i] = (uint32_t)(r * k * 2) + (((lane & 7) ^ swz(r)) << 4);
+  }
+  // Weight chunks: rows past n fall past qrec/drec and read zeros; chunk
+  // indices past the tile (only when T does not divide it) are moved past the
+  // buffers too and their stores are skipped.  Chunk c of a row covers logical
+  // 16-byte positions NV c .. NV c + NV - 1; since NV c is a multiple of NV the
+  // stored position of part q is (NV c ^ swz(r)) ^ q, so wl ^ (16 q).
+  uint32_t qo[BCH], dof[BCH], wl[BCH];
+#pragma unroll
+  for (int i = 0; i < BCH; ++i) {
+    const int idx = min(tid + i * T, WCH), r = idx / WCPR, c = idx % WCPR;
+    const int blk = (QT == EB_Q8_0) ? (c >> 1) : c;
+    qo[i] = (uint32_t)((r * nb + blk) * QSB + ((QT == EB_Q8_0) ? (c & 1) * 16 : 0));
+    dof[i] = (uint32_t)((r * ds + blk) * 2);
+    wl[i] = (uint32_t)(r * (kBK * 2) + (((NV * c) ^ swz(r)) << 4));
+  }
+
+  auto load_x = [&](uint8_t *sA, int kt) __attribute__((always_inline)) {
+    const uint32_t adv = (uint32_t)kt * (kBK * 2);
+    const auto xr = rsrc(xbase + adv, xrec - adv);
+#pragma unroll
+    for (int i = 0; i < ADMA; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          xr, (lds_void *)(sA + (i * WAVES + wave) * 1024), 16, (int)xv[i], 0, 0, 0);
+  };
+
+  // Raw weight registers of one K-tile.  The K-tail block of an odd block count
+  // reads a zero scale from the scale-plane padding, so its weights are zeros.
+  struct Raw {
+    uint4 b[BCH];
+    uint16_t d[BCH];
+  };
+  Raw S0, S1, S2;
+  auto load_w = [&](Raw &S, int kt) __attribute__((always_inline)) {
+    const uint32_t qadv = (uint32_t)kt * (2 * QSB), dadv = (uint32_t)kt * 4;
+    const auto qr = rsrc(qbase + qadv, qrec - qadv);
+    const auto dr = rsrc(dbase + dadv, drec - dadv);
 #pragma unroll
     for (int i = 0; i < BCH; ++i) {
-      const int idx = tid + i * T;
-      const int r = idx / WCPR, c = idx % WCPR;
-      int64_t gn = n0 + r;
-      if (gn >= n) gn = n - 1;  // clamped rows produce columns that are never stored
-      const int64_t blk = kt * 2 + ((QT == EB_Q8_0) ? (c >> 1) : c);
-      if (blk < nb) {
-        const uint8_t *src = wdata + (gn * nb + blk) * qsb + ((QT == EB_Q8_0) ? (c & 1) * 16 : 0);
-        breg[i] = *reinterpret_cast<const uint4 *>(src);
-        dreg[i] = dplane[gn * ds + blk];
-      } else {
-        breg[i] = make_uint4(0, 0, 0, 0);
-        dreg[i] = 0;
-      }
+      S.b[i] = bload(qr, qo[i]);
+      S.d[i] = __builtin_amdgcn_raw_buffer_load_b16(dr, (int)dof[i], 0, 0);
     }
+  };
+  auto store_w = [&](const Raw &S, uint8_t *sB, int i) __attribute__((always_inline)) {
+    if (WCH % T != 0 && i == BCH - 1 && tid + i * T >= WCH) return;
+    uint4 v[NV];
+    dequant_chunk<QT, XT>(S.b[i], (float)__builtin_bit_cast(_Float16, S.d[i]), v);
+#pragma unroll
+    for (int q = 0; q < NV; ++q) *reinterpret_cast<uint4 *>(sB + (wl[i] ^ (16u * q))) = v[q];
   };
 
-  auto store_x = [&](uint16_t *A) {
+  // Fragment addresses: lane reads row (lane & 31) of a fragment, logical
+  // chunk 2 ks + lane / 32, stored at (2 ks + lane / 32) ^ swz(row); since 2 ks
+  // is even that is base ^ (32 ks).
+  uint32_t abase[FM], bbase[FN];
 #pragma unroll
-    for (int i = 0; i < ACH; ++i) {
-      const int idx = tid + i * T;
-      const int r = idx / (kBK / 8), c8 = idx % (kBK / 8);
-      *reinterpret_cast<uint4 *>(&A[r * kLds + c8 * 8]) = areg[i];
-    }
-  };
-  auto store_w = [&](uint16_t *B, int i) {
-    const int idx = tid + i * T;
-    const int r = idx / WCPR, c = idx % WCPR;
-    dequant_chunk<QT, XT>(breg[i], (float)__builtin_bit_cast(_Float16, dreg[i]),
-                          &B[r * kLds + c * WTile<QT>::kElemsPerChunk]);
-  };
+  for (int i = 0; i < FM; ++i) {
+    const uint32_t r = wm * TM + i * 32 + (lane & 31);
+    abase[i] = r * (kBK * 2) + ((((uint32_t)lane >> 5) ^ swz(r)) << 4);
+  }
+#pragma unroll
+  for (int j = 0; j < FN; ++j) {
+    const uint32_t r = wn * TN + j * 32 + (lane & 31);
+    bbase[j] = r * (kBK * 2) + ((((uint32_t)lane >> 5) ^ swz(r)) << 4);
+  }
 
   f32x16_t acc[FM][FN];
 #pragma unroll
@@ -204,45 +314,90 @@ __global__ void __launch_bounds__(WM *WN * 64)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  const int64_t nk = (k + kBK - 1) / kBK;
-  load_tile(0);
-  store_x(Abuf(0));
-#pragma unroll
-  for (int i = 0; i < BCH; ++i) store_w(Bbuf(0), i);
-  if (nk > 1) load_tile(1);
-  __syncthreads();
-
-  for (int64_t kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    const uint16_t *A = Abuf(cur), *B = Bbuf(cur);
-    const bool more = kt + 1 < nk;
-    if (more) store_x(Abuf(cur ^ 1));
+  // MFMAs of the tile in (sA, sB); the dequantizing stores of the next tile
+  // (raw set `nxt`, already in registers) into sBn are spread over the k-steps
+  // so the VALU work overlaps the matrix cores.
+  auto compute = [&](const uint8_t *sA, const uint8_t *sB, const Raw &nxt, uint8_t *sBn,
+                     bool more) __attribute__((always_inline)) {
 #pragma unroll
     for (int ks = 0; ks < KSTEPS; ++ks) {
-      const int koff = ks * 16 + 8 * (lane >> 5);
       uint4 af[FM], bfr[FN];
 #pragma unroll
       for (int i = 0; i < FM; ++i)
-        af[i] = *reinterpret_cast<const uint4 *>(&A[(wm * TM + i * 32 + (lane & 31)) * kLds + koff]);
+        af[i] = *reinterpret_cast<const uint4 *>(sA + (abase[i] ^ (32u * ks)));
 #pragma unroll
       for (int j = 0; j < FN; ++j)
-        bfr[j] = *reinterpret_cast<const uint4 *>(&B[(wn * TN + j * 32 + (lane & 31)) * kLds + koff]);
+        bfr[j] = *reinterpret_cast<const uint4 *>(sB + (bbase[j] ^ (32u * ks)));
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j) acc[i][j] = mfma32<XT>(af[i], bfr[j], acc[i][j]);
-      // a share of the next tile's dequantization between MFMA groups
       if (more) {
-        if constexpr (BCH >= KSTEPS) {
+        constexpr int per = (BCH + KSTEPS - 1) / KSTEPS;
 #pragma unroll
-          for (int i = ks * (BCH / KSTEPS); i < (ks + 1) * (BCH / KSTEPS); ++i) store_w(Bbuf(cur ^ 1), i);
-        } else {
-          if (ks % (KSTEPS / BCH) == 0) store_w(Bbuf(cur ^ 1), ks / (KSTEPS / BCH));
-        }
+        for (int i = ks * per; i < ks * per + per && i < BCH; ++i) store_w(nxt, sBn, i);
       }
     }
-    if (kt + 2 < nk) load_tile(kt + 2);
-    __syncthreads();
+  };
+
+  // Rows of the x buffers that no copy fills (past m) keep these zeros.
+  {
+    constexpr int Z = 3 * ABYTES / 16 / T;
+    static_assert(Z * T * 16 == 3 * ABYTES, "zero fill must cover the x buffers");
+#pragma unroll
+    for (int i = 0; i < Z; ++i) {
+      const int o = (tid + i * T) * 16;
+      uint8_t *dst = o < ABYTES ? sA0 + o : (o < 2 * ABYTES ? sA1 + (o - ABYTES) : sA2 + (o - 2 * ABYTES));
+      *reinterpret_cast<uint4 *>(dst) = make_uint4(0, 0, 0, 0);
+    }
+  }
+  __syncthreads();
+
+  // Pipeline: entering the step of tile t, x tile t is in LDS, x tile t+1 is
+  // being copied, the weights of tile t+1 are in registers (or arriving) and
+  // those of tile t+2 are in flight.  The step issues x tile t+2 and weight
+  // tile t+3, runs the MFMAs of tile t while dequantizing weight tile t+1 into
+  // the other weight buffer, then waits only for x tile t+1 (issued one step
+  // earlier) before the barrier: every load has about two steps to land.
+  load_x(sA0, 0);
+  load_w(S0, 0);
+  if (nk > 1) load_x(sA1, 1);
+  if (nk > 1) load_w(S1, 1);
+  if (nk > 2) load_w(S2, 2);
+#pragma unroll
+  for (int i = 0; i < BCH; ++i) store_w(S0, sB0, i);
+  __syncthreads();
+
+  // In the main loop every load is in range, so the steps issue them
+  // unconditionally and the compiler's own wait counts stay exact across the
+  // loop; the last (up to 8) tiles run through guarded copies of the steps.
+  auto step = [&](int t, const uint8_t *A, uint8_t *A2, const uint8_t *B, uint8_t *Bn,
+                  const Raw &deq, Raw &ld, bool guarded) __attribute__((always_inline)) {
+    if (guarded && t >= nk) return;
+    if (!guarded || t + 2 < nk) load_x(A2, t + 2);
+    if (!guarded || t + 3 < nk) load_w(ld, t + 3);
+    compute(A, B, deq, Bn, !guarded || t + 1 < nk);
+    if (!guarded || t + 3 < nk)
+      wait_vm_barrier<2 * NW + NX>();
+    else
+      wait_vm_barrier<0>();
+  };
+  int kt = 0;
+  for (; kt + 8 < nk; kt += 6) {
+    step(kt + 0, sA0, sA2, sB0, sB1, S1, S0, false);
+    step(kt + 1, sA1, sA0, sB1, sB0, S2, S1, false);
+    step(kt + 2, sA2, sA1, sB0, sB1, S0, S2, false);
+    step(kt + 3, sA0, sA2, sB1, sB0, S1, S0, false);
+    step(kt + 4, sA1, sA0, sB0, sB1, S2, S1, false);
+    step(kt + 5, sA2, sA1, sB1, sB0, S0, S2, false);
+  }
+  for (; kt < nk; kt += 6) {
+    step(kt + 0, sA0, sA2, sB0, sB1, S1, S0, true);
+    step(kt + 1, sA1, sA0, sB1, sB0, S2, S1, true);
+    step(kt + 2, sA2, sA1, sB0, sB1, S0, S2, true);
+    step(kt + 3, sA0, sA2, sB1, sB0, S1, S0, true);
+    step(kt + 4, sA1, sA0, sB0, sB1, S2, S1, true);
+    step(kt + 5, sA2, sA1, sB1, sB0, S0, S2, true);
   }
 
   // epilogue: lane holds column (lane & 31), rows 8*(r/4) + 4*(lane/32) + r%4
@@ -250,76 +405,231 @@ __global__ void __launch_bounds__(WM *WN * 64)
   for (int i = 0; i < FM; ++i)
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
-      const int64_t col = n0 + wn * TN + j * 32 + (lane & 31);
-      if (col >= n) continue;
+      const int cl = wn * TN + j * 32 + (lane & 31);
+      if (cl >= rows_n) continue;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int64_t row = m0 + wm * TM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        if (row >= m) continue;
-        if (yt == EB_F32)
-          reinterpret_cast<float *>(y)[row * n + col] = acc[i][j][r];
+        const int rl = wm * TM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        if (rl >= rows_m) continue;
+        const int64_t o = (m0 + rl) * n + n0 + cl;
+        if (ws)
+          ws[split * ws_stride + o] = acc[i][j][r];
+        else if (yt == EB_F32)
+          reinterpret_cast<float *>(y)[o] = acc[i][j][r];
         else
-          reinterpret_cast<__bf16 *>(y)[row * n + col] = (__bf16)acc[i][j][r];
+          reinterpret_cast<__bf16 *>(y)[o] = (__bf16)acc[i][j][r];
       }
     }
 }
 
+// Whether every byte span one workgroup addresses through a 32-bit buffer
+// offset fits (tile rows x row bytes of x, codes and scales).  The template
+// tile sizes are used unless bm/bn are given.
+template <int QT, int BM, int BN>
+bool fits_offsets(int64_t n, int64_t k, int bm = BM, int bn = BN) {
+  const Layout L = layout_of(QT, n, k);
+  const int64_t qsb = (QT == EB_Q8_0) ? 32 : 16;
+  const int64_t lim = 0xffffffffLL;
+  return (int64_t)bm * k * 2 <= lim && (int64_t)bn * (k / kQK) * qsb <= lim &&
+         (int64_t)bn * L.ds * 2 <= lim;
+}
+
 template <int QT, int XT, int BM, int BN, int WM, int WN>
 hipError_t launch_t(const void *wdata, int64_t n, int64_t k, const void *x, int64_t m, void *y,
-                    int32_t yt, hipStream_t s) {
+                    int32_t yt, int splits, int kts, float *ws, int64_t ws_stride, hipStream_t s) {
   const Layout L = layout_of(QT, n, k);
   const int64_t tiles = ((m + BM - 1) / BM) * ((n + BN - 1) / BN);
-  if (tiles > 0x7fffffff) return hipErrorInvalidValue;
-  const size_t lds = (size_t)2 * (BM + BN) * kLds * sizeof(uint16_t);
-  auto kern = mfma_kernel<QT, XT, BM, BN, WM, WN>;
-  static bool attr_set = false;  // idempotent; a race only repeats the same call
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void *)kern,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
-  kern<<<(unsigned)tiles, WM * WN * 64, lds, s>>>((const uint8_t *)wdata, n, k, L.d_off, L.ds,
-                                                  (const uint16_t *)x, m, y, yt);
+  if (tiles * splits > 0x7fffffff) return hipErrorInvalidValue;
+  if (!fits_offsets<QT, BM, BN>(n, k)) return hipErrorInvalidValue;
+  mfma_kernel<QT, XT, BM, BN, WM, WN><<<(unsigned)(tiles * splits), WM * WN * 64, 0, s>>>(
+      (const uint8_t *)wdata, n, k, L.d_off, L.ds, (const uint16_t *)x, m, y, yt, kts,
+      splits > 1 ? ws : nullptr, ws_stride);
   return hipGetLastError();
 }
 
-// Tile configuration; EB_MFMA_CFG=<index> forces one (tuning).
-int mfma_cfg_override() {
-  static const int v = [] {
-    const char *e = getenv("EB_MFMA_CFG");
-    return e ? atoi(e) : -1;
-  }();
-  return v;
+// y = sum over s of ws[s] (in order s = 0, 1, ..., so the result does not
+// depend on scheduling), converted to the output type.  Four outputs per
+// thread; ws_stride is a multiple of 4 so every float4 access is aligned.
+__global__ void __launch_bounds__(256)
+    splitk_reduce(const float *__restrict__ ws, int splits, int64_t ws_stride, int64_t count,
+                  void *__restrict__ y, int yt) {
+  const int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
+  if (i >= count) return;
+  if (i + 4 <= count) {
+    float4 a = *reinterpret_cast<const float4 *>(ws + i);
+    for (int p = 1; p < splits; ++p) {
+      const float4 b = *reinterpret_cast<const float4 *>(ws + p * ws_stride + i);
+      a.x += b.x;
+      a.y += b.y;
+      a.z += b.z;
+      a.w += b.w;
+    }
+    if (yt == EB_F32) {
+      *reinterpret_cast<float4 *>(reinterpret_cast<float *>(y) + i) = a;
+    } else {
+      typedef __bf16 bf4 __attribute__((ext_vector_type(4)));
+      const bf4 v = {(__bf16)a.x, (__bf16)a.y, (__bf16)a.z, (__bf16)a.w};
+      *reinterpret_cast<bf4 *>(reinterpret_cast<__bf16 *>(y) + i) = v;
+    }
+    return;
+  }
+  for (int64_t j = i; j < count; ++j) {
+    float a = ws[j];
+    for (int p = 1; p < splits; ++p) a += ws[p * ws_stride + j];
+    if (yt == EB_F32)
+      reinterpret_cast<float *>(y)[j] = a;
+    else
+      reinterpret_cast<__bf16 *>(y)[j] = (__bf16)a;
+  }
 }
+
+// Tile configurations: {BM, BN, WM, WN, workgroups per CU (LDS-bound),
+// full-chip rate in TFLOP/s on large problems (measured)}.  The rate only
+// ranks configurations against each other.
+struct Cfg {
+  int bm, bn, wm, wn, per_cu;
+  double rate;
+};
+constexpr Cfg kCfgs[] = {
+    {64, 128, 2, 2, 2, 546},   {128, 128, 2, 2, 2, 769},  {128, 256, 2, 4, 1, 773},
+    {256, 128, 4, 2, 1, 812},  {256, 192, 4, 2, 1, 900},  {256, 256, 4, 2, 1, 902},
+    {256, 256, 2, 4, 1, 977},  {256, 256, 2, 2, 1, 835},
+};
+constexpr int kNumCfgs = sizeof(kCfgs) / sizeof(kCfgs[0]);
+
+std::atomic<int> g_force_cfg{-1}, g_force_splits{0};
+
+// Tuning hook: EB_MFMA_CFG=<index> in the environment sets the initial forced
+// configuration.
+int forced_cfg() {
+  static const bool init = [] {
+    const char *e = getenv("EB_MFMA_CFG");
+    if (e) g_force_cfg.store(atoi(e));
+    return true;
+  }();
+  (void)init;
+  return g_force_cfg.load(std::memory_order_relaxed);
+}
+
+constexpr int64_t kMaxWorkspace = int64_t(64) << 20;  // bytes of fp32 partials per call
+constexpr int kMinSplitTiles = 4;                      // K-tiles per split, at least
+
+// Estimated time (s) of one configuration and split count.  Workgroups run in
+// rounds over the CUs; a CU holding w of a configuration's per_cu workgroups
+// delivers rate/cus * sqrt(w / per_cu) (fewer resident waves hide less
+// latency), each round also pays a fixed cost for pipeline fill and epilogue,
+// the whole call is at least as long as streaming the weights from HBM, and
+// splits > 1 add the traffic and launch of the reduction.
+double estimate(int32_t type, const Cfg &g, int64_t m, int64_t n, int64_t k, int splits, int cus) {
+  const int64_t nk = (k + kBK - 1) / kBK;
+  const int64_t tiles = ((m + g.bm - 1) / g.bm) * ((n + g.bn - 1) / g.bn);
+  const int64_t kts = (nk + splits - 1) / splits;
+  const int64_t units = tiles * splits;
+  const int64_t slots = (int64_t)cus * g.per_cu;
+  const double cu_rate = g.rate * 1e12 / cus;
+  const double wg_flops = 2.0 * g.bm * g.bn * kts * kBK;
+  double t = 0;
+  for (int64_t left = units; left > 0; left -= std::min(left, slots)) {
+    const int64_t w = std::min<int64_t>(g.per_cu, (std::min(left, slots) + cus - 1) / cus);
+    t += w * wg_flops / (cu_rate * std::sqrt((double)w / g.per_cu)) + 1e-6;
+  }
+  const double wbytes = (double)n * k * (type == EB_Q8_0 ? 34.0 : 18.0) / 32.0;
+  t = std::max(t, wbytes / 5e12);
+  if (splits > 1) t += (2.0 * splits + 1.0) * (double)m * n * 4 / 4e12 + 3e-6;
+  return t;
+}
+}  // namespace
+
+int mfma_tile_count() { return kNumCfgs; }
+
+void mfma_force(int cfg, int splits) {
+  (void)forced_cfg();
+  g_force_cfg.store(cfg);
+  g_force_splits.store(splits);
+}
+
+int mfma_force_key() { return (forced_cfg() + 1) * 64 + g_force_splits.load(); }
+
+MfmaPlan plan_mfma(int32_t type, int64_t m, int64_t n, int64_t k, bool allow_split) {
+  const int64_t nk = (k + kBK - 1) / kBK;
+  const int cus = device_cu_count();
+  const int fc = forced_cfg(), fs = g_force_splits.load(std::memory_order_relaxed);
+  MfmaPlan best;
+  double best_t = 0;
+  bool have = false;
+  for (int c = 0; c < kNumCfgs; ++c) {
+    if (fc >= 0 && fc < kNumCfgs && c != fc) continue;
+    const Cfg &g = kCfgs[c];
+    const bool fits = type == EB_Q4_0 ? fits_offsets<EB_Q4_0, 0, 0>(n, k, g.bm, g.bn)
+                                      : fits_offsets<EB_Q8_0, 0, 0>(n, k, g.bm, g.bn);
+    if (!fits) continue;
+    for (int sp = 1; sp <= 16; ++sp) {
+      if (sp > 1 && !allow_split) break;
+      if (fs > 0 && sp != fs) continue;
+      const int64_t kts = (nk + sp - 1) / sp;
+      if (sp > 1 && (kts < kMinSplitTiles || (nk + kts - 1) / kts != sp)) continue;
+      const int64_t stride = (m * n + 63) / 64 * 64;
+      const int64_t wsb = sp > 1 ? stride * sp * 4 : 0;
+      if (wsb > kMaxWorkspace && fs <= 0) continue;
+      const double t = estimate(type, g, m, n, k, sp, cus);
+      if (!have || t < best_t * 0.999) {
+        have = true;
+        best_t = t;
+        best.cfg = c;
+        best.splits = sp;
+        best.kts = (int)kts;
+        best.ws_stride = sp > 1 ? stride : 0;
+        best.ws_bytes = (size_t)wsb;
+      }
+    }
+  }
+  if (!have) {  // every accepted shape fits the first configuration unsplit
+    best.cfg = 0;
+    best.splits = 1;
+    best.kts = (int)nk;
+    best.ws_stride = 0;
+    best.ws_bytes = 0;
+  }
+  return best;
+}
+
+namespace {
 
 template <int QT, int XT>
 hipError_t launch_q(const void *wdata, int64_t n, int64_t k, const void *x, int64_t m, void *y,
-                    int32_t yt, hipStream_t s) {
-  int cfg = mfma_cfg_override();
-  if (cfg < 0) cfg = m <= 64 ? 0 : (m <= 128 ? 1 : 2);
-  switch (cfg) {
-    case 0: return launch_t<QT, XT, 64, 128, 2, 2>(wdata, n, k, x, m, y, yt, s);
-    case 1: return launch_t<QT, XT, 128, 128, 2, 2>(wdata, n, k, x, m, y, yt, s);
-    case 2: return launch_t<QT, XT, 256, 256, 2, 2>(wdata, n, k, x, m, y, yt, s);
-    case 3: return launch_t<QT, XT, 256, 256, 2, 4>(wdata, n, k, x, m, y, yt, s);
-    case 4: return launch_t<QT, XT, 128, 256, 2, 2>(wdata, n, k, x, m, y, yt, s);
-    case 5: return launch_t<QT, XT, 256, 128, 2, 2>(wdata, n, k, x, m, y, yt, s);
-    case 6: return launch_t<QT, XT, 128, 256, 2, 4>(wdata, n, k, x, m, y, yt, s);
-    default: return launch_t<QT, XT, 256, 256, 4, 2>(wdata, n, k, x, m, y, yt, s);
+                    int32_t yt, const MfmaPlan &P, float *ws, hipStream_t s) {
+  const int sp = ws ? P.splits : 1;
+  const int kts = ws ? P.kts : (int)((k + kBK - 1) / kBK);
+  const int64_t st = P.ws_stride;
+  hipError_t e;
+  switch (P.cfg) {
+    case 0: e = launch_t<QT, XT, 64, 128, 2, 2>(wdata, n, k, x, m, y, yt, sp, kts, ws, st, s); break;
+    case 1: e = launch_t<QT, XT, 128, 128, 2, 2>(wdata, n, k, x, m, y, yt, sp, kts, ws, st, s); break;
+    case 2: e = launch_t<QT, XT, 128, 256, 2, 4>(wdata, n, k, x, m, y, yt, sp, kts, ws, st, s); break;
+    case 3: e = launch_t<QT, XT, 256, 128, 4, 2>(wdata, n, k, x, m, y, yt, sp, kts, ws, st, s); break;
+    case 4: e = launch_t<QT, XT, 256, 192, 4, 2>(wdata, n, k, x, m, y, yt, sp, kts, ws, st, s); break;
+    case 5: e = launch_t<QT, XT, 256, 256, 4, 2>(wdata, n, k, x, m, y, yt, sp, kts, ws, st, s); break;
+    case 6: e = launch_t<QT, XT, 256, 256, 2, 4>(wdata, n, k, x, m, y, yt, sp, kts, ws, st, s); break;
+    default: e = launch_t<QT, XT, 256, 256, 2, 2>(wdata, n, k, x, m, y, yt, sp, kts, ws, st, s); break;
   }
+  if (e != hipSuccess || sp == 1) return e;
+  const int64_t count = m * n;
+  const int64_t blocks = (count + 1023) / 1024;
+  splitk_reduce<<<(unsigned)blocks, 256, 0, s>>>(ws, sp, st, count, y, yt);
+  return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_mfma(int32_t type, const void *wdata, int64_t n, int64_t k, const void *x,
-                       int32_t xt, int64_t m, void *y, int32_t yt, hipStream_t s) {
+                       int32_t xt, int64_t m, void *y, int32_t yt, const MfmaPlan &plan, float *ws,
+                       hipStream_t s) {
   if (type == EB_Q4_0) {
-    if (xt == EB_F16) return launch_q<EB_Q4_0, EB_F16>(wdata, n, k, x, m, y, yt, s);
-    return launch_q<EB_Q4_0, EB_BF16>(wdata, n, k, x, m, y, yt, s);
+    if (xt == EB_F16) return launch_q<EB_Q4_0, EB_F16>(wdata, n, k, x, m, y, yt, plan, ws, s);
+    return launch_q<EB_Q4_0, EB_BF16>(wdata, n, k, x, m, y, yt, plan, ws, s);
   }
-  if (xt == EB_F16) return launch_q<EB_Q8_0, EB_F16>(wdata, n, k, x, m, y, yt, s);
-  return launch_q<EB_Q8_0, EB_BF16>(wdata, n, k, x, m, y, yt, s);
+  if (xt == EB_F16) return launch_q<EB_Q8_0, EB_F16>(wdata, n, k, x, m, y, yt, plan, ws, s);
+  return launch_q<EB_Q8_0, EB_BF16>(wdata, n, k, x, m, y, yt, plan, ws, s);
 }
 
 }  // namespace eb

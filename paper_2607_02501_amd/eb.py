@@ -87,6 +87,10 @@ lib.eb_qlinear_stack_launches.restype = _i32
 lib.eb_qlinear_stack_launches.argtypes = [ctypes.POINTER(eb_qlinear_op), _i32]
 lib.eb_stack_cache_clear.restype = _i32
 lib.eb_stack_cache_clear.argtypes = []
+lib.eb_mfma_tile_count.restype = _i32
+lib.eb_mfma_tile_count.argtypes = []
+lib.eb_mfma_force.restype = _i32
+lib.eb_mfma_force.argtypes = [_i32, _i32]
 
 
 class EBError(RuntimeError):
@@ -221,3 +225,12 @@ def stack_launches(ops: ctypes.Array) -> int:
 
 def stack_cache_clear() -> None:
     _check(lib.eb_stack_cache_clear(), "eb_stack_cache_clear")
+
+
+def mfma_tile_count() -> int:
+    return int(lib.eb_mfma_tile_count())
+
+
+def mfma_force(tile: int = -1, splits: int = 0) -> None:
+    """Force the MFMA tile configuration / split-K factor (-1 / 0: automatic)."""
+    _check(lib.eb_mfma_force(tile, splits), "eb_mfma_force")

@@ -230,3 +230,27 @@ def test_stack_breaks_runs_on_format_and_m(eb, monkeypatch):
     assert _launches(eb, [a[0]]) == 1
     bad = a + [_op(eb, 5 * GB, 10 * GB, 11 * GB, k=33)]
     assert _launches(eb, bad) == eb.EB_ERR_INVALID
+
+
+def test_mfma_force_validation(eb):
+    count = eb.lib.eb_mfma_tile_count()
+    assert count >= 1
+    f = eb.lib.eb_mfma_force
+    assert f(-2, 0) == eb.EB_ERR_INVALID
+    assert f(count, 0) == eb.EB_ERR_INVALID
+    assert f(0, 17) == eb.EB_ERR_INVALID
+    assert f(0, -1) == eb.EB_ERR_INVALID
+    assert f(-1, 0) == eb.EB_OK
+
+
+def test_stack_counts_split_k_reduction(eb):
+    # a long-k MFMA op: one launch unsplit, two (GEMM + reduction) when split
+    op = [_op(eb, 1 * GB, 8 * GB, 9 * GB, k=16384, n=2048, m=816, qtype=eb.EB_Q8_0,
+              xt=eb.EB_BF16)]
+    try:
+        assert eb.lib.eb_mfma_force(-1, 1) == eb.EB_OK
+        assert _launches(eb, op) == 1
+        assert eb.lib.eb_mfma_force(-1, 4) == eb.EB_OK
+        assert _launches(eb, op) == 2
+    finally:
+        eb.lib.eb_mfma_force(-1, 0)

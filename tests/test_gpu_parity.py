@@ -128,6 +128,48 @@ def test_qlinear_mfma_parity(eb, oracle, qtype, xdtype, n, k):
     assert_parity(y, y_ref, bound, TOL_BF16, "mfma bf16 out")
 
 
+@pytest.fixture
+def forced(eb):
+    """eb.mfma_force, restored to the automatic choice afterwards."""
+    yield eb.mfma_force
+    eb.mfma_force(-1, 0)
+
+
+@pytest.mark.parametrize("qtype,xdtype", [("q8_0", torch.bfloat16), ("q4_0", torch.float16),
+                                          ("q4_0", torch.bfloat16)])
+def test_every_mfma_tile_and_split(eb, oracle, forced, qtype, xdtype):
+    # ragged m and n for every tile shape, an odd block count (K tail), 33 K-tiles
+    m, n, k = 300, 520, 2080
+    w, x = _case(77, n, k, m, xdtype)
+    qw = eb.quantize(w.to(DEV), qtype)
+    _, y_ref, bound = oracle_reference(oracle, qtype, w.numpy(), x)
+    xd = x.to(DEV)
+    for tile in range(eb.mfma_tile_count()):
+        for splits in (1, 3):
+            forced(tile, splits)
+            y = eb.qlinear(qw, xd, path="mfma")
+            assert_parity(y, y_ref, bound, TOL_F32, f"tile {tile} splits {splits}")
+        forced(tile, 4)
+        y = eb.qlinear(qw, xd[:70], out_dtype=torch.bfloat16, path="mfma")
+        assert_parity(y, y_ref[:70], bound[:70], TOL_BF16, f"tile {tile} splits 4 bf16 out")
+
+
+def test_split_k_deterministic_and_matches_unsplit(eb, forced):
+    n, k = 384, 8192
+    w, x = _case(43, n, k, 96, torch.bfloat16)
+    qw = eb.quantize(w.to(DEV), "q8_0")
+    xd = x.to(DEV)
+    forced(1, 1)
+    whole = eb.qlinear(qw, xd, path="mfma")
+    forced(1, 6)
+    a = eb.qlinear(qw, xd, path="mfma")
+    b = eb.qlinear(qw, xd, path="mfma")
+    assert torch.equal(a, b)
+    # same products, summed in another order: close, not necessarily equal
+    scale = (x.float().abs() @ w.abs().t()).to(DEV)
+    assert float(((a - whole).abs() / scale).max()) < 1e-4
+
+
 @pytest.mark.parametrize("qtype", ["q8_0", "q4_0"])
 def test_qlinear_auto_matches_forced_path(eb, qtype):
     n, k = 300, 1024
@@ -199,7 +241,8 @@ def test_minimum_and_empty_shapes(eb, oracle):
 
 def test_stack_matches_single_calls(eb, monkeypatch):
     shapes = [("q4_0", torch.float16, 1, 300, 512), ("q8_0", torch.bfloat16, 50, 200, 1024),
-              ("q4_0", torch.bfloat16, 130, 260, 352), ("q8_0", torch.float16, 3, 96, 4096)]
+              ("q4_0", torch.bfloat16, 130, 260, 352), ("q8_0", torch.float16, 3, 96, 4096),
+              ("q8_0", torch.bfloat16, 64, 256, 8192), ("q4_0", torch.bfloat16, 100, 192, 6144)]
     entries, refs = [], []
     for i, (qt, xdt, m, n, k) in enumerate(shapes):
         w, x = _case(500 + i, n, k, m, xdt)
