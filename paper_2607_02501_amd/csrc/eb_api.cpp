@@ -195,16 +195,21 @@ struct Step {
   int op = -1;        // single op index, or -1 for a fused launch
   bool mfma = false;  // single op on the MFMA path, run with plan `mp`
   MfmaPlan mp;
-  int32_t type = 0, xt = 0;
+  bool mm = false;    // fused MFMA launch (op == -1)
+  int32_t type = 0, xt = 0, yt = 0;
   int ns = 0;
-  size_t table = 0;   // first entry in the device table
+  size_t table = 0;   // first entry in the device table (M1Op or MMOp)
   int nops = 0;
   int64_t units = 0, rows = 0;
+  int mm_cfg = 0, groups = 0;
+  size_t wg = 0;      // first entry of the workgroup ranges
 };
 
 struct Plan {
   std::vector<Step> steps;
-  M1Op *table = nullptr;  // device copy of every fused launch's op table
+  M1Op *table = nullptr;  // device copy of every fused GEMV launch's op table
+  MMOp *mmtable = nullptr;  // same for fused MFMA launches
+  int64_t *mmwg = nullptr;  // their workgroup unit ranges
   float *ws = nullptr;    // split-K workspace shared by the plan's MFMA steps (run in order)
   size_t ws_bytes = 0;
   hipGraph_t graph = nullptr;
@@ -220,14 +225,83 @@ bool fusable(const eb_qlinear_op &o) {
   return o.m == 1 && gemv_fits(1, o.w.k) && m1_fusable(o.w.type, o.m, o.w.k);
 }
 
+// small-m MFMA ops, whose single launches are latency-bound
+bool mm_fusable(const eb_qlinear_op &o) {
+  return o.m >= 1 && o.m <= kMMaxM && o.w.k <= kMMaxK &&
+         pick_path(o.w.type, o.x_type, o.m, o.w.n, o.w.k) == EB_PATH_MFMA;
+}
+
 // Builds the plan; with `alloc`, also allocates and fills its device table
 // when any run is fused (without it the plan is only counted).
 eb_status build_plan(const eb_qlinear_op *ops, int32_t n_ops, bool alloc, Plan &P) {
-  const bool allow_fuse = true;
   std::vector<M1Op> host;
-  const bool fuse = allow_fuse && !env_off("EB_STACK_FUSE");
+  std::vector<MMOp> mmhost;
+  std::vector<int64_t> mmwg;
+  const bool fuse = !env_off("EB_STACK_FUSE");
   int32_t i = 0;
   while (i < n_ops) {
+    if (fuse && mm_fusable(ops[i])) {
+      // run of independent small-m MFMA ops with the same formats
+      std::vector<OpSpan> spans{span_of(ops[i])};
+      int32_t j = i + 1;
+      for (; j < n_ops; ++j) {
+        const eb_qlinear_op &o = ops[j];
+        if (!mm_fusable(o) || o.w.type != ops[i].w.type || o.x_type != ops[i].x_type ||
+            o.y_type != ops[i].y_type)
+          break;
+        const OpSpan sj = span_of(o);
+        bool ok = true;
+        for (const OpSpan &sp : spans) ok = ok && independent(sp, sj);
+        if (!ok) break;
+        spans.push_back(sj);
+      }
+      if (j - i == 1) {
+        Step s;
+        s.op = i++;
+        P.steps.push_back(s);
+        continue;
+      }
+      int64_t max_m = 0;
+      for (int32_t r = i; r < j; ++r) max_m = std::max(max_m, ops[r].m);
+      Step s;
+      s.mm = true;
+      s.type = ops[i].w.type;
+      s.xt = ops[i].x_type;
+      s.yt = ops[i].y_type;
+      s.mm_cfg = mm_cfg(max_m);
+      s.table = mmhost.size();
+      std::vector<MMOp> run;
+      int64_t units = 0;
+      for (int32_t r = i; r < j; ++r) {
+        const eb_qlinear_op &o = ops[r];
+        const Layout L = layout_of(o.w.type, o.w.n, o.w.k);
+        MMOp e{};
+        e.w = static_cast<const uint8_t *>(o.w.data);
+        e.x = static_cast<const uint16_t *>(o.x);
+        e.y = o.y;
+        e.d_off = L.d_off;
+        units += mm_tiles(s.mm_cfg, o.m, o.w.n);
+        e.unit_end = units;
+        e.ds = (int32_t)L.ds;
+        e.m = (int32_t)o.m;
+        e.n = (int32_t)o.w.n;
+        e.k = (int32_t)o.w.k;
+        e.tiles_n = (int32_t)mm_tiles(s.mm_cfg, 1, o.w.n);
+        e.nk = (int32_t)((o.w.k + 63) / 64);
+        e.yt = o.y_type;
+        run.push_back(e);
+      }
+      std::vector<int64_t> wg;
+      s.groups = mm_partition(run, s.mm_cfg, wg);
+      s.nops = (int)run.size();
+      s.units = units;
+      s.wg = mmwg.size();
+      mmhost.insert(mmhost.end(), run.begin(), run.end());
+      mmwg.insert(mmwg.end(), wg.begin(), wg.end());
+      P.steps.push_back(s);
+      i = j;
+      continue;
+    }
     if (!fuse || !fusable(ops[i])) {
       Step s;
       s.op = i++;
@@ -278,6 +352,21 @@ eb_status build_plan(const eb_qlinear_op *ops, int32_t n_ops, bool alloc, Plan &
     }
     i = j;
   }
+  if (alloc && !mmhost.empty()) {
+    if (hipMalloc((void **)&P.mmtable, mmhost.size() * sizeof(MMOp)) != hipSuccess) {
+      P.mmtable = nullptr;
+      return EB_ERR_HIP;
+    }
+    if (hipMalloc((void **)&P.mmwg, mmwg.size() * sizeof(int64_t)) != hipSuccess) {
+      P.mmwg = nullptr;
+      return EB_ERR_HIP;
+    }
+    if (hipMemcpy(P.mmtable, mmhost.data(), mmhost.size() * sizeof(MMOp),
+                  hipMemcpyHostToDevice) != hipSuccess ||
+        hipMemcpy(P.mmwg, mmwg.data(), mmwg.size() * sizeof(int64_t), hipMemcpyHostToDevice) !=
+            hipSuccess)
+      return EB_ERR_HIP;
+  }
   for (Step &s : P.steps) {
     if (s.op < 0) continue;
     const eb_qlinear_op &o = ops[s.op];
@@ -304,7 +393,11 @@ eb_status build_plan(const eb_qlinear_op *ops, int32_t n_ops, bool alloc, Plan &
 
 eb_status run_plan(const eb_qlinear_op *ops, const Plan &P, hipStream_t s) {
   for (const Step &st : P.steps) {
-    if (st.mfma) {
+    if (st.mm) {
+      if (launch_mfma_multi(st.type, st.xt, st.yt, st.mm_cfg, P.mmtable + st.table, st.nops,
+                            P.mmwg + st.wg, st.groups, s) != hipSuccess)
+        return EB_ERR_HIP;
+    } else if (st.mfma) {
       const eb_qlinear_op &o = ops[st.op];
       if (launch_mfma(o.w.type, o.w.data, o.w.n, o.w.k, o.x, o.x_type, o.m, o.y, o.y_type, st.mp,
                       st.mp.splits > 1 ? P.ws : nullptr, s) != hipSuccess)
@@ -325,6 +418,8 @@ void destroy_plan(Plan &p) {
   if (p.exec) (void)hipGraphExecDestroy(p.exec);
   if (p.graph) (void)hipGraphDestroy(p.graph);
   if (p.table) (void)hipFree(p.table);
+  if (p.mmtable) (void)hipFree(p.mmtable);
+  if (p.mmwg) (void)hipFree(p.mmwg);
   if (p.ws) (void)hipFree(p.ws);
   p = Plan();
 }

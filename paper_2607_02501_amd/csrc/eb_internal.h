@@ -6,6 +6,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <vector>
+
 #include "../../include/eb.h"
 
 namespace eb {
@@ -88,6 +90,31 @@ hipError_t launch_mfma(int32_t type, const void *wdata, int64_t n, int64_t k, co
                        int32_t xt, int64_t m, void *y, int32_t yt, const MfmaPlan &plan, float *ws,
                        hipStream_t s);
 int mfma_tile_count();
+
+// Fused MFMA launch over several independent ops of a stack: one persistent
+// launch whose workgroups each run a contiguous range of output tiles
+// (units), balanced by K-tile steps, as one continuous load/compute pipeline.
+// The table and the per-workgroup unit ranges live in device memory.
+struct MMOp {
+  const uint8_t *w;    // planar weights
+  const uint16_t *x;   // activations [m][k]
+  void *y;             // outputs [m][n]
+  int64_t d_off;       // scale-plane offset
+  int64_t unit_end;    // tiles of this op and all ops before it
+  int32_t ds, m, n, k; // ds: scale-plane row stride (elements)
+  int32_t tiles_n, nk, yt, pad;
+};
+constexpr int kMMaxM = 128;               // rows an op may have to join a fused run
+constexpr int64_t kMMaxK = int64_t(1) << 22;  // keeps every per-tile byte span within 32 bits
+int mm_cfg(int64_t max_m);                // tile configuration for a run
+int64_t mm_tiles(int cfg, int64_t m, int64_t n);
+// Fills the unit ranges wg[0..groups] (balanced by steps) for a table whose
+// unit_end / nk are set; returns the number of workgroups to launch.
+int mm_partition(const std::vector<MMOp> &ops, int cfg, std::vector<int64_t> &wg);
+// All ops of one launch share the weight format, x type and y type.
+// groups must be a positive multiple of 8 (mm_partition's result).
+hipError_t launch_mfma_multi(int32_t type, int32_t xt, int32_t yt, int cfg, const MMOp *dev_ops,
+                             int nops, const int64_t *dev_wg, int groups, hipStream_t s);
 void mfma_force(int cfg, int splits);  // cfg -1 / splits 0: automatic
 int mfma_force_key();                  // changes whenever the forced state does
 

@@ -254,3 +254,24 @@ def test_stack_counts_split_k_reduction(eb):
         assert _launches(eb, op) == 2
     finally:
         eb.lib.eb_mfma_force(-1, 0)
+
+
+def test_stack_fuses_independent_small_m_mfma_ops(eb, monkeypatch):
+    monkeypatch.delenv("EB_STACK_FUSE", raising=False)
+    bf = eb.EB_BF16
+    ops = [_op(eb, 1 * GB + i * (64 << 20), 8 * GB + i * (1 << 20), 9 * GB + i * (1 << 20),
+               k=1024, n=2048, m=50, qtype=eb.EB_Q8_0, xt=bf) for i in range(8)]
+    assert _launches(eb, ops) == 1
+    # a different output type starts a new run (the lone op may be split-K: 2 launches)
+    odd = _op(eb, 5 * GB, 10 * GB, 11 * GB, k=1024, n=2048, m=50, qtype=eb.EB_Q8_0, xt=bf, yt=bf)
+    assert _launches(eb, ops[:4] + [odd] + ops[4:]) == 2 + _launches(eb, [odd])
+    # m above the fused limit runs alone
+    big = _op(eb, 5 * GB, 10 * GB, 11 * GB, k=1024, n=2048, m=200, qtype=eb.EB_Q8_0, xt=bf)
+    assert _launches(eb, ops[:4] + [big] + ops[4:]) == 2 + _launches(eb, [big])
+    # read-after-write: the second op reads the first one's output
+    W0, W1 = 1 * GB, 2 * GB
+    raw = [_op(eb, W0, 8 * GB, 9 * GB, k=1024, n=1024, m=50, qtype=eb.EB_Q8_0, xt=bf, yt=bf),
+           _op(eb, W1, 9 * GB, 10 * GB, k=1024, n=1024, m=50, qtype=eb.EB_Q8_0, xt=bf)]
+    assert _launches(eb, raw) == _launches(eb, raw[:1]) + _launches(eb, raw[1:])
+    monkeypatch.setenv("EB_STACK_FUSE", "0")
+    assert _launches(eb, ops) == 8 * _launches(eb, ops[:1])
