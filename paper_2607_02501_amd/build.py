@@ -22,12 +22,14 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libeb.so")
 
 ARCH = "gfx950"
-SOURCES = ["eb_api.cpp", "quantize.hip", "gemv.hip", "mfma.hip"]
+SOURCES = ["eb_api.cpp", "quantize.hip", "gemv.hip", "mfma.hip", "mfma_multi.hip"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-I", INCLUDE, "-I", CSRC,
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
           "-fhip-fp32-correctly-rounded-divide-sqrt", "-fno-gpu-flush-denormals-to-zero",
           "-Wall", "-Wno-unused-function", "-Wno-unknown-pragmas"]
-PER_FILE = {"quantize.hip": ["-ffp-contract=off"]}
+PER_FILE = {"quantize.hip": ["-ffp-contract=off"],
+            # keep MFMA accumulators in VGPRs in the fused persistent kernel
+            "mfma_multi.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]}
 
 
 def hipcc() -> str:

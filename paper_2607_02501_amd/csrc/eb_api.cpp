@@ -227,7 +227,9 @@ bool fusable(const eb_qlinear_op &o) {
 
 // small-m MFMA ops, whose single launches are latency-bound
 bool mm_fusable(const eb_qlinear_op &o) {
+  // the fused kernel addresses outputs with 32-bit offsets over 128-row tiles
   return o.m >= 1 && o.m <= kMMaxM && o.w.k <= kMMaxK &&
+         o.w.n * kMMaxM * (int64_t)dsize(o.y_type) < (int64_t(1) << 31) &&
          pick_path(o.w.type, o.x_type, o.m, o.w.n, o.w.k) == EB_PATH_MFMA;
 }
 

@@ -36,136 +36,11 @@
 #include <cstdlib>
 
 #include "eb_internal.h"
+#include "mfma_common.h"
+
 
 namespace eb {
 namespace {
-
-typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
-typedef float f32x16_t __attribute__((ext_vector_type(16)));
-
-constexpr int kBK = 64;        // K elements per tile (2 blocks)
-constexpr int kXcds = 8;
-
-template <int XT>
-__device__ inline uint32_t pack2(float a, float b) {
-  if (XT == EB_BF16) {
-    typedef __bf16 bf2 __attribute__((ext_vector_type(2)));
-    bf2 v = {(__bf16)a, (__bf16)b};  // v_cvt_pk_bf16_f32, round to nearest even
-    return __builtin_bit_cast(uint32_t, v);
-  }
-  return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)a) |
-         ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)b) << 16);
-}
-
-template <int XT>
-__device__ inline f32x16_t mfma32(const uint4 a, const uint4 b, f32x16_t c) {
-  if (XT == EB_BF16)
-    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
-                                                   __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
-  return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8_t, a),
-                                                __builtin_bit_cast(f16x8_t, b), c, 0, 0, 0);
-}
-
-template <int QT>
-struct WTile {
-  // 16-byte weight chunks per row per K-tile: Q8_0 four half-blocks, Q4_0 two blocks
-  static constexpr int kChunksPerRow = (QT == EB_Q8_0) ? 4 : 2;
-  static constexpr int kElemsPerChunk = (QT == EB_Q8_0) ? 16 : 32;
-};
-
-// Dequantize one 16-byte chunk of codes into 16-byte vectors of 16-bit
-// weights, in k order: Q8_0 16 codes -> 2 vectors, Q4_0 one block -> 4.
-// Each code c in 0..255 (Q8_0: q + 128) or 0..15 (Q4_0 nibble) is placed
-// under the binary16 exponent of 1024 by one byte permute per two codes,
-// giving the binary16 value 1024 + c exactly; then
-//   fma(1024 + c, d, -(1024 + z) d) = (c - z) d,   z = 128 (Q8_0) or 8 (Q4_0),
-// is exact (1152 d and 1032 d need at most 19 significant bits), and the one
-// rounding to the 16-bit activation type is round-to-nearest-even.
-template <int QT>
-struct Deq {
-  static constexpr int kVecs = (QT == EB_Q8_0) ? 2 : 4;
-};
-
-// two codes in bytes b0, b1 of v -> 16-bit halves 0x64bb of the result
-__device__ inline uint32_t under_1024(uint32_t v, uint32_t sel) {
-  return __builtin_amdgcn_perm(0x64646464u, v, sel);
-}
-
-template <int XT>
-__device__ inline uint32_t deq_pair(uint32_t h2, float d, float c) {
-  const _Float16 a = __builtin_bit_cast(_Float16, (uint16_t)(h2 & 0xffffu));
-  const _Float16 b = __builtin_bit_cast(_Float16, (uint16_t)(h2 >> 16));
-  return pack2<XT>(__builtin_fmaf((float)a, d, c), __builtin_fmaf((float)b, d, c));
-}
-
-template <int QT, int XT>
-__device__ inline void dequant_chunk(const uint4 q, float d, uint4 (&v)[Deq<QT>::kVecs]) {
-  const uint32_t w[4] = {q.x, q.y, q.z, q.w};
-  // byte selectors: {S1.b0, 0x64, S1.b1, 0x64} and {S1.b2, 0x64, S1.b3, 0x64}
-  constexpr uint32_t kSelLo = 0x04010400u, kSelHi = 0x04030402u;
-  if constexpr (QT == EB_Q8_0) {
-    const float c = -1152.0f * d;
-    uint32_t o[8];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const uint32_t u = w[j] ^ 0x80808080u;
-      o[2 * j] = deq_pair<XT>(under_1024(u, kSelLo), d, c);
-      o[2 * j + 1] = deq_pair<XT>(under_1024(u, kSelHi), d, c);
-    }
-    v[0] = make_uint4(o[0], o[1], o[2], o[3]);
-    v[1] = make_uint4(o[4], o[5], o[6], o[7]);
-  } else {
-    const float c = -1032.0f * d;
-    uint32_t lo[8], hi[8];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const uint32_t l = w[j] & 0x0f0f0f0fu, h = (w[j] >> 4) & 0x0f0f0f0fu;
-      lo[2 * j] = deq_pair<XT>(under_1024(l, kSelLo), d, c);
-      lo[2 * j + 1] = deq_pair<XT>(under_1024(l, kSelHi), d, c);
-      hi[2 * j] = deq_pair<XT>(under_1024(h, kSelLo), d, c);
-      hi[2 * j + 1] = deq_pair<XT>(under_1024(h, kSelHi), d, c);
-    }
-    v[0] = make_uint4(lo[0], lo[1], lo[2], lo[3]);
-    v[1] = make_uint4(lo[4], lo[5], lo[6], lo[7]);
-    v[2] = make_uint4(hi[0], hi[1], hi[2], hi[3]);
-    v[3] = make_uint4(hi[4], hi[5], hi[6], hi[7]);
-  }
-}
-
-// Raw buffer descriptor over [base, base + bytes): every lane whose offset is
-// at or past `bytes` reads zeros, which is how the kernel handles rows past m
-// or n without branches.  The descriptor is rebuilt per K-tile (scalar work),
-// so the hardware range check always covers the whole access.
-__device__ inline __amdgpu_buffer_rsrc_t rsrc(const void *base, uint32_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes,
-                                           0x00020000);
-}
-
-__device__ inline uint4 bload(__amdgpu_buffer_rsrc_t r, uint32_t voff) {
-  const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, 0, 0);
-  return make_uint4(v[0], v[1], v[2], v[3]);
-}
-
-typedef __attribute__((address_space(3))) void lds_void;
-
-// Position of 16-byte chunk c of row r in the unpadded x tile (128-byte rows):
-// c ^ swz(r).  Any 16 consecutive rows read at one chunk index hit 16 distinct
-// 16-byte bank groups, and any 8 consecutive rows 8 distinct ones.
-__device__ inline uint32_t swz(uint32_t r) { return (r ^ (r >> 3)) & 7; }
-
-// Wait until at most N vector-memory operations of this wave are outstanding
-// and its LDS writes are done, then barrier.  Unlike __syncthreads this does
-// not drain every load, so loads issued for later K-tiles stay in flight.  The
-// "memory" clobber keeps IR passes, and the scheduling barriers the machine
-// scheduler, from moving memory accesses across it.
-template <int N>
-__device__ inline void wait_vm_barrier() {
-  // sched_barrier(0): the machine scheduler moves nothing across this point
-  __builtin_amdgcn_sched_barrier(0);
-  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
-  __builtin_amdgcn_sched_barrier(0);
-}
 
 template <int QT, int XT, int BM, int BN, int WM, int WN>
 __global__ void __launch_bounds__(WM *WN * 64)
@@ -422,315 +297,6 @@ __global__ void __launch_bounds__(WM *WN * 64)
     }
 }
 
-// ---------------------------------------------------------------------------
-// Fused launch over many independent ops (small m).  Workgroup p runs the
-// tiles (units) [wg[p], wg[p+1]) of the op table in order, as one stream of
-// K-tile steps: the pipeline of mfma_kernel (x tile t+2 and weight tile t+3 in
-// flight during the MFMAs of tile t) runs across unit and op boundaries, and
-// a unit's epilogue is written when its last step is done.  Three cursors walk
-// the stream: the step being computed, the x copy two steps ahead and the
-// weight loads three steps ahead.  Loads past the end of the range are issued
-// with an empty range (they read zeros and touch no memory), so every step
-// issues the same instructions.
-// ---------------------------------------------------------------------------
-struct MMCursor {
-  int op;       // table index
-  int64_t u;    // global unit index
-  int kt;       // K-tile within the unit
-  bool valid;
-  int nk;
-  int64_t op_end;
-  int64_t m0, n0;
-  int rows_m, rows_n;
-  // fields of the op, copied when the cursor enters a unit
-  const uint16_t *x;
-  const uint8_t *w;
-  void *y;
-  int64_t d_off;
-  int k, ds, n, yt;
-};
-
-template <int BM, int BN>
-__device__ inline void mm_enter(const MMOp *__restrict__ ops, MMCursor &c) {
-  const MMOp o = ops[c.op];
-  const int64_t first = c.op ? ops[c.op - 1].unit_end : 0;
-  const uint32_t uin = (uint32_t)(c.u - first), tiles_n = (uint32_t)o.tiles_n;
-  const uint32_t tm = uin / tiles_n, tn = uin - tm * tiles_n;
-  c.nk = o.nk;
-  c.op_end = o.unit_end;
-  c.m0 = (int64_t)tm * BM;
-  c.n0 = (int64_t)tn * BN;
-  c.rows_m = (int)min((int64_t)BM, (int64_t)o.m - c.m0);
-  c.rows_n = (int)min((int64_t)BN, (int64_t)o.n - c.n0);
-  c.x = o.x;
-  c.w = o.w;
-  c.y = o.y;
-  c.d_off = o.d_off;
-  c.k = o.k;
-  c.ds = o.ds;
-  c.n = o.n;
-  c.yt = o.yt;
-}
-
-template <int BM, int BN>
-__device__ inline void mm_advance(const MMOp *__restrict__ ops, MMCursor &c, int64_t u_end) {
-  if (!c.valid) return;
-  if (++c.kt < c.nk) return;
-  c.kt = 0;
-  if (++c.u >= u_end) {
-    c.valid = false;
-    return;
-  }
-  if (c.u >= c.op_end) ++c.op;
-  mm_enter<BM, BN>(ops, c);
-}
-
-template <int QT, int XT, int YT, int BM, int BN, int WM, int WN>
-__global__ void __launch_bounds__(WM *WN * 64)
-    mfma_multi_kernel(const MMOp *__restrict__ ops, int nops, const int64_t *__restrict__ wg,
-                      int groups) {
-  constexpr int T = WM * WN * 64;
-  constexpr int WAVES = WM * WN;
-  constexpr int TM = BM / WM, TN = BN / WN;
-  constexpr int FM = TM / 32, FN = TN / 32;
-  constexpr int ADMA = BM / (8 * WAVES);
-  constexpr int WCPR = WTile<QT>::kChunksPerRow;
-  constexpr int WCH = BN * WCPR;
-  constexpr int BCH = (WCH + T - 1) / T;
-  constexpr int KSTEPS = kBK / 16;
-  constexpr int QSB = (QT == EB_Q8_0) ? 32 : 16;
-  constexpr int NV = Deq<QT>::kVecs;
-  constexpr int ABYTES = BM * kBK * 2, BBYTES = BN * kBK * 2;
-  constexpr int NX = ADMA, NW = 2 * BCH;
-  static_assert(ADMA >= 1 && ADMA * 8 * WAVES == BM, "x tile must split into 8-row copies");
-  static_assert(TM % 32 == 0 && TN % 32 == 0, "wave sub-tile must be whole fragments");
-  static_assert(2 * NW + NX <= 63, "vmcnt range");
-
-  __shared__ __attribute__((aligned(1024))) uint8_t sA0[ABYTES];
-  __shared__ __attribute__((aligned(1024))) uint8_t sA1[ABYTES];
-  __shared__ __attribute__((aligned(1024))) uint8_t sA2[ABYTES];
-  __shared__ __attribute__((aligned(1024))) uint8_t sB0[BBYTES];
-  __shared__ __attribute__((aligned(1024))) uint8_t sB1[BBYTES];
-
-  // consecutive unit ranges go to workgroups on the same XCD (shared L2)
-  const int g = blockIdx.x;
-  const int p = (groups % kXcds == 0) ? (g % kXcds) * (groups / kXcds) + g / kXcds : g;
-  const int64_t u_begin = wg[p], u_end = wg[p + 1];
-  if (u_begin >= u_end) return;
-
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave / WN, wn = wave % WN;
-
-  // first op of the range: binary search over the ascending unit_end (the
-  // last op's unit_end is the total, which exceeds u_begin)
-  int lo = 0, hi = nops - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi) / 2;
-    if (ops[mid].unit_end <= u_begin) lo = mid + 1; else hi = mid;
-  }
-  // steps of the range
-  int64_t nsteps = 0;
-  for (int o = lo;; ++o) {
-    const int64_t first = o ? ops[o - 1].unit_end : 0;
-    const int64_t a = max(first, u_begin), b = min(ops[o].unit_end, u_end);
-    nsteps += (b - a) * ops[o].nk;
-    if (ops[o].unit_end >= u_end) break;
-  }
-
-  MMCursor C;
-  C.op = lo;
-  C.u = u_begin;
-  C.kt = 0;
-  C.valid = true;
-  mm_enter<BM, BN>(ops, C);
-  MMCursor X = C;
-  mm_advance<BM, BN>(ops, X, u_end);
-  MMCursor W = X;
-  mm_advance<BM, BN>(ops, W, u_end);
-
-  // per-thread tile-local parts of the x copies and weight loads
-  uint32_t xr_[ADMA], xc_[ADMA];
-#pragma unroll
-  for (int i = 0; i < ADMA; ++i) {
-    const uint32_t r = 8 * (i * WAVES + wave) + (lane >> 3);
-    xr_[i] = r;
-    xc_[i] = ((lane & 7) ^ swz(r)) << 4;
-  }
-  uint32_t wr_[BCH], wq_[BCH], wd_[BCH], wl[BCH];
-#pragma unroll
-  for (int i = 0; i < BCH; ++i) {
-    const int idx = min(tid + i * T, WCH), r = idx / WCPR, c = idx % WCPR;
-    const int blk = (QT == EB_Q8_0) ? (c >> 1) : c;
-    wr_[i] = r;
-    wq_[i] = blk * QSB + ((QT == EB_Q8_0) ? (c & 1) * 16 : 0);
-    wd_[i] = blk * 2;
-    wl[i] = (uint32_t)(r * (kBK * 2) + (((NV * c) ^ swz(r)) << 4));
-  }
-
-  auto load_x = [&](uint8_t *sA, const MMCursor &c) __attribute__((always_inline)) {
-    const uint32_t row = (uint32_t)c.k * 2;
-    const uint8_t *base = reinterpret_cast<const uint8_t *>(c.x) + (c.m0 * c.k + c.kt * kBK) * 2;
-    const uint32_t rec = c.valid ? (uint32_t)(c.rows_m * row - c.kt * (kBK * 2)) : 0u;
-    const auto xr = rsrc(base, rec);
-#pragma unroll
-    for (int i = 0; i < ADMA; ++i)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(
-          xr, (lds_void *)(sA + (i * WAVES + wave) * 1024), 16, (int)(xr_[i] * row + xc_[i]), 0,
-          0, 0);
-  };
-
-  struct Raw {
-    uint4 b[BCH];
-    uint16_t d[BCH];
-  };
-  Raw S0, S1, S2;
-  auto load_w = [&](Raw &S, const MMCursor &c) __attribute__((always_inline)) {
-    const int64_t nb = c.k / kQK;
-    const uint32_t qrow = (uint32_t)(nb * QSB), drow = (uint32_t)c.ds * 2;
-    const uint8_t *qb = c.w + (c.n0 * nb + c.kt * 2) * QSB;
-    const uint8_t *db = c.w + c.d_off + (c.n0 * c.ds + c.kt * 2) * 2;
-    const uint32_t qrec = c.valid ? (uint32_t)(c.rows_n * qrow - c.kt * (2 * QSB)) : 0u;
-    const uint32_t drec = c.valid ? (uint32_t)(c.rows_n * drow - c.kt * 4) : 0u;
-    const auto qr = rsrc(qb, qrec);
-    const auto dr = rsrc(db, drec);
-#pragma unroll
-    for (int i = 0; i < BCH; ++i) {
-      S.b[i] = bload(qr, wr_[i] * qrow + wq_[i]);
-      S.d[i] = __builtin_amdgcn_raw_buffer_load_b16(dr, (int)(wr_[i] * drow + wd_[i]), 0, 0);
-    }
-  };
-  auto store_w = [&](const Raw &S, uint8_t *sB, int i) __attribute__((always_inline)) {
-    if (WCH % T != 0 && i == BCH - 1 && tid + i * T >= WCH) return;
-    uint4 v[NV];
-    dequant_chunk<QT, XT>(S.b[i], (float)__builtin_bit_cast(_Float16, S.d[i]), v);
-#pragma unroll
-    for (int q = 0; q < NV; ++q) *reinterpret_cast<uint4 *>(sB + (wl[i] ^ (16u * q))) = v[q];
-  };
-
-  uint32_t abase[FM], bbase[FN];
-#pragma unroll
-  for (int i = 0; i < FM; ++i) {
-    const uint32_t r = wm * TM + i * 32 + (lane & 31);
-    abase[i] = r * (kBK * 2) + ((((uint32_t)lane >> 5) ^ swz(r)) << 4);
-  }
-#pragma unroll
-  for (int j = 0; j < FN; ++j) {
-    const uint32_t r = wn * TN + j * 32 + (lane & 31);
-    bbase[j] = r * (kBK * 2) + ((((uint32_t)lane >> 5) ^ swz(r)) << 4);
-  }
-
-  f32x16_t acc[FM][FN];
-  auto zero_acc = [&]() __attribute__((always_inline)) {
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-      for (int j = 0; j < FN; ++j)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-  };
-  zero_acc();
-
-  auto compute = [&](const uint8_t *sA, const uint8_t *sB, const Raw &nxt, uint8_t *sBn)
-                     __attribute__((always_inline)) {
-#pragma unroll
-    for (int ks = 0; ks < KSTEPS; ++ks) {
-      uint4 af[FM], bfr[FN];
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-        af[i] = *reinterpret_cast<const uint4 *>(sA + (abase[i] ^ (32u * ks)));
-#pragma unroll
-      for (int j = 0; j < FN; ++j)
-        bfr[j] = *reinterpret_cast<const uint4 *>(sB + (bbase[j] ^ (32u * ks)));
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j) acc[i][j] = mfma32<XT>(af[i], bfr[j], acc[i][j]);
-      constexpr int per = (BCH + KSTEPS - 1) / KSTEPS;
-#pragma unroll
-      for (int i = ks * per; i < ks * per + per && i < BCH; ++i) store_w(nxt, sBn, i);
-    }
-  };
-
-  // global-address-space views of the output, so stores are global stores
-  typedef __attribute__((address_space(1))) float gfloat;
-  typedef __attribute__((address_space(1))) __bf16 gbf16;
-  auto epilogue = [&](const MMCursor &c) __attribute__((always_inline)) {
-    gfloat *yf = (gfloat *)c.y;
-    gbf16 *yb = (gbf16 *)c.y;
-    const int64_t n = c.n;
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-      for (int j = 0; j < FN; ++j) {
-        const int cl = wn * TN + j * 32 + (lane & 31);
-        if (cl >= c.rows_n) continue;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int rl = wm * TM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-          if (rl >= c.rows_m) continue;
-          const int64_t off = (c.m0 + rl) * n + c.n0 + cl;
-          if constexpr (YT == EB_F32)
-            yf[off] = acc[i][j][r];
-          else
-            yb[off] = (__bf16)acc[i][j][r];
-        }
-      }
-  };
-
-  {
-    constexpr int Z = 3 * ABYTES / 16 / T;
-    static_assert(Z * T * 16 == 3 * ABYTES, "zero fill must cover the x buffers");
-#pragma unroll
-    for (int i = 0; i < Z; ++i) {
-      const int o = (tid + i * T) * 16;
-      uint8_t *dst = o < ABYTES ? sA0 + o : (o < 2 * ABYTES ? sA1 + (o - ABYTES) : sA2 + (o - 2 * ABYTES));
-      *reinterpret_cast<uint4 *>(dst) = make_uint4(0, 0, 0, 0);
-    }
-  }
-  __syncthreads();
-
-  // prologue: x of steps 0, 1 and weights of steps 0, 1, 2
-  load_x(sA0, C);
-  load_w(S0, C);
-  load_x(sA1, X);
-  load_w(S1, X);
-  load_w(S2, W);
-#pragma unroll
-  for (int i = 0; i < BCH; ++i) store_w(S0, sB0, i);
-  __syncthreads();
-  mm_advance<BM, BN>(ops, X, u_end);  // X: step 2
-  mm_advance<BM, BN>(ops, W, u_end);  // W: step 3
-
-  auto step = [&](const uint8_t *A, uint8_t *A2, const uint8_t *B, uint8_t *Bn, const Raw &deq,
-                  Raw &ld) __attribute__((always_inline)) {
-    load_x(A2, X);
-    load_w(ld, W);
-    compute(A, B, deq, Bn);
-    if (C.valid && C.kt == C.nk - 1) {
-      epilogue(C);
-      zero_acc();
-      wait_vm_barrier<0>();
-    } else {
-      wait_vm_barrier<2 * NW + NX>();
-    }
-    mm_advance<BM, BN>(ops, C, u_end);
-    mm_advance<BM, BN>(ops, X, u_end);
-    mm_advance<BM, BN>(ops, W, u_end);
-  };
-  // The step count is rounded up to whole groups of six; the extra steps run on
-  // zeros (their loads are empty) and write nothing.
-  for (int64_t j = 0; j < nsteps; j += 6) {
-    step(sA0, sA2, sB0, sB1, S1, S0);
-    step(sA1, sA0, sB1, sB0, S2, S1);
-    step(sA2, sA1, sB0, sB1, S0, S2);
-    step(sA0, sA2, sB1, sB0, S1, S0);
-    step(sA1, sA0, sB0, sB1, S2, S1);
-    step(sA2, sA1, sB1, sB0, S0, S2);
-  }
-}
-
 // Whether every byte span one workgroup addresses through a 32-bit buffer
 // offset fits (tile rows x row bytes of x, codes and scales).  The template
 // tile sizes are used unless bm/bn are given.
@@ -939,82 +505,6 @@ hipError_t launch_mfma(int32_t type, const void *wdata, int64_t n, int64_t k, co
   }
   if (xt == EB_F16) return launch_q<EB_Q8_0, EB_F16>(wdata, n, k, x, m, y, yt, plan, ws, s);
   return launch_q<EB_Q8_0, EB_BF16>(wdata, n, k, x, m, y, yt, plan, ws, s);
-}
-
-namespace {
-
-template <int QT, int XT, int YT>
-hipError_t launch_multi_q(int cfg, const MMOp *ops, int nops, const int64_t *wg, int groups,
-                          hipStream_t s) {
-  if (cfg == 0)
-    mfma_multi_kernel<QT, XT, YT, 64, 128, 2, 2><<<groups, 256, 0, s>>>(ops, nops, wg, groups);
-  else
-    mfma_multi_kernel<QT, XT, YT, 128, 128, 2, 2><<<groups, 256, 0, s>>>(ops, nops, wg, groups);
-  return hipGetLastError();
-}
-
-template <int QT, int XT>
-hipError_t launch_multi_y(int32_t yt, int cfg, const MMOp *ops, int nops, const int64_t *wg,
-                          int groups, hipStream_t s) {
-  if (yt == EB_F32) return launch_multi_q<QT, XT, EB_F32>(cfg, ops, nops, wg, groups, s);
-  return launch_multi_q<QT, XT, EB_BF16>(cfg, ops, nops, wg, groups, s);
-}
-
-constexpr int kMMTiles[2][2] = {{64, 128}, {128, 128}};
-
-}  // namespace
-
-int mm_cfg(int64_t max_m) { return max_m <= 64 ? 0 : 1; }
-
-int64_t mm_tiles(int cfg, int64_t m, int64_t n) {
-  const int bm = kMMTiles[cfg][0], bn = kMMTiles[cfg][1];
-  return ((m + bm - 1) / bm) * ((n + bn - 1) / bn);
-}
-
-int mm_partition(const std::vector<MMOp> &ops, int cfg, std::vector<int64_t> &wg) {
-  (void)cfg;
-  int64_t steps = 0, units = 0;
-  for (const MMOp &o : ops) {
-    const int64_t u = o.unit_end - units;
-    steps += u * o.nk;
-    units = o.unit_end;
-  }
-  // two workgroups per CU (LDS allows two of either tile), a multiple of 8
-  int64_t groups = (int64_t)device_cu_count() * 2;
-  groups = std::min(groups, units);
-  groups = std::max<int64_t>(8, (groups + 7) / 8 * 8);
-  wg.assign(groups + 1, units);
-  wg[0] = 0;
-  // walk the units in order; workgroup p ends at the first unit boundary at or
-  // past the step target (p + 1) * steps / groups
-  int64_t acc = 0, u = 0;
-  size_t oi = 0;
-  int64_t first = 0;
-  for (int64_t p = 0; p + 1 < groups; ++p) {
-    const int64_t target = (p + 1) * steps / groups;
-    while (u < units && acc < target) {
-      while (ops[oi].unit_end <= u) first = ops[oi++].unit_end;
-      const int64_t take = std::min(ops[oi].unit_end - u,
-                                    std::max<int64_t>(1, (target - acc + ops[oi].nk - 1) / ops[oi].nk));
-      acc += take * ops[oi].nk;
-      u += take;
-    }
-    wg[p + 1] = u;
-  }
-  (void)first;
-  return (int)groups;
-}
-
-hipError_t launch_mfma_multi(int32_t type, int32_t xt, int32_t yt, int cfg, const MMOp *dev_ops,
-                             int nops, const int64_t *dev_wg, int groups, hipStream_t s) {
-  if (nops < 1 || groups < 8 || groups % kXcds != 0) return hipErrorInvalidValue;
-  if (type == EB_Q4_0) {
-    if (xt == EB_F16)
-      return launch_multi_y<EB_Q4_0, EB_F16>(yt, cfg, dev_ops, nops, dev_wg, groups, s);
-    return launch_multi_y<EB_Q4_0, EB_BF16>(yt, cfg, dev_ops, nops, dev_wg, groups, s);
-  }
-  if (xt == EB_F16) return launch_multi_y<EB_Q8_0, EB_F16>(yt, cfg, dev_ops, nops, dev_wg, groups, s);
-  return launch_multi_y<EB_Q8_0, EB_BF16>(yt, cfg, dev_ops, nops, dev_wg, groups, s);
 }
 
 }  // namespace eb

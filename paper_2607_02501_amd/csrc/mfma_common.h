@@ -1,0 +1,145 @@
+// mfma_common.h -- device helpers shared by the single-op and fused MFMA
+// kernels: 16-bit packing, the 32x32x16 MFMA, dequantization of code chunks,
+// raw buffer descriptors, the x-tile swizzle and the partial-drain barrier.
+#ifndef EB_MFMA_COMMON_H
+#define EB_MFMA_COMMON_H
+
+#include <hip/hip_runtime.h>
+
+#include "eb_internal.h"
+
+namespace eb {
+namespace {
+
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+constexpr int kBK = 64;        // K elements per tile (2 blocks)
+constexpr int kXcds = 8;
+
+template <int XT>
+__device__ inline uint32_t pack2(float a, float b) {
+  if (XT == EB_BF16) {
+    typedef __bf16 bf2 __attribute__((ext_vector_type(2)));
+    bf2 v = {(__bf16)a, (__bf16)b};  // v_cvt_pk_bf16_f32, round to nearest even
+    return __builtin_bit_cast(uint32_t, v);
+  }
+  return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)a) |
+         ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)b) << 16);
+}
+
+template <int XT>
+__device__ inline f32x16_t mfma32(const uint4 a, const uint4 b, f32x16_t c) {
+  if (XT == EB_BF16)
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                   __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8_t, a),
+                                                __builtin_bit_cast(f16x8_t, b), c, 0, 0, 0);
+}
+
+template <int QT>
+struct WTile {
+  // 16-byte weight chunks per row per K-tile: Q8_0 four half-blocks, Q4_0 two blocks
+  static constexpr int kChunksPerRow = (QT == EB_Q8_0) ? 4 : 2;
+  static constexpr int kElemsPerChunk = (QT == EB_Q8_0) ? 16 : 32;
+};
+
+// Dequantize one 16-byte chunk of codes into 16-byte vectors of 16-bit
+// weights, in k order: Q8_0 16 codes -> 2 vectors, Q4_0 one block -> 4.
+// Each code c in 0..255 (Q8_0: q + 128) or 0..15 (Q4_0 nibble) is placed
+// under the binary16 exponent of 1024 by one byte permute per two codes,
+// giving the binary16 value 1024 + c exactly; then
+//   fma(1024 + c, d, -(1024 + z) d) = (c - z) d,   z = 128 (Q8_0) or 8 (Q4_0),
+// is exact (1152 d and 1032 d need at most 19 significant bits), and the one
+// rounding to the 16-bit activation type is round-to-nearest-even.
+template <int QT>
+struct Deq {
+  static constexpr int kVecs = (QT == EB_Q8_0) ? 2 : 4;
+};
+
+// two codes in bytes b0, b1 of v -> 16-bit halves 0x64bb of the result
+__device__ inline uint32_t under_1024(uint32_t v, uint32_t sel) {
+  return __builtin_amdgcn_perm(0x64646464u, v, sel);
+}
+
+template <int XT>
+__device__ inline uint32_t deq_pair(uint32_t h2, float d, float c) {
+  const _Float16 a = __builtin_bit_cast(_Float16, (uint16_t)(h2 & 0xffffu));
+  const _Float16 b = __builtin_bit_cast(_Float16, (uint16_t)(h2 >> 16));
+  return pack2<XT>(__builtin_fmaf((float)a, d, c), __builtin_fmaf((float)b, d, c));
+}
+
+template <int QT, int XT>
+__device__ inline void dequant_chunk(const uint4 q, float d, uint4 (&v)[Deq<QT>::kVecs]) {
+  const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+  // byte selectors: {S1.b0, 0x64, S1.b1, 0x64} and {S1.b2, 0x64, S1.b3, 0x64}
+  constexpr uint32_t kSelLo = 0x04010400u, kSelHi = 0x04030402u;
+  if constexpr (QT == EB_Q8_0) {
+    const float c = -1152.0f * d;
+    uint32_t o[8];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t u = w[j] ^ 0x80808080u;
+      o[2 * j] = deq_pair<XT>(under_1024(u, kSelLo), d, c);
+      o[2 * j + 1] = deq_pair<XT>(under_1024(u, kSelHi), d, c);
+    }
+    v[0] = make_uint4(o[0], o[1], o[2], o[3]);
+    v[1] = make_uint4(o[4], o[5], o[6], o[7]);
+  } else {
+    const float c = -1032.0f * d;
+    uint32_t lo[8], hi[8];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t l = w[j] & 0x0f0f0f0fu, h = (w[j] >> 4) & 0x0f0f0f0fu;
+      lo[2 * j] = deq_pair<XT>(under_1024(l, kSelLo), d, c);
+      lo[2 * j + 1] = deq_pair<XT>(under_1024(l, kSelHi), d, c);
+      hi[2 * j] = deq_pair<XT>(under_1024(h, kSelLo), d, c);
+      hi[2 * j + 1] = deq_pair<XT>(under_1024(h, kSelHi), d, c);
+    }
+    v[0] = make_uint4(lo[0], lo[1], lo[2], lo[3]);
+    v[1] = make_uint4(lo[4], lo[5], lo[6], lo[7]);
+    v[2] = make_uint4(hi[0], hi[1], hi[2], hi[3]);
+    v[3] = make_uint4(hi[4], hi[5], hi[6], hi[7]);
+  }
+}
+
+// Raw buffer descriptor over [base, base + bytes): every lane whose offset is
+// at or past `bytes` reads zeros, which is how the kernel handles rows past m
+// or n without branches.  The descriptor is rebuilt per K-tile (scalar work),
+// so the hardware range check always covers the whole access.
+__device__ inline __amdgpu_buffer_rsrc_t rsrc(const void *base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes,
+                                           0x00020000);
+}
+
+__device__ inline uint4 bload(__amdgpu_buffer_rsrc_t r, uint32_t voff) {
+  const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, 0, 0);
+  return make_uint4(v[0], v[1], v[2], v[3]);
+}
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+// Position of 16-byte chunk c of row r in the unpadded x tile (128-byte rows):
+// c ^ swz(r).  Any 16 consecutive rows read at one chunk index hit 16 distinct
+// 16-byte bank groups, and any 8 consecutive rows 8 distinct ones.
+__device__ inline uint32_t swz(uint32_t r) { return (r ^ (r >> 3)) & 7; }
+
+// Wait until at most N vector-memory operations of this wave are outstanding
+// and its LDS writes are done, then barrier.  Unlike __syncthreads this does
+// not drain every load, so loads issued for later K-tiles stay in flight.  The
+// "memory" clobber keeps IR passes, and the scheduling barriers the machine
+// scheduler, from moving memory accesses across it.
+template <int N>
+__device__ inline void wait_vm_barrier() {
+  // sched_barrier(0): the machine scheduler moves nothing across this point
+  __builtin_amdgcn_sched_barrier(0);
+  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+}  // namespace
+}  // namespace eb
+
+#endif  // EB_MFMA_COMMON_H

@@ -1,0 +1,467 @@
+// mfma_multi.hip -- fused MFMA launch over many independent small-m ops of
+// a stack (paper section 3.2: operator fusion and graph replay for batch-1
+// execution; the action-chunk denoising steps of section 2.1 / Table 1 run
+// hundreds of such layers per pass).  Built with the MFMA accumulators in
+// VGPRs: its persistent loop otherwise moves them between register files on
+// every trip.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdlib>
+#include <vector>
+
+#include "eb_internal.h"
+#include "mfma_common.h"
+
+namespace eb {
+namespace {
+
+// ---------------------------------------------------------------------------
+// Fused launch over many independent ops (small m).  The tiles (units) of
+// the op table are split into one contiguous range per workgroup, balanced by
+// K-tile steps; consecutive ranges go to workgroups on the same XCD (shared
+// L2).  A workgroup runs its units as one stream of K-tile steps, with the
+// pipeline of mfma_kernel one step deeper (x copies three steps ahead, weight
+// loads four), running across unit and op boundaries; a unit's epilogue is
+// written when its last step is done.  Cursors walk the stream: the step being
+// computed, the x copy ahead and the weight loads ahead.  Loads past the end
+// of the range are issued with an empty range (they read zeros and touch no
+// memory), so every step issues the same instructions.  The deeper pipeline
+// suits a launch that keeps every CU streaming weights, where memory latency
+// is longer than in a single-op launch.
+// ---------------------------------------------------------------------------
+// Position in a workgroup's stream of units: the unit, its op and K-tile.
+struct MMPos {
+  int op;
+  int64_t u;
+  int kt, nk;
+  int64_t op_end;
+  bool valid;
+};
+
+// Moves to the first step of unit p.u (p.op must not be past its op).
+__host__ __device__ inline void mm_seek(const MMOp *__restrict__ ops, MMPos &p, int64_t u_end) {
+  p.kt = 0;
+  if (p.u >= u_end) {
+    p.valid = false;
+    return;
+  }
+  while (p.u >= ops[p.op].unit_end) ++p.op;
+  p.nk = ops[p.op].nk;
+  p.op_end = ops[p.op].unit_end;
+}
+
+// Advances one step; returns true when a new unit starts (p.valid tells
+// whether there is one).
+__host__ __device__ inline bool mm_step(const MMOp *__restrict__ ops, MMPos &p, int64_t u_end) {
+  if (!p.valid) return false;
+  if (++p.kt < p.nk) return false;
+  ++p.u;
+  mm_seek(ops, p, u_end);
+  return true;
+}
+
+// Tile (m0, n0) and valid extent of unit p.u of op p.op.
+template <int BM, int BN>
+__host__ __device__ inline void mm_tile(const MMOp *__restrict__ ops, const MMPos &p, int64_t &m0,
+                               int64_t &n0, int &rows_m, int &rows_n) {
+  const MMOp &o = ops[p.op];
+  const int64_t first = p.op ? ops[p.op - 1].unit_end : 0;
+  const uint32_t uin = (uint32_t)(p.u - first), tiles_n = (uint32_t)o.tiles_n;
+  const uint32_t tm = uin / tiles_n, tn = uin - tm * tiles_n;
+  m0 = (int64_t)tm * BM;
+  n0 = (int64_t)tn * BN;
+  rows_m = (int)std::min((int64_t)BM, (int64_t)o.m - m0);
+  rows_n = (int)std::min((int64_t)BN, (int64_t)o.n - n0);
+}
+
+template <int QT, int XT, int YT, int BM, int BN, int WM, int WN>
+__global__ void __launch_bounds__(WM *WN * 64)
+    mfma_multi_kernel(const MMOp *__restrict__ ops, int nops, const int64_t *__restrict__ wg,
+                      int groups) {
+  // The body is device code only: the host pass (which only needs the launch
+  // stub) does not see it.
+#if defined(__HIP_DEVICE_COMPILE__)
+  constexpr int T = WM * WN * 64;
+  constexpr int WAVES = WM * WN;
+  constexpr int TM = BM / WM, TN = BN / WN;
+  constexpr int FM = TM / 32, FN = TN / 32;
+  constexpr int ADMA = BM / (8 * WAVES);
+  constexpr int WCPR = WTile<QT>::kChunksPerRow;
+  constexpr int WCH = BN * WCPR;
+  constexpr int BCH = (WCH + T - 1) / T;
+  constexpr int KSTEPS = kBK / 16;
+  constexpr int QSB = (QT == EB_Q8_0) ? 32 : 16;
+  constexpr int NV = Deq<QT>::kVecs;
+  constexpr int ABYTES = BM * kBK * 2, BBYTES = BN * kBK * 2;
+  constexpr int YSZ = (YT == EB_F32) ? 4 : 2;
+  constexpr int NX = ADMA, NW = 2 * BCH;
+  static_assert(ADMA >= 1 && ADMA * 8 * WAVES == BM, "x tile must split into 8-row copies");
+  static_assert(TM % 32 == 0 && TN % 32 == 0, "wave sub-tile must be whole fragments");
+  // x copies run three steps ahead (four x buffers), weight loads four (four
+  // register sets): a step waits at its barrier for the x copy issued two
+  // steps before it.
+  constexpr int NWAIT = 2 * NX + 3 * NW;
+  static_assert(NWAIT <= 63, "vmcnt range");
+
+  __shared__ __attribute__((aligned(1024))) uint8_t sA0[ABYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t sA1[ABYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t sA2[ABYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t sA3[ABYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t sB0[BBYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t sB1[BBYTES];
+
+  // workgroups are dispatched to the XCDs round-robin (g % 8 is the XCD):
+  // range p goes to XCD p / (groups / 8)
+  const int g = blockIdx.x;
+  const int p = (g % kXcds) * (groups / kXcds) + g / kXcds;
+  const int64_t u_begin = wg[p], u_end = wg[p + 1];
+  if (u_begin >= u_end) return;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / WN, wn = wave % WN;
+
+  // first op of the range: binary search over the ascending unit_end (the
+  // last op's unit_end is the total, which exceeds u_begin)
+  int lo = 0, hi = nops - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi) / 2;
+    if (ops[mid].unit_end <= u_begin) lo = mid + 1; else hi = mid;
+  }
+  // steps of the range, rounded up to whole groups of four (the extra steps
+  // run on zeros, their loads are empty, and write nothing)
+  int64_t nsteps = 0;
+  for (int o = lo;; ++o) {
+    const int64_t first = o ? ops[o - 1].unit_end : 0;
+    nsteps += (min(ops[o].unit_end, u_end) - max(first, u_begin)) * ops[o].nk;
+    if (ops[o].unit_end >= u_end) break;
+  }
+
+  // per-thread tile-local parts of the x copies and weight loads
+  uint32_t xr_[ADMA], xc_[ADMA];
+#pragma unroll
+  for (int i = 0; i < ADMA; ++i) {
+    const uint32_t r = 8 * (i * WAVES + wave) + (lane >> 3);
+    xr_[i] = r;
+    xc_[i] = ((lane & 7) ^ swz(r)) << 4;
+  }
+  uint32_t wr_[BCH], wq_[BCH], wd_[BCH], wl[BCH];
+#pragma unroll
+  for (int i = 0; i < BCH; ++i) {
+    const int idx = min(tid + i * T, WCH), r = idx / WCPR, c = idx % WCPR;
+    const int blk = (QT == EB_Q8_0) ? (c >> 1) : c;
+    wr_[i] = r;
+    wq_[i] = blk * QSB + ((QT == EB_Q8_0) ? (c & 1) * 16 : 0);
+    wd_[i] = blk * 2;
+    wl[i] = (uint32_t)(r * (kBK * 2) + (((NV * c) ^ swz(r)) << 4));
+  }
+
+  // --- x copies: base and byte count advance by one K-tile per step ---------
+  struct XState {
+    MMPos p;
+    const uint8_t *base;
+    uint32_t rec;
+    uint32_t v[ADMA];
+  };
+  auto x_enter = [&](XState &s) __attribute__((always_inline)) {
+    if (!s.p.valid) {
+      s.rec = 0;
+      return;
+    }
+    int64_t m0, n0;
+    int rm, rn;
+    mm_tile<BM, BN>(ops, s.p, m0, n0, rm, rn);
+    const MMOp &o = ops[s.p.op];
+    const uint32_t row = (uint32_t)o.k * 2;
+    s.base = reinterpret_cast<const uint8_t *>(o.x) + m0 * row;
+    s.rec = (uint32_t)rm * row;
+#pragma unroll
+    for (int i = 0; i < ADMA; ++i) s.v[i] = xr_[i] * row + xc_[i];
+  };
+  auto x_issue = [&](uint8_t *sA, XState &s) __attribute__((always_inline)) {
+    const auto r = rsrc(s.base, s.rec);
+#pragma unroll
+    for (int i = 0; i < ADMA; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void *)(sA + (i * WAVES + wave) * 1024), 16,
+                                               (int)s.v[i], 0, 0, 0);
+    if (mm_step(ops, s.p, u_end)) {
+      x_enter(s);
+    } else if (s.p.valid) {
+      s.base += kBK * 2;
+      s.rec -= kBK * 2;
+    }
+  };
+
+  // --- weight loads --------------------------------------------------------
+  struct Raw {
+    uint4 b[BCH];
+    uint16_t d[BCH];
+  };
+  struct WState {
+    MMPos p;
+    const uint8_t *qb, *db;
+    uint32_t qrec, drec;
+    uint32_t qv[BCH], dv[BCH];
+  };
+  auto w_enter = [&](WState &s) __attribute__((always_inline)) {
+    if (!s.p.valid) {
+      s.qrec = s.drec = 0;
+      return;
+    }
+    int64_t m0, n0;
+    int rm, rn;
+    mm_tile<BM, BN>(ops, s.p, m0, n0, rm, rn);
+    const MMOp &o = ops[s.p.op];
+    const uint32_t qrow = (uint32_t)(o.k / kQK) * QSB, drow = (uint32_t)o.ds * 2;
+    s.qb = o.w + n0 * qrow;
+    s.db = o.w + o.d_off + n0 * drow;
+    s.qrec = (uint32_t)rn * qrow;
+    s.drec = (uint32_t)rn * drow;
+#pragma unroll
+    for (int i = 0; i < BCH; ++i) {
+      s.qv[i] = wr_[i] * qrow + wq_[i];
+      s.dv[i] = wr_[i] * drow + wd_[i];
+    }
+  };
+  auto w_issue = [&](Raw &S, WState &s) __attribute__((always_inline)) {
+    const auto qr = rsrc(s.qb, s.qrec);
+    const auto dr = rsrc(s.db, s.drec);
+#pragma unroll
+    for (int i = 0; i < BCH; ++i) {
+      S.b[i] = bload(qr, s.qv[i]);
+      S.d[i] = __builtin_amdgcn_raw_buffer_load_b16(dr, (int)s.dv[i], 0, 0);
+    }
+    if (mm_step(ops, s.p, u_end)) {
+      w_enter(s);
+    } else if (s.p.valid) {
+      s.qb += 2 * QSB;
+      s.qrec -= 2 * QSB;
+      s.db += 4;
+      s.drec -= 4;
+    }
+  };
+  auto store_w = [&](const Raw &S, uint8_t *sB, int i) __attribute__((always_inline)) {
+    if (WCH % T != 0 && i == BCH - 1 && tid + i * T >= WCH) return;
+    uint4 v[NV];
+    dequant_chunk<QT, XT>(S.b[i], (float)__builtin_bit_cast(_Float16, S.d[i]), v);
+#pragma unroll
+    for (int q = 0; q < NV; ++q) *reinterpret_cast<uint4 *>(sB + (wl[i] ^ (16u * q))) = v[q];
+  };
+
+  // --- MFMAs -----------------------------------------------------------------
+  uint32_t abase[FM], bbase[FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+    const uint32_t r = wm * TM + i * 32 + (lane & 31);
+    abase[i] = r * (kBK * 2) + ((((uint32_t)lane >> 5) ^ swz(r)) << 4);
+  }
+#pragma unroll
+  for (int j = 0; j < FN; ++j) {
+    const uint32_t r = wn * TN + j * 32 + (lane & 31);
+    bbase[j] = r * (kBK * 2) + ((((uint32_t)lane >> 5) ^ swz(r)) << 4);
+  }
+  f32x16_t acc[FM][FN];
+  auto zero_acc = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+  };
+  zero_acc();
+  auto compute = [&](const uint8_t *sA, const uint8_t *sB, const Raw &nxt, uint8_t *sBn)
+                     __attribute__((always_inline)) {
+#pragma unroll
+    for (int ks = 0; ks < KSTEPS; ++ks) {
+      uint4 af[FM], bfr[FN];
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+        af[i] = *reinterpret_cast<const uint4 *>(sA + (abase[i] ^ (32u * ks)));
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        bfr[j] = *reinterpret_cast<const uint4 *>(sB + (bbase[j] ^ (32u * ks)));
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[i][j] = mfma32<XT>(af[i], bfr[j], acc[i][j]);
+      constexpr int per = (BCH + KSTEPS - 1) / KSTEPS;
+#pragma unroll
+      for (int i = ks * per; i < ks * per + per && i < BCH; ++i) store_w(nxt, sBn, i);
+    }
+  };
+
+  // --- epilogue: buffer stores whose range check drops rows past m; lanes of
+  // columns past n use an offset past the range ---------------------------
+  auto epilogue = [&](const MMPos &c) __attribute__((always_inline)) {
+    int64_t m0, n0;
+    int rm, rn;
+    mm_tile<BM, BN>(ops, c, m0, n0, rm, rn);
+    const MMOp &o = ops[c.op];
+    const uint32_t n = (uint32_t)o.n;
+    const auto yr = rsrc(o.y, (uint32_t)o.m * n * YSZ);
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int cl = wn * TN + j * 32 + (lane & 31);
+#pragma unroll
+      for (int i = 0; i < FM; ++i) {
+        const uint32_t row0 = (uint32_t)m0 + wm * TM + i * 32 + 4 * (lane >> 5);
+        const uint32_t base = cl < rn ? (row0 * n + (uint32_t)n0 + cl) * YSZ : 0x80000000u;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const uint32_t off = base + (uint32_t)(8 * (r >> 2) + (r & 3)) * n * YSZ;
+          // copy the element out first: a bit cast of a vector element lvalue
+          // reads the wrong element
+          const float v = acc[i][j][r];
+          if constexpr (YT == EB_F32)
+            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), yr, (int)off, 0, 0);
+          else
+            __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(uint16_t, (__bf16)v), yr,
+                                                  (int)off, 0, 0);
+        }
+      }
+    }
+  };
+
+  {
+    constexpr int Z = ABYTES / 16 / T;
+    static_assert(Z * T * 16 == ABYTES, "zero fill must cover the x buffers");
+#pragma unroll
+    for (int i = 0; i < Z; ++i) {
+      const int o = (tid + i * T) * 16;
+      *reinterpret_cast<uint4 *>(sA0 + o) = make_uint4(0, 0, 0, 0);
+      *reinterpret_cast<uint4 *>(sA1 + o) = make_uint4(0, 0, 0, 0);
+      *reinterpret_cast<uint4 *>(sA2 + o) = make_uint4(0, 0, 0, 0);
+      *reinterpret_cast<uint4 *>(sA3 + o) = make_uint4(0, 0, 0, 0);
+    }
+  }
+  __syncthreads();
+
+  MMPos C;
+  C.op = lo;
+  C.u = u_begin;
+  C.valid = true;
+  mm_seek(ops, C, u_end);
+  XState X;
+  X.p = C;
+  x_enter(X);
+  WState Wc;
+  Wc.p = C;
+  w_enter(Wc);
+
+  // prologue: x of steps 0..2 and weights of steps 0..3
+  Raw S0, S1, S2, S3;
+  x_issue(sA0, X);
+  x_issue(sA1, X);
+  x_issue(sA2, X);
+  w_issue(S0, Wc);
+  w_issue(S1, Wc);
+  w_issue(S2, Wc);
+  w_issue(S3, Wc);
+#pragma unroll
+  for (int i = 0; i < BCH; ++i) store_w(S0, sB0, i);
+  __syncthreads();
+
+  auto step = [&](const uint8_t *A, uint8_t *A3, const uint8_t *B, uint8_t *Bn, const Raw &deq,
+                  Raw &ld) __attribute__((always_inline)) {
+    x_issue(A3, X);
+    w_issue(ld, Wc);
+    compute(A, B, deq, Bn);
+    if (C.valid && C.kt == C.nk - 1) {
+      epilogue(C);
+      zero_acc();
+      wait_vm_barrier<0>();
+    } else {
+      wait_vm_barrier<NWAIT>();
+    }
+    mm_step(ops, C, u_end);
+  };
+  for (int64_t j = 0; j < nsteps; j += 4) {
+    step(sA0, sA3, sB0, sB1, S1, S0);
+    step(sA1, sA0, sB1, sB0, S2, S1);
+    step(sA2, sA1, sB0, sB1, S3, S2);
+    step(sA3, sA2, sB1, sB0, S0, S3);
+  }
+#endif  // __HIP_DEVICE_COMPILE__
+}
+
+template <int QT, int XT, int YT>
+hipError_t launch_multi_q(int cfg, const MMOp *ops, int nops, const int64_t *wg, int groups,
+                          hipStream_t s) {
+  if (cfg == 0)
+    mfma_multi_kernel<QT, XT, YT, 64, 128, 2, 2><<<groups, 256, 0, s>>>(ops, nops, wg, groups);
+  else if (cfg == 1)
+    mfma_multi_kernel<QT, XT, YT, 128, 128, 2, 2><<<groups, 256, 0, s>>>(ops, nops, wg, groups);
+  else
+    mfma_multi_kernel<QT, XT, YT, 64, 256, 2, 4><<<groups, 512, 0, s>>>(ops, nops, wg, groups);
+  return hipGetLastError();
+}
+
+template <int QT, int XT>
+hipError_t launch_multi_y(int32_t yt, int cfg, const MMOp *ops, int nops, const int64_t *wg,
+                          int groups, hipStream_t s) {
+  if (yt == EB_F32) return launch_multi_q<QT, XT, EB_F32>(cfg, ops, nops, wg, groups, s);
+  return launch_multi_q<QT, XT, EB_BF16>(cfg, ops, nops, wg, groups, s);
+}
+
+// {BM, BN, workgroups per CU}
+constexpr int kMMTiles[3][3] = {{64, 128, 2}, {128, 128, 1}, {64, 256, 1}};
+
+}  // namespace
+
+int mm_cfg(int64_t max_m) {
+  static const int forced = [] {
+    const char *e = getenv("EB_MM_CFG");  // tuning: force the fused tile
+    return e ? atoi(e) : -1;
+  }();
+  if (forced >= 0 && forced <= 2 && (max_m <= 64 || forced == 1)) return forced;
+  return max_m <= 64 ? 0 : 1;
+}
+
+int64_t mm_tiles(int cfg, int64_t m, int64_t n) {
+  const int bm = kMMTiles[cfg][0], bn = kMMTiles[cfg][1];
+  return ((m + bm - 1) / bm) * ((n + bn - 1) / bn);
+}
+
+int mm_partition(const std::vector<MMOp> &ops, int cfg, std::vector<int64_t> &wg) {
+  int64_t steps = 0, units = 0;
+  for (const MMOp &o : ops) {
+    steps += (o.unit_end - units) * o.nk;
+    units = o.unit_end;
+  }
+  // as many workgroups as fit on the CUs at once, a multiple of 8
+  int64_t groups = std::min<int64_t>((int64_t)device_cu_count() * kMMTiles[cfg][2], units);
+  groups = std::max<int64_t>(kXcds, (groups + kXcds - 1) / kXcds * kXcds);
+  // workgroup p ends at the first unit boundary at or past (p + 1) * steps / groups
+  wg.assign(groups + 1, units);
+  wg[0] = 0;
+  int64_t acc = 0, u = 0;
+  size_t oi = 0;
+  for (int64_t p = 0; p + 1 < groups; ++p) {
+    const int64_t target = (p + 1) * steps / groups;
+    while (u < units && acc < target) {
+      while (ops[oi].unit_end <= u) ++oi;
+      const int64_t take = std::min(ops[oi].unit_end - u,
+                                    std::max<int64_t>(1, (target - acc + ops[oi].nk - 1) / ops[oi].nk));
+      acc += take * ops[oi].nk;
+      u += take;
+    }
+    wg[p + 1] = u;
+  }
+  return (int)groups;
+}
+
+hipError_t launch_mfma_multi(int32_t type, int32_t xt, int32_t yt, int cfg, const MMOp *dev_ops,
+                             int nops, const int64_t *dev_wg, int groups, hipStream_t s) {
+  if (nops < 1 || groups < kXcds || groups % kXcds != 0) return hipErrorInvalidValue;
+  if (type == EB_Q4_0) {
+    if (xt == EB_F16)
+      return launch_multi_y<EB_Q4_0, EB_F16>(yt, cfg, dev_ops, nops, dev_wg, groups, s);
+    return launch_multi_y<EB_Q4_0, EB_BF16>(yt, cfg, dev_ops, nops, dev_wg, groups, s);
+  }
+  if (xt == EB_F16) return launch_multi_y<EB_Q8_0, EB_F16>(yt, cfg, dev_ops, nops, dev_wg, groups, s);
+  return launch_multi_y<EB_Q8_0, EB_BF16>(yt, cfg, dev_ops, nops, dev_wg, groups, s);
+}
+}  // namespace eb

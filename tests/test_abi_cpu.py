@@ -35,6 +35,11 @@ def test_header_declares_the_boundary():
         assert required in names
 
 
+def test_library_resolves_every_symbol_at_load(eb):
+    # RTLD_NOW binds every reference (kernel launch stubs included) at load time
+    ctypes.CDLL(eb.LIB_PATH, mode=os.RTLD_NOW)
+
+
 def test_every_declared_symbol_is_exported(eb):
     lib = ctypes.CDLL(eb.LIB_PATH)
     missing = [n for n in declared_functions() if not hasattr(lib, n)]
