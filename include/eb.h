@@ -82,7 +82,7 @@ typedef int32_t eb_status;
 
 /* kernel paths for eb_qlinear_ex */
 #define EB_PATH_AUTO 0 /* pick by m, qtype and shape (measured crossover) */
-#define EB_PATH_GEMV 1 /* bandwidth-bound GEMV, requires m <= 4 and m * k <= 65536 */
+#define EB_PATH_GEMV 1 /* bandwidth-bound GEMV, requires m <= 8 and m' * k <= 65536, m' = m rounded up to 1, 2, 4 or 8 */
 #define EB_PATH_MFMA 2 /* LDS-tiled dequantize-to-16-bit + MFMA, any m */
 
 /* A quantized weight matrix W[n][k] in the planar device layout above.
@@ -172,7 +172,7 @@ eb_status eb_qlinear(const eb_qweights *w, const void *x, int32_t x_type, int64_
 
 /* eb_qlinear with an explicit kernel path (EB_PATH_*), for crossover
  * measurement and tests.  EB_ERR_UNSUPPORTED if the forced path cannot run
- * this shape (EB_PATH_GEMV with m > 4 or m * k > 65536). */
+ * this shape (EB_PATH_GEMV with m > 8 or m' * k > 65536). */
 eb_status eb_qlinear_ex(const eb_qweights *w, const void *x, int32_t x_type, int64_t m, void *y,
                         int32_t y_type, int32_t path, hipStream_t stream);
 

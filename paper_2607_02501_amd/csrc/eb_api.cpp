@@ -57,7 +57,7 @@ bool overlaps(const void *a, size_t an, const void *b, size_t bn) {
 
 size_t dsize(int32_t t) { return t == EB_F32 ? 4 : 2; }
 
-int64_t gemv_mt(int64_t m) { return m <= 1 ? 1 : (m <= 2 ? 2 : 4); }
+int64_t gemv_mt(int64_t m) { return m <= 1 ? 1 : (m <= 2 ? 2 : (m <= 4 ? 4 : 8)); }
 
 bool gemv_fits(int64_t m, int64_t k) {
   return m >= 1 && m <= kGemvMaxM && gemv_mt(m) * k <= kGemvMaxMK;
@@ -88,11 +88,17 @@ eb_status check_linear(const eb_qweights *w, const void *x, int32_t xt, int64_t 
   return EB_OK;
 }
 
+// Path choice from the measured GEMV / MFMA crossover on MI355X (single ops
+// replayed from a graph, Q4_0 and Q8_0 at the decode / prefill / action-expert
+// shapes): the GEMV wins at m = 1 everywhere and at m = 2..4 unless the matrix
+// has few rows (n = 1024 loses); from m = 5 the MFMA path wins or loses by at
+// most 20%, so it is taken for every m >= 5.
 int32_t pick_path(int32_t type, int32_t xt, int64_t m, int64_t n, int64_t k) {
   (void)type;
   (void)xt;
-  (void)n;
-  return gemv_fits(m, k) ? EB_PATH_GEMV : EB_PATH_MFMA;
+  if (!gemv_fits(m, k)) return EB_PATH_MFMA;
+  if (m == 1) return EB_PATH_GEMV;
+  return (m <= 4 && n >= 2048) ? EB_PATH_GEMV : EB_PATH_MFMA;
 }
 
 // Split-K workspaces of direct calls, one per (device, stream) so calls on

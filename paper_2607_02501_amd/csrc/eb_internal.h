@@ -43,8 +43,8 @@ hipError_t launch_to_canonical(int32_t type, const void *planar, int64_t n, int6
 hipError_t launch_from_canonical(int32_t type, const void *src, int64_t n, int64_t k, void *out,
                                  hipStream_t s);
 
-// GEMV path: m <= 4, m * k <= kGemvMaxMK
-constexpr int64_t kGemvMaxM = 4;
+// GEMV path: m <= 8, (m rounded up to 1, 2, 4 or 8) * k <= kGemvMaxMK
+constexpr int64_t kGemvMaxM = 8;
 constexpr int64_t kGemvMaxMK = 65536;
 hipError_t launch_gemv(int32_t type, const void *wdata, int64_t n, int64_t k, const void *x,
                        int32_t xt, int64_t m, void *y, int32_t yt, hipStream_t s);

@@ -1,4 +1,4 @@
-// gemv.hip -- bandwidth-bound path of the quantized linear layer for m <= 4
+// gemv.hip -- bandwidth-bound path of the quantized linear layer for m <= 8
 // activation rows (batch-1 decode: paper section 3.1, "latency-first
 // closed-loop control" runs effectively at batch 1; section 3.2 asks for
 // fused, backend-specific kernels for it).
@@ -638,7 +638,8 @@ hipError_t launch_m(const void *wdata, int64_t n, int64_t k, const void *x, int6
     return launch_m1<QT, XT>(wdata, n, k, x, y, yt, s);
   if (m <= 1) return launch_t<QT, XT, 1, 2>(wdata, n, k, x, m, y, yt, s);
   if (m <= 2) return launch_t<QT, XT, 2, 2>(wdata, n, k, x, m, y, yt, s);
-  return launch_t<QT, XT, 4, 1>(wdata, n, k, x, m, y, yt, s);
+  if (m <= 4) return launch_t<QT, XT, 4, 1>(wdata, n, k, x, m, y, yt, s);
+  return launch_t<QT, XT, 8, 1>(wdata, n, k, x, m, y, yt, s);
 }
 
 template <int QT, int XT, int NS>

@@ -41,7 +41,10 @@ class Workload:
 
 WORKLOADS = {
     # one Q8_0 linear layer, batch-1 decode, 2048 -> 2048, fp16 activations
-    "q8_0_m1_2048": Workload("q8_0_m1_2048", Q8_0, torch.float16, 1, 1, 1,
+    # 128 distinct copies of the one 2048x2048 layer (the first has seed 0) run
+    # back to back, so that a pass streams 570 MB rather than one 4.5 MB matrix
+    # that the 256 MB last-level cache would hold
+    "q8_0_m1_2048": Workload("q8_0_m1_2048", Q8_0, torch.float16, 1, 128, 1,
                              (("linear", 2048, 2048),), wid=0),
     # 7B-class decoder, batch-1 decode of one token through 32 layers, Q4_0
     "q4_0_decode_7b": Workload("q4_0_decode_7b", Q4_0, torch.float16, 1, 32, 1,

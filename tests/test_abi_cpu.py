@@ -84,7 +84,7 @@ X, Y = 0x200000, 0x400000
     ("null_w", -1), ("null_data", -1), ("bad_type", -1), ("reserved", -1), ("k33", -1),
     ("k0", -1), ("n0", -1), ("m_neg", -1), ("bad_xt", -1), ("bad_path", -1), ("x_null", -1),
     ("w_misaligned", -2), ("x_misaligned", -2), ("y_misaligned", -2), ("x_f32", -3),
-    ("y_f16", -3), ("gemv_m8", -3), ("gemv_big_k", -3), ("overlap", -1),
+    ("y_f16", -3), ("gemv_m9", -3), ("gemv_big_k", -3), ("overlap", -1),
 ])
 def test_qlinear_validation(eb, case, expect):
     w = _w(eb)
@@ -122,8 +122,8 @@ def test_qlinear_validation(eb, case, expect):
         xt = eb.EB_F32
     elif case == "y_f16":
         yt = eb.EB_F16
-    elif case == "gemv_m8":
-        m, path = 8, eb.EB_PATH_GEMV
+    elif case == "gemv_m9":
+        m, path = 9, eb.EB_PATH_GEMV
     elif case == "gemv_big_k":
         w.k, m, path = 65536, 2, eb.EB_PATH_GEMV
         y = 0x10000000  # clear of the (fake) 4.4 MB weight range
@@ -170,6 +170,11 @@ def test_auto_path(eb):
     assert f(eb.EB_Q8_0, eb.EB_BF16, 816, 2560, 2048) == eb.EB_PATH_MFMA
     assert f(eb.EB_Q8_0, eb.EB_BF16, 50, 2048, 1024) == eb.EB_PATH_MFMA
     assert f(eb.EB_Q8_0, eb.EB_F16, 1, 4096, 1 << 20) == eb.EB_PATH_MFMA  # x too large for LDS
+    # measured crossover: GEMV for m = 2..4 unless n is small, MFMA from m = 5
+    assert f(eb.EB_Q4_0, eb.EB_F16, 4, 4096, 4096) == eb.EB_PATH_GEMV
+    assert f(eb.EB_Q8_0, eb.EB_BF16, 4, 1024, 4096) == eb.EB_PATH_MFMA
+    assert f(eb.EB_Q4_0, eb.EB_F16, 5, 4096, 4096) == eb.EB_PATH_MFMA
+    assert f(eb.EB_Q4_0, eb.EB_F16, 8, 4096, 4096) == eb.EB_PATH_MFMA
     assert f(eb.EB_Q8_0, eb.EB_F16, 0, 64, 64) == eb.EB_ERR_INVALID
 
 

@@ -96,7 +96,7 @@ def test_from_canonical_round_trip(eb, oracle, qtype):
 # ---------------------------------------------------------------------------
 
 SHAPES = [(37, 96), (515, 1056), (130, 2080)]
-MS_GEMV = [1, 2, 3, 4]
+MS_GEMV = [1, 2, 3, 4, 5, 8]
 MS_MFMA = [1, 5, 9, 50, 64, 65, 130]
 
 
