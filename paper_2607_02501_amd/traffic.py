@@ -1,14 +1,16 @@
 """HBM traffic per kernel launch from two rocprofv3 counter runs.
 
     python -m paper_2607_02501_amd.traffic <FETCH_SIZE csv> <WRITE_SIZE csv> \
-        <workload> <kernel label> <kernel symbol substring> <calibration bytes> [out.json]
+        <workload> <kernel label> <kernel symbol substring> <calibration bytes> [out.json] [a:b]
 
 Both runs execute `bench.py --calibrate-copy <bytes>`, which starts with one
 plain device-to-device copy of known size.  Each counter is scaled by
 (bytes copied) / (counter value of that copy dispatch), so the reported
 traffic is in true bytes whatever unit the counter reports in.  The record
 is stamped with a hash of the kernel sources; bench.py ignores it once the
-sources change.
+sources change.  The optional a:b keeps only the a-th to (b-1)-th dispatches of
+the symbol, in launch order (when one kernel symbol serves launches of
+different sizes, e.g. a fused launch of a whole pass and of one kernel group).
 """
 import csv
 import json
@@ -17,23 +19,28 @@ import sys
 from paper_2607_02501_amd.srchash import kernel_sources_sha
 
 
-def per_dispatch(path, symbol):
+def per_dispatch(path, symbol, pick=None):
     vals, copy = [], []
-    for r in csv.DictReader(open(path)):
+    rows = sorted(csv.DictReader(open(path)), key=lambda r: int(r["Dispatch_Id"]))
+    for r in rows:
         v = float(r["Counter_Value"]) * 1024.0  # counters are reported in KiB
         if "copyBuffer" in r["Kernel_Name"]:
             copy.append(v)
         elif symbol in r["Kernel_Name"]:
             vals.append(v)
+    if pick:
+        a, b = (int(t) for t in pick.split(":"))
+        vals = vals[a:b]
     return vals, max(copy) if copy else None
 
 
 def main():
     fcsv, wcsv, workload, label, symbol, calib = sys.argv[1:7]
     out = sys.argv[7] if len(sys.argv) > 7 else "profiles/traffic.json"
+    pick = sys.argv[8] if len(sys.argv) > 8 else None
     calib = float(calib)
-    fv, fc = per_dispatch(fcsv, symbol)
-    wv, wc = per_dispatch(wcsv, symbol)
+    fv, fc = per_dispatch(fcsv, symbol, pick)
+    wv, wc = per_dispatch(wcsv, symbol, pick)
     fscale, wscale = calib / fc, calib / wc
     fetch = sum(fv) / len(fv) * fscale
     write = sum(wv) / len(wv) * wscale
@@ -43,7 +50,7 @@ def main():
         db = {}
     path = label.split("_")[0]
     db.setdefault(workload, {})[label] = {
-        "kernel_symbol": symbol, "dispatches": len(fv),
+        "kernel_symbol": symbol, "dispatches": len(fv), "dispatch_range": pick,
         "fetch_bytes_per_launch": round(fetch), "write_bytes_per_launch": round(write),
         "hbm_bytes_per_launch": round(fetch + write),
         "fetch_scale": round(fscale, 4), "write_scale": round(wscale, 4),
