@@ -398,3 +398,45 @@ def test_workload_sampled_parity(eb, oracle, name):
             assert_parity(got, y_ref, bound, TOL_F32, f"{name} layer {layer} {pname}")
             del w, qw, y
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("name", list(W.WORKLOADS))
+def test_workload_stack_sampled_parity(eb, oracle, name, monkeypatch):
+    """A whole pass of the workload through eb_qlinear_stack, in the launch
+    configuration the benchmark times (fused launches, graph replay), checked
+    on sampled outputs of the first and last layer (and step) of every
+    projection."""
+    monkeypatch.delenv("EB_STACK_FUSE", raising=False)
+    monkeypatch.delenv("EB_STACK_GRAPH", raising=False)
+    wl = W.WORKLOADS[name]
+    rng = np.random.default_rng(78)
+    qws, entries, where = {}, [], {}
+    for layer in range(wl.layers):
+        for p, (_, k, n) in enumerate(wl.projections):
+            qws[layer, p] = eb.quantize(W.weights(wl, layer, p, DEV), wl.qtype)
+    for step in range(wl.steps):
+        for layer in range(wl.layers):
+            for p, (_, k, n) in enumerate(wl.projections):
+                x = W.activations(wl, layer, p, DEV, step=step)
+                y = torch.full((wl.m, n), float("nan"), device=DEV)
+                where[step, layer, p] = len(entries)
+                entries.append((qws[layer, p], x, y))
+    ops = eb.make_ops(entries)
+    print(f"[parity] {name}: {len(entries)} ops in {eb.stack_launches(ops)} launches", flush=True)
+    eb.qlinear_stack(ops)
+    eb.qlinear_stack(ops)  # second call replays the cached graph
+    torch.cuda.synchronize()
+    for step in sorted({0, wl.steps - 1}):
+        for layer in sorted({0, wl.layers - 1}):
+            for p, (pname, k, n) in enumerate(wl.projections):
+                qw, x, y = entries[where[step, layer, p]]
+                cols = _sample_idx(n, 24, rng, extra=(127, 128, 255, 256))
+                rows = _sample_idx(wl.m, 12, rng, extra=(49, 63, 64))
+                wrows = W.weights(wl, layer, p, DEV, rows=torch.from_numpy(cols).to(DEV)).cpu().numpy()
+                _, y_ref, bound = oracle_reference(oracle, wl.qtype, wrows,
+                                                   x[torch.from_numpy(rows).to(DEV)])
+                got = y[torch.from_numpy(rows).to(DEV)][:, torch.from_numpy(cols).to(DEV)]
+                assert_parity(got, y_ref, bound, TOL_F32, f"{name} step {step} layer {layer} {pname}")
+    del entries, qws, ops
+    eb.stack_cache_clear()
+    torch.cuda.empty_cache()
