@@ -231,11 +231,21 @@ bool fusable(const eb_qlinear_op &o) {
   return o.m == 1 && gemv_fits(1, o.w.k) && m1_fusable(o.w.type, o.m, o.w.k);
 }
 
-// small-m MFMA ops, whose single launches are latency-bound
+// MFMA ops that may join a fused launch.  The fused kernel addresses tiles of
+// up to 256 rows with 31-bit offsets.  EB_STACK_FUSE_MAXM (default 128) caps
+// the rows of a fused op; small-m single launches are latency-bound, large-m
+// ones less so.
+int64_t mm_max_m() {
+  static const int64_t v = [] {
+    const char *e = std::getenv("EB_STACK_FUSE_MAXM");
+    return e ? std::atoll(e) : 128;
+  }();
+  return v;
+}
+
 bool mm_fusable(const eb_qlinear_op &o) {
-  // the fused kernel addresses outputs with 32-bit offsets over 128-row tiles
-  return o.m >= 1 && o.m <= kMMaxM && o.w.k <= kMMaxK &&
-         o.w.n * kMMaxM * (int64_t)dsize(o.y_type) < (int64_t(1) << 31) &&
+  return o.m >= 1 && o.m <= mm_max_m() && o.w.k < kMMaxK &&
+         (o.m + 256) * o.w.n * (int64_t)dsize(o.y_type) < (int64_t(1) << 31) &&
          pick_path(o.w.type, o.x_type, o.m, o.w.n, o.w.k) == EB_PATH_MFMA;
 }
 

@@ -104,8 +104,7 @@ struct MMOp {
   int32_t ds, m, n, k; // ds: scale-plane row stride (elements)
   int32_t tiles_n, nk, yt, pad;
 };
-constexpr int kMMaxM = 128;               // rows an op may have to join a fused run
-constexpr int64_t kMMaxK = int64_t(1) << 22;  // keeps every per-tile byte span within 32 bits
+constexpr int64_t kMMaxK = int64_t(1) << 22;  // k < this keeps per-tile byte spans in 31 bits
 int mm_cfg(int64_t max_m);                // tile configuration for a run
 int64_t mm_tiles(int cfg, int64_t m, int64_t n);
 // Fills the unit ranges wg[0..groups] (balanced by steps) for a table whose

@@ -75,7 +75,7 @@ __host__ __device__ inline void mm_tile(const MMOp *__restrict__ ops, const MMPo
   rows_n = (int)std::min((int64_t)BN, (int64_t)o.n - n0);
 }
 
-template <int QT, int XT, int YT, int BM, int BN, int WM, int WN>
+template <int QT, int XT, int YT, int BM, int BN, int WM, int WN, int D>
 __global__ void __launch_bounds__(WM *WN * 64)
     mfma_multi_kernel(const MMOp *__restrict__ ops, int nops, const int64_t *__restrict__ wg,
                       int groups) {
@@ -98,16 +98,18 @@ __global__ void __launch_bounds__(WM *WN * 64)
   constexpr int NX = ADMA, NW = 2 * BCH;
   static_assert(ADMA >= 1 && ADMA * 8 * WAVES == BM, "x tile must split into 8-row copies");
   static_assert(TM % 32 == 0 && TN % 32 == 0, "wave sub-tile must be whole fragments");
-  // x copies run three steps ahead (four x buffers), weight loads four (four
-  // register sets): a step waits at its barrier for the x copy issued two
-  // steps before it.
-  constexpr int NWAIT = 2 * NX + 3 * NW;
+  // Pipeline depth D: x copies run D steps ahead (D + 1 x buffers), weight
+  // loads D + 1 (D + 1 register sets); a step waits at its barrier for the x
+  // copy issued D - 1 steps before it.  D = 3 for the small tiles; the large
+  // tiles take D = 2, which is what fits in 160 KB of LDS.
+  static_assert(D == 2 || D == 3, "pipeline depth");
+  constexpr int NWAIT = (D - 1) * NX + D * NW;
   static_assert(NWAIT <= 63, "vmcnt range");
 
   __shared__ __attribute__((aligned(1024))) uint8_t sA0[ABYTES];
   __shared__ __attribute__((aligned(1024))) uint8_t sA1[ABYTES];
   __shared__ __attribute__((aligned(1024))) uint8_t sA2[ABYTES];
-  __shared__ __attribute__((aligned(1024))) uint8_t sA3[ABYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t sA3[D == 3 ? ABYTES : 16];
   __shared__ __attribute__((aligned(1024))) uint8_t sB0[BBYTES];
   __shared__ __attribute__((aligned(1024))) uint8_t sB1[BBYTES];
 
@@ -130,8 +132,9 @@ __global__ void __launch_bounds__(WM *WN * 64)
     const int mid = (lo + hi) / 2;
     if (ops[mid].unit_end <= u_begin) lo = mid + 1; else hi = mid;
   }
-  // steps of the range, rounded up to whole groups of four (the extra steps
-  // run on zeros, their loads are empty, and write nothing)
+  // steps of the range, rounded up to whole groups of 4 (D = 3) or 6 (D = 2)
+  // by the loops below (the extra steps run on zeros, their loads are empty,
+  // and write nothing)
   int64_t nsteps = 0;
   for (int o = lo;; ++o) {
     const int64_t first = o ? ops[o - 1].unit_end : 0;
@@ -334,6 +337,310 @@ __global__ void __launch_bounds__(WM *WN * 64)
       *reinterpret_cast<uint4 *>(sA0 + o) = make_uint4(0, 0, 0, 0);
       *reinterpret_cast<uint4 *>(sA1 + o) = make_uint4(0, 0, 0, 0);
       *reinterpret_cast<uint4 *>(sA2 + o) = make_uint4(0, 0, 0, 0);
+      if constexpr (D == 3) *reinterpret_cast<uint4 *>(sA3 + o) = make_uint4(0, 0, 0, 0);
+    }
+  }
+  __syncthreads();
+
+  MMPos C;
+  C.op = lo;
+  C.u = u_begin;
+  C.valid = true;
+  mm_seek(ops, C, u_end);
+  XState X;
+  X.p = C;
+  x_enter(X);
+  WState Wc;
+  Wc.p = C;
+  w_enter(Wc);
+
+  // prologue: x of steps 0..D-1 and weights of steps 0..D
+  Raw S0, S1, S2, S3;
+  x_issue(sA0, X);
+  x_issue(sA1, X);
+  if constexpr (D == 3) x_issue(sA2, X);
+  w_issue(S0, Wc);
+  w_issue(S1, Wc);
+  w_issue(S2, Wc);
+  if constexpr (D == 3) w_issue(S3, Wc);
+#pragma unroll
+  for (int i = 0; i < BCH; ++i) store_w(S0, sB0, i);
+  __syncthreads();
+
+  auto step = [&](const uint8_t *A, uint8_t *Anew, const uint8_t *B, uint8_t *Bn, const Raw &deq,
+                  Raw &ld) __attribute__((always_inline)) {
+    x_issue(Anew, X);
+    w_issue(ld, Wc);
+    compute(A, B, deq, Bn);
+    if (C.valid && C.kt == C.nk - 1) {
+      epilogue(C);
+      zero_acc();
+      wait_vm_barrier<0>();
+    } else {
+      wait_vm_barrier<NWAIT>();
+    }
+    mm_step(ops, C, u_end);
+  };
+  if constexpr (D == 3) {
+    for (int64_t j = 0; j < nsteps; j += 4) {
+      step(sA0, sA3, sB0, sB1, S1, S0);
+      step(sA1, sA0, sB1, sB0, S2, S1);
+      step(sA2, sA1, sB0, sB1, S3, S2);
+      step(sA3, sA2, sB1, sB0, S0, S3);
+    }
+  } else {
+    for (int64_t j = 0; j < nsteps; j += 6) {
+      step(sA0, sA2, sB0, sB1, S1, S0);
+      step(sA1, sA0, sB1, sB0, S2, S1);
+      step(sA2, sA1, sB0, sB1, S0, S2);
+      step(sA0, sA2, sB1, sB0, S1, S0);
+      step(sA1, sA0, sB0, sB1, S2, S1);
+      step(sA2, sA1, sB1, sB0, S0, S2);
+    }
+  }
+#endif  // __HIP_DEVICE_COMPILE__
+}
+
+// ---------------------------------------------------------------------------
+// Fused small-m launch with the weights dequantized straight into MFMA
+// B-operand registers.  At m <= 128 one workgroup tile holds every row, so
+// each of the 4 waves owns a disjoint set of 32 FN output columns: its weights
+// are used by that wave only and need no LDS round trip.  Only the x tile
+// goes through LDS (copied by buffer loads, four buffers, three steps ahead).
+//
+// Within a K-tile of 64, MFMA step s (16 values of k) takes from the lane
+// with column c and half h = lane / 32 the weights k = 32 h + 8 s .. + 7, and
+// from the x row the same k; over s = 0..3 every k of the tile is used once.
+// So a lane's weights for the whole K-tile are block h of its row (Q8_0: 32
+// codes = two 16-byte loads, Q4_0: 16 bytes holding k and k + 16 in the low
+// and high nibbles) plus its scale, loaded four steps ahead into one of four
+// register sets.
+// ---------------------------------------------------------------------------
+template <int QT, int XT>
+__device__ inline void dequant_b(const uint4 (&q)[QT == EB_Q8_0 ? 2 : 1], float d, uint4 (&b)[4]) {
+  constexpr uint32_t kSelLo = 0x04010400u, kSelHi = 0x04030402u;
+  if constexpr (QT == EB_Q8_0) {
+    const float c = -1152.0f * d;
+    const uint32_t w[8] = {q[0].x, q[0].y, q[0].z, q[0].w, q[1].x, q[1].y, q[1].z, q[1].w};
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const uint32_t u0 = w[2 * s] ^ 0x80808080u, u1 = w[2 * s + 1] ^ 0x80808080u;
+      b[s] = make_uint4(deq_pair<XT>(under_1024(u0, kSelLo), d, c),
+                        deq_pair<XT>(under_1024(u0, kSelHi), d, c),
+                        deq_pair<XT>(under_1024(u1, kSelLo), d, c),
+                        deq_pair<XT>(under_1024(u1, kSelHi), d, c));
+    }
+  } else {
+    const float c = -1032.0f * d;
+    const uint32_t w[4] = {q[0].x, q[0].y, q[0].z, q[0].w};
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      // s = 0, 1: low nibbles of bytes 0..7, 8..15; s = 2, 3: high nibbles
+      const uint32_t sh = s < 2 ? 0 : 4;
+      const uint32_t l0 = (w[2 * (s & 1)] >> sh) & 0x0f0f0f0fu;
+      const uint32_t l1 = (w[2 * (s & 1) + 1] >> sh) & 0x0f0f0f0fu;
+      b[s] = make_uint4(deq_pair<XT>(under_1024(l0, kSelLo), d, c),
+                        deq_pair<XT>(under_1024(l0, kSelHi), d, c),
+                        deq_pair<XT>(under_1024(l1, kSelLo), d, c),
+                        deq_pair<XT>(under_1024(l1, kSelHi), d, c));
+    }
+  }
+}
+
+template <int QT, int XT, int YT, int BM, int FN>
+__global__ void __launch_bounds__(256)
+    mm_breg_kernel(const MMOp *__restrict__ ops, int nops, const int64_t *__restrict__ wg,
+                   int groups) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  constexpr int WAVES = 4;
+  constexpr int BN = WAVES * 32 * FN;
+  constexpr int FM = BM / 32;
+  constexpr int ADMA = BM / (8 * WAVES);
+  constexpr int QSB = (QT == EB_Q8_0) ? 32 : 16;
+  constexpr int NQ = (QT == EB_Q8_0) ? 2 : 1;  // 16-byte code loads per fragment
+  constexpr int ABYTES = BM * kBK * 2;
+  constexpr int YSZ = (YT == EB_F32) ? 4 : 2;
+  constexpr int NX = ADMA, NW = FN * (NQ + 1);
+  constexpr int NWAIT = 2 * NX + 3 * NW;  // at a barrier: all but x tile t+1 may be in flight
+  static_assert(ADMA >= 1 && ADMA * 8 * WAVES == BM, "x tile must split into 8-row copies");
+  static_assert(NWAIT <= 63, "vmcnt range");
+
+  __shared__ __attribute__((aligned(1024))) uint8_t sA0[ABYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t sA1[ABYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t sA2[ABYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t sA3[ABYTES];
+
+  const int g = blockIdx.x;
+  const int p = (g % kXcds) * (groups / kXcds) + g / kXcds;
+  const int64_t u_begin = wg[p], u_end = wg[p + 1];
+  if (u_begin >= u_end) return;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+
+  int lo = 0, hi = nops - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi) / 2;
+    if (ops[mid].unit_end <= u_begin) lo = mid + 1; else hi = mid;
+  }
+  int64_t nsteps = 0;
+  for (int o = lo;; ++o) {
+    const int64_t first = o ? ops[o - 1].unit_end : 0;
+    nsteps += (min(ops[o].unit_end, u_end) - max(first, u_begin)) * ops[o].nk;
+    if (ops[o].unit_end >= u_end) break;
+  }
+
+  // --- x copies (as in mfma_multi_kernel) -------------------------------------
+  uint32_t xr_[ADMA], xc_[ADMA];
+#pragma unroll
+  for (int i = 0; i < ADMA; ++i) {
+    const uint32_t r = 8 * (i * WAVES + wave) + (lane >> 3);
+    xr_[i] = r;
+    xc_[i] = ((lane & 7) ^ swz(r)) << 4;
+  }
+  struct XState {
+    MMPos p;
+    const uint8_t *base;
+    uint32_t rec;
+    uint32_t v[ADMA];
+  };
+  auto x_enter = [&](XState &s) __attribute__((always_inline)) {
+    if (!s.p.valid) {
+      s.rec = 0;
+      return;
+    }
+    int64_t m0, n0;
+    int rm, rn;
+    mm_tile<BM, BN>(ops, s.p, m0, n0, rm, rn);
+    const MMOp &o = ops[s.p.op];
+    const uint32_t row = (uint32_t)o.k * 2;
+    s.base = reinterpret_cast<const uint8_t *>(o.x) + m0 * row;
+    s.rec = (uint32_t)rm * row;
+#pragma unroll
+    for (int i = 0; i < ADMA; ++i) s.v[i] = xr_[i] * row + xc_[i];
+  };
+  auto x_issue = [&](uint8_t *sA, XState &s) __attribute__((always_inline)) {
+    const auto r = rsrc(s.base, s.rec);
+#pragma unroll
+    for (int i = 0; i < ADMA; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void *)(sA + (i * WAVES + wave) * 1024), 16,
+                                               (int)s.v[i], 0, 0, 0);
+    if (mm_step(ops, s.p, u_end)) {
+      x_enter(s);
+    } else if (s.p.valid) {
+      s.base += kBK * 2;
+      s.rec -= kBK * 2;
+    }
+  };
+
+  // --- weights: this wave's 32 FN columns, block h = lane / 32 of each row ---
+  const uint32_t wrow0 = (uint32_t)(wave * 32 * FN + (lane & 31));  // tile-local row of fragment 0
+  const uint32_t wh = (uint32_t)(lane >> 5);
+  struct Raw {
+    uint4 q[FN][NQ];
+    uint16_t d[FN];
+  };
+  struct WState {
+    MMPos p;
+    const uint8_t *qb, *db;
+    uint32_t qrec, drec;
+    uint32_t qv, dv;  // lane offsets of fragment 0; fragment j adds 32 j rows
+    uint32_t qrow32, drow32;
+  };
+  auto w_enter = [&](WState &s) __attribute__((always_inline)) {
+    if (!s.p.valid) {
+      s.qrec = s.drec = 0;
+      return;
+    }
+    int64_t m0, n0;
+    int rm, rn;
+    mm_tile<BM, BN>(ops, s.p, m0, n0, rm, rn);
+    const MMOp &o = ops[s.p.op];
+    const uint32_t qrow = (uint32_t)(o.k / kQK) * QSB, drow = (uint32_t)o.ds * 2;
+    s.qb = o.w + n0 * qrow;
+    s.db = o.w + o.d_off + n0 * drow;
+    s.qrec = (uint32_t)rn * qrow;
+    s.drec = (uint32_t)rn * drow;
+    s.qv = wrow0 * qrow + wh * QSB;
+    s.dv = wrow0 * drow + wh * 2;
+    s.qrow32 = 32 * qrow;
+    s.drow32 = 32 * drow;
+  };
+  auto w_issue = [&](Raw &S, WState &s) __attribute__((always_inline)) {
+    const auto qr = rsrc(s.qb, s.qrec);
+    const auto dr = rsrc(s.db, s.drec);
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+#pragma unroll
+      for (int h = 0; h < NQ; ++h) S.q[j][h] = bload(qr, s.qv + j * s.qrow32 + 16 * h);
+      S.d[j] = __builtin_amdgcn_raw_buffer_load_b16(dr, (int)(s.dv + j * s.drow32), 0, 0);
+    }
+    if (mm_step(ops, s.p, u_end)) {
+      w_enter(s);
+    } else if (s.p.valid) {
+      s.qb += 2 * QSB;
+      s.qrec -= 2 * QSB;
+      s.db += 4;
+      s.drec -= 4;
+    }
+  };
+
+  // --- MFMAs: A fragment i, step s at chunk (4 h + s) ^ swz(row) -------------
+  uint32_t abase[FM];
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+    const uint32_t r = i * 32 + (lane & 31);
+    abase[i] = r * (kBK * 2) + (((4u * wh) ^ swz(r)) << 4);
+  }
+  f32x16_t acc[FM][FN];
+  auto zero_acc = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+  };
+  zero_acc();
+
+  auto epilogue = [&](const MMPos &c) __attribute__((always_inline)) {
+    int64_t m0, n0;
+    int rm, rn;
+    mm_tile<BM, BN>(ops, c, m0, n0, rm, rn);
+    const MMOp &o = ops[c.op];
+    const uint32_t n = (uint32_t)o.n;
+    const auto yr = rsrc(o.y, (uint32_t)o.m * n * YSZ);
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int cl = wave * 32 * FN + j * 32 + (lane & 31);
+#pragma unroll
+      for (int i = 0; i < FM; ++i) {
+        const uint32_t row0 = (uint32_t)m0 + i * 32 + 4 * (lane >> 5);
+        const uint32_t base = cl < rn ? (row0 * n + (uint32_t)n0 + cl) * YSZ : 0x80000000u;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const uint32_t off = base + (uint32_t)(8 * (r >> 2) + (r & 3)) * n * YSZ;
+          const float v = acc[i][j][r];  // copy first: see mfma_multi_kernel
+          if constexpr (YT == EB_F32)
+            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), yr, (int)off, 0, 0);
+          else
+            __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(uint16_t, (__bf16)v), yr,
+                                                  (int)off, 0, 0);
+        }
+      }
+    }
+  };
+
+  {
+    constexpr int Z = ABYTES / 16 / 256;
+    static_assert(Z * 256 * 16 == ABYTES, "zero fill must cover the x buffers");
+#pragma unroll
+    for (int i = 0; i < Z; ++i) {
+      const int o = (tid + i * 256) * 16;
+      *reinterpret_cast<uint4 *>(sA0 + o) = make_uint4(0, 0, 0, 0);
+      *reinterpret_cast<uint4 *>(sA1 + o) = make_uint4(0, 0, 0, 0);
+      *reinterpret_cast<uint4 *>(sA2 + o) = make_uint4(0, 0, 0, 0);
       *reinterpret_cast<uint4 *>(sA3 + o) = make_uint4(0, 0, 0, 0);
     }
   }
@@ -351,7 +658,7 @@ __global__ void __launch_bounds__(WM *WN * 64)
   Wc.p = C;
   w_enter(Wc);
 
-  // prologue: x of steps 0..2 and weights of steps 0..3
+  // prologue: x of steps 0..2, weights of steps 0..3
   Raw S0, S1, S2, S3;
   x_issue(sA0, X);
   x_issue(sA1, X);
@@ -360,15 +667,28 @@ __global__ void __launch_bounds__(WM *WN * 64)
   w_issue(S1, Wc);
   w_issue(S2, Wc);
   w_issue(S3, Wc);
-#pragma unroll
-  for (int i = 0; i < BCH; ++i) store_w(S0, sB0, i);
   __syncthreads();
 
-  auto step = [&](const uint8_t *A, uint8_t *A3, const uint8_t *B, uint8_t *Bn, const Raw &deq,
-                  Raw &ld) __attribute__((always_inline)) {
-    x_issue(A3, X);
-    w_issue(ld, Wc);
-    compute(A, B, deq, Bn);
+  // step t: copy x tile t+3, dequantize weight tile t (set t % 4), then reuse
+  // that set for weight tile t+4, run the MFMAs of tile t
+  auto step = [&](const uint8_t *A, uint8_t *Anew, Raw &S) __attribute__((always_inline)) {
+    x_issue(Anew, X);
+    uint4 bq[FN][4];
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+      dequant_b<QT, XT>(S.q[j], (float)__builtin_bit_cast(_Float16, S.d[j]), bq[j]);
+    w_issue(S, Wc);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      uint4 af[FM];
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+        af[i] = *reinterpret_cast<const uint4 *>(A + (abase[i] ^ (16u * s)));
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[i][j] = mfma32<XT>(af[i], bq[j][s], acc[i][j]);
+    }
     if (C.valid && C.kt == C.nk - 1) {
       epilogue(C);
       zero_acc();
@@ -379,10 +699,278 @@ __global__ void __launch_bounds__(WM *WN * 64)
     mm_step(ops, C, u_end);
   };
   for (int64_t j = 0; j < nsteps; j += 4) {
-    step(sA0, sA3, sB0, sB1, S1, S0);
-    step(sA1, sA0, sB1, sB0, S2, S1);
-    step(sA2, sA1, sB0, sB1, S3, S2);
-    step(sA3, sA2, sB1, sB0, S0, S3);
+    step(sA0, sA3, S0);
+    step(sA1, sA0, S1);
+    step(sA2, sA1, S2);
+    step(sA3, sA2, S3);
+  }
+#endif  // __HIP_DEVICE_COMPILE__
+}
+
+// ---------------------------------------------------------------------------
+// Fused small-m launch, weights through LDS as raw codes.  Per K-tile step a
+// workgroup copies, with buffer loads that write LDS directly and read whole
+// row segments (Q8_0: 16 rows x 64 B per instruction, Q4_0: 32 rows x 32 B),
+// the x tile, the packed codes of its 256 weight rows and their two scales;
+// each of the 4 waves then reads the codes of its own 64 columns from LDS,
+// dequantizes them into MFMA B-operand registers (k order as in
+// mm_breg_kernel) and runs its 64 x 64 sub-tile.  Loads keep whole-row
+// coalescing; LDS carries 1 B per Q8_0 weight each way instead of 2.
+// Three stages of every buffer; copies run two steps ahead.
+// Code chunk c (16 B) of tile row r sits at chunk c ^ g(r) of the row
+// (g(r) = (r >> 2) & 3 for 64-byte Q8_0 rows, (r >> 3) & 1 for 32-byte Q4_0
+// rows), so the 16-lane phases of the per-column reads hit distinct banks.
+// ---------------------------------------------------------------------------
+template <int QT, int XT, int YT>
+__global__ void __launch_bounds__(256)
+    mm_ldsw_kernel(const MMOp *__restrict__ ops, int nops, const int64_t *__restrict__ wg,
+                   int groups) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  constexpr int WAVES = 4, BM = 64, FN = 2, BN = WAVES * 32 * FN;  // 256 columns
+  constexpr int FM = BM / 32;
+  constexpr int ADMA = BM / (8 * WAVES);                             // x copies per wave
+  constexpr int QSB = (QT == EB_Q8_0) ? 32 : 16;
+  constexpr int ROWB = 2 * QSB;                  // code bytes per row per K-tile
+  constexpr int RPI = 1024 / ROWB;               // rows per 1 KB copy
+  constexpr int WDMA = BN / RPI / WAVES;         // code copies per wave
+  constexpr int ABYTES = BM * kBK * 2, WBYTES = BN * ROWB, SBYTES = BN * 4;
+  constexpr int YSZ = (YT == EB_F32) ? 4 : 2;
+  constexpr int NSTEP = ADMA + WDMA + 1;         // vector-memory ops per thread per step
+  static_assert(ADMA * 8 * WAVES == BM && WDMA * RPI * WAVES == BN, "copies must tile");
+  static_assert(SBYTES == WAVES * 256, "one 256-byte scale copy per wave");
+
+  __shared__ __attribute__((aligned(1024))) uint8_t sA0[ABYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t sA1[ABYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t sA2[ABYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t sW0[WBYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t sW1[WBYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t sW2[WBYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t sS0[SBYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t sS1[SBYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t sS2[SBYTES];
+
+  const int g = blockIdx.x;
+  const int p = (g % kXcds) * (groups / kXcds) + g / kXcds;
+  const int64_t u_begin = wg[p], u_end = wg[p + 1];
+  if (u_begin >= u_end) return;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+
+  int lo = 0, hi = nops - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi) / 2;
+    if (ops[mid].unit_end <= u_begin) lo = mid + 1; else hi = mid;
+  }
+  int64_t nsteps = 0;
+  for (int o = lo;; ++o) {
+    const int64_t first = o ? ops[o - 1].unit_end : 0;
+    nsteps += (min(ops[o].unit_end, u_end) - max(first, u_begin)) * ops[o].nk;
+    if (ops[o].unit_end >= u_end) break;
+  }
+
+  auto gsw = [](uint32_t r) -> uint32_t {
+    return QT == EB_Q8_0 ? ((r >> 2) & 3) : ((r >> 3) & 1);
+  };
+
+  // --- lane parts of the copies (tile-local) ----------------------------------
+  uint32_t xr_[ADMA], xc_[ADMA];
+#pragma unroll
+  for (int i = 0; i < ADMA; ++i) {
+    const uint32_t r = 8 * (i * WAVES + wave) + (lane >> 3);
+    xr_[i] = r;
+    xc_[i] = ((lane & 7) ^ swz(r)) << 4;
+  }
+  uint32_t wr_[WDMA], wc_[WDMA];
+#pragma unroll
+  for (int i = 0; i < WDMA; ++i) {
+    const uint32_t r = RPI * (i * WAVES + wave) + lane / (ROWB / 16);
+    const uint32_t c = lane % (ROWB / 16);
+    wr_[i] = r;
+    wc_[i] = (c ^ gsw(r)) * 16;  // lane writes stored chunk c, which holds logical chunk c ^ g
+  }
+  const uint32_t sr_ = wave * 64 + lane;  // scale copy: one row per lane, 4 bytes
+
+  // --- the copy cursor: x, codes and scales of one step ---------------------
+  struct LState {
+    MMPos p;
+    const uint8_t *xb, *qb, *db;
+    uint32_t xrec, qrec, drec;
+    uint32_t xv[ADMA], qv[WDMA], dv;
+  };
+  auto l_enter = [&](LState &s) __attribute__((always_inline)) {
+    if (!s.p.valid) {
+      s.xrec = s.qrec = s.drec = 0;
+      return;
+    }
+    int64_t m0, n0;
+    int rm, rn;
+    mm_tile<BM, BN>(ops, s.p, m0, n0, rm, rn);
+    const MMOp &o = ops[s.p.op];
+    const uint32_t xrow = (uint32_t)o.k * 2;
+    const uint32_t qrow = (uint32_t)(o.k / kQK) * QSB, drow = (uint32_t)o.ds * 2;
+    s.xb = reinterpret_cast<const uint8_t *>(o.x) + m0 * xrow;
+    s.xrec = (uint32_t)rm * xrow;
+    s.qb = o.w + n0 * qrow;
+    s.qrec = (uint32_t)rn * qrow;
+    s.db = o.w + o.d_off + n0 * drow;
+    s.drec = (uint32_t)rn * drow;
+#pragma unroll
+    for (int i = 0; i < ADMA; ++i) s.xv[i] = xr_[i] * xrow + xc_[i];
+#pragma unroll
+    for (int i = 0; i < WDMA; ++i) s.qv[i] = wr_[i] * qrow + wc_[i];
+    s.dv = sr_ * drow;
+  };
+  auto l_issue = [&](uint8_t *sA, uint8_t *sW, uint8_t *sS, LState &s) __attribute__((always_inline)) {
+    const auto xr = rsrc(s.xb, s.xrec);
+    const auto qr = rsrc(s.qb, s.qrec);
+    const auto dr = rsrc(s.db, s.drec);
+#pragma unroll
+    for (int i = 0; i < ADMA; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lds_void *)(sA + (i * WAVES + wave) * 1024), 16,
+                                               (int)s.xv[i], 0, 0, 0);
+#pragma unroll
+    for (int i = 0; i < WDMA; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(qr, (lds_void *)(sW + (i * WAVES + wave) * 1024), 16,
+                                               (int)s.qv[i], 0, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(dr, (lds_void *)(sS + wave * 256), 4, (int)s.dv, 0, 0, 0);
+    if (mm_step(ops, s.p, u_end)) {
+      l_enter(s);
+    } else if (s.p.valid) {
+      s.xb += kBK * 2;
+      s.xrec -= kBK * 2;
+      s.qb += ROWB;
+      s.qrec -= ROWB;
+      s.db += 4;
+      s.drec -= 4;
+    }
+  };
+
+  // --- per-lane reads of its columns' codes and scales --------------------
+  const uint32_t wh = (uint32_t)(lane >> 5);
+  uint32_t bq_off[FN][QT == EB_Q8_0 ? 2 : 1], bs_off[FN];
+#pragma unroll
+  for (int j = 0; j < FN; ++j) {
+    const uint32_t r = wave * 64 + j * 32 + (lane & 31);
+    if constexpr (QT == EB_Q8_0) {
+      bq_off[j][0] = r * ROWB + (((2 * wh) ^ gsw(r)) << 4);
+      bq_off[j][1] = r * ROWB + (((2 * wh + 1) ^ gsw(r)) << 4);
+    } else {
+      bq_off[j][0] = r * ROWB + ((wh ^ gsw(r)) << 4);
+    }
+    bs_off[j] = r * 4 + 2 * wh;
+  }
+  uint32_t abase[FM];
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+    const uint32_t r = i * 32 + (lane & 31);
+    abase[i] = r * (kBK * 2) + (((4u * wh) ^ swz(r)) << 4);
+  }
+  f32x16_t acc[FM][FN];
+  auto zero_acc = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+  };
+  zero_acc();
+
+  auto epilogue = [&](const MMPos &c) __attribute__((always_inline)) {
+    int64_t m0, n0;
+    int rm, rn;
+    mm_tile<BM, BN>(ops, c, m0, n0, rm, rn);
+    const MMOp &o = ops[c.op];
+    const uint32_t n = (uint32_t)o.n;
+    const auto yr = rsrc(o.y, (uint32_t)o.m * n * YSZ);
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int cl = wave * 64 + j * 32 + (lane & 31);
+#pragma unroll
+      for (int i = 0; i < FM; ++i) {
+        const uint32_t row0 = (uint32_t)m0 + i * 32 + 4 * (lane >> 5);
+        const uint32_t base = cl < rn ? (row0 * n + (uint32_t)n0 + cl) * YSZ : 0x80000000u;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const uint32_t off = base + (uint32_t)(8 * (r >> 2) + (r & 3)) * n * YSZ;
+          const float v = acc[i][j][r];  // copy first: see mfma_multi_kernel
+          if constexpr (YT == EB_F32)
+            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), yr, (int)off, 0, 0);
+          else
+            __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(uint16_t, (__bf16)v), yr,
+                                                  (int)off, 0, 0);
+        }
+      }
+    }
+  };
+
+  {
+    constexpr int Z = ABYTES / 16 / 256;
+    static_assert(Z * 256 * 16 == ABYTES, "zero fill must cover the x buffers");
+#pragma unroll
+    for (int i = 0; i < Z; ++i) {
+      const int o = (tid + i * 256) * 16;
+      *reinterpret_cast<uint4 *>(sA0 + o) = make_uint4(0, 0, 0, 0);
+      *reinterpret_cast<uint4 *>(sA1 + o) = make_uint4(0, 0, 0, 0);
+      *reinterpret_cast<uint4 *>(sA2 + o) = make_uint4(0, 0, 0, 0);
+    }
+  }
+  __syncthreads();
+
+  MMPos C;
+  C.op = lo;
+  C.u = u_begin;
+  C.valid = true;
+  mm_seek(ops, C, u_end);
+  LState L;
+  L.p = C;
+  l_enter(L);
+  // prologue: steps 0 and 1
+  l_issue(sA0, sW0, sS0, L);
+  l_issue(sA1, sW1, sS1, L);
+  wait_vm_barrier<NSTEP>();
+
+  // step t: copy step t+2 into the free stage, read this wave's codes of step t,
+  // dequantize, MFMAs, then wait for the copies of step t+1
+  auto step = [&](const uint8_t *A, const uint8_t *Wt, const uint8_t *St, uint8_t *A2, uint8_t *W2,
+                  uint8_t *S2) __attribute__((always_inline)) {
+    l_issue(A2, W2, S2, L);
+    uint4 bq[FN][4];
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      uint4 q[QT == EB_Q8_0 ? 2 : 1];
+#pragma unroll
+      for (int h = 0; h < (QT == EB_Q8_0 ? 2 : 1); ++h)
+        q[h] = *reinterpret_cast<const uint4 *>(Wt + bq_off[j][h]);
+      const uint16_t d = *reinterpret_cast<const uint16_t *>(St + bs_off[j]);
+      dequant_b<QT, XT>(q, (float)__builtin_bit_cast(_Float16, d), bq[j]);
+    }
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      uint4 af[FM];
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+        af[i] = *reinterpret_cast<const uint4 *>(A + (abase[i] ^ (16u * s)));
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[i][j] = mfma32<XT>(af[i], bq[j][s], acc[i][j]);
+    }
+    if (C.valid && C.kt == C.nk - 1) {
+      epilogue(C);
+      zero_acc();
+      wait_vm_barrier<0>();
+    } else {
+      wait_vm_barrier<NSTEP>();
+    }
+    mm_step(ops, C, u_end);
+  };
+  for (int64_t j = 0; j < nsteps; j += 3) {
+    step(sA0, sW0, sS0, sA2, sW2, sS2);
+    step(sA1, sW1, sS1, sA0, sW0, sS0);
+    step(sA2, sW2, sS2, sA1, sW1, sS1);
   }
 #endif  // __HIP_DEVICE_COMPILE__
 }
@@ -390,12 +978,23 @@ __global__ void __launch_bounds__(WM *WN * 64)
 template <int QT, int XT, int YT>
 hipError_t launch_multi_q(int cfg, const MMOp *ops, int nops, const int64_t *wg, int groups,
                           hipStream_t s) {
-  if (cfg == 0)
-    mfma_multi_kernel<QT, XT, YT, 64, 128, 2, 2><<<groups, 256, 0, s>>>(ops, nops, wg, groups);
-  else if (cfg == 1)
-    mfma_multi_kernel<QT, XT, YT, 128, 128, 2, 2><<<groups, 256, 0, s>>>(ops, nops, wg, groups);
-  else
-    mfma_multi_kernel<QT, XT, YT, 64, 256, 2, 4><<<groups, 512, 0, s>>>(ops, nops, wg, groups);
+  switch (cfg) {
+    case 0:
+      mm_breg_kernel<QT, XT, YT, 64, 2><<<groups, 256, 0, s>>>(ops, nops, wg, groups);
+      break;
+    case 4:
+      mm_ldsw_kernel<QT, XT, YT><<<groups, 256, 0, s>>>(ops, nops, wg, groups);
+      break;
+    case 1:
+      mm_breg_kernel<QT, XT, YT, 128, 1><<<groups, 256, 0, s>>>(ops, nops, wg, groups);
+      break;
+    case 2:
+      mfma_multi_kernel<QT, XT, YT, 64, 128, 2, 2, 3><<<groups, 256, 0, s>>>(ops, nops, wg, groups);
+      break;
+    default:
+      mfma_multi_kernel<QT, XT, YT, 256, 256, 2, 4, 2><<<groups, 512, 0, s>>>(ops, nops, wg, groups);
+      break;
+  }
   return hipGetLastError();
 }
 
@@ -406,8 +1005,9 @@ hipError_t launch_multi_y(int32_t yt, int cfg, const MMOp *ops, int nops, const 
   return launch_multi_q<QT, XT, EB_BF16>(cfg, ops, nops, wg, groups, s);
 }
 
-// {BM, BN, workgroups per CU}
-constexpr int kMMTiles[3][3] = {{64, 128, 2}, {128, 128, 1}, {64, 256, 1}};
+// {BM, BN, workgroups per CU}: 0, 1 weights in registers (m <= 64, m <= 128),
+// 2, 3 weights through LDS (64 x 128 kept for comparison, 256 x 256 for m > 128)
+constexpr int kMMTiles[5][3] = {{64, 256, 2}, {128, 128, 2}, {64, 128, 2}, {256, 256, 1}, {64, 256, 2}};
 
 }  // namespace
 
@@ -416,8 +1016,8 @@ int mm_cfg(int64_t max_m) {
     const char *e = getenv("EB_MM_CFG");  // tuning: force the fused tile
     return e ? atoi(e) : -1;
   }();
-  if (forced >= 0 && forced <= 2 && (max_m <= 64 || forced == 1)) return forced;
-  return max_m <= 64 ? 0 : 1;
+  if (forced >= 0 && forced <= 4 && (max_m <= 64 || forced == 1 || forced == 3)) return forced;
+  return max_m <= 64 ? 0 : (max_m <= 128 ? 1 : 3);
 }
 
 int64_t mm_tiles(int cfg, int64_t m, int64_t n) {
