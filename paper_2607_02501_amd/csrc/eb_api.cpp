@@ -305,7 +305,7 @@ eb_status build_plan(const eb_qlinear_op *ops, int32_t n_ops, bool alloc, Plan &
         e.n = (int32_t)o.w.n;
         e.k = (int32_t)o.w.k;
         e.tiles_n = (int32_t)mm_tiles(s.mm_cfg, 1, o.w.n);
-        e.nk = (int32_t)((o.w.k + 63) / 64);
+        e.nk = (int32_t)((o.w.k + mm_bk(s.mm_cfg) - 1) / mm_bk(s.mm_cfg));
         e.yt = o.y_type;
         run.push_back(e);
       }

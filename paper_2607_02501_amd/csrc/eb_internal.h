@@ -107,6 +107,7 @@ struct MMOp {
 constexpr int64_t kMMaxK = int64_t(1) << 22;  // k < this keeps per-tile byte spans in 31 bits
 int mm_cfg(int64_t max_m);                // tile configuration for a run
 int64_t mm_tiles(int cfg, int64_t m, int64_t n);
+int mm_bk(int cfg);                       // k covered by one step of the configuration
 // Fills the unit ranges wg[0..groups] (balanced by steps) for a table whose
 // unit_end / nk are set; returns the number of workgroups to launch.
 int mm_partition(const std::vector<MMOp> &ops, int cfg, std::vector<int64_t> &wg);

@@ -15,6 +15,8 @@ namespace {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 
 constexpr int kBK = 64;        // K elements per tile (2 blocks)
 constexpr int kXcds = 8;
@@ -112,6 +114,18 @@ __device__ inline void dequant_chunk(const uint4 q, float d, uint4 (&v)[Deq<QT>:
 __device__ inline __amdgpu_buffer_rsrc_t rsrc(const void *base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes,
                                            0x00020000);
+}
+
+// The same for a base and size that are uniform across the wave but that the
+// compiler cannot prove uniform (cursor state carried through loops): without
+// the read-first-lane it keeps them in vector registers and wraps every load
+// in a loop over distinct descriptor values.
+__device__ inline __amdgpu_buffer_rsrc_t ursrc(const void *base, uint32_t bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
+  return rsrc(reinterpret_cast<const void *>(((uint64_t)hi << 32) | lo),
+              __builtin_amdgcn_readfirstlane(bytes));
 }
 
 __device__ inline uint4 bload(__amdgpu_buffer_rsrc_t r, uint32_t voff) {
