@@ -108,6 +108,9 @@ constexpr int64_t kMMaxK = int64_t(1) << 22;  // k < this keeps per-tile byte sp
 int mm_cfg(int64_t max_m);                // tile configuration for a run
 int64_t mm_tiles(int cfg, int64_t m, int64_t n);
 int mm_bk(int cfg);                       // k covered by one step of the configuration
+// The 128-wide-step fused kernel (configuration 6), in its own source file.
+hipError_t launch_lds2(int32_t type, int32_t xt, int32_t yt, const MMOp *ops, int nops,
+                       const int64_t *wg, int groups, hipStream_t s);
 // Fills the unit ranges wg[0..groups] (balanced by steps) for a table whose
 // unit_end / nk are set; returns the number of workgroups to launch.
 int mm_partition(const std::vector<MMOp> &ops, int cfg, std::vector<int64_t> &wg);

@@ -12,6 +12,7 @@
 
 #include "eb_internal.h"
 #include "mfma_common.h"
+#include "mm_common.h"
 
 namespace eb {
 namespace {
@@ -30,51 +31,6 @@ namespace {
 // suits a launch that keeps every CU streaming weights, where memory latency
 // is longer than in a single-op launch.
 // ---------------------------------------------------------------------------
-// Position in a workgroup's stream of units: the unit, its op and K-tile.
-struct MMPos {
-  int op;
-  int64_t u;
-  int kt, nk;
-  int64_t op_end;
-  bool valid;
-};
-
-// Moves to the first step of unit p.u (p.op must not be past its op).
-__host__ __device__ inline void mm_seek(const MMOp *__restrict__ ops, MMPos &p, int64_t u_end) {
-  p.kt = 0;
-  if (p.u >= u_end) {
-    p.valid = false;
-    return;
-  }
-  while (p.u >= ops[p.op].unit_end) ++p.op;
-  p.nk = ops[p.op].nk;
-  p.op_end = ops[p.op].unit_end;
-}
-
-// Advances one step; returns true when a new unit starts (p.valid tells
-// whether there is one).
-__host__ __device__ inline bool mm_step(const MMOp *__restrict__ ops, MMPos &p, int64_t u_end) {
-  if (!p.valid) return false;
-  if (++p.kt < p.nk) return false;
-  ++p.u;
-  mm_seek(ops, p, u_end);
-  return true;
-}
-
-// Tile (m0, n0) and valid extent of unit p.u of op p.op.
-template <int BM, int BN>
-__host__ __device__ inline void mm_tile(const MMOp *__restrict__ ops, const MMPos &p, int64_t &m0,
-                               int64_t &n0, int &rows_m, int &rows_n) {
-  const MMOp &o = ops[p.op];
-  const int64_t first = p.op ? ops[p.op - 1].unit_end : 0;
-  const uint32_t uin = (uint32_t)(p.u - first), tiles_n = (uint32_t)o.tiles_n;
-  const uint32_t tm = uin / tiles_n, tn = uin - tm * tiles_n;
-  m0 = (int64_t)tm * BM;
-  n0 = (int64_t)tn * BN;
-  rows_m = (int)std::min((int64_t)BM, (int64_t)o.m - m0);
-  rows_n = (int)std::min((int64_t)BN, (int64_t)o.n - n0);
-}
-
 template <int QT, int XT, int YT, int BM, int BN, int WM, int WN, int D>
 __global__ void __launch_bounds__(WM *WN * 64)
     mfma_multi_kernel(const MMOp *__restrict__ ops, int nops, const int64_t *__restrict__ wg,
@@ -416,37 +372,6 @@ __global__ void __launch_bounds__(WM *WN * 64)
 // and high nibbles) plus its scale, loaded four steps ahead into one of four
 // register sets.
 // ---------------------------------------------------------------------------
-template <int QT, int XT>
-__device__ inline void dequant_b(const uint4 (&q)[QT == EB_Q8_0 ? 2 : 1], float d, uint4 (&b)[4]) {
-  constexpr uint32_t kSelLo = 0x04010400u, kSelHi = 0x04030402u;
-  if constexpr (QT == EB_Q8_0) {
-    const float c = -1152.0f * d;
-    const uint32_t w[8] = {q[0].x, q[0].y, q[0].z, q[0].w, q[1].x, q[1].y, q[1].z, q[1].w};
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      const uint32_t u0 = w[2 * s] ^ 0x80808080u, u1 = w[2 * s + 1] ^ 0x80808080u;
-      b[s] = make_uint4(deq_pair<XT>(under_1024(u0, kSelLo), d, c),
-                        deq_pair<XT>(under_1024(u0, kSelHi), d, c),
-                        deq_pair<XT>(under_1024(u1, kSelLo), d, c),
-                        deq_pair<XT>(under_1024(u1, kSelHi), d, c));
-    }
-  } else {
-    const float c = -1032.0f * d;
-    const uint32_t w[4] = {q[0].x, q[0].y, q[0].z, q[0].w};
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      // s = 0, 1: low nibbles of bytes 0..7, 8..15; s = 2, 3: high nibbles
-      const uint32_t sh = s < 2 ? 0 : 4;
-      const uint32_t l0 = (w[2 * (s & 1)] >> sh) & 0x0f0f0f0fu;
-      const uint32_t l1 = (w[2 * (s & 1) + 1] >> sh) & 0x0f0f0f0fu;
-      b[s] = make_uint4(deq_pair<XT>(under_1024(l0, kSelLo), d, c),
-                        deq_pair<XT>(under_1024(l0, kSelHi), d, c),
-                        deq_pair<XT>(under_1024(l1, kSelLo), d, c),
-                        deq_pair<XT>(under_1024(l1, kSelHi), d, c));
-    }
-  }
-}
-
 template <int QT, int XT, int YT, int BM, int FN>
 __global__ void __launch_bounds__(256)
     mm_breg_kernel(const MMOp *__restrict__ ops, int nops, const int64_t *__restrict__ wg,
@@ -1030,372 +955,6 @@ __global__ void __launch_bounds__(256)
 #endif  // __HIP_DEVICE_COMPILE__
 }
 
-// ---------------------------------------------------------------------------
-// Fused small-m launch with 128-wide K steps.  Memory cost here follows the
-// number of cache lines a load touches more than its bytes, so every load is
-// shaped to use whole lines:
-//  * codes: a step covers two K-tiles, so a Q8_0 row segment is a full
-//    128-byte line (Q4_0: 64 bytes); copied into LDS by 8 (16) rows per
-//    1 KB buffer load that writes LDS directly, three stages, two steps ahead;
-//  * x: 64 rows x 256 bytes per step, two stages, one step ahead (x is small
-//    and stays in L2);
-//  * scales: once per group of four steps (16 blocks, 32 bytes of a row),
-//    two 16-byte lanes per row, loaded into registers a step ahead and written
-//    to one of two LDS stages at the end of the next step.  Steps without a
-//    scale load issue the same loads with an empty range (no memory access),
-//    so every step has the same number of vector-memory ops in flight.
-// One 256-thread workgroup per CU; wave w owns columns 64w..64w+63 of the
-// 64 x 256 tile and dequantizes its codes straight into MFMA registers, with
-// the k order of mm_breg_kernel applied to each 64-wide half of the step.
-// The weights are the MFMA A operand, so y leaves in 4-column packed stores.
-// Chunk (16 B) swizzles keep the 16-lane phases of every LDS read on distinct
-// banks: x chunk c of row r at c ^ (r & 15); Q8_0 codes at c ^ ((r >> 1) & 7);
-// Q4_0 codes at c ^ ((r >> 2) & 3).
-// ---------------------------------------------------------------------------
-template <int QT, int XT, int YT>
-__global__ void __launch_bounds__(256)
-    mm_lds2_kernel(const MMOp *__restrict__ ops, int nops, const int64_t *__restrict__ wg,
-                   int groups) {
-#if defined(__HIP_DEVICE_COMPILE__)
-  constexpr int WAVES = 4, BM = 64, FN = 2, BN = WAVES * 32 * FN, FM = BM / 32;
-  constexpr int BKS = 2 * kBK;                    // k per step
-  constexpr int QSB = (QT == EB_Q8_0) ? 32 : 16;  // code bytes per block
-  constexpr int NQ = (QT == EB_Q8_0) ? 2 : 1;     // 16-byte chunks per block
-  constexpr int CROW = 4 * QSB;                   // code bytes per row per step
-  constexpr int CCH = CROW / 16;                  // code chunks per row per step
-  constexpr int XROW = BKS * 2;                   // x bytes per row per step
-  constexpr int XBYTES = BM * XROW, WBYTES = BN * CROW, SBYTES = BN * 32;
-  constexpr int NX = XBYTES / 1024 / WAVES;       // x copies per lane per step
-  constexpr int NW = WBYTES / 1024 / WAVES;       // code copies per lane per step
-  constexpr int NS = SBYTES / 16 / (WAVES * 64);  // scale loads per lane per step
-  constexpr int NST = FM * FN * 4;                // packed y stores per lane per tile
-  constexpr int YSZ = (YT == EB_F32) ? 4 : 2;
-  static_assert(NX * 1024 * WAVES == XBYTES && NW * 1024 * WAVES == WBYTES, "copies must tile");
-  static_assert(NS == 2 && NW + NS + NST <= 63, "scale loads / wait count range");
-
-  __shared__ __attribute__((aligned(1024))) uint8_t sX0[XBYTES];
-  __shared__ __attribute__((aligned(1024))) uint8_t sX1[XBYTES];
-  __shared__ __attribute__((aligned(1024))) uint8_t sW0[WBYTES];
-  __shared__ __attribute__((aligned(1024))) uint8_t sW1[WBYTES];
-  __shared__ __attribute__((aligned(1024))) uint8_t sW2[WBYTES];
-  __shared__ __attribute__((aligned(1024))) uint8_t sS[2 * SBYTES];
-
-  const int g = blockIdx.x;
-  const int p = (g % kXcds) * (groups / kXcds) + g / kXcds;
-  const int64_t u_begin = wg[p], u_end = wg[p + 1];
-  if (u_begin >= u_end) return;
-
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const uint32_t wh = (uint32_t)(lane >> 5);
-
-  int lo = 0, hi = nops - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi) / 2;
-    if (ops[mid].unit_end <= u_begin) lo = mid + 1; else hi = mid;
-  }
-  int64_t nsteps = 0;
-  for (int o = lo;; ++o) {
-    const int64_t first = o ? ops[o - 1].unit_end : 0;
-    nsteps += (min(ops[o].unit_end, u_end) - max(first, u_begin)) * ops[o].nk;
-    if (ops[o].unit_end >= u_end) break;
-  }
-
-  auto gsw = [](uint32_t r) -> uint32_t {
-    return QT == EB_Q8_0 ? ((r >> 1) & 7) : ((r >> 2) & 3);
-  };
-
-  // --- lane parts of the loads (tile-local offsets) ----------------------------
-  uint32_t xo_[NX], wo_[NW], so_[NS], sd_[NS];
-#pragma unroll
-  for (int i = 0; i < NX; ++i) {
-    const uint32_t r = 4 * (i * WAVES + wave) + (lane >> 4);
-    xo_[i] = r;  // row; chunk part added per op (row stride differs)
-  }
-  const uint32_t xc_ = (uint32_t)(lane & 15);
-#pragma unroll
-  for (int i = 0; i < NW; ++i) wo_[i] = (1024 / CROW) * (i * WAVES + wave) + lane / CCH;
-  const uint32_t wc_ = (uint32_t)(lane % CCH);
-#pragma unroll
-  for (int i = 0; i < NS; ++i) {
-    const uint32_t r = i * 128 + (tid >> 1);
-    so_[i] = r;
-    sd_[i] = r * 32 + (tid & 1) * 16;  // LDS offset within a scale stage
-  }
-
-  // --- x cursor (one step ahead) ----------------------------------------------
-  struct XState {
-    MMPos p;
-    const uint8_t *b;
-    uint32_t rec, v[NX];
-  };
-  auto x_enter = [&](XState &s) __attribute__((always_inline)) {
-    if (!s.p.valid) {
-      s.rec = 0;
-      return;
-    }
-    int64_t m0, n0;
-    int rm, rn;
-    mm_tile<BM, BN>(ops, s.p, m0, n0, rm, rn);
-    const MMOp &o = ops[s.p.op];
-    const uint32_t xrow = (uint32_t)o.k * 2;
-    s.b = reinterpret_cast<const uint8_t *>(o.x) + m0 * xrow;
-    s.rec = (uint32_t)rm * xrow;
-#pragma unroll
-    for (int i = 0; i < NX; ++i) s.v[i] = xo_[i] * xrow + ((xc_ ^ (xo_[i] & 15)) << 4);
-  };
-  auto x_issue = [&](uint8_t *sX, XState &s) __attribute__((always_inline)) {
-    const auto r = ursrc(s.b, s.rec);
-#pragma unroll
-    for (int i = 0; i < NX; ++i)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void *)(sX + (i * WAVES + wave) * 1024), 16,
-                                               (int)s.v[i], 0, 0, 0);
-    if (mm_step(ops, s.p, u_end)) {
-      x_enter(s);
-    } else if (s.p.valid) {
-      s.b += XROW;
-      s.rec -= XROW;
-    }
-  };
-
-  // --- codes + scales cursor (two steps ahead) -------------------------------
-  struct WState {
-    MMPos p;
-    const uint8_t *qb, *db;
-    uint32_t qrec, drec, qv[NW], dv[NS];
-  };
-  auto w_enter = [&](WState &s) __attribute__((always_inline)) {
-    if (!s.p.valid) {
-      s.qrec = s.drec = 0;
-      return;
-    }
-    int64_t m0, n0;
-    int rm, rn;
-    mm_tile<BM, BN>(ops, s.p, m0, n0, rm, rn);
-    const MMOp &o = ops[s.p.op];
-    const uint32_t qrow = (uint32_t)(o.k / kQK) * QSB, drow = (uint32_t)o.ds * 2;
-    s.qb = o.w + n0 * qrow;
-    s.qrec = (uint32_t)rn * qrow;
-    s.db = o.w + o.d_off + n0 * drow;
-    s.drec = (uint32_t)rn * drow;
-#pragma unroll
-    for (int i = 0; i < NW; ++i) s.qv[i] = wo_[i] * qrow + ((wc_ ^ gsw(wo_[i])) << 4);
-#pragma unroll
-    for (int i = 0; i < NS; ++i) s.dv[i] = so_[i] * drow + (tid & 1) * 16;
-  };
-  // returns whether the scale loads were real (the step starts a group)
-  auto w_issue = [&](uint8_t *sW, uint4 (&sreg)[NS], WState &s) __attribute__((always_inline)) -> bool {
-    const auto qr = ursrc(s.qb, s.qrec);
-#pragma unroll
-    for (int i = 0; i < NW; ++i)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(qr, (lds_void *)(sW + (i * WAVES + wave) * 1024), 16,
-                                               (int)s.qv[i], 0, 0, 0);
-    const bool grp = s.p.valid && (s.p.kt & 3) == 0;
-    const auto dr = ursrc(s.db, grp ? s.drec : 0u);
-#pragma unroll
-    for (int i = 0; i < NS; ++i) sreg[i] = bload(dr, s.dv[i]);
-    if (mm_step(ops, s.p, u_end)) {
-      w_enter(s);
-    } else if (s.p.valid) {
-      s.qb += CROW;
-      s.qrec -= CROW;
-      if ((s.p.kt & 3) == 0) {
-        s.db += 32;
-        s.drec -= 32;
-      }
-    }
-    return grp;
-  };
-
-  // --- per-lane LDS read offsets ---------------------------------------------
-  uint32_t bq_off[FN][2][NQ], bs_off[FN];
-#pragma unroll
-  for (int j = 0; j < FN; ++j) {
-    const uint32_t r = wave * 64 + j * 32 + (lane & 31);
-#pragma unroll
-    for (int q = 0; q < 2; ++q)
-#pragma unroll
-      for (int h = 0; h < NQ; ++h) {
-        const uint32_t c = (2 * q + wh) * NQ + h;  // chunk of block 2q + wh
-        bq_off[j][q][h] = r * CROW + ((c ^ gsw(r)) << 4);
-      }
-    bs_off[j] = r * 32;
-  }
-  uint32_t abase[FM];
-#pragma unroll
-  for (int i = 0; i < FM; ++i) {
-    const uint32_t r = i * 32 + (lane & 31);
-    abase[i] = r * XROW + (((4u * wh) ^ (r & 15)) << 4);
-  }
-
-  f32x16_t acc[FM][FN];
-  auto zero_acc = [&]() __attribute__((always_inline)) {
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-      for (int j = 0; j < FN; ++j)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-  };
-  zero_acc();
-
-  // lane (l, reg r) of sub-tile (i, j) holds y[m0 + 32 i + l % 32][n0 + 64 wave +
-  // 32 j + 8 (r / 4) + 4 (l / 32) + r % 4]; see mm_ldsw_kernel for the bounds.
-  auto epilogue = [&](const MMPos &c) __attribute__((always_inline)) -> bool {
-    int64_t m0, n0;
-    int rm, rn;
-    mm_tile<BM, BN>(ops, c, m0, n0, rm, rn);
-    const MMOp &o = ops[c.op];
-    const uint32_t n = (uint32_t)o.n;
-    const auto yr = ursrc(o.y, (uint32_t)o.m * n * YSZ);
-    const bool packed = (n & 3) == 0;
-#pragma unroll
-    for (int i = 0; i < FM; ++i) {
-      const uint32_t row = (uint32_t)m0 + i * 32 + (lane & 31);
-#pragma unroll
-      for (int j = 0; j < FN; ++j) {
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int cl = wave * 64 + j * 32 + 8 * q + 4 * (int)wh;
-          const uint32_t base = (row * n + (uint32_t)n0 + cl) * YSZ;
-          float v[4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * q + e];  // copy first: see mfma_multi_kernel
-          if (packed) {
-            const uint32_t off = cl < rn ? base : 0x80000000u;
-            if constexpr (YT == EB_F32) {
-              u32x4_t w;
-#pragma unroll
-              for (int e = 0; e < 4; ++e) w[e] = __builtin_bit_cast(uint32_t, v[e]);
-              __builtin_amdgcn_raw_buffer_store_b128(w, yr, (int)off, 0, 0);
-            } else {
-              u32x2_t w;
-#pragma unroll
-              for (int e = 0; e < 2; ++e)
-                w[e] = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)v[2 * e]) |
-                       ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)v[2 * e + 1]) << 16);
-              __builtin_amdgcn_raw_buffer_store_b64(w, yr, (int)off, 0, 0);
-            }
-          } else {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const uint32_t off = cl + e < rn ? base + e * YSZ : 0x80000000u;
-              if constexpr (YT == EB_F32)
-                __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v[e]), yr, (int)off, 0, 0);
-              else
-                __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(uint16_t, (__bf16)v[e]), yr,
-                                                      (int)off, 0, 0);
-            }
-          }
-        }
-      }
-    }
-    return packed;
-  };
-
-  {
-    constexpr int Z = XBYTES / 16 / 256;
-    static_assert(Z * 256 * 16 == XBYTES, "zero fill must cover the x buffers");
-#pragma unroll
-    for (int i = 0; i < Z; ++i) {
-      const int o = (tid + i * 256) * 16;
-      *reinterpret_cast<uint4 *>(sX0 + o) = make_uint4(0, 0, 0, 0);
-      *reinterpret_cast<uint4 *>(sX1 + o) = make_uint4(0, 0, 0, 0);
-    }
-  }
-  __syncthreads();
-
-  MMPos C;
-  C.op = lo;
-  C.u = u_begin;
-  C.valid = true;
-  mm_seek(ops, C, u_end);
-  XState X;
-  X.p = C;
-  x_enter(X);
-  WState W;
-  W.p = C;
-  w_enter(W);
-
-  // prologue: x of step 0, codes and scales of steps 0 and 1; the scales of
-  // step 0 (always a group start) go to stage 0 once they have arrived
-  uint4 sa[NS], sb[NS];
-  x_issue(sX0, X);
-  w_issue(sW0, sa, W);
-  bool spend = w_issue(sW1, sb, W);
-  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(NW + NS) : "memory");
-#pragma unroll
-  for (int i = 0; i < NS; ++i) *reinterpret_cast<uint4 *>(sS + sd_[i]) = sa[i];
-  wait_vm_barrier<NW + NS>();
-
-  uint32_t gstage = 0;  // LDS scale stage of the current step's group
-  // step t: x of step t+1, codes and scales of step t+2; read this step's
-  // scales and codes, dequantize, MFMAs; at a tile's last step store y; write
-  // the scales loaded in the previous step (group starting at step t+1) to
-  // the other stage; wait for step t+1's copies.
-  auto step = [&](const uint8_t *Xc, const uint8_t *Wc, uint8_t *Xn, uint8_t *Wn, uint4 (&sprev)[NS],
-                  uint4 (&snew)[NS]) __attribute__((always_inline)) {
-    x_issue(Xn, X);
-    const bool snext = w_issue(Wn, snew, W);
-    const uint8_t *Sc = sS + gstage * SBYTES + 8 * (C.kt & 3);
-#pragma unroll
-    for (int q = 0; q < 2; ++q) {
-      uint4 bq[FN][4];
-#pragma unroll
-      for (int j = 0; j < FN; ++j) {
-        uint4 cq[NQ];
-#pragma unroll
-        for (int h = 0; h < NQ; ++h) cq[h] = *reinterpret_cast<const uint4 *>(Wc + bq_off[j][q][h]);
-        const uint32_t d2 = *reinterpret_cast<const uint32_t *>(Sc + bs_off[j] + 4 * q);
-        const uint16_t d = (uint16_t)(d2 >> (16 * wh));
-        dequant_b<QT, XT>(cq, (float)__builtin_bit_cast(_Float16, d), bq[j]);
-      }
-#pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        uint4 af[FM];
-#pragma unroll
-        for (int i = 0; i < FM; ++i)
-          af[i] = *reinterpret_cast<const uint4 *>(Xc + (abase[i] ^ ((8u * q + s) << 4)));
-#pragma unroll
-        for (int i = 0; i < FM; ++i)
-#pragma unroll
-          for (int j = 0; j < FN; ++j) acc[i][j] = mfma32<XT>(bq[j][s], af[i], acc[i][j]);
-      }
-    }
-    // before the y stores: the wait for sprev then covers only older loads
-    if (spend) {
-#pragma unroll
-      for (int i = 0; i < NS; ++i)
-        *reinterpret_cast<uint4 *>(sS + (gstage ^ 1) * SBYTES + sd_[i]) = sprev[i];
-    }
-    spend = snext;
-    bool stored = false;
-    if (C.valid && C.kt == C.nk - 1) {
-      stored = epilogue(C);
-      zero_acc();
-      if (!stored) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    }
-    if (stored) {
-      wait_vm_barrier<NW + NS + NST>();
-    } else {
-      wait_vm_barrier<NW + NS>();
-    }
-    mm_step(ops, C, u_end);
-    if (C.valid && (C.kt & 3) == 0) gstage ^= 1;
-  };
-  for (int64_t j = 0; j < nsteps; j += 6) {
-    step(sX0, sW0, sX1, sW2, sb, sa);
-    step(sX1, sW1, sX0, sW0, sa, sb);
-    step(sX0, sW2, sX1, sW1, sb, sa);
-    step(sX1, sW0, sX0, sW2, sa, sb);
-    step(sX0, sW1, sX1, sW0, sb, sa);
-    step(sX1, sW2, sX0, sW1, sa, sb);
-  }
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-#endif  // __HIP_DEVICE_COMPILE__
-}
-
 template <int QT, int XT, int YT>
 hipError_t launch_multi_q(int cfg, const MMOp *ops, int nops, const int64_t *wg, int groups,
                           hipStream_t s) {
@@ -1410,8 +969,7 @@ hipError_t launch_multi_q(int cfg, const MMOp *ops, int nops, const int64_t *wg,
       mm_ldsw_kernel<QT, XT, YT, 1><<<groups, 256, 0, s>>>(ops, nops, wg, groups);
       break;
     case 6:
-      mm_lds2_kernel<QT, XT, YT><<<groups, 256, 0, s>>>(ops, nops, wg, groups);
-      break;
+      return launch_lds2(QT, XT, YT, ops, nops, wg, groups, s);
     case 1:
       mm_breg_kernel<QT, XT, YT, 128, 1><<<groups, 256, 0, s>>>(ops, nops, wg, groups);
       break;
