@@ -45,8 +45,12 @@ def log(*a):
 def parse():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--warmup-seconds", type=float, default=0.5,
+                    help="keep warming up until this much time has passed as well (the "
+                         "GPU takes some tens of milliseconds of load to reach its "
+                         "steady clock)")
     ap.add_argument("--workload", default="q4_0_decode_7b")
     ap.add_argument("--cpu-layers", type=int, default=None, help="layers in the oracle sample")
     ap.add_argument("--cpu-rows", type=int, default=None, help="activation rows in the oracle sample")
@@ -136,9 +140,14 @@ def main():
     mfma_bound = wl.m >= 512
 
     # ---- timed region: K graph-replayed passes -----------------------------
-    for _ in range(args.warmup):
+    warm, t_warm = 0, time.time()
+    while warm < args.warmup or time.time() - t_warm < args.warmup_seconds:
         eb.qlinear_stack(ops)
+        warm += 1
+        if warm % 8 == 0:
+            torch.cuda.synchronize()
     torch.cuda.synchronize()
+    args.warmup = warm
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
     for _ in range(args.steps):
