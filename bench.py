@@ -54,6 +54,8 @@ def parse():
     ap.add_argument("--workload", default="q4_0_decode_7b")
     ap.add_argument("--cpu-layers", type=int, default=None, help="layers in the oracle sample")
     ap.add_argument("--cpu-rows", type=int, default=None, help="activation rows in the oracle sample")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="oracle time the CPU baseline sample is sized to")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="first run a plain device-to-device copy of BYTES (for scaling "
@@ -241,7 +243,10 @@ def main():
 
 def cpu_baseline(args, wl, W, dev, mfma_bound):
     """Time the CPU oracle (binary64 qlinear over its own quantization of the
-    same seeded weights) on the first few layers / rows of the workload."""
+    same seeded weights) on a bounded sample of the workload: its projections
+    layer by layer (cycling over the layers already quantized when the
+    workload is shorter than the time target) on the first rows of x, until
+    about --cpu-seconds of timed oracle work has been done."""
     import numpy as np
     import torch
 
@@ -249,26 +254,44 @@ def cpu_baseline(args, wl, W, dev, mfma_bound):
 
     orc = O.get()
     cores = min(O.available_cores(), MAX_HOST_THREADS)
-    layers = args.cpu_layers or (32 if wl.m == 1 else 1)
-    layers = min(layers, wl.layers)
+    max_layers = min(args.cpu_layers or wl.layers, wl.layers)
     rows = min(args.cpu_rows or (wl.m if wl.m <= 8 else 8), wl.m)
     qt = O.Q8_0 if wl.qtype == "q8_0" else O.Q4_0
     xt = O.X_F16 if wl.x_dtype == torch.float16 else O.X_BF16
-    secs, nbytes, flops = 0.0, 0, 0
-    for layer in range(layers):
+    cache, cache_bytes = [], 0
+    secs, nbytes, flops, ops, layers_seen = 0.0, 0, 0, 0, 0
+
+    def run(blocks, xb, n, k):
+        nonlocal secs, nbytes, flops, ops
+        t = time.perf_counter()
+        orc.qlinear(qt, blocks, n, k, xb, xt, nthreads=cores)
+        secs += time.perf_counter() - t
+        nbytes += op_bytes(wl.qtype, rows, n, k)
+        flops += 2 * rows * n * k
+        ops += 1
+
+    for layer in range(max_layers):
+        if secs >= args.cpu_seconds:
+            break
+        layers_seen += 1
         for p, (_, k, n) in enumerate(wl.projections):
             w = W.weights(wl, layer, p, dev).cpu().numpy()
             x = W.activations(wl, layer, p, dev)[:rows]
             xb = x.cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
             blocks = orc.quantize(qt, w, nthreads=cores)  # untimed: weights load once
             del w
-            t = time.perf_counter()
-            orc.qlinear(qt, blocks, n, k, xb, xt, nthreads=cores)
-            secs += time.perf_counter() - t
-            nbytes += op_bytes(wl.qtype, rows, n, k)
-            flops += 2 * rows * n * k
-    sample = (f"{layers} of {wl.layers} layers x {len(wl.projections)} projections, "
-              f"{rows} of {wl.m} activation rows, 1 step; {secs:.2f}s wall")
+            run(blocks, xb, n, k)
+            if cache_bytes + blocks.nbytes <= (2 << 30):
+                cache.append((blocks, xb, n, k))
+                cache_bytes += blocks.nbytes
+    while secs < args.cpu_seconds and cache:
+        for blocks, xb, n, k in cache:
+            run(blocks, xb, n, k)
+            if secs >= args.cpu_seconds:
+                break
+    sample = (f"{ops} projection calls over the first {layers_seen} of {wl.layers} layers "
+              f"({len(wl.projections)} projections each, cycling), {rows} of {wl.m} "
+              f"activation rows; {secs:.1f}s of oracle time")
     log(f"[bench] cpu oracle: {sample}")
     if mfma_bound:
         return {"value": round(flops / secs / 1e12, 6), "unit": "TFLOP/s", "cores": cores,
