@@ -209,6 +209,9 @@ struct Step {
   int64_t units = 0, rows = 0;
   int mm_cfg = 0, groups = 0;
   size_t wg = 0;      // first entry of the workgroup ranges
+  bool gm = false;    // grouped MFMA launch (op == -1): table entries from `table`,
+  size_t order = 0;   // workgroup entries from `order`
+  int64_t entries = 0;
 };
 
 struct Plan {
@@ -216,6 +219,8 @@ struct Plan {
   M1Op *table = nullptr;  // device copy of every fused GEMV launch's op table
   MMOp *mmtable = nullptr;  // same for fused MFMA launches
   int64_t *mmwg = nullptr;  // their workgroup unit ranges
+  GOp *gmtable = nullptr;   // grouped MFMA launches: op table
+  int2 *gmorder = nullptr;  // and workgroup (op, tile) entries
   float *ws = nullptr;    // split-K workspace shared by the plan's MFMA steps (run in order)
   size_t ws_bytes = 0;
   hipGraph_t graph = nullptr;
@@ -243,6 +248,13 @@ int64_t mm_max_m() {
   return v;
 }
 
+// MFMA ops with more rows than a fused small-m launch takes, which may share a
+// grouped launch (EB_STACK_GROUP=0 turns that off).
+bool gm_fusable(const eb_qlinear_op &o) {
+  return o.m > mm_max_m() && !env_off("EB_STACK_GROUP") &&
+         pick_path(o.w.type, o.x_type, o.m, o.w.n, o.w.k) == EB_PATH_MFMA;
+}
+
 bool mm_fusable(const eb_qlinear_op &o) {
   return o.m >= 1 && o.m <= mm_max_m() && o.w.k < kMMaxK &&
          (o.m + 256) * o.w.n * (int64_t)dsize(o.y_type) < (int64_t(1) << 31) &&
@@ -255,9 +267,63 @@ eb_status build_plan(const eb_qlinear_op *ops, int32_t n_ops, bool alloc, Plan &
   std::vector<M1Op> host;
   std::vector<MMOp> mmhost;
   std::vector<int64_t> mmwg;
+  std::vector<GOp> gmhost;
+  std::vector<int2> gmorder;
   const bool fuse = !env_off("EB_STACK_FUSE");
   int32_t i = 0;
   while (i < n_ops) {
+    if (fuse && gm_fusable(ops[i])) {
+      // run of independent large-m MFMA ops with the same weight and x formats
+      std::vector<OpSpan> spans{span_of(ops[i])};
+      int32_t j = i + 1;
+      for (; j < n_ops; ++j) {
+        const eb_qlinear_op &o = ops[j];
+        if (!gm_fusable(o) || o.w.type != ops[i].w.type || o.x_type != ops[i].x_type) break;
+        const OpSpan sj = span_of(o);
+        bool ok = true;
+        for (const OpSpan &sp : spans) ok = ok && independent(sp, sj);
+        if (!ok) break;
+        spans.push_back(sj);
+      }
+      if (j - i > 1) {
+        std::vector<GOp> run;
+        for (int32_t r = i; r < j; ++r) {
+          const eb_qlinear_op &o = ops[r];
+          const Layout L = layout_of(o.w.type, o.w.n, o.w.k);
+          GOp e{};
+          e.w = static_cast<const uint8_t *>(o.w.data);
+          e.x = static_cast<const uint16_t *>(o.x);
+          e.y = o.y;
+          e.n = o.w.n;
+          e.k = o.w.k;
+          e.d_off = L.d_off;
+          e.ds = L.ds;
+          e.m = o.m;
+          e.yt = o.y_type;
+          run.push_back(e);
+        }
+        std::vector<int2> order;
+        const int cfg = plan_grouped(ops[i].w.type, run, order);
+        if (cfg >= 0) {
+          for (int2 &e : order)
+            if (e.x >= 0) e.x += (int)gmhost.size();
+          Step s;
+          s.gm = true;
+          s.type = ops[i].w.type;
+          s.xt = ops[i].x_type;
+          s.mm_cfg = cfg;
+          s.table = gmhost.size();
+          s.nops = (int)run.size();
+          s.order = gmorder.size();
+          s.entries = (int64_t)order.size();
+          gmhost.insert(gmhost.end(), run.begin(), run.end());
+          gmorder.insert(gmorder.end(), order.begin(), order.end());
+          P.steps.push_back(s);
+          i = j;
+          continue;
+        }
+      }
+    }
     if (fuse && mm_fusable(ops[i])) {
       // run of independent small-m MFMA ops with the same formats
       std::vector<OpSpan> spans{span_of(ops[i])};
@@ -385,6 +451,21 @@ eb_status build_plan(const eb_qlinear_op *ops, int32_t n_ops, bool alloc, Plan &
             hipSuccess)
       return EB_ERR_HIP;
   }
+  if (alloc && !gmhost.empty()) {
+    if (hipMalloc((void **)&P.gmtable, gmhost.size() * sizeof(GOp)) != hipSuccess) {
+      P.gmtable = nullptr;
+      return EB_ERR_HIP;
+    }
+    if (hipMalloc((void **)&P.gmorder, gmorder.size() * sizeof(int2)) != hipSuccess) {
+      P.gmorder = nullptr;
+      return EB_ERR_HIP;
+    }
+    if (hipMemcpy(P.gmtable, gmhost.data(), gmhost.size() * sizeof(GOp), hipMemcpyHostToDevice) !=
+            hipSuccess ||
+        hipMemcpy(P.gmorder, gmorder.data(), gmorder.size() * sizeof(int2),
+                  hipMemcpyHostToDevice) != hipSuccess)
+      return EB_ERR_HIP;
+  }
   for (Step &s : P.steps) {
     if (s.op < 0) continue;
     const eb_qlinear_op &o = ops[s.op];
@@ -411,7 +492,12 @@ eb_status build_plan(const eb_qlinear_op *ops, int32_t n_ops, bool alloc, Plan &
 
 eb_status run_plan(const eb_qlinear_op *ops, const Plan &P, hipStream_t s) {
   for (const Step &st : P.steps) {
-    if (st.mm) {
+    if (st.gm) {
+      // the table entries index the whole plan's op table
+      if (launch_mfma_grouped(st.type, st.xt, st.mm_cfg, P.gmtable, P.gmorder + st.order,
+                              st.entries, s) != hipSuccess)
+        return EB_ERR_HIP;
+    } else if (st.mm) {
       if (launch_mfma_multi(st.type, st.xt, st.yt, st.mm_cfg, P.mmtable + st.table, st.nops,
                             P.mmwg + st.wg, st.groups, s) != hipSuccess)
         return EB_ERR_HIP;
@@ -438,6 +524,8 @@ void destroy_plan(Plan &p) {
   if (p.table) (void)hipFree(p.table);
   if (p.mmtable) (void)hipFree(p.mmtable);
   if (p.mmwg) (void)hipFree(p.mmwg);
+  if (p.gmtable) (void)hipFree(p.gmtable);
+  if (p.gmorder) (void)hipFree(p.gmorder);
   if (p.ws) (void)hipFree(p.ws);
   p = Plan();
 }
@@ -572,6 +660,7 @@ eb_status eb_qlinear_stack(const eb_qlinear_op *ops, int32_t n_ops, hipStream_t 
   std::string key(reinterpret_cast<const char *>(&dev), sizeof(dev));
   key.push_back(use_graph ? 'g' : 'd');
   key.push_back(env_off("EB_STACK_FUSE") ? 'u' : 'f');
+  key.push_back(env_off("EB_STACK_GROUP") ? 'n' : 'g');
   const int fk = mfma_force_key();
   key.append(reinterpret_cast<const char *>(&fk), sizeof(fk));
   key.append(reinterpret_cast<const char *>(ops), sizeof(eb_qlinear_op) * (size_t)n_ops);

@@ -91,6 +91,22 @@ hipError_t launch_mfma(int32_t type, const void *wdata, int64_t n, int64_t k, co
                        hipStream_t s);
 int mfma_tile_count();
 
+// Grouped MFMA launch over independent ops with more rows than a fused
+// small-m launch takes: one workgroup per output tile of any op, in a table
+// ordered longest tiles first (section 3.2: fewer, fuller launches).
+struct GOp {
+  const uint8_t *w;   // quantized weights (planar layout)
+  const uint16_t *x;  // activations [m][k]
+  void *y;            // outputs [m][n]
+  int64_t n, k, d_off, ds, m;
+  int32_t yt, pad;
+};
+// Chooses the tile configuration for the group and fills the workgroup table
+// (op, tile); returns the configuration, or -1 when none fits every op.
+int plan_grouped(int32_t type, const std::vector<GOp> &ops, std::vector<int2> &order);
+hipError_t launch_mfma_grouped(int32_t type, int32_t xt, int cfg, const GOp *ops, const int2 *order,
+                                int64_t entries, hipStream_t s);
+
 // Fused MFMA launch over several independent ops of a stack: one persistent
 // launch whose workgroups each run a contiguous range of output tiles
 // (units), balanced by K-tile steps, as one continuous load/compute pipeline.

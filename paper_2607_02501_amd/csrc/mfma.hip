@@ -34,6 +34,8 @@
 #include <atomic>
 #include <cmath>
 #include <cstdlib>
+#include <iterator>
+#include <vector>
 
 #include "eb_internal.h"
 #include "mfma_common.h"
@@ -42,11 +44,37 @@
 namespace eb {
 namespace {
 
-template <int QT, int XT, int BM, int BN, int WM, int WN>
+// G: grouped launch over several independent ops -- workgroup b runs tile
+// gorder[b].y of op gorder[b].x (entries with a negative op do nothing), with
+// the op's operands from gops; the scalar arguments are then unused.
+template <int QT, int XT, int BM, int BN, int WM, int WN, bool G = false>
 __global__ void __launch_bounds__(WM *WN * 64)
-    mfma_kernel(const uint8_t *__restrict__ wdata, int64_t n, int64_t k, int64_t d_off, int64_t ds,
-                const uint16_t *__restrict__ x, int64_t m, void *__restrict__ y, int yt, int kts,
-                float *__restrict__ ws, int64_t ws_stride) {
+    mfma_kernel(const uint8_t *__restrict__ wdata_, int64_t n_, int64_t k_, int64_t d_off_,
+                int64_t ds_, const uint16_t *__restrict__ x_, int64_t m_, void *__restrict__ y_,
+                int yt_, int kts_, float *__restrict__ ws, int64_t ws_stride,
+                const GOp *__restrict__ gops, const int2 *__restrict__ gorder) {
+  const uint8_t *wdata = wdata_;
+  const uint16_t *x = x_;
+  void *y = y_;
+  int64_t n = n_, k = k_, d_off = d_off_, ds = ds_, m = m_;
+  int yt = yt_, kts = kts_;
+  int64_t gtile = 0;
+  if constexpr (G) {
+    const int2 e = gorder[blockIdx.x];
+    if (e.x < 0) return;
+    const GOp &o = gops[e.x];
+    wdata = o.w;
+    x = o.x;
+    y = o.y;
+    n = o.n;
+    k = o.k;
+    d_off = o.d_off;
+    ds = o.ds;
+    m = o.m;
+    yt = o.yt;
+    kts = (int)((k + kBK - 1) / kBK);
+    gtile = e.y;
+  }
   constexpr int T = WM * WN * 64;
   constexpr int WAVES = WM * WN;
   constexpr int TM = BM / WM, TN = BN / WN;        // wave sub-tile
@@ -81,11 +109,11 @@ __global__ void __launch_bounds__(WM *WN * 64)
   // writes its fp32 partial tile to ws + s ws_stride; a second kernel sums them.
   const int64_t tiles_m = (m + BM - 1) / BM, tiles_n = (n + BN - 1) / BN;
   const int64_t tiles = tiles_m * tiles_n;
-  const int split = (int)(blockIdx.x / tiles);
-  const int64_t bid = blockIdx.x % tiles;
-  // XCD-aware tile order
-  int64_t t = bid;
-  if (tiles % kXcds == 0) t = (bid % kXcds) * (tiles / kXcds) + bid / kXcds;
+  const int split = G ? 0 : (int)(blockIdx.x / tiles);
+  const int64_t bid = G ? 0 : blockIdx.x % tiles;
+  // XCD-aware tile order (a grouped launch's table is already in that order)
+  int64_t t = G ? gtile : bid;
+  if (!G && tiles % kXcds == 0) t = (bid % kXcds) * (tiles / kXcds) + bid / kXcds;
   const int64_t tm = t / tiles_n, tn = t % tiles_n;
   const int64_t m0 = tm * BM, n0 = tn * BN;
   const int64_t nb = k / kQK;
@@ -318,7 +346,15 @@ hipError_t launch_t(const void *wdata, int64_t n, int64_t k, const void *x, int6
   if (!fits_offsets<QT, BM, BN>(n, k)) return hipErrorInvalidValue;
   mfma_kernel<QT, XT, BM, BN, WM, WN><<<(unsigned)(tiles * splits), WM * WN * 64, 0, s>>>(
       (const uint8_t *)wdata, n, k, L.d_off, L.ds, (const uint16_t *)x, m, y, yt, kts,
-      splits > 1 ? ws : nullptr, ws_stride);
+      splits > 1 ? ws : nullptr, ws_stride, nullptr, nullptr);
+  return hipGetLastError();
+}
+
+template <int QT, int XT, int BM, int BN, int WM, int WN>
+hipError_t launch_g(const GOp *ops, const int2 *order, int64_t entries, hipStream_t s) {
+  if (entries <= 0 || entries > 0x7fffffff) return hipErrorInvalidValue;
+  mfma_kernel<QT, XT, BM, BN, WM, WN, true><<<(unsigned)entries, WM * WN * 64, 0, s>>>(
+      nullptr, 0, 0, 0, 0, nullptr, 0, nullptr, 0, 0, nullptr, 0, ops, order);
   return hipGetLastError();
 }
 
@@ -468,7 +504,69 @@ MfmaPlan plan_mfma(int32_t type, int64_t m, int64_t n, int64_t k, bool allow_spl
   return best;
 }
 
+// Configurations a grouped launch may use (instantiated with G = true).
+constexpr int kGroupCfgs[] = {1, 2, 4, 6};
+
+int plan_grouped(int32_t type, const std::vector<GOp> &ops, std::vector<int2> &order) {
+  const int cus = device_cu_count();
+  const int fc = forced_cfg();
+  int best = -1;
+  double best_t = 0;
+  for (int c : kGroupCfgs) {
+    if (fc >= 0 && fc < kNumCfgs && c != fc &&
+        std::find(std::begin(kGroupCfgs), std::end(kGroupCfgs), fc) != std::end(kGroupCfgs))
+      continue;
+    const Cfg &g = kCfgs[c];
+    bool fits = true;
+    double work = 0, longest = 0;
+    for (const GOp &o : ops) {
+      fits = fits && (type == EB_Q4_0 ? fits_offsets<EB_Q4_0, 0, 0>(o.n, o.k, g.bm, g.bn)
+                                      : fits_offsets<EB_Q8_0, 0, 0>(o.n, o.k, g.bm, g.bn));
+      const double nk = (double)((o.k + kBK - 1) / kBK);
+      work += (double)(((o.m + g.bm - 1) / g.bm) * ((o.n + g.bn - 1) / g.bn)) * nk;
+      longest = std::max(longest, nk);
+    }
+    if (!fits) continue;
+    // padded tile work at the configuration's rate, plus half a longest tile of tail
+    const double step_s = 2.0 * g.bm * g.bn * kBK / (g.rate * 1e12);
+    const double t = work * step_s + 0.5 * longest * step_s * cus * g.per_cu;
+    if (best < 0 || t < best_t) {
+      best = c;
+      best_t = t;
+    }
+  }
+  if (best < 0) return -1;
+  const Cfg &g = kCfgs[best];
+  // longest tiles first; each op's tiles start at a multiple of 8 entries and
+  // run in the XCD-aware order of the single-op launch
+  std::vector<int> idx(ops.size());
+  for (size_t i = 0; i < ops.size(); ++i) idx[i] = (int)i;
+  std::stable_sort(idx.begin(), idx.end(), [&](int a, int b) { return ops[a].k > ops[b].k; });
+  order.clear();
+  for (int oi : idx) {
+    const GOp &o = ops[oi];
+    const int64_t tiles = ((o.m + g.bm - 1) / g.bm) * ((o.n + g.bn - 1) / g.bn);
+    for (int64_t b = 0; b < tiles; ++b) {
+      const int64_t t = tiles % kXcds == 0 ? (b % kXcds) * (tiles / kXcds) + b / kXcds : b;
+      order.push_back(make_int2(oi, (int)t));
+    }
+    while (order.size() % kXcds) order.push_back(make_int2(-1, 0));
+  }
+  return best;
+}
+
 namespace {
+
+template <int QT, int XT>
+hipError_t launch_gq(int cfg, const GOp *ops, const int2 *order, int64_t entries, hipStream_t s) {
+  switch (cfg) {
+    case 1: return launch_g<QT, XT, 128, 128, 2, 2>(ops, order, entries, s);
+    case 2: return launch_g<QT, XT, 128, 256, 2, 4>(ops, order, entries, s);
+    case 4: return launch_g<QT, XT, 256, 192, 4, 2>(ops, order, entries, s);
+    case 6: return launch_g<QT, XT, 256, 256, 2, 4>(ops, order, entries, s);
+    default: return hipErrorInvalidValue;
+  }
+}
 
 template <int QT, int XT>
 hipError_t launch_q(const void *wdata, int64_t n, int64_t k, const void *x, int64_t m, void *y,
@@ -505,6 +603,16 @@ hipError_t launch_mfma(int32_t type, const void *wdata, int64_t n, int64_t k, co
   }
   if (xt == EB_F16) return launch_q<EB_Q8_0, EB_F16>(wdata, n, k, x, m, y, yt, plan, ws, s);
   return launch_q<EB_Q8_0, EB_BF16>(wdata, n, k, x, m, y, yt, plan, ws, s);
+}
+
+hipError_t launch_mfma_grouped(int32_t type, int32_t xt, int cfg, const GOp *ops, const int2 *order,
+                                int64_t entries, hipStream_t s) {
+  if (type == EB_Q4_0) {
+    if (xt == EB_F16) return launch_gq<EB_Q4_0, EB_F16>(cfg, ops, order, entries, s);
+    return launch_gq<EB_Q4_0, EB_BF16>(cfg, ops, order, entries, s);
+  }
+  if (xt == EB_F16) return launch_gq<EB_Q8_0, EB_F16>(cfg, ops, order, entries, s);
+  return launch_gq<EB_Q8_0, EB_BF16>(cfg, ops, order, entries, s);
 }
 
 }  // namespace eb

@@ -285,3 +285,26 @@ def test_stack_fuses_independent_small_m_mfma_ops(eb, monkeypatch):
     assert _launches(eb, raw) == _launches(eb, raw[:1]) + _launches(eb, raw[1:])
     monkeypatch.setenv("EB_STACK_FUSE", "0")
     assert _launches(eb, ops) == 8 * _launches(eb, ops[:1])
+
+
+def test_stack_groups_independent_large_m_mfma_ops(eb, monkeypatch):
+    monkeypatch.delenv("EB_STACK_FUSE", raising=False)
+    monkeypatch.delenv("EB_STACK_GROUP", raising=False)
+    bf = eb.EB_BF16
+    # four projections of one layer with large m: one grouped launch, output
+    # types may differ within it
+    shapes = [(2048, 2560), (2048, 2048), (2048, 32768), (16384, 2048)]
+    ops = [_op(eb, (1 + 2 * i) * GB, 16 * GB + i * GB, 24 * GB + i * GB, k=k, n=n, m=816,
+               qtype=eb.EB_Q8_0, xt=bf, yt=(bf if i == 1 else eb.EB_F32))
+           for i, (k, n) in enumerate(shapes)]
+    assert _launches(eb, ops) == 1
+    # a different activation format starts a new group
+    f16 = _op(eb, 12 * GB, 40 * GB, 41 * GB, k=2048, n=2048, m=816, qtype=eb.EB_Q8_0,
+              xt=eb.EB_F16)
+    assert _launches(eb, ops[:2] + [f16] + ops[2:]) == 2 + _launches(eb, [f16])
+    # read-after-write: the second op reads the first one's output
+    raw = [_op(eb, 1 * GB, 8 * GB, 9 * GB, k=1024, n=1024, m=512, qtype=eb.EB_Q4_0, xt=bf, yt=bf),
+           _op(eb, 2 * GB, 9 * GB, 10 * GB, k=1024, n=1024, m=512, qtype=eb.EB_Q4_0, xt=bf)]
+    assert _launches(eb, raw) == _launches(eb, raw[:1]) + _launches(eb, raw[1:])
+    monkeypatch.setenv("EB_STACK_GROUP", "0")
+    assert _launches(eb, ops) == sum(_launches(eb, [o]) for o in ops)

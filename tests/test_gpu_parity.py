@@ -337,6 +337,53 @@ def test_fused_mfma_stack(eb, oracle, qtype, xdtype, ydtype, ms, monkeypatch):
     eb.stack_cache_clear()
 
 
+@pytest.mark.parametrize("qtype,xdtype,ms", [
+    ("q8_0", torch.bfloat16, (129, 300, 257, 520)),
+    ("q4_0", torch.float16, (816, 130, 200, 384)),
+])
+def test_grouped_mfma_stack(eb, oracle, qtype, xdtype, ms, monkeypatch):
+    """Independent large-m MFMA ops run as one grouped launch of the tile
+    kernel: every output within the oracle bound, the same bits on every run
+    and in every stack mode, and bit-identical to unsplit single calls (same
+    per-output summation order)."""
+    monkeypatch.delenv("EB_STACK_FUSE", raising=False)
+    monkeypatch.delenv("EB_STACK_GROUP", raising=False)
+    shapes = [(300, 1056), (128, 96), (1000, 2080), (130, 4096)]  # odd block counts, ragged n
+    ydt = [torch.float32, torch.bfloat16, torch.float32, torch.bfloat16]
+    entries, cases = [], []
+    for i, ((n, k), m) in enumerate(zip(shapes, ms)):
+        w, x = _case(950 + i, n, k, m, xdtype)
+        qw = eb.quantize(w.to(DEV), qtype)
+        y = torch.full((m, n), float("nan"), device=DEV, dtype=ydt[i])
+        entries.append((qw, x.to(DEV), y))
+        cases.append((w, x))
+    ops = eb.make_ops(entries)
+    assert eb.stack_launches(ops) == 1
+    first = None
+    for mode in ("1", "1", "0"):  # capture, replay, direct
+        monkeypatch.setenv("EB_STACK_GRAPH", mode)
+        for _, _, y in entries:
+            y.fill_(float("nan"))
+        eb.qlinear_stack(ops)
+        torch.cuda.synchronize()
+        outs = [y.clone() for _, _, y in entries]
+        if first is None:
+            first = outs
+        for a, b in zip(first, outs):
+            assert torch.equal(a, b)
+    eb.mfma_force(-1, 1)
+    try:
+        for (w, x), (qw, xd, y) in zip(cases, entries):
+            tol = TOL_F32 if y.dtype == torch.float32 else TOL_BF16
+            _, y_ref, bound = oracle_reference(oracle, qtype, w.numpy(), x)
+            assert_parity(y, y_ref, bound, tol, f"grouped m={x.shape[0]}")
+            single = eb.qlinear(qw, xd, out_dtype=y.dtype, path="mfma")
+            assert torch.equal(y, single)
+    finally:
+        eb.mfma_force(-1, 0)
+    eb.stack_cache_clear()
+
+
 def test_stack_dependent_chain(eb, oracle, monkeypatch):
     """op 1 reads op 0's bf16 output: the plan must not fuse them."""
     monkeypatch.delenv("EB_STACK_FUSE", raising=False)
