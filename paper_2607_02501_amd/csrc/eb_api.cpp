@@ -270,6 +270,46 @@ eb_status build_plan(const eb_qlinear_op *ops, int32_t n_ops, bool alloc, Plan &
   std::vector<GOp> gmhost;
   std::vector<int2> gmorder;
   const bool fuse = !env_off("EB_STACK_FUSE");
+  // one fused small-m launch over `list` (same weight, x and y formats)
+  auto add_mm_step = [&](const std::vector<eb_qlinear_op> &list) {
+    int64_t max_m = 0;
+    for (const eb_qlinear_op &o : list) max_m = std::max(max_m, o.m);
+    Step s;
+    s.mm = true;
+    s.type = list[0].w.type;
+    s.xt = list[0].x_type;
+    s.yt = list[0].y_type;
+    s.mm_cfg = mm_cfg(max_m);
+    s.table = mmhost.size();
+    std::vector<MMOp> run;
+    int64_t units = 0;
+    for (const eb_qlinear_op &o : list) {
+      const Layout L = layout_of(o.w.type, o.w.n, o.w.k);
+      MMOp e{};
+      e.w = static_cast<const uint8_t *>(o.w.data);
+      e.x = static_cast<const uint16_t *>(o.x);
+      e.y = o.y;
+      e.d_off = L.d_off;
+      units += mm_tiles(s.mm_cfg, o.m, o.w.n);
+      e.unit_end = units;
+      e.ds = (int32_t)L.ds;
+      e.m = (int32_t)o.m;
+      e.n = (int32_t)o.w.n;
+      e.k = (int32_t)o.w.k;
+      e.tiles_n = (int32_t)mm_tiles(s.mm_cfg, 1, o.w.n);
+      e.nk = (int32_t)((o.w.k + mm_bk(s.mm_cfg) - 1) / mm_bk(s.mm_cfg));
+      e.yt = o.y_type;
+      run.push_back(e);
+    }
+    std::vector<int64_t> wg;
+    s.groups = mm_partition(run, s.mm_cfg, wg);
+    s.nops = (int)run.size();
+    s.units = units;
+    s.wg = mmwg.size();
+    mmhost.insert(mmhost.end(), run.begin(), run.end());
+    mmwg.insert(mmwg.end(), wg.begin(), wg.end());
+    P.steps.push_back(s);
+  };
   int32_t i = 0;
   while (i < n_ops) {
     if (fuse && gm_fusable(ops[i])) {
@@ -286,24 +326,69 @@ eb_status build_plan(const eb_qlinear_op *ops, int32_t n_ops, bool alloc, Plan &
         spans.push_back(sj);
       }
       if (j - i > 1) {
-        std::vector<GOp> run;
-        for (int32_t r = i; r < j; ++r) {
-          const eb_qlinear_op &o = ops[r];
-          const Layout L = layout_of(o.w.type, o.w.n, o.w.k);
-          GOp e{};
-          e.w = static_cast<const uint8_t *>(o.w.data);
-          e.x = static_cast<const uint16_t *>(o.x);
-          e.y = o.y;
-          e.n = o.w.n;
-          e.k = o.w.k;
-          e.d_off = L.d_off;
-          e.ds = L.ds;
-          e.m = o.m;
-          e.yt = o.y_type;
-          run.push_back(e);
-        }
+        auto gops_of = [](const std::vector<eb_qlinear_op> &list) {
+          std::vector<GOp> run;
+          for (const eb_qlinear_op &o : list) {
+            const Layout L = layout_of(o.w.type, o.w.n, o.w.k);
+            GOp e{};
+            e.w = static_cast<const uint8_t *>(o.w.data);
+            e.x = static_cast<const uint16_t *>(o.x);
+            e.y = o.y;
+            e.n = o.w.n;
+            e.k = o.w.k;
+            e.d_off = L.d_off;
+            e.ds = L.ds;
+            e.m = o.m;
+            e.yt = o.y_type;
+            run.push_back(e);
+          }
+          return run;
+        };
+        std::vector<eb_qlinear_op> mains(ops + i, ops + j), tails;
+        std::vector<GOp> run = gops_of(mains);
         std::vector<int2> order;
-        const int cfg = plan_grouped(ops[i].w.type, run, order);
+        int cfg = plan_grouped(ops[i].w.type, run, order);
+        // An op whose last row tile would be mostly padding (m = 816 in
+        // 256-row tiles: 48 rows) gives those rows to a fused small-m launch
+        // when the padded MFMA work saved outweighs reading its weights again.
+        if (cfg >= 0 && !env_off("EB_STACK_SPLIT_TAIL")) {
+          const int64_t bm = mfma_cfg_bm(cfg);
+          const double rate = mfma_cfg_rate(cfg) * 1e12;
+          std::vector<eb_qlinear_op> m2, t2;
+          for (const eb_qlinear_op &o : mains) {
+            const int64_t rem = o.m % bm;
+            eb_qlinear_op t = o;
+            t.m = rem;
+            t.x = static_cast<const uint8_t *>(o.x) + (o.m - rem) * o.w.k * 2;
+            t.y = static_cast<uint8_t *>(o.y) + (o.m - rem) * o.w.n * dsize(o.y_type);
+            bool split = rem > 0 && o.m > bm && mm_fusable(t);
+            if (split) {
+              const double row_flops = 2.0 * o.w.n * o.w.k;
+              const double wbytes =
+                  (double)o.w.n * o.w.k * (o.w.type == EB_Q8_0 ? 34.0 : 18.0) / 32.0;
+              const double saved = (double)(bm - rem) * row_flops / rate;
+              const double cost = std::max(wbytes / 4.5e12, (double)rem * row_flops / 0.35e15);
+              split = saved > 1.2 * cost;
+            }
+            eb_qlinear_op mo = o;
+            if (split) {
+              mo.m = o.m - rem;
+              t2.push_back(t);
+            }
+            m2.push_back(mo);
+          }
+          if (!t2.empty()) {
+            std::vector<int2> order2;
+            std::vector<GOp> run2 = gops_of(m2);
+            const int cfg2 = plan_grouped(ops[i].w.type, run2, order2);
+            if (cfg2 >= 0) {
+              cfg = cfg2;
+              run.swap(run2);
+              order.swap(order2);
+              tails.swap(t2);
+            }
+          }
+        }
         if (cfg >= 0) {
           for (int2 &e : order)
             if (e.x >= 0) e.x += (int)gmhost.size();
@@ -319,6 +404,13 @@ eb_status build_plan(const eb_qlinear_op *ops, int32_t n_ops, bool alloc, Plan &
           gmhost.insert(gmhost.end(), run.begin(), run.end());
           gmorder.insert(gmorder.end(), order.begin(), order.end());
           P.steps.push_back(s);
+          // the split-off rows: one fused launch per output type
+          for (int32_t yt : {EB_F32, EB_BF16, EB_F16}) {
+            std::vector<eb_qlinear_op> cls;
+            for (const eb_qlinear_op &t : tails)
+              if (t.y_type == yt) cls.push_back(t);
+            if (!cls.empty()) add_mm_step(cls);
+          }
           i = j;
           continue;
         }
@@ -345,44 +437,7 @@ eb_status build_plan(const eb_qlinear_op *ops, int32_t n_ops, bool alloc, Plan &
         P.steps.push_back(s);
         continue;
       }
-      int64_t max_m = 0;
-      for (int32_t r = i; r < j; ++r) max_m = std::max(max_m, ops[r].m);
-      Step s;
-      s.mm = true;
-      s.type = ops[i].w.type;
-      s.xt = ops[i].x_type;
-      s.yt = ops[i].y_type;
-      s.mm_cfg = mm_cfg(max_m);
-      s.table = mmhost.size();
-      std::vector<MMOp> run;
-      int64_t units = 0;
-      for (int32_t r = i; r < j; ++r) {
-        const eb_qlinear_op &o = ops[r];
-        const Layout L = layout_of(o.w.type, o.w.n, o.w.k);
-        MMOp e{};
-        e.w = static_cast<const uint8_t *>(o.w.data);
-        e.x = static_cast<const uint16_t *>(o.x);
-        e.y = o.y;
-        e.d_off = L.d_off;
-        units += mm_tiles(s.mm_cfg, o.m, o.w.n);
-        e.unit_end = units;
-        e.ds = (int32_t)L.ds;
-        e.m = (int32_t)o.m;
-        e.n = (int32_t)o.w.n;
-        e.k = (int32_t)o.w.k;
-        e.tiles_n = (int32_t)mm_tiles(s.mm_cfg, 1, o.w.n);
-        e.nk = (int32_t)((o.w.k + mm_bk(s.mm_cfg) - 1) / mm_bk(s.mm_cfg));
-        e.yt = o.y_type;
-        run.push_back(e);
-      }
-      std::vector<int64_t> wg;
-      s.groups = mm_partition(run, s.mm_cfg, wg);
-      s.nops = (int)run.size();
-      s.units = units;
-      s.wg = mmwg.size();
-      mmhost.insert(mmhost.end(), run.begin(), run.end());
-      mmwg.insert(mmwg.end(), wg.begin(), wg.end());
-      P.steps.push_back(s);
+      add_mm_step(std::vector<eb_qlinear_op>(ops + i, ops + j));
       i = j;
       continue;
     }
@@ -661,6 +716,7 @@ eb_status eb_qlinear_stack(const eb_qlinear_op *ops, int32_t n_ops, hipStream_t 
   key.push_back(use_graph ? 'g' : 'd');
   key.push_back(env_off("EB_STACK_FUSE") ? 'u' : 'f');
   key.push_back(env_off("EB_STACK_GROUP") ? 'n' : 'g');
+  key.push_back(env_off("EB_STACK_SPLIT_TAIL") ? 'w' : 's');
   const int fk = mfma_force_key();
   key.append(reinterpret_cast<const char *>(&fk), sizeof(fk));
   key.append(reinterpret_cast<const char *>(ops), sizeof(eb_qlinear_op) * (size_t)n_ops);

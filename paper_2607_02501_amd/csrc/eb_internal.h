@@ -90,6 +90,8 @@ hipError_t launch_mfma(int32_t type, const void *wdata, int64_t n, int64_t k, co
                        int32_t xt, int64_t m, void *y, int32_t yt, const MfmaPlan &plan, float *ws,
                        hipStream_t s);
 int mfma_tile_count();
+int mfma_cfg_bm(int cfg);        // rows of a tile configuration
+double mfma_cfg_rate(int cfg);   // its measured full-chip rate, TFLOP/s
 
 // Grouped MFMA launch over independent ops with more rows than a fused
 // small-m launch takes: one workgroup per output tile of any op, in a table

@@ -452,6 +452,8 @@ double estimate(int32_t type, const Cfg &g, int64_t m, int64_t n, int64_t k, int
 }  // namespace
 
 int mfma_tile_count() { return kNumCfgs; }
+int mfma_cfg_bm(int cfg) { return kCfgs[cfg].bm; }
+double mfma_cfg_rate(int cfg) { return kCfgs[cfg].rate; }
 
 void mfma_force(int cfg, int splits) {
   (void)forced_cfg();

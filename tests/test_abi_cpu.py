@@ -308,3 +308,12 @@ def test_stack_groups_independent_large_m_mfma_ops(eb, monkeypatch):
     assert _launches(eb, raw) == _launches(eb, raw[:1]) + _launches(eb, raw[1:])
     monkeypatch.setenv("EB_STACK_GROUP", "0")
     assert _launches(eb, ops) == sum(_launches(eb, [o]) for o in ops)
+    monkeypatch.delenv("EB_STACK_GROUP")
+    # a whole 18-layer pass picks 256-row tiles; m = 816 leaves 48 rows in the
+    # last row tile, which go to fused small-m launches (one per output type)
+    full = [_op(eb, (1 + 3 * i) * GB, (2 + 3 * i) * GB, (3 + 3 * i) * GB, k=k, n=n, m=816,
+                qtype=eb.EB_Q8_0, xt=bf, yt=(bf if i % 4 == 1 else eb.EB_F32))
+            for i, (k, n) in enumerate(shapes * 18)]
+    assert _launches(eb, full) == 3
+    monkeypatch.setenv("EB_STACK_SPLIT_TAIL", "0")
+    assert _launches(eb, full) == 1
