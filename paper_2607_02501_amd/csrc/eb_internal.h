@@ -126,7 +126,7 @@ constexpr int64_t kMMaxK = int64_t(1) << 22;  // k < this keeps per-tile byte sp
 int mm_cfg(int64_t max_m);                // tile configuration for a run
 int64_t mm_tiles(int cfg, int64_t m, int64_t n);
 int mm_bk(int cfg);                       // k covered by one step of the configuration
-// The 128-wide-step fused kernel (configuration 6), in its own source file.
+// The 128-wide-step fused kernel (configuration 0), in its own source file.
 hipError_t launch_lds2(int32_t type, int32_t xt, int32_t yt, const MMOp *ops, int nops,
                        const int64_t *wg, int groups, hipStream_t s);
 // Fills the unit ranges wg[0..groups] (balanced by steps) for a table whose
