@@ -293,11 +293,17 @@ def cpu_baseline(args, wl, W, dev, mfma_bound):
               f"({len(wl.projections)} projections each, cycling), {rows} of {wl.m} "
               f"activation rows; {secs:.1f}s of oracle time")
     log(f"[bench] cpu oracle: {sample}")
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as fh:
+            model = next((l.split(":", 1)[1].strip() for l in fh if l.startswith("model name")), "")
+    except OSError:
+        pass
     if mfma_bound:
         return {"value": round(flops / secs / 1e12, 6), "unit": "TFLOP/s", "cores": cores,
-                "kind": "oracle", "sample": sample}
+                "kind": "oracle", "sample": sample, "cpu_model": model}
     return {"value": round(nbytes / secs / 1e9, 4), "unit": "GB/s", "cores": cores,
-            "kind": "oracle", "sample": sample}
+            "kind": "oracle", "sample": sample, "cpu_model": model}
 
 
 if __name__ == "__main__":
