@@ -17,3 +17,12 @@ def oracle():
     from oracle import oracle as O
 
     return O.get()
+
+
+def pytest_terminal_summary(terminalreporter):
+    """Worst normalised error per parity-check label of the GPU tests."""
+    mod = sys.modules.get("tests.gpu_helpers")
+    worst = getattr(mod, "WORST", None) if mod else None
+    if worst:
+        terminalreporter.write_line("worst normalised error per check: " + ", ".join(
+            f"{k} {v:.3e}" for k, v in sorted(worst.items())))

@@ -8,9 +8,14 @@ QT = {"q8_0": O.Q8_0, "q4_0": O.Q4_0}
 XT = {torch.float16: O.X_F16, torch.bfloat16: O.X_BF16}
 
 # Error bound of the method: fp32 accumulation of 16-bit inputs, normalised by
-# sum_k |x||w_hat| per output.  A bfloat16 output adds one rounding of |y| <= bound.
+# sum_k |x||w_hat| per output.  A bfloat16 output adds one round-to-nearest of
+# |y| <= bound: bfloat16 keeps 8 significant bits, so up to 2^-8 relative.
 TOL_F32 = 2e-3
-TOL_BF16 = 2e-3 + 2.0 ** -9 * (1 + 2e-3)
+TOL_BF16 = 2e-3 + 2.0 ** -8 * (1 + 2e-3)
+
+# Worst normalised error seen per check label (the text before the first
+# space), printed at the end of the session by conftest.py.
+WORST = {}
 
 
 def bits16(t: torch.Tensor) -> np.ndarray:
@@ -35,6 +40,8 @@ def assert_parity(y_gpu, y_ref, bound, tol, what=""):
     if (~zero).any():
         rel = np.abs(y[~zero] - y_ref[~zero]) / bound[~zero]
         worst = float(rel.max())
+        label = what.split(" ")[0] if what else "unlabelled"
+        WORST[label] = max(WORST.get(label, 0.0), worst)
         assert worst <= tol, f"{what}: max normalised error {worst:.3e} > {tol:.3e}"
         return worst
     return 0.0
