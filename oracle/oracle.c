@@ -43,6 +43,11 @@
  * normalised.  Threads (pthreads) only split the set of outputs; each output
  * is still one sequential binary64 loop.
  *
+ * Layer steps on either side of the product (section 3.2, operator fusion),
+ * each in binary64: rounding to binary16 / bfloat16 (nearest, ties to even),
+ * RMS normalisation h * gamma / sqrt(eps + mean h^2) and the SiLU-gated
+ * product silu(g) * u, silu(t) = t / (1 + exp(-t)).
+ *
  * Build: gcc -O2 -fno-fast-math -ffp-contract=off -shared -fPIC -pthread
  */
 #include <math.h>
@@ -388,4 +393,80 @@ done:
   free(tids);
   free(xd);
   return rc;
+}
+
+/* ---------------------------------------------------------------------- */
+/* The steps on either side of the linear layer in a decoder layer (paper  */
+/* section 3.2: operator fusion on the batch-1 path; the backbones of      */
+/* section 2.1 / Table 1 are decoder stacks): RMS normalisation of the     */
+/* residual stream before a projection, the SiLU-gated product of a        */
+/* gate/up projection pair, and (in the Python layer) the residual         */
+/* addition after a projection.                                            */
+/* ---------------------------------------------------------------------- */
+
+/* Nearest value of a binary floating-point format with p significant bits
+ * (p - 1 stored fraction bits), exponent bias `bias` and normal exponents
+ * 1 - bias .. bias, to v, ties to the even significand, with gradual
+ * underflow and overflow to infinity; returns the 16-bit encoding. */
+static uint16_t round_to_format16(double v, int p, int bias) {
+  const int fb = p - 1;
+  const int emin = 1 - bias, emax = bias;
+  const uint16_t sign = signbit(v) ? 0x8000u : 0u;
+  const uint16_t inf = (uint16_t)((2 * bias + 1) << fb);
+  if (isnan(v)) return (uint16_t)(sign | inf | (1u << (fb - 1)));
+  if (isinf(v)) return (uint16_t)(sign | inf);
+  double a = fabs(v);
+  if (a == 0.0) return sign;
+  /* a lies in [2^E, 2^(E+1)); the format's spacing there is 2^(E - fb), and
+   * below the normal range it stays 2^(emin - fb). */
+  int e2;
+  (void)frexp(a, &e2);
+  int E = e2 - 1;
+  if (E < emin) E = emin;
+  double spacing = ldexp(1.0, E - fb);
+  double r = rint(a / spacing); /* a / spacing is exact; rint rounds ties to even */
+  double q = r * spacing;       /* exact */
+  if (q >= ldexp(1.0, emax + 1)) return (uint16_t)(sign | inf);
+  if (q < ldexp(1.0, emin)) return (uint16_t)(sign | (uint16_t)(q / ldexp(1.0, emin - fb)));
+  int ev;
+  double m = frexp(q, &ev); /* q = m * 2^ev, m in [0.5, 1) */
+  int biased = ev - 1 + bias;
+  int frac = (int)((2.0 * m - 1.0) * (double)(1 << fb));
+  return (uint16_t)(sign | (biased << fb) | frac);
+}
+
+/* out[i] = the binary16 (xtype F16: 11 significant bits, bias 15) or
+ * bfloat16 (BF16: 8 significant bits, bias 127) encoding nearest to v[i]. */
+int oracle_round_x16(const double *v, int64_t count, int xtype, uint16_t *out) {
+  if (count < 0 || (xtype != ORACLE_X_F16 && xtype != ORACLE_X_BF16)) return ORACLE_EINVAL;
+  for (int64_t i = 0; i < count; ++i)
+    out[i] = xtype == ORACLE_X_F16 ? round_to_format16(v[i], 11, 15) : round_to_format16(v[i], 8, 127);
+  return ORACLE_OK;
+}
+
+/* RMS normalisation of every row of h[m][k] (binary32) with per-feature
+ * weights gamma[k]: r_i = 1 / sqrt(eps + (1/k) sum_j h[i][j]^2) and
+ * out[i][j] = h[i][j] * gamma[j] * r_i, all in binary64.  eps >= 0; a row of
+ * zeros needs eps > 0. */
+int oracle_rmsnorm(const float *h, const float *gamma, double eps, int64_t m, int64_t k,
+                   double *out) {
+  if (m < 0 || k <= 0 || !(eps >= 0.0)) return ORACLE_EINVAL;
+  for (int64_t i = 0; i < m; ++i) {
+    const float *row = h + i * k;
+    double ss = 0.0;
+    for (int64_t j = 0; j < k; ++j) ss += (double)row[j] * (double)row[j];
+    double ms = ss / (double)k + eps;
+    if (!(ms > 0.0)) return ORACLE_EINVAL;
+    double r = 1.0 / sqrt(ms);
+    for (int64_t j = 0; j < k; ++j) out[i * k + j] = (double)row[j] * (double)gamma[j] * r;
+  }
+  return ORACLE_OK;
+}
+
+/* out[i] = silu(g[i]) * u[i], silu(t) = t / (1 + exp(-t)) (the sigmoid-
+ * weighted linear unit), in binary64. */
+int oracle_silu_mul(const double *g, const double *u, int64_t count, double *out) {
+  if (count < 0) return ORACLE_EINVAL;
+  for (int64_t i = 0; i < count; ++i) out[i] = g[i] / (1.0 + exp(-g[i])) * u[i];
+  return ORACLE_OK;
 }

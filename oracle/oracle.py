@@ -8,7 +8,10 @@ own shared object from ``oracle.c`` with gcc.
 Every function follows the definition in the header of ``oracle.c``: the
 Q8_0 / Q4_0 block formats (32 weights per block along k, one binary16 scale)
 that realise the paper's 8-bit and 4-bit configurations (section 4, Table 3),
-and the binary64 linear layer y = x . w_hat^T.
+and the binary64 linear layer y = x . w_hat^T, plus the decoder-layer steps
+fused around it (section 3.2, operator fusion): RMS normalisation before a
+projection, the SiLU-gated product of a gate/up pair and the residual addition
+after one (``fused_qlinear``).
 """
 from __future__ import annotations
 
@@ -65,6 +68,15 @@ class Oracle:
                                      ctypes.c_int64, ctypes.c_void_p, ctypes.c_int,
                                      ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64,
                                      ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int]
+        L.oracle_round_x16.restype = ctypes.c_int
+        L.oracle_round_x16.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int,
+                                       ctypes.c_void_p]
+        L.oracle_rmsnorm.restype = ctypes.c_int
+        L.oracle_rmsnorm.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_double,
+                                     ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p]
+        L.oracle_silu_mul.restype = ctypes.c_int
+        L.oracle_silu_mul.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                                      ctypes.c_void_p]
 
     # -- scalar format helpers ------------------------------------------------
     def half_to_double(self, h: int) -> float:
@@ -122,6 +134,87 @@ class Oracle:
         if rc != 0:
             raise ValueError("oracle_qlinear rejected the arguments")
         return y, bound
+
+
+    # -- the steps around the linear layer in a decoder layer ---------------
+    def round_x16(self, v: np.ndarray, xdtype: int) -> np.ndarray:
+        """Nearest binary16 (X_F16) or bfloat16 (X_BF16) words to float64 values, ties to even."""
+        v = np.ascontiguousarray(v, dtype=np.float64)
+        out = np.empty(v.shape, dtype=np.uint16)
+        if self.lib.oracle_round_x16(v.ctypes.data, v.size, xdtype, out.ctypes.data) != 0:
+            raise ValueError("oracle_round_x16 rejected the arguments")
+        return out
+
+    def rmsnorm(self, h: np.ndarray, gamma: np.ndarray, eps: float) -> np.ndarray:
+        """float64 h[i][j] * gamma[j] / sqrt(eps + mean_j h[i][j]^2) for binary32 h [m, k]."""
+        h = np.ascontiguousarray(h, dtype=np.float32)
+        if h.ndim == 1:
+            h = h.reshape(1, -1)
+        gamma = np.ascontiguousarray(gamma, dtype=np.float32)
+        m, k = h.shape
+        assert gamma.shape == (k,)
+        out = np.empty((m, k), dtype=np.float64)
+        if self.lib.oracle_rmsnorm(h.ctypes.data, gamma.ctypes.data, float(eps), m, k,
+                                   out.ctypes.data) != 0:
+            raise ValueError("oracle_rmsnorm rejected the arguments")
+        return out
+
+    def silu_mul(self, g: np.ndarray, u: np.ndarray) -> np.ndarray:
+        """float64 silu(g) * u, silu(t) = t / (1 + exp(-t))."""
+        g = np.ascontiguousarray(g, dtype=np.float64)
+        u = np.ascontiguousarray(u, dtype=np.float64)
+        assert g.shape == u.shape
+        out = np.empty(g.shape, dtype=np.float64)
+        if self.lib.oracle_silu_mul(g.ctypes.data, u.ctypes.data, g.size, out.ctypes.data) != 0:
+            raise ValueError("oracle_silu_mul rejected the arguments")
+        return out
+
+    def fused_qlinear(self, qtype: int, blocks: np.ndarray, n: int, k: int, x, xdtype: int,
+                      prologue: str = "none", gamma=None, eps: float = 0.0,
+                      epilogue: str = "none", residual=None, rows=None, nthreads: int = 1):
+        """One projection of a decoder layer with its neighbouring steps.
+
+        prologue "none": x is uint16 [m, k] raw activation words of xdtype.
+        prologue "rmsnorm": x is binary32 h [m, k]; the product takes
+            round_x16(rmsnorm(h, gamma, eps)), the normalised activations in
+            the activation type the linear layer consumes.
+        epilogue "none": y = x . w_hat^T; "add": y + residual (float64 [m, n]);
+        "glu": rows 2j and 2j + 1 of W are the gate and up rows of feature j,
+            y[:, j] = silu(gate) * up, shape [m, n / 2].
+        rows: which rows of x (the others are not computed).
+
+        Returns (y, scale, x_words): the error of an fp32-accumulating
+        implementation is measured against scale (|x||w_hat| summed over k for
+        "none" and "add"; for "glu", with Bg, Bu those sums of the gate and up
+        outputs g, u: 1.1 Bg |u| + |silu(g)| Bu + 0.0022 Bg Bu, the first-order
+        propagation of errors tau Bg, tau Bu through silu (|silu'| < 1.1) and
+        the product, plus their product term for tau <= 2e-3).
+        """
+        if prologue == "rmsnorm":
+            h = np.asarray(x, dtype=np.float32)
+            h = h if rows is None else h[rows]
+            xw = self.round_x16(self.rmsnorm(h, gamma, eps), xdtype)
+        elif prologue == "none":
+            xw = np.asarray(x, dtype=np.uint16)
+            xw = xw if rows is None else xw[rows]
+        else:
+            raise ValueError(prologue)
+        y, bound = self.qlinear(qtype, blocks, n, k, xw, xdtype, nthreads=nthreads)
+        if epilogue == "none":
+            return y, bound, xw
+        if epilogue == "add":
+            r = np.asarray(residual, dtype=np.float64)
+            r = r if rows is None else r[rows]
+            return y + r, bound, xw
+        if epilogue == "glu":
+            assert n % 2 == 0
+            g, u = y[:, 0::2], y[:, 1::2]
+            bg, bu = bound[:, 0::2], bound[:, 1::2]
+            s = self.silu_mul(g, u)
+            silu = self.silu_mul(g, np.ones_like(g))
+            scale = 1.1 * bg * np.abs(u) + np.abs(silu) * bu + 0.0022 * bg * bu
+            return s, scale, xw
+        raise ValueError(epilogue)
 
 
 _ORACLE = None
