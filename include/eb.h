@@ -106,14 +106,52 @@ typedef struct {
   int64_t canonical_bytes; /* n * (k/32) * (2 + QB), size of the canonical form */
 } eb_layout;
 
-/* One linear layer of a stack: y[m][n] = x[m][k] . w_hat^T. */
+/* Steps of a decoder layer fused around one projection (paper section 3.2,
+ * operator fusion on the batch-1 path; the backbones of section 2.1 are
+ * decoder stacks whose projections sit between an RMS normalisation and a
+ * residual addition, with a SiLU-gated feed-forward).
+ *
+ * Prologue EB_PRO_RMSNORM: x is the fp32 residual stream h[m][k]; the product
+ *   takes x_hat[i][j] = round(h[i][j] * g[j] * r_i), r_i = 1 / sqrt(eps +
+ *   (1/k) sum_j h[i][j]^2), rounded to nearest even in x_type, g = norm_weight.
+ *   On the GEMV path every workgroup normalises while it stages x (no extra
+ *   launch); on the MFMA path a row kernel writes x_hat first (one more launch)
+ *   into library-owned memory: the stream's workspace for direct calls (at
+ *   most 64 MiB together with split-K partial sums; during a capture the
+ *   workspace is not grown and a call needing more returns
+ *   EB_ERR_UNSUPPORTED), or the stack plan's own buffer.
+ * Epilogue EB_EPI_ADD: y = x_hat . w_hat^T + r, r = residual[m][n] of y_type;
+ *   residual may be y itself (in-place update of the residual stream) but
+ *   must not otherwise overlap y.
+ * Epilogue EB_EPI_GLU: rows 2j and 2j + 1 of W are the gate and up rows of
+ *   feature j (n even); y is [m][n/2] with y[i][j] = silu(gate) * up,
+ *   silu(t) = t / (1 + exp(-t)) evaluated in fp32.
+ * Accuracy: with e_g, e_u the accuracy bar of the two products (2e-3 of their
+ *   sums of |x_hat||w_hat|, B_g and B_u), a GLU output is within
+ *   2e-3 * (1.1 B_g |u| + |silu(g)| B_u + 0.0022 B_g B_u) (|silu'| < 1.1);
+ *   an ADD output within the product's bar plus one fp32 rounding. */
+#define EB_PRO_NONE 0
+#define EB_PRO_RMSNORM 1
+#define EB_EPI_NONE 0
+#define EB_EPI_ADD 1
+#define EB_EPI_GLU 2
+
+/* One linear layer of a stack: y[m][n] = x[m][k] . w_hat^T, with optional
+ * fused steps.  Fields after y_type may be left zero (no fused step). */
 typedef struct {
   eb_qweights w;
-  const void *x; /* device, [m][k] of x_type, row-major, 16-byte aligned */
-  void *y;       /* device, [m][n] of y_type, row-major, 16-byte aligned */
+  const void *x; /* device, row-major, 16-byte aligned: [m][k] of x_type, or fp32 [m][k]
+                    with EB_PRO_RMSNORM */
+  void *y;       /* device, [m][n] (EB_EPI_GLU: [m][n/2]) of y_type, row-major, 16-byte aligned */
   int64_t m;
-  int32_t x_type; /* EB_F16 or EB_BF16 */
-  int32_t y_type; /* EB_F32 or EB_BF16 */
+  int32_t x_type; /* EB_F16 or EB_BF16: the activations the product consumes */
+  int32_t y_type; /* EB_F32, EB_BF16 or EB_F16 */
+  int32_t prologue;        /* EB_PRO_NONE or EB_PRO_RMSNORM */
+  int32_t epilogue;        /* EB_EPI_NONE, EB_EPI_ADD or EB_EPI_GLU */
+  const float *norm_weight; /* EB_PRO_RMSNORM: g[k], fp32, device, 16-byte aligned */
+  const void *residual;    /* EB_EPI_ADD: [m][n] of y_type, device, 16-byte aligned */
+  float norm_eps;          /* EB_PRO_RMSNORM: finite, >= 0 (a zero row needs eps > 0) */
+  int32_t reserved;        /* must be 0 */
 } eb_qlinear_op;
 
 /* Library version string (static storage). */
@@ -161,14 +199,24 @@ eb_status eb_qweights_from_canonical(int32_t type, const void *src, int64_t n, i
  * stream's workspace is too small the call runs unsplit.  A graph captured
  * from stream S uses S's workspace: do not replay it concurrently with other
  * calls made on S.  x: device [m][k] of x_type (EB_F16 or EB_BF16); y: device
- * [m][n] of y_type (EB_F32 or EB_BF16, bf16 rounded to nearest even).
+ * [m][n] of y_type (EB_F32, EB_BF16 or EB_F16, 16-bit outputs rounded to
+ * nearest even).
  * No bias.  Accuracy: |y - y_exact| <= 2e-3 * sum_k |x||w_hat| per output
- * (plus the bf16 output rounding when y_type is EB_BF16).
+ * (plus the output rounding when y_type is 16-bit).
  * EB_ERR_INVALID: w or its data NULL, bad type/sizes, x/y NULL with m > 0.
  * EB_ERR_ALIGN: x or y not 16-byte aligned, w->data not 256-byte aligned.
  * EB_ERR_UNSUPPORTED: other dtypes. EB_ERR_HIP: launch failure. */
 eb_status eb_qlinear(const eb_qweights *w, const void *x, int32_t x_type, int64_t m, void *y,
                      int32_t y_type, hipStream_t stream);
+
+/* One projection with its fused steps (eb_qlinear_op: prologue, epilogue),
+ * on `path` (EB_PATH_*; AUTO picks as eb_qlinear does for the op's m, n, k).
+ * Errors as eb_qlinear, and EB_ERR_INVALID for an unknown prologue or
+ * epilogue, a missing norm_weight or residual, a negative or non-finite eps,
+ * an odd n with EB_EPI_GLU, reserved != 0, or a residual overlapping y
+ * without being y; EB_ERR_ALIGN for norm_weight or residual not 16-byte
+ * aligned; EB_ERR_UNSUPPORTED as described for the prologue above. */
+eb_status eb_qlinear_fused(const eb_qlinear_op *op, int32_t path, hipStream_t stream);
 
 /* eb_qlinear with an explicit kernel path (EB_PATH_*), for crossover
  * measurement and tests.  EB_ERR_UNSUPPORTED if the forced path cannot run
@@ -183,19 +231,29 @@ int32_t eb_qlinear_auto_path(int32_t type, int32_t x_type, int64_t m, int64_t n,
  * each as eb_qlinear would (paper section 3.2: graph replay, operator fusion,
  * buffer reuse).  `ops` is a HOST array.  All ops are validated before
  * anything is enqueued; n_ops == 0 is a no-op.
- *   Fusion: a run of consecutive m == 1 ops with the same formats in which no
- *   op reads or writes memory that an earlier op of the run writes (decided by
- *   address ranges of x, y and the weights) is executed by one persistent
- *   launch per K size class instead of one launch per op.  Results are bitwise
- *   identical to the unfused order.  EB_STACK_FUSE=0 disables fusion.
+ *   Each op may carry fused steps (prologue, epilogue) as eb_qlinear_fused.
+ *   Fusion: a run of consecutive ops in which no op reads or writes memory
+ *   that an earlier op of the run writes (decided by address ranges of x, y,
+ *   the weights, norm_weight and residual) is executed by fewer launches: m == 1
+ *   ops with the same formats by one persistent GEMV launch per K size class,
+ *   small-m MFMA ops (m <= 128) by one persistent launch, larger-m MFMA ops
+ *   with the same formats by one grouped launch over all their output tiles
+ *   (whose mostly-padded last row tiles may go to a small-m launch).  Results
+ *   are those of running the ops in order; the m == 1 fusion is bitwise
+ *   identical to single calls.  EB_STACK_FUSE=0 disables fusion,
+ *   EB_STACK_GROUP=0 the grouped launch, EB_STACK_SPLIT_TAIL=0 its tail split.
  *   Graph replay: the first call with a given op list (same pointers, sizes,
  *   types) builds a plan, records it into a HIP graph on a library-owned
  *   stream and caches both; later calls replay the graph with one launch.
- *   EB_STACK_GRAPH=0 launches the plan directly instead.  Called while
+ *   EB_STACK_GRAPH=0 launches the plan directly instead; EB_STACK_DEBUG=1
+ *   prints each plan's steps to stderr when it is built.  Called while
  *   `stream` itself is being captured, the ops are launched plainly into it.
- * Memory: a plan with fused runs owns a small device table (about 64 bytes
- * per fused op), allocated once when the plan is built and freed by
- * eb_stack_cache_clear (or when more than 64 plans are cached). */
+ * Memory: a plan with fused runs owns a small device table (about 100 bytes
+ * per fused op), a split-K workspace when one of its ops is split, and, for
+ * EB_PRO_RMSNORM ops on the MFMA path, a buffer for the normalised
+ * activations (the largest total m * k * 2 bytes of one launch step),
+ * allocated once when the plan is built and freed by eb_stack_cache_clear
+ * (or when more than 64 plans are cached). */
 eb_status eb_qlinear_stack(const eb_qlinear_op *ops, int32_t n_ops, hipStream_t stream);
 
 /* Number of kernel launches eb_qlinear_stack makes for this op list (host

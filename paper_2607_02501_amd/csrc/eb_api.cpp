@@ -8,6 +8,8 @@
 
 #include <algorithm>
 #include <atomic>
+#include <cmath>
+#include <cstdio>
 #include <cstdlib>
 #include <cstring>
 #include <map>
@@ -70,21 +72,66 @@ eb_status check_weights(const eb_qweights *w) {
   return EB_OK;
 }
 
-eb_status check_linear(const eb_qweights *w, const void *x, int32_t xt, int64_t m, const void *y,
-                       int32_t yt, int32_t path) {
-  eb_status st = check_weights(w);
+// One op as a plain projection (no fused steps).
+eb_qlinear_op plain_op(const eb_qweights *w, const void *x, int32_t xt, int64_t m, void *y,
+                       int32_t yt) {
+  eb_qlinear_op o{};
+  o.w = *w;
+  o.x = x;
+  o.y = y;
+  o.m = m;
+  o.x_type = xt;
+  o.y_type = yt;
+  return o;
+}
+
+// Output columns of an op (the gate/up epilogue halves them).
+int64_t n_out(const eb_qlinear_op &o) { return o.epilogue == EB_EPI_GLU ? o.w.n / 2 : o.w.n; }
+// Bytes of x the op reads (fp32 residual stream under the normalisation prologue).
+size_t x_bytes(const eb_qlinear_op &o) {
+  return (size_t)o.m * (size_t)o.w.k * (o.prologue == EB_PRO_RMSNORM ? 4 : 2);
+}
+
+Fuse fuse_of(const eb_qlinear_op &o) {
+  Fuse f{};
+  f.gamma = o.prologue == EB_PRO_RMSNORM ? o.norm_weight : nullptr;
+  f.r = o.epilogue == EB_EPI_ADD ? o.residual : nullptr;
+  f.eps = o.norm_eps;
+  f.pro = (int16_t)o.prologue;
+  f.epi = (int16_t)o.epilogue;
+  return f;
+}
+
+eb_status check_op(const eb_qlinear_op &o, int32_t path) {
+  eb_status st = check_weights(&o.w);
   if (st != EB_OK) return st;
+  const int64_t m = o.m;
   if (m < 0 || m > kMaxM) return EB_ERR_INVALID;
-  if (!known_dtype(xt) || !known_dtype(yt)) return EB_ERR_INVALID;
+  if (!known_dtype(o.x_type) || !known_dtype(o.y_type)) return EB_ERR_INVALID;
   if (path != EB_PATH_AUTO && path != EB_PATH_GEMV && path != EB_PATH_MFMA) return EB_ERR_INVALID;
-  if (xt == EB_F32 || yt == EB_F16) return EB_ERR_UNSUPPORTED;
+  if (o.prologue != EB_PRO_NONE && o.prologue != EB_PRO_RMSNORM) return EB_ERR_INVALID;
+  if (o.epilogue != EB_EPI_NONE && o.epilogue != EB_EPI_ADD && o.epilogue != EB_EPI_GLU)
+    return EB_ERR_INVALID;
+  if (o.reserved != 0) return EB_ERR_INVALID;
+  if (o.prologue == EB_PRO_RMSNORM && !(std::isfinite(o.norm_eps) && o.norm_eps >= 0.0f))
+    return EB_ERR_INVALID;
+  if (o.epilogue == EB_EPI_GLU && o.w.n % 2 != 0) return EB_ERR_INVALID;
+  if (o.x_type == EB_F32) return EB_ERR_UNSUPPORTED;
   if (m == 0) return EB_OK;
-  if (!x || !y) return EB_ERR_INVALID;
-  if (!aligned(x, 16) || !aligned(y, 16)) return EB_ERR_ALIGN;
-  const size_t xb = (size_t)m * (size_t)w->k * 2, yb = (size_t)m * (size_t)w->n * dsize(yt);
-  const size_t wb = eb_qweights_bytes(w->type, w->n, w->k);
-  if (overlaps(y, yb, x, xb) || overlaps(y, yb, w->data, wb)) return EB_ERR_INVALID;
-  if (path == EB_PATH_GEMV && !gemv_fits(m, w->k)) return EB_ERR_UNSUPPORTED;
+  if (!o.x || !o.y) return EB_ERR_INVALID;
+  if (o.prologue == EB_PRO_RMSNORM && !o.norm_weight) return EB_ERR_INVALID;
+  if (o.epilogue == EB_EPI_ADD && !o.residual) return EB_ERR_INVALID;
+  if (!aligned(o.x, 16) || !aligned(o.y, 16)) return EB_ERR_ALIGN;
+  if (o.prologue == EB_PRO_RMSNORM && !aligned(o.norm_weight, 16)) return EB_ERR_ALIGN;
+  if (o.epilogue == EB_EPI_ADD && !aligned(o.residual, 16)) return EB_ERR_ALIGN;
+  const size_t yb = (size_t)m * (size_t)n_out(o) * dsize(o.y_type);
+  const size_t wb = eb_qweights_bytes(o.w.type, o.w.n, o.w.k);
+  if (overlaps(o.y, yb, o.x, x_bytes(o)) || overlaps(o.y, yb, o.w.data, wb)) return EB_ERR_INVALID;
+  if (o.prologue == EB_PRO_RMSNORM && overlaps(o.y, yb, o.norm_weight, (size_t)o.w.k * 4))
+    return EB_ERR_INVALID;
+  if (o.epilogue == EB_EPI_ADD && o.residual != o.y && overlaps(o.y, yb, o.residual, yb))
+    return EB_ERR_INVALID;
+  if (path == EB_PATH_GEMV && !gemv_fits(m, o.w.k)) return EB_ERR_UNSUPPORTED;
   return EB_OK;
 }
 
@@ -118,13 +165,13 @@ WsCache &ws_cache() {
 // Workspace of at least `bytes` for stream s, or nullptr (then the caller runs
 // unsplit): allocation failed, or s is being captured and the buffer it has is
 // too small (no allocation inside a capture).
-float *stream_workspace(hipStream_t s, size_t bytes) {
+uint8_t *stream_workspace(hipStream_t s, size_t bytes) {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return nullptr;
   WsCache &C = ws_cache();
   std::lock_guard<std::mutex> lock(C.mu);
   auto &slot = C.live[{dev, s}];
-  if (slot.first && slot.second >= bytes) return static_cast<float *>(slot.first);
+  if (slot.first && slot.second >= bytes) return static_cast<uint8_t *>(slot.first);
   hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
   if (hipStreamIsCapturing(s, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone)
     return nullptr;
@@ -136,21 +183,48 @@ float *stream_workspace(hipStream_t s, size_t bytes) {
   }
   if (slot.first) C.retired.push_back(slot.first);
   slot = {p, want};
-  return static_cast<float *>(p);
+  return static_cast<uint8_t *>(p);
 }
 
-eb_status launch_linear(const eb_qweights *w, const void *x, int32_t xt, int64_t m, void *y,
-                        int32_t yt, int32_t path, hipStream_t s) {
-  if (m == 0) return EB_OK;
-  if (path == EB_PATH_AUTO) path = pick_path(w->type, xt, m, w->n, w->k);
+// Bytes of normalised activations an op on the MFMA path needs (256-aligned).
+size_t xhat_bytes(const eb_qlinear_op &o) {
+  return o.prologue == EB_PRO_RMSNORM ? (size_t)round_up(o.m * o.w.k * 2, 256) : 0;
+}
+
+// One op on the MFMA path with a fixed plan: the prologue's row kernel writes
+// the normalised activations to xbuf, then the product reads them.
+hipError_t launch_mfma_op(const eb_qlinear_op &o, const MfmaPlan &P, void *xbuf, float *ws,
+                          hipStream_t s) {
+  const void *x = o.x;
+  Fuse f = fuse_of(o);
+  if (o.prologue == EB_PRO_RMSNORM) {
+    hipError_t e = launch_rmsnorm(static_cast<const float *>(o.x), o.norm_weight, o.norm_eps, o.m,
+                                  o.w.k, o.x_type, xbuf, s);
+    if (e != hipSuccess) return e;
+    x = xbuf;
+    f.pro = EB_PRO_NONE;
+    f.gamma = nullptr;
+  }
+  return launch_mfma(o.w.type, o.w.data, o.w.n, o.w.k, x, o.x_type, o.m, o.y, o.y_type, f, P, ws, s);
+}
+
+eb_status launch_op(const eb_qlinear_op &o, int32_t path, hipStream_t s) {
+  if (o.m == 0) return EB_OK;
+  if (path == EB_PATH_AUTO) path = pick_path(o.w.type, o.x_type, o.m, o.w.n, o.w.k);
   hipError_t e;
   if (path == EB_PATH_GEMV) {
-    e = launch_gemv(w->type, w->data, w->n, w->k, x, xt, m, y, yt, s);
+    e = launch_gemv(o.w.type, o.w.data, o.w.n, o.w.k, o.x, o.x_type, o.m, o.y, o.y_type, fuse_of(o), s);
   } else {
-    MfmaPlan P = plan_mfma(w->type, m, w->n, w->k, true);
-    float *ws = P.splits > 1 ? stream_workspace(s, P.ws_bytes) : nullptr;
-    if (P.splits > 1 && !ws) P = plan_mfma(w->type, m, w->n, w->k, false);
-    e = launch_mfma(w->type, w->data, w->n, w->k, x, xt, m, y, yt, P, ws, s);
+    // the stream's workspace holds the normalised activations, then any
+    // split-K partial sums
+    const size_t xb = xhat_bytes(o);
+    MfmaPlan P = plan_mfma(o.w.type, o.m, o.w.n, o.w.k, true);
+    uint8_t *ws = nullptr;
+    if (P.splits > 1) ws = stream_workspace(s, xb + P.ws_bytes);
+    if (P.splits > 1 && !ws) P = plan_mfma(o.w.type, o.m, o.w.n, o.w.k, false);
+    if (!ws && xb) ws = stream_workspace(s, xb);
+    if (xb && !ws) return EB_ERR_UNSUPPORTED;
+    e = launch_mfma_op(o, P, ws, P.splits > 1 ? reinterpret_cast<float *>(ws + xb) : nullptr, s);
   }
   return e == hipSuccess ? EB_OK : EB_ERR_HIP;
 }
@@ -178,24 +252,52 @@ struct Range {
   bool hits(const Range &o) const { return a < o.b && o.a < b; }
 };
 
+// What an op reads (x, weights, normalisation weights, residual) and writes (y).
 struct OpSpan {
-  Range x, y, w;
+  Range rd[4];
+  int nrd = 0;
+  Range y;
 };
 
 OpSpan span_of(const eb_qlinear_op &o) {
+  auto range = [](const void *p, size_t bytes) {
+    const uintptr_t a = reinterpret_cast<uintptr_t>(p);
+    return Range{a, a + (uintptr_t)bytes};
+  };
   OpSpan s;
-  const uintptr_t x = reinterpret_cast<uintptr_t>(o.x), y = reinterpret_cast<uintptr_t>(o.y),
-                  w = reinterpret_cast<uintptr_t>(o.w.data);
-  s.x = {x, x + (uintptr_t)(o.m * o.w.k * 2)};
-  s.y = {y, y + (uintptr_t)(o.m * o.w.n * (int64_t)dsize(o.y_type))};
-  s.w = {w, w + (uintptr_t)eb_qweights_bytes(o.w.type, o.w.n, o.w.k)};
+  s.rd[s.nrd++] = range(o.x, x_bytes(o));
+  s.rd[s.nrd++] = range(o.w.data, eb_qweights_bytes(o.w.type, o.w.n, o.w.k));
+  if (o.prologue == EB_PRO_RMSNORM) s.rd[s.nrd++] = range(o.norm_weight, (size_t)o.w.k * 4);
+  const size_t yb = (size_t)o.m * (size_t)n_out(o) * dsize(o.y_type);
+  if (o.epilogue == EB_EPI_ADD) s.rd[s.nrd++] = range(o.residual, yb);
+  s.y = range(o.y, yb);
   return s;
 }
 
 // op b may join a run containing op a only if neither observes the other
 bool independent(const OpSpan &a, const OpSpan &b) {
-  return !(b.x.hits(a.y) || b.y.hits(a.y) || b.y.hits(a.x) || b.y.hits(a.w) || b.w.hits(a.y));
+  if (b.y.hits(a.y)) return false;
+  for (int i = 0; i < b.nrd; ++i)
+    if (b.rd[i].hits(a.y)) return false;
+  for (int i = 0; i < a.nrd; ++i)
+    if (b.y.hits(a.rd[i])) return false;
+  return true;
 }
+
+// The prologue of an op on the MFMA path: its row kernel writes the
+// normalised activations into the plan's buffer at `off`.
+struct NormJob {
+  const float *h, *gamma;
+  float eps;
+  int32_t xt;
+  int64_t m, k;
+  size_t off;
+};
+
+// Internal copies of ops whose x was replaced by an offset into the plan's
+// normalised-activation buffer carry this marker in `reserved` (user ops must
+// have reserved == 0).
+constexpr int32_t kRelX = 1;
 
 struct Step {
   int op = -1;        // single op index, or -1 for a fused launch
@@ -212,6 +314,7 @@ struct Step {
   bool gm = false;    // grouped MFMA launch (op == -1): table entries from `table`,
   size_t order = 0;   // workgroup entries from `order`
   int64_t entries = 0;
+  std::vector<NormJob> norms;  // prologue row kernels run before the step
 };
 
 struct Plan {
@@ -223,6 +326,8 @@ struct Plan {
   int2 *gmorder = nullptr;  // and workgroup (op, tile) entries
   float *ws = nullptr;    // split-K workspace shared by the plan's MFMA steps (run in order)
   size_t ws_bytes = 0;
+  uint8_t *xbuf = nullptr;  // normalised activations of prologue ops on the MFMA path
+  size_t xbuf_bytes = 0;
   hipGraph_t graph = nullptr;
   hipGraphExec_t exec = nullptr;
 };
@@ -233,7 +338,7 @@ bool env_off(const char *name) {
 }
 
 bool fusable(const eb_qlinear_op &o) {
-  return o.m == 1 && gemv_fits(1, o.w.k) && m1_fusable(o.w.type, o.m, o.w.k);
+  return o.m == 1 && gemv_fits(1, o.w.k) && m1_fusable(o.w.type, o.m, o.w.k, o.epilogue);
 }
 
 // MFMA ops that may join a fused launch.  The fused kernel addresses tiles of
@@ -261,8 +366,8 @@ bool mm_fusable(const eb_qlinear_op &o) {
          pick_path(o.w.type, o.x_type, o.m, o.w.n, o.w.k) == EB_PATH_MFMA;
 }
 
-// Builds the plan; with `alloc`, also allocates and fills its device table
-// when any run is fused (without it the plan is only counted).
+// Builds the plan; with `alloc`, also allocates and fills its device tables
+// and buffers (without it the plan is only counted).
 eb_status build_plan(const eb_qlinear_op *ops, int32_t n_ops, bool alloc, Plan &P) {
   std::vector<M1Op> host;
   std::vector<MMOp> mmhost;
@@ -270,6 +375,24 @@ eb_status build_plan(const eb_qlinear_op *ops, int32_t n_ops, bool alloc, Plan &
   std::vector<GOp> gmhost;
   std::vector<int2> gmorder;
   const bool fuse = !env_off("EB_STACK_FUSE");
+  // Normalisation jobs of the current iteration (one fused run, or one op):
+  // their buffers are laid out from offset 0, since the steps of one
+  // iteration run after those of the previous one.
+  std::vector<NormJob> jobs;
+  size_t xoff = 0;
+  // an MFMA op with the prologue reads the plan's buffer instead of h
+  auto prep = [&](const eb_qlinear_op &o) {
+    if (o.prologue != EB_PRO_RMSNORM) return o;
+    NormJob j{static_cast<const float *>(o.x), o.norm_weight, o.norm_eps, o.x_type, o.m, o.w.k, xoff};
+    jobs.push_back(j);
+    eb_qlinear_op c = o;
+    c.x = reinterpret_cast<const void *>((uintptr_t)xoff);
+    c.prologue = EB_PRO_NONE;
+    c.norm_weight = nullptr;
+    c.reserved = kRelX;
+    xoff += xhat_bytes(o);
+    return c;
+  };
   // one fused small-m launch over `list` (same weight, x and y formats)
   auto add_mm_step = [&](const std::vector<eb_qlinear_op> &list) {
     int64_t max_m = 0;
@@ -299,6 +422,8 @@ eb_status build_plan(const eb_qlinear_op *ops, int32_t n_ops, bool alloc, Plan &
       e.tiles_n = (int32_t)mm_tiles(s.mm_cfg, 1, o.w.n);
       e.nk = (int32_t)((o.w.k + mm_bk(s.mm_cfg) - 1) / mm_bk(s.mm_cfg));
       e.yt = o.y_type;
+      e.pad = o.reserved == kRelX;  // x is an offset into the plan's buffer
+      e.f = fuse_of(o);
       run.push_back(e);
     }
     std::vector<int64_t> wg;
@@ -310,41 +435,54 @@ eb_status build_plan(const eb_qlinear_op *ops, int32_t n_ops, bool alloc, Plan &
     mmwg.insert(mmwg.end(), wg.begin(), wg.end());
     P.steps.push_back(s);
   };
+  auto gops_of = [](const std::vector<eb_qlinear_op> &list) {
+    std::vector<GOp> run;
+    for (const eb_qlinear_op &o : list) {
+      const Layout L = layout_of(o.w.type, o.w.n, o.w.k);
+      GOp e{};
+      e.w = static_cast<const uint8_t *>(o.w.data);
+      e.x = static_cast<const uint16_t *>(o.x);
+      e.y = o.y;
+      e.n = o.w.n;
+      e.k = o.w.k;
+      e.d_off = L.d_off;
+      e.ds = L.ds;
+      e.m = o.m;
+      e.yt = o.y_type;
+      e.pad = o.reserved == kRelX;
+      e.f = fuse_of(o);
+      run.push_back(e);
+    }
+    return run;
+  };
   int32_t i = 0;
   while (i < n_ops) {
-    if (fuse && gm_fusable(ops[i])) {
-      // run of independent large-m MFMA ops with the same weight and x formats
+    jobs.clear();
+    xoff = 0;
+    const size_t first_step = P.steps.size();
+    // run [i, j) of consecutive ops that `ok` accepts and that are independent
+    auto run_end = [&](auto ok) {
       std::vector<OpSpan> spans{span_of(ops[i])};
       int32_t j = i + 1;
       for (; j < n_ops; ++j) {
-        const eb_qlinear_op &o = ops[j];
-        if (!gm_fusable(o) || o.w.type != ops[i].w.type || o.x_type != ops[i].x_type) break;
-        const OpSpan sj = span_of(o);
-        bool ok = true;
-        for (const OpSpan &sp : spans) ok = ok && independent(sp, sj);
-        if (!ok) break;
+        if (!ok(ops[j])) break;
+        const OpSpan sj = span_of(ops[j]);
+        bool indep = true;
+        for (const OpSpan &sp : spans) indep = indep && independent(sp, sj);
+        if (!indep) break;
         spans.push_back(sj);
       }
+      return j;
+    };
+    bool done = false;
+    if (fuse && gm_fusable(ops[i])) {
+      // run of independent large-m MFMA ops with the same weight and x formats
+      const int32_t j = run_end([&](const eb_qlinear_op &o) {
+        return gm_fusable(o) && o.w.type == ops[i].w.type && o.x_type == ops[i].x_type;
+      });
       if (j - i > 1) {
-        auto gops_of = [](const std::vector<eb_qlinear_op> &list) {
-          std::vector<GOp> run;
-          for (const eb_qlinear_op &o : list) {
-            const Layout L = layout_of(o.w.type, o.w.n, o.w.k);
-            GOp e{};
-            e.w = static_cast<const uint8_t *>(o.w.data);
-            e.x = static_cast<const uint16_t *>(o.x);
-            e.y = o.y;
-            e.n = o.w.n;
-            e.k = o.w.k;
-            e.d_off = L.d_off;
-            e.ds = L.ds;
-            e.m = o.m;
-            e.yt = o.y_type;
-            run.push_back(e);
-          }
-          return run;
-        };
-        std::vector<eb_qlinear_op> mains(ops + i, ops + j), tails;
+        std::vector<eb_qlinear_op> mains, tails;
+        for (int32_t r = i; r < j; ++r) mains.push_back(prep(ops[r]));
         std::vector<GOp> run = gops_of(mains);
         std::vector<int2> order;
         int cfg = plan_grouped(ops[i].w.type, run, order);
@@ -356,11 +494,13 @@ eb_status build_plan(const eb_qlinear_op *ops, int32_t n_ops, bool alloc, Plan &
           const double rate = mfma_cfg_rate(cfg) * 1e12;
           std::vector<eb_qlinear_op> m2, t2;
           for (const eb_qlinear_op &o : mains) {
-            const int64_t rem = o.m % bm;
+            const int64_t rem = o.m % bm, m0 = o.m - rem;
             eb_qlinear_op t = o;
             t.m = rem;
-            t.x = static_cast<const uint8_t *>(o.x) + (o.m - rem) * o.w.k * 2;
-            t.y = static_cast<uint8_t *>(o.y) + (o.m - rem) * o.w.n * dsize(o.y_type);
+            t.x = static_cast<const uint8_t *>(o.x) + m0 * o.w.k * 2;
+            t.y = static_cast<uint8_t *>(o.y) + m0 * n_out(o) * dsize(o.y_type);
+            if (o.epilogue == EB_EPI_ADD)
+              t.residual = static_cast<const uint8_t *>(o.residual) + m0 * o.w.n * dsize(o.y_type);
             bool split = rem > 0 && o.m > bm && mm_fusable(t);
             if (split) {
               const double row_flops = 2.0 * o.w.n * o.w.k;
@@ -372,7 +512,7 @@ eb_status build_plan(const eb_qlinear_op *ops, int32_t n_ops, bool alloc, Plan &
             }
             eb_qlinear_op mo = o;
             if (split) {
-              mo.m = o.m - rem;
+              mo.m = m0;
               t2.push_back(t);
             }
             m2.push_back(mo);
@@ -404,94 +544,101 @@ eb_status build_plan(const eb_qlinear_op *ops, int32_t n_ops, bool alloc, Plan &
           gmhost.insert(gmhost.end(), run.begin(), run.end());
           gmorder.insert(gmorder.end(), order.begin(), order.end());
           P.steps.push_back(s);
-          // the split-off rows: one fused launch per output type
-          for (int32_t yt : {EB_F32, EB_BF16, EB_F16}) {
+          // the split-off rows: one fused launch per output size
+          for (int wide = 1; wide >= 0; --wide) {
             std::vector<eb_qlinear_op> cls;
             for (const eb_qlinear_op &t : tails)
-              if (t.y_type == yt) cls.push_back(t);
+              if ((t.y_type == EB_F32) == (wide == 1)) cls.push_back(t);
             if (!cls.empty()) add_mm_step(cls);
           }
           i = j;
-          continue;
+          done = true;
+        } else {
+          jobs.clear();
+          xoff = 0;
         }
       }
     }
-    if (fuse && mm_fusable(ops[i])) {
-      // run of independent small-m MFMA ops with the same formats
-      std::vector<OpSpan> spans{span_of(ops[i])};
-      int32_t j = i + 1;
-      for (; j < n_ops; ++j) {
-        const eb_qlinear_op &o = ops[j];
-        if (!mm_fusable(o) || o.w.type != ops[i].w.type || o.x_type != ops[i].x_type ||
-            o.y_type != ops[i].y_type)
-          break;
-        const OpSpan sj = span_of(o);
-        bool ok = true;
-        for (const OpSpan &sp : spans) ok = ok && independent(sp, sj);
-        if (!ok) break;
-        spans.push_back(sj);
+    if (!done && fuse && mm_fusable(ops[i])) {
+      // run of independent small-m MFMA ops with the same formats (16-bit
+      // output types share a launch)
+      const bool wide = ops[i].y_type == EB_F32;
+      const int32_t j = run_end([&](const eb_qlinear_op &o) {
+        return mm_fusable(o) && o.w.type == ops[i].w.type && o.x_type == ops[i].x_type &&
+               (o.y_type == EB_F32) == wide;
+      });
+      if (j - i > 1) {
+        std::vector<eb_qlinear_op> list;
+        for (int32_t r = i; r < j; ++r) list.push_back(prep(ops[r]));
+        add_mm_step(list);
+        i = j;
+        done = true;
       }
-      if (j - i == 1) {
-        Step s;
-        s.op = i++;
-        P.steps.push_back(s);
-        continue;
-      }
-      add_mm_step(std::vector<eb_qlinear_op>(ops + i, ops + j));
-      i = j;
-      continue;
     }
-    if (!fuse || !fusable(ops[i])) {
+    if (!done && fuse && fusable(ops[i])) {
+      // run of independent m == 1 GEMV ops with the same formats
+      const int32_t j = run_end([&](const eb_qlinear_op &o) {
+        return fusable(o) && o.w.type == ops[i].w.type && o.x_type == ops[i].x_type;
+      });
+      if (j - i > 1) {
+        // one fused launch per slot count, in order of first appearance
+        std::vector<int> classes;
+        for (int32_t r = i; r < j; ++r) {
+          const int ns = m1_slots(ops[r].w.type, ops[r].w.k);
+          if (std::find(classes.begin(), classes.end(), ns) == classes.end()) classes.push_back(ns);
+        }
+        for (int ns : classes) {
+          Step s;
+          s.type = ops[i].w.type;
+          s.xt = ops[i].x_type;
+          s.ns = ns;
+          s.table = host.size();
+          for (int32_t r = i; r < j; ++r) {
+            const eb_qlinear_op &o = ops[r];
+            if (m1_slots(o.w.type, o.w.k) != ns) continue;
+            M1Op e;
+            s.units += m1_fill(o.w.type, o.w.data, o.w.n, o.w.k, o.x, o.y, o.y_type, fuse_of(o),
+                               s.units, &e);
+            s.rows += o.w.n;
+            host.push_back(e);
+            ++s.nops;
+          }
+          P.steps.push_back(s);
+        }
+        i = j;
+        done = true;
+      }
+    }
+    if (!done) {
       Step s;
       s.op = i++;
       P.steps.push_back(s);
-      continue;
     }
-    std::vector<int32_t> run{i};
-    std::vector<OpSpan> spans{span_of(ops[i])};
-    int32_t j = i + 1;
-    for (; j < n_ops; ++j) {
-      const eb_qlinear_op &o = ops[j];
-      if (!fusable(o) || o.w.type != ops[i].w.type || o.x_type != ops[i].x_type) break;
-      const OpSpan sj = span_of(o);
-      bool ok = true;
-      for (const OpSpan &sp : spans) ok = ok && independent(sp, sj);
-      if (!ok) break;
-      run.push_back(j);
-      spans.push_back(sj);
-    }
-    if (run.size() == 1) {
-      Step s;
-      s.op = i;
-      P.steps.push_back(s);
-    } else {
-      // one fused launch per slot count, in order of first appearance
-      std::vector<int> classes;
-      for (int32_t r : run) {
-        const int ns = m1_slots(ops[r].w.type, ops[r].w.k);
-        if (std::find(classes.begin(), classes.end(), ns) == classes.end()) classes.push_back(ns);
-      }
-      for (int ns : classes) {
-        Step s;
-        s.type = ops[i].w.type;
-        s.xt = ops[i].x_type;
-        s.ns = ns;
-        s.table = host.size();
-        for (int32_t r : run) {
-          const eb_qlinear_op &o = ops[r];
-          if (m1_slots(o.w.type, o.w.k) != ns) continue;
-          M1Op e;
-          s.units += m1_fill(o.w.type, o.w.data, o.w.n, o.w.k, o.x, o.y, o.y_type, s.units, &e);
-          s.rows += o.w.n;
-          host.push_back(e);
-          ++s.nops;
-        }
-        P.steps.push_back(s);
-      }
-    }
-    i = j;
+    if (!jobs.empty()) P.steps[first_step].norms = jobs;
+    P.xbuf_bytes = std::max(P.xbuf_bytes, xoff);
   }
-  if (alloc && !mmhost.empty()) {
+  for (Step &s : P.steps) {
+    if (s.op < 0) continue;
+    const eb_qlinear_op &o = ops[s.op];
+    if (o.m == 0 || pick_path(o.w.type, o.x_type, o.m, o.w.n, o.w.k) != EB_PATH_MFMA) continue;
+    s.mfma = true;
+    s.mp = plan_mfma(o.w.type, o.m, o.w.n, o.w.k, true);
+    P.ws_bytes = std::max(P.ws_bytes, s.mp.ws_bytes);
+    P.xbuf_bytes = std::max(P.xbuf_bytes, xhat_bytes(o));
+  }
+  if (!alloc) return EB_OK;
+  if (P.xbuf_bytes > 0) {
+    if (hipMalloc((void **)&P.xbuf, P.xbuf_bytes) != hipSuccess) {
+      P.xbuf = nullptr;
+      return EB_ERR_HIP;
+    }
+    // table entries whose x is an offset into the buffer
+    for (MMOp &e : mmhost)
+      if (e.pad) e.x = reinterpret_cast<const uint16_t *>(P.xbuf + reinterpret_cast<uintptr_t>(e.x));
+    for (GOp &e : gmhost)
+      if (e.pad) e.x = reinterpret_cast<const uint16_t *>(P.xbuf + reinterpret_cast<uintptr_t>(e.x));
+  }
+  if (!mmhost.empty()) {
     if (hipMalloc((void **)&P.mmtable, mmhost.size() * sizeof(MMOp)) != hipSuccess) {
       P.mmtable = nullptr;
       return EB_ERR_HIP;
@@ -506,7 +653,7 @@ eb_status build_plan(const eb_qlinear_op *ops, int32_t n_ops, bool alloc, Plan &
             hipSuccess)
       return EB_ERR_HIP;
   }
-  if (alloc && !gmhost.empty()) {
+  if (!gmhost.empty()) {
     if (hipMalloc((void **)&P.gmtable, gmhost.size() * sizeof(GOp)) != hipSuccess) {
       P.gmtable = nullptr;
       return EB_ERR_HIP;
@@ -521,19 +668,11 @@ eb_status build_plan(const eb_qlinear_op *ops, int32_t n_ops, bool alloc, Plan &
                   hipMemcpyHostToDevice) != hipSuccess)
       return EB_ERR_HIP;
   }
-  for (Step &s : P.steps) {
-    if (s.op < 0) continue;
-    const eb_qlinear_op &o = ops[s.op];
-    if (o.m == 0 || pick_path(o.w.type, o.x_type, o.m, o.w.n, o.w.k) != EB_PATH_MFMA) continue;
-    s.mfma = true;
-    s.mp = plan_mfma(o.w.type, o.m, o.w.n, o.w.k, true);
-    P.ws_bytes = std::max(P.ws_bytes, s.mp.ws_bytes);
-  }
-  if (alloc && P.ws_bytes > 0 && hipMalloc((void **)&P.ws, P.ws_bytes) != hipSuccess) {
+  if (P.ws_bytes > 0 && hipMalloc((void **)&P.ws, P.ws_bytes) != hipSuccess) {
     P.ws = nullptr;
     return EB_ERR_HIP;
   }
-  if (alloc && !host.empty()) {
+  if (!host.empty()) {
     if (hipMalloc((void **)&P.table, host.size() * sizeof(M1Op)) != hipSuccess) {
       P.table = nullptr;
       return EB_ERR_HIP;
@@ -545,8 +684,28 @@ eb_status build_plan(const eb_qlinear_op *ops, int32_t n_ops, bool alloc, Plan &
   return EB_OK;
 }
 
+// EB_STACK_DEBUG=1 prints each plan's steps to stderr when it is built.
+void print_plan(const eb_qlinear_op *ops, const Plan &P) {
+  std::fprintf(stderr, "[eb plan] %zu steps, xbuf %p (%zu B), ws %p (%zu B)\n", P.steps.size(),
+               (void *)P.xbuf, P.xbuf_bytes, (void *)P.ws, P.ws_bytes);
+  for (size_t i = 0; i < P.steps.size(); ++i) {
+    const Step &st = P.steps[i];
+    const char *kind = st.gm ? "grouped" : st.mm ? "small-m" : st.mfma ? "mfma" : st.op >= 0 ? "single" : "gemv-multi";
+    std::fprintf(stderr, "[eb plan]  step %zu %s op %d nops %d cfg %d splits %d norms %zu", i, kind,
+                 st.op, st.nops, st.mm_cfg, st.mfma ? st.mp.splits : 0, st.norms.size());
+    for (const NormJob &j : st.norms) std::fprintf(stderr, " [h %p off %zu]", (const void *)j.h, j.off);
+    if (st.op >= 0)
+      std::fprintf(stderr, " x %p y %p pro %d epi %d", ops[st.op].x, ops[st.op].y, ops[st.op].prologue,
+                   ops[st.op].epilogue);
+    std::fprintf(stderr, "\n");
+  }
+}
+
 eb_status run_plan(const eb_qlinear_op *ops, const Plan &P, hipStream_t s) {
   for (const Step &st : P.steps) {
+    for (const NormJob &j : st.norms)
+      if (launch_rmsnorm(j.h, j.gamma, j.eps, j.m, j.k, j.xt, P.xbuf + j.off, s) != hipSuccess)
+        return EB_ERR_HIP;
     if (st.gm) {
       // the table entries index the whole plan's op table
       if (launch_mfma_grouped(st.type, st.xt, st.mm_cfg, P.gmtable, P.gmorder + st.order,
@@ -558,12 +717,10 @@ eb_status run_plan(const eb_qlinear_op *ops, const Plan &P, hipStream_t s) {
         return EB_ERR_HIP;
     } else if (st.mfma) {
       const eb_qlinear_op &o = ops[st.op];
-      if (launch_mfma(o.w.type, o.w.data, o.w.n, o.w.k, o.x, o.x_type, o.m, o.y, o.y_type, st.mp,
-                      st.mp.splits > 1 ? P.ws : nullptr, s) != hipSuccess)
+      if (launch_mfma_op(o, st.mp, P.xbuf, st.mp.splits > 1 ? P.ws : nullptr, s) != hipSuccess)
         return EB_ERR_HIP;
     } else if (st.op >= 0) {
-      const eb_qlinear_op &o = ops[st.op];
-      eb_status r = launch_linear(&o.w, o.x, o.x_type, o.m, o.y, o.y_type, EB_PATH_AUTO, s);
+      eb_status r = launch_op(ops[st.op], EB_PATH_AUTO, s);
       if (r != EB_OK) return r;
     } else if (launch_gemv_m1_multi(st.type, st.xt, st.ns, P.table + st.table, st.nops, st.units,
                                     st.rows, s) != hipSuccess) {
@@ -582,6 +739,7 @@ void destroy_plan(Plan &p) {
   if (p.gmtable) (void)hipFree(p.gmtable);
   if (p.gmorder) (void)hipFree(p.gmorder);
   if (p.ws) (void)hipFree(p.ws);
+  if (p.xbuf) (void)hipFree(p.xbuf);
   p = Plan();
 }
 
@@ -606,8 +764,7 @@ void clear_cache_locked(StackCache &C) {
 
 eb_status run_ops_direct(const eb_qlinear_op *ops, int32_t n_ops, hipStream_t s) {
   for (int32_t i = 0; i < n_ops; ++i) {
-    const eb_qlinear_op &o = ops[i];
-    eb_status st = launch_linear(&o.w, o.x, o.x_type, o.m, o.y, o.y_type, EB_PATH_AUTO, s);
+    eb_status st = launch_op(ops[i], EB_PATH_AUTO, s);
     if (st != EB_OK) return st;
   }
   return EB_OK;
@@ -680,9 +837,18 @@ eb_status eb_qweights_from_canonical(int32_t type, const void *src, int64_t n, i
 
 eb_status eb_qlinear_ex(const eb_qweights *w, const void *x, int32_t x_type, int64_t m, void *y,
                         int32_t y_type, int32_t path, hipStream_t stream) {
-  eb_status st = check_linear(w, x, x_type, m, y, y_type, path);
+  if (!w) return EB_ERR_INVALID;
+  const eb_qlinear_op o = plain_op(w, x, x_type, m, y, y_type);
+  eb_status st = check_op(o, path);
   if (st != EB_OK) return st;
-  return launch_linear(w, x, x_type, m, y, y_type, path, stream);
+  return launch_op(o, path, stream);
+}
+
+eb_status eb_qlinear_fused(const eb_qlinear_op *op, int32_t path, hipStream_t stream) {
+  if (!op) return EB_ERR_INVALID;
+  eb_status st = check_op(*op, path);
+  if (st != EB_OK) return st;
+  return launch_op(*op, path, stream);
 }
 
 eb_status eb_qlinear(const eb_qweights *w, const void *x, int32_t x_type, int64_t m, void *y,
@@ -701,7 +867,7 @@ eb_status eb_qlinear_stack(const eb_qlinear_op *ops, int32_t n_ops, hipStream_t 
   if (!ops) return EB_ERR_INVALID;
   for (int32_t i = 0; i < n_ops; ++i) {
     const eb_qlinear_op &o = ops[i];
-    eb_status st = check_linear(&o.w, o.x, o.x_type, o.m, o.y, o.y_type, EB_PATH_AUTO);
+    eb_status st = check_op(o, EB_PATH_AUTO);
     if (st != EB_OK) return st;
   }
   // Inside a caller's own stream capture, record plain launches into it.
@@ -732,6 +898,7 @@ eb_status eb_qlinear_stack(const eb_qlinear_op *ops, int32_t n_ops, hipStream_t 
       destroy_plan(P);
       return st;
     }
+    if (std::getenv("EB_STACK_DEBUG")) print_plan(ops, P);
     if (use_graph) {
       if (!C.capture_stream[dev] &&
           hipStreamCreateWithFlags(&C.capture_stream[dev], hipStreamNonBlocking) != hipSuccess) {
@@ -763,14 +930,18 @@ int32_t eb_qlinear_stack_launches(const eb_qlinear_op *ops, int32_t n_ops) {
   if (n_ops < 0 || (n_ops > 0 && !ops)) return EB_ERR_INVALID;
   for (int32_t i = 0; i < n_ops; ++i) {
     const eb_qlinear_op &o = ops[i];
-    eb_status st = check_linear(&o.w, o.x, o.x_type, o.m, o.y, o.y_type, EB_PATH_AUTO);
+    eb_status st = check_op(o, EB_PATH_AUTO);
     if (st != EB_OK) return st;
   }
   Plan P;
   build_plan(ops, n_ops, false, P);
   int32_t launches = 0;
-  for (const Step &st : P.steps)
-    if (st.op < 0 || ops[st.op].m > 0) launches += (st.mfma && st.mp.splits > 1) ? 2 : 1;
+  for (const Step &st : P.steps) {
+    launches += (int32_t)st.norms.size();
+    if (st.op >= 0 && ops[st.op].m == 0) continue;
+    launches += (st.mfma && st.mp.splits > 1) ? 2 : 1;
+    if (st.mfma && ops[st.op].prologue == EB_PRO_RMSNORM) ++launches;
+  }
   return launches;
 }
 

@@ -35,6 +35,19 @@ inline Layout layout_of(int32_t type, int64_t n, int64_t k) {
   return L;
 }
 
+// Fused steps of one op (EB_PRO_*, EB_EPI_*) as the kernels take them.  The
+// GEMV kernels apply the RMS-normalisation prologue themselves while staging
+// x (x is then the fp32 residual stream, `gamma` its weights); the MFMA
+// kernels read activations normalised beforehand by launch_rmsnorm and only
+// apply the epilogue.  `r` is the residual of EB_EPI_ADD ([m][n] of the
+// output type, possibly the output itself).
+struct Fuse {
+  const float *gamma;
+  const void *r;
+  float eps;
+  int16_t pro, epi;
+};
+
 // ---- launchers (each returns hipSuccess or the launch error) ----
 hipError_t launch_quantize(int32_t type, const float *w, int64_t n, int64_t k, void *out,
                            hipStream_t s);
@@ -47,14 +60,19 @@ hipError_t launch_from_canonical(int32_t type, const void *src, int64_t n, int64
 constexpr int64_t kGemvMaxM = 8;
 constexpr int64_t kGemvMaxMK = 65536;
 hipError_t launch_gemv(int32_t type, const void *wdata, int64_t n, int64_t k, const void *x,
-                       int32_t xt, int64_t m, void *y, int32_t yt, hipStream_t s);
+                       int32_t xt, int64_t m, void *y, int32_t yt, const Fuse &f, hipStream_t s);
+
+// x_hat[i][j] = round_xt(h[i][j] * gamma[j] / sqrt(eps + mean_j h[i][j]^2)),
+// h fp32 [m][k], x_hat [m][k] of xt (EB_F16 / EB_BF16); one workgroup per row.
+hipError_t launch_rmsnorm(const float *h, const float *gamma, float eps, int64_t m, int64_t k,
+                          int32_t xt, void *out, hipStream_t s);
 
 // Fused m == 1 GEMV over several independent matrices (one launch).  The
 // table lives in device memory; unit_begin (prefix sum of n * ku) ascends.
 struct M1Op {
   const uint8_t *w;   // planar weights
-  const uint16_t *x;  // activations [k]
-  void *y;            // outputs [n]
+  const void *x;      // activations [k] (16-bit; fp32 h with the normalisation prologue)
+  void *y;            // outputs [n] (gate/up epilogue: [n / 2])
   int64_t n;
   int64_t d_off;      // scale-plane offset
   int64_t ds;         // scale-plane row stride (elements)
@@ -63,12 +81,15 @@ struct M1Op {
   int32_t ku;         // 16-byte code units per row
   int32_t yt;
   int32_t pad;
+  Fuse f;
 };
-bool m1_fusable(int32_t type, int64_t m, int64_t k);
+// An m == 1 op the fused GEMV launch takes (k within its slot range; the
+// gate/up epilogue needs at least two rows per wave).
+bool m1_fusable(int32_t type, int64_t m, int64_t k, int32_t epi);
 int m1_slots(int32_t type, int64_t k);
 // Fills *o for one matrix; returns its number of work units (n * ku).
 int64_t m1_fill(int32_t type, const void *wdata, int64_t n, int64_t k, const void *x, void *y,
-                int32_t yt, int64_t unit_begin, M1Op *o);
+                int32_t yt, const Fuse &f, int64_t unit_begin, M1Op *o);
 // All matrices of one launch have the same slot count ns (m1_slots); units
 // and rows are the totals over the table.
 hipError_t launch_gemv_m1_multi(int32_t type, int32_t xt, int ns, const M1Op *dev_ops, int nops,
@@ -87,8 +108,8 @@ struct MfmaPlan {
 MfmaPlan plan_mfma(int32_t type, int64_t m, int64_t n, int64_t k, bool allow_split);
 // ws == nullptr runs the plan's configuration unsplit.
 hipError_t launch_mfma(int32_t type, const void *wdata, int64_t n, int64_t k, const void *x,
-                       int32_t xt, int64_t m, void *y, int32_t yt, const MfmaPlan &plan, float *ws,
-                       hipStream_t s);
+                       int32_t xt, int64_t m, void *y, int32_t yt, const Fuse &f,
+                       const MfmaPlan &plan, float *ws, hipStream_t s);
 int mfma_tile_count();
 int mfma_cfg_bm(int cfg);        // rows of a tile configuration
 double mfma_cfg_rate(int cfg);   // its measured full-chip rate, TFLOP/s
@@ -102,6 +123,7 @@ struct GOp {
   void *y;            // outputs [m][n]
   int64_t n, k, d_off, ds, m;
   int32_t yt, pad;
+  Fuse f;
 };
 // Chooses the tile configuration for the group and fills the workgroup table
 // (op, tile); returns the configuration, or -1 when none fits every op.
@@ -121,6 +143,7 @@ struct MMOp {
   int64_t unit_end;    // tiles of this op and all ops before it
   int32_t ds, m, n, k; // ds: scale-plane row stride (elements)
   int32_t tiles_n, nk, yt, pad;
+  Fuse f;
 };
 constexpr int64_t kMMaxK = int64_t(1) << 22;  // k < this keeps per-tile byte spans in 31 bits
 int mm_cfg(int64_t max_m);                // tile configuration for a run

@@ -30,6 +30,7 @@
 #include <cstdlib>
 
 #include "eb_internal.h"
+#include "epilogue.h"
 
 namespace eb {
 namespace {
@@ -163,19 +164,83 @@ __device__ inline double x_to_f64(uint32_t h) {
   return (double)__builtin_bit_cast(float, h << 16);
 }
 
+// Per-row factors of the RMS-normalisation prologue, r_i = 1 / sqrt(eps +
+// mean_j h[i][j]^2) for the m <= MT rows of the fp32 residual stream h, in
+// every thread of the workgroup.  Each thread sums the squares of a strided
+// part of every row in fp32; the 64 lanes of a wave, then the waves (through
+// `red`, kWaves * MT floats of LDS), are added in a fixed order.  Ends with a
+// barrier after which `red` may be reused.
+template <int MT>
+__device__ inline void norm_factors(const float *__restrict__ h, int m, int64_t k, float eps,
+                                    float *red, float (&rs)[MT]) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int mm = 0; mm < MT; ++mm) {
+    float ss = 0.f;
+    if (mm < m) {
+      const float4 *row = reinterpret_cast<const float4 *>(h + (int64_t)mm * k);
+      for (int64_t i = threadIdx.x; i < k / 4; i += blockDim.x) {
+        const float4 v = row[i];
+        ss = __builtin_fmaf(v.x, v.x, ss);
+        ss = __builtin_fmaf(v.y, v.y, ss);
+        ss = __builtin_fmaf(v.z, v.z, ss);
+        ss = __builtin_fmaf(v.w, v.w, ss);
+      }
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) ss += __shfl_xor(ss, o);
+    if (lane == 0) red[wave * MT + mm] = ss;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int mm = 0; mm < MT; ++mm) {
+    float ss = 0.f;
+    for (int w = 0; w < kWaves; ++w) ss += red[w * MT + mm];
+    rs[mm] = 1.0f / __builtin_sqrtf(ss / (float)k + eps);
+  }
+  __syncthreads();
+}
+
+template <int XT>
+__device__ inline uint32_t pack_x16(float a, float b) {
+  if (XT == EB_F16)
+    return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)a) |
+           ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)b) << 16);
+  return (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)a) |
+         ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)b) << 16);
+}
+
 // Stage x[m][k] (m <= MT rows; missing rows are zero) into LDS in the pair
-// order of unit_dot<QT, XT>, plus one offset per (row, unit).
+// order of unit_dot<QT, XT>, plus one offset per (row, unit).  With the
+// normalisation prologue (norm) x is the fp32 residual stream and
+// the staged activations are round_XT(h * gamma * rs[row]).
 template <int QT, int XT, int MT>
-__device__ inline void stage_x(const uint16_t *__restrict__ x, int m, int64_t k, int64_t ku,
-                               uint4 *xs, float *xoff, int64_t pitch) {
+__device__ __attribute__((always_inline)) inline void stage_x(
+    const void *__restrict__ xv, int m, int64_t k, int64_t ku, uint4 *xs, float *xoff,
+    int64_t pitch, bool norm, const float *__restrict__ gamma, const float (&rs)[MT]) {
   constexpr int E = Unit<QT>::kElems;
   constexpr int CH = Unit<QT>::kChunks;
   for (int64_t idx = threadIdx.x; idx < (int64_t)MT * ku; idx += blockDim.x) {
     const int mm = (int)(idx / ku);
     const int64_t u = idx % ku;
     uint32_t r[E / 2];  // raw dwords: r[j] = (h[2j], h[2j+1])
-    if (mm < m) {
-      const uint4 *src = reinterpret_cast<const uint4 *>(x + (int64_t)mm * k + u * E);
+    if (mm < m && norm) {
+      const float4 *src = reinterpret_cast<const float4 *>(static_cast<const float *>(xv) +
+                                                           (int64_t)mm * k + u * E);
+      const float4 *gs = reinterpret_cast<const float4 *>(gamma + u * E);
+      float f = 0.f;
+#pragma unroll
+      for (int i = 0; i < MT; ++i)
+        if (i == mm) f = rs[i];
+#pragma unroll
+      for (int c = 0; c < E / 4; ++c) {
+        const float4 v = src[c], g = gs[c];
+        r[2 * c] = pack_x16<XT>(v.x * g.x * f, v.y * g.y * f);
+        r[2 * c + 1] = pack_x16<XT>(v.z * g.z * f, v.w * g.w * f);
+      }
+    } else if (mm < m) {
+      const uint4 *src = reinterpret_cast<const uint4 *>(static_cast<const uint16_t *>(xv) +
+                                                         (int64_t)mm * k + u * E);
 #pragma unroll
       for (int c = 0; c < E / 8; ++c) {
         uint4 t = src[c];
@@ -231,14 +296,17 @@ __device__ inline void stage_x(const uint16_t *__restrict__ x, int m, int64_t k,
 template <int QT, int XT, int MT, int RS>
 __global__ void __launch_bounds__(64 * kWaves)
     gemv_kernel(const uint8_t *__restrict__ wdata, int64_t n, int64_t k, int64_t d_off, int64_t ds,
-                const uint16_t *__restrict__ x, int m, void *__restrict__ y, int yt) {
+                const void *__restrict__ x, int m, void *__restrict__ y, int yt, Fuse f) {
   constexpr int CH = Unit<QT>::kChunks;
   const int64_t ku = k / Unit<QT>::kElems;
   extern __shared__ uint4 smem[];
   uint4 *xs = smem;
   float *xoff = reinterpret_cast<float *>(smem + (int64_t)MT * CH * ku);
 
-  stage_x<QT, XT, MT>(x, m, k, ku, xs, xoff, ku);
+  float rs[MT];
+  const bool norm = f.pro == EB_PRO_RMSNORM;
+  if (norm) norm_factors<MT>(static_cast<const float *>(x), m, k, f.eps, reinterpret_cast<float *>(xs), rs);
+  stage_x<QT, XT, MT>(x, m, k, ku, xs, xoff, ku, norm, f.gamma, rs);
   __syncthreads();
 
   const uint4 *__restrict__ qs = reinterpret_cast<const uint4 *>(wdata);
@@ -291,7 +359,18 @@ __global__ void __launch_bounds__(64 * kWaves)
 #pragma unroll
       for (int mm = 0; mm < MT; ++mm) acc[s][mm] = dpp_row_sum(acc[s][mm]);
 
-    if (c == 0) {
+    if (f.epi == EB_EPI_GLU) {
+      // rows r (even rsub: gate) and r + 1 (odd rsub: up) sit 16 lanes apart
+#pragma unroll
+      for (int s = 0; s < RS; ++s)
+#pragma unroll
+        for (int mm = 0; mm < MT; ++mm) {
+          const float up = __shfl_xor(acc[s][mm], 16);
+          const int64_t r = it * kRowsPerItem + s * kRowsPerSet + rsub;
+          if (c == 0 && (rsub & 1) == 0 && r < n && mm < m)
+            store_y(y, (int64_t)mm * (n / 2) + r / 2, silu_mul(acc[s][mm], up), yt);
+        }
+    } else if (c == 0) {
 #pragma unroll
       for (int s = 0; s < RS; ++s) {
         const int64_t r = it * kRowsPerItem + s * kRowsPerSet + rsub;
@@ -299,10 +378,7 @@ __global__ void __launch_bounds__(64 * kWaves)
 #pragma unroll
         for (int mm = 0; mm < MT; ++mm) {
           if (mm >= m) continue;
-          if (yt == EB_F32)
-            reinterpret_cast<float *>(y)[(int64_t)mm * n + r] = acc[s][mm];
-          else
-            reinterpret_cast<__bf16 *>(y)[(int64_t)mm * n + r] = (__bf16)acc[s][mm];
+          put_y(y, (int64_t)mm * n + r, acc[s][mm], yt, f);
         }
       }
     }
@@ -407,8 +483,8 @@ __device__ inline __amdgpu_buffer_rsrc_t rsrc(const void *base, uint32_t bytes) 
 // with the staging.
 template <int QT, int XT, int NS, int R>
 __device__ __attribute__((always_inline)) inline void m1_rows(const uint8_t *__restrict__ wdata, int64_t n, int64_t k,
-                               int64_t d_off, int64_t ds, const uint16_t *__restrict__ x,
-                               void *__restrict__ y, int yt, int64_t g, int64_t g_end,
+                               int64_t d_off, int64_t ds, const void *__restrict__ x,
+                               void *__restrict__ y, int yt, const Fuse &f, int64_t g, int64_t g_end,
                                int64_t gstride, uint4 *smem) {
   constexpr int CH = Unit<QT>::kChunks;
   // LDS: CH chunk rows of P entries; entry 64 * NS of every row is zero and
@@ -452,9 +528,19 @@ __device__ __attribute__((always_inline)) inline void m1_rows(const uint8_t *__r
       }
     }
   };
-  // weight loads of the first group are in flight while x is staged
-  if (g < g_end) load_group(g);
-  stage_x<QT, XT, 1>(x, 1, k, ku, xs, xoff, P);
+  float rs[1] = {0.f};
+  if (f.pro == EB_PRO_RMSNORM) {
+    // normalise x first, then load the first group: the fp32 staging needs
+    // registers that the group's weights would otherwise hold
+    norm_factors<1>(static_cast<const float *>(x), 1, k, f.eps, reinterpret_cast<float *>(xs), rs);
+    stage_x<QT, XT, 1>(x, 1, k, ku, xs, xoff, P, true, f.gamma, rs);
+    __builtin_amdgcn_sched_barrier(0);
+    if (g < g_end) load_group(g);
+  } else {
+    // weight loads of the first group are in flight while x is staged
+    if (g < g_end) load_group(g);
+    stage_x<QT, XT, 1>(x, 1, k, ku, xs, xoff, P, false, f.gamma, rs);
+  }
   if (threadIdx.x < CH) xs[threadIdx.x * P + 64 * NS] = make_uint4(0, 0, 0, 0);
   if (threadIdx.x == 0) xoff[64 * NS] = 0.f;
   __syncthreads();
@@ -479,11 +565,17 @@ __device__ __attribute__((always_inline)) inline void m1_rows(const uint8_t *__r
     bool writer;
     const float tot = reduce_rows<R>(acc, lane, rr, writer);
     const int64_t row = g * R + rr;
-    if (writer && row < n) {
-      if (yt == EB_F32)
-        reinterpret_cast<float *>(y)[row] = tot;
-      else
-        reinterpret_cast<__bf16 *>(y)[row] = (__bf16)tot;
+    if constexpr (R >= 2) {
+      if (f.epi == EB_EPI_GLU) {
+        // the up row (odd) of a pair is held R/2 ... lanes away: 8 (R = 8),
+        // 16 (R = 4) or 32 (R = 2) lanes, see reduce_rows
+        const float up = __shfl_xor(tot, R == 8 ? 8 : (R == 4 ? 16 : 32));
+        if (writer && (rr & 1) == 0 && row < n) store_y(y, row / 2, silu_mul(tot, up), yt);
+      } else if (writer && row < n) {
+        put_y(y, row, tot, yt, f);
+      }
+    } else {
+      if (writer && row < n) put_y(y, row, tot, yt, f);
     }
     g += gstride;
     // the weight registers are free again: load the next group into them
@@ -498,10 +590,10 @@ __device__ __attribute__((always_inline)) inline void m1_rows(const uint8_t *__r
 template <int QT, int XT, int NS, int R, int WPE>
 __global__ void __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(WPE)))
     gemv_m1_kernel(const uint8_t *__restrict__ wdata, int64_t n, int64_t k, int64_t d_off,
-                   int64_t ds, const uint16_t *__restrict__ x, void *__restrict__ y, int yt) {
+                   int64_t ds, const void *__restrict__ x, void *__restrict__ y, int yt, Fuse f) {
   extern __shared__ uint4 smem[];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
-  m1_rows<QT, XT, NS, R>(wdata, n, k, d_off, ds, x, y, yt, (int64_t)blockIdx.x * kWaves + wave,
+  m1_rows<QT, XT, NS, R>(wdata, n, k, d_off, ds, x, y, yt, f, (int64_t)blockIdx.x * kWaves + wave,
                          (n + R - 1) / R, (int64_t)gridDim.x * kWaves, smem);
 }
 
@@ -543,7 +635,7 @@ __global__ void __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_e
     };
     const int64_t r0 = row_at(u0), r1 = row_at(u1);
     if (r0 >= r1) continue;  // uniform across the workgroup
-    m1_rows<QT, XT, NS, R>(o.w, o.n, o.k, o.d_off, o.ds, o.x, o.y, o.yt, r0 / R + wave,
+    m1_rows<QT, XT, NS, R>(o.w, o.n, o.k, o.d_off, o.ds, o.x, o.y, o.yt, o.f, r0 / R + wave,
                            (r1 + R - 1) / R, kWaves, smem);
     __syncthreads();  // the next matrix restages LDS
   }
@@ -552,7 +644,7 @@ __global__ void __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_e
 // ---------------------------------------------------------------------------
 template <int QT, int XT, int NS, int R, int WPE>
 hipError_t launch_m1_t(const void *wdata, int64_t n, int64_t k, const void *x, void *y, int32_t yt,
-                       hipStream_t s, int wg_per_cu) {
+                       const Fuse &f, hipStream_t s, int wg_per_cu) {
   const Layout L = layout_of(QT, n, k);
   const int64_t ku = k / Unit<QT>::kElems;
   const size_t lds = (size_t)(64 * NS + 1) * (Unit<QT>::kChunks * 16 + 4);
@@ -562,7 +654,7 @@ hipError_t launch_m1_t(const void *wdata, int64_t n, int64_t k, const void *x, v
   const int64_t cap = (int64_t)device_cu_count() * wg_per_cu;
   if (grid > cap) grid = cap;
   gemv_m1_kernel<QT, XT, NS, R, WPE><<<(unsigned)grid, 64 * kWaves, lds, s>>>(
-      (const uint8_t *)wdata, n, k, L.d_off, L.ds, (const uint16_t *)x, y, yt);
+      (const uint8_t *)wdata, n, k, L.d_off, L.ds, x, y, yt, f);
   return hipGetLastError();
 }
 
@@ -584,11 +676,11 @@ M1Shape m1_shape(int64_t ns) {
 
 template <int QT, int XT, int NS>
 hipError_t launch_m1_ns(const void *wdata, int64_t n, int64_t k, const void *x, void *y, int32_t yt,
-                        hipStream_t s) {
+                        const Fuse &f, hipStream_t s) {
   const M1Shape v = m1_shape(NS);
 #define EB_M1(R_, W_)                                                                      \
   if (v.r == R_ && v.wpe == W_)                                                           \
-    return launch_m1_t<QT, XT, NS, R_, W_>(wdata, n, k, x, y, yt, s, v.wg);
+    return launch_m1_t<QT, XT, NS, R_, W_>(wdata, n, k, x, y, yt, f, s, v.wg);
   EB_M1(1, 4) EB_M1(2, 4) EB_M1(4, 4) EB_M1(1, 2) EB_M1(2, 2) EB_M1(4, 2)
 #undef EB_M1
   return hipErrorInvalidValue;
@@ -596,23 +688,23 @@ hipError_t launch_m1_ns(const void *wdata, int64_t n, int64_t k, const void *x, 
 
 template <int QT, int XT>
 hipError_t launch_m1(const void *wdata, int64_t n, int64_t k, const void *x, void *y, int32_t yt,
-                     hipStream_t s) {
+                     const Fuse &f, hipStream_t s) {
   const int64_t ns = (k / Unit<QT>::kElems + 63) / 64;
   switch (ns) {
-    case 1: return launch_m1_ns<QT, XT, 1>(wdata, n, k, x, y, yt, s);
-    case 2: return launch_m1_ns<QT, XT, 2>(wdata, n, k, x, y, yt, s);
-    case 3: return launch_m1_ns<QT, XT, 3>(wdata, n, k, x, y, yt, s);
-    case 4: return launch_m1_ns<QT, XT, 4>(wdata, n, k, x, y, yt, s);
-    case 5: return launch_m1_ns<QT, XT, 5>(wdata, n, k, x, y, yt, s);
-    case 6: return launch_m1_ns<QT, XT, 6>(wdata, n, k, x, y, yt, s);
-    case 7: return launch_m1_ns<QT, XT, 7>(wdata, n, k, x, y, yt, s);
-    default: return launch_m1_ns<QT, XT, 8>(wdata, n, k, x, y, yt, s);
+    case 1: return launch_m1_ns<QT, XT, 1>(wdata, n, k, x, y, yt, f, s);
+    case 2: return launch_m1_ns<QT, XT, 2>(wdata, n, k, x, y, yt, f, s);
+    case 3: return launch_m1_ns<QT, XT, 3>(wdata, n, k, x, y, yt, f, s);
+    case 4: return launch_m1_ns<QT, XT, 4>(wdata, n, k, x, y, yt, f, s);
+    case 5: return launch_m1_ns<QT, XT, 5>(wdata, n, k, x, y, yt, f, s);
+    case 6: return launch_m1_ns<QT, XT, 6>(wdata, n, k, x, y, yt, f, s);
+    case 7: return launch_m1_ns<QT, XT, 7>(wdata, n, k, x, y, yt, f, s);
+    default: return launch_m1_ns<QT, XT, 8>(wdata, n, k, x, y, yt, f, s);
   }
 }
 
 template <int QT, int XT, int MT, int RS>
 hipError_t launch_t(const void *wdata, int64_t n, int64_t k, const void *x, int64_t m, void *y,
-                    int32_t yt, hipStream_t s) {
+                    int32_t yt, const Fuse &f, hipStream_t s) {
   const Layout L = layout_of(QT, n, k);
   const int64_t ku = k / Unit<QT>::kElems;
   const size_t lds = (size_t)MT * ku * (Unit<QT>::kChunks * 16 + 4);
@@ -626,20 +718,22 @@ hipError_t launch_t(const void *wdata, int64_t n, int64_t k, const void *x, int6
                                        (int)lds);
     if (e != hipSuccess) return e;
   }
-  kern<<<(unsigned)grid, 64 * kWaves, lds, s>>>((const uint8_t *)wdata, n, k, L.d_off, L.ds,
-                                                (const uint16_t *)x, (int)m, y, yt);
+  kern<<<(unsigned)grid, 64 * kWaves, lds, s>>>((const uint8_t *)wdata, n, k, L.d_off, L.ds, x,
+                                                (int)m, y, yt, f);
   return hipGetLastError();
 }
 
 template <int QT, int XT>
 hipError_t launch_m(const void *wdata, int64_t n, int64_t k, const void *x, int64_t m, void *y,
-                    int32_t yt, hipStream_t s) {
-  if (m <= 1 && k / Unit<QT>::kElems <= 64 * kM1MaxSlots)
-    return launch_m1<QT, XT>(wdata, n, k, x, y, yt, s);
-  if (m <= 1) return launch_t<QT, XT, 1, 2>(wdata, n, k, x, m, y, yt, s);
-  if (m <= 2) return launch_t<QT, XT, 2, 2>(wdata, n, k, x, m, y, yt, s);
-  if (m <= 4) return launch_t<QT, XT, 4, 1>(wdata, n, k, x, m, y, yt, s);
-  return launch_t<QT, XT, 8, 1>(wdata, n, k, x, m, y, yt, s);
+                    int32_t yt, const Fuse &f, hipStream_t s) {
+  const int64_t ns = (k / Unit<QT>::kElems + 63) / 64;
+  // the gate/up epilogue needs both rows of a pair in one wave (R >= 2)
+  const bool m1_ok = ns <= kM1MaxSlots && (f.epi != EB_EPI_GLU || m1_shape(ns).r >= 2);
+  if (m <= 1 && m1_ok) return launch_m1<QT, XT>(wdata, n, k, x, y, yt, f, s);
+  if (m <= 1) return launch_t<QT, XT, 1, 2>(wdata, n, k, x, m, y, yt, f, s);
+  if (m <= 2) return launch_t<QT, XT, 2, 2>(wdata, n, k, x, m, y, yt, f, s);
+  if (m <= 4) return launch_t<QT, XT, 4, 1>(wdata, n, k, x, m, y, yt, f, s);
+  return launch_t<QT, XT, 8, 1>(wdata, n, k, x, m, y, yt, f, s);
 }
 
 template <int QT, int XT, int NS>
@@ -671,9 +765,10 @@ hipError_t launch_multi_q(const M1Op *ops, int nops, int64_t items, int64_t rows
 
 }  // namespace
 
-bool m1_fusable(int32_t type, int64_t m, int64_t k) {
+bool m1_fusable(int32_t type, int64_t m, int64_t k, int32_t epi) {
   const int64_t e = (type == EB_Q4_0) ? Unit<EB_Q4_0>::kElems : Unit<EB_Q8_0>::kElems;
-  return m == 1 && (k / e + 63) / 64 <= kM1MaxSlots;
+  const int64_t ns = (k / e + 63) / 64;
+  return m == 1 && ns <= kM1MaxSlots && (epi != EB_EPI_GLU || m1_multi_rows((int)ns) >= 2);
 }
 
 int m1_slots(int32_t type, int64_t k) {
@@ -682,12 +777,13 @@ int m1_slots(int32_t type, int64_t k) {
 }
 
 int64_t m1_fill(int32_t type, const void *wdata, int64_t n, int64_t k, const void *x, void *y,
-                int32_t yt, int64_t unit_begin, M1Op *o) {
+                int32_t yt, const Fuse &f, int64_t unit_begin, M1Op *o) {
   const int64_t e = (type == EB_Q4_0) ? Unit<EB_Q4_0>::kElems : Unit<EB_Q8_0>::kElems;
   const Layout L = layout_of(type, n, k);
   o->w = (const uint8_t *)wdata;
-  o->x = (const uint16_t *)x;
+  o->x = x;
   o->y = y;
+  o->f = f;
   o->n = n;
   o->d_off = L.d_off;
   o->ds = L.ds;
@@ -709,13 +805,13 @@ hipError_t launch_gemv_m1_multi(int32_t type, int32_t xt, int ns, const M1Op *de
 }
 
 hipError_t launch_gemv(int32_t type, const void *wdata, int64_t n, int64_t k, const void *x,
-                       int32_t xt, int64_t m, void *y, int32_t yt, hipStream_t s) {
+                       int32_t xt, int64_t m, void *y, int32_t yt, const Fuse &f, hipStream_t s) {
   if (type == EB_Q4_0) {
-    if (xt == EB_F16) return launch_m<EB_Q4_0, EB_F16>(wdata, n, k, x, m, y, yt, s);
-    return launch_m<EB_Q4_0, EB_BF16>(wdata, n, k, x, m, y, yt, s);
+    if (xt == EB_F16) return launch_m<EB_Q4_0, EB_F16>(wdata, n, k, x, m, y, yt, f, s);
+    return launch_m<EB_Q4_0, EB_BF16>(wdata, n, k, x, m, y, yt, f, s);
   }
-  if (xt == EB_F16) return launch_m<EB_Q8_0, EB_F16>(wdata, n, k, x, m, y, yt, s);
-  return launch_m<EB_Q8_0, EB_BF16>(wdata, n, k, x, m, y, yt, s);
+  if (xt == EB_F16) return launch_m<EB_Q8_0, EB_F16>(wdata, n, k, x, m, y, yt, f, s);
+  return launch_m<EB_Q8_0, EB_BF16>(wdata, n, k, x, m, y, yt, f, s);
 }
 
 }  // namespace eb

@@ -38,6 +38,7 @@
 #include <vector>
 
 #include "eb_internal.h"
+#include "epilogue.h"
 #include "mfma_common.h"
 
 
@@ -51,13 +52,14 @@ template <int QT, int XT, int BM, int BN, int WM, int WN, bool G = false>
 __global__ void __launch_bounds__(WM *WN * 64)
     mfma_kernel(const uint8_t *__restrict__ wdata_, int64_t n_, int64_t k_, int64_t d_off_,
                 int64_t ds_, const uint16_t *__restrict__ x_, int64_t m_, void *__restrict__ y_,
-                int yt_, int kts_, float *__restrict__ ws, int64_t ws_stride,
+                int yt_, Fuse f_, int kts_, float *__restrict__ ws, int64_t ws_stride,
                 const GOp *__restrict__ gops, const int2 *__restrict__ gorder) {
   const uint8_t *wdata = wdata_;
   const uint16_t *x = x_;
   void *y = y_;
   int64_t n = n_, k = k_, d_off = d_off_, ds = ds_, m = m_;
   int yt = yt_, kts = kts_;
+  Fuse f = f_;
   int64_t gtile = 0;
   if constexpr (G) {
     const int2 e = gorder[blockIdx.x];
@@ -72,6 +74,7 @@ __global__ void __launch_bounds__(WM *WN * 64)
     ds = o.ds;
     m = o.m;
     yt = o.yt;
+    f = o.f;
     kts = (int)((k + kBK - 1) / kBK);
     gtile = e.y;
   }
@@ -303,7 +306,27 @@ __global__ void __launch_bounds__(WM *WN * 64)
     step(kt + 5, sA2, sA1, sB1, sB0, S0, S2, true);
   }
 
-  // epilogue: lane holds column (lane & 31), rows 8*(r/4) + 4*(lane/32) + r%4
+  // epilogue: lane holds column (lane & 31), rows 8*(r/4) + 4*(lane/32) + r%4;
+  // the gate/up pair of columns 2c, 2c + 1 sits in lanes l, l ^ 1 (n is even,
+  // so both or neither are inside the tile)
+  if (!ws && f.epi == EB_EPI_GLU) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const int cl = wn * TN + j * 32 + (lane & 31);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float g = acc[i][j][r];
+          const float u = __builtin_bit_cast(
+              float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, g), 0xB1, 0xF, 0xF, true));
+          const int rl = wm * TM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+          if (cl >= rows_n || rl >= rows_m || (cl & 1)) continue;
+          store_y(y, (m0 + rl) * (n / 2) + (n0 + cl) / 2, silu_mul(g, u), yt);
+        }
+      }
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < FM; ++i)
 #pragma unroll
@@ -317,10 +340,8 @@ __global__ void __launch_bounds__(WM *WN * 64)
         const int64_t o = (m0 + rl) * n + n0 + cl;
         if (ws)
           ws[split * ws_stride + o] = acc[i][j][r];
-        else if (yt == EB_F32)
-          reinterpret_cast<float *>(y)[o] = acc[i][j][r];
         else
-          reinterpret_cast<__bf16 *>(y)[o] = (__bf16)acc[i][j][r];
+          put_y(y, o, acc[i][j][r], yt, f);
       }
     }
 }
@@ -339,13 +360,14 @@ bool fits_offsets(int64_t n, int64_t k, int bm = BM, int bn = BN) {
 
 template <int QT, int XT, int BM, int BN, int WM, int WN>
 hipError_t launch_t(const void *wdata, int64_t n, int64_t k, const void *x, int64_t m, void *y,
-                    int32_t yt, int splits, int kts, float *ws, int64_t ws_stride, hipStream_t s) {
+                    int32_t yt, const Fuse &f, int splits, int kts, float *ws, int64_t ws_stride,
+                    hipStream_t s) {
   const Layout L = layout_of(QT, n, k);
   const int64_t tiles = ((m + BM - 1) / BM) * ((n + BN - 1) / BN);
   if (tiles * splits > 0x7fffffff) return hipErrorInvalidValue;
   if (!fits_offsets<QT, BM, BN>(n, k)) return hipErrorInvalidValue;
   mfma_kernel<QT, XT, BM, BN, WM, WN><<<(unsigned)(tiles * splits), WM * WN * 64, 0, s>>>(
-      (const uint8_t *)wdata, n, k, L.d_off, L.ds, (const uint16_t *)x, m, y, yt, kts,
+      (const uint8_t *)wdata, n, k, L.d_off, L.ds, (const uint16_t *)x, m, y, yt, f, kts,
       splits > 1 ? ws : nullptr, ws_stride, nullptr, nullptr);
   return hipGetLastError();
 }
@@ -354,43 +376,50 @@ template <int QT, int XT, int BM, int BN, int WM, int WN>
 hipError_t launch_g(const GOp *ops, const int2 *order, int64_t entries, hipStream_t s) {
   if (entries <= 0 || entries > 0x7fffffff) return hipErrorInvalidValue;
   mfma_kernel<QT, XT, BM, BN, WM, WN, true><<<(unsigned)entries, WM * WN * 64, 0, s>>>(
-      nullptr, 0, 0, 0, 0, nullptr, 0, nullptr, 0, 0, nullptr, 0, ops, order);
+      nullptr, 0, 0, 0, 0, nullptr, 0, nullptr, 0, Fuse{}, 0, nullptr, 0, ops, order);
   return hipGetLastError();
 }
 
 // y = sum over s of ws[s] (in order s = 0, 1, ..., so the result does not
-// depend on scheduling), converted to the output type.  Four outputs per
-// thread; ws_stride is a multiple of 4 so every float4 access is aligned.
+// depend on scheduling), converted to the output type, with the op's
+// epilogue.  Four outputs per thread; ws_stride is a multiple of 4 so every
+// float4 access is aligned; with the gate/up epilogue n is even, so the four
+// (a multiple of 4 into the flat [m][n] index) are two gate/up pairs.
 __global__ void __launch_bounds__(256)
     splitk_reduce(const float *__restrict__ ws, int splits, int64_t ws_stride, int64_t count,
-                  void *__restrict__ y, int yt) {
+                  void *__restrict__ y, int yt, Fuse f) {
   const int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
   if (i >= count) return;
-  if (i + 4 <= count) {
-    float4 a = *reinterpret_cast<const float4 *>(ws + i);
+  float a[4] = {0.f, 0.f, 0.f, 0.f};
+  const int e = (int)(count - i < 4 ? count - i : 4);
+  if (e == 4) {
+    float4 v = *reinterpret_cast<const float4 *>(ws + i);
     for (int p = 1; p < splits; ++p) {
       const float4 b = *reinterpret_cast<const float4 *>(ws + p * ws_stride + i);
-      a.x += b.x;
-      a.y += b.y;
-      a.z += b.z;
-      a.w += b.w;
+      v.x += b.x;
+      v.y += b.y;
+      v.z += b.z;
+      v.w += b.w;
     }
-    if (yt == EB_F32) {
-      *reinterpret_cast<float4 *>(reinterpret_cast<float *>(y) + i) = a;
-    } else {
-      typedef __bf16 bf4 __attribute__((ext_vector_type(4)));
-      const bf4 v = {(__bf16)a.x, (__bf16)a.y, (__bf16)a.z, (__bf16)a.w};
-      *reinterpret_cast<bf4 *>(reinterpret_cast<__bf16 *>(y) + i) = v;
+    if (f.epi == EB_EPI_NONE && yt == EB_F32) {
+      *reinterpret_cast<float4 *>(reinterpret_cast<float *>(y) + i) = v;
+      return;
     }
-    return;
+    a[0] = v.x;
+    a[1] = v.y;
+    a[2] = v.z;
+    a[3] = v.w;
+  } else {
+    for (int t = 0; t < e; ++t) {
+      float v = ws[i + t];
+      for (int p = 1; p < splits; ++p) v += ws[p * ws_stride + i + t];
+      a[t] = v;
+    }
   }
-  for (int64_t j = i; j < count; ++j) {
-    float a = ws[j];
-    for (int p = 1; p < splits; ++p) a += ws[p * ws_stride + j];
-    if (yt == EB_F32)
-      reinterpret_cast<float *>(y)[j] = a;
-    else
-      reinterpret_cast<__bf16 *>(y)[j] = (__bf16)a;
+  if (f.epi == EB_EPI_GLU) {
+    for (int t = 0; t + 1 < e; t += 2) store_y(y, (i + t) / 2, silu_mul(a[t], a[t + 1]), yt);
+  } else {
+    for (int t = 0; t < e; ++t) put_y(y, i + t, a[t], yt, f);
   }
 }
 
@@ -572,39 +601,39 @@ hipError_t launch_gq(int cfg, const GOp *ops, const int2 *order, int64_t entries
 
 template <int QT, int XT>
 hipError_t launch_q(const void *wdata, int64_t n, int64_t k, const void *x, int64_t m, void *y,
-                    int32_t yt, const MfmaPlan &P, float *ws, hipStream_t s) {
+                    int32_t yt, const Fuse &f, const MfmaPlan &P, float *ws, hipStream_t s) {
   const int sp = ws ? P.splits : 1;
   const int kts = ws ? P.kts : (int)((k + kBK - 1) / kBK);
   const int64_t st = P.ws_stride;
   hipError_t e;
   switch (P.cfg) {
-    case 0: e = launch_t<QT, XT, 64, 128, 2, 2>(wdata, n, k, x, m, y, yt, sp, kts, ws, st, s); break;
-    case 1: e = launch_t<QT, XT, 128, 128, 2, 2>(wdata, n, k, x, m, y, yt, sp, kts, ws, st, s); break;
-    case 2: e = launch_t<QT, XT, 128, 256, 2, 4>(wdata, n, k, x, m, y, yt, sp, kts, ws, st, s); break;
-    case 3: e = launch_t<QT, XT, 256, 128, 4, 2>(wdata, n, k, x, m, y, yt, sp, kts, ws, st, s); break;
-    case 4: e = launch_t<QT, XT, 256, 192, 4, 2>(wdata, n, k, x, m, y, yt, sp, kts, ws, st, s); break;
-    case 5: e = launch_t<QT, XT, 256, 256, 4, 2>(wdata, n, k, x, m, y, yt, sp, kts, ws, st, s); break;
-    case 6: e = launch_t<QT, XT, 256, 256, 2, 4>(wdata, n, k, x, m, y, yt, sp, kts, ws, st, s); break;
-    default: e = launch_t<QT, XT, 256, 256, 2, 2>(wdata, n, k, x, m, y, yt, sp, kts, ws, st, s); break;
+    case 0: e = launch_t<QT, XT, 64, 128, 2, 2>(wdata, n, k, x, m, y, yt, f, sp, kts, ws, st, s); break;
+    case 1: e = launch_t<QT, XT, 128, 128, 2, 2>(wdata, n, k, x, m, y, yt, f, sp, kts, ws, st, s); break;
+    case 2: e = launch_t<QT, XT, 128, 256, 2, 4>(wdata, n, k, x, m, y, yt, f, sp, kts, ws, st, s); break;
+    case 3: e = launch_t<QT, XT, 256, 128, 4, 2>(wdata, n, k, x, m, y, yt, f, sp, kts, ws, st, s); break;
+    case 4: e = launch_t<QT, XT, 256, 192, 4, 2>(wdata, n, k, x, m, y, yt, f, sp, kts, ws, st, s); break;
+    case 5: e = launch_t<QT, XT, 256, 256, 4, 2>(wdata, n, k, x, m, y, yt, f, sp, kts, ws, st, s); break;
+    case 6: e = launch_t<QT, XT, 256, 256, 2, 4>(wdata, n, k, x, m, y, yt, f, sp, kts, ws, st, s); break;
+    default: e = launch_t<QT, XT, 256, 256, 2, 2>(wdata, n, k, x, m, y, yt, f, sp, kts, ws, st, s); break;
   }
   if (e != hipSuccess || sp == 1) return e;
   const int64_t count = m * n;
   const int64_t blocks = (count + 1023) / 1024;
-  splitk_reduce<<<(unsigned)blocks, 256, 0, s>>>(ws, sp, st, count, y, yt);
+  splitk_reduce<<<(unsigned)blocks, 256, 0, s>>>(ws, sp, st, count, y, yt, f);
   return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_mfma(int32_t type, const void *wdata, int64_t n, int64_t k, const void *x,
-                       int32_t xt, int64_t m, void *y, int32_t yt, const MfmaPlan &plan, float *ws,
-                       hipStream_t s) {
+                       int32_t xt, int64_t m, void *y, int32_t yt, const Fuse &f,
+                       const MfmaPlan &plan, float *ws, hipStream_t s) {
   if (type == EB_Q4_0) {
-    if (xt == EB_F16) return launch_q<EB_Q4_0, EB_F16>(wdata, n, k, x, m, y, yt, plan, ws, s);
-    return launch_q<EB_Q4_0, EB_BF16>(wdata, n, k, x, m, y, yt, plan, ws, s);
+    if (xt == EB_F16) return launch_q<EB_Q4_0, EB_F16>(wdata, n, k, x, m, y, yt, f, plan, ws, s);
+    return launch_q<EB_Q4_0, EB_BF16>(wdata, n, k, x, m, y, yt, f, plan, ws, s);
   }
-  if (xt == EB_F16) return launch_q<EB_Q8_0, EB_F16>(wdata, n, k, x, m, y, yt, plan, ws, s);
-  return launch_q<EB_Q8_0, EB_BF16>(wdata, n, k, x, m, y, yt, plan, ws, s);
+  if (xt == EB_F16) return launch_q<EB_Q8_0, EB_F16>(wdata, n, k, x, m, y, yt, f, plan, ws, s);
+  return launch_q<EB_Q8_0, EB_BF16>(wdata, n, k, x, m, y, yt, f, plan, ws, s);
 }
 
 hipError_t launch_mfma_grouped(int32_t type, int32_t xt, int cfg, const GOp *ops, const int2 *order,

@@ -7,6 +7,7 @@
 #include <hip/hip_runtime.h>
 
 #include "eb_internal.h"
+#include "epilogue.h"
 #include "mfma_common.h"
 #include "mm_common.h"
 
@@ -225,13 +226,23 @@ __global__ void __launch_bounds__(WAVES * 64)
 
   // lane (l, reg r) of sub-tile (i, j) holds y[m0 + 32 i + l % 32][n0 + 64 wave +
   // 32 j + 8 (r / 4) + 4 (l / 32) + r % 4]; see mm_ldsw_kernel for the bounds.
+  //
+  // Fused steps: the residual of EB_EPI_ADD is read with the same packed
+  // accesses as the stores; with EB_EPI_GLU the four columns of a packed
+  // store are two gate/up pairs, giving two adjacent outputs, so the packed
+  // path still issues NST stores per tile.  YT only fixes the output size:
+  // 16-bit outputs are bf16 or fp16 by the op's type.
   auto epilogue = [&](const MMPos &c) __attribute__((always_inline)) -> bool {
     int64_t m0, n0;
     int rm, rn;
     mm_tile<BM, BN>(ops, c, m0, n0, rm, rn);
     const MMOp &o = ops[c.op];
     const uint32_t n = (uint32_t)o.n;
-    const auto yr = ursrc(o.y, (uint32_t)o.m * n * YSZ);
+    const int yt = o.yt;
+    const bool glu = o.f.epi == EB_EPI_GLU, add = o.f.epi == EB_EPI_ADD;
+    const uint32_t nout = glu ? n / 2 : n;
+    const auto yr = ursrc(o.y, (uint32_t)o.m * nout * YSZ);
+    const auto rr = ursrc(add ? o.f.r : o.y, (uint32_t)o.m * n * YSZ);
     const bool packed = (n & 3) == 0;
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
@@ -241,34 +252,76 @@ __global__ void __launch_bounds__(WAVES * 64)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           const int cl = wave * 32 * FN + j * 32 + 8 * q + 4 * (int)wh;
-          const uint32_t base = (row * n + (uint32_t)n0 + cl) * YSZ;
           float v[4];
 #pragma unroll
           for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * q + e];  // copy first: see mfma_multi_kernel
+          if (glu) {
+            const float g0 = silu_mul(v[0], v[1]), g1 = silu_mul(v[2], v[3]);
+            const uint32_t gb = (row * nout + ((uint32_t)n0 + cl) / 2) * YSZ;
+            if (packed) {
+              const uint32_t off = cl < rn ? gb : 0x80000000u;
+              if constexpr (YT == EB_F32) {
+                u32x2_t w;
+                w[0] = __builtin_bit_cast(uint32_t, g0);
+                w[1] = __builtin_bit_cast(uint32_t, g1);
+                __builtin_amdgcn_raw_buffer_store_b64(w, yr, (int)off, 0, 0);
+              } else {
+                const uint32_t w = (uint32_t)to_y16(g0, yt) | ((uint32_t)to_y16(g1, yt) << 16);
+                __builtin_amdgcn_raw_buffer_store_b32(w, yr, (int)off, 0, 0);
+              }
+            } else {
+#pragma unroll
+              for (int e = 0; e < 2; ++e) {
+                const uint32_t off = cl + 2 * e < rn ? gb + e * YSZ : 0x80000000u;
+                const float g = e ? g1 : g0;
+                if constexpr (YT == EB_F32)
+                  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, g), yr, (int)off, 0, 0);
+                else
+                  __builtin_amdgcn_raw_buffer_store_b16(to_y16(g, yt), yr, (int)off, 0, 0);
+              }
+            }
+            continue;
+          }
+          const uint32_t base = (row * n + (uint32_t)n0 + cl) * YSZ;
           if (packed) {
             const uint32_t off = cl < rn ? base : 0x80000000u;
             if constexpr (YT == EB_F32) {
+              if (add) {
+                const u32x4_t r = __builtin_amdgcn_raw_buffer_load_b128(rr, (int)off, 0, 0);
+                // convert element values: this compiler turns __builtin_bit_cast of a
+                // vector element into element 0 of the vector (one dword loaded)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) v[e] += __uint_as_float((uint32_t)r[e]);
+              }
               u32x4_t w;
 #pragma unroll
               for (int e = 0; e < 4; ++e) w[e] = __builtin_bit_cast(uint32_t, v[e]);
               __builtin_amdgcn_raw_buffer_store_b128(w, yr, (int)off, 0, 0);
             } else {
+              if (add) {
+                const u32x2_t r = __builtin_amdgcn_raw_buffer_load_b64(rr, (int)off, 0, 0);
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                  v[e] += from_y16((uint16_t)(r[e >> 1] >> (16 * (e & 1))), yt);
+              }
               u32x2_t w;
 #pragma unroll
               for (int e = 0; e < 2; ++e)
-                w[e] = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)v[2 * e]) |
-                       ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)v[2 * e + 1]) << 16);
+                w[e] = (uint32_t)to_y16(v[2 * e], yt) | ((uint32_t)to_y16(v[2 * e + 1], yt) << 16);
               __builtin_amdgcn_raw_buffer_store_b64(w, yr, (int)off, 0, 0);
             }
           } else {
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
               const uint32_t off = cl + e < rn ? base + e * YSZ : 0x80000000u;
-              if constexpr (YT == EB_F32)
+              if constexpr (YT == EB_F32) {
+                if (add)
+                  v[e] += __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rr, (int)off, 0, 0));
                 __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v[e]), yr, (int)off, 0, 0);
-              else
-                __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(uint16_t, (__bf16)v[e]), yr,
-                                                      (int)off, 0, 0);
+              } else {
+                if (add) v[e] += from_y16(__builtin_amdgcn_raw_buffer_load_b16(rr, (int)off, 0, 0), yt);
+                __builtin_amdgcn_raw_buffer_store_b16(to_y16(v[e], yt), yr, (int)off, 0, 0);
+              }
             }
           }
         }
@@ -441,6 +494,7 @@ __global__ void __launch_bounds__(WAVES * 64)
 #endif  // __HIP_DEVICE_COMPILE__
 }
 
+// YT = EB_F32 for fp32 outputs, EB_BF16 for either 16-bit output type.
 template <int QT, int XT, int WAVES>
 hipError_t lds2_y(int32_t yt, const MMOp *ops, int nops, const int64_t *wg, int groups, hipStream_t s) {
   if (yt == EB_F32)

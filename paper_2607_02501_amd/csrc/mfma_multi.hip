@@ -13,6 +13,7 @@
 #include <vector>
 
 #include "eb_internal.h"
+#include "epilogue.h"
 #include "mfma_common.h"
 #include "mm_common.h"
 
@@ -191,29 +192,48 @@ __global__ void __launch_bounds__(256)
   };
   zero_acc();
 
+  // Fused steps: EB_EPI_ADD reads the residual at the store's offset; with
+  // EB_EPI_GLU the gate/up columns 2c, 2c + 1 sit in lanes l, l ^ 1 and the
+  // even lane stores silu(gate) * up into column c of n / 2.  YT only fixes
+  // the output size (16-bit outputs are bf16 or fp16 by the op's type).
   auto epilogue = [&](const MMPos &c) __attribute__((always_inline)) {
     int64_t m0, n0;
     int rm, rn;
     mm_tile<BM, BN>(ops, c, m0, n0, rm, rn);
     const MMOp &o = ops[c.op];
     const uint32_t n = (uint32_t)o.n;
-    const auto yr = ursrc(o.y, (uint32_t)o.m * n * YSZ);
+    const int yt = o.yt;
+    const bool glu = o.f.epi == EB_EPI_GLU, add = o.f.epi == EB_EPI_ADD;
+    const uint32_t nout = glu ? n / 2 : n;
+    const auto yr = ursrc(o.y, (uint32_t)o.m * nout * YSZ);
+    const auto rr = ursrc(add ? o.f.r : o.y, (uint32_t)o.m * n * YSZ);
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
       const int cl = wave * 32 * FN + j * 32 + (lane & 31);
 #pragma unroll
       for (int i = 0; i < FM; ++i) {
         const uint32_t row0 = (uint32_t)m0 + i * 32 + 4 * (lane >> 5);
-        const uint32_t base = cl < rn ? (row0 * n + (uint32_t)n0 + cl) * YSZ : 0x80000000u;
+        const uint32_t col = glu ? ((uint32_t)n0 + cl) / 2 : (uint32_t)n0 + cl;
+        const bool keep = cl < rn && (!glu || (cl & 1) == 0);
+        const uint32_t base = keep ? (row0 * nout + col) * YSZ : 0x80000000u;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const uint32_t off = base + (uint32_t)(8 * (r >> 2) + (r & 3)) * n * YSZ;
-          const float v = acc[i][j][r];  // copy first: see mfma_multi_kernel
+          const uint32_t off = base + (uint32_t)(8 * (r >> 2) + (r & 3)) * nout * YSZ;
+          float v = acc[i][j][r];  // copy first: see mfma_multi_kernel
+          if (glu) {
+            const float u = __builtin_bit_cast(
+                float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, true));
+            v = silu_mul(v, u);
+          } else if (add) {
+            if constexpr (YT == EB_F32)
+              v += __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rr, (int)off, 0, 0));
+            else
+              v += from_y16(__builtin_amdgcn_raw_buffer_load_b16(rr, (int)off, 0, 0), yt);
+          }
           if constexpr (YT == EB_F32)
             __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), yr, (int)off, 0, 0);
           else
-            __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(uint16_t, (__bf16)v), yr,
-                                                  (int)off, 0, 0);
+            __builtin_amdgcn_raw_buffer_store_b16(to_y16(v, yt), yr, (int)off, 0, 0);
         }
       }
     }

@@ -31,10 +31,17 @@ EB_BF16 = 2
 EB_PATH_AUTO = 0
 EB_PATH_GEMV = 1
 EB_PATH_MFMA = 2
+EB_PRO_NONE = 0
+EB_PRO_RMSNORM = 1
+EB_EPI_NONE = 0
+EB_EPI_ADD = 1
+EB_EPI_GLU = 2
 
 QTYPES = {"q8_0": EB_Q8_0, "q4_0": EB_Q4_0}
 DTYPES = {torch.float32: EB_F32, torch.float16: EB_F16, torch.bfloat16: EB_BF16}
 PATHS = {"auto": EB_PATH_AUTO, "gemv": EB_PATH_GEMV, "mfma": EB_PATH_MFMA}
+PROLOGUES = {None: EB_PRO_NONE, "none": EB_PRO_NONE, "rmsnorm": EB_PRO_RMSNORM}
+EPILOGUES = {None: EB_EPI_NONE, "none": EB_EPI_NONE, "add": EB_EPI_ADD, "glu": EB_EPI_GLU}
 
 
 class eb_qweights(ctypes.Structure):
@@ -50,7 +57,10 @@ class eb_layout(ctypes.Structure):
 
 class eb_qlinear_op(ctypes.Structure):
     _fields_ = [("w", eb_qweights), ("x", ctypes.c_void_p), ("y", ctypes.c_void_p),
-                ("m", ctypes.c_int64), ("x_type", ctypes.c_int32), ("y_type", ctypes.c_int32)]
+                ("m", ctypes.c_int64), ("x_type", ctypes.c_int32), ("y_type", ctypes.c_int32),
+                ("prologue", ctypes.c_int32), ("epilogue", ctypes.c_int32),
+                ("norm_weight", ctypes.c_void_p), ("residual", ctypes.c_void_p),
+                ("norm_eps", ctypes.c_float), ("reserved", ctypes.c_int32)]
 
 
 if not os.path.exists(LIB_PATH):
@@ -79,6 +89,8 @@ lib.eb_qlinear.restype = _i32
 lib.eb_qlinear.argtypes = [ctypes.POINTER(eb_qweights), _vp, _i32, _i64, _vp, _i32, _vp]
 lib.eb_qlinear_ex.restype = _i32
 lib.eb_qlinear_ex.argtypes = [ctypes.POINTER(eb_qweights), _vp, _i32, _i64, _vp, _i32, _i32, _vp]
+lib.eb_qlinear_fused.restype = _i32
+lib.eb_qlinear_fused.argtypes = [ctypes.POINTER(eb_qlinear_op), _i32, _vp]
 lib.eb_qlinear_auto_path.restype = _i32
 lib.eb_qlinear_auto_path.argtypes = [_i32, _i32, _i64, _i64, _i64]
 lib.eb_qlinear_stack.restype = _i32
@@ -201,14 +213,45 @@ def auto_path(qtype: str, x_dtype, m: int, n: int, k: int) -> str:
     return {EB_PATH_GEMV: "gemv", EB_PATH_MFMA: "mfma"}.get(p, "invalid")
 
 
+def make_op(qw: QWeights, x: torch.Tensor, y: torch.Tensor, x_dtype=None, prologue=None,
+            norm_weight: torch.Tensor | None = None, eps: float = 0.0, epilogue=None,
+            residual: torch.Tensor | None = None) -> eb_qlinear_op:
+    """One eb_qlinear_op.  With prologue="rmsnorm", x is the fp32 residual
+    stream and x_dtype the 16-bit type the product consumes (default bf16)."""
+    if x_dtype is None:
+        x_dtype = torch.bfloat16 if x.dtype == torch.float32 else x.dtype
+    return eb_qlinear_op(qw.c, x.data_ptr(), y.data_ptr(), x.shape[0], DTYPES[x_dtype],
+                         DTYPES[y.dtype], PROLOGUES[prologue], EPILOGUES[epilogue],
+                         norm_weight.data_ptr() if norm_weight is not None else None,
+                         residual.data_ptr() if residual is not None else None, float(eps), 0)
+
+
 def make_ops(entries) -> ctypes.Array:
-    """entries: iterable of (QWeights, x, y).  Returns a ctypes eb_qlinear_op array."""
+    """entries: iterable of (QWeights, x, y) or (QWeights, x, y, {make_op keywords}).
+    Returns a ctypes eb_qlinear_op array."""
     entries = list(entries)
     arr = (eb_qlinear_op * len(entries))()
-    for i, (qw, x, y) in enumerate(entries):
-        arr[i] = eb_qlinear_op(qw.c, x.data_ptr(), y.data_ptr(), x.shape[0], DTYPES[x.dtype],
-                               DTYPES[y.dtype])
+    for i, e in enumerate(entries):
+        arr[i] = make_op(*e[:3], **(e[3] if len(e) > 3 else {}))
     return arr
+
+
+def qlinear_fused(qw: QWeights, x: torch.Tensor, out_dtype=torch.float32, x_dtype=None,
+                  prologue=None, norm_weight=None, eps: float = 0.0, epilogue=None,
+                  residual=None, path: str = "auto", out: torch.Tensor | None = None) -> torch.Tensor:
+    """One projection with fused steps (eb_qlinear_fused): optional RMS
+    normalisation of x before the product, residual addition ("add") or the
+    SiLU-gated product of interleaved gate/up rows ("glu", output n / 2)."""
+    assert x.is_cuda and x.dim() == 2 and x.shape[1] == qw.k
+    x = x.contiguous()
+    m = x.shape[0]
+    if out is None:
+        n_out = qw.n // 2 if epilogue == "glu" else qw.n
+        out = torch.empty((m, n_out), dtype=out_dtype, device=x.device)
+    op = make_op(qw, x, out, x_dtype, prologue, norm_weight, eps, epilogue, residual)
+    _check(lib.eb_qlinear_fused(ctypes.byref(op), PATHS[path], _stream(x.device)),
+           "eb_qlinear_fused")
+    return out
 
 
 def qlinear_stack(ops: ctypes.Array, device=None) -> None:

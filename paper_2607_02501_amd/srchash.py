@@ -5,8 +5,9 @@ import os
 
 _CSRC = os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc")
 _FILES = {
-    "gemv": ("gemv.hip", "eb_internal.h", "eb_api.cpp"),
-    "mfma": ("mfma.hip", "mfma_multi.hip", "mfma_lds2.hip", "mfma_common.h", "mm_common.h",
+    "gemv": ("gemv.hip", "epilogue.h", "eb_internal.h", "eb_api.cpp"),
+    "mfma": ("mfma.hip", "mfma_multi.hip", "mfma_lds2.hip", "mfma_common.h", "mm_common.h", "norm.hip",
+             "epilogue.h",
              "eb_internal.h", "eb_api.cpp"),
 }
 

@@ -84,7 +84,7 @@ X, Y = 0x200000, 0x400000
     ("null_w", -1), ("null_data", -1), ("bad_type", -1), ("reserved", -1), ("k33", -1),
     ("k0", -1), ("n0", -1), ("m_neg", -1), ("bad_xt", -1), ("bad_path", -1), ("x_null", -1),
     ("w_misaligned", -2), ("x_misaligned", -2), ("y_misaligned", -2), ("x_f32", -3),
-    ("y_f16", -3), ("gemv_m9", -3), ("gemv_big_k", -3), ("overlap", -1),
+    ("bad_yt", -1), ("gemv_m9", -3), ("gemv_big_k", -3), ("overlap", -1),
 ])
 def test_qlinear_validation(eb, case, expect):
     w = _w(eb)
@@ -120,8 +120,8 @@ def test_qlinear_validation(eb, case, expect):
         y = Y + 4
     elif case == "x_f32":
         xt = eb.EB_F32
-    elif case == "y_f16":
-        yt = eb.EB_F16
+    elif case == "bad_yt":
+        yt = 7
     elif case == "gemv_m9":
         m, path = 9, eb.EB_PATH_GEMV
     elif case == "gemv_big_k":
@@ -130,6 +130,90 @@ def test_qlinear_validation(eb, case, expect):
     elif case == "overlap":
         y = X + 64
     assert eb.lib.eb_qlinear_ex(wp, x, xt, m, y, yt, path, None) == expect
+
+
+G, R = 0x600000, 0x800000  # fake norm-weight and residual addresses
+
+
+@pytest.mark.parametrize("case,expect", [
+    ("bad_prologue", -1), ("bad_epilogue", -1), ("reserved", -1), ("no_gamma", -1),
+    ("neg_eps", -1), ("nan_eps", -1), ("inf_eps", -1), ("no_residual", -1), ("glu_odd_n", -1),
+    ("gamma_misaligned", -2), ("residual_misaligned", -2), ("residual_overlaps_y", -1),
+    ("y_overlaps_gamma", -1), ("y_overlaps_h", -1), ("x_f32", -3), ("gemv_m9", -3),
+])
+def test_fused_validation(eb, case, expect):
+    """eb_qlinear_fused rejects bad fused-step fields on the host (nothing launches)."""
+    w = _w(eb)
+    op = eb.eb_qlinear_op(w, X, Y, 4, eb.EB_BF16, eb.EB_F32, eb.EB_PRO_RMSNORM, eb.EB_EPI_ADD,
+                          G, R, 1e-5, 0)
+    path = eb.EB_PATH_AUTO
+    if case == "bad_prologue":
+        op.prologue = 2
+    elif case == "bad_epilogue":
+        op.epilogue = 3
+    elif case == "reserved":
+        op.reserved = 1
+    elif case == "no_gamma":
+        op.norm_weight = None
+    elif case == "neg_eps":
+        op.norm_eps = -1e-6
+    elif case == "nan_eps":
+        op.norm_eps = float("nan")
+    elif case == "inf_eps":
+        op.norm_eps = float("inf")
+    elif case == "no_residual":
+        op.residual = None
+    elif case == "glu_odd_n":
+        op.w.n, op.epilogue = 63, eb.EB_EPI_GLU
+    elif case == "gamma_misaligned":
+        op.norm_weight = G + 4
+    elif case == "residual_misaligned":
+        op.residual = R + 8
+    elif case == "residual_overlaps_y":
+        op.residual = Y + 16  # not y itself, but inside y's 4 x 64 fp32 outputs
+    elif case == "y_overlaps_gamma":
+        op.norm_weight = Y + 32
+    elif case == "y_overlaps_h":
+        op.y = X + 4 * 64 * 3  # h is fp32 under the prologue: 4 rows x 64 x 4 bytes
+    elif case == "x_f32":
+        op.x_type = eb.EB_F32
+    elif case == "gemv_m9":
+        op.m, path = 9, eb.EB_PATH_GEMV
+    assert eb.lib.eb_qlinear_fused(ctypes.byref(op), path, None) == expect
+    assert eb.lib.eb_qlinear_fused(None, path, None) == eb.EB_ERR_INVALID
+
+
+def test_fused_stack_counts_prologue_launches(eb):
+    """A normalisation prologue costs a row-kernel launch on the MFMA path and
+    nothing on the GEMV path; dependencies through the residual stream split runs."""
+    k, n = 256, 512
+    WB = eb.lib.eb_qweights_bytes(eb.EB_Q8_0, n, k)
+    ws = [0x10000000 + i * ((WB + 4095) // 4096 * 4096) for i in range(4)]
+    H, A, Q, GU, ACT = 0x20000000, 0x21000000, 0x22000000, 0x23000000, 0x24000000
+
+    def op(i, x, y, m, pro=0, epi=0, res=None, nn=n, kk=k, yt=None):
+        w = eb.eb_qweights(eb.EB_Q8_0, 0, nn, kk, ws[i])
+        return eb.eb_qlinear_op(w, x, y, m, eb.EB_BF16, eb.EB_F32 if yt is None else yt, pro, epi,
+                                G if pro else None, res, 1e-5, 0)
+
+    def launches(lst):
+        arr = (eb.eb_qlinear_op * len(lst))(*lst)
+        return eb.lib.eb_qlinear_stack_launches(arr, len(lst))
+
+    # one decoder layer at m = 1: normalised QKV, O adding into h, normalised
+    # gate/up with the gated product, down adding into h
+    for m, pro_cost in ((1, 0), (50, 1)):
+        layer = [op(0, H, Q, m, pro=1),
+                 op(1, A, H, m, epi=1, res=H),
+                 op(2, H, GU, m, pro=1, epi=2, yt=eb.EB_BF16),
+                 op(3, GU, H, m, epi=1, res=H, kk=n // 2)]
+        # every op depends on the one before (h, then the gate/up output), so
+        # nothing fuses: 4 launches plus the prologue row kernels
+        assert launches(layer) == 4 + 2 * pro_cost, m
+    # two independent normalised projections of one h fuse into one launch
+    for m, expect in ((1, 1), (50, 3)):
+        two = [op(0, H, Q, m, pro=1), op(2, H, GU, m, pro=1)]
+        assert launches(two) == expect, m
 
 
 def test_qlinear_m0_is_noop(eb):
