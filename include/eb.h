@@ -116,8 +116,8 @@ typedef struct {
  *   (1/k) sum_j h[i][j]^2), rounded to nearest even in x_type, g = norm_weight.
  *   On the GEMV path every workgroup normalises while it stages x (no extra
  *   launch); on the MFMA path a row kernel writes x_hat first (one more launch)
- *   into library-owned memory: the stream's workspace for direct calls
- *   (m * k * 2 bytes besides any split-K partial sums; during a capture the
+ *   into library-owned memory: the stream's workspace for direct calls (at
+ *   most 64 MiB together with split-K partial sums; during a capture the
  *   workspace is not grown and a call needing more returns
  *   EB_ERR_UNSUPPORTED), or the stack plan's own buffer.
  * Epilogue EB_EPI_ADD: y = x_hat . w_hat^T + r, r = residual[m][n] of y_type;
@@ -191,13 +191,9 @@ eb_status eb_qweights_from_canonical(int32_t type, const void *src, int64_t n, i
  * automatically.
  * On the MFMA path, a problem with too few output tiles to fill the GPU (few
  * rows and columns, long k) may be split along k: each split writes fp32
- * partial sums to a workspace and the last split of each output tile to
- * finish (counted with a per-tile atomic counter that it resets) adds them in
- * split order, so results stay deterministic and the call is one launch
- * (EB_SPLITK_TWO_PASS=1 adds them in a second kernel instead, in the same
- * order).  Direct calls use a workspace owned by the library per (device,
- * stream): 64 KiB of tile counters and at most 64 MiB of partial sums per
- * call, grown on demand and
+ * partial sums to a workspace and a second kernel adds them in a fixed order,
+ * so results stay deterministic.  Direct calls use a workspace owned by the
+ * library per (device, stream), at most 64 MiB per call, grown on demand and
  * never freed before process exit (a graph captured from the stream may refer
  * to it).  While the stream is being captured nothing is allocated: if the
  * stream's workspace is too small the call runs unsplit.  A graph captured

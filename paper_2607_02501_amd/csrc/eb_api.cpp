@@ -181,12 +181,6 @@ uint8_t *stream_workspace(hipStream_t s, size_t bytes) {
     (void)hipGetLastError();
     return nullptr;
   }
-  // the split-K tile counters at its start must begin at zero
-  if (hipMemset(p, 0, kSplitCounterBytes) != hipSuccess) {
-    (void)hipGetLastError();
-    (void)hipFree(p);
-    return nullptr;
-  }
   if (slot.first) C.retired.push_back(slot.first);
   slot = {p, want};
   return static_cast<uint8_t *>(p);
@@ -198,10 +192,9 @@ size_t xhat_bytes(const eb_qlinear_op &o) {
 }
 
 // One op on the MFMA path with a fixed plan: the prologue's row kernel writes
-// the normalised activations to xbuf, then the product reads them.  ws / ctr:
-// split-K partial sums and tile counters (nullptr: unsplit).
+// the normalised activations to xbuf, then the product reads them.
 hipError_t launch_mfma_op(const eb_qlinear_op &o, const MfmaPlan &P, void *xbuf, float *ws,
-                          unsigned *ctr, hipStream_t s) {
+                          hipStream_t s) {
   const void *x = o.x;
   Fuse f = fuse_of(o);
   if (o.prologue == EB_PRO_RMSNORM) {
@@ -212,8 +205,7 @@ hipError_t launch_mfma_op(const eb_qlinear_op &o, const MfmaPlan &P, void *xbuf,
     f.pro = EB_PRO_NONE;
     f.gamma = nullptr;
   }
-  return launch_mfma(o.w.type, o.w.data, o.w.n, o.w.k, x, o.x_type, o.m, o.y, o.y_type, f, P, ws,
-                     ctr, s);
+  return launch_mfma(o.w.type, o.w.data, o.w.n, o.w.k, x, o.x_type, o.m, o.y, o.y_type, f, P, ws, s);
 }
 
 eb_status launch_op(const eb_qlinear_op &o, int32_t path, hipStream_t s) {
@@ -223,18 +215,16 @@ eb_status launch_op(const eb_qlinear_op &o, int32_t path, hipStream_t s) {
   if (path == EB_PATH_GEMV) {
     e = launch_gemv(o.w.type, o.w.data, o.w.n, o.w.k, o.x, o.x_type, o.m, o.y, o.y_type, fuse_of(o), s);
   } else {
-    // the stream's workspace holds the split-K tile counters, the
-    // normalised activations, then any split-K partial sums
-    const size_t cb = kSplitCounterBytes, xb = xhat_bytes(o);
+    // the stream's workspace holds the normalised activations, then any
+    // split-K partial sums
+    const size_t xb = xhat_bytes(o);
     MfmaPlan P = plan_mfma(o.w.type, o.m, o.w.n, o.w.k, true);
     uint8_t *ws = nullptr;
-    if (P.splits > 1) ws = stream_workspace(s, cb + xb + P.ws_bytes);
+    if (P.splits > 1) ws = stream_workspace(s, xb + P.ws_bytes);
     if (P.splits > 1 && !ws) P = plan_mfma(o.w.type, o.m, o.w.n, o.w.k, false);
-    if (!ws && xb) ws = stream_workspace(s, cb + xb);
+    if (!ws && xb) ws = stream_workspace(s, xb);
     if (xb && !ws) return EB_ERR_UNSUPPORTED;
-    e = launch_mfma_op(o, P, ws ? ws + cb : nullptr,
-                       P.splits > 1 ? reinterpret_cast<float *>(ws + cb + xb) : nullptr,
-                       reinterpret_cast<unsigned *>(ws), s);
+    e = launch_mfma_op(o, P, ws, P.splits > 1 ? reinterpret_cast<float *>(ws + xb) : nullptr, s);
   }
   return e == hipSuccess ? EB_OK : EB_ERR_HIP;
 }
@@ -334,8 +324,8 @@ struct Plan {
   int64_t *mmwg = nullptr;  // their workgroup unit ranges
   GOp *gmtable = nullptr;   // grouped MFMA launches: op table
   int2 *gmorder = nullptr;  // and workgroup (op, tile) entries
-  uint8_t *ws = nullptr;  // split-K tile counters + partial sums, shared by the plan's
-  size_t ws_bytes = 0;    // MFMA steps (run in order); ws_bytes: the partial sums
+  float *ws = nullptr;    // split-K workspace shared by the plan's MFMA steps (run in order)
+  size_t ws_bytes = 0;
   uint8_t *xbuf = nullptr;  // normalised activations of prologue ops on the MFMA path
   size_t xbuf_bytes = 0;
   hipGraph_t graph = nullptr;
@@ -678,14 +668,9 @@ eb_status build_plan(const eb_qlinear_op *ops, int32_t n_ops, bool alloc, Plan &
                   hipMemcpyHostToDevice) != hipSuccess)
       return EB_ERR_HIP;
   }
-  if (P.ws_bytes > 0) {
-    // split-K tile counters (zeroed once; every launch leaves them at zero),
-    // then the partial sums
-    if (hipMalloc((void **)&P.ws, kSplitCounterBytes + P.ws_bytes) != hipSuccess) {
-      P.ws = nullptr;
-      return EB_ERR_HIP;
-    }
-    if (hipMemset(P.ws, 0, kSplitCounterBytes) != hipSuccess) return EB_ERR_HIP;
+  if (P.ws_bytes > 0 && hipMalloc((void **)&P.ws, P.ws_bytes) != hipSuccess) {
+    P.ws = nullptr;
+    return EB_ERR_HIP;
   }
   if (!host.empty()) {
     if (hipMalloc((void **)&P.table, host.size() * sizeof(M1Op)) != hipSuccess) {
@@ -732,8 +717,7 @@ eb_status run_plan(const eb_qlinear_op *ops, const Plan &P, hipStream_t s) {
         return EB_ERR_HIP;
     } else if (st.mfma) {
       const eb_qlinear_op &o = ops[st.op];
-      float *part = st.mp.splits > 1 ? reinterpret_cast<float *>(P.ws + kSplitCounterBytes) : nullptr;
-      if (launch_mfma_op(o, st.mp, P.xbuf, part, reinterpret_cast<unsigned *>(P.ws), s) != hipSuccess)
+      if (launch_mfma_op(o, st.mp, P.xbuf, st.mp.splits > 1 ? P.ws : nullptr, s) != hipSuccess)
         return EB_ERR_HIP;
     } else if (st.op >= 0) {
       eb_status r = launch_op(ops[st.op], EB_PATH_AUTO, s);
@@ -899,8 +883,6 @@ eb_status eb_qlinear_stack(const eb_qlinear_op *ops, int32_t n_ops, hipStream_t 
   key.push_back(env_off("EB_STACK_FUSE") ? 'u' : 'f');
   key.push_back(env_off("EB_STACK_GROUP") ? 'n' : 'g');
   key.push_back(env_off("EB_STACK_SPLIT_TAIL") ? 'w' : 's');
-  const char *two = std::getenv("EB_SPLITK_TWO_PASS");
-  key.push_back(two && two[0] == '1' ? 'r' : 'k');
   const int fk = mfma_force_key();
   key.append(reinterpret_cast<const char *>(&fk), sizeof(fk));
   key.append(reinterpret_cast<const char *>(ops), sizeof(eb_qlinear_op) * (size_t)n_ops);
@@ -957,8 +939,7 @@ int32_t eb_qlinear_stack_launches(const eb_qlinear_op *ops, int32_t n_ops) {
   for (const Step &st : P.steps) {
     launches += (int32_t)st.norms.size();
     if (st.op >= 0 && ops[st.op].m == 0) continue;
-    const eb_qlinear_op *o = st.op >= 0 ? &ops[st.op] : nullptr;
-    launches += st.mfma ? mfma_launches(o->w.type, o->m, o->w.n, st.mp) : 1;
+    launches += (st.mfma && st.mp.splits > 1) ? 2 : 1;
     if (st.mfma && ops[st.op].prologue == EB_PRO_RMSNORM) ++launches;
   }
   return launches;

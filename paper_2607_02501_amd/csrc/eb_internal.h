@@ -106,15 +106,10 @@ struct MfmaPlan {
   size_t ws_bytes = 0;
 };
 MfmaPlan plan_mfma(int32_t type, int64_t m, int64_t n, int64_t k, bool allow_split);
-// ws == nullptr runs the plan's configuration unsplit.  ctr: kSplitCounters
-// per-tile counters, zero before the call and left at zero by it (nullptr:
-// the partials are summed by a second kernel).
-constexpr int64_t kSplitCounters = 16384;
-constexpr size_t kSplitCounterBytes = kSplitCounters * 4;
+// ws == nullptr runs the plan's configuration unsplit.
 hipError_t launch_mfma(int32_t type, const void *wdata, int64_t n, int64_t k, const void *x,
                        int32_t xt, int64_t m, void *y, int32_t yt, const Fuse &f,
-                       const MfmaPlan &plan, float *ws, unsigned *ctr, hipStream_t s);
-int mfma_launches(int32_t type, int64_t m, int64_t n, const MfmaPlan &plan);  // 1 or 2
+                       const MfmaPlan &plan, float *ws, hipStream_t s);
 int mfma_tile_count();
 int mfma_cfg_bm(int cfg);        // rows of a tile configuration
 double mfma_cfg_rate(int cfg);   // its measured full-chip rate, TFLOP/s

@@ -22,11 +22,7 @@
 // has about two steps of MFMA work to land.
 //
 // Problems with too few tiles to fill the GPU split k over workgroups; each
-// split writes an fp32 partial tile, and the last split of a tile to finish
-// (an atomic counter per tile) sums all of them in split order and writes the
-// output, so the result does not depend on which split finishes last.  (With
-// more tiles than counters, or EB_SPLITK_TWO_PASS=1, a second kernel sums
-// them in the same order.)
+// split writes an fp32 partial tile and a second kernel sums them in order.
 //
 // Tiles are ordered for the 8 XCDs of MI355X (workgroups are dispatched to
 // XCDs round-robin, each XCD has its own L2): each XCD gets a contiguous range
@@ -57,8 +53,7 @@ __global__ void __launch_bounds__(WM *WN * 64)
     mfma_kernel(const uint8_t *__restrict__ wdata_, int64_t n_, int64_t k_, int64_t d_off_,
                 int64_t ds_, const uint16_t *__restrict__ x_, int64_t m_, void *__restrict__ y_,
                 int yt_, Fuse f_, int kts_, float *__restrict__ ws, int64_t ws_stride,
-                unsigned *__restrict__ counters, const GOp *__restrict__ gops,
-                const int2 *__restrict__ gorder) {
+                const GOp *__restrict__ gops, const int2 *__restrict__ gorder) {
   const uint8_t *wdata = wdata_;
   const uint16_t *x = x_;
   void *y = y_;
@@ -349,48 +344,6 @@ __global__ void __launch_bounds__(WM *WN * 64)
           put_y(y, o, acc[i][j][r], yt, f);
       }
     }
-  if (!ws || !counters) return;
-
-  // The last split of this tile to arrive sums the partials of every split
-  // in split order (the order of the two-kernel reduction) and applies the
-  // epilogue.  Release: this split's partials are visible before its count.
-  // (the flag reuses the first word of an x buffer: every wave is past its
-  // last LDS read at the barrier below)
-  int &s_last = *reinterpret_cast<int *>(sA0);
-  __threadfence();
-  __syncthreads();
-  const int splits = (int)(gridDim.x / tiles);
-  if (tid == 0) {
-    const unsigned prev =
-        __hip_atomic_fetch_add(counters + t, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-    s_last = prev == (unsigned)(splits - 1);
-    // the counter is left at zero for the next launch
-    if (s_last) __hip_atomic_store(counters + t, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
-  __syncthreads();
-  if (!s_last) return;
-  __threadfence();  // acquire: the other splits' partials
-  if (f.epi == EB_EPI_GLU) {
-    const int pairs = rows_n / 2;  // n even: whole pairs in every tile
-    for (int e = tid; e < rows_m * pairs; e += T) {
-      const int rl = e / pairs, cl = 2 * (e - rl * pairs);
-      const int64_t o = (m0 + rl) * n + n0 + cl;
-      float g = ws[o], u = ws[o + 1];
-      for (int p = 1; p < splits; ++p) {
-        g += ws[p * ws_stride + o];
-        u += ws[p * ws_stride + o + 1];
-      }
-      store_y(y, (m0 + rl) * (n / 2) + (n0 + cl) / 2, silu_mul(g, u), yt);
-    }
-  } else {
-    for (int e = tid; e < rows_m * rows_n; e += T) {
-      const int rl = e / rows_n, cl = e - rl * rows_n;
-      const int64_t o = (m0 + rl) * n + n0 + cl;
-      float a = ws[o];
-      for (int p = 1; p < splits; ++p) a += ws[p * ws_stride + o];
-      put_y(y, o, a, yt, f);
-    }
-  }
 }
 
 // Whether every byte span one workgroup addresses through a 32-bit buffer
@@ -408,14 +361,14 @@ bool fits_offsets(int64_t n, int64_t k, int bm = BM, int bn = BN) {
 template <int QT, int XT, int BM, int BN, int WM, int WN>
 hipError_t launch_t(const void *wdata, int64_t n, int64_t k, const void *x, int64_t m, void *y,
                     int32_t yt, const Fuse &f, int splits, int kts, float *ws, int64_t ws_stride,
-                    unsigned *counters, hipStream_t s) {
+                    hipStream_t s) {
   const Layout L = layout_of(QT, n, k);
   const int64_t tiles = ((m + BM - 1) / BM) * ((n + BN - 1) / BN);
   if (tiles * splits > 0x7fffffff) return hipErrorInvalidValue;
   if (!fits_offsets<QT, BM, BN>(n, k)) return hipErrorInvalidValue;
   mfma_kernel<QT, XT, BM, BN, WM, WN><<<(unsigned)(tiles * splits), WM * WN * 64, 0, s>>>(
       (const uint8_t *)wdata, n, k, L.d_off, L.ds, (const uint16_t *)x, m, y, yt, f, kts,
-      splits > 1 ? ws : nullptr, ws_stride, splits > 1 ? counters : nullptr, nullptr, nullptr);
+      splits > 1 ? ws : nullptr, ws_stride, nullptr, nullptr);
   return hipGetLastError();
 }
 
@@ -423,7 +376,7 @@ template <int QT, int XT, int BM, int BN, int WM, int WN>
 hipError_t launch_g(const GOp *ops, const int2 *order, int64_t entries, hipStream_t s) {
   if (entries <= 0 || entries > 0x7fffffff) return hipErrorInvalidValue;
   mfma_kernel<QT, XT, BM, BN, WM, WN, true><<<(unsigned)entries, WM * WN * 64, 0, s>>>(
-      nullptr, 0, 0, 0, 0, nullptr, 0, nullptr, 0, Fuse{}, 0, nullptr, 0, nullptr, ops, order);
+      nullptr, 0, 0, 0, 0, nullptr, 0, nullptr, 0, Fuse{}, 0, nullptr, 0, ops, order);
   return hipGetLastError();
 }
 
@@ -499,13 +452,6 @@ int forced_cfg() {
 }
 
 constexpr int64_t kMaxWorkspace = int64_t(64) << 20;  // bytes of fp32 partials per call
-
-// EB_SPLITK_TWO_PASS=1: sum split-K partials in a second kernel (the order is
-// the same, so the results are too; for tests and measurements).
-bool splitk_two_pass() {
-  const char *e = getenv("EB_SPLITK_TWO_PASS");
-  return e && e[0] == '1';
-}
 constexpr int kMinSplitTiles = 4;                      // K-tiles per split, at least
 
 // Estimated time (s) of one configuration and split count.  Workgroups run in
@@ -529,7 +475,7 @@ double estimate(int32_t type, const Cfg &g, int64_t m, int64_t n, int64_t k, int
   }
   const double wbytes = (double)n * k * (type == EB_Q8_0 ? 34.0 : 18.0) / 32.0;
   t = std::max(t, wbytes / 5e12);
-  if (splits > 1) t += (2.0 * splits + 1.0) * (double)m * n * 4 / 4e12 + 1e-6;
+  if (splits > 1) t += (2.0 * splits + 1.0) * (double)m * n * 4 / 4e12 + 3e-6;
   return t;
 }
 }  // namespace
@@ -655,26 +601,22 @@ hipError_t launch_gq(int cfg, const GOp *ops, const int2 *order, int64_t entries
 
 template <int QT, int XT>
 hipError_t launch_q(const void *wdata, int64_t n, int64_t k, const void *x, int64_t m, void *y,
-                    int32_t yt, const Fuse &f, const MfmaPlan &P, float *ws, unsigned *ctr,
-                    hipStream_t s) {
+                    int32_t yt, const Fuse &f, const MfmaPlan &P, float *ws, hipStream_t s) {
   const int sp = ws ? P.splits : 1;
   const int kts = ws ? P.kts : (int)((k + kBK - 1) / kBK);
   const int64_t st = P.ws_stride;
-  const int64_t tiles = ((m + kCfgs[P.cfg].bm - 1) / kCfgs[P.cfg].bm) *
-                        ((n + kCfgs[P.cfg].bn - 1) / kCfgs[P.cfg].bn);
-  if (tiles > kSplitCounters || splitk_two_pass()) ctr = nullptr;
   hipError_t e;
   switch (P.cfg) {
-    case 0: e = launch_t<QT, XT, 64, 128, 2, 2>(wdata, n, k, x, m, y, yt, f, sp, kts, ws, st, ctr, s); break;
-    case 1: e = launch_t<QT, XT, 128, 128, 2, 2>(wdata, n, k, x, m, y, yt, f, sp, kts, ws, st, ctr, s); break;
-    case 2: e = launch_t<QT, XT, 128, 256, 2, 4>(wdata, n, k, x, m, y, yt, f, sp, kts, ws, st, ctr, s); break;
-    case 3: e = launch_t<QT, XT, 256, 128, 4, 2>(wdata, n, k, x, m, y, yt, f, sp, kts, ws, st, ctr, s); break;
-    case 4: e = launch_t<QT, XT, 256, 192, 4, 2>(wdata, n, k, x, m, y, yt, f, sp, kts, ws, st, ctr, s); break;
-    case 5: e = launch_t<QT, XT, 256, 256, 4, 2>(wdata, n, k, x, m, y, yt, f, sp, kts, ws, st, ctr, s); break;
-    case 6: e = launch_t<QT, XT, 256, 256, 2, 4>(wdata, n, k, x, m, y, yt, f, sp, kts, ws, st, ctr, s); break;
-    default: e = launch_t<QT, XT, 256, 256, 2, 2>(wdata, n, k, x, m, y, yt, f, sp, kts, ws, st, ctr, s); break;
+    case 0: e = launch_t<QT, XT, 64, 128, 2, 2>(wdata, n, k, x, m, y, yt, f, sp, kts, ws, st, s); break;
+    case 1: e = launch_t<QT, XT, 128, 128, 2, 2>(wdata, n, k, x, m, y, yt, f, sp, kts, ws, st, s); break;
+    case 2: e = launch_t<QT, XT, 128, 256, 2, 4>(wdata, n, k, x, m, y, yt, f, sp, kts, ws, st, s); break;
+    case 3: e = launch_t<QT, XT, 256, 128, 4, 2>(wdata, n, k, x, m, y, yt, f, sp, kts, ws, st, s); break;
+    case 4: e = launch_t<QT, XT, 256, 192, 4, 2>(wdata, n, k, x, m, y, yt, f, sp, kts, ws, st, s); break;
+    case 5: e = launch_t<QT, XT, 256, 256, 4, 2>(wdata, n, k, x, m, y, yt, f, sp, kts, ws, st, s); break;
+    case 6: e = launch_t<QT, XT, 256, 256, 2, 4>(wdata, n, k, x, m, y, yt, f, sp, kts, ws, st, s); break;
+    default: e = launch_t<QT, XT, 256, 256, 2, 2>(wdata, n, k, x, m, y, yt, f, sp, kts, ws, st, s); break;
   }
-  if (e != hipSuccess || sp == 1 || ctr) return e;
+  if (e != hipSuccess || sp == 1) return e;
   const int64_t count = m * n;
   const int64_t blocks = (count + 1023) / 1024;
   splitk_reduce<<<(unsigned)blocks, 256, 0, s>>>(ws, sp, st, count, y, yt, f);
@@ -685,21 +627,13 @@ hipError_t launch_q(const void *wdata, int64_t n, int64_t k, const void *x, int6
 
 hipError_t launch_mfma(int32_t type, const void *wdata, int64_t n, int64_t k, const void *x,
                        int32_t xt, int64_t m, void *y, int32_t yt, const Fuse &f,
-                       const MfmaPlan &plan, float *ws, unsigned *ctr, hipStream_t s) {
+                       const MfmaPlan &plan, float *ws, hipStream_t s) {
   if (type == EB_Q4_0) {
-    if (xt == EB_F16) return launch_q<EB_Q4_0, EB_F16>(wdata, n, k, x, m, y, yt, f, plan, ws, ctr, s);
-    return launch_q<EB_Q4_0, EB_BF16>(wdata, n, k, x, m, y, yt, f, plan, ws, ctr, s);
+    if (xt == EB_F16) return launch_q<EB_Q4_0, EB_F16>(wdata, n, k, x, m, y, yt, f, plan, ws, s);
+    return launch_q<EB_Q4_0, EB_BF16>(wdata, n, k, x, m, y, yt, f, plan, ws, s);
   }
-  if (xt == EB_F16) return launch_q<EB_Q8_0, EB_F16>(wdata, n, k, x, m, y, yt, f, plan, ws, ctr, s);
-  return launch_q<EB_Q8_0, EB_BF16>(wdata, n, k, x, m, y, yt, f, plan, ws, ctr, s);
-}
-
-int mfma_launches(int32_t type, int64_t m, int64_t n, const MfmaPlan &plan) {
-  (void)type;
-  if (plan.splits <= 1) return 1;
-  const int64_t tiles = ((m + kCfgs[plan.cfg].bm - 1) / kCfgs[plan.cfg].bm) *
-                        ((n + kCfgs[plan.cfg].bn - 1) / kCfgs[plan.cfg].bn);
-  return (tiles > kSplitCounters || splitk_two_pass()) ? 2 : 1;
+  if (xt == EB_F16) return launch_q<EB_Q8_0, EB_F16>(wdata, n, k, x, m, y, yt, f, plan, ws, s);
+  return launch_q<EB_Q8_0, EB_BF16>(wdata, n, k, x, m, y, yt, f, plan, ws, s);
 }
 
 hipError_t launch_mfma_grouped(int32_t type, int32_t xt, int cfg, const GOp *ops, const int2 *order,

@@ -337,18 +337,14 @@ def test_mfma_force_validation(eb):
     assert f(-1, 0) == eb.EB_OK
 
 
-def test_stack_counts_split_k_reduction(eb, monkeypatch):
-    # a long-k MFMA op: one launch unsplit, and one when split (the last
-    # workgroup of each tile sums the partials); two (GEMM + reduction kernel)
-    # with EB_SPLITK_TWO_PASS=1
+def test_stack_counts_split_k_reduction(eb):
+    # a long-k MFMA op: one launch unsplit, two (GEMM + reduction) when split
     op = [_op(eb, 1 * GB, 8 * GB, 9 * GB, k=16384, n=2048, m=816, qtype=eb.EB_Q8_0,
               xt=eb.EB_BF16)]
     try:
         assert eb.lib.eb_mfma_force(-1, 1) == eb.EB_OK
         assert _launches(eb, op) == 1
         assert eb.lib.eb_mfma_force(-1, 4) == eb.EB_OK
-        assert _launches(eb, op) == 1
-        monkeypatch.setenv("EB_SPLITK_TWO_PASS", "1")
         assert _launches(eb, op) == 2
     finally:
         eb.lib.eb_mfma_force(-1, 0)

@@ -118,24 +118,6 @@ def test_fused_single_calls(eb, oracle, pro, epi, qtype, xdtype, ydtype):
         assert_fused(y, y_ref, scale, f"fused_{pro}_{epi} {qtype} m={m} {path} splits={splits}")
 
 
-@pytest.mark.parametrize("pro,epi", [(None, "add"), ("rmsnorm", "glu")])
-def test_split_k_epilogue_in_kernel_matches_two_pass(eb, pro, epi, monkeypatch):
-    """A split of k reduced by the last workgroup of each tile gives the bits of
-    the two-kernel reduction, with the epilogue applied by either."""
-    c = Case(eb, 1050, "q8_0", 198, 2368, 150, torch.bfloat16, pro, epi, torch.float32)
-    eb.mfma_force(-1, 4)
-    try:
-        one = c.run(eb, "mfma")
-        monkeypatch.setenv("EB_SPLITK_TWO_PASS", "1")
-        two = c.run(eb, "mfma")
-        monkeypatch.delenv("EB_SPLITK_TWO_PASS")
-        again = c.run(eb, "mfma")
-    finally:
-        eb.mfma_force(-1, 0)
-    torch.cuda.synchronize()
-    assert torch.equal(one, two) and torch.equal(one, again)
-
-
 def test_glu_on_long_rows_uses_paired_rows(eb, oracle):
     """m = 1 with k = 9216 (Q4_0: 288 units, one row per wave in the one-row
     kernel): the gate/up product runs on the general GEMV kernel instead."""

@@ -165,16 +165,6 @@ def test_split_k_deterministic_and_matches_unsplit(eb, forced):
     a = eb.qlinear(qw, xd, path="mfma")
     b = eb.qlinear(qw, xd, path="mfma")
     assert torch.equal(a, b)
-    # the last split of each tile sums the partials in split order, as the
-    # two-kernel reduction does: the same bits
-    os.environ["EB_SPLITK_TWO_PASS"] = "1"
-    try:
-        c = eb.qlinear(qw, xd, path="mfma")
-    finally:
-        del os.environ["EB_SPLITK_TWO_PASS"]
-    assert torch.equal(a, c)
-    for _ in range(3):  # counters are left at zero: repeated calls agree
-        assert torch.equal(eb.qlinear(qw, xd, path="mfma"), a)
     # same products, summed in another order: close, not necessarily equal
     scale = (x.float().abs() @ w.abs().t()).to(DEV)
     assert float(((a - whole).abs() / scale).max()) < 1e-4
