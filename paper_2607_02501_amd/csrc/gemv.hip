@@ -528,19 +528,13 @@ __device__ __attribute__((always_inline)) inline void m1_rows(const uint8_t *__r
       }
     }
   };
+  // weight loads of the first group are in flight while x is staged (and,
+  // with the prologue, normalised)
+  if (g < g_end) load_group(g);
   float rs[1] = {0.f};
-  if (f.pro == EB_PRO_RMSNORM) {
-    // normalise x first, then load the first group: the fp32 staging needs
-    // registers that the group's weights would otherwise hold
-    norm_factors<1>(static_cast<const float *>(x), 1, k, f.eps, reinterpret_cast<float *>(xs), rs);
-    stage_x<QT, XT, 1>(x, 1, k, ku, xs, xoff, P, true, f.gamma, rs);
-    __builtin_amdgcn_sched_barrier(0);
-    if (g < g_end) load_group(g);
-  } else {
-    // weight loads of the first group are in flight while x is staged
-    if (g < g_end) load_group(g);
-    stage_x<QT, XT, 1>(x, 1, k, ku, xs, xoff, P, false, f.gamma, rs);
-  }
+  const bool norm = f.pro == EB_PRO_RMSNORM;
+  if (norm) norm_factors<1>(static_cast<const float *>(x), 1, k, f.eps, reinterpret_cast<float *>(xs), rs);
+  stage_x<QT, XT, 1>(x, 1, k, ku, xs, xoff, P, norm, f.gamma, rs);
   if (threadIdx.x < CH) xs[threadIdx.x * P + 64 * NS] = make_uint4(0, 0, 0, 0);
   if (threadIdx.x == 0) xoff[64 * NS] = 0.f;
   __syncthreads();
