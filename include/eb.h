@@ -40,14 +40,16 @@
  *   - All pointers are DEVICE pointers unless stated otherwise; the caller owns
  *     every buffer (weights, activations, outputs).  The library never
  *     synchronises the stream.  It allocates device memory only for cached
- *     stack plans (eb_qlinear_stack) and for split-K workspaces (below).
+ *     stack plans (eb_qlinear_stack) and for per-stream workspaces of direct
+ *     calls (split-K partial sums, normalised activations; below).
  *   - Work is enqueued on `stream` (0 = the null stream); EB_OK means the work
  *     was enqueued, not that it finished.
  *   - Arguments are validated on the host before anything is launched; on any
  *     error nothing is launched and the output buffers are untouched.
  *   - Inputs must be finite.  Quantization requires max|w| / 127 <= 65504 per
  *     block (the binary16 scale must not overflow).
- *   - Outputs must not overlap inputs.
+ *   - Outputs must not overlap inputs (one exception: the residual of a
+ *     residual-adding epilogue may be the output itself, see below).
  *   - Sizes: 1 <= n <= 2^31 - 1, 32 <= k <= 2^24 with k % 32 == 0,
  *     0 <= m <= 2^24 (m == 0 is a no-op).
  *   - Thread-compatible: concurrent calls must use different output buffers.
@@ -203,9 +205,10 @@ eb_status eb_qweights_from_canonical(int32_t type, const void *src, int64_t n, i
  * nearest even).
  * No bias.  Accuracy: |y - y_exact| <= 2e-3 * sum_k |x||w_hat| per output
  * (plus the output rounding when y_type is 16-bit).
- * EB_ERR_INVALID: w or its data NULL, bad type/sizes, x/y NULL with m > 0.
+ * EB_ERR_INVALID: w or its data NULL, bad type/sizes, an unknown x_type or
+ * y_type, x/y NULL with m > 0, y overlapping x or the weights.
  * EB_ERR_ALIGN: x or y not 16-byte aligned, w->data not 256-byte aligned.
- * EB_ERR_UNSUPPORTED: other dtypes. EB_ERR_HIP: launch failure. */
+ * EB_ERR_UNSUPPORTED: x_type EB_F32. EB_ERR_HIP: launch failure. */
 eb_status eb_qlinear(const eb_qweights *w, const void *x, int32_t x_type, int64_t m, void *y,
                      int32_t y_type, hipStream_t stream);
 
