@@ -183,6 +183,23 @@ def test_fused_validation(eb, case, expect):
     assert eb.lib.eb_qlinear_fused(None, path, None) == eb.EB_ERR_INVALID
 
 
+def test_fused_m0_is_noop_and_still_validated(eb):
+    """m == 0 with fused steps launches nothing (null x, y, norm weight and
+    residual are allowed), but enum and shape fields are still checked."""
+    w = _w(eb)
+    op = eb.eb_qlinear_op(w, None, None, 0, eb.EB_BF16, eb.EB_F32, eb.EB_PRO_RMSNORM,
+                          eb.EB_EPI_ADD, None, None, 1e-5, 0)
+    assert eb.lib.eb_qlinear_fused(ctypes.byref(op), eb.EB_PATH_AUTO, None) == eb.EB_OK
+    arr = (eb.eb_qlinear_op * 2)(op, op)
+    assert eb.lib.eb_qlinear_stack_launches(arr, 2) == 0
+    op.epilogue = 7
+    assert eb.lib.eb_qlinear_fused(ctypes.byref(op), eb.EB_PATH_AUTO, None) == eb.EB_ERR_INVALID
+    op.epilogue, op.norm_eps = eb.EB_EPI_GLU, -1.0
+    assert eb.lib.eb_qlinear_fused(ctypes.byref(op), eb.EB_PATH_AUTO, None) == eb.EB_ERR_INVALID
+    op.norm_eps, op.w.n = 1e-5, 63  # odd n with the gate/up epilogue
+    assert eb.lib.eb_qlinear_fused(ctypes.byref(op), eb.EB_PATH_AUTO, None) == eb.EB_ERR_INVALID
+
+
 def test_fused_stack_counts_prologue_launches(eb):
     """A normalisation prologue costs a row-kernel launch on the MFMA path and
     nothing on the GEMV path; dependencies through the residual stream split runs."""
