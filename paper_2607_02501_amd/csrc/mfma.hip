@@ -45,6 +45,14 @@
 namespace eb {
 namespace {
 
+// A 1 KiB-aligned LDS array of its own (one per BYTES, ID), allocated only in
+// kernels that call this.
+template <int BYTES, int ID>
+__device__ inline uint8_t *lds_array() {
+  __shared__ __attribute__((aligned(1024))) uint8_t a[BYTES];
+  return a;
+}
+
 // G: grouped launch over several independent ops -- workgroup b runs tile
 // gorder[b].y of op gorder[b].x (entries with a negative op do nothing), with
 // the op's operands from gops; the scalar arguments are then unused.
@@ -95,17 +103,22 @@ __global__ void __launch_bounds__(WM *WN * 64)
   static_assert(ADMA >= 1 && ADMA * 8 * WAVES == BM, "x tile must split into 8-row copies");
   static_assert(TM % 32 == 0 && TN % 32 == 0, "wave sub-tile must be whole fragments");
   static_assert(2 * NW + NX <= 63, "vmcnt range");
+  // x buffers: three when they fit the 160 KiB of LDS beside the two weight
+  // buffers (x tile t + 2 is copied during step t), else two (x tile t + 1).
+  constexpr int NA = (3 * ABYTES + 2 * BBYTES <= 160 * 1024) ? 3 : 2;
+  static_assert(NA * ABYTES + 2 * BBYTES <= 160 * 1024, "tile does not fit the LDS");
 
-  // Three x buffers (tile kt in use, kt+1 landing, kt+2 being copied) and two
-  // weight buffers.  Separate objects, so the compiler can tell the
+  // NA x buffers (tile kt in use, kt+1 landing, kt+2 being copied; or tile kt
+  // in use, kt+1 being copied) and two weight buffers.  Separate objects, so the compiler can tell the
   // asynchronous copies into one x buffer from the reads of another.  Both
   // tiles use unpadded 128-byte rows with 16-byte chunk c of row r stored at
   // position c ^ swz(r).
   __shared__ __attribute__((aligned(1024))) uint8_t sA0[ABYTES];
   __shared__ __attribute__((aligned(1024))) uint8_t sA1[ABYTES];
-  __shared__ __attribute__((aligned(1024))) uint8_t sA2[ABYTES];
   __shared__ __attribute__((aligned(1024))) uint8_t sB0[BBYTES];
   __shared__ __attribute__((aligned(1024))) uint8_t sB1[BBYTES];
+  uint8_t *sA2 = nullptr;
+  if constexpr (NA == 3) sA2 = lds_array<ABYTES, 2>();
 
   // Workgroup -> (K split, output tile).  Split s covers K-tiles
   // [s kts, (s + 1) kts) and, when there are several splits (ws != null),
@@ -198,18 +211,23 @@ __global__ void __launch_bounds__(WM *WN * 64)
   };
 
   // Fragment addresses: lane reads row (lane & 31) of a fragment, logical
-  // chunk 2 ks + lane / 32, stored at (2 ks + lane / 32) ^ swz(row); since 2 ks
-  // is even that is base ^ (32 ks).
-  uint32_t abase[FM], bbase[FN];
+  // chunk 2 ks + lane / 32, stored at (2 ks + lane / 32) ^ swz(row).  Adding
+  // 32 to a row flips bit 2 of swz (adding 4 to the 3-bit row / 8 term), so
+  // fragment i of k-step ks sits at
+  //   (a0 ^ 32 (ks ^ 2 (i & 1))) + 4096 i,
+  // a0 = this lane's address in fragment 0 of k-step 0: four lane addresses
+  // per operand serve every fragment of every k-step, the rest is an
+  // immediate offset.
+  uint32_t aq[4], bq[4];
+  {
+    const uint32_t ra = wm * TM + (lane & 31), rb = wn * TN + (lane & 31);
+    const uint32_t a0 = ra * (kBK * 2) + ((((uint32_t)lane >> 5) ^ swz(ra)) << 4);
+    const uint32_t b0 = rb * (kBK * 2) + ((((uint32_t)lane >> 5) ^ swz(rb)) << 4);
 #pragma unroll
-  for (int i = 0; i < FM; ++i) {
-    const uint32_t r = wm * TM + i * 32 + (lane & 31);
-    abase[i] = r * (kBK * 2) + ((((uint32_t)lane >> 5) ^ swz(r)) << 4);
-  }
-#pragma unroll
-  for (int j = 0; j < FN; ++j) {
-    const uint32_t r = wn * TN + j * 32 + (lane & 31);
-    bbase[j] = r * (kBK * 2) + ((((uint32_t)lane >> 5) ^ swz(r)) << 4);
+    for (int q = 0; q < 4; ++q) {
+      aq[q] = a0 ^ (32u * q);
+      bq[q] = b0 ^ (32u * q);
+    }
   }
 
   f32x16_t acc[FM][FN];
@@ -220,54 +238,73 @@ __global__ void __launch_bounds__(WM *WN * 64)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
+  auto read_frags = [&](const uint8_t *sA, const uint8_t *sB, int ks, uint4 (&af)[FM],
+                        uint4 (&bfr)[FN]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+      af[i] = *reinterpret_cast<const uint4 *>(sA + aq[ks ^ (2 * (i & 1))] + 4096 * i);
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+      bfr[j] = *reinterpret_cast<const uint4 *>(sB + bq[ks ^ (2 * (j & 1))] + 4096 * j);
+  };
+
   // MFMAs of the tile in (sA, sB); the dequantizing stores of the next tile
   // (raw set `nxt`, already in registers) into sBn are spread over the k-steps
-  // so the VALU work overlaps the matrix cores.
+  // so the VALU work overlaps the matrix cores.  The fragments of k-step ks + 1
+  // are read while the MFMAs of k-step ks run (two register sets), and the
+  // scheduling groups at the end keep that order: each LDS read then has a
+  // whole k-step of MFMA work to land instead of stalling the chain.
   auto compute = [&](const uint8_t *sA, const uint8_t *sB, const Raw &nxt, uint8_t *sBn,
                      bool more) __attribute__((always_inline)) {
+    uint4 af[2][FM], bfr[2][FN];
+    read_frags(sA, sB, 0, af[0], bfr[0]);
 #pragma unroll
     for (int ks = 0; ks < KSTEPS; ++ks) {
-      uint4 af[FM], bfr[FN];
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-        af[i] = *reinterpret_cast<const uint4 *>(sA + (abase[i] ^ (32u * ks)));
-#pragma unroll
-      for (int j = 0; j < FN; ++j)
-        bfr[j] = *reinterpret_cast<const uint4 *>(sB + (bbase[j] ^ (32u * ks)));
+      if (ks + 1 < KSTEPS) read_frags(sA, sB, ks + 1, af[(ks + 1) & 1], bfr[(ks + 1) & 1]);
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
-        for (int j = 0; j < FN; ++j) acc[i][j] = mfma32<XT>(af[i], bfr[j], acc[i][j]);
+        for (int j = 0; j < FN; ++j) acc[i][j] = mfma32<XT>(af[ks & 1][i], bfr[ks & 1][j], acc[i][j]);
       if (more) {
         constexpr int per = (BCH + KSTEPS - 1) / KSTEPS;
 #pragma unroll
         for (int i = ks * per; i < ks * per + per && i < BCH; ++i) store_w(nxt, sBn, i);
       }
     }
+    // reads of k-step 0, the step's weight loads, then per k-step the reads
+    // of the next k-step ahead of this k-step's MFMAs
+    __builtin_amdgcn_sched_group_barrier(0x100, FM + FN, 0);
+    __builtin_amdgcn_sched_group_barrier(0x020, NW, 0);
+#pragma unroll
+    for (int ks = 0; ks < KSTEPS; ++ks) {
+      if (ks + 1 < KSTEPS) __builtin_amdgcn_sched_group_barrier(0x100, FM + FN, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, FM * FN, 0);
+    }
   };
 
   // Rows of the x buffers that no copy fills (past m) keep these zeros.
   {
-    constexpr int Z = 3 * ABYTES / 16 / T;
-    static_assert(Z * T * 16 == 3 * ABYTES, "zero fill must cover the x buffers");
+    constexpr int Z = NA * ABYTES / 16 / T;
+    static_assert(Z * T * 16 == NA * ABYTES, "zero fill must cover the x buffers");
 #pragma unroll
     for (int i = 0; i < Z; ++i) {
       const int o = (tid + i * T) * 16;
-      uint8_t *dst = o < ABYTES ? sA0 + o : (o < 2 * ABYTES ? sA1 + (o - ABYTES) : sA2 + (o - 2 * ABYTES));
+      uint8_t *dst = o < ABYTES ? sA0 + o : (NA == 2 || o < 2 * ABYTES ? sA1 + (o - ABYTES) : sA2 + (o - 2 * ABYTES));
       *reinterpret_cast<uint4 *>(dst) = make_uint4(0, 0, 0, 0);
     }
   }
   __syncthreads();
 
   // Pipeline: entering the step of tile t, x tile t is in LDS, x tile t+1 is
-  // being copied, the weights of tile t+1 are in registers (or arriving) and
-  // those of tile t+2 are in flight.  The step issues x tile t+2 and weight
-  // tile t+3, runs the MFMAs of tile t while dequantizing weight tile t+1 into
-  // the other weight buffer, then waits only for x tile t+1 (issued one step
-  // earlier) before the barrier: every load has about two steps to land.
+  // being copied (NA = 3), the weights of tile t+1 are in registers (or
+  // arriving) and those of tile t+2 are in flight.  The step issues x tile
+  // t + NA - 1 and weight tile t+3, runs the MFMAs of tile t while
+  // dequantizing weight tile t+1 into the other weight buffer, then waits only
+  // for x tile t+1 before the barrier: weight loads have about two steps to
+  // land, x copies NA - 1.
   load_x(sA0, 0);
   load_w(S0, 0);
-  if (nk > 1) load_x(sA1, 1);
+  if (NA == 3 && nk > 1) load_x(sA1, 1);
   if (nk > 1) load_w(S1, 1);
   if (nk > 2) load_w(S2, 2);
 #pragma unroll
@@ -280,30 +317,54 @@ __global__ void __launch_bounds__(WM *WN * 64)
   auto step = [&](int t, const uint8_t *A, uint8_t *A2, const uint8_t *B, uint8_t *Bn,
                   const Raw &deq, Raw &ld, bool guarded) __attribute__((always_inline)) {
     if (guarded && t >= nk) return;
-    if (!guarded || t + 2 < nk) load_x(A2, t + 2);
+    if (!guarded || t + NA - 1 < nk) load_x(A2, t + NA - 1);
+    // the x copies stay ahead of the weight loads: the wait below counts on
+    // the copy of tile t + 1 being older than the last 2 NW + NX operations
+    // (NA = 3: weights t + 2, x t + 2, weights t + 3), or NW (NA = 2: weights
+    // t + 3)
+    __builtin_amdgcn_sched_barrier(0);
     if (!guarded || t + 3 < nk) load_w(ld, t + 3);
     compute(A, B, deq, Bn, !guarded || t + 1 < nk);
     if (!guarded || t + 3 < nk)
-      wait_vm_barrier<2 * NW + NX>();
+      wait_vm_barrier<NA == 3 ? 2 * NW + NX : NW>();
     else
       wait_vm_barrier<0>();
   };
   int kt = 0;
-  for (; kt + 8 < nk; kt += 6) {
-    step(kt + 0, sA0, sA2, sB0, sB1, S1, S0, false);
-    step(kt + 1, sA1, sA0, sB1, sB0, S2, S1, false);
-    step(kt + 2, sA2, sA1, sB0, sB1, S0, S2, false);
-    step(kt + 3, sA0, sA2, sB1, sB0, S1, S0, false);
-    step(kt + 4, sA1, sA0, sB0, sB1, S2, S1, false);
-    step(kt + 5, sA2, sA1, sB1, sB0, S0, S2, false);
-  }
-  for (; kt < nk; kt += 6) {
-    step(kt + 0, sA0, sA2, sB0, sB1, S1, S0, true);
-    step(kt + 1, sA1, sA0, sB1, sB0, S2, S1, true);
-    step(kt + 2, sA2, sA1, sB0, sB1, S0, S2, true);
-    step(kt + 3, sA0, sA2, sB1, sB0, S1, S0, true);
-    step(kt + 4, sA1, sA0, sB0, sB1, S2, S1, true);
-    step(kt + 5, sA2, sA1, sB1, sB0, S0, S2, true);
+  if constexpr (NA == 3) {
+    for (; kt + 8 < nk; kt += 6) {
+      step(kt + 0, sA0, sA2, sB0, sB1, S1, S0, false);
+      step(kt + 1, sA1, sA0, sB1, sB0, S2, S1, false);
+      step(kt + 2, sA2, sA1, sB0, sB1, S0, S2, false);
+      step(kt + 3, sA0, sA2, sB1, sB0, S1, S0, false);
+      step(kt + 4, sA1, sA0, sB0, sB1, S2, S1, false);
+      step(kt + 5, sA2, sA1, sB1, sB0, S0, S2, false);
+    }
+    for (; kt < nk; kt += 6) {
+      step(kt + 0, sA0, sA2, sB0, sB1, S1, S0, true);
+      step(kt + 1, sA1, sA0, sB1, sB0, S2, S1, true);
+      step(kt + 2, sA2, sA1, sB0, sB1, S0, S2, true);
+      step(kt + 3, sA0, sA2, sB1, sB0, S1, S0, true);
+      step(kt + 4, sA1, sA0, sB0, sB1, S2, S1, true);
+      step(kt + 5, sA2, sA1, sB1, sB0, S0, S2, true);
+    }
+  } else {
+    for (; kt + 8 < nk; kt += 6) {
+      step(kt + 0, sA0, sA1, sB0, sB1, S1, S0, false);
+      step(kt + 1, sA1, sA0, sB1, sB0, S2, S1, false);
+      step(kt + 2, sA0, sA1, sB0, sB1, S0, S2, false);
+      step(kt + 3, sA1, sA0, sB1, sB0, S1, S0, false);
+      step(kt + 4, sA0, sA1, sB0, sB1, S2, S1, false);
+      step(kt + 5, sA1, sA0, sB1, sB0, S0, S2, false);
+    }
+    for (; kt < nk; kt += 6) {
+      step(kt + 0, sA0, sA1, sB0, sB1, S1, S0, true);
+      step(kt + 1, sA1, sA0, sB1, sB0, S2, S1, true);
+      step(kt + 2, sA0, sA1, sB0, sB1, S0, S2, true);
+      step(kt + 3, sA1, sA0, sB1, sB0, S1, S0, true);
+      step(kt + 4, sA0, sA1, sB0, sB1, S2, S1, true);
+      step(kt + 5, sA1, sA0, sB1, sB0, S0, S2, true);
+    }
   }
 
   // epilogue: lane holds column (lane & 31), rows 8*(r/4) + 4*(lane/32) + r%4;
@@ -424,17 +485,23 @@ __global__ void __launch_bounds__(256)
 }
 
 // Tile configurations: {BM, BN, WM, WN, workgroups per CU (LDS-bound),
-// full-chip rate in TFLOP/s on large problems (measured)}.  The rate only
-// ranks configurations against each other.
+// full-chip rate in TFLOP/s on large problems (measured), weight formats it
+// is planned for (bit 0: Q8_0, bit 1: Q4_0)}.  The rate only ranks
+// configurations against each other.  512 x 128 (two x buffers) halves the
+// dequantization per flop of the 256-row tiles; with Q4_0 only half of its
+// threads have a 32-weight chunk to dequantize per K-tile, which made it
+// slower than 256 x 256 there (measured), so it is planned for Q8_0 only.
 struct Cfg {
   int bm, bn, wm, wn, per_cu;
   double rate;
+  int formats;
 };
 constexpr Cfg kCfgs[] = {
-    {64, 128, 2, 2, 2, 546},   {128, 128, 2, 2, 2, 769},  {128, 256, 2, 4, 1, 773},
-    {256, 128, 4, 2, 1, 812},  {256, 192, 4, 2, 1, 900},  {256, 256, 4, 2, 1, 902},
-    {256, 256, 2, 4, 1, 977},  {256, 256, 2, 2, 1, 835},
+    {64, 128, 2, 2, 2, 546, 3},  {128, 128, 2, 2, 2, 769, 3}, {128, 256, 2, 4, 1, 773, 3},
+    {256, 128, 4, 2, 1, 812, 3}, {256, 192, 4, 2, 1, 900, 3}, {256, 256, 4, 2, 1, 902, 3},
+    {256, 256, 2, 4, 1, 977, 3}, {256, 256, 2, 2, 1, 835, 3}, {512, 128, 4, 2, 1, 1035, 1},
 };
+bool planned_for(const Cfg &g, int32_t type) { return g.formats & (type == EB_Q8_0 ? 1 : 2); }
 constexpr int kNumCfgs = sizeof(kCfgs) / sizeof(kCfgs[0]);
 
 std::atomic<int> g_force_cfg{-1}, g_force_splits{0};
@@ -502,6 +569,7 @@ MfmaPlan plan_mfma(int32_t type, int64_t m, int64_t n, int64_t k, bool allow_spl
   for (int c = 0; c < kNumCfgs; ++c) {
     if (fc >= 0 && fc < kNumCfgs && c != fc) continue;
     const Cfg &g = kCfgs[c];
+    if (c != fc && !planned_for(g, type)) continue;
     const bool fits = type == EB_Q4_0 ? fits_offsets<EB_Q4_0, 0, 0>(n, k, g.bm, g.bn)
                                       : fits_offsets<EB_Q8_0, 0, 0>(n, k, g.bm, g.bn);
     if (!fits) continue;
@@ -614,7 +682,8 @@ hipError_t launch_q(const void *wdata, int64_t n, int64_t k, const void *x, int6
     case 4: e = launch_t<QT, XT, 256, 192, 4, 2>(wdata, n, k, x, m, y, yt, f, sp, kts, ws, st, s); break;
     case 5: e = launch_t<QT, XT, 256, 256, 4, 2>(wdata, n, k, x, m, y, yt, f, sp, kts, ws, st, s); break;
     case 6: e = launch_t<QT, XT, 256, 256, 2, 4>(wdata, n, k, x, m, y, yt, f, sp, kts, ws, st, s); break;
-    default: e = launch_t<QT, XT, 256, 256, 2, 2>(wdata, n, k, x, m, y, yt, f, sp, kts, ws, st, s); break;
+    case 7: e = launch_t<QT, XT, 256, 256, 2, 2>(wdata, n, k, x, m, y, yt, f, sp, kts, ws, st, s); break;
+    default: e = launch_t<QT, XT, 512, 128, 4, 2>(wdata, n, k, x, m, y, yt, f, sp, kts, ws, st, s); break;
   }
   if (e != hipSuccess || sp == 1) return e;
   const int64_t count = m * n;
