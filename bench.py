@@ -85,7 +85,7 @@ def load_traffic(workload, kernel):
     """HBM bytes per launch from committed rocprofv3 counter runs
     (profiles/traffic.json, written by paper_2607_02501_amd.traffic), if they
     were taken on the current kernel sources; otherwise None."""
-    from paper_2607_02501_amd.srchash import kernel_sources_sha
+    from paper_2607_02501_amd.srchash import family, kernel_sources_sha
 
     path = os.path.join(ROOT, "profiles", "traffic.json")
     try:
@@ -93,7 +93,8 @@ def load_traffic(workload, kernel):
             rec = json.load(fh).get(workload, {}).get(kernel)
     except (OSError, ValueError):
         return None
-    if not rec or rec.get("kernel_sources_sha") != kernel_sources_sha(kernel.split("_")[0]):
+    if not rec or rec.get("kernel_sources_sha") != kernel_sources_sha(
+            family(rec.get("kernel_symbol", ""))):
         return None
     return rec.get("hbm_bytes_per_launch")
 

@@ -4,17 +4,29 @@ import hashlib
 import os
 
 _CSRC = os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc")
+_COMMON = ("epilogue.h", "eb_internal.h", "eb_api.cpp")
 _FILES = {
-    "gemv": ("gemv.hip", "epilogue.h", "eb_internal.h", "eb_api.cpp"),
-    "mfma": ("mfma.hip", "mfma_multi.hip", "mfma_lds2.hip", "mfma_common.h", "mm_common.h", "norm.hip",
-             "epilogue.h",
-             "eb_internal.h", "eb_api.cpp"),
+    # GEMV kernels (m <= 8)
+    "gemv": ("gemv.hip",) + _COMMON,
+    # tile kernel of the MFMA path (single ops, split-K, grouped launches)
+    "mfma": ("mfma.hip", "mfma_common.h", "norm.hip") + _COMMON,
+    # fused small-m MFMA kernels (m <= 128)
+    "mm": ("mfma_lds2.hip", "mfma_multi.hip", "mfma_common.h", "mm_common.h", "norm.hip") + _COMMON,
 }
 
 
-def kernel_sources_sha(path: str) -> str:
+def family(symbol: str) -> str:
+    """Kernel family of a kernel symbol (as the profiler names it)."""
+    if symbol.startswith("gemv"):
+        return "gemv"
+    if symbol.startswith("mm_"):
+        return "mm"
+    return "mfma"
+
+
+def kernel_sources_sha(fam: str) -> str:
     h = hashlib.sha256()
-    for f in _FILES[path]:
+    for f in _FILES[fam]:
         with open(os.path.join(_CSRC, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]

@@ -16,7 +16,7 @@ import csv
 import json
 import sys
 
-from paper_2607_02501_amd.srchash import kernel_sources_sha
+from paper_2607_02501_amd.srchash import family, kernel_sources_sha
 
 
 def per_dispatch(path, symbol, pick=None):
@@ -48,14 +48,13 @@ def main():
         db = json.load(open(out))
     except (OSError, ValueError):
         db = {}
-    path = label.split("_")[0]
     db.setdefault(workload, {})[label] = {
         "kernel_symbol": symbol, "dispatches": len(fv), "dispatch_range": pick,
         "fetch_bytes_per_launch": round(fetch), "write_bytes_per_launch": round(write),
         "hbm_bytes_per_launch": round(fetch + write),
         "fetch_scale": round(fscale, 4), "write_scale": round(wscale, 4),
         "calibration_copy_bytes": int(calib),
-        "kernel_sources_sha": kernel_sources_sha(path),
+        "kernel_sources_sha": kernel_sources_sha(family(symbol)),
     }
     json.dump(db, open(out, "w"), indent=1, sort_keys=True)
     print(json.dumps(db[workload][label]))
