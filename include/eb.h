@@ -243,8 +243,12 @@ int32_t eb_qlinear_auto_path(int32_t type, int32_t x_type, int64_t m, int64_t n,
  *   with the same formats by one grouped launch over all their output tiles
  *   (whose mostly-padded last row tiles may go to a small-m launch).  Results
  *   are those of running the ops in order; the m == 1 fusion is bitwise
- *   identical to single calls.  EB_STACK_FUSE=0 disables fusion,
- *   EB_STACK_GROUP=0 the grouped launch, EB_STACK_SPLIT_TAIL=0 its tail split.
+ *   identical to single calls.  The small-m launch of split-off rows runs
+ *   beside its grouped launch on a second, library-owned stream (default
+ *   priority), forked from and joined back into `stream` inside the recorded
+ *   graph.  EB_STACK_FUSE=0 disables fusion, EB_STACK_GROUP=0 the grouped
+ *   launch, EB_STACK_SPLIT_TAIL=0 its tail split, EB_STACK_OVERLAP_TAIL=0 the
+ *   second stream (the tail launch then follows the grouped one).
  *   Graph replay: the first call with a given op list (same pointers, sizes,
  *   types) builds a plan, records it into a HIP graph on a library-owned
  *   stream and caches both; later calls replay the graph with one launch.

@@ -299,6 +299,20 @@ struct NormJob {
 // have reserved == 0).
 constexpr int32_t kRelX = 1;
 
+// Cap on the workgroups of a split-off-rows launch running beside a grouped
+// launch (0: one per CU, as alone).  Measured on the m = 816 VLM prefill pass:
+// no cap 3.89 ms, 128 or 64 workgroups 3.91-3.93 ms, 32 4.17 ms, 16 7.47 ms,
+// the launch after the grouped one instead of beside it 4.00 ms.  Tuning hook:
+// EB_STACK_SIDE_GROUPS (read once).
+int side_groups() {
+  static const int g = [] {
+    const char *e = std::getenv("EB_STACK_SIDE_GROUPS");
+    const int v = e ? std::atoi(e) : 0;
+    return v >= 8 ? v : 0;
+  }();
+  return g;
+}
+
 struct Step {
   int op = -1;        // single op index, or -1 for a fused launch
   bool mfma = false;  // single op on the MFMA path, run with plan `mp`
@@ -315,6 +329,8 @@ struct Step {
   size_t order = 0;   // workgroup entries from `order`
   int64_t entries = 0;
   std::vector<NormJob> norms;  // prologue row kernels run before the step
+  bool side = false;  // fused launch of split-off rows that runs on the side stream,
+                      // beside the grouped launch before it
 };
 
 struct Plan {
@@ -328,6 +344,7 @@ struct Plan {
   size_t ws_bytes = 0;
   uint8_t *xbuf = nullptr;  // normalised activations of prologue ops on the MFMA path
   size_t xbuf_bytes = 0;
+  hipEvent_t fork = nullptr, join = nullptr;  // side-stream steps (created when there are any)
   hipGraph_t graph = nullptr;
   hipGraphExec_t exec = nullptr;
 };
@@ -394,7 +411,7 @@ eb_status build_plan(const eb_qlinear_op *ops, int32_t n_ops, bool alloc, Plan &
     return c;
   };
   // one fused small-m launch over `list` (same weight, x and y formats)
-  auto add_mm_step = [&](const std::vector<eb_qlinear_op> &list) {
+  auto add_mm_step = [&](const std::vector<eb_qlinear_op> &list, int max_groups = 0) {
     int64_t max_m = 0;
     for (const eb_qlinear_op &o : list) max_m = std::max(max_m, o.m);
     Step s;
@@ -427,7 +444,7 @@ eb_status build_plan(const eb_qlinear_op *ops, int32_t n_ops, bool alloc, Plan &
       run.push_back(e);
     }
     std::vector<int64_t> wg;
-    s.groups = mm_partition(run, s.mm_cfg, wg);
+    s.groups = mm_partition(run, s.mm_cfg, wg, max_groups);
     s.nops = (int)run.size();
     s.units = units;
     s.wg = mmwg.size();
@@ -544,12 +561,18 @@ eb_status build_plan(const eb_qlinear_op *ops, int32_t n_ops, bool alloc, Plan &
           gmhost.insert(gmhost.end(), run.begin(), run.end());
           gmorder.insert(gmorder.end(), order.begin(), order.end());
           P.steps.push_back(s);
-          // the split-off rows: one fused launch per output size
+          // the split-off rows: one fused launch per output size.  They are
+          // independent of the grouped launch (other output rows), so they run
+          // beside it on a side stream: their weight streaming overlaps the
+          // grouped launch's matrix-core work instead of following it.
+          const bool overlap = !env_off("EB_STACK_OVERLAP_TAIL");
           for (int wide = 1; wide >= 0; --wide) {
             std::vector<eb_qlinear_op> cls;
             for (const eb_qlinear_op &t : tails)
               if ((t.y_type == EB_F32) == (wide == 1)) cls.push_back(t);
-            if (!cls.empty()) add_mm_step(cls);
+            if (cls.empty()) continue;
+            add_mm_step(cls, overlap ? side_groups() : 0);
+            P.steps.back().side = overlap;
           }
           i = j;
           done = true;
@@ -701,11 +724,30 @@ void print_plan(const eb_qlinear_op *ops, const Plan &P) {
   }
 }
 
-eb_status run_plan(const eb_qlinear_op *ops, const Plan &P, hipStream_t s) {
-  for (const Step &st : P.steps) {
+eb_status run_plan(const eb_qlinear_op *ops, const Plan &P, hipStream_t s, hipStream_t side) {
+  for (size_t i = 0; i < P.steps.size(); ++i) {
+    const Step &st = P.steps[i];
+    if (st.side) continue;  // launched with the grouped step before it
     for (const NormJob &j : st.norms)
       if (launch_rmsnorm(j.h, j.gamma, j.eps, j.m, j.k, j.xt, P.xbuf + j.off, s) != hipSuccess)
         return EB_ERR_HIP;
+    // side steps after a grouped step: fork them onto the side stream first
+    // (their workgroups take a few CUs before the grouped launch fills the
+    // rest), and join them back after the grouped launch
+    size_t nside = 0;
+    while (st.gm && i + 1 + nside < P.steps.size() && P.steps[i + 1 + nside].side) ++nside;
+    if (nside > 0) {
+      if (!side || hipEventRecord(P.fork, s) != hipSuccess ||
+          hipStreamWaitEvent(side, P.fork, 0) != hipSuccess)
+        return EB_ERR_HIP;
+      for (size_t q = 1; q <= nside; ++q) {
+        const Step &t = P.steps[i + q];
+        if (launch_mfma_multi(t.type, t.xt, t.yt, t.mm_cfg, P.mmtable + t.table, t.nops,
+                              P.mmwg + t.wg, t.groups, side) != hipSuccess)
+          return EB_ERR_HIP;
+      }
+      if (hipEventRecord(P.join, side) != hipSuccess) return EB_ERR_HIP;
+    }
     if (st.gm) {
       // the table entries index the whole plan's op table
       if (launch_mfma_grouped(st.type, st.xt, st.mm_cfg, P.gmtable, P.gmorder + st.order,
@@ -726,6 +768,7 @@ eb_status run_plan(const eb_qlinear_op *ops, const Plan &P, hipStream_t s) {
                                     st.rows, s) != hipSuccess) {
       return EB_ERR_HIP;
     }
+    if (nside > 0 && hipStreamWaitEvent(s, P.join, 0) != hipSuccess) return EB_ERR_HIP;
   }
   return EB_OK;
 }
@@ -740,6 +783,8 @@ void destroy_plan(Plan &p) {
   if (p.gmorder) (void)hipFree(p.gmorder);
   if (p.ws) (void)hipFree(p.ws);
   if (p.xbuf) (void)hipFree(p.xbuf);
+  if (p.fork) (void)hipEventDestroy(p.fork);
+  if (p.join) (void)hipEventDestroy(p.join);
   p = Plan();
 }
 
@@ -747,6 +792,7 @@ struct StackCache {
   std::mutex mu;
   std::unordered_map<std::string, Plan> map;
   hipStream_t capture_stream[64] = {};
+  hipStream_t side_stream[64] = {};  // default priority, like every stream here
 };
 
 StackCache &cache() {
@@ -883,6 +929,7 @@ eb_status eb_qlinear_stack(const eb_qlinear_op *ops, int32_t n_ops, hipStream_t 
   key.push_back(env_off("EB_STACK_FUSE") ? 'u' : 'f');
   key.push_back(env_off("EB_STACK_GROUP") ? 'n' : 'g');
   key.push_back(env_off("EB_STACK_SPLIT_TAIL") ? 'w' : 's');
+  key.push_back(env_off("EB_STACK_OVERLAP_TAIL") ? 'q' : 'o');
   const int fk = mfma_force_key();
   key.append(reinterpret_cast<const char *>(&fk), sizeof(fk));
   key.append(reinterpret_cast<const char *>(ops), sizeof(eb_qlinear_op) * (size_t)n_ops);
@@ -899,6 +946,19 @@ eb_status eb_qlinear_stack(const eb_qlinear_op *ops, int32_t n_ops, hipStream_t 
       return st;
     }
     if (std::getenv("EB_STACK_DEBUG")) print_plan(ops, P);
+    bool has_side = false;
+    for (const Step &s : P.steps) has_side = has_side || s.side;
+    if (has_side && !C.side_stream[dev] &&
+        hipStreamCreateWithFlags(&C.side_stream[dev], hipStreamNonBlocking) != hipSuccess) {
+      C.side_stream[dev] = nullptr;
+      destroy_plan(P);
+      return EB_ERR_HIP;
+    }
+    if (has_side && (hipEventCreateWithFlags(&P.fork, hipEventDisableTiming) != hipSuccess ||
+                     hipEventCreateWithFlags(&P.join, hipEventDisableTiming) != hipSuccess)) {
+      destroy_plan(P);
+      return EB_ERR_HIP;
+    }
     if (use_graph) {
       if (!C.capture_stream[dev] &&
           hipStreamCreateWithFlags(&C.capture_stream[dev], hipStreamNonBlocking) != hipSuccess) {
@@ -911,7 +971,7 @@ eb_status eb_qlinear_stack(const eb_qlinear_op *ops, int32_t n_ops, hipStream_t 
         destroy_plan(P);
         return EB_ERR_HIP;
       }
-      st = run_plan(ops, P, cap);
+      st = run_plan(ops, P, cap, C.side_stream[dev]);
       hipError_t e = hipStreamEndCapture(cap, &P.graph);
       if (st != EB_OK || e != hipSuccess || !P.graph ||
           hipGraphInstantiate(&P.exec, P.graph, nullptr, nullptr, 0) != hipSuccess) {
@@ -923,7 +983,7 @@ eb_status eb_qlinear_stack(const eb_qlinear_op *ops, int32_t n_ops, hipStream_t 
   }
   const Plan &P = it->second;
   if (P.exec) return hipGraphLaunch(P.exec, stream) == hipSuccess ? EB_OK : EB_ERR_HIP;
-  return run_plan(ops, P, stream);
+  return run_plan(ops, P, stream, C.side_stream[dev]);
 }
 
 int32_t eb_qlinear_stack_launches(const eb_qlinear_op *ops, int32_t n_ops) {

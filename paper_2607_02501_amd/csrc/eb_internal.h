@@ -154,7 +154,10 @@ hipError_t launch_lds2(int32_t type, int32_t xt, int32_t yt, const MMOp *ops, in
                        const int64_t *wg, int groups, hipStream_t s);
 // Fills the unit ranges wg[0..groups] (balanced by steps) for a table whose
 // unit_end / nk are set; returns the number of workgroups to launch.
-int mm_partition(const std::vector<MMOp> &ops, int cfg, std::vector<int64_t> &wg);
+// Workgroup unit ranges of a fused small-m launch; max_groups > 0 caps the
+// workgroup count (rounded to a multiple of 8).
+int mm_partition(const std::vector<MMOp> &ops, int cfg, std::vector<int64_t> &wg,
+                 int max_groups = 0);
 // All ops of one launch share the weight format, x type and y type.
 // groups must be a positive multiple of 8 (mm_partition's result).
 hipError_t launch_mfma_multi(int32_t type, int32_t xt, int32_t yt, int cfg, const MMOp *dev_ops,

@@ -353,7 +353,8 @@ int64_t mm_tiles(int cfg, int64_t m, int64_t n) {
   return ((m + bm - 1) / bm) * ((n + bn - 1) / bn);
 }
 
-int mm_partition(const std::vector<MMOp> &ops, int cfg, std::vector<int64_t> &wg) {
+int mm_partition(const std::vector<MMOp> &ops, int cfg, std::vector<int64_t> &wg,
+                 int max_groups) {
   int64_t steps = 0, units = 0;
   for (const MMOp &o : ops) {
     steps += (o.unit_end - units) * o.nk;
@@ -361,6 +362,7 @@ int mm_partition(const std::vector<MMOp> &ops, int cfg, std::vector<int64_t> &wg
   }
   // as many workgroups as fit on the CUs at once, a multiple of 8
   int64_t groups = std::min<int64_t>((int64_t)device_cu_count() * kMMTiles[cfg][2], units);
+  if (max_groups > 0) groups = std::min<int64_t>(groups, max_groups);
   groups = std::max<int64_t>(kXcds, (groups + kXcds - 1) / kXcds * kXcds);
   // workgroup p ends at the first unit boundary at or past (p + 1) * steps / groups
   wg.assign(groups + 1, units);
