@@ -363,8 +363,11 @@ def test_grouped_mfma_stack(eb, oracle, qtype, xdtype, ms, monkeypatch):
     # split off mostly-padded last row tiles
     assert 1 <= eb.stack_launches(ops) <= 3
     first = None
-    for mode in ("1", "1", "0"):  # capture, replay, direct
+    # capture, replay, direct; then the split-off rows after the grouped launch
+    # instead of beside it on the second stream, recorded and direct
+    for mode, overlap in (("1", "1"), ("1", "1"), ("0", "1"), ("1", "0"), ("0", "0")):
         monkeypatch.setenv("EB_STACK_GRAPH", mode)
+        monkeypatch.setenv("EB_STACK_OVERLAP_TAIL", overlap)
         for _, _, y in entries:
             y.fill_(float("nan"))
         eb.qlinear_stack(ops)
@@ -373,7 +376,8 @@ def test_grouped_mfma_stack(eb, oracle, qtype, xdtype, ms, monkeypatch):
         if first is None:
             first = outs
         for a, b in zip(first, outs):
-            assert torch.equal(a, b)
+            assert torch.equal(a, b), (mode, overlap)
+    monkeypatch.delenv("EB_STACK_OVERLAP_TAIL", raising=False)
     eb.mfma_force(-1, 1)
     try:
         for (w, x), (qw, xd, y) in zip(cases, entries):
