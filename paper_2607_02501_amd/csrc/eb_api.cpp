@@ -714,8 +714,9 @@ void print_plan(const eb_qlinear_op *ops, const Plan &P) {
   for (size_t i = 0; i < P.steps.size(); ++i) {
     const Step &st = P.steps[i];
     const char *kind = st.gm ? "grouped" : st.mm ? "small-m" : st.mfma ? "mfma" : st.op >= 0 ? "single" : "gemv-multi";
-    std::fprintf(stderr, "[eb plan]  step %zu %s op %d nops %d cfg %d splits %d norms %zu", i, kind,
-                 st.op, st.nops, st.mm_cfg, st.mfma ? st.mp.splits : 0, st.norms.size());
+    std::fprintf(stderr, "[eb plan]  step %zu %s%s op %d nops %d cfg %d splits %d norms %zu", i, kind,
+                 st.side ? " (side stream)" : "", st.op, st.nops, st.mm_cfg,
+                 st.mfma ? st.mp.splits : 0, st.norms.size());
     for (const NormJob &j : st.norms) std::fprintf(stderr, " [h %p off %zu]", (const void *)j.h, j.off);
     if (st.op >= 0)
       std::fprintf(stderr, " x %p y %p pro %d epi %d", ops[st.op].x, ops[st.op].y, ops[st.op].prologue,
