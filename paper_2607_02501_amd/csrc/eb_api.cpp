@@ -193,11 +193,18 @@ size_t xhat_bytes(const eb_qlinear_op &o) {
 
 // One op on the MFMA path with a fixed plan: the prologue's row kernel writes
 // the normalised activations to xbuf, then the product reads them.
+// pre_normed: xbuf already holds them (written by the reduction of the op
+// before, see NormOut); norm_next: this op's reduction writes the next op's.
 hipError_t launch_mfma_op(const eb_qlinear_op &o, const MfmaPlan &P, void *xbuf, float *ws,
-                          hipStream_t s) {
+                          hipStream_t s, bool pre_normed = false,
+                          const NormOut *norm_next = nullptr) {
   const void *x = o.x;
   Fuse f = fuse_of(o);
-  if (o.prologue == EB_PRO_RMSNORM) {
+  if (o.prologue == EB_PRO_RMSNORM && pre_normed) {
+    x = xbuf;
+    f.pro = EB_PRO_NONE;
+    f.gamma = nullptr;
+  } else if (o.prologue == EB_PRO_RMSNORM) {
     hipError_t e = launch_rmsnorm(static_cast<const float *>(o.x), o.norm_weight, o.norm_eps, o.m,
                                   o.w.k, o.x_type, xbuf, s);
     if (e != hipSuccess) return e;
@@ -205,7 +212,8 @@ hipError_t launch_mfma_op(const eb_qlinear_op &o, const MfmaPlan &P, void *xbuf,
     f.pro = EB_PRO_NONE;
     f.gamma = nullptr;
   }
-  return launch_mfma(o.w.type, o.w.data, o.w.n, o.w.k, x, o.x_type, o.m, o.y, o.y_type, f, P, ws, s);
+  return launch_mfma(o.w.type, o.w.data, o.w.n, o.w.k, x, o.x_type, o.m, o.y, o.y_type, f, P, ws, s,
+                     norm_next);
 }
 
 eb_status launch_op(const eb_qlinear_op &o, int32_t path, hipStream_t s) {
@@ -331,6 +339,9 @@ struct Step {
   std::vector<NormJob> norms;  // prologue row kernels run before the step
   bool side = false;  // fused launch of split-off rows that runs on the side stream,
                       // beside the grouped launch before it
+  bool norm_next = false;   // single split MFMA op whose reduction also normalises
+                            // its fp32 output for the next step's prologue
+  bool pre_normed = false;  // single MFMA op whose prologue that reduction ran
 };
 
 struct Plan {
@@ -649,6 +660,23 @@ eb_status build_plan(const eb_qlinear_op *ops, int32_t n_ops, bool alloc, Plan &
     P.ws_bytes = std::max(P.ws_bytes, s.mp.ws_bytes);
     P.xbuf_bytes = std::max(P.xbuf_bytes, xhat_bytes(o));
   }
+  // In a dependent layer chain, a split op writing the fp32 stream h (after
+  // O and down: + h) is followed by an op normalising that h: the reduction,
+  // which already holds every element of h, writes the normalised rows too
+  // (one row kernel launch fewer per pair).  Both are single MFMA steps on
+  // one stream; the reduction writes xbuf after its own op's product has read
+  // it, and the next op reads it.
+  if (!env_off("EB_STACK_FUSE_NORM")) {
+    for (size_t q = 0; q + 1 < P.steps.size(); ++q) {
+      Step &a = P.steps[q], &b = P.steps[q + 1];
+      if (!a.mfma || !b.mfma || a.side || b.side || a.mp.splits <= 1 || !b.norms.empty()) continue;
+      const eb_qlinear_op &oa = ops[a.op], &ob = ops[b.op];
+      if (oa.y_type != EB_F32 || oa.epilogue == EB_EPI_GLU || ob.prologue != EB_PRO_RMSNORM) continue;
+      if (ob.x != oa.y || ob.m != oa.m || ob.w.k != oa.w.n || oa.m == 0) continue;
+      a.norm_next = true;
+      b.pre_normed = true;
+    }
+  }
   if (!alloc) return EB_OK;
   if (P.xbuf_bytes > 0) {
     if (hipMalloc((void **)&P.xbuf, P.xbuf_bytes) != hipSuccess) {
@@ -718,6 +746,8 @@ void print_plan(const eb_qlinear_op *ops, const Plan &P) {
                  st.side ? " (side stream)" : "", st.op, st.nops, st.mm_cfg,
                  st.mfma ? st.mp.splits : 0, st.norms.size());
     for (const NormJob &j : st.norms) std::fprintf(stderr, " [h %p off %zu]", (const void *)j.h, j.off);
+    if (st.pre_normed) std::fprintf(stderr, " (prologue ran in the previous reduction)");
+    if (st.norm_next) std::fprintf(stderr, " (reduction normalises for the next step)");
     if (st.op >= 0)
       std::fprintf(stderr, " x %p y %p pro %d epi %d", ops[st.op].x, ops[st.op].y, ops[st.op].prologue,
                    ops[st.op].epilogue);
@@ -760,7 +790,13 @@ eb_status run_plan(const eb_qlinear_op *ops, const Plan &P, hipStream_t s, hipSt
         return EB_ERR_HIP;
     } else if (st.mfma) {
       const eb_qlinear_op &o = ops[st.op];
-      if (launch_mfma_op(o, st.mp, P.xbuf, st.mp.splits > 1 ? P.ws : nullptr, s) != hipSuccess)
+      NormOut no{};
+      if (st.norm_next) {
+        const eb_qlinear_op &nx = ops[P.steps[i + 1].op];
+        no = NormOut{nx.norm_weight, nx.norm_eps, nx.x_type, P.xbuf};
+      }
+      if (launch_mfma_op(o, st.mp, P.xbuf, st.mp.splits > 1 ? P.ws : nullptr, s, st.pre_normed,
+                         st.norm_next ? &no : nullptr) != hipSuccess)
         return EB_ERR_HIP;
     } else if (st.op >= 0) {
       eb_status r = launch_op(ops[st.op], EB_PATH_AUTO, s);
@@ -1001,7 +1037,7 @@ int32_t eb_qlinear_stack_launches(const eb_qlinear_op *ops, int32_t n_ops) {
     launches += (int32_t)st.norms.size();
     if (st.op >= 0 && ops[st.op].m == 0) continue;
     launches += (st.mfma && st.mp.splits > 1) ? 2 : 1;
-    if (st.mfma && ops[st.op].prologue == EB_PRO_RMSNORM) ++launches;
+    if (st.mfma && ops[st.op].prologue == EB_PRO_RMSNORM && !st.pre_normed) ++launches;
   }
   return launches;
 }

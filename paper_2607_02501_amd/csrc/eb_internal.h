@@ -67,6 +67,21 @@ hipError_t launch_gemv(int32_t type, const void *wdata, int64_t n, int64_t k, co
 hipError_t launch_rmsnorm(const float *h, const float *gamma, float eps, int64_t m, int64_t k,
                           int32_t xt, void *out, hipStream_t s);
 
+// The normalisation prologue of the next projection, fused into the split-K
+// reduction of a projection whose fp32 output h is that projection's input:
+// the reduction writes h (+ the residual) as the plain reduction does, then
+// x_hat = round_xt(h * gamma * r_i) into xout, with the same bits as
+// launch_rmsnorm on that h.  One workgroup per row; n % 4 == 0.
+struct NormOut {
+  const float *gamma;
+  float eps;
+  int32_t xt;
+  void *xout;
+};
+hipError_t launch_splitk_reduce_rmsnorm(const float *ws, int splits, int64_t ws_stride, int64_t m,
+                                        int64_t n, float *y, const float *residual,
+                                        const NormOut &no, hipStream_t s);
+
 // Fused m == 1 GEMV over several independent matrices (one launch).  The
 // table lives in device memory; unit_begin (prefix sum of n * ku) ascends.
 struct M1Op {
@@ -106,10 +121,13 @@ struct MfmaPlan {
   size_t ws_bytes = 0;
 };
 MfmaPlan plan_mfma(int32_t type, int64_t m, int64_t n, int64_t k, bool allow_split);
-// ws == nullptr runs the plan's configuration unsplit.
+// ws == nullptr runs the plan's configuration unsplit.  norm_next (split runs
+// with an fp32 output and no gated product only) fuses the next projection's
+// normalisation into the reduction.
 hipError_t launch_mfma(int32_t type, const void *wdata, int64_t n, int64_t k, const void *x,
                        int32_t xt, int64_t m, void *y, int32_t yt, const Fuse &f,
-                       const MfmaPlan &plan, float *ws, hipStream_t s);
+                       const MfmaPlan &plan, float *ws, hipStream_t s,
+                       const NormOut *norm_next = nullptr);
 int mfma_tile_count();
 int mfma_cfg_bm(int cfg);        // rows of a tile configuration
 double mfma_cfg_rate(int cfg);   // its measured full-chip rate, TFLOP/s

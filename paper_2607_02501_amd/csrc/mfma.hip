@@ -678,7 +678,8 @@ hipError_t launch_gq(int cfg, const GOp *ops, const int2 *order, int64_t entries
 
 template <int QT, int XT>
 hipError_t launch_q(const void *wdata, int64_t n, int64_t k, const void *x, int64_t m, void *y,
-                    int32_t yt, const Fuse &f, const MfmaPlan &P, float *ws, hipStream_t s) {
+                    int32_t yt, const Fuse &f, const MfmaPlan &P, float *ws, hipStream_t s,
+                    const NormOut *no) {
   const int sp = ws ? P.splits : 1;
   const int kts = ws ? P.kts : (int)((k + kBK - 1) / kBK);
   const int64_t st = P.ws_stride;
@@ -695,6 +696,12 @@ hipError_t launch_q(const void *wdata, int64_t n, int64_t k, const void *x, int6
     default: e = launch_t<QT, XT, 512, 128, 4, 2>(wdata, n, k, x, m, y, yt, f, sp, kts, ws, st, s); break;
   }
   if (e != hipSuccess || sp == 1) return e;
+  if (no) {
+    if (yt != EB_F32 || f.epi == EB_EPI_GLU) return hipErrorInvalidValue;
+    return launch_splitk_reduce_rmsnorm(ws, sp, st, m, n, static_cast<float *>(y),
+                                        f.epi == EB_EPI_ADD ? static_cast<const float *>(f.r) : nullptr,
+                                        *no, s);
+  }
   const int64_t count = m * n;
   const int64_t blocks = (count + 1023) / 1024;
   splitk_reduce<<<(unsigned)blocks, 256, 0, s>>>(ws, sp, st, count, y, yt, f);
@@ -705,13 +712,13 @@ hipError_t launch_q(const void *wdata, int64_t n, int64_t k, const void *x, int6
 
 hipError_t launch_mfma(int32_t type, const void *wdata, int64_t n, int64_t k, const void *x,
                        int32_t xt, int64_t m, void *y, int32_t yt, const Fuse &f,
-                       const MfmaPlan &plan, float *ws, hipStream_t s) {
+                       const MfmaPlan &plan, float *ws, hipStream_t s, const NormOut *no) {
   if (type == EB_Q4_0) {
-    if (xt == EB_F16) return launch_q<EB_Q4_0, EB_F16>(wdata, n, k, x, m, y, yt, f, plan, ws, s);
-    return launch_q<EB_Q4_0, EB_BF16>(wdata, n, k, x, m, y, yt, f, plan, ws, s);
+    if (xt == EB_F16) return launch_q<EB_Q4_0, EB_F16>(wdata, n, k, x, m, y, yt, f, plan, ws, s, no);
+    return launch_q<EB_Q4_0, EB_BF16>(wdata, n, k, x, m, y, yt, f, plan, ws, s, no);
   }
-  if (xt == EB_F16) return launch_q<EB_Q8_0, EB_F16>(wdata, n, k, x, m, y, yt, f, plan, ws, s);
-  return launch_q<EB_Q8_0, EB_BF16>(wdata, n, k, x, m, y, yt, f, plan, ws, s);
+  if (xt == EB_F16) return launch_q<EB_Q8_0, EB_F16>(wdata, n, k, x, m, y, yt, f, plan, ws, s, no);
+  return launch_q<EB_Q8_0, EB_BF16>(wdata, n, k, x, m, y, yt, f, plan, ws, s, no);
 }
 
 hipError_t launch_mfma_grouped(int32_t type, int32_t xt, int cfg, const GOp *ops, const int2 *order,

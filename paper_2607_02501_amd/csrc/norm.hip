@@ -31,23 +31,16 @@ __device__ inline uint32_t pack2(float a, float b) {
          ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)b) << 16);
 }
 
+// The rest of a row's normalisation once every thread holds the sum of the
+// squares of its float4 columns j = t, t + 256, ... (summed in that order):
+// the 64 lanes of a wave, then the four waves in order, then the row written
+// from h.  Both row kernels below end here, so the split-K reduction with the
+// normalisation fused writes the same bits as its reduction followed by
+// rmsnorm_kernel.
 template <int XT>
-__global__ void __launch_bounds__(kThreads)
-    rmsnorm_kernel(const float *__restrict__ h, const float *__restrict__ g, float eps, int64_t k,
-                   uint32_t *__restrict__ out) {
-  __shared__ float red[kThreads / 64];
-  const int64_t row = blockIdx.x;
-  const float4 *src = reinterpret_cast<const float4 *>(h + row * k);
-  const float4 *gs = reinterpret_cast<const float4 *>(g);
-  const int64_t k4 = k / 4;
-  float ss = 0.f;
-  for (int64_t i = threadIdx.x; i < k4; i += kThreads) {
-    const float4 v = src[i];
-    ss = __builtin_fmaf(v.x, v.x, ss);
-    ss = __builtin_fmaf(v.y, v.y, ss);
-    ss = __builtin_fmaf(v.z, v.z, ss);
-    ss = __builtin_fmaf(v.w, v.w, ss);
-  }
+__device__ inline void finish_row(float ss, float *red, const float *__restrict__ h,
+                                  const float *__restrict__ g, float eps, int64_t k,
+                                  uint32_t *__restrict__ out) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) ss += __shfl_xor(ss, o);
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
@@ -56,11 +49,69 @@ __global__ void __launch_bounds__(kThreads)
 #pragma unroll
   for (int w = 0; w < kThreads / 64; ++w) tot += red[w];
   const float r = 1.0f / __builtin_sqrtf(tot / (float)k + eps);
-  uint2 *dst = reinterpret_cast<uint2 *>(out + row * (k / 2));
-  for (int64_t i = threadIdx.x; i < k4; i += kThreads) {
+  const float4 *src = reinterpret_cast<const float4 *>(h);
+  const float4 *gs = reinterpret_cast<const float4 *>(g);
+  uint2 *dst = reinterpret_cast<uint2 *>(out);
+  for (int64_t i = threadIdx.x; i < k / 4; i += kThreads) {
     const float4 v = src[i], w = gs[i];
     dst[i] = make_uint2(pack2<XT>(v.x * w.x * r, v.y * w.y * r), pack2<XT>(v.z * w.z * r, v.w * w.w * r));
   }
+}
+
+__device__ inline float sum_sq(float ss, const float4 &v) {
+  ss = __builtin_fmaf(v.x, v.x, ss);
+  ss = __builtin_fmaf(v.y, v.y, ss);
+  ss = __builtin_fmaf(v.z, v.z, ss);
+  return __builtin_fmaf(v.w, v.w, ss);
+}
+
+template <int XT>
+__global__ void __launch_bounds__(kThreads)
+    rmsnorm_kernel(const float *__restrict__ h, const float *__restrict__ g, float eps, int64_t k,
+                   uint32_t *__restrict__ out) {
+  __shared__ float red[kThreads / 64];
+  const int64_t row = blockIdx.x;
+  const float4 *src = reinterpret_cast<const float4 *>(h + row * k);
+  float ss = 0.f;
+  for (int64_t i = threadIdx.x; i < k / 4; i += kThreads) ss = sum_sq(ss, src[i]);
+  finish_row<XT>(ss, red, h + row * k, g, eps, k, out + row * (k / 2));
+}
+
+// Split-K reduction of a projection with n outputs per row whose fp32 output
+// row h is the next projection's input under a normalisation prologue: row
+// `row` of y = the partials summed in split order (+ the residual), as the
+// plain reduction computes each element, then the row is normalised into
+// `out` for the next projection.  One workgroup per row; every thread reads
+// back only the y elements it wrote itself.
+template <int XT>
+__global__ void __launch_bounds__(kThreads)
+    reduce_rmsnorm_kernel(const float *__restrict__ ws, int splits, int64_t ws_stride, int64_t n,
+                          float *y, const float *r, const float *__restrict__ g, float eps,
+                          uint32_t *__restrict__ out) {
+  __shared__ float red[kThreads / 64];
+  const int64_t row = blockIdx.x;
+  float ss = 0.f;
+  for (int64_t i = threadIdx.x; i < n / 4; i += kThreads) {
+    const int64_t o = row * n + 4 * i;
+    float4 v = *reinterpret_cast<const float4 *>(ws + o);
+    for (int p = 1; p < splits; ++p) {
+      const float4 b = *reinterpret_cast<const float4 *>(ws + p * ws_stride + o);
+      v.x += b.x;
+      v.y += b.y;
+      v.z += b.z;
+      v.w += b.w;
+    }
+    if (r) {
+      const float4 a = *reinterpret_cast<const float4 *>(r + o);
+      v.x += a.x;
+      v.y += a.y;
+      v.z += a.z;
+      v.w += a.w;
+    }
+    *reinterpret_cast<float4 *>(y + o) = v;
+    ss = sum_sq(ss, v);
+  }
+  finish_row<XT>(ss, red, y + row * n, g, eps, n, out + row * (n / 2));
 }
 
 }  // namespace
@@ -73,6 +124,21 @@ hipError_t launch_rmsnorm(const float *h, const float *gamma, float eps, int64_t
     rmsnorm_kernel<EB_F16><<<(unsigned)m, kThreads, 0, s>>>(h, gamma, eps, k, static_cast<uint32_t *>(out));
   else
     rmsnorm_kernel<EB_BF16><<<(unsigned)m, kThreads, 0, s>>>(h, gamma, eps, k, static_cast<uint32_t *>(out));
+  return hipGetLastError();
+}
+
+hipError_t launch_splitk_reduce_rmsnorm(const float *ws, int splits, int64_t ws_stride, int64_t m,
+                                        int64_t n, float *y, const float *residual,
+                                        const NormOut &no, hipStream_t s) {
+  if (m <= 0) return hipSuccess;
+  if (m > 0x7fffffff || n % 4 != 0 || ws_stride % 4 != 0 || splits < 1) return hipErrorInvalidValue;
+  uint32_t *out = static_cast<uint32_t *>(no.xout);
+  if (no.xt == EB_F16)
+    reduce_rmsnorm_kernel<EB_F16><<<(unsigned)m, kThreads, 0, s>>>(ws, splits, ws_stride, n, y, residual,
+                                                                  no.gamma, no.eps, out);
+  else
+    reduce_rmsnorm_kernel<EB_BF16><<<(unsigned)m, kThreads, 0, s>>>(ws, splits, ws_stride, n, y, residual,
+                                                                   no.gamma, no.eps, out);
   return hipGetLastError();
 }
 

@@ -233,6 +233,37 @@ def test_fused_stack_counts_prologue_launches(eb):
         assert launches(two) == expect, m
 
 
+def test_reduction_runs_next_prologue(eb, monkeypatch):
+    """In a dependent layer chain the split-K reduction that writes the fp32
+    stream h (O and down, + h) also normalises it for the next projection, so
+    those prologues cost no row-kernel launch; EB_STACK_FUSE_NORM=0 keeps them."""
+    d, f, m = 1024, 4096, 50   # the action-expert layer shape
+    H, A, Q, GU = 0x20000000, 0x21000000, 0x22000000, 0x23000000
+    ops, base = [], 0x10000000
+    for _ in range(2):
+        for n, k, x, y, pro, epi, res, yt in ((3 * d, d, H, Q, 1, 0, None, eb.EB_BF16),
+                                              (d, d, A, H, 0, 1, H, eb.EB_F32),
+                                              (2 * f, d, H, GU, 1, 2, None, eb.EB_BF16),
+                                              (d, f, GU, H, 0, 1, H, eb.EB_F32)):
+            w = eb.eb_qweights(eb.EB_Q8_0, 0, n, k, base)
+            base += (eb.lib.eb_qweights_bytes(eb.EB_Q8_0, n, k) + 4095) // 4096 * 4096
+            ops.append(eb.eb_qlinear_op(w, x, y, m, eb.EB_BF16, yt, pro, epi, G if pro else None,
+                                        res, 1e-5, 0))
+    arr = (eb.eb_qlinear_op * len(ops))(*ops)
+    # 8 projections, each split along k (product + reduction), and 4 prologues
+    monkeypatch.setenv("EB_STACK_FUSE_NORM", "0")
+    assert eb.lib.eb_qlinear_stack_launches(arr, len(ops)) == 16 + 4
+    # every prologue but the first follows the reduction of O or down
+    monkeypatch.delenv("EB_STACK_FUSE_NORM")
+    assert eb.lib.eb_qlinear_stack_launches(arr, len(ops)) == 16 + 1
+    # a 16-bit stream (no fp32 h to reduce into) keeps the row kernels
+    ops16 = [eb.eb_qlinear_op(o.w, o.x, o.y, o.m, o.x_type,
+                              eb.EB_BF16 if o.epilogue == 1 else o.y_type, o.prologue, o.epilogue,
+                              o.norm_weight, o.residual, o.norm_eps, 0) for o in ops]
+    arr16 = (eb.eb_qlinear_op * len(ops16))(*ops16)
+    assert eb.lib.eb_qlinear_stack_launches(arr16, len(ops16)) == 16 + 4
+
+
 def test_qlinear_m0_is_noop(eb):
     w = _w(eb)
     assert eb.lib.eb_qlinear(ctypes.byref(w), None, eb.EB_F16, 0, None, eb.EB_F32, None) == 0

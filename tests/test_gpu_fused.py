@@ -205,14 +205,19 @@ def _chain_reference(orc, L, qtype, xdtype, h0):
     return blocks, (qkv_ref, s_qkv), (h1_ref, s_h1)
 
 
-@pytest.mark.parametrize("qtype,xdtype,m", [("q4_0", torch.float16, 1), ("q8_0", torch.bfloat16, 50),
-                                            ("q4_0", torch.bfloat16, 100), ("q8_0", torch.bfloat16, 300)])
-def test_decoder_layer_chain(eb, oracle, qtype, xdtype, m, monkeypatch):
+@pytest.mark.parametrize("qtype,xdtype,m,d,f", [("q4_0", torch.float16, 1, 512, 704),
+                                                ("q8_0", torch.bfloat16, 50, 512, 704),
+                                                ("q4_0", torch.bfloat16, 100, 512, 704),
+                                                ("q8_0", torch.bfloat16, 300, 512, 704),
+                                                ("q8_0", torch.bfloat16, 50, 1024, 4096),
+                                                ("q4_0", torch.float16, 50, 1024, 4096)])
+def test_decoder_layer_chain(eb, oracle, qtype, xdtype, m, d, f, monkeypatch):
     """The four projections of a layer as one stack: results equal the ops run
-    one by one through eb_qlinear_fused, bit for bit, and each step is within
-    the oracle bound given its (GPU) inputs."""
+    one by one through eb_qlinear_fused, bit for bit (with and without the
+    gate/up normalisation fused into the split O projection's reduction, which
+    the d = 1024 layer of the action expert gets), and each step is within the
+    oracle bound given its (GPU) inputs."""
     monkeypatch.delenv("EB_STACK_FUSE", raising=False)
-    d, f = 512, 704
     L = _layer_chain(eb, 1400 + m, qtype, xdtype, m, d, f)
     h0 = L["h"].clone()
     # reference run: the same ops one at a time
@@ -228,15 +233,22 @@ def test_decoder_layer_chain(eb, oracle, qtype, xdtype, m, monkeypatch):
                      norm_weight=L["g2"], eps=1e-5, epilogue="glu", out=ref_act)
     eb.qlinear_fused(qws[3], ref_act, epilogue="add", residual=ref_h, out=ref_h)
     # the stack, in every mode
-    for mode in ("1", "1", "0"):
-        monkeypatch.setenv("EB_STACK_GRAPH", mode)
-        L["h"].copy_(h0)
-        eb.qlinear_stack(L["ops"])
-        torch.cuda.synchronize()
-        assert torch.equal(L["qkv"], ref_qkv), mode
-        assert torch.equal(L["act"], ref_act), mode
-        assert torch.equal(L["h"], ref_h), mode
+    counts = {}
+    for fuse_norm in ("1", "0"):
+        monkeypatch.setenv("EB_STACK_FUSE_NORM", fuse_norm)
+        eb.stack_cache_clear()
+        counts[fuse_norm] = eb.stack_launches(L["ops"])
+        for mode in ("1", "1", "0"):
+            monkeypatch.setenv("EB_STACK_GRAPH", mode)
+            L["h"].copy_(h0)
+            eb.qlinear_stack(L["ops"])
+            torch.cuda.synchronize()
+            assert torch.equal(L["qkv"], ref_qkv), (fuse_norm, mode)
+            assert torch.equal(L["act"], ref_act), (fuse_norm, mode)
+            assert torch.equal(L["h"], ref_h), (fuse_norm, mode)
     eb.stack_cache_clear()
+    if d == 1024:
+        assert counts["1"] == counts["0"] - 1, counts
     # each step against the oracle
     hn = h0.cpu().numpy()
     blocks, (qkv_ref, s_qkv), (h1_ref, s_h1) = _chain_reference(oracle, L, qtype, xdtype, hn)
