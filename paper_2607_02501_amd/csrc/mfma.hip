@@ -464,6 +464,8 @@ __global__ void __launch_bounds__(256)
   const int e = (int)(count - i < 4 ? count - i : 4);
   if (e == 4) {
     float4 v = *reinterpret_cast<const float4 *>(ws + i);
+    // unrolled so several partial loads are in flight; the sum stays in split order
+#pragma unroll 4
     for (int p = 1; p < splits; ++p) {
       const float4 b = *reinterpret_cast<const float4 *>(ws + p * ws_stride + i);
       v.x += b.x;

@@ -94,6 +94,8 @@ __global__ void __launch_bounds__(kThreads)
   for (int64_t i = threadIdx.x; i < n / 4; i += kThreads) {
     const int64_t o = row * n + 4 * i;
     float4 v = *reinterpret_cast<const float4 *>(ws + o);
+    // unrolled so several partial loads are in flight; the sum stays in split order
+#pragma unroll 4
     for (int p = 1; p < splits; ++p) {
       const float4 b = *reinterpret_cast<const float4 *>(ws + p * ws_stride + o);
       v.x += b.x;
