@@ -249,6 +249,12 @@ int32_t eb_qlinear_auto_path(int32_t type, int32_t x_type, int64_t m, int64_t n,
  *   graph.  EB_STACK_FUSE=0 disables fusion, EB_STACK_GROUP=0 the grouped
  *   launch, EB_STACK_SPLIT_TAIL=0 its tail split, EB_STACK_OVERLAP_TAIL=0 the
  *   second stream (the tail launch then follows the grouped one).
+ *   Dependent chains: when an op on the MFMA path is split along k, writes
+ *   fp32 output without the gated product, and the next op normalises that
+ *   output (EB_PRO_RMSNORM with x == this y, same m, k == this n), the
+ *   split's reduction also writes the next op's normalised activations, with
+ *   the same bits as its own row kernel; EB_STACK_FUSE_NORM=0 keeps the row
+ *   kernel.
  *   Graph replay: the first call with a given op list (same pointers, sizes,
  *   types) builds a plan, records it into a HIP graph on a library-owned
  *   stream and caches both; later calls replay the graph with one launch.
