@@ -203,8 +203,18 @@ eb_status eb_qweights_from_canonical(int32_t type, const void *src, int64_t n, i
  * calls made on S.  x: device [m][k] of x_type (EB_F16 or EB_BF16); y: device
  * [m][n] of y_type (EB_F32, EB_BF16 or EB_F16, 16-bit outputs rounded to
  * nearest even).
- * No bias.  Accuracy: |y - y_exact| <= 2e-3 * sum_k |x||w_hat| per output
- * (plus the output rounding when y_type is 16-bit).
+ * No bias.  Accuracy, with B = sum_k |x||w_hat| per output (plus the output
+ * rounding when y_type is 16-bit):
+ *   - GEMV path (m <= 8), any x_type: |y - y_exact| <= 2e-3 B;
+ *   - MFMA path, EB_BF16 x, m <= 128: w_hat enters the matrix cores as a pair
+ *     of bfloat16 values (hi + lo, within 2^-16 of w_hat): <= 2e-3 B;
+ *   - MFMA path, EB_BF16 x, m > 128 (matrix-core bound): w_hat is rounded once
+ *     to bfloat16 (8 significant bits): <= (2e-3 + 2^-8) B;
+ *   - MFMA path, EB_F16 x: w_hat is rounded once to binary16 (11 significant
+ *     bits, subnormal below 2^-14): <= 2e-3 B + 2^-25 sum_k |x|; requires
+ *     |w_hat| <= 65504, i.e. max |w| <= 65504 in every block.
+ *   (paper section 4, Table 3: the 8-/4-bit configurations are judged by the
+ *   outputs they give; these bounds are this library's contract for them.)
  * EB_ERR_INVALID: w or its data NULL, bad type/sizes, an unknown x_type or
  * y_type, x/y NULL with m > 0, y overlapping x or the weights.
  * EB_ERR_ALIGN: x or y not 16-byte aligned, w->data not 256-byte aligned.

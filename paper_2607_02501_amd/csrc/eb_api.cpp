@@ -226,10 +226,10 @@ eb_status launch_op(const eb_qlinear_op &o, int32_t path, hipStream_t s) {
     // the stream's workspace holds the normalised activations, then any
     // split-K partial sums
     const size_t xb = xhat_bytes(o);
-    MfmaPlan P = plan_mfma(o.w.type, o.m, o.w.n, o.w.k, true);
+    MfmaPlan P = plan_mfma(o.w.type, o.x_type, o.m, o.w.n, o.w.k, true);
     uint8_t *ws = nullptr;
     if (P.splits > 1) ws = stream_workspace(s, xb + P.ws_bytes);
-    if (P.splits > 1 && !ws) P = plan_mfma(o.w.type, o.m, o.w.n, o.w.k, false);
+    if (P.splits > 1 && !ws) P = plan_mfma(o.w.type, o.x_type, o.m, o.w.n, o.w.k, false);
     if (!ws && xb) ws = stream_workspace(s, xb);
     if (xb && !ws) return EB_ERR_UNSUPPORTED;
     e = launch_mfma_op(o, P, ws, P.splits > 1 ? reinterpret_cast<float *>(ws + xb) : nullptr, s);
@@ -656,7 +656,7 @@ eb_status build_plan(const eb_qlinear_op *ops, int32_t n_ops, bool alloc, Plan &
     const eb_qlinear_op &o = ops[s.op];
     if (o.m == 0 || pick_path(o.w.type, o.x_type, o.m, o.w.n, o.w.k) != EB_PATH_MFMA) continue;
     s.mfma = true;
-    s.mp = plan_mfma(o.w.type, o.m, o.w.n, o.w.k, true);
+    s.mp = plan_mfma(o.w.type, o.x_type, o.m, o.w.n, o.w.k, true);
     P.ws_bytes = std::max(P.ws_bytes, s.mp.ws_bytes);
     P.xbuf_bytes = std::max(P.xbuf_bytes, xhat_bytes(o));
   }

@@ -115,12 +115,13 @@ hipError_t launch_gemv_m1_multi(int32_t type, int32_t xt, int ns, const M1Op *de
 // (partial sums, summed in order by a second kernel).
 struct MfmaPlan {
   int cfg = 0;
+  bool hl = false;        // bfloat16 activations at m <= 128: hi/lo weight tiles
   int splits = 1;
   int kts = 0;            // K-tiles of 64 per split
   int64_t ws_stride = 0;  // floats between the partial outputs of two splits
   size_t ws_bytes = 0;
 };
-MfmaPlan plan_mfma(int32_t type, int64_t m, int64_t n, int64_t k, bool allow_split);
+MfmaPlan plan_mfma(int32_t type, int32_t xt, int64_t m, int64_t n, int64_t k, bool allow_split);
 // ws == nullptr runs the plan's configuration unsplit.  norm_next (split runs
 // with an fp32 output and no gated product only) fuses the next projection's
 // normalisation into the reduction.
@@ -128,6 +129,16 @@ hipError_t launch_mfma(int32_t type, const void *wdata, int64_t n, int64_t k, co
                        int32_t xt, int64_t m, void *y, int32_t yt, const Fuse &f,
                        const MfmaPlan &plan, float *ws, hipStream_t s,
                        const NormOut *norm_next = nullptr);
+// One launch of the tile kernel for tile configuration `cfg` (hi/lo weight
+// tiles when hl) over `sp` splits of k of kts K-tiles each (the reduction of
+// the splits is not part of it).  Defined in mfma_tile.h and instantiated for
+// each weight format and activation type in its own translation unit.
+template <int QT, int XT>
+hipError_t mfma_tile_launch(int cfg, bool hl, const void *wdata, int64_t n, int64_t k, const void *x,
+                            int64_t m, void *y, int32_t yt, const Fuse &f, int sp, int kts,
+                            float *ws, int64_t st, hipStream_t s);
+// Whether a workgroup's byte spans of a bm x bn tile fit 32-bit buffer offsets.
+bool mfma_fits_offsets(int32_t type, int64_t n, int64_t k, int bm, int bn);
 int mfma_tile_count();
 int mfma_cfg_bm(int cfg);        // rows of a tile configuration
 double mfma_cfg_rate(int cfg);   // its measured full-chip rate, TFLOP/s
@@ -148,6 +159,9 @@ struct GOp {
 int plan_grouped(int32_t type, const std::vector<GOp> &ops, std::vector<int2> &order);
 hipError_t launch_mfma_grouped(int32_t type, int32_t xt, int cfg, const GOp *ops, const int2 *order,
                                 int64_t entries, hipStream_t s);
+template <int QT, int XT>
+hipError_t mfma_tile_launch_grouped(int cfg, const GOp *ops, const int2 *order, int64_t entries,
+                                    hipStream_t s);
 
 // Fused MFMA launch over several independent ops of a stack: one persistent
 // launch whose workgroups each run a contiguous range of output tiles

@@ -73,6 +73,25 @@ __device__ inline uint32_t deq_pair(uint32_t h2, float d, float c) {
   return pack2<XT>(__builtin_fmaf((float)a, d, c), __builtin_fmaf((float)b, d, c));
 }
 
+// bfloat16 activations: w_hat = (c - z) d is exact in fp32 but needs up to 19
+// significant bits, while bfloat16 keeps 8 (one rounding costs up to 2^-8 of
+// |w_hat|, which a one-hot x exposes whole).  A hi/lo pair keeps 16:
+// hi = bf16_RNE(w), lo = bf16_RNE(w - hi) (w - hi is exact in fp32), so
+// |w - hi - lo| <= 2^-16 |w| and x hi + x lo, each product exact in fp32 and
+// accumulated by the matrix cores, carries w_hat to within 2^-16.
+__device__ inline void split2_bf16(float a, float b, uint32_t &hi, uint32_t &lo) {
+  hi = pack2<EB_BF16>(a, b);
+  const float ha = __uint_as_float(hi << 16), hb = __uint_as_float(hi & 0xffff0000u);
+  lo = pack2<EB_BF16>(a - ha, b - hb);
+}
+
+// two codes (binary16 1024 + c halves of h2) -> hi and lo bfloat16 pairs of (c - z) d
+__device__ inline void deq_pair_hl(uint32_t h2, float d, float c, uint32_t &hi, uint32_t &lo) {
+  const _Float16 a = __builtin_bit_cast(_Float16, (uint16_t)(h2 & 0xffffu));
+  const _Float16 b = __builtin_bit_cast(_Float16, (uint16_t)(h2 >> 16));
+  split2_bf16(__builtin_fmaf((float)a, d, c), __builtin_fmaf((float)b, d, c), hi, lo);
+}
+
 template <int QT, int XT>
 __device__ inline void dequant_chunk(const uint4 q, float d, uint4 (&v)[Deq<QT>::kVecs]) {
   const uint32_t w[4] = {q.x, q.y, q.z, q.w};
@@ -104,6 +123,45 @@ __device__ inline void dequant_chunk(const uint4 q, float d, uint4 (&v)[Deq<QT>:
     v[1] = make_uint4(lo[4], lo[5], lo[6], lo[7]);
     v[2] = make_uint4(hi[0], hi[1], hi[2], hi[3]);
     v[3] = make_uint4(hi[4], hi[5], hi[6], hi[7]);
+  }
+}
+
+// dequant_chunk for bfloat16 activations, as hi/lo pairs (split2_bf16):
+// vh holds the bfloat16 roundings, vl the roundings of the remainders.
+template <int QT>
+__device__ inline void dequant_chunk_hl(const uint4 q, float d, uint4 (&vh)[Deq<QT>::kVecs],
+                                        uint4 (&vl)[Deq<QT>::kVecs]) {
+  const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+  constexpr uint32_t kSelLo = 0x04010400u, kSelHi = 0x04030402u;
+  if constexpr (QT == EB_Q8_0) {
+    const float c = -1152.0f * d;
+    uint32_t h[8], l[8];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t u = w[j] ^ 0x80808080u;
+      deq_pair_hl(under_1024(u, kSelLo), d, c, h[2 * j], l[2 * j]);
+      deq_pair_hl(under_1024(u, kSelHi), d, c, h[2 * j + 1], l[2 * j + 1]);
+    }
+    vh[0] = make_uint4(h[0], h[1], h[2], h[3]);
+    vh[1] = make_uint4(h[4], h[5], h[6], h[7]);
+    vl[0] = make_uint4(l[0], l[1], l[2], l[3]);
+    vl[1] = make_uint4(l[4], l[5], l[6], l[7]);
+  } else {
+    const float c = -1032.0f * d;
+    uint32_t h[16], l[16];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t lo4 = w[j] & 0x0f0f0f0fu, hi4 = (w[j] >> 4) & 0x0f0f0f0fu;
+      deq_pair_hl(under_1024(lo4, kSelLo), d, c, h[2 * j], l[2 * j]);
+      deq_pair_hl(under_1024(lo4, kSelHi), d, c, h[2 * j + 1], l[2 * j + 1]);
+      deq_pair_hl(under_1024(hi4, kSelLo), d, c, h[8 + 2 * j], l[8 + 2 * j]);
+      deq_pair_hl(under_1024(hi4, kSelHi), d, c, h[8 + 2 * j + 1], l[8 + 2 * j + 1]);
+    }
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      vh[v] = make_uint4(h[4 * v], h[4 * v + 1], h[4 * v + 2], h[4 * v + 3]);
+      vl[v] = make_uint4(l[4 * v], l[4 * v + 1], l[4 * v + 2], l[4 * v + 3]);
+    }
   }
 }
 

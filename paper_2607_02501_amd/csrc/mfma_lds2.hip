@@ -58,8 +58,9 @@ __global__ void __launch_bounds__(WAVES * 64)
   constexpr int YSZ = (YT == EB_F32) ? 4 : 2;
   static_assert(NX * 1024 * WAVES == XBYTES && NW * 1024 * WAVES == WBYTES, "copies must tile");
   static_assert(NS * 16 * T == SBYTES && NW + NS + NST <= 63, "scale loads / wait count range");
-  // vector ALU instructions of one block's dequantization (dequant_b)
-  constexpr int kDeqValu = (QT == EB_Q8_0) ? 72 : 80;
+  // bfloat16 activations take w_hat as hi/lo bfloat16 pairs (two MFMAs per
+  // product, w_hat carried to 2^-16; binary16 holds w_hat to 2^-11 in one)
+  constexpr bool HL = (XT == EB_BF16);
 
   __shared__ __attribute__((aligned(1024))) uint8_t sX0[XBYTES];
   __shared__ __attribute__((aligned(1024))) uint8_t sX1[XBYTES];
@@ -410,8 +411,13 @@ __global__ void __launch_bounds__(WAVES * 64)
         dq[q][j] = (uint16_t)(d2 >> (16 * wh));
       }
     uint4 bq[2][FN][4];
+    uint4 bl[2][FN][HL ? 4 : 1];  // bfloat16: the low parts of the hi/lo pairs
     auto deq = [&](int q, int j) __attribute__((always_inline)) {
-      dequant_b<QT, XT>(cq[q][j], (float)__builtin_bit_cast(_Float16, dq[q][j]), bq[q][j]);
+      const float d = (float)__builtin_bit_cast(_Float16, dq[q][j]);
+      if constexpr (HL)
+        dequant_b_hl<QT>(cq[q][j], d, bq[q][j], bl[q][j]);
+      else
+        dequant_b<QT, XT>(cq[q][j], d, bq[q][j]);
     };
     auto mm = [&](int q, int s) __attribute__((always_inline)) {
       uint4 af[FM];
@@ -422,6 +428,12 @@ __global__ void __launch_bounds__(WAVES * 64)
       for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j) acc[i][j] = mfma32<XT>(bq[q][j][s], af[i], acc[i][j]);
+      if constexpr (HL) {
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+          for (int j = 0; j < FN; ++j) acc[i][j] = mfma32<XT>(bl[q][j][HL ? s : 0], af[i], acc[i][j]);
+      }
     };
     // copy c of this step: x copies first, then codes, then scale loads (the
     // order the barrier's wait counts assume)

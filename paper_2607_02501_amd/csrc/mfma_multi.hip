@@ -52,6 +52,9 @@ __global__ void __launch_bounds__(256)
   constexpr int NWAIT = 2 * NX + 3 * NW;  // at a barrier: all but x tile t+1 may be in flight
   static_assert(ADMA >= 1 && ADMA * 8 * WAVES == BM, "x tile must split into 8-row copies");
   static_assert(NWAIT <= 63, "vmcnt range");
+  // bfloat16 activations take w_hat as hi/lo bfloat16 pairs (two MFMAs per
+  // product, w_hat carried to 2^-16; binary16 holds w_hat to 2^-11 in one)
+  constexpr bool HL = (XT == EB_BF16);
 
   __shared__ __attribute__((aligned(1024))) uint8_t sA0[ABYTES];
   __shared__ __attribute__((aligned(1024))) uint8_t sA1[ABYTES];
@@ -281,9 +284,15 @@ __global__ void __launch_bounds__(256)
   auto step = [&](const uint8_t *A, uint8_t *Anew, Raw &S) __attribute__((always_inline)) {
     x_issue(Anew, X);
     uint4 bq[FN][4];
+    uint4 bl[FN][HL ? 4 : 1];  // bfloat16: the low parts of the hi/lo pairs
 #pragma unroll
-    for (int j = 0; j < FN; ++j)
-      dequant_b<QT, XT>(S.q[j], (float)__builtin_bit_cast(_Float16, S.d[j]), bq[j]);
+    for (int j = 0; j < FN; ++j) {
+      const float d = (float)__builtin_bit_cast(_Float16, S.d[j]);
+      if constexpr (HL)
+        dequant_b_hl<QT>(S.q[j], d, bq[j], bl[j]);
+      else
+        dequant_b<QT, XT>(S.q[j], d, bq[j]);
+    }
     w_issue(S, Wc);
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
@@ -295,6 +304,12 @@ __global__ void __launch_bounds__(256)
       for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j) acc[i][j] = mfma32<XT>(af[i], bq[j][s], acc[i][j]);
+      if constexpr (HL) {
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+          for (int j = 0; j < FN; ++j) acc[i][j] = mfma32<XT>(af[i], bl[j][HL ? s : 0], acc[i][j]);
+      }
     }
     if (C.valid && C.kt == C.nk - 1) {
       epilogue(C);

@@ -94,6 +94,45 @@ __device__ inline void dequant_b(const uint4 (&q)[QT == EB_Q8_0 ? 2 : 1], float 
   }
 }
 
+// dequant_b for bfloat16 activations as hi/lo pairs (split2_bf16 in
+// mfma_common.h): bh[s] the bfloat16 roundings, bl[s] those of the remainders.
+template <int QT>
+__device__ inline void dequant_b_hl(const uint4 (&q)[QT == EB_Q8_0 ? 2 : 1], float d, uint4 (&bh)[4],
+                                    uint4 (&bl)[4]) {
+  constexpr uint32_t kSelLo = 0x04010400u, kSelHi = 0x04030402u;
+  uint32_t h[16], l[16];
+  if constexpr (QT == EB_Q8_0) {
+    const float c = -1152.0f * d;
+    const uint32_t w[8] = {q[0].x, q[0].y, q[0].z, q[0].w, q[1].x, q[1].y, q[1].z, q[1].w};
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const uint32_t u0 = w[2 * s] ^ 0x80808080u, u1 = w[2 * s + 1] ^ 0x80808080u;
+      deq_pair_hl(under_1024(u0, kSelLo), d, c, h[4 * s], l[4 * s]);
+      deq_pair_hl(under_1024(u0, kSelHi), d, c, h[4 * s + 1], l[4 * s + 1]);
+      deq_pair_hl(under_1024(u1, kSelLo), d, c, h[4 * s + 2], l[4 * s + 2]);
+      deq_pair_hl(under_1024(u1, kSelHi), d, c, h[4 * s + 3], l[4 * s + 3]);
+    }
+  } else {
+    const float c = -1032.0f * d;
+    const uint32_t w[4] = {q[0].x, q[0].y, q[0].z, q[0].w};
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const uint32_t sh = s < 2 ? 0 : 4;
+      const uint32_t l0 = (w[2 * (s & 1)] >> sh) & 0x0f0f0f0fu;
+      const uint32_t l1 = (w[2 * (s & 1) + 1] >> sh) & 0x0f0f0f0fu;
+      deq_pair_hl(under_1024(l0, kSelLo), d, c, h[4 * s], l[4 * s]);
+      deq_pair_hl(under_1024(l0, kSelHi), d, c, h[4 * s + 1], l[4 * s + 1]);
+      deq_pair_hl(under_1024(l1, kSelLo), d, c, h[4 * s + 2], l[4 * s + 2]);
+      deq_pair_hl(under_1024(l1, kSelHi), d, c, h[4 * s + 3], l[4 * s + 3]);
+    }
+  }
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    bh[s] = make_uint4(h[4 * s], h[4 * s + 1], h[4 * s + 2], h[4 * s + 3]);
+    bl[s] = make_uint4(l[4 * s], l[4 * s + 1], l[4 * s + 2], l[4 * s + 3]);
+  }
+}
+
 }  // namespace
 }  // namespace eb
 

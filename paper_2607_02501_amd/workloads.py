@@ -106,3 +106,43 @@ def bits16(t: torch.Tensor):
     """Raw 16-bit words of an fp16/bf16 tensor as a numpy uint16 array (host copy)."""
     assert t.dtype in (torch.float16, torch.bfloat16)
     return t.detach().cpu().contiguous().view(torch.int16).numpy().view("uint16")
+
+
+# ---------------------------------------------------------------------------
+# Activation structures beyond N(0, 1) rows, for accuracy checks of every
+# kernel path: what a backbone's activations can look like besides dense
+# Gaussian rows.  Only random draws and index placement, no arithmetic of the
+# method.
+# ---------------------------------------------------------------------------
+
+def onehot_rows(m: int, k: int, seed: int, device="cpu") -> torch.Tensor:
+    """fp32 [m, k]: row i has one N(0, 1) entry at a random column, zeros elsewhere."""
+    g = _gen("cpu", seed)
+    cols = torch.randint(0, k, (m,), generator=g)
+    vals = torch.randn(m, generator=g)
+    x = torch.zeros((m, k), dtype=torch.float32)
+    x[torch.arange(m), cols] = vals
+    return x.to(device)
+
+
+def sparse_rows(m: int, k: int, seed: int, nnz=(4, 8), device="cpu") -> torch.Tensor:
+    """fp32 [m, k]: row i has between nnz[0] and nnz[1] N(0, 1) entries at
+    distinct random columns, zeros elsewhere."""
+    g = _gen("cpu", seed)
+    x = torch.zeros((m, k), dtype=torch.float32)
+    for i in range(m):
+        c = int(torch.randint(nnz[0], nnz[1] + 1, (1,), generator=g))
+        cols = torch.randperm(k, generator=g)[:c]
+        x[i, cols] = torch.randn(c, generator=g)
+    return x.to(device)
+
+
+def outlier_rows(m: int, k: int, seed: int, channels: int = 4, scale: float = 1000.0,
+                 device="cpu") -> torch.Tensor:
+    """fp32 [m, k] ~ N(0, 1) with `channels` random columns (the same in every
+    row) multiplied by `scale`: the outlier feature channels of a backbone."""
+    g = _gen("cpu", seed)
+    x = torch.randn((m, k), generator=g)
+    cols = torch.randperm(k, generator=g)[:channels]
+    x[:, cols] *= scale
+    return x.to(device)

@@ -358,6 +358,34 @@ def test_qlinear_onehot_reads_out_weights(oracle):
         assert np.array_equal(y, what.T)
 
 
+@pytest.mark.parametrize("qtype", [O.Q8_0, O.Q4_0])
+def test_qlinear_constant_blocks_closed_form(oracle, qtype):
+    """Blocks holding one value c each: every Q8_0 code is 127 sign(c) with
+    d16 = binary16(|c| / 127), every Q4_0 code -8 with d16 = binary16(c / -8)
+    (the extreme element maps to -8), so y = sum_b coef_b * sum_{j in b} x_j
+    with coef_b = 127 sign(c) d16 or -8 d16 (closed form; the binary16
+    roundings come from numpy)."""
+    rng = np.random.default_rng(29)
+    n, k = 6, 256
+    nb = k // 32
+    c = (rng.uniform(0.005, 0.08, (n, nb)) * rng.choice([-1.0, 1.0], (n, nb))).astype(np.float32)
+    w = np.repeat(c, 32, axis=1)
+    q = oracle.quantize(qtype, w)
+    if qtype == O.Q8_0:
+        d16 = (np.abs(c) / np.float32(127)).astype(np.float16).astype(np.float64)
+        coef = 127.0 * np.sign(c) * d16
+    else:
+        d16 = (c / np.float32(-8)).astype(np.float16).astype(np.float64)
+        coef = -8.0 * d16
+    x = rng.standard_normal((5, k)).astype(np.float16)
+    xs = x.astype(np.float64).reshape(5, nb, 32).sum(axis=2)
+    y, bound = oracle.qlinear(qtype, q, n, k, x.view(np.uint16), O.X_F16)
+    ref = xs @ coef.T
+    assert np.allclose(y, ref, rtol=0, atol=1e-12 * np.abs(bound).max())
+    assert np.allclose(bound, np.abs(x.astype(np.float64)).reshape(5, nb, 32).sum(axis=2) @ np.abs(coef).T,
+                       rtol=1e-13, atol=0)
+
+
 def test_oracle_rejects_bad_arguments(oracle):
     with pytest.raises(ValueError):
         oracle.quantize(O.Q8_0, np.zeros((2, 33), np.float32))
