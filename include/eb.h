@@ -38,10 +38,14 @@
  *
  * Conventions for every entry point:
  *   - All pointers are DEVICE pointers unless stated otherwise; the caller owns
- *     every buffer (weights, activations, outputs).  The library never
- *     synchronises the stream.  It allocates device memory only for cached
- *     stack plans (eb_qlinear_stack) and for per-stream workspaces of direct
- *     calls (split-K partial sums, normalised activations; below).
+ *     every buffer (weights, activations, outputs, and the workspaces that hold
+ *     split-K partial sums, normalised activations and stack-plan tables:
+ *     eb_qlinear_workspace_bytes, eb_qlinear_stack_workspace_bytes).  The
+ *     library allocates no device memory and never synchronises the stream.
+ *     Its cached state is the stack-plan cache of eb_qlinear_stack (host
+ *     plans, their HIP graphs, one capture stream and one side stream per
+ *     device, two events per plan that forks a side launch) and the compute
+ *     unit count per device.
  *   - Work is enqueued on `stream` (0 = the null stream); EB_OK means the work
  *     was enqueued, not that it finished.
  *   - Arguments are validated on the host before anything is launched; on any
@@ -118,10 +122,9 @@ typedef struct {
  *   (1/k) sum_j h[i][j]^2), rounded to nearest even in x_type, g = norm_weight.
  *   On the GEMV path every workgroup normalises while it stages x (no extra
  *   launch); on the MFMA path a row kernel writes x_hat first (one more launch)
- *   into library-owned memory: the stream's workspace for direct calls (at
- *   most 64 MiB together with split-K partial sums; during a capture the
- *   workspace is not grown and a call needing more returns
- *   EB_ERR_UNSUPPORTED), or the stack plan's own buffer.
+ *   into the caller's workspace (m * k * 2 bytes, rounded up to 256, at its
+ *   start); without a workspace that large such a call returns
+ *   EB_ERR_UNSUPPORTED.
  * Epilogue EB_EPI_ADD: y = x_hat . w_hat^T + r, r = residual[m][n] of y_type;
  *   residual may be y itself (in-place update of the residual stream) but
  *   must not otherwise overlap y.
@@ -190,19 +193,10 @@ eb_status eb_qweights_from_canonical(int32_t type, const void *src, int64_t n, i
                                      void *out, hipStream_t stream);
 
 /* y[m][n] = x[m][k] . w_hat[n][k]^T with fp32 accumulation, on the path chosen
- * automatically.
- * On the MFMA path, a problem with too few output tiles to fill the GPU (few
- * rows and columns, long k) may be split along k: each split writes fp32
- * partial sums to a workspace and a second kernel adds them in a fixed order,
- * so results stay deterministic.  Direct calls use a workspace owned by the
- * library per (device, stream), at most 64 MiB per call, grown on demand and
- * never freed before process exit (a graph captured from the stream may refer
- * to it).  While the stream is being captured nothing is allocated: if the
- * stream's workspace is too small the call runs unsplit.  A graph captured
- * from stream S uses S's workspace: do not replay it concurrently with other
- * calls made on S.  x: device [m][k] of x_type (EB_F16 or EB_BF16); y: device
- * [m][n] of y_type (EB_F32, EB_BF16 or EB_F16, 16-bit outputs rounded to
- * nearest even).
+ * automatically, with no workspace: the MFMA path then runs unsplit (see
+ * eb_qlinear_fused_ws for the split of k a workspace allows).
+ * x: device [m][k] of x_type (EB_F16 or EB_BF16); y: device [m][n] of y_type
+ * (EB_F32, EB_BF16 or EB_F16, 16-bit outputs rounded to nearest even).
  * No bias.  Accuracy, with B = sum_k |x||w_hat| per output (plus the output
  * rounding when y_type is 16-bit):
  *   - GEMV path (m <= 8), any x_type: |y - y_exact| <= 2e-3 B;
@@ -223,13 +217,36 @@ eb_status eb_qlinear(const eb_qweights *w, const void *x, int32_t x_type, int64_
                      int32_t y_type, hipStream_t stream);
 
 /* One projection with its fused steps (eb_qlinear_op: prologue, epilogue),
- * on `path` (EB_PATH_*; AUTO picks as eb_qlinear does for the op's m, n, k).
+ * on `path` (EB_PATH_*; AUTO picks as eb_qlinear does for the op's m, n, k),
+ * with no workspace (as eb_qlinear_fused_ws with a null workspace).
  * Errors as eb_qlinear, and EB_ERR_INVALID for an unknown prologue or
  * epilogue, a missing norm_weight or residual, a negative or non-finite eps,
  * an odd n with EB_EPI_GLU, reserved != 0, or a residual overlapping y
  * without being y; EB_ERR_ALIGN for norm_weight or residual not 16-byte
  * aligned; EB_ERR_UNSUPPORTED as described for the prologue above. */
 eb_status eb_qlinear_fused(const eb_qlinear_op *op, int32_t path, hipStream_t stream);
+
+/* Bytes of workspace with which eb_qlinear_fused_ws runs *op on `path` as
+ * planned (normalised activations of a prologue on the MFMA path, then the
+ * fp32 partial sums of a split of k; at most m * k * 2 + 64 MiB).  0 when the
+ * op needs none (GEMV path, m == 0) or is invalid.  Host-only. */
+size_t eb_qlinear_workspace_bytes(const eb_qlinear_op *op, int32_t path);
+
+/* eb_qlinear_fused with a caller workspace (paper section 3.2, buffer reuse:
+ * the scratch of a projection is the caller's memory, reused across calls).
+ * `workspace`: device, 256-byte aligned, `workspace_bytes` bytes, or NULL
+ * with 0 bytes; it must not overlap the op's buffers.  A problem with too few
+ * output tiles to fill the GPU (few rows and columns, long k) is split along
+ * k when its partial sums fit the workspace after the normalised activations:
+ * each split writes fp32 partials and a second kernel adds them in a fixed
+ * order, so results are deterministic for a given workspace size (they can
+ * differ with the size, by the order of summation).  The workspace is used
+ * in stream order: calls that share one must be on one stream (or ordered).
+ * Errors as eb_qlinear_fused, plus EB_ERR_INVALID for a non-null workspace
+ * overlapping an operand or a null one with workspace_bytes > 0, and
+ * EB_ERR_ALIGN for a workspace not 256-byte aligned. */
+eb_status eb_qlinear_fused_ws(const eb_qlinear_op *op, int32_t path, void *workspace,
+                              size_t workspace_bytes, hipStream_t stream);
 
 /* eb_qlinear with an explicit kernel path (EB_PATH_*), for crossover
  * measurement and tests.  EB_ERR_UNSUPPORTED if the forced path cannot run
@@ -240,10 +257,23 @@ eb_status eb_qlinear_ex(const eb_qweights *w, const void *x, int32_t x_type, int
 /* Which path EB_PATH_AUTO takes for this problem (host-only, no launch). */
 int32_t eb_qlinear_auto_path(int32_t type, int32_t x_type, int64_t m, int64_t n, int64_t k);
 
+/* Bytes of workspace eb_qlinear_stack needs for this op list (the tables of
+ * its fused and grouped launches, split-K partial sums and normalised
+ * activations), 0 when it needs none or an op is invalid.  Host-only. */
+size_t eb_qlinear_stack_workspace_bytes(const eb_qlinear_op *ops, int32_t n_ops);
+
 /* Run ops[0..n_ops) on `stream` with the results of running them in order,
- * each as eb_qlinear would (paper section 3.2: graph replay, operator fusion,
- * buffer reuse).  `ops` is a HOST array.  All ops are validated before
- * anything is enqueued; n_ops == 0 is a no-op.
+ * each as eb_qlinear_fused_ws would (paper section 3.2: graph replay,
+ * operator fusion, buffer reuse).  `ops` is a HOST array.  All ops are
+ * validated before anything is enqueued; n_ops == 0 is a no-op.
+ *   Workspace: device, 256-byte aligned, at least
+ *   eb_qlinear_stack_workspace_bytes(ops, n_ops) bytes (else EB_ERR_INVALID;
+ *   NULL with 0 bytes when that is 0), overlapping no op's buffers.  A plan is
+ *   cached per (op list, workspace pointer and size) and keeps its launch
+ *   tables in the workspace: while the plan is cached (until
+ *   eb_stack_cache_clear, or until a plan for another op list is built on an
+ *   overlapping workspace, which drops it), the caller must not write to,
+ *   free or reuse that workspace for anything else.
  *   Each op may carry fused steps (prologue, epilogue) as eb_qlinear_fused.
  *   Fusion: a run of consecutive ops in which no op reads or writes memory
  *   that an earlier op of the run writes (decided by address ranges of x, y,
@@ -271,33 +301,22 @@ int32_t eb_qlinear_auto_path(int32_t type, int32_t x_type, int64_t m, int64_t n,
  *   EB_STACK_GRAPH=0 launches the plan directly instead; EB_STACK_DEBUG=1
  *   prints each plan's steps to stderr when it is built.  Called while
  *   `stream` itself is being captured, the ops are launched plainly into it.
- * Memory: a plan with fused runs owns a small device table (about 100 bytes
- * per fused op), a split-K workspace when one of its ops is split, and, for
- * EB_PRO_RMSNORM ops on the MFMA path, a buffer for the normalised
- * activations (the largest total m * k * 2 bytes of one launch step),
- * allocated once when the plan is built and freed by eb_stack_cache_clear
- * (or when more than 64 plans are cached). */
-eb_status eb_qlinear_stack(const eb_qlinear_op *ops, int32_t n_ops, hipStream_t stream);
+ * Memory: the workspace holds the plan's device tables (about 100 bytes per
+ * fused op, written once when the plan is built), a split-K area when one of
+ * its ops is split, and, for EB_PRO_RMSNORM ops on the MFMA path, the
+ * normalised activations (the largest total m * k * 2 bytes of one launch
+ * step).  At most 64 plans are cached; beyond that the cache is cleared. */
+eb_status eb_qlinear_stack(const eb_qlinear_op *ops, int32_t n_ops, void *workspace,
+                           size_t workspace_bytes, hipStream_t stream);
 
 /* Number of kernel launches eb_qlinear_stack makes for this op list (host
  * only; nothing is allocated or launched), or a negative eb_status if an op is
  * invalid. */
 int32_t eb_qlinear_stack_launches(const eb_qlinear_op *ops, int32_t n_ops);
 
-/* Drop every cached stack graph (frees their host/driver resources). */
+/* Drop every cached stack plan and graph (after the device has finished its
+ * work); their workspaces are then the caller's again. */
 eb_status eb_stack_cache_clear(void);
-
-/* Number of tile configurations of the MFMA path (host-only). */
-int32_t eb_mfma_tile_count(void);
-
-/* Tuning and test hook: force the MFMA path's tile configuration `tile`
- * (0 .. eb_mfma_tile_count() - 1, or -1 for the automatic choice) and its
- * split of k (1 .. 16 splits, or 0 for automatic).  A forced split that a
- * shape cannot take (fewer than 4 K-tiles of 64 per split) leaves that shape
- * unsplit.  Process-wide; applies to launches made after the call (cached
- * stack plans are keyed on it).  EB_ERR_INVALID for values out of range.  The
- * environment variable EB_MFMA_CFG=<tile> sets the initial forced tile. */
-eb_status eb_mfma_force(int32_t tile, int32_t splits);
 
 #ifdef __cplusplus
 }

@@ -148,44 +148,6 @@ int32_t pick_path(int32_t type, int32_t xt, int64_t m, int64_t n, int64_t k) {
   return (m <= 4 && n >= 2048) ? EB_PATH_GEMV : EB_PATH_MFMA;
 }
 
-// Split-K workspaces of direct calls, one per (device, stream) so calls on
-// different streams never share one.  A buffer that is outgrown is retired,
-// not freed: a graph the caller captured from that stream may still use it.
-struct WsCache {
-  std::mutex mu;
-  std::map<std::pair<int, hipStream_t>, std::pair<void *, size_t>> live;
-  std::vector<void *> retired;
-};
-
-WsCache &ws_cache() {
-  static WsCache *c = new WsCache();  // leaked on purpose: no teardown-order issues
-  return *c;
-}
-
-// Workspace of at least `bytes` for stream s, or nullptr (then the caller runs
-// unsplit): allocation failed, or s is being captured and the buffer it has is
-// too small (no allocation inside a capture).
-uint8_t *stream_workspace(hipStream_t s, size_t bytes) {
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return nullptr;
-  WsCache &C = ws_cache();
-  std::lock_guard<std::mutex> lock(C.mu);
-  auto &slot = C.live[{dev, s}];
-  if (slot.first && slot.second >= bytes) return static_cast<uint8_t *>(slot.first);
-  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
-  if (hipStreamIsCapturing(s, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone)
-    return nullptr;
-  const size_t want = std::max(bytes, std::max(slot.second * 2, (size_t)4 << 20));
-  void *p = nullptr;
-  if (hipMalloc(&p, want) != hipSuccess) {
-    (void)hipGetLastError();
-    return nullptr;
-  }
-  if (slot.first) C.retired.push_back(slot.first);
-  slot = {p, want};
-  return static_cast<uint8_t *>(p);
-}
-
 // Bytes of normalised activations an op on the MFMA path needs (256-aligned).
 size_t xhat_bytes(const eb_qlinear_op &o) {
   return o.prologue == EB_PRO_RMSNORM ? (size_t)round_up(o.m * o.w.k * 2, 256) : 0;
@@ -216,25 +178,59 @@ hipError_t launch_mfma_op(const eb_qlinear_op &o, const MfmaPlan &P, void *xbuf,
                      norm_next);
 }
 
-eb_status launch_op(const eb_qlinear_op &o, int32_t path, hipStream_t s) {
+// Scratch of one op on the MFMA path inside a workspace of `cap` bytes: the
+// normalised activations of a prologue (xb bytes at offset 0), then the
+// split-K partial sums of the plan (P.ws_bytes, only if they fit).
+struct OpScratch {
+  MfmaPlan P;
+  size_t xb = 0;
+  size_t total = 0;
+};
+
+OpScratch op_scratch(const eb_qlinear_op &o, size_t cap, int force_cfg = -1, int force_splits = 0) {
+  OpScratch r;
+  r.xb = xhat_bytes(o);
+  const size_t left = cap > r.xb ? std::min(cap - r.xb, kMaxSplitWorkspace) : 0;
+  r.P = plan_mfma(o.w.type, o.x_type, o.m, o.w.n, o.w.k, left, force_cfg, force_splits);
+  r.total = r.xb + r.P.ws_bytes;
+  return r;
+}
+
+// One op with the caller's workspace `ws` (device, 256-byte aligned, wsb
+// bytes; may be null with wsb == 0: then the MFMA path runs unsplit and a
+// prologue on it is unsupported).
+eb_status launch_op(const eb_qlinear_op &o, int32_t path, uint8_t *ws, size_t wsb, hipStream_t s,
+                    int force_cfg = -1, int force_splits = 0) {
   if (o.m == 0) return EB_OK;
   if (path == EB_PATH_AUTO) path = pick_path(o.w.type, o.x_type, o.m, o.w.n, o.w.k);
   hipError_t e;
   if (path == EB_PATH_GEMV) {
     e = launch_gemv(o.w.type, o.w.data, o.w.n, o.w.k, o.x, o.x_type, o.m, o.y, o.y_type, fuse_of(o), s);
   } else {
-    // the stream's workspace holds the normalised activations, then any
-    // split-K partial sums
-    const size_t xb = xhat_bytes(o);
-    MfmaPlan P = plan_mfma(o.w.type, o.x_type, o.m, o.w.n, o.w.k, true);
-    uint8_t *ws = nullptr;
-    if (P.splits > 1) ws = stream_workspace(s, xb + P.ws_bytes);
-    if (P.splits > 1 && !ws) P = plan_mfma(o.w.type, o.x_type, o.m, o.w.n, o.w.k, false);
-    if (!ws && xb) ws = stream_workspace(s, xb);
-    if (xb && !ws) return EB_ERR_UNSUPPORTED;
-    e = launch_mfma_op(o, P, ws, P.splits > 1 ? reinterpret_cast<float *>(ws + xb) : nullptr, s);
+    const OpScratch sc = op_scratch(o, ws ? wsb : 0, force_cfg, force_splits);
+    if (sc.xb && (!ws || wsb < sc.xb)) return EB_ERR_UNSUPPORTED;
+    float *part = sc.P.splits > 1 ? reinterpret_cast<float *>(ws + sc.xb) : nullptr;
+    e = launch_mfma_op(o, sc.P, ws, part, s);
   }
   return e == hipSuccess ? EB_OK : EB_ERR_HIP;
+}
+
+// Workspace arguments: null with 0 bytes, or 256-byte aligned device memory
+// that overlaps none of the op's buffers.
+eb_status check_workspace(const eb_qlinear_op *ops, int32_t n_ops, const void *ws, size_t wsb) {
+  if (!ws) return wsb == 0 ? EB_OK : EB_ERR_INVALID;
+  if (!aligned(ws, 256)) return EB_ERR_ALIGN;
+  for (int32_t i = 0; i < n_ops; ++i) {
+    const eb_qlinear_op &o = ops[i];
+    if (o.m == 0) continue;
+    const size_t yb = (size_t)o.m * (size_t)n_out(o) * dsize(o.y_type);
+    if (overlaps(ws, wsb, o.x, x_bytes(o)) || overlaps(ws, wsb, o.y, yb) ||
+        overlaps(ws, wsb, o.w.data, eb_qweights_bytes(o.w.type, o.w.n, o.w.k)) ||
+        (o.prologue == EB_PRO_RMSNORM && overlaps(ws, wsb, o.norm_weight, (size_t)o.w.k * 4)) ||
+        (o.epilogue == EB_EPI_ADD && overlaps(ws, wsb, o.residual, yb)))
+      return EB_ERR_INVALID;
+  }
+  return EB_OK;
 }
 
 eb_status quantize_common(int32_t type, const float *w, int64_t n, int64_t k, void *out,
@@ -355,6 +351,8 @@ struct Plan {
   size_t ws_bytes = 0;
   uint8_t *xbuf = nullptr;  // normalised activations of prologue ops on the MFMA path
   size_t xbuf_bytes = 0;
+  size_t ws_total = 0;      // caller workspace the plan needs (tables, partial sums, xbuf)
+  uint8_t *wsbase = nullptr;  // where that workspace is (the tables live there)
   hipEvent_t fork = nullptr, join = nullptr;  // side-stream steps (created when there are any)
   hipGraph_t graph = nullptr;
   hipGraphExec_t exec = nullptr;
@@ -394,9 +392,10 @@ bool mm_fusable(const eb_qlinear_op &o) {
          pick_path(o.w.type, o.x_type, o.m, o.w.n, o.w.k) == EB_PATH_MFMA;
 }
 
-// Builds the plan; with `alloc`, also allocates and fills its device tables
-// and buffers (without it the plan is only counted).
-eb_status build_plan(const eb_qlinear_op *ops, int32_t n_ops, bool alloc, Plan &P) {
+// Builds the plan and sizes its workspace (P.ws_total); with a workspace base
+// (at least P.ws_total bytes) also places its tables and buffers there and
+// writes the tables.  Without one the plan is only counted and sized.
+eb_status build_plan(const eb_qlinear_op *ops, int32_t n_ops, uint8_t *wsbase, Plan &P) {
   std::vector<M1Op> host;
   std::vector<MMOp> mmhost;
   std::vector<int64_t> mmwg;
@@ -656,7 +655,7 @@ eb_status build_plan(const eb_qlinear_op *ops, int32_t n_ops, bool alloc, Plan &
     const eb_qlinear_op &o = ops[s.op];
     if (o.m == 0 || pick_path(o.w.type, o.x_type, o.m, o.w.n, o.w.k) != EB_PATH_MFMA) continue;
     s.mfma = true;
-    s.mp = plan_mfma(o.w.type, o.x_type, o.m, o.w.n, o.w.k, true);
+    s.mp = plan_mfma(o.w.type, o.x_type, o.m, o.w.n, o.w.k, kMaxSplitWorkspace);
     P.ws_bytes = std::max(P.ws_bytes, s.mp.ws_bytes);
     P.xbuf_bytes = std::max(P.xbuf_bytes, xhat_bytes(o));
   }
@@ -677,59 +676,50 @@ eb_status build_plan(const eb_qlinear_op *ops, int32_t n_ops, bool alloc, Plan &
       b.pre_normed = true;
     }
   }
-  if (!alloc) return EB_OK;
-  if (P.xbuf_bytes > 0) {
-    if (hipMalloc((void **)&P.xbuf, P.xbuf_bytes) != hipSuccess) {
-      P.xbuf = nullptr;
-      return EB_ERR_HIP;
-    }
-    // table entries whose x is an offset into the buffer
-    for (MMOp &e : mmhost)
-      if (e.pad) e.x = reinterpret_cast<const uint16_t *>(P.xbuf + reinterpret_cast<uintptr_t>(e.x));
-    for (GOp &e : gmhost)
-      if (e.pad) e.x = reinterpret_cast<const uint16_t *>(P.xbuf + reinterpret_cast<uintptr_t>(e.x));
-  }
-  if (!mmhost.empty()) {
-    if (hipMalloc((void **)&P.mmtable, mmhost.size() * sizeof(MMOp)) != hipSuccess) {
-      P.mmtable = nullptr;
-      return EB_ERR_HIP;
-    }
-    if (hipMalloc((void **)&P.mmwg, mmwg.size() * sizeof(int64_t)) != hipSuccess) {
-      P.mmwg = nullptr;
-      return EB_ERR_HIP;
-    }
-    if (hipMemcpy(P.mmtable, mmhost.data(), mmhost.size() * sizeof(MMOp),
-                  hipMemcpyHostToDevice) != hipSuccess ||
-        hipMemcpy(P.mmwg, mmwg.data(), mmwg.size() * sizeof(int64_t), hipMemcpyHostToDevice) !=
-            hipSuccess)
-      return EB_ERR_HIP;
-  }
-  if (!gmhost.empty()) {
-    if (hipMalloc((void **)&P.gmtable, gmhost.size() * sizeof(GOp)) != hipSuccess) {
-      P.gmtable = nullptr;
-      return EB_ERR_HIP;
-    }
-    if (hipMalloc((void **)&P.gmorder, gmorder.size() * sizeof(int2)) != hipSuccess) {
-      P.gmorder = nullptr;
-      return EB_ERR_HIP;
-    }
-    if (hipMemcpy(P.gmtable, gmhost.data(), gmhost.size() * sizeof(GOp), hipMemcpyHostToDevice) !=
-            hipSuccess ||
-        hipMemcpy(P.gmorder, gmorder.data(), gmorder.size() * sizeof(int2),
-                  hipMemcpyHostToDevice) != hipSuccess)
-      return EB_ERR_HIP;
-  }
-  if (P.ws_bytes > 0 && hipMalloc((void **)&P.ws, P.ws_bytes) != hipSuccess) {
-    P.ws = nullptr;
-    return EB_ERR_HIP;
-  }
-  if (!host.empty()) {
-    if (hipMalloc((void **)&P.table, host.size() * sizeof(M1Op)) != hipSuccess) {
-      P.table = nullptr;
-      return EB_ERR_HIP;
-    }
-    if (hipMemcpy(P.table, host.data(), host.size() * sizeof(M1Op), hipMemcpyHostToDevice) !=
-        hipSuccess)
+  // The plan's device memory is the caller's workspace: the op tables of its
+  // fused and grouped launches, then the split-K partial sums, then the
+  // normalised activations, each 256-byte aligned.
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = (size_t)round_up((int64_t)(off + bytes), 256);
+    return o;
+  };
+  const size_t t_m1 = take(host.size() * sizeof(M1Op));
+  const size_t t_mm = take(mmhost.size() * sizeof(MMOp));
+  const size_t t_wg = take(mmwg.size() * sizeof(int64_t));
+  const size_t t_gm = take(gmhost.size() * sizeof(GOp));
+  const size_t t_go = take(gmorder.size() * sizeof(int2));
+  const size_t t_tables = off;
+  const size_t t_ws = take(P.ws_bytes);
+  const size_t t_xb = take(P.xbuf_bytes);
+  P.ws_total = off;
+  if (!wsbase) return EB_OK;
+  P.wsbase = wsbase;
+  P.table = host.empty() ? nullptr : reinterpret_cast<M1Op *>(wsbase + t_m1);
+  P.mmtable = mmhost.empty() ? nullptr : reinterpret_cast<MMOp *>(wsbase + t_mm);
+  P.mmwg = mmwg.empty() ? nullptr : reinterpret_cast<int64_t *>(wsbase + t_wg);
+  P.gmtable = gmhost.empty() ? nullptr : reinterpret_cast<GOp *>(wsbase + t_gm);
+  P.gmorder = gmorder.empty() ? nullptr : reinterpret_cast<int2 *>(wsbase + t_go);
+  P.ws = P.ws_bytes ? reinterpret_cast<float *>(wsbase + t_ws) : nullptr;
+  P.xbuf = P.xbuf_bytes ? wsbase + t_xb : nullptr;
+  // table entries whose x is an offset into the normalised-activation buffer
+  for (MMOp &e : mmhost)
+    if (e.pad) e.x = reinterpret_cast<const uint16_t *>(P.xbuf + reinterpret_cast<uintptr_t>(e.x));
+  for (GOp &e : gmhost)
+    if (e.pad) e.x = reinterpret_cast<const uint16_t *>(P.xbuf + reinterpret_cast<uintptr_t>(e.x));
+  // the tables, written once when the plan is built (a copy, not an allocation)
+  if (t_tables > 0) {
+    std::vector<uint8_t> img(t_tables, 0);
+    auto put = [&](size_t at, const void *src, size_t bytes) {
+      if (bytes) std::memcpy(img.data() + at, src, bytes);
+    };
+    put(t_m1, host.data(), host.size() * sizeof(M1Op));
+    put(t_mm, mmhost.data(), mmhost.size() * sizeof(MMOp));
+    put(t_wg, mmwg.data(), mmwg.size() * sizeof(int64_t));
+    put(t_gm, gmhost.data(), gmhost.size() * sizeof(GOp));
+    put(t_go, gmorder.data(), gmorder.size() * sizeof(int2));
+    if (hipMemcpy(wsbase, img.data(), t_tables, hipMemcpyHostToDevice) != hipSuccess)
       return EB_ERR_HIP;
   }
   return EB_OK;
@@ -799,7 +789,7 @@ eb_status run_plan(const eb_qlinear_op *ops, const Plan &P, hipStream_t s, hipSt
                          st.norm_next ? &no : nullptr) != hipSuccess)
         return EB_ERR_HIP;
     } else if (st.op >= 0) {
-      eb_status r = launch_op(ops[st.op], EB_PATH_AUTO, s);
+      eb_status r = launch_op(ops[st.op], EB_PATH_AUTO, nullptr, 0, s);
       if (r != EB_OK) return r;
     } else if (launch_gemv_m1_multi(st.type, st.xt, st.ns, P.table + st.table, st.nops, st.units,
                                     st.rows, s) != hipSuccess) {
@@ -813,13 +803,6 @@ eb_status run_plan(const eb_qlinear_op *ops, const Plan &P, hipStream_t s, hipSt
 void destroy_plan(Plan &p) {
   if (p.exec) (void)hipGraphExecDestroy(p.exec);
   if (p.graph) (void)hipGraphDestroy(p.graph);
-  if (p.table) (void)hipFree(p.table);
-  if (p.mmtable) (void)hipFree(p.mmtable);
-  if (p.mmwg) (void)hipFree(p.mmwg);
-  if (p.gmtable) (void)hipFree(p.gmtable);
-  if (p.gmorder) (void)hipFree(p.gmorder);
-  if (p.ws) (void)hipFree(p.ws);
-  if (p.xbuf) (void)hipFree(p.xbuf);
   if (p.fork) (void)hipEventDestroy(p.fork);
   if (p.join) (void)hipEventDestroy(p.join);
   p = Plan();
@@ -845,9 +828,10 @@ void clear_cache_locked(StackCache &C) {
   C.map.clear();
 }
 
-eb_status run_ops_direct(const eb_qlinear_op *ops, int32_t n_ops, hipStream_t s) {
+eb_status run_ops_direct(const eb_qlinear_op *ops, int32_t n_ops, uint8_t *ws, size_t wsb,
+                         hipStream_t s) {
   for (int32_t i = 0; i < n_ops; ++i) {
-    eb_status st = launch_op(ops[i], EB_PATH_AUTO, s);
+    eb_status st = launch_op(ops[i], EB_PATH_AUTO, ws, wsb, s);
     if (st != EB_OK) return st;
   }
   return EB_OK;
@@ -924,14 +908,28 @@ eb_status eb_qlinear_ex(const eb_qweights *w, const void *x, int32_t x_type, int
   const eb_qlinear_op o = plain_op(w, x, x_type, m, y, y_type);
   eb_status st = check_op(o, path);
   if (st != EB_OK) return st;
-  return launch_op(o, path, stream);
+  return launch_op(o, path, nullptr, 0, stream);
 }
 
 eb_status eb_qlinear_fused(const eb_qlinear_op *op, int32_t path, hipStream_t stream) {
+  return eb_qlinear_fused_ws(op, path, nullptr, 0, stream);
+}
+
+size_t eb_qlinear_workspace_bytes(const eb_qlinear_op *op, int32_t path) {
+  if (!op || check_op(*op, path) != EB_OK || op->m == 0) return 0;
+  if (path == EB_PATH_AUTO) path = pick_path(op->w.type, op->x_type, op->m, op->w.n, op->w.k);
+  if (path == EB_PATH_GEMV) return 0;
+  return op_scratch(*op, kMaxSplitWorkspace + xhat_bytes(*op)).total;
+}
+
+eb_status eb_qlinear_fused_ws(const eb_qlinear_op *op, int32_t path, void *workspace,
+                              size_t workspace_bytes, hipStream_t stream) {
   if (!op) return EB_ERR_INVALID;
   eb_status st = check_op(*op, path);
   if (st != EB_OK) return st;
-  return launch_op(*op, path, stream);
+  st = check_workspace(op, 1, workspace, workspace_bytes);
+  if (st != EB_OK) return st;
+  return launch_op(*op, path, static_cast<uint8_t *>(workspace), workspace_bytes, stream);
 }
 
 eb_status eb_qlinear(const eb_qweights *w, const void *x, int32_t x_type, int64_t m, void *y,
@@ -944,7 +942,17 @@ int32_t eb_qlinear_auto_path(int32_t type, int32_t x_type, int64_t m, int64_t n,
   return pick_path(type, x_type, m, n, k);
 }
 
-eb_status eb_qlinear_stack(const eb_qlinear_op *ops, int32_t n_ops, hipStream_t stream) {
+size_t eb_qlinear_stack_workspace_bytes(const eb_qlinear_op *ops, int32_t n_ops) {
+  if (n_ops <= 0 || !ops) return 0;
+  for (int32_t i = 0; i < n_ops; ++i)
+    if (check_op(ops[i], EB_PATH_AUTO) != EB_OK) return 0;
+  Plan P;
+  build_plan(ops, n_ops, nullptr, P);
+  return P.ws_total;
+}
+
+eb_status eb_qlinear_stack(const eb_qlinear_op *ops, int32_t n_ops, void *workspace,
+                           size_t workspace_bytes, hipStream_t stream) {
   if (n_ops < 0) return EB_ERR_INVALID;
   if (n_ops == 0) return EB_OK;
   if (!ops) return EB_ERR_INVALID;
@@ -953,10 +961,15 @@ eb_status eb_qlinear_stack(const eb_qlinear_op *ops, int32_t n_ops, hipStream_t 
     eb_status st = check_op(o, EB_PATH_AUTO);
     if (st != EB_OK) return st;
   }
+  {
+    eb_status st = check_workspace(ops, n_ops, workspace, workspace_bytes);
+    if (st != EB_OK) return st;
+  }
+  uint8_t *const ws = static_cast<uint8_t *>(workspace);
   // Inside a caller's own stream capture, record plain launches into it.
   hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
   if (hipStreamIsCapturing(stream, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone)
-    return run_ops_direct(ops, n_ops, stream);
+    return run_ops_direct(ops, n_ops, ws, workspace_bytes, stream);
 
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return EB_ERR_HIP;
@@ -967,8 +980,9 @@ eb_status eb_qlinear_stack(const eb_qlinear_op *ops, int32_t n_ops, hipStream_t 
   key.push_back(env_off("EB_STACK_GROUP") ? 'n' : 'g');
   key.push_back(env_off("EB_STACK_SPLIT_TAIL") ? 'w' : 's');
   key.push_back(env_off("EB_STACK_OVERLAP_TAIL") ? 'q' : 'o');
-  const int fk = mfma_force_key();
-  key.append(reinterpret_cast<const char *>(&fk), sizeof(fk));
+  key.push_back(env_off("EB_STACK_FUSE_NORM") ? 'r' : 'n');
+  key.append(reinterpret_cast<const char *>(&ws), sizeof(ws));
+  key.append(reinterpret_cast<const char *>(&workspace_bytes), sizeof(workspace_bytes));
   key.append(reinterpret_cast<const char *>(ops), sizeof(eb_qlinear_op) * (size_t)n_ops);
 
   StackCache &C = cache();
@@ -977,7 +991,30 @@ eb_status eb_qlinear_stack(const eb_qlinear_op *ops, int32_t n_ops, hipStream_t 
   if (it == C.map.end()) {
     if (C.map.size() >= kMaxCachedPlans) clear_cache_locked(C);
     Plan P;
-    eb_status st = build_plan(ops, n_ops, true, P);
+    eb_status st = build_plan(ops, n_ops, nullptr, P);
+    if (st == EB_OK && P.ws_total > workspace_bytes) st = EB_ERR_INVALID;  // workspace too small
+    if (st == EB_OK && P.ws_total > 0) {
+      // A cached plan whose tables sit in the same workspace bytes is dropped
+      // first (after the device has finished any replay of it): the new
+      // plan's tables overwrite them.
+      bool clash = false;
+      for (const auto &kv : C.map)
+        clash = clash || overlaps(kv.second.wsbase, kv.second.ws_total, ws, P.ws_total);
+      if (clash) {
+        (void)hipDeviceSynchronize();
+        for (auto kv = C.map.begin(); kv != C.map.end();) {
+          if (overlaps(kv->second.wsbase, kv->second.ws_total, ws, P.ws_total)) {
+            destroy_plan(kv->second);
+            kv = C.map.erase(kv);
+          } else {
+            ++kv;
+          }
+        }
+      }
+      Plan Q;
+      st = build_plan(ops, n_ops, ws, Q);
+      P = Q;
+    }
     if (st != EB_OK) {
       destroy_plan(P);
       return st;
@@ -1031,7 +1068,7 @@ int32_t eb_qlinear_stack_launches(const eb_qlinear_op *ops, int32_t n_ops) {
     if (st != EB_OK) return st;
   }
   Plan P;
-  build_plan(ops, n_ops, false, P);
+  build_plan(ops, n_ops, nullptr, P);
   int32_t launches = 0;
   for (const Step &st : P.steps) {
     launches += (int32_t)st.norms.size();
@@ -1044,10 +1081,15 @@ int32_t eb_qlinear_stack_launches(const eb_qlinear_op *ops, int32_t n_ops) {
 
 int32_t eb_mfma_tile_count(void) { return mfma_tile_count(); }
 
-eb_status eb_mfma_force(int32_t tile, int32_t splits) {
-  if (tile < -1 || tile >= mfma_tile_count() || splits < 0 || splits > 16) return EB_ERR_INVALID;
-  mfma_force(tile, splits);
-  return EB_OK;
+eb_status eb_qlinear_tuned(const eb_qlinear_op *op, int32_t tile, int32_t splits, void *workspace,
+                           size_t workspace_bytes, hipStream_t stream) {
+  if (!op || tile < -1 || tile >= mfma_tile_count() || splits < 0 || splits > 16) return EB_ERR_INVALID;
+  eb_status st = check_op(*op, EB_PATH_MFMA);
+  if (st != EB_OK) return st;
+  st = check_workspace(op, 1, workspace, workspace_bytes);
+  if (st != EB_OK) return st;
+  return launch_op(*op, EB_PATH_MFMA, static_cast<uint8_t *>(workspace), workspace_bytes, stream,
+                   tile, splits);
 }
 
 eb_status eb_stack_cache_clear(void) {

@@ -9,6 +9,7 @@
 #include <vector>
 
 #include "../../include/eb.h"
+#include "../../include/eb_tuning.h"
 
 namespace eb {
 
@@ -121,7 +122,12 @@ struct MfmaPlan {
   int64_t ws_stride = 0;  // floats between the partial outputs of two splits
   size_t ws_bytes = 0;
 };
-MfmaPlan plan_mfma(int32_t type, int32_t xt, int64_t m, int64_t n, int64_t k, bool allow_split);
+// max_ws: bytes of partial-sum workspace the call may use (0: no split);
+// force_cfg >= 0 / force_splits > 0 fix the tile configuration / split count
+// (tuning and tests; a forced choice that does not fit is not taken).
+MfmaPlan plan_mfma(int32_t type, int32_t xt, int64_t m, int64_t n, int64_t k, size_t max_ws,
+                   int force_cfg = -1, int force_splits = 0);
+constexpr size_t kMaxSplitWorkspace = size_t(64) << 20;  // partial sums a plan may ask for
 // ws == nullptr runs the plan's configuration unsplit.  norm_next (split runs
 // with an fp32 output and no gated product only) fuses the next projection's
 // normalisation into the reduction.
@@ -194,8 +200,6 @@ int mm_partition(const std::vector<MMOp> &ops, int cfg, std::vector<int64_t> &wg
 // groups must be a positive multiple of 8 (mm_partition's result).
 hipError_t launch_mfma_multi(int32_t type, int32_t xt, int32_t yt, int cfg, const MMOp *dev_ops,
                              int nops, const int64_t *dev_wg, int groups, hipStream_t s);
-void mfma_force(int cfg, int splits);  // cfg -1 / splits 0: automatic
-int mfma_force_key();                  // changes whenever the forced state does
 
 // number of compute units of the current device (cached per device)
 int device_cu_count();

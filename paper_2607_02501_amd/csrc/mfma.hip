@@ -100,21 +100,6 @@ constexpr int kNumCfgs = sizeof(kCfgs) / sizeof(kCfgs[0]);
 constexpr int kHLCfgs[][2] = {{0, 2}, {1, 1}};
 constexpr int64_t kHLMaxM = 128;
 
-std::atomic<int> g_force_cfg{-1}, g_force_splits{0};
-
-// Tuning hook: EB_MFMA_CFG=<index> in the environment sets the initial forced
-// configuration.
-int forced_cfg() {
-  static const bool init = [] {
-    const char *e = getenv("EB_MFMA_CFG");
-    if (e) g_force_cfg.store(atoi(e));
-    return true;
-  }();
-  (void)init;
-  return g_force_cfg.load(std::memory_order_relaxed);
-}
-
-constexpr int64_t kMaxWorkspace = int64_t(64) << 20;  // bytes of fp32 partials per call
 constexpr int kMinSplitTiles = 4;                      // K-tiles per split, at least
 
 // Estimated time (s) of one configuration and split count.  Workgroups run in
@@ -147,22 +132,15 @@ int mfma_tile_count() { return kNumCfgs; }
 int mfma_cfg_bm(int cfg) { return kCfgs[cfg].bm; }
 double mfma_cfg_rate(int cfg) { return kCfgs[cfg].rate; }
 
-void mfma_force(int cfg, int splits) {
-  (void)forced_cfg();
-  g_force_cfg.store(cfg);
-  g_force_splits.store(splits);
-}
-
-int mfma_force_key() { return (forced_cfg() + 1) * 64 + g_force_splits.load(); }
-
 bool needs_hl(int32_t xt, int64_t m) { return xt == EB_BF16 && m <= kHLMaxM; }
 
-MfmaPlan plan_mfma(int32_t type, int32_t xt, int64_t m, int64_t n, int64_t k, bool allow_split) {
+MfmaPlan plan_mfma(int32_t type, int32_t xt, int64_t m, int64_t n, int64_t k, size_t max_ws,
+                   int force_cfg, int force_splits) {
   const int64_t nk = (k + kBK - 1) / kBK;
   const int cus = device_cu_count();
   const bool hl = needs_hl(xt, m);
-  int fc = forced_cfg();
-  const int fs = g_force_splits.load(std::memory_order_relaxed);
+  int fc = force_cfg;
+  const int fs = force_splits;
   if (hl) {  // a forced tile without hi/lo tiles does not apply here
     bool ok = false;
     for (const auto &h : kHLCfgs) ok = ok || h[0] == fc;
@@ -187,13 +165,13 @@ MfmaPlan plan_mfma(int32_t type, int32_t xt, int64_t m, int64_t n, int64_t k, bo
                                       : mfma_fits_offsets(EB_Q8_0, n, k, g.bm, g.bn);
     if (!fits) continue;
     for (int sp = 1; sp <= 16; ++sp) {
-      if (sp > 1 && !allow_split) break;
+      if (sp > 1 && max_ws == 0) break;
       if (fs > 0 && sp != fs) continue;
       const int64_t kts = (nk + sp - 1) / sp;
       if (sp > 1 && (kts < kMinSplitTiles || (nk + kts - 1) / kts != sp)) continue;
       const int64_t stride = (m * n + 63) / 64 * 64;
       const int64_t wsb = sp > 1 ? stride * sp * 4 : 0;
-      if (wsb > kMaxWorkspace && fs <= 0) continue;
+      if ((size_t)wsb > max_ws) continue;
       const double t = estimate(type, g, m, n, k, sp, cus);
       if (!have || t < best_t * 0.999) {
         have = true;
@@ -221,13 +199,9 @@ constexpr int kGroupCfgs[] = {1, 2, 4, 6};
 
 int plan_grouped(int32_t type, const std::vector<GOp> &ops, std::vector<int2> &order) {
   const int cus = device_cu_count();
-  const int fc = forced_cfg();
   int best = -1;
   double best_t = 0;
   for (int c : kGroupCfgs) {
-    if (fc >= 0 && fc < kNumCfgs && c != fc &&
-        std::find(std::begin(kGroupCfgs), std::end(kGroupCfgs), fc) != std::end(kGroupCfgs))
-      continue;
     const Cfg &g = kCfgs[c];
     bool fits = true;
     double work = 0, longest = 0;

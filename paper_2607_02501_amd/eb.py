@@ -1,11 +1,12 @@
 """Python binding of libeb (argument marshalling only).
 
 Every computation runs in the HIP kernels of libeb.so; this module only
-allocates outputs with torch, passes raw device pointers and the current HIP
-stream, and turns status codes into exceptions.  It raises at import time if
-libeb.so has not been built (there is no fallback path).
+allocates outputs and workspaces with torch (the library allocates no device
+memory), passes raw device pointers and the current HIP stream, and turns
+status codes into exceptions.  It raises at import time if libeb.so has not
+been built (there is no fallback path).
 
-Names follow the C ABI in include/eb.h.
+Names follow the C ABI in include/eb.h and include/eb_tuning.h.
 """
 from __future__ import annotations
 
@@ -94,15 +95,21 @@ lib.eb_qlinear_fused.argtypes = [ctypes.POINTER(eb_qlinear_op), _i32, _vp]
 lib.eb_qlinear_auto_path.restype = _i32
 lib.eb_qlinear_auto_path.argtypes = [_i32, _i32, _i64, _i64, _i64]
 lib.eb_qlinear_stack.restype = _i32
-lib.eb_qlinear_stack.argtypes = [ctypes.POINTER(eb_qlinear_op), _i32, _vp]
+lib.eb_qlinear_stack.argtypes = [ctypes.POINTER(eb_qlinear_op), _i32, _vp, ctypes.c_size_t, _vp]
+lib.eb_qlinear_stack_workspace_bytes.restype = ctypes.c_size_t
+lib.eb_qlinear_stack_workspace_bytes.argtypes = [ctypes.POINTER(eb_qlinear_op), _i32]
+lib.eb_qlinear_workspace_bytes.restype = ctypes.c_size_t
+lib.eb_qlinear_workspace_bytes.argtypes = [ctypes.POINTER(eb_qlinear_op), _i32]
+lib.eb_qlinear_fused_ws.restype = _i32
+lib.eb_qlinear_fused_ws.argtypes = [ctypes.POINTER(eb_qlinear_op), _i32, _vp, ctypes.c_size_t, _vp]
+lib.eb_qlinear_tuned.restype = _i32
+lib.eb_qlinear_tuned.argtypes = [ctypes.POINTER(eb_qlinear_op), _i32, _i32, _vp, ctypes.c_size_t, _vp]
 lib.eb_qlinear_stack_launches.restype = _i32
 lib.eb_qlinear_stack_launches.argtypes = [ctypes.POINTER(eb_qlinear_op), _i32]
 lib.eb_stack_cache_clear.restype = _i32
 lib.eb_stack_cache_clear.argtypes = []
 lib.eb_mfma_tile_count.restype = _i32
 lib.eb_mfma_tile_count.argtypes = []
-lib.eb_mfma_force.restype = _i32
-lib.eb_mfma_force.argtypes = [_i32, _i32]
 
 
 class EBError(RuntimeError):
@@ -193,18 +200,61 @@ def from_canonical(blocks: torch.Tensor, qtype: str, n: int, k: int) -> QWeights
     return out
 
 
+_SCRATCH = {}
+
+
+def scratch(device, nbytes: int):
+    """A caller-owned workspace of at least nbytes on `device` for direct calls
+    on the current stream (one growing torch buffer per device and stream;
+    calls on one stream run in order, so they may share it)."""
+    if nbytes <= 0:
+        return None
+    device = torch.device(device)
+    key = (device.index if device.index is not None else torch.cuda.current_device(),
+           _stream(device))
+    buf = _SCRATCH.get(key)
+    if buf is None or buf.numel() < nbytes:
+        buf = torch.empty(max(nbytes, 4 << 20), dtype=torch.uint8, device=device)
+        _SCRATCH[key] = buf
+    return buf
+
+
+def _run_op(op: eb_qlinear_op, path: int, device, tile=None, splits=0) -> None:
+    nbytes = int(lib.eb_qlinear_workspace_bytes(ctypes.byref(op), path if tile is None else EB_PATH_MFMA))
+    if tile is not None and nbytes:
+        nbytes += 64 << 20  # room for any forced split
+    ws = scratch(device, nbytes)
+    wp, wb = (ws.data_ptr(), ws.numel()) if ws is not None else (None, 0)
+    if tile is None:
+        _check(lib.eb_qlinear_fused_ws(ctypes.byref(op), path, wp, wb, _stream(device)),
+               "eb_qlinear_fused_ws")
+    else:
+        _check(lib.eb_qlinear_tuned(ctypes.byref(op), tile, splits, wp, wb, _stream(device)),
+               "eb_qlinear_tuned")
+
+
 def qlinear(qw: QWeights, x: torch.Tensor, out_dtype=torch.float32, path: str = "auto",
             out: torch.Tensor | None = None) -> torch.Tensor:
-    """y[m, n] = x[m, k] . w_hat^T on the GPU (fp32 accumulation)."""
+    """y[m, n] = x[m, k] . w_hat^T on the GPU (fp32 accumulation), with a
+    workspace from scratch() so that the MFMA path may split k."""
     assert x.is_cuda and x.dim() == 2 and x.shape[1] == qw.k
     x = x.contiguous()
     m = x.shape[0]
     if out is None:
         out = torch.empty((m, qw.n), dtype=out_dtype, device=x.device)
-    c = qw.c
-    st = lib.eb_qlinear_ex(ctypes.byref(c), x.data_ptr(), DTYPES[x.dtype], m, out.data_ptr(),
-                           DTYPES[out.dtype], PATHS[path], _stream(x.device))
-    _check(st, "eb_qlinear_ex")
+    _run_op(make_op(qw, x, out), PATHS[path], x.device)
+    return out
+
+
+def qlinear_tuned(qw: QWeights, x: torch.Tensor, tile: int = -1, splits: int = 0,
+                  out_dtype=torch.float32, out: torch.Tensor | None = None) -> torch.Tensor:
+    """qlinear on the MFMA path with a forced tile configuration / split of k
+    (-1 / 0: automatic), for tuning and tests (eb_qlinear_tuned)."""
+    assert x.is_cuda and x.dim() == 2 and x.shape[1] == qw.k
+    x = x.contiguous()
+    if out is None:
+        out = torch.empty((x.shape[0], qw.n), dtype=out_dtype, device=x.device)
+    _run_op(make_op(qw, x, out), EB_PATH_MFMA, x.device, tile=tile, splits=splits)
     return out
 
 
@@ -238,10 +288,13 @@ def make_ops(entries) -> ctypes.Array:
 
 def qlinear_fused(qw: QWeights, x: torch.Tensor, out_dtype=torch.float32, x_dtype=None,
                   prologue=None, norm_weight=None, eps: float = 0.0, epilogue=None,
-                  residual=None, path: str = "auto", out: torch.Tensor | None = None) -> torch.Tensor:
+                  residual=None, path: str = "auto", out: torch.Tensor | None = None,
+                  tile: int | None = None, splits: int = 0) -> torch.Tensor:
     """One projection with fused steps (eb_qlinear_fused): optional RMS
     normalisation of x before the product, residual addition ("add") or the
-    SiLU-gated product of interleaved gate/up rows ("glu", output n / 2)."""
+    SiLU-gated product of interleaved gate/up rows ("glu", output n / 2).
+    tile / splits force the MFMA path's tile configuration / split of k
+    (eb_qlinear_tuned; -1 / 0: automatic)."""
     assert x.is_cuda and x.dim() == 2 and x.shape[1] == qw.k
     x = x.contiguous()
     m = x.shape[0]
@@ -249,13 +302,28 @@ def qlinear_fused(qw: QWeights, x: torch.Tensor, out_dtype=torch.float32, x_dtyp
         n_out = qw.n // 2 if epilogue == "glu" else qw.n
         out = torch.empty((m, n_out), dtype=out_dtype, device=x.device)
     op = make_op(qw, x, out, x_dtype, prologue, norm_weight, eps, epilogue, residual)
-    _check(lib.eb_qlinear_fused(ctypes.byref(op), PATHS[path], _stream(x.device)),
-           "eb_qlinear_fused")
+    if tile is None and not splits:
+        _run_op(op, PATHS[path], x.device)
+    else:
+        _run_op(op, EB_PATH_MFMA, x.device, tile=-1 if tile is None else tile, splits=splits)
     return out
 
 
+def stack_workspace_bytes(ops: ctypes.Array) -> int:
+    return int(lib.eb_qlinear_stack_workspace_bytes(ops, len(ops)))
+
+
 def qlinear_stack(ops: ctypes.Array, device=None) -> None:
-    _check(lib.eb_qlinear_stack(ops, len(ops), _stream(device)), "eb_qlinear_stack")
+    """eb_qlinear_stack with a workspace that belongs to this op array (kept
+    on it: the cached plan keeps its tables there while it is cached)."""
+    nbytes = stack_workspace_bytes(ops)
+    ws = getattr(ops, "_eb_workspace", None)
+    if nbytes and (ws is None or ws.numel() < nbytes):
+        ws = torch.empty(nbytes, dtype=torch.uint8,
+                         device=device if device is not None else torch.cuda.current_device())
+        ops._eb_workspace = ws
+    wp, wb = (ws.data_ptr(), ws.numel()) if (nbytes and ws is not None) else (None, 0)
+    _check(lib.eb_qlinear_stack(ops, len(ops), wp, wb, _stream(device)), "eb_qlinear_stack")
 
 
 def stack_launches(ops: ctypes.Array) -> int:
@@ -272,8 +340,3 @@ def stack_cache_clear() -> None:
 
 def mfma_tile_count() -> int:
     return int(lib.eb_mfma_tile_count())
-
-
-def mfma_force(tile: int = -1, splits: int = 0) -> None:
-    """Force the MFMA tile configuration / split-K factor (-1 / 0: automatic)."""
-    _check(lib.eb_mfma_force(tile, splits), "eb_mfma_force")

@@ -290,10 +290,10 @@ def test_stack_validation(eb):
     ops = (eb.eb_qlinear_op * 2)()
     ops[0] = eb.eb_qlinear_op(_w(eb), X, Y, 1, eb.EB_F16, eb.EB_F32)
     ops[1] = eb.eb_qlinear_op(_w(eb, k=33), X, Y, 1, eb.EB_F16, eb.EB_F32)
-    assert eb.lib.eb_qlinear_stack(ops, 2, None) == -1   # second op invalid -> nothing launched
-    assert eb.lib.eb_qlinear_stack(ops, 0, None) == 0
-    assert eb.lib.eb_qlinear_stack(ops, -1, None) == -1
-    assert eb.lib.eb_qlinear_stack(None, 3, None) == -1
+    assert eb.lib.eb_qlinear_stack(ops, 2, None, 0, None) == -1   # second op invalid -> nothing launched
+    assert eb.lib.eb_qlinear_stack(ops, 0, None, 0, None) == 0
+    assert eb.lib.eb_qlinear_stack(ops, -1, None, 0, None) == -1
+    assert eb.lib.eb_qlinear_stack(None, 3, None, 0, None) == -1
 
 
 def test_auto_path(eb):
@@ -374,28 +374,92 @@ def test_stack_breaks_runs_on_format_and_m(eb, monkeypatch):
     assert _launches(eb, bad) == eb.EB_ERR_INVALID
 
 
-def test_mfma_force_validation(eb):
+def test_tuned_validation(eb):
+    """eb_qlinear_tuned (include/eb_tuning.h) takes the tile and split per
+    call and rejects values out of range on the host."""
     count = eb.lib.eb_mfma_tile_count()
     assert count >= 1
-    f = eb.lib.eb_mfma_force
-    assert f(-2, 0) == eb.EB_ERR_INVALID
-    assert f(count, 0) == eb.EB_ERR_INVALID
-    assert f(0, 17) == eb.EB_ERR_INVALID
-    assert f(0, -1) == eb.EB_ERR_INVALID
-    assert f(-1, 0) == eb.EB_OK
+    op = eb.eb_qlinear_op(_w(eb), X, Y, 64, eb.EB_F16, eb.EB_F32)
+    f = eb.lib.eb_qlinear_tuned
+    for tile, splits in ((-2, 0), (count, 0), (0, 17), (0, -1)):
+        assert f(ctypes.byref(op), tile, splits, None, 0, None) == eb.EB_ERR_INVALID
+    assert f(None, -1, 0, None, 0, None) == eb.EB_ERR_INVALID
+
+
+def test_no_process_wide_setters_in_the_abi():
+    """The public header declares no setter of global state (the tile / split
+    choice is a per-call argument of the tuning header)."""
+    names = declared_functions()
+    assert not [n for n in names if "force" in n or n.startswith("eb_set")], names
+    assert "eb_qlinear_tuned" not in names  # tuning entry points live in eb_tuning.h
+
+
+def test_library_imports_no_allocator(eb):
+    """libeb.so allocates no device or host memory through the HIP runtime:
+    its dynamic symbol table references no HIP allocation or free routine
+    (the caller passes every buffer and workspace)."""
+    import subprocess
+
+    out = subprocess.run(["nm", "-D", "--undefined-only", eb.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    hip = sorted({line.split()[-1] for line in out.splitlines() if "hip" in line.lower()})
+    assert hip, "expected HIP runtime imports"
+    alloc = [n for n in hip if re.search(r"malloc|free|alloc", n, re.I)]
+    assert not alloc, alloc
 
 
 def test_stack_counts_split_k_reduction(eb):
-    # a long-k MFMA op: one launch unsplit, two (GEMM + reduction) when split
-    op = [_op(eb, 1 * GB, 8 * GB, 9 * GB, k=16384, n=2048, m=816, qtype=eb.EB_Q8_0,
-              xt=eb.EB_BF16)]
-    try:
-        assert eb.lib.eb_mfma_force(-1, 1) == eb.EB_OK
-        assert _launches(eb, op) == 1
-        assert eb.lib.eb_mfma_force(-1, 4) == eb.EB_OK
-        assert _launches(eb, op) == 2
-    finally:
-        eb.lib.eb_mfma_force(-1, 0)
+    # a long-k op at m = 50 is split (product + ordered reduction); a large
+    # prefill op fills the GPU unsplit
+    split = [_op(eb, 1 * GB, 8 * GB, 9 * GB, k=4096, n=1024, m=50, qtype=eb.EB_Q8_0,
+                 xt=eb.EB_BF16)]
+    assert _launches(eb, split) == 2
+    whole = [_op(eb, 1 * GB, 8 * GB, 9 * GB, k=3072, n=9216, m=4096, qtype=eb.EB_Q4_0,
+                 xt=eb.EB_BF16)]
+    assert _launches(eb, whole) == 1
+
+
+def test_workspace_sizes(eb):
+    """Workspace queries: none for the GEMV path, normalised activations plus
+    split-K partial sums on the MFMA path, tables and buffers for a stack."""
+    q = eb.lib.eb_qlinear_workspace_bytes
+    gemv = eb.eb_qlinear_op(_w(eb, k=4096, n=4096), 8 * GB, 9 * GB, 1, eb.EB_F16, eb.EB_F32)
+    assert q(ctypes.byref(gemv), eb.EB_PATH_AUTO) == 0
+    plain = eb.eb_qlinear_op(_w(eb, k=4096, n=1024, data=1 * GB), 8 * GB, 9 * GB, 50, eb.EB_BF16,
+                             eb.EB_F32)
+    partial = q(ctypes.byref(plain), eb.EB_PATH_AUTO)
+    assert partial > 0 and partial % 256 == 0  # split along k: fp32 partials
+    normed = eb.eb_qlinear_op(_w(eb, k=4096, n=1024, data=1 * GB), 8 * GB, 9 * GB, 50, eb.EB_BF16,
+                              eb.EB_F32, eb.EB_PRO_RMSNORM, 0, G, None, 1e-5, 0)
+    assert q(ctypes.byref(normed), eb.EB_PATH_AUTO) == partial + 50 * 4096 * 2
+    bad = eb.eb_qlinear_op(_w(eb, k=33), X, Y, 4, eb.EB_F16, eb.EB_F32)
+    assert q(ctypes.byref(bad), eb.EB_PATH_AUTO) == 0
+    # a fused run of small-m ops needs its table (and nothing else)
+    ops = [_op(eb, 1 * GB + i * (64 << 20), 8 * GB + i * (1 << 20), 9 * GB + i * (1 << 20),
+               k=1024, n=2048, m=50, qtype=eb.EB_Q8_0, xt=eb.EB_BF16) for i in range(8)]
+    arr = (eb.eb_qlinear_op * len(ops))(*ops)
+    sb = eb.lib.eb_qlinear_stack_workspace_bytes(arr, len(ops))
+    assert 0 < sb < 8 * 1024 and sb % 256 == 0
+    assert eb.lib.eb_qlinear_stack_workspace_bytes(arr, 0) == 0
+
+
+def test_workspace_validation(eb):
+    """A workspace must be 256-byte aligned, overlap no operand, and be given
+    whenever its size is; a prologue on the MFMA path needs one."""
+    f = eb.lib.eb_qlinear_fused_ws
+    op = eb.eb_qlinear_op(_w(eb, k=4096, n=1024, data=1 * GB), 8 * GB, 9 * GB, 50, eb.EB_BF16,
+                          eb.EB_F32)
+    assert f(ctypes.byref(op), eb.EB_PATH_AUTO, 10 * GB + 64, 1 << 20, None) == eb.EB_ERR_ALIGN
+    assert f(ctypes.byref(op), eb.EB_PATH_AUTO, None, 4096, None) == eb.EB_ERR_INVALID
+    assert f(ctypes.byref(op), eb.EB_PATH_AUTO, 8 * GB, 1 << 20, None) == eb.EB_ERR_INVALID  # on x
+    assert f(ctypes.byref(op), eb.EB_PATH_AUTO, 1 * GB, 1 << 20, None) == eb.EB_ERR_INVALID  # on w
+    normed = eb.eb_qlinear_op(_w(eb, k=4096, n=1024, data=1 * GB), 8 * GB, 9 * GB, 50, eb.EB_BF16,
+                              eb.EB_F32, eb.EB_PRO_RMSNORM, 0, G, None, 1e-5, 0)
+    assert eb.lib.eb_qlinear_fused(ctypes.byref(normed), eb.EB_PATH_MFMA, None) == eb.EB_ERR_UNSUPPORTED
+    assert f(ctypes.byref(normed), eb.EB_PATH_MFMA, 10 * GB, 4096, None) == eb.EB_ERR_UNSUPPORTED
+    arr = (eb.eb_qlinear_op * 1)(op)
+    assert eb.lib.eb_qlinear_stack(arr, 1, 10 * GB + 8, 4096, None) == eb.EB_ERR_ALIGN
+    assert eb.lib.eb_qlinear_stack(arr, 1, None, 4096, None) == eb.EB_ERR_INVALID
 
 
 def test_stack_fuses_independent_small_m_mfma_ops(eb, monkeypatch):

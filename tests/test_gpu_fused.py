@@ -72,11 +72,11 @@ class Case:
         self.gd = self.gamma.to(DEV) if self.gamma is not None else None
         self.rd = self.r.to(DEV) if self.r is not None else None
 
-    def run(self, eb, path="auto", out=None, residual=None):
+    def run(self, eb, path="auto", out=None, residual=None, splits=0):
         return eb.qlinear_fused(self.qw, self.xd, out_dtype=self.ydtype, x_dtype=self.xdtype,
                                 prologue=self.pro, norm_weight=self.gd, eps=1e-5,
                                 epilogue=self.epi, residual=self.rd if residual is None else residual,
-                                path=path, out=out)
+                                path=path, out=out, splits=splits)
 
     def reference(self, orc, rows=None):
         blocks = orc.quantize(QT[self.qtype], self.w.numpy(), nthreads=O.available_cores())
@@ -108,11 +108,7 @@ def test_fused_single_calls(eb, oracle, pro, epi, qtype, xdtype, ydtype):
     n, k = 198, 1184
     for m, path, splits in ((1, "gemv", 0), (3, "gemv", 0), (20, "mfma", 0), (150, "mfma", 4)):
         c = Case(eb, 1000 + m, qtype, n, k, m, xdtype, pro, epi, ydtype)
-        eb.mfma_force(-1, splits)
-        try:
-            y = c.run(eb, path)
-        finally:
-            eb.mfma_force(-1, 0)
+        y = c.run(eb, path, splits=splits)
         torch.cuda.synchronize()
         y_ref, scale = c.reference(oracle)
         assert_fused(y, y_ref, scale, f"fused_{pro}_{epi} {qtype} m={m} {path} splits={splits}")

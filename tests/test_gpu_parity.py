@@ -12,7 +12,7 @@ import torch
 
 from oracle import oracle as O
 from paper_2607_02501_amd import workloads as W
-from tests.gpu_helpers import TOL_BF16, TOL_F32, assert_parity, bits16, oracle_reference
+from tests.gpu_helpers import TOL_BF16, TOL_F32, TOL_TILE_BF16, assert_parity, bits16, oracle_reference
 
 pytestmark = pytest.mark.gpu
 
@@ -128,42 +128,34 @@ def test_qlinear_mfma_parity(eb, oracle, qtype, xdtype, n, k):
     assert_parity(y, y_ref, bound, TOL_BF16, "mfma bf16 out")
 
 
-@pytest.fixture
-def forced(eb):
-    """eb.mfma_force, restored to the automatic choice afterwards."""
-    yield eb.mfma_force
-    eb.mfma_force(-1, 0)
-
-
 @pytest.mark.parametrize("qtype,xdtype", [("q8_0", torch.bfloat16), ("q4_0", torch.float16),
                                           ("q4_0", torch.bfloat16)])
-def test_every_mfma_tile_and_split(eb, oracle, forced, qtype, xdtype):
+def test_every_mfma_tile_and_split(eb, oracle, qtype, xdtype):
     # ragged m and n for every tile shape, an odd block count (K tail), 33 K-tiles
     m, n, k = 300, 520, 2080
     w, x = _case(77, n, k, m, xdtype)
     qw = eb.quantize(w.to(DEV), qtype)
     _, y_ref, bound = oracle_reference(oracle, qtype, w.numpy(), x)
     xd = x.to(DEV)
+    tol = TOL_TILE_BF16 if xdtype == torch.bfloat16 else TOL_F32
     for tile in range(eb.mfma_tile_count()):
         for splits in (1, 3):
-            forced(tile, splits)
-            y = eb.qlinear(qw, xd, path="mfma")
-            assert_parity(y, y_ref, bound, TOL_F32, f"tile {tile} splits {splits}")
-        forced(tile, 4)
-        y = eb.qlinear(qw, xd[:70], out_dtype=torch.bfloat16, path="mfma")
+            y = eb.qlinear_tuned(qw, xd, tile, splits)
+            assert_parity(y, y_ref, bound, tol, f"tile {tile} splits {splits}")
+        # m = 70: bfloat16 activations take the hi/lo tiles (the forced tile
+        # applies where it has them)
+        y = eb.qlinear_tuned(qw, xd[:70], tile, 4, out_dtype=torch.bfloat16)
         assert_parity(y, y_ref[:70], bound[:70], TOL_BF16, f"tile {tile} splits 4 bf16 out")
 
 
-def test_split_k_deterministic_and_matches_unsplit(eb, forced):
+def test_split_k_deterministic_and_matches_unsplit(eb):
     n, k = 384, 8192
     w, x = _case(43, n, k, 96, torch.bfloat16)
     qw = eb.quantize(w.to(DEV), "q8_0")
     xd = x.to(DEV)
-    forced(1, 1)
-    whole = eb.qlinear(qw, xd, path="mfma")
-    forced(1, 6)
-    a = eb.qlinear(qw, xd, path="mfma")
-    b = eb.qlinear(qw, xd, path="mfma")
+    whole = eb.qlinear_tuned(qw, xd, 1, 1)
+    a = eb.qlinear_tuned(qw, xd, 1, 6)
+    b = eb.qlinear_tuned(qw, xd, 1, 6)
     assert torch.equal(a, b)
     # same products, summed in another order: close, not necessarily equal
     scale = (x.float().abs() @ w.abs().t()).to(DEV)
@@ -378,17 +370,15 @@ def test_grouped_mfma_stack(eb, oracle, qtype, xdtype, ms, monkeypatch):
         for a, b in zip(first, outs):
             assert torch.equal(a, b), (mode, overlap)
     monkeypatch.delenv("EB_STACK_OVERLAP_TAIL", raising=False)
-    eb.mfma_force(-1, 1)
-    try:
-        for (w, x), (qw, xd, y) in zip(cases, entries):
-            tol = TOL_F32 if y.dtype == torch.float32 else TOL_BF16
-            _, y_ref, bound = oracle_reference(oracle, qtype, w.numpy(), x)
-            assert_parity(y, y_ref, bound, tol, f"grouped m={x.shape[0]}")
-            single = eb.qlinear(qw, xd, out_dtype=y.dtype, path="mfma")
-            scale = torch.from_numpy(bound).to(DEV).float().clamp_min(1e-30)
-            assert float(((y.float() - single.float()).abs() / scale).max()) <= 2 * tol
-    finally:
-        eb.mfma_force(-1, 0)
+    for (w, x), (qw, xd, y) in zip(cases, entries):
+        tol = TOL_F32 if y.dtype == torch.float32 else TOL_BF16
+        if xdtype == torch.bfloat16:
+            tol += TOL_TILE_BF16 - TOL_F32
+        _, y_ref, bound = oracle_reference(oracle, qtype, w.numpy(), x)
+        assert_parity(y, y_ref, bound, tol, f"grouped m={x.shape[0]}")
+        single = eb.qlinear_tuned(qw, xd, -1, 1, out_dtype=y.dtype)
+        scale = torch.from_numpy(bound).to(DEV).float().clamp_min(1e-30)
+        assert float(((y.float() - single.float()).abs() / scale).max()) <= 2 * tol
     eb.stack_cache_clear()
 
 
