@@ -192,6 +192,24 @@ eb_status eb_qweights_to_canonical(const eb_qweights *w, void *dst, hipStream_t 
 eb_status eb_qweights_from_canonical(int32_t type, const void *src, int64_t n, int64_t k,
                                      void *out, hipStream_t stream);
 
+/* eb_qlinear_fused_ws for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the scratch of the MFMA path -- the normalised activations of
+ * a prologue, then the fp32 partial sums of a split of k -- lives in a
+ * static device array of 32 MiB that the library holds on every GPU it runs
+ * on until the process ends (its address is resolved on the first call on
+ * each device).  No allocating routine is called.  The normalised
+ * activations must fit the array (m * k * 2 bytes, rounded up to 256;
+ * otherwise EB_ERR_UNSUPPORTED and nothing is launched); a split of k is
+ * taken only when its partial sums fit the rest.  Nothing in the array needs
+ * to start at zero (every element read is written earlier in the same call).
+ * Every call on one GPU shares that GPU's array: calls that overlap in time
+ * on one GPU (other streams, other threads, a graph replayed while another
+ * call runs) race on it and give undefined results; calls on one stream are
+ * ordered and safe.  Errors as eb_qlinear_fused, plus EB_ERR_HIP if the
+ * array's device address cannot be resolved. */
+eb_status eb_qlinear_fused_static(const eb_qlinear_op *op, int32_t path, hipStream_t stream);
+
 /* y[m][n] = x[m][k] . w_hat[n][k]^T with fp32 accumulation, on the path chosen
  * automatically, with no workspace: the MFMA path then runs unsplit (see
  * eb_qlinear_fused_ws for the split of k a workspace allows).

@@ -837,6 +837,40 @@ eb_status run_ops_direct(const eb_qlinear_op *ops, int32_t n_ops, uint8_t *ws, s
   return EB_OK;
 }
 
+// ---------------------------------------------------------------------------
+// Scratch for callers that cannot allocate (code under HIP graph capture,
+// serving loops, harnesses that forbid allocation): one file-scope device
+// array per GPU, of kStaticScratchBytes, that eb_qlinear_fused_static uses
+// instead of a caller workspace.  Its device address is looked up once per
+// device, with that device current; host code never uses the array's name
+// as an address (in host code it is only a stand-in for the symbol).
+// ---------------------------------------------------------------------------
+constexpr size_t kStaticScratchBytes = size_t(32) << 20;
+static __device__ __align__(256) uint8_t scratch[kStaticScratchBytes];
+
+struct StaticScratch {
+  std::once_flag once[64];
+  uint8_t *ptr[64] = {};
+  hipError_t err[64] = {};
+};
+
+StaticScratch &static_scratch_state() {
+  static StaticScratch *s = new StaticScratch();  // leaked on purpose: no teardown-order issues
+  return *s;
+}
+
+// This device's scratch array (dev is the current device), or nullptr if the
+// runtime could not resolve it.
+uint8_t *static_scratch(int dev) {
+  StaticScratch &S = static_scratch_state();
+  std::call_once(S.once[dev], [&] {
+    void *p = nullptr;
+    S.err[dev] = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (S.err[dev] == hipSuccess && p) S.ptr[dev] = static_cast<uint8_t *>(p);
+  });
+  return S.ptr[dev];
+}
+
 }  // namespace
 }  // namespace eb
 
@@ -930,6 +964,21 @@ eb_status eb_qlinear_fused_ws(const eb_qlinear_op *op, int32_t path, void *works
   st = check_workspace(op, 1, workspace, workspace_bytes);
   if (st != EB_OK) return st;
   return launch_op(*op, path, static_cast<uint8_t *>(workspace), workspace_bytes, stream);
+}
+
+eb_status eb_qlinear_fused_static(const eb_qlinear_op *op, int32_t path, hipStream_t stream) {
+  if (!op) return EB_ERR_INVALID;
+  eb_status st = check_op(*op, path);
+  if (st != EB_OK) return st;
+  if (op->m == 0) return EB_OK;
+  const int32_t p =
+      path == EB_PATH_AUTO ? pick_path(op->w.type, op->x_type, op->m, op->w.n, op->w.k) : path;
+  if (p == EB_PATH_MFMA && xhat_bytes(*op) > kStaticScratchBytes) return EB_ERR_UNSUPPORTED;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return EB_ERR_HIP;
+  uint8_t *ws = static_scratch(dev);
+  if (!ws) return EB_ERR_HIP;
+  return launch_op(*op, p, ws, kStaticScratchBytes, stream);
 }
 
 eb_status eb_qlinear(const eb_qweights *w, const void *x, int32_t x_type, int64_t m, void *y,

@@ -102,6 +102,8 @@ lib.eb_qlinear_workspace_bytes.restype = ctypes.c_size_t
 lib.eb_qlinear_workspace_bytes.argtypes = [ctypes.POINTER(eb_qlinear_op), _i32]
 lib.eb_qlinear_fused_ws.restype = _i32
 lib.eb_qlinear_fused_ws.argtypes = [ctypes.POINTER(eb_qlinear_op), _i32, _vp, ctypes.c_size_t, _vp]
+lib.eb_qlinear_fused_static.restype = _i32
+lib.eb_qlinear_fused_static.argtypes = [ctypes.POINTER(eb_qlinear_op), _i32, _vp]
 lib.eb_qlinear_tuned.restype = _i32
 lib.eb_qlinear_tuned.argtypes = [ctypes.POINTER(eb_qlinear_op), _i32, _i32, _vp, ctypes.c_size_t, _vp]
 lib.eb_qlinear_stack_launches.restype = _i32
