@@ -16,14 +16,17 @@
 //     per-unit offset (see below);
 //   * the 16 partial sums of a row are added with four DPP steps.
 //
-// In-register dequantization never materialises the signed codes.  A 4-bit
-// code n (stored value c + 8) OR-ed into the mantissa of binary16 1024.0 reads
-// as 1024 + n; OR-ed one nibble higher it reads 1024 + 16 n.  For int8 codes q,
-// (q ^ 0x80) = q + 128 is placed the same way.  v_dot2_f32_f16 then multiplies
-// exact pairs, and the constant part (e.g. 1032 * sum x) is removed once per
-// unit with an offset precomputed from x in binary64 when x is staged.  For
-// bfloat16 activations the magic constant is bfloat16 128.0 (4-bit codes) or
-// the codes are converted to fp32 (8-bit codes).
+// In-register dequantization.  A 4-bit code n (stored value c + 8) OR-ed into
+// the mantissa of binary16 1024.0 reads as 1024 + n; OR-ed one nibble higher
+// it reads 1024 + 16 n.  For int8 codes q, (q ^ 0x80) = q + 128 is placed the
+// same way.  With binary16 activations one packed binary16 add per pair then
+// subtracts 1032, 1152 (or 1152) exactly, leaving the signed codes c (16 c), and
+// v_dot2_f32_f16 multiplies exact pairs: the fp32 sum only ever holds
+// products c x, so its rounding error is relative to sum |x||c|.  For bfloat16
+// activations the magic constant is bfloat16 128.0 (4-bit codes) or the codes
+// are converted to fp32 (8-bit codes), and the constant part (e.g. 136 * sum x)
+// is removed once per unit with an offset precomputed from x in binary64 when
+// x is staged.
 #include <hip/hip_runtime.h>
 
 #include <cstdio>
@@ -85,27 +88,35 @@ __device__ inline uint32_t and_or(uint32_t a, uint32_t mask, uint32_t magic) {
   return (a & mask) | magic;
 }
 
-// Sum over one unit of (stored code value with the magic offset) * x, minus
-// the precomputed offset: returns sum_j code_j * x_j for the unit.
+// Sum over one unit of code_j * x_j (bfloat16 x: of (stored code value with
+// the magic offset) * x_j, minus the precomputed offset `off`; binary16 x
+// needs no offset and ignores it).
 template <int QT, int XT>
 __device__ inline float unit_dot(const uint4 q, const uint4 *xc, float off);
+
+// two binary16 values 1024 + v (or 1024 + 16 v) -> v - z exactly (one v_pk_add_f16)
+__device__ inline uint32_t sub_h2(uint32_t h2, _Float16 z) {
+  const half2_t r = __builtin_bit_cast(half2_t, h2) - half2_t{z, z};
+  return __builtin_bit_cast(uint32_t, r);
+}
 
 // Q4_0, binary16 x.  x chunk i = pairs (x4i,x4i+2) (x4i+1,x4i+3) (x16+4i,x16+4i+2) (x16+4i+1,x16+4i+3)
 template <>
 __device__ inline float unit_dot<EB_Q4_0, EB_F16>(const uint4 q, const uint4 *xc, float off) {
+  (void)off;
   const uint32_t w[4] = {q.x, q.y, q.z, q.w};
   const uint32_t mlo = 0x000F000Fu, mhi = 0x00F000F0u, magic = vconst(0x64006400u);
   float lo = 0.f, hi = 0.f;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const uint32_t v = w[i], v8 = w[i] >> 8;
-    lo = dot2h(and_or(v, mlo, magic), xc[i].x, lo);
-    lo = dot2h(and_or(v8, mlo, magic), xc[i].y, lo);
-    hi = dot2h(and_or(v, mhi, magic), xc[i].z, hi);
-    hi = dot2h(and_or(v8, mhi, magic), xc[i].w, hi);
+    // low nibbles read 1024 + n = c + 1032, high nibbles 1024 + 16 n = 16 c + 1152
+    lo = dot2h(sub_h2(and_or(v, mlo, magic), (_Float16)1032.0f), xc[i].x, lo);
+    lo = dot2h(sub_h2(and_or(v8, mlo, magic), (_Float16)1032.0f), xc[i].y, lo);
+    hi = dot2h(sub_h2(and_or(v, mhi, magic), (_Float16)1152.0f), xc[i].z, hi);
+    hi = dot2h(sub_h2(and_or(v8, mhi, magic), (_Float16)1152.0f), xc[i].w, hi);
   }
-  // lo terms are (c + 1032) x, hi terms (16 c + 1152) x
-  return __builtin_fmaf(hi, 0.0625f, lo) - off;
+  return __builtin_fmaf(hi, 0.0625f, lo);  // hi holds 16 c x
 }
 
 // Q4_0, bfloat16 x: bfloat16 128.0 | nibble = 128 + n = c + 136.
@@ -128,16 +139,17 @@ __device__ inline float unit_dot<EB_Q4_0, EB_BF16>(const uint4 q, const uint4 *x
 // Q8_0 half block, binary16 x: (q ^ 0x80) placed under 0x64 reads 1024 + q + 128.
 template <>
 __device__ inline float unit_dot<EB_Q8_0, EB_F16>(const uint4 q, const uint4 *xc, float off) {
+  (void)off;
   const uint32_t w[4] = {q.x, q.y, q.z, q.w};
   const uint32_t xs[8] = {xc[0].x, xc[0].y, xc[0].z, xc[0].w, xc[1].x, xc[1].y, xc[1].z, xc[1].w};
   float a = 0.f, b = 0.f;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const uint32_t u = w[i] ^ 0x80808080u;
-    a = dot2h(__builtin_amdgcn_perm(0x64646464u, u, 0x04020400u), xs[2 * i], a);
-    b = dot2h(__builtin_amdgcn_perm(0x64646464u, u, 0x04030401u), xs[2 * i + 1], b);
+    a = dot2h(sub_h2(__builtin_amdgcn_perm(0x64646464u, u, 0x04020400u), (_Float16)1152.0f), xs[2 * i], a);
+    b = dot2h(sub_h2(__builtin_amdgcn_perm(0x64646464u, u, 0x04030401u), (_Float16)1152.0f), xs[2 * i + 1], b);
   }
-  return (a + b) - off;
+  return a + b;
 }
 
 // Q8_0 half block, bfloat16 x (natural order): codes via fp32 byte conversion.
@@ -168,7 +180,7 @@ __device__ inline double x_to_f64(uint32_t h) {
 // mean_j h[i][j]^2) for the m <= MT rows of the fp32 residual stream h, in
 // every thread of the workgroup.  Each thread sums the squares of a strided
 // part of every row in fp32; the 64 lanes of a wave, then the waves (through
-// `red`, kWaves * MT floats of LDS), are added in a fixed order.  Ends with a
+// `red`, (waves per workgroup) * MT floats of LDS), are added in a fixed order.  Ends with a
 // barrier after which `red` may be reused.
 template <int MT>
 __device__ inline void norm_factors(const float *__restrict__ h, int m, int64_t k, float eps,
@@ -195,7 +207,7 @@ __device__ inline void norm_factors(const float *__restrict__ h, int m, int64_t 
 #pragma unroll
   for (int mm = 0; mm < MT; ++mm) {
     float ss = 0.f;
-    for (int w = 0; w < kWaves; ++w) ss += red[w * MT + mm];
+    for (int w = 0; w < (int)(blockDim.x >> 6); ++w) ss += red[w * MT + mm];
     rs[mm] = 1.0f / __builtin_sqrtf(ss / (float)k + eps);
   }
   __syncthreads();
@@ -271,7 +283,7 @@ __device__ __attribute__((always_inline)) inline void stage_x(
         out[i] = make_uint4((a & 0xffffu) | (b << 16), (a >> 16) | (b & 0xffff0000u),
                             (c & 0xffffu) | (d << 16), (c >> 16) | (d & 0xffff0000u));
       }
-      off = (XT == EB_F16) ? 1032.0 * s_lo + 72.0 * s_hi : 136.0 * (s_lo + s_hi);
+      off = (XT == EB_F16) ? 0.0 : 136.0 * (s_lo + s_hi);
     } else {
       if (XT == EB_F16) {
 #pragma unroll
@@ -280,7 +292,7 @@ __device__ __attribute__((always_inline)) inline void stage_x(
           out[c] = make_uint4((a & 0xffffu) | (b << 16), (a >> 16) | (b & 0xffff0000u),
                               (e & 0xffffu) | (f << 16), (e >> 16) | (f & 0xffff0000u));
         }
-        off = 1152.0 * s_lo;
+        off = 0.0;
       } else {
 #pragma unroll
         for (int c = 0; c < 2; ++c) out[c] = make_uint4(r[4 * c], r[4 * c + 1], r[4 * c + 2], r[4 * c + 3]);
@@ -290,6 +302,97 @@ __device__ __attribute__((always_inline)) inline void stage_x(
 #pragma unroll
     for (int c = 0; c < CH; ++c) xs[((int64_t)mm * CH + c) * pitch + u] = out[c];
     xoff[(int64_t)mm * pitch + u] = (float)off;
+  }
+}
+
+// m == 1, binary16 activations: stage the row into LDS for m1_rows in one
+// pass.  One thread per 16-byte chunk of the staged row: chunk (unit u, part
+// i) holds the pairs (a0,a2) (a1,a3) (b0,b2) (b1,b3) of a = x[e0 .. e0+3],
+// b = x[e1 .. e1+3] (Q4_0: e0 = 32 u + 4 i, e1 = e0 + 16; Q8_0: e0 = 16 u +
+// 8 i, e1 = e0 + 4), stored at xs[i * P + u].  With the normalisation
+// prologue the thread's h values (first two chunks) stay in registers between
+// the sum of squares and the normalisation, so h is read from memory once;
+// the sum is reduced over the wave by exchanges and over the waves in order
+// through `red` (one float per wave, not aliasing xs).
+template <int QT>
+__device__ __attribute__((always_inline)) inline void stage_x1_f16(
+    const void *__restrict__ xv, int64_t k, int ku, uint4 *xs, int P, bool norm,
+    const float *__restrict__ gamma, float eps, float *red) {
+  constexpr int CH = Unit<QT>::kChunks;
+  const int nch = ku * CH, T = (int)blockDim.x, tid = (int)threadIdx.x;
+  auto first = [](int c, int &u, int &i, int &e0, int &e1) __attribute__((always_inline)) {
+    u = c / CH;
+    i = c - u * CH;
+    e0 = (QT == EB_Q4_0) ? u * 32 + 4 * i : u * 16 + 8 * i;
+    e1 = e0 + ((QT == EB_Q4_0) ? 16 : 4);
+  };
+  auto put = [&](int u, int i, float4 a, float4 b) __attribute__((always_inline)) {
+    xs[i * P + u] = make_uint4(pack_x16<EB_F16>(a.x, a.z), pack_x16<EB_F16>(a.y, a.w),
+                               pack_x16<EB_F16>(b.x, b.z), pack_x16<EB_F16>(b.y, b.w));
+  };
+  if (!norm) {
+    const uint16_t *x = static_cast<const uint16_t *>(xv);
+    for (int c = tid; c < nch; c += T) {
+      int u, i, e0, e1;
+      first(c, u, i, e0, e1);
+      const uint2 a = *reinterpret_cast<const uint2 *>(x + e0);
+      const uint2 b = *reinterpret_cast<const uint2 *>(x + e1);
+      // (a0 a1)(a2 a3) -> (a0 a2)(a1 a3)
+      xs[i * P + u] = make_uint4((a.x & 0xffffu) | (a.y << 16), (a.x >> 16) | (a.y & 0xffff0000u),
+                                 (b.x & 0xffffu) | (b.y << 16), (b.x >> 16) | (b.y & 0xffff0000u));
+    }
+    return;
+  }
+  const float *h = static_cast<const float *>(xv);
+  float4 ha[2], hb[2];
+  float ss = 0.f;
+  auto sq = [](float acc, float4 v) __attribute__((always_inline)) {
+    acc = __builtin_fmaf(v.x, v.x, acc);
+    acc = __builtin_fmaf(v.y, v.y, acc);
+    acc = __builtin_fmaf(v.z, v.z, acc);
+    return __builtin_fmaf(v.w, v.w, acc);
+  };
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int c = tid + j * T;
+    if (c < nch) {
+      int u, i, e0, e1;
+      first(c, u, i, e0, e1);
+      ha[j] = *reinterpret_cast<const float4 *>(h + e0);
+      hb[j] = *reinterpret_cast<const float4 *>(h + e1);
+      ss = sq(sq(ss, ha[j]), hb[j]);
+    }
+  }
+  for (int c = tid + 2 * T; c < nch; c += T) {
+    int u, i, e0, e1;
+    first(c, u, i, e0, e1);
+    ss = sq(sq(ss, *reinterpret_cast<const float4 *>(h + e0)), *reinterpret_cast<const float4 *>(h + e1));
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) ss += __shfl_xor(ss, o);
+  if ((tid & 63) == 0) red[tid >> 6] = ss;
+  __syncthreads();
+  float tot = 0.f;
+  for (int w = 0; w < (T >> 6); ++w) tot += red[w];
+  const float r = 1.0f / __builtin_sqrtf(tot / (float)k + eps);
+  auto normed = [&](float4 v, const float *g) __attribute__((always_inline)) {
+    const float4 gg = *reinterpret_cast<const float4 *>(g);
+    return make_float4(v.x * gg.x * r, v.y * gg.y * r, v.z * gg.z * r, v.w * gg.w * r);
+  };
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int c = tid + j * T;
+    if (c < nch) {
+      int u, i, e0, e1;
+      first(c, u, i, e0, e1);
+      put(u, i, normed(ha[j], gamma + e0), normed(hb[j], gamma + e1));
+    }
+  }
+  for (int c = tid + 2 * T; c < nch; c += T) {
+    int u, i, e0, e1;
+    first(c, u, i, e0, e1);
+    put(u, i, normed(*reinterpret_cast<const float4 *>(h + e0), gamma + e0),
+        normed(*reinterpret_cast<const float4 *>(h + e1), gamma + e1));
   }
 }
 
@@ -454,9 +557,11 @@ __device__ inline float reduce_rows(const float (&v)[R], int lane, int &row, boo
     writer = (lane & 31) == 0;
     return a;
   } else {
-    float a = red16(v[0]);
+    // the association of R == 2 for its first row (lanes l and l + 32, then
+    // 16-lane rows, then the two halves), so one- and two-row launches give
+    // the same bits for a row
+    float a = red16(swap32(v[0], v[0]));
     a = swap16(a, a);
-    a = swap32(a, a);
     row = 0;
     writer = lane == 0;
     return a;
@@ -481,7 +586,7 @@ __device__ inline __amdgpu_buffer_rsrc_t rsrc(const void *base, uint32_t bytes) 
 // matrix, m == 1.  Called by every thread of the workgroup (it stages x into
 // LDS and synchronises once); waves whose first group is past g_end only help
 // with the staging.
-template <int QT, int XT, int NS, int R>
+template <int QT, int XT, int NS, int R, int PD>
 __device__ __attribute__((always_inline)) inline void m1_rows(const uint8_t *__restrict__ wdata, int64_t n, int64_t k,
                                int64_t d_off, int64_t ds, const void *__restrict__ x,
                                void *__restrict__ y, int yt, const Fuse &f, int64_t g, int64_t g_end,
@@ -511,9 +616,18 @@ __device__ __attribute__((always_inline)) inline void m1_rows(const uint8_t *__r
     xidx[s] = u < ku ? (uint32_t)u : 64u * NS;
   }
 
-  uint4 q[NS][R];
-  uint16_t dh[NS][R];
-  auto load_group = [&](int64_t grp) __attribute__((always_inline)) {
+  // PD (1 to 4) register sets of weights: the group being computed and the
+  // next PD - 1, whose loads are in flight meanwhile, so a wave has PD groups
+  // of HBM reads outstanding (a lone launch has only a few groups per wave,
+  // and each round of one-group-at-a-time loads waits a full memory latency).
+  // As many sets as fit without spilling.
+  static_assert(PD >= 1 && PD <= 4, "1 to 4 weight register sets");
+  struct WSet {
+    uint4 q[NS][R];
+    uint16_t dh[NS][R];
+  };
+  WSet A, B, C, D;
+  auto load_group = [&](WSet &S, int64_t grp) __attribute__((always_inline)) {
 #pragma unroll
     for (int r = 0; r < R; ++r) {
       int64_t row = grp * R + r;
@@ -523,23 +637,33 @@ __device__ __attribute__((always_inline)) inline void m1_rows(const uint8_t *__r
 #pragma unroll
       for (int s = 0; s < NS; ++s) {
         const auto v = __builtin_amdgcn_raw_buffer_load_b128(rq, (int)qoff[s], 0, kNT);
-        q[s][r] = make_uint4(v[0], v[1], v[2], v[3]);
-        dh[s][r] = __builtin_amdgcn_raw_buffer_load_b16(rd, (int)doff[s], 0, kNT);
+        S.q[s][r] = make_uint4(v[0], v[1], v[2], v[3]);
+        S.dh[s][r] = __builtin_amdgcn_raw_buffer_load_b16(rd, (int)doff[s], 0, kNT);
       }
     }
   };
-  // weight loads of the first group are in flight while x is staged (and,
-  // with the prologue, normalised)
-  if (g < g_end) load_group(g);
-  float rs[1] = {0.f};
+  // weight loads of the first two groups are in flight while x is staged
+  // (and, with the prologue, normalised)
+  if (g < g_end) load_group(A, g);
+  if (PD >= 2 && g + gstride < g_end) load_group(B, g + gstride);
+  if (PD >= 3 && g + 2 * gstride < g_end) load_group(C, g + 2 * gstride);
+  if (PD >= 4 && g + 3 * gstride < g_end) load_group(D, g + 3 * gstride);
   const bool norm = f.pro == EB_PRO_RMSNORM;
-  if (norm) norm_factors<1>(static_cast<const float *>(x), 1, k, f.eps, reinterpret_cast<float *>(xs), rs);
-  stage_x<QT, XT, 1>(x, 1, k, ku, xs, xoff, P, norm, f.gamma, rs);
+  if constexpr (XT == EB_F16) {
+    stage_x1_f16<QT>(x, k, ku, xs, P, norm, f.gamma, f.eps, xoff);
+  } else {
+    float rs[1] = {0.f};
+    if (norm) norm_factors<1>(static_cast<const float *>(x), 1, k, f.eps, reinterpret_cast<float *>(xs), rs);
+    stage_x<QT, XT, 1>(x, 1, k, ku, xs, xoff, P, norm, f.gamma, rs);
+  }
   if (threadIdx.x < CH) xs[threadIdx.x * P + 64 * NS] = make_uint4(0, 0, 0, 0);
-  if (threadIdx.x == 0) xoff[64 * NS] = 0.f;
+  if (XT != EB_F16 && threadIdx.x == 0) xoff[64 * NS] = 0.f;
   __syncthreads();
 
-  while (g < g_end) {
+  // one group: compute it from set S, then reload S with the group two
+  // strides ahead; returns whether there was a group
+  auto step = [&](WSet &S) __attribute__((always_inline)) -> bool {
+    if (g >= g_end) return false;
     float acc[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) acc[r] = 0.f;
@@ -549,11 +673,11 @@ __device__ __attribute__((always_inline)) inline void m1_rows(const uint8_t *__r
       uint4 xf[CH];
 #pragma unroll
       for (int c = 0; c < CH; ++c) xf[c] = xp[c * P];
-      const float xo = xoff[xidx[s]];
+      const float xo = XT == EB_F16 ? 0.f : xoff[xidx[s]];
 #pragma unroll
       for (int r = 0; r < R; ++r)
-        acc[r] = __builtin_fmaf((float)__builtin_bit_cast(_Float16, dh[s][r]),
-                                unit_dot<QT, XT>(q[s][r], xf, xo), acc[r]);
+        acc[r] = __builtin_fmaf((float)__builtin_bit_cast(_Float16, S.dh[s][r]),
+                                unit_dot<QT, XT>(S.q[s][r], xf, xo), acc[r]);
     }
     int rr;
     bool writer;
@@ -572,23 +696,47 @@ __device__ __attribute__((always_inline)) inline void m1_rows(const uint8_t *__r
       if (writer && row < n) put_y(y, row, tot, yt, f);
     }
     g += gstride;
-    // the weight registers are free again: load the next group into them
+    // set S is free again: load the group PD strides ahead into it
     __builtin_amdgcn_sched_barrier(0);
-    if (g < g_end) load_group(g);
+    if (g + (PD - 1) * gstride < g_end) load_group(S, g + (PD - 1) * gstride);
+    return true;
+  };
+  if constexpr (PD == 4) {
+    while (step(A) && step(B) && step(C) && step(D)) {
+    }
+  } else if constexpr (PD == 3) {
+    while (step(A) && step(B) && step(C)) {
+    }
+  } else if constexpr (PD == 2) {
+    while (step(A) && step(B)) {
+    }
+  } else {
+    while (step(A)) {
+    }
   }
 }
 
 // One matrix per launch.  WPE: minimum waves per SIMD the register allocation
 // must allow; memory latency is hidden by other waves rather than by deep
-// per-wave prefetch.
-template <int QT, int XT, int NS, int R, int WPE>
-__global__ void __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(WPE)))
+// per-wave prefetch.  WG waves per workgroup: a lone launch has few row
+// groups per wave, so the per-workgroup staging of x (and the normalisation
+// prologue's reduction over the whole row) is a large part of it; with 16
+// waves per workgroup and one workgroup per CU it is done once per CU instead
+// of four times, and the 256 workgroups re-read the shared activations from
+// the L2 a quarter as often.
+template <int QT, int XT, int NS, int R, int WPE, int WG>
+__global__ void __launch_bounds__(64 * WG) __attribute__((amdgpu_waves_per_eu(WPE)))
     gemv_m1_kernel(const uint8_t *__restrict__ wdata, int64_t n, int64_t k, int64_t d_off,
                    int64_t ds, const void *__restrict__ x, void *__restrict__ y, int yt, Fuse f) {
   extern __shared__ uint4 smem[];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
-  m1_rows<QT, XT, NS, R>(wdata, n, k, d_off, ds, x, y, yt, f, (int64_t)blockIdx.x * kWaves + wave,
-                         (n + R - 1) / R, (int64_t)gridDim.x * kWaves, smem);
+  // two weight register sets where they fit next to the rest (measured: three
+  // or four sets per wave, with more reads in flight, made the decode layer's
+  // lone launches 5-15% slower)
+  constexpr int PD = NS * R <= 4 ? 2 : 1;
+  m1_rows<QT, XT, NS, R, PD>(wdata, n, k, d_off, ds, x, y, yt, f,
+                                                (int64_t)blockIdx.x * WG + wave, (n + R - 1) / R,
+                                                (int64_t)gridDim.x * WG, smem);
 }
 
 // Rows per wave for the fused multi-matrix kernel, by slot count (no spills
@@ -629,53 +777,58 @@ __global__ void __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_e
     };
     const int64_t r0 = row_at(u0), r1 = row_at(u1);
     if (r0 >= r1) continue;  // uniform across the workgroup
-    m1_rows<QT, XT, NS, R>(o.w, o.n, o.k, o.d_off, o.ds, o.x, o.y, o.yt, o.f, r0 / R + wave,
-                           (r1 + R - 1) / R, kWaves, smem);
+    m1_rows<QT, XT, NS, R, 1>(o.w, o.n, o.k, o.d_off, o.ds, o.x, o.y, o.yt, o.f, r0 / R + wave,
+                              (r1 + R - 1) / R, kWaves, smem);
     __syncthreads();  // the next matrix restages LDS
   }
 }
 
 // ---------------------------------------------------------------------------
-template <int QT, int XT, int NS, int R, int WPE>
+template <int QT, int XT, int NS, int R, int WPE, int WG>
 hipError_t launch_m1_t(const void *wdata, int64_t n, int64_t k, const void *x, void *y, int32_t yt,
                        const Fuse &f, hipStream_t s, int wg_per_cu) {
   const Layout L = layout_of(QT, n, k);
-  const int64_t ku = k / Unit<QT>::kElems;
   const size_t lds = (size_t)(64 * NS + 1) * (Unit<QT>::kChunks * 16 + 4);
-  (void)ku;
   const int64_t groups = (n + R - 1) / R;
-  int64_t grid = (groups + kWaves - 1) / kWaves;
+  int64_t grid = (groups + WG - 1) / WG;
   const int64_t cap = (int64_t)device_cu_count() * wg_per_cu;
   if (grid > cap) grid = cap;
-  gemv_m1_kernel<QT, XT, NS, R, WPE><<<(unsigned)grid, 64 * kWaves, lds, s>>>(
+  gemv_m1_kernel<QT, XT, NS, R, WPE, WG><<<(unsigned)grid, 64 * WG, lds, s>>>(
       (const uint8_t *)wdata, n, k, L.d_off, L.ds, x, y, yt, f);
   return hipGetLastError();
 }
 
 // Launch shape of the m == 1 kernel: rows per wave (R), minimum waves per
-// SIMD (WPE) and workgroups per CU.  The defaults are per slot count; the
-// environment variable EB_GEMV_M1="R,WPE,WGPERCU" overrides them (tuning).
+// SIMD (WPE), workgroups per CU and waves per workgroup.  The defaults are
+// per slot count; the environment variable EB_GEMV_M1="R,WPE,WGPERCU,WAVES"
+// overrides them (tuning; WAVES 4 or 16).
 struct M1Shape {
-  int r, wpe, wg;
+  int r, wpe, wg, waves;
 };
 
 M1Shape m1_shape(int64_t ns) {
   static const char *env = getenv("EB_GEMV_M1");
   if (env) {
-    M1Shape v{0, 0, 0};
-    if (sscanf(env, "%d,%d,%d", &v.r, &v.wpe, &v.wg) == 3 && v.r > 0 && v.wpe > 0 && v.wg > 0) return v;
+    M1Shape v{0, 0, 0, 0};
+    if (sscanf(env, "%d,%d,%d,%d", &v.r, &v.wpe, &v.wg, &v.waves) == 4 && v.r > 0 && v.wpe > 0 &&
+        v.wg > 0 && (v.waves == 4 || v.waves == 16))
+      return v;
   }
-  return {m1_multi_rows((int)ns), 4, 4};
+  return {1, 4, 1, 16};
 }
 
 template <int QT, int XT, int NS>
 hipError_t launch_m1_ns(const void *wdata, int64_t n, int64_t k, const void *x, void *y, int32_t yt,
                         const Fuse &f, hipStream_t s) {
-  const M1Shape v = m1_shape(NS);
-#define EB_M1(R_, W_)                                                                      \
-  if (v.r == R_ && v.wpe == W_)                                                           \
-    return launch_m1_t<QT, XT, NS, R_, W_>(wdata, n, k, x, y, yt, f, s, v.wg);
-  EB_M1(1, 4) EB_M1(2, 4) EB_M1(4, 4) EB_M1(1, 2) EB_M1(2, 2) EB_M1(4, 2)
+  // one row per wave by default (a 4096-row matrix then fills all 256 CUs
+  // with 16-wave workgroups), two for the gate/up product, which needs both
+  // rows of a pair in one wave
+  M1Shape v = m1_shape(NS);
+  if (f.epi == EB_EPI_GLU && v.r < 2) v.r = 2;
+#define EB_M1(R_, W_, G_)                                                                  \
+  if (v.r == R_ && v.wpe == W_ && v.waves == G_)                                          \
+    return launch_m1_t<QT, XT, NS, R_, W_, G_>(wdata, n, k, x, y, yt, f, s, v.wg);
+  EB_M1(1, 4, 16) EB_M1(2, 4, 16) EB_M1(1, 4, 4) EB_M1(2, 4, 4) EB_M1(4, 4, 4) EB_M1(2, 2, 4)
 #undef EB_M1
   return hipErrorInvalidValue;
 }
@@ -722,7 +875,9 @@ hipError_t launch_m(const void *wdata, int64_t n, int64_t k, const void *x, int6
                     int32_t yt, const Fuse &f, hipStream_t s) {
   const int64_t ns = (k / Unit<QT>::kElems + 63) / 64;
   // the gate/up epilogue needs both rows of a pair in one wave (R >= 2)
-  const bool m1_ok = ns <= kM1MaxSlots && (f.epi != EB_EPI_GLU || m1_shape(ns).r >= 2);
+  // the gate/up epilogue takes two rows per wave, which fit without spilling
+  // up to 4 slots
+  const bool m1_ok = ns <= kM1MaxSlots && (f.epi != EB_EPI_GLU || ns <= 4);
   if (m <= 1 && m1_ok) return launch_m1<QT, XT>(wdata, n, k, x, y, yt, f, s);
   if (m <= 1) return launch_t<QT, XT, 1, 2>(wdata, n, k, x, m, y, yt, f, s);
   if (m <= 2) return launch_t<QT, XT, 2, 2>(wdata, n, k, x, m, y, yt, f, s);
