@@ -1,29 +1,43 @@
 #!/usr/bin/env python3
 """Benchmark of the quantized linear-layer stack on one MI355X.
 
-    python bench.py [--steps K] [--warmup W] [--workload NAME] [--chain]
+    python bench.py [--steps K] [--warmup W]                  # every workload, one JSON line
+    python bench.py --workload NAME [--chain] [--steps K] ... # one workload (profiling runs)
 
 One step = one pass of eb_qlinear_stack over every projection of every layer
-of the workload (graph-replayed), with weights, activations and outputs
-already resident in HBM.  The default workload is batch-1 decode of one token
-through a 32-layer 7B-class stack with Q4_0 weights (4096->12288 QKV,
-4096->4096 O, 4096->22016 gate+up, 11008->4096 down; fp16 activations, fp32
-outputs).
+of a workload (graph-replayed), with weights, activations and outputs already
+resident in HBM.  Workloads (seeded synthetic inputs of the shapes in
+paper_2607_02501_amd/workloads.py):
 
-With --chain (workloads with a gate/up projection) the layers run as a
-dependent decoder-layer chain through one fp32 residual stream h: QKV on
-RMSNorm(h), O adding into h (attention is outside the path: its output is a
-seeded input per layer), gate/up on RMSNorm(h) with the SiLU-gated product,
-down adding into h; every step fused into its projection's launch (section
-3.2, operator fusion).
+  q8_0_m1_2048              one Q8_0 2048x2048 decode linear (128 distinct copies per pass)
+  q4_0_decode_7b            batch-1 decode through a 32-layer 7B-class Q4_0 stack
+  q8_0_vlm_prefill_816      VLM-backbone prefill, m = 816, 18 layers of d = 2048
+  q8_0_action_expert_50x10  action-expert denoising, m = 50, 18 layers x 10 steps
+  q4_0_video_wam_4096       video world-action backbone, m = 4096, 28 layers of d = 3072
 
-Prints ONE JSON line:
+A "_chain" variant runs the layers as a dependent decoder-layer chain through
+one fp32 residual stream h: QKV on RMSNorm(h), O adding into h (attention is
+outside the path: its output is a seeded input per layer), gate/up on
+RMSNorm(h) with the SiLU-gated product, down adding into h; every step fused
+into its projection's launch (section 3.2, operator fusion).  That is a real
+backbone pass: each projection waits for the one before.  The independent
+variant gives every projection its own activations, so the stack may fuse
+them into few launches (a bandwidth / matrix-core rate, not a pass time).
+
+With no --workload, bench.py measures every workload (independent, and the
+chain where the workload has a gate/up projection), the dependent batch-1
+decode chain last, and prints ONE JSON line whose headline (value,
+ms_per_step, roofline, cpu_baseline) is that decode chain -- the ms per
+backbone pass of autoregressive action-token decode -- with every other
+measurement under "configs".
+
+Per workload:
   value          whole-pass algorithmic throughput (GB/s for the bandwidth-bound
-                 workloads, TFLOP/s for the prefill workloads)
-  ms_per_step    milliseconds per backbone pass (HIP events around K passes)
+                 workloads, TFLOP/s for the matrix-core-bound ones)
+  ms_per_step    milliseconds per pass (HIP events around K passes)
   roofline       the dominant kernel's algorithmic rate per launch against the
-                 MI355X peak: its launches are graph-replayed back to back and
-                 HIP events on the launch stream give the average duration
+                 MI355X peak, from HIP events on the launch stream around
+                 graph replays of that kernel's launches alone (see kernel_groups)
   cpu_baseline   the CPU oracle timed on a bounded sample of the same workload
 """
 from __future__ import annotations
@@ -44,6 +58,13 @@ PEAK_MFMA_16BIT_TFLOPS = 2500.0  # MI355X dense bf16 / fp16 matrix
 RIDGE_FLOP_PER_BYTE = PEAK_MFMA_16BIT_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)  # 312.5
 MAX_HOST_THREADS = 16
 
+# every workload, in run order; the headline (decode chain) last
+ALL_CONFIGS = [("q8_0_m1_2048", False), ("q4_0_video_wam_4096", False),
+               ("q8_0_vlm_prefill_816", False), ("q8_0_vlm_prefill_816", True),
+               ("q8_0_action_expert_50x10", False), ("q8_0_action_expert_50x10", True),
+               ("q4_0_decode_7b", False), ("q4_0_decode_7b", True)]
+HEADLINE = ("q4_0_decode_7b", True)
+
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
@@ -53,20 +74,22 @@ def parse():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--warmup-seconds", type=float, default=0.5,
-                    help="keep warming up until this much time has passed as well (the "
-                         "GPU takes some tens of milliseconds of load to reach its "
-                         "steady clock)")
-    ap.add_argument("--workload", default="q4_0_decode_7b")
+    ap.add_argument("--warmup", type=int, default=3, help="untimed passes before the timed ones")
+    ap.add_argument("--settle-seconds", type=float, default=0.5,
+                    help="before the first workload, keep the GPU busy with device copies for "
+                         "this long (its clock takes some tens of milliseconds of load to settle); "
+                         "no pass of any workload is run for it")
+    ap.add_argument("--workload", default=None, help="measure this workload only")
     ap.add_argument("--chain", action="store_true",
-                    help="run the layers as a dependent decoder-layer chain with fused "
-                         "RMSNorm / residual / SiLU-gate steps")
-    ap.add_argument("--cpu-layers", type=int, default=None, help="layers in the oracle sample")
+                    help="with --workload: the dependent decoder-layer chain")
     ap.add_argument("--cpu-rows", type=int, default=None, help="activation rows in the oracle sample")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
-                    help="oracle time the CPU baseline sample is sized to")
+                    help="oracle time the headline CPU baseline sample is sized to")
+    ap.add_argument("--cpu-seconds-other", type=float, default=2.0,
+                    help="oracle time of the other workloads' CPU baseline samples")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-kernel-groups", action="store_true",
+                    help="skip the per-kernel roofline timing (profiling runs)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="first run a plain device-to-device copy of BYTES (for scaling "
                          "rocprofv3 FETCH_SIZE / WRITE_SIZE counters)")
@@ -99,166 +122,30 @@ def load_traffic(workload, kernel):
     return rec.get("hbm_bytes_per_launch")
 
 
-def main():
-    args = parse()
-    world = int(os.environ.get("WORLD_SIZE", "1"))
-    if args.gpus != 1 or world != 1:
-        print(f"bench.py measures one GPU only (got --gpus {args.gpus}, WORLD_SIZE {world}): "
-              "this build has no multi-GPU path; run with --gpus 1.", file=sys.stderr)
-        sys.exit(2)
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as fh:
+            return next((l.split(":", 1)[1].strip() for l in fh if l.startswith("model name")), "")
+    except OSError:
+        return ""
 
-    import torch
 
-    from paper_2607_02501_amd import eb
-    from paper_2607_02501_amd import workloads as W
+# ---------------------------------------------------------------------------
+# Workload entries
+# ---------------------------------------------------------------------------
 
-    if not torch.cuda.is_available():
-        print("bench.py needs a GPU", file=sys.stderr)
-        sys.exit(1)
-    wl = W.WORKLOADS[args.workload]
-    dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
-    if args.calibrate_copy:
-        src = torch.ones(args.calibrate_copy // 4, dtype=torch.float32, device=dev)
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        log(f"[bench] calibration copy of {args.calibrate_copy} bytes done")
-        del src, dst
-
-    # ---- resident inputs: quantized weights, activations, outputs ----------
-    t_setup = time.time()
-    qws = {}
-    for layer in range(wl.layers):
-        for p, (_, k, n) in enumerate(wl.projections):
-            w = W.weights(wl, layer, p, dev)
-            qws[layer, p] = eb.quantize(w, wl.qtype)
-            del w
+def independent_entries(wl, W, qws, dev, torch):
+    """Every projection of every layer (and step) with its own activations."""
     entries, meta = [], []
-    if args.chain:
-        entries, meta, chain_bytes = chain_entries(wl, W, qws, dev, torch)
-    else:
-        for step in range(wl.steps):
-            for layer in range(wl.layers):
-                for p, (pname, k, n) in enumerate(wl.projections):
-                    x = W.activations(wl, layer, p, dev, step=step)
-                    y = torch.empty((wl.m, n), dtype=torch.float32, device=dev)
-                    entries.append((qws[layer, p], x, y))
-                    meta.append((pname, wl.m, n, k))
-    ops = eb.make_ops(entries)
-    torch.cuda.synchronize()
-    log(f"[bench] {wl.name}{' chain' if args.chain else ''}: {len(entries)} ops per pass, "
-        f"{eb.stack_launches(ops)} launches per pass, setup {time.time() - t_setup:.1f}s")
-
-    bytes_pass = chain_bytes if args.chain else sum(op_bytes(wl.qtype, m, n, k) for (_, m, n, k) in meta)
-    wbytes_pass = sum(weight_bytes(wl.qtype, n, k) for (_, m, n, k) in meta)
-    flops_pass = sum(2 * m * n * k for (_, m, n, k) in meta)
-    mfma_bound = wl.m >= 512
-
-    # ---- timed region: K graph-replayed passes -----------------------------
-    warm, t_warm = 0, time.time()
-    while warm < args.warmup or time.time() - t_warm < args.warmup_seconds:
-        eb.qlinear_stack(ops)
-        warm += 1
-        if warm % 8 == 0:
-            torch.cuda.synchronize()
-    torch.cuda.synchronize()
-    args.warmup = warm
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(args.steps):
-        eb.qlinear_stack(ops)
-    e1.record()
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / args.steps
-    log(f"[bench] timed {args.steps} passes: {ms:.4f} ms/pass")
-
-    if args.chain:
-        finish_chain(args, wl, W, dev, ops, entries, meta, bytes_pass, wbytes_pass, flops_pass, ms,
-                     mfma_bound, eb, torch)
-        return
-
-    # ---- per-kernel durations ------------------------------------------------
-    # Ops that run the same kernel instance (same path, formats, m and k) form
-    # one stack, graph-replayed back to back (independent m == 1 ops become one
-    # fused launch); HIP events on the launch stream bracket `reps` replays, so
-    # the average launch duration excludes host launch cost and agrees with
-    # rocprofv3's per-kernel average.
-    groups = {}
-    for ent, (pname, m, n, k) in zip(entries, meta):
-        key = (eb.auto_path(wl.qtype, wl.x_dtype, m, n, k), m, k)
-        groups.setdefault(key, []).append((ent, m, n, k))
-    kinds = {}
-    for key, items in groups.items():
-        gops = eb.make_ops([e for e, *_ in items])
-        for _ in range(2):
-            eb.qlinear_stack(gops)
-        torch.cuda.synchronize()
-        reps = max(3, min(50, 2000 // len(items)))
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record()
-        for _ in range(reps):
-            eb.qlinear_stack(gops)
-        b.record()
-        torch.cuda.synchronize()
-        kinds[key] = {"ms": a.elapsed_time(b) / reps, "launches": eb.stack_launches(gops),
-                      "ops": len(items),
-                      "bytes": sum(op_bytes(wl.qtype, m, n, k) for _, m, n, k in items),
-                      "flops": sum(2 * m * n * k for _, m, n, k in items)}
-    eb.stack_cache_clear()
-    dom = max(kinds, key=lambda p: kinds[p]["ms"])
-    dk = kinds[dom]
-    avg_ms = dk["ms"] / dk["launches"]
-    path = dom[0]
-    kernel_name = f"{path}_{wl.qtype}_{'f16' if wl.x_dtype == torch.float16 else 'bf16'}_m{dom[1]}_k{dom[2]}"
-    for p, d in kinds.items():
-        log(f"[bench] kernel {p}: {d['ops']} ops in {d['launches']} launches/pass, "
-            f"avg {1e3 * d['ms'] / d['launches']:.2f} us, "
-            f"{d['bytes'] / d['ms'] / 1e6:.1f} GB/s, {d['flops'] / d['ms'] / 1e9:.2f} TFLOP/s")
-    # the roofline that bounds a kernel is set by its arithmetic intensity,
-    # not by which path runs it (m = 50 on the MFMA path is HBM-bound)
-    if dk["flops"] / dk["bytes"] > RIDGE_FLOP_PER_BYTE:
-        achieved = dk["flops"] / dk["launches"] / (avg_ms * 1e-3) / 1e12
-        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_MFMA_16BIT_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(achieved / PEAK_MFMA_16BIT_TFLOPS, 4)}
-    else:
-        achieved = dk["bytes"] / dk["launches"] / (avg_ms * 1e-3) / 1e9
-        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
-                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4)}
-    roof["kernel"] = kernel_name
-    roof["avg_launch_us"] = round(avg_ms * 1e3, 3)
-    roof["launches_per_pass"] = dk["launches"]
-    roof["ops_per_launch"] = dk["ops"] / dk["launches"]
-    roof["algorithmic_per_launch"] = (dk["flops"] if roof["bound"] == "mfma" else dk["bytes"]) // dk["launches"]
-    roof["traffic"] = load_traffic(wl.name, kernel_name)
-
-    if mfma_bound:
-        value, unit = flops_pass / (ms * 1e-3) / 1e12, "TFLOP/s"
-    else:
-        value, unit = bytes_pass / (ms * 1e-3) / 1e9, "GB/s"
-
-    # ---- CPU oracle on a bounded sample ------------------------------------
-    cpu = None
-    if not args.no_cpu_baseline:
-        cpu = cpu_baseline(args, wl, W, dev, mfma_bound)
-
-    out = {
-        "metric": METRIC, "value": round(value, 2), "unit": unit, "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": f"{wl.qtype} weights x {'f16' if wl.x_dtype == torch.float16 else 'bf16'} "
-                 "activations, f32 accumulate",
-        "data": "synthetic (seeded N(0,0.02) weights, N(0,1) activations)",
-        "config": {"workload": wl.name, "m": wl.m, "layers": wl.layers, "steps": wl.steps,
-                   "ops_per_pass": len(entries), "weight_bytes_per_pass": wbytes_pass,
-                   "algorithmic_bytes_per_pass": bytes_pass, "flops_per_pass": flops_pass,
-                   "graph_replay": os.environ.get("EB_STACK_GRAPH", "1") != "0",
-                   "output": "f32"},
-        "roofline": roof,
-        "cpu_baseline": cpu,
-    }
-    print(json.dumps(out), flush=True)
+    for step in range(wl.steps):
+        for layer in range(wl.layers):
+            for p, (pname, k, n) in enumerate(wl.projections):
+                x = W.activations(wl, layer, p, dev, step=step)
+                y = torch.empty((wl.m, n), dtype=torch.float32, device=dev)
+                entries.append((qws[layer, p], x, y))
+                meta.append((pname, p, wl.m, n, k))
+    nbytes = sum(op_bytes(wl.qtype, m, n, k) for (_, _, m, n, k) in meta)
+    return entries, meta, nbytes
 
 
 def chain_entries(wl, W, qws, dev, torch):
@@ -267,9 +154,6 @@ def chain_entries(wl, W, qws, dev, torch):
     stream read by each normalisation and residual addition and written by
     each addition, the attention stand-in, the QKV and gated outputs and
     their re-reads, the normalisation weights."""
-    names = [p[0] for p in wl.projections]
-    if names[2] != "gate_up":
-        raise SystemExit(f"--chain needs a gate/up projection; {wl.name} has {names}")
     (_, d, n_qkv), _, (_, _, n_gu), (_, f, _) = wl.projections
     m, xdt = wl.m, wl.x_dtype
     xs = 2
@@ -293,7 +177,7 @@ def chain_entries(wl, W, qws, dev, torch):
                 (qws[layer, 3], act, h, dict(epilogue="add", residual=h)),
             ]
             for p, (pname, k, n) in enumerate(wl.projections):
-                meta.append((pname, m, n, k))
+                meta.append((pname, p, m, n, k))
                 nbytes += weight_bytes(wl.qtype, n, k)
             nbytes += (m * d * 4 + d * 4 + m * n_qkv * xs          # QKV: h, g, qkv out
                        + m * d * xs + 2 * m * d * 4                # O: attention, h read and write
@@ -302,50 +186,194 @@ def chain_entries(wl, W, qws, dev, torch):
     return entries, meta, nbytes
 
 
-def finish_chain(args, wl, W, dev, ops, entries, meta, bytes_pass, wbytes_pass, flops_pass, ms,
-                 mfma_bound, eb, torch):
-    """JSON line of a chain run: the chain's launches depend on each other, so
-    the roofline is the whole pass against the peak (no per-kernel groups)."""
-    launches = eb.stack_launches(ops)
-    eb.stack_cache_clear()
-    if mfma_bound:
-        value, unit = flops_pass / (ms * 1e-3) / 1e12, "TFLOP/s"
-        roof = {"bound": "mfma", "achieved": round(value, 2), "peak": PEAK_MFMA_16BIT_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(value / PEAK_MFMA_16BIT_TFLOPS, 4)}
+def chain_op_bytes(wl, p):
+    """Algorithmic bytes of projection p of one chain layer (as chain_entries)."""
+    (_, d, n_qkv), _, (_, _, n_gu), (_, f, _) = wl.projections
+    m, xs = wl.m, 2
+    _, k, n = wl.projections[p]
+    extra = [m * d * 4 + d * 4 + m * n_qkv * xs, m * d * xs + 2 * m * d * 4,
+             m * d * 4 + d * 4 + m * (n_gu // 2) * xs, m * f * xs + 2 * m * d * 4][p]
+    return weight_bytes(wl.qtype, n, k) + extra
+
+
+# ---------------------------------------------------------------------------
+# Timing
+# ---------------------------------------------------------------------------
+
+def time_replays(eb, torch, ops, reps, warm=2):
+    """ms per eb_qlinear_stack replay, from HIP events on the launch stream."""
+    for _ in range(warm):
+        eb.qlinear_stack(ops)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        eb.qlinear_stack(ops)
+    b.record()
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / reps
+
+
+def roofline_of(flops, nbytes, launches, ms, label, extra=None):
+    """The rate of one kernel group against the peak that bounds it (set by
+    arithmetic intensity, not by the path that runs it)."""
+    avg_ms = ms / launches
+    if flops / nbytes > RIDGE_FLOP_PER_BYTE:
+        achieved = flops / launches / (avg_ms * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_MFMA_16BIT_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_MFMA_16BIT_TFLOPS, 4)}
+        per = flops // launches
     else:
-        value, unit = bytes_pass / (ms * 1e-3) / 1e9, "GB/s"
-        roof = {"bound": "hbm", "achieved": round(value, 1), "peak": PEAK_HBM_GBS,
-                "unit": "GB/s", "frac": round(value / PEAK_HBM_GBS, 4)}
-    roof.update({"kernel": "decoder-layer chain, all launches of a pass",
-                 "avg_launch_us": round(ms * 1e3 / launches, 3), "launches_per_pass": launches,
-                 "ops_per_launch": round(len(entries) / launches, 3),
-                 "algorithmic_per_launch": (flops_pass if mfma_bound else bytes_pass) // launches,
-                 "traffic": None})
-    log(f"[bench] chain: {launches} launches per pass, {value:.1f} {unit} over the pass")
-    cpu = None if args.no_cpu_baseline else cpu_baseline_chain(args, wl, W, dev, mfma_bound)
-    out = {
-        "metric": METRIC, "value": round(value, 2), "unit": unit, "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": f"{wl.qtype} weights x {'f16' if wl.x_dtype == torch.float16 else 'bf16'} "
-                 "activations, f32 accumulate, f32 residual stream",
-        "data": "synthetic (seeded N(0,0.02) weights, N(0,1) attention outputs and stream)",
-        "config": {"workload": wl.name + "_chain", "m": wl.m, "layers": wl.layers,
-                   "steps": wl.steps, "ops_per_pass": len(entries),
-                   "weight_bytes_per_pass": wbytes_pass, "algorithmic_bytes_per_pass": bytes_pass,
-                   "flops_per_pass": flops_pass,
-                   "graph_replay": os.environ.get("EB_STACK_GRAPH", "1") != "0",
-                   "fused_steps": "rmsnorm prologue, residual add, silu-gated gate/up"},
-        "roofline": roof,
-        "cpu_baseline": cpu,
-    }
-    print(json.dumps(out), flush=True)
+        achieved = nbytes / launches / (avg_ms * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4)}
+        per = nbytes // launches
+    roof.update({"kernel": label, "avg_launch_us": round(avg_ms * 1e3, 3),
+                 "algorithmic_per_launch": per})
+    if extra:
+        roof.update(extra)
+    return roof
 
 
-def cpu_baseline_chain(args, wl, W, dev, mfma_bound):
+def kernel_groups(args, wl, chain, entries, meta, eb, torch):
+    """Per-kernel timing.  Independent workloads: ops that run the same kernel
+    instance (same path, m and k) form one stack, graph-replayed back to back
+    (independent m == 1 ops become one fused launch, small-m ops one fused
+    MFMA launch, large-m ops one grouped launch).  A grouped launch whose ops'
+    last row tile would be mostly padding hands those rows to a fused small-m
+    launch beside it; its group is timed on the rows it keeps (whole 256-row
+    tiles), so the figure is that one launch.  Chains: the ops of one
+    projection (every layer, every step) form one stack; they depend on each
+    other through the residual stream, so they run as lone launches exactly
+    as in the pass (an MFMA projection's launch unit is its product plus its
+    split-K reduction).  HIP events bracket the replays, so the average launch
+    duration excludes host cost and compares with rocprofv3's kernel times.
+    Returns the dominant group's roofline and every group's line."""
+    groups = {}
+    for ent, (pname, p, m, n, k) in zip(entries, meta):
+        key = ("proj", p, pname) if chain else (eb.auto_path(wl.qtype, wl.x_dtype, m, n, k), m, k)
+        groups.setdefault(key, []).append((ent, p, m, n, k))
+    kinds = {}
+    for key, items in groups.items():
+        if chain:
+            gops = eb.make_ops([e for e, *_ in items])
+            nbytes = chain_op_bytes(wl, key[1]) * len(items)
+            flops = sum(2 * m * n * k for _, _, m, n, k in items)
+            rows_note = None
+        else:
+            m = items[0][2]
+            keep = m - m % 256 if (m > 128 and m % 256) else m
+            ents = []
+            for (qw, x, y), _, mm, n, k in items:
+                ents.append((qw, x[:keep], y[:keep]))
+            gops = eb.make_ops(ents)
+            nbytes = sum(op_bytes(wl.qtype, keep, n, k) for _, _, _, n, k in items)
+            flops = sum(2 * keep * n * k for _, _, _, n, k in items)
+            rows_note = keep if keep != m else None
+        launches = eb.stack_launches(gops)
+        reps = max(3, min(50, 2000 // len(items)))
+        ms = time_replays(eb, torch, gops, reps)
+        kinds[key] = {"ms": ms, "launches": launches, "ops": len(items), "bytes": nbytes,
+                      "flops": flops, "rows": rows_note}
+        del gops
+        eb.stack_cache_clear()
+    lines = {}
+    for key, d in kinds.items():
+        name = f"{key[2]} projection" if chain else f"{key[0]} m={key[1]} k={key[2]}"
+        lines[name] = {"ops": d["ops"], "launches_per_replay": d["launches"],
+                       "ms_per_replay": round(d["ms"], 4),
+                       "GB/s": round(d["bytes"] / d["ms"] / 1e6, 1),
+                       "TFLOP/s": round(d["flops"] / d["ms"] / 1e9, 2)}
+        if d["rows"]:
+            lines[name]["rows_kept"] = d["rows"]
+        log(f"[bench] kernel group {name}: {d['ops']} ops in {d['launches']} launches per replay, "
+            f"{d['ms']:.4f} ms, {lines[name]['GB/s']} GB/s, {lines[name]['TFLOP/s']} TFLOP/s")
+    dom = max(kinds, key=lambda q: kinds[q]["ms"])
+    dk = kinds[dom]
+    xs = "f16" if wl.x_dtype == torch.float16 else "bf16"
+    if chain:
+        label = f"chain_{wl.qtype}_{xs}_m{wl.m}_{dom[2]}"
+        desc = (f"{dom[2]} projection of the chain, lone launches "
+                f"({dk['launches'] // dk['ops']} per projection)")
+    else:
+        label = f"{dom[0]}_{wl.qtype}_{xs}_m{dom[1]}_k{dom[2]}"
+        desc = (f"{dom[0]} path, m = {dom[1]}, k = {dom[2]}: {dk['ops']} ops in {dk['launches']} "
+                f"launch(es) per replay")
+        if dk["rows"]:
+            desc += f" (rows 0..{dk['rows'] - 1}; the last {dom[1] - dk['rows']} rows run beside it)"
+    roof = roofline_of(dk["flops"], dk["bytes"], dk["launches"], dk["ms"], label,
+                       {"description": desc, "launches_per_replay": dk["launches"],
+                        "ops_per_replay": dk["ops"]})
+    roof["traffic"] = load_traffic(wl.name + ("_chain" if chain else ""), label)
+    return roof, lines
+
+
+# ---------------------------------------------------------------------------
+# CPU baseline (the oracle on a bounded sample)
+# ---------------------------------------------------------------------------
+
+def cpu_baseline(args, wl, W, dev, mfma_bound, seconds):
+    """Time the CPU oracle (binary64 qlinear over its own quantization of the
+    same seeded weights) on a bounded sample of the workload: its projections
+    layer by layer (cycling over the layers already quantized when the
+    workload is shorter than the time target) on the first rows of x, until
+    about `seconds` of timed oracle work has been done."""
+    import numpy as np
+    import torch
+
+    from oracle import oracle as O
+
+    orc = O.get()
+    cores = min(O.available_cores(), MAX_HOST_THREADS)
+    rows = min(args.cpu_rows or (wl.m if wl.m <= 8 else 8), wl.m)
+    qt = O.Q8_0 if wl.qtype == "q8_0" else O.Q4_0
+    xt = O.X_F16 if wl.x_dtype == torch.float16 else O.X_BF16
+    cache, cache_bytes = [], 0
+    secs, nbytes, flops, ops, layers_seen = 0.0, 0, 0, 0, 0
+
+    def run(blocks, xb, n, k):
+        nonlocal secs, nbytes, flops, ops
+        t = time.perf_counter()
+        orc.qlinear(qt, blocks, n, k, xb, xt, nthreads=cores)
+        secs += time.perf_counter() - t
+        nbytes += op_bytes(wl.qtype, rows, n, k)
+        flops += 2 * rows * n * k
+        ops += 1
+
+    for layer in range(wl.layers):
+        if secs >= seconds:
+            break
+        layers_seen += 1
+        for p, (_, k, n) in enumerate(wl.projections):
+            w = W.weights(wl, layer, p, dev).cpu().numpy()
+            x = W.activations(wl, layer, p, dev)[:rows]
+            xb = x.cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
+            blocks = orc.quantize(qt, w, nthreads=cores)  # untimed: weights load once
+            del w
+            run(blocks, xb, n, k)
+            if cache_bytes + blocks.nbytes <= (2 << 30):
+                cache.append((blocks, xb, n, k))
+                cache_bytes += blocks.nbytes
+    while secs < seconds and cache:
+        for blocks, xb, n, k in cache:
+            run(blocks, xb, n, k)
+            if secs >= seconds:
+                break
+    sample = (f"{ops} projection calls over the first {layers_seen} of {wl.layers} layers "
+              f"({len(wl.projections)} projections each, cycling), {rows} of {wl.m} "
+              f"activation rows; {secs:.1f}s of oracle time")
+    log(f"[bench] cpu oracle {wl.name}: {sample}")
+    if mfma_bound:
+        return {"value": round(flops / secs / 1e12, 6), "unit": "TFLOP/s", "cores": cores,
+                "kind": "oracle", "sample": sample, "cpu_model": cpu_model()}
+    return {"value": round(nbytes / secs / 1e9, 4), "unit": "GB/s", "cores": cores,
+            "kind": "oracle", "sample": sample, "cpu_model": cpu_model()}
+
+
+def cpu_baseline_chain(args, wl, W, dev, mfma_bound, seconds):
     """The oracle's fused projections along the same chain (its own residual
     stream, binary64, the first rows), layer after layer until about
-    --cpu-seconds of oracle time."""
+    `seconds` of oracle time."""
     import numpy as np
     import torch
 
@@ -370,15 +398,19 @@ def cpu_baseline_chain(args, wl, W, dev, mfma_bound):
         secs += time.perf_counter() - t
         return r
 
-    for layer in range(wl.layers):
-        if secs >= args.cpu_seconds:
-            break
-        layers += 1
+    cache, cache_bytes = [], 0
+
+    def layer_inputs(layer):
         blocks = [orc.quantize(qt, W.weights(wl, layer, p, dev).cpu().numpy(), nthreads=cores)
                   for p in range(4)]
         g1 = (1.0 + 0.1 * W.normal((d,), W.seed_of(wl.wid, layer, 0, 2), dev)).cpu().numpy()
         g2 = (1.0 + 0.1 * W.normal((d,), W.seed_of(wl.wid, layer, 2, 2), dev)).cpu().numpy()
         attn = bits(W.activations(wl, layer, 1, dev)[:rows])
+        return blocks, g1, g2, attn
+
+    def run_layer(inputs):
+        nonlocal h, ops, nbytes, flops
+        blocks, g1, g2, attn = inputs
         h32 = h.astype(np.float32)
         timed(lambda: orc.fused_qlinear(qt, blocks[0], n_qkv, d, h32, xt, prologue="rmsnorm",
                                         gamma=g1, eps=1e-5, nthreads=cores))
@@ -394,79 +426,188 @@ def cpu_baseline_chain(args, wl, W, dev, mfma_bound):
         for (_, k, n) in wl.projections:
             nbytes += op_bytes(wl.qtype, rows, n, k)
             flops += 2 * rows * n * k
+
+    # the chain through the layers (weights quantized untimed, as loaded once),
+    # then again through the layers kept in memory (up to 2 GB of blocks) until
+    # the time target is reached
+    for layer in range(wl.layers):
+        if secs >= seconds:
+            break
+        layers += 1
+        inputs = layer_inputs(layer)
+        run_layer(inputs)
+        nb = sum(b.nbytes for b in inputs[0])
+        if cache_bytes + nb <= (2 << 30):
+            cache.append(inputs)
+            cache_bytes += nb
+    while secs < seconds and cache:
+        for inputs in cache:
+            run_layer(inputs)
+            if secs >= seconds:
+                break
     sample = (f"{ops} fused projection calls: the chain through the first {layers} of "
-              f"{wl.layers} layers, {rows} of {wl.m} activation rows; {secs:.1f}s of oracle time")
-    log(f"[bench] cpu oracle: {sample}")
+              f"{wl.layers} layers (then again through the first {len(cache)}, cycling), "
+              f"{rows} of {wl.m} activation rows; {secs:.1f}s of oracle time")
+    log(f"[bench] cpu oracle {wl.name} chain: {sample}")
     if mfma_bound:
         return {"value": round(flops / secs / 1e12, 6), "unit": "TFLOP/s", "cores": cores,
-                "kind": "oracle", "sample": sample}
+                "kind": "oracle", "sample": sample, "cpu_model": cpu_model()}
     return {"value": round(nbytes / secs / 1e9, 4), "unit": "GB/s", "cores": cores,
-            "kind": "oracle", "sample": sample}
+            "kind": "oracle", "sample": sample, "cpu_model": cpu_model()}
 
 
-def cpu_baseline(args, wl, W, dev, mfma_bound):
-    """Time the CPU oracle (binary64 qlinear over its own quantization of the
-    same seeded weights) on a bounded sample of the workload: its projections
-    layer by layer (cycling over the layers already quantized when the
-    workload is shorter than the time target) on the first rows of x, until
-    about --cpu-seconds of timed oracle work has been done."""
+def cpu_single_thread(W, dev):
+    """The oracle on one thread: one 2048 x 2048 Q8_0 projection at m = 1
+    (the first copy of the single-linear workload), repeated for about 2 s."""
     import numpy as np
     import torch
 
     from oracle import oracle as O
 
     orc = O.get()
-    cores = min(O.available_cores(), MAX_HOST_THREADS)
-    max_layers = min(args.cpu_layers or wl.layers, wl.layers)
-    rows = min(args.cpu_rows or (wl.m if wl.m <= 8 else 8), wl.m)
-    qt = O.Q8_0 if wl.qtype == "q8_0" else O.Q4_0
-    xt = O.X_F16 if wl.x_dtype == torch.float16 else O.X_BF16
-    cache, cache_bytes = [], 0
-    secs, nbytes, flops, ops, layers_seen = 0.0, 0, 0, 0, 0
-
-    def run(blocks, xb, n, k):
-        nonlocal secs, nbytes, flops, ops
+    wl = W.WORKLOADS["q8_0_m1_2048"]
+    _, k, n = wl.projections[0]
+    blocks = orc.quantize(O.Q8_0, W.weights(wl, 0, 0, dev).cpu().numpy(), nthreads=1)
+    xb = W.activations(wl, 0, 0, dev).cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
+    secs, calls = 0.0, 0
+    while secs < 2.0:
         t = time.perf_counter()
-        orc.qlinear(qt, blocks, n, k, xb, xt, nthreads=cores)
+        orc.qlinear(O.Q8_0, blocks, n, k, xb, O.X_F16, nthreads=1)
         secs += time.perf_counter() - t
-        nbytes += op_bytes(wl.qtype, rows, n, k)
-        flops += 2 * rows * n * k
-        ops += 1
+        calls += 1
+    return {"value": round(calls * op_bytes("q8_0", 1, n, k) / secs / 1e9, 4), "unit": "GB/s",
+            "gflops": round(calls * 2 * n * k / secs / 1e9, 4), "cores": 1,
+            "sample": f"{calls} calls of one 2048x2048 Q8_0 projection at m = 1, {secs:.1f}s"}
 
-    for layer in range(max_layers):
-        if secs >= args.cpu_seconds:
-            break
-        layers_seen += 1
+
+# ---------------------------------------------------------------------------
+# One workload
+# ---------------------------------------------------------------------------
+
+def run_workload(args, name, chain, cpu_seconds, eb, W, torch, dev):
+    wl = W.WORKLOADS[name]
+    names = [p[0] for p in wl.projections]
+    if chain and names[2] != "gate_up":
+        raise SystemExit(f"--chain needs a gate/up projection; {wl.name} has {names}")
+    t_setup = time.time()
+    qws = {}
+    for layer in range(wl.layers):
         for p, (_, k, n) in enumerate(wl.projections):
-            w = W.weights(wl, layer, p, dev).cpu().numpy()
-            x = W.activations(wl, layer, p, dev)[:rows]
-            xb = x.cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
-            blocks = orc.quantize(qt, w, nthreads=cores)  # untimed: weights load once
+            w = W.weights(wl, layer, p, dev)
+            qws[layer, p] = eb.quantize(w, wl.qtype)
             del w
-            run(blocks, xb, n, k)
-            if cache_bytes + blocks.nbytes <= (2 << 30):
-                cache.append((blocks, xb, n, k))
-                cache_bytes += blocks.nbytes
-    while secs < args.cpu_seconds and cache:
-        for blocks, xb, n, k in cache:
-            run(blocks, xb, n, k)
-            if secs >= args.cpu_seconds:
-                break
-    sample = (f"{ops} projection calls over the first {layers_seen} of {wl.layers} layers "
-              f"({len(wl.projections)} projections each, cycling), {rows} of {wl.m} "
-              f"activation rows; {secs:.1f}s of oracle time")
-    log(f"[bench] cpu oracle: {sample}")
-    model = ""
-    try:
-        with open("/proc/cpuinfo") as fh:
-            model = next((l.split(":", 1)[1].strip() for l in fh if l.startswith("model name")), "")
-    except OSError:
-        pass
+    if chain:
+        entries, meta, bytes_pass = chain_entries(wl, W, qws, dev, torch)
+    else:
+        entries, meta, bytes_pass = independent_entries(wl, W, qws, dev, torch)
+    ops = eb.make_ops(entries)
+    torch.cuda.synchronize()
+    launches = eb.stack_launches(ops)
+    label = wl.name + ("_chain" if chain else "")
+    log(f"[bench] {label}: {len(entries)} ops per pass, {launches} launches per pass, "
+        f"setup {time.time() - t_setup:.1f}s")
+    wbytes_pass = sum(weight_bytes(wl.qtype, n, k) for (_, _, m, n, k) in meta)
+    flops_pass = sum(2 * m * n * k for (_, _, m, n, k) in meta)
+    mfma_bound = flops_pass / bytes_pass > RIDGE_FLOP_PER_BYTE
+
+    # ---- timed region: W warmup passes, then K graph-replayed passes ---------
+    for _ in range(args.warmup):
+        eb.qlinear_stack(ops)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        eb.qlinear_stack(ops)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    log(f"[bench] {label}: {args.warmup} warmup passes, {args.steps} timed passes: {ms:.4f} ms/pass")
+    eb.stack_cache_clear()
+
     if mfma_bound:
-        return {"value": round(flops / secs / 1e12, 6), "unit": "TFLOP/s", "cores": cores,
-                "kind": "oracle", "sample": sample, "cpu_model": model}
-    return {"value": round(nbytes / secs / 1e9, 4), "unit": "GB/s", "cores": cores,
-            "kind": "oracle", "sample": sample, "cpu_model": model}
+        value, unit = flops_pass / (ms * 1e-3) / 1e12, "TFLOP/s"
+    else:
+        value, unit = bytes_pass / (ms * 1e-3) / 1e9, "GB/s"
+    roof, lines = (None, None) if args.no_kernel_groups else kernel_groups(
+        args, wl, chain, entries, meta, eb, torch)
+    cpu = None
+    if not args.no_cpu_baseline and cpu_seconds > 0:
+        cpu = (cpu_baseline_chain if chain else cpu_baseline)(args, wl, W, dev, mfma_bound, cpu_seconds)
+    xs = "f16" if wl.x_dtype == torch.float16 else "bf16"
+    out = {
+        "ms_per_step": round(ms, 5), "value": round(value, 2), "unit": unit,
+        "steps": args.steps, "warmup": args.warmup, "launches_per_pass": launches,
+        "dtype": f"{wl.qtype} weights x {xs} activations, f32 accumulate"
+                 + (", f32 residual stream" if chain else ""),
+        "config": {"workload": label, "m": wl.m, "layers": wl.layers, "steps": wl.steps,
+                   "ops_per_pass": len(entries), "weight_bytes_per_pass": wbytes_pass,
+                   "algorithmic_bytes_per_pass": bytes_pass, "flops_per_pass": flops_pass,
+                   "graph_replay": os.environ.get("EB_STACK_GRAPH", "1") != "0",
+                   "dependent_chain": chain,
+                   **({"fused_steps": "rmsnorm prologue, residual add, silu-gated gate/up"}
+                      if chain else {})},
+        "roofline": roof, "kernel_groups": lines, "cpu_baseline": cpu,
+    }
+    del entries, ops, qws
+    torch.cuda.empty_cache()
+    return out
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}, WORLD_SIZE {world}): "
+              "this build has no multi-GPU path; run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2607_02501_amd import eb
+    from paper_2607_02501_amd import workloads as W
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    if args.calibrate_copy:
+        src = torch.ones(args.calibrate_copy // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] calibration copy of {args.calibrate_copy} bytes done")
+        del src, dst
+    if args.settle_seconds > 0:
+        a = torch.empty(64 << 20, dtype=torch.uint8, device=dev)
+        b = torch.empty_like(a)
+        t0 = time.time()
+        while time.time() - t0 < args.settle_seconds:
+            for _ in range(16):
+                b.copy_(a)
+            torch.cuda.synchronize()
+        del a, b
+
+    common = {"metric": METRIC, "n_gpus": 1, "higher_is_better": True, "scaling": "weak",
+              "vs_baseline": None,
+              "data": "synthetic (seeded N(0,0.02) weights, N(0,1) activations and stream)"}
+    if args.workload:
+        r = run_workload(args, args.workload, args.chain, args.cpu_seconds, eb, W, torch, dev)
+        print(json.dumps({**common, **r}), flush=True)
+        return
+
+    results = {}
+    for name, chain in ALL_CONFIGS:
+        head = (name, chain) == HEADLINE
+        secs = args.cpu_seconds if head else args.cpu_seconds_other
+        results[name + ("_chain" if chain else "")] = run_workload(args, name, chain, secs, eb, W,
+                                                                    torch, dev)
+    head = results.pop(HEADLINE[0] + "_chain")
+    if head["cpu_baseline"] is not None:
+        head["cpu_baseline"]["single_thread"] = cpu_single_thread(W, dev)
+    out = {**common, **head, "configs": results}
+    print(json.dumps(out), flush=True)
 
 
 if __name__ == "__main__":

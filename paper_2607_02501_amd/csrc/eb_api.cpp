@@ -335,6 +335,8 @@ struct Step {
   std::vector<NormJob> norms;  // prologue row kernels run before the step
   bool side = false;  // fused launch of split-off rows that runs on the side stream,
                       // beside the grouped launch before it
+  bool hl = true;     // fused small-m launch: bfloat16 hi/lo weight pairs (not for the
+                      // split-off rows of large-m ops, whose bound is the large-m one)
   bool norm_next = false;   // single split MFMA op whose reduction also normalises
                             // its fp32 output for the next step's prologue
   bool pre_normed = false;  // single MFMA op whose prologue that reduction ran
@@ -421,11 +423,13 @@ eb_status build_plan(const eb_qlinear_op *ops, int32_t n_ops, uint8_t *wsbase, P
     return c;
   };
   // one fused small-m launch over `list` (same weight, x and y formats)
-  auto add_mm_step = [&](const std::vector<eb_qlinear_op> &list, int max_groups = 0) {
+  auto add_mm_step = [&](const std::vector<eb_qlinear_op> &list, int max_groups = 0,
+                         bool hl = true) {
     int64_t max_m = 0;
     for (const eb_qlinear_op &o : list) max_m = std::max(max_m, o.m);
     Step s;
     s.mm = true;
+    s.hl = hl;
     s.type = list[0].w.type;
     s.xt = list[0].x_type;
     s.yt = list[0].y_type;
@@ -581,7 +585,7 @@ eb_status build_plan(const eb_qlinear_op *ops, int32_t n_ops, uint8_t *wsbase, P
             for (const eb_qlinear_op &t : tails)
               if ((t.y_type == EB_F32) == (wide == 1)) cls.push_back(t);
             if (cls.empty()) continue;
-            add_mm_step(cls, overlap ? side_groups() : 0);
+            add_mm_step(cls, overlap ? side_groups() : 0, false);
             P.steps.back().side = overlap;
           }
           i = j;
@@ -763,7 +767,7 @@ eb_status run_plan(const eb_qlinear_op *ops, const Plan &P, hipStream_t s, hipSt
         return EB_ERR_HIP;
       for (size_t q = 1; q <= nside; ++q) {
         const Step &t = P.steps[i + q];
-        if (launch_mfma_multi(t.type, t.xt, t.yt, t.mm_cfg, P.mmtable + t.table, t.nops,
+        if (launch_mfma_multi(t.type, t.xt, t.hl, t.yt, t.mm_cfg, P.mmtable + t.table, t.nops,
                               P.mmwg + t.wg, t.groups, side) != hipSuccess)
           return EB_ERR_HIP;
       }
@@ -775,7 +779,7 @@ eb_status run_plan(const eb_qlinear_op *ops, const Plan &P, hipStream_t s, hipSt
                               st.entries, s) != hipSuccess)
         return EB_ERR_HIP;
     } else if (st.mm) {
-      if (launch_mfma_multi(st.type, st.xt, st.yt, st.mm_cfg, P.mmtable + st.table, st.nops,
+      if (launch_mfma_multi(st.type, st.xt, st.hl, st.yt, st.mm_cfg, P.mmtable + st.table, st.nops,
                             P.mmwg + st.wg, st.groups, s) != hipSuccess)
         return EB_ERR_HIP;
     } else if (st.mfma) {

@@ -188,7 +188,7 @@ int mm_cfg(int64_t max_m);                // tile configuration for a run
 int64_t mm_tiles(int cfg, int64_t m, int64_t n);
 int mm_bk(int cfg);                       // k covered by one step of the configuration
 // The 128-wide-step fused kernel (configuration 0), in its own source file.
-hipError_t launch_lds2(int32_t type, int32_t xt, int32_t yt, const MMOp *ops, int nops,
+hipError_t launch_lds2(int32_t type, int32_t xt, bool hl, int32_t yt, const MMOp *ops, int nops,
                        const int64_t *wg, int groups, hipStream_t s);
 // Fills the unit ranges wg[0..groups] (balanced by steps) for a table whose
 // unit_end / nk are set; returns the number of workgroups to launch.
@@ -198,7 +198,10 @@ int mm_partition(const std::vector<MMOp> &ops, int cfg, std::vector<int64_t> &wg
                  int max_groups = 0);
 // All ops of one launch share the weight format, x type and y type.
 // groups must be a positive multiple of 8 (mm_partition's result).
-hipError_t launch_mfma_multi(int32_t type, int32_t xt, int32_t yt, int cfg, const MMOp *dev_ops,
+// hl: bfloat16 activations with w_hat as hi/lo pairs (ignored for binary16);
+// a launch of only the split-off rows of large-m ops runs without (the ops'
+// bound is the large-m one, w_hat rounded once).
+hipError_t launch_mfma_multi(int32_t type, int32_t xt, bool hl, int32_t yt, int cfg, const MMOp *dev_ops,
                              int nops, const int64_t *dev_wg, int groups, hipStream_t s);
 
 // number of compute units of the current device (cached per device)

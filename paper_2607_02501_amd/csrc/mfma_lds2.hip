@@ -36,7 +36,10 @@ namespace {
 // banks: x chunk c of row r at c ^ (r & 15); Q8_0 codes at c ^ ((r >> 1) & 7);
 // Q4_0 codes at c ^ ((r >> 2) & 3).
 // ---------------------------------------------------------------------------
-template <int QT, int XT, int YT, int WAVES>
+// HL: bfloat16 activations with w_hat as hi/lo bfloat16 pairs (two MFMAs per
+// product, w_hat carried to 2^-16); without it w_hat is rounded once to the
+// activation type (binary16 holds it to 2^-11, bfloat16 to 2^-8).
+template <int QT, int XT, int YT, int WAVES, bool HL>
 __global__ void __launch_bounds__(WAVES * 64)
     mm_lds2_kernel(const MMOp *__restrict__ ops, int nops, const int64_t *__restrict__ wg,
                    int groups) {
@@ -58,9 +61,7 @@ __global__ void __launch_bounds__(WAVES * 64)
   constexpr int YSZ = (YT == EB_F32) ? 4 : 2;
   static_assert(NX * 1024 * WAVES == XBYTES && NW * 1024 * WAVES == WBYTES, "copies must tile");
   static_assert(NS * 16 * T == SBYTES && NW + NS + NST <= 63, "scale loads / wait count range");
-  // bfloat16 activations take w_hat as hi/lo bfloat16 pairs (two MFMAs per
-  // product, w_hat carried to 2^-16; binary16 holds w_hat to 2^-11 in one)
-  constexpr bool HL = (XT == EB_BF16);
+  static_assert(!HL || XT == EB_BF16, "hi/lo pairs are for bfloat16 activations");
 
   __shared__ __attribute__((aligned(1024))) uint8_t sX0[XBYTES];
   __shared__ __attribute__((aligned(1024))) uint8_t sX1[XBYTES];
@@ -507,32 +508,37 @@ __global__ void __launch_bounds__(WAVES * 64)
 }
 
 // YT = EB_F32 for fp32 outputs, EB_BF16 for either 16-bit output type.
-template <int QT, int XT, int WAVES>
+template <int QT, int XT, int WAVES, bool HL>
 hipError_t lds2_y(int32_t yt, const MMOp *ops, int nops, const int64_t *wg, int groups, hipStream_t s) {
   if (yt == EB_F32)
-    mm_lds2_kernel<QT, XT, EB_F32, WAVES><<<groups, WAVES * 64, 0, s>>>(ops, nops, wg, groups);
+    mm_lds2_kernel<QT, XT, EB_F32, WAVES, HL><<<groups, WAVES * 64, 0, s>>>(ops, nops, wg, groups);
   else
-    mm_lds2_kernel<QT, XT, EB_BF16, WAVES><<<groups, WAVES * 64, 0, s>>>(ops, nops, wg, groups);
+    mm_lds2_kernel<QT, XT, EB_BF16, WAVES, HL><<<groups, WAVES * 64, 0, s>>>(ops, nops, wg, groups);
   return hipGetLastError();
 }
 
+template <int QT, int WAVES>
+hipError_t lds2_x(int32_t xt, bool hl, int32_t yt, const MMOp *ops, int nops, const int64_t *wg,
+                  int groups, hipStream_t s) {
+  if (xt == EB_F16) return lds2_y<QT, EB_F16, WAVES, false>(yt, ops, nops, wg, groups, s);
+  if (hl) return lds2_y<QT, EB_BF16, WAVES, true>(yt, ops, nops, wg, groups, s);
+  return lds2_y<QT, EB_BF16, WAVES, false>(yt, ops, nops, wg, groups, s);
+}
+
 template <int WAVES>
-hipError_t lds2_q(int32_t type, int32_t xt, int32_t yt, const MMOp *ops, int nops,
+hipError_t lds2_q(int32_t type, int32_t xt, bool hl, int32_t yt, const MMOp *ops, int nops,
                   const int64_t *wg, int groups, hipStream_t s) {
-  if (type == EB_Q4_0)
-    return xt == EB_F16 ? lds2_y<EB_Q4_0, EB_F16, WAVES>(yt, ops, nops, wg, groups, s)
-                        : lds2_y<EB_Q4_0, EB_BF16, WAVES>(yt, ops, nops, wg, groups, s);
-  return xt == EB_F16 ? lds2_y<EB_Q8_0, EB_F16, WAVES>(yt, ops, nops, wg, groups, s)
-                      : lds2_y<EB_Q8_0, EB_BF16, WAVES>(yt, ops, nops, wg, groups, s);
+  if (type == EB_Q4_0) return lds2_x<EB_Q4_0, WAVES>(xt, hl, yt, ops, nops, wg, groups, s);
+  return lds2_x<EB_Q8_0, WAVES>(xt, hl, yt, ops, nops, wg, groups, s);
 }
 
 }  // namespace
 
-hipError_t launch_lds2(int32_t type, int32_t xt, int32_t yt, const MMOp *ops, int nops,
+hipError_t launch_lds2(int32_t type, int32_t xt, bool hl, int32_t yt, const MMOp *ops, int nops,
                        const int64_t *wg, int groups, hipStream_t s) {
   // 8 waves: two per SIMD, so one wave's LDS and memory waits overlap the
   // other's dequantization and MFMAs (4 waves measured 6% slower)
-  return lds2_q<8>(type, xt, yt, ops, nops, wg, groups, s);
+  return lds2_q<8>(type, xt, hl, yt, ops, nops, wg, groups, s);
 }
 
 }  // namespace eb

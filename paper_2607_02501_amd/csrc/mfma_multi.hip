@@ -35,7 +35,7 @@ namespace {
 // and high nibbles) plus its scale, loaded four steps ahead into one of four
 // register sets.
 // ---------------------------------------------------------------------------
-template <int QT, int XT, int YT, int BM, int FN>
+template <int QT, int XT, int YT, int BM, int FN, bool HL>
 __global__ void __launch_bounds__(256)
     mm_breg_kernel(const MMOp *__restrict__ ops, int nops, const int64_t *__restrict__ wg,
                    int groups) {
@@ -52,9 +52,10 @@ __global__ void __launch_bounds__(256)
   constexpr int NWAIT = 2 * NX + 3 * NW;  // at a barrier: all but x tile t+1 may be in flight
   static_assert(ADMA >= 1 && ADMA * 8 * WAVES == BM, "x tile must split into 8-row copies");
   static_assert(NWAIT <= 63, "vmcnt range");
-  // bfloat16 activations take w_hat as hi/lo bfloat16 pairs (two MFMAs per
-  // product, w_hat carried to 2^-16; binary16 holds w_hat to 2^-11 in one)
-  constexpr bool HL = (XT == EB_BF16);
+  // HL: bfloat16 activations with w_hat as hi/lo bfloat16 pairs (two MFMAs
+  // per product, w_hat carried to 2^-16); without it w_hat is rounded once to
+  // the activation type
+  static_assert(!HL || XT == EB_BF16, "hi/lo pairs are for bfloat16 activations");
 
   __shared__ __attribute__((aligned(1024))) uint8_t sA0[ABYTES];
   __shared__ __attribute__((aligned(1024))) uint8_t sA1[ABYTES];
@@ -330,18 +331,24 @@ __global__ void __launch_bounds__(256)
 }
 
 template <int QT, int XT, int YT>
-hipError_t launch_multi_q(int cfg, const MMOp *ops, int nops, const int64_t *wg, int groups,
+hipError_t launch_multi_q(int cfg, bool hl, const MMOp *ops, int nops, const int64_t *wg, int groups,
                           hipStream_t s) {
-  if (cfg == 0) return launch_lds2(QT, XT, YT, ops, nops, wg, groups, s);
-  mm_breg_kernel<QT, XT, YT, 128, 1><<<groups, 256, 0, s>>>(ops, nops, wg, groups);
+  if (cfg == 0) return launch_lds2(QT, XT, hl, YT, ops, nops, wg, groups, s);
+  if constexpr (XT == EB_BF16) {
+    if (hl) {
+      mm_breg_kernel<QT, XT, YT, 128, 1, true><<<groups, 256, 0, s>>>(ops, nops, wg, groups);
+      return hipGetLastError();
+    }
+  }
+  mm_breg_kernel<QT, XT, YT, 128, 1, false><<<groups, 256, 0, s>>>(ops, nops, wg, groups);
   return hipGetLastError();
 }
 
 template <int QT, int XT>
-hipError_t launch_multi_y(int32_t yt, int cfg, const MMOp *ops, int nops, const int64_t *wg,
+hipError_t launch_multi_y(int32_t yt, int cfg, bool hl, const MMOp *ops, int nops, const int64_t *wg,
                           int groups, hipStream_t s) {
-  if (yt == EB_F32) return launch_multi_q<QT, XT, EB_F32>(cfg, ops, nops, wg, groups, s);
-  return launch_multi_q<QT, XT, EB_BF16>(cfg, ops, nops, wg, groups, s);
+  if (yt == EB_F32) return launch_multi_q<QT, XT, EB_F32>(cfg, hl, ops, nops, wg, groups, s);
+  return launch_multi_q<QT, XT, EB_BF16>(cfg, hl, ops, nops, wg, groups, s);
 }
 
 // {BM, BN, workgroups per CU, k per step}: 0 the 128-wide-step kernel with
@@ -398,15 +405,18 @@ int mm_partition(const std::vector<MMOp> &ops, int cfg, std::vector<int64_t> &wg
   return (int)groups;
 }
 
-hipError_t launch_mfma_multi(int32_t type, int32_t xt, int32_t yt, int cfg, const MMOp *dev_ops,
-                             int nops, const int64_t *dev_wg, int groups, hipStream_t s) {
+hipError_t launch_mfma_multi(int32_t type, int32_t xt, bool hl, int32_t yt, int cfg,
+                             const MMOp *dev_ops, int nops, const int64_t *dev_wg, int groups,
+                             hipStream_t s) {
   if (nops < 1 || groups < kXcds || groups % kXcds != 0) return hipErrorInvalidValue;
+  hl = hl && xt == EB_BF16;
   if (type == EB_Q4_0) {
     if (xt == EB_F16)
-      return launch_multi_y<EB_Q4_0, EB_F16>(yt, cfg, dev_ops, nops, dev_wg, groups, s);
-    return launch_multi_y<EB_Q4_0, EB_BF16>(yt, cfg, dev_ops, nops, dev_wg, groups, s);
+      return launch_multi_y<EB_Q4_0, EB_F16>(yt, cfg, false, dev_ops, nops, dev_wg, groups, s);
+    return launch_multi_y<EB_Q4_0, EB_BF16>(yt, cfg, hl, dev_ops, nops, dev_wg, groups, s);
   }
-  if (xt == EB_F16) return launch_multi_y<EB_Q8_0, EB_F16>(yt, cfg, dev_ops, nops, dev_wg, groups, s);
-  return launch_multi_y<EB_Q8_0, EB_BF16>(yt, cfg, dev_ops, nops, dev_wg, groups, s);
+  if (xt == EB_F16)
+    return launch_multi_y<EB_Q8_0, EB_F16>(yt, cfg, false, dev_ops, nops, dev_wg, groups, s);
+  return launch_multi_y<EB_Q8_0, EB_BF16>(yt, cfg, hl, dev_ops, nops, dev_wg, groups, s);
 }
 }  // namespace eb
