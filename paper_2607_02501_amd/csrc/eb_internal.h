@@ -117,6 +117,7 @@ hipError_t launch_gemv_m1_multi(int32_t type, int32_t xt, int ns, const M1Op *de
 struct MfmaPlan {
   int cfg = 0;
   bool hl = false;        // bfloat16 activations at m <= 128: hi/lo weight tiles
+  bool narrow = false;    // m <= kNarrowMaxM: the one-launch narrow kernel (no tiles, no split)
   int splits = 1;
   int kts = 0;            // K-tiles of 64 per split
   int64_t ws_stride = 0;  // floats between the partial outputs of two splits
@@ -143,6 +144,15 @@ template <int QT, int XT>
 hipError_t mfma_tile_launch(int cfg, bool hl, const void *wdata, int64_t n, int64_t k, const void *x,
                             int64_t m, void *y, int32_t yt, const Fuse &f, int sp, int kts,
                             float *ws, int64_t st, hipStream_t s);
+// Lone small-m projections (m <= kNarrowMaxM) in one launch: 16 weight rows
+// and the whole of k per workgroup, k split over its waves and the partial
+// tiles added through LDS (mfma_narrow.hip).  hl: bfloat16 hi/lo pairs.
+constexpr int64_t kNarrowMaxM = 64;
+constexpr int64_t kNarrowMaxK = 2048;
+bool narrow_fits(int64_t m, int64_t n, int64_t k);
+hipError_t launch_mfma_narrow(int32_t type, const void *wdata, int64_t n, int64_t k, const void *x,
+                              int32_t xt, bool hl, int64_t m, void *y, int32_t yt, const Fuse &f,
+                              hipStream_t s);
 // Whether a workgroup's byte spans of a bm x bn tile fit 32-bit buffer offsets.
 bool mfma_fits_offsets(int32_t type, int64_t n, int64_t k, int bm, int bn);
 int mfma_tile_count();

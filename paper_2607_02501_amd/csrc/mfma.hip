@@ -148,6 +148,14 @@ MfmaPlan plan_mfma(int32_t type, int32_t xt, int64_t m, int64_t n, int64_t k, si
   }
   MfmaPlan best;
   best.hl = hl;
+  // a lone small-m projection: one launch of the narrow kernel, whole k per
+  // workgroup (measured on the action-expert chain: the tiled kernel split
+  // along k plus its reduction took about 16 us per projection)
+  if (fc < 0 && fs <= 0 && narrow_fits(m, n, k)) {
+    best.narrow = true;
+    best.kts = (int)nk;
+    return best;
+  }
   double best_t = 0;
   bool have = false;
   for (int c = 0; c < kNumCfgs; ++c) {
@@ -250,6 +258,7 @@ hipError_t launch_q(const void *wdata, int64_t n, int64_t k, const void *x, int6
   const int sp = ws ? P.splits : 1;
   const int kts = ws ? P.kts : (int)((k + kBK - 1) / kBK);
   const int64_t st = P.ws_stride;
+  if (P.narrow) return launch_mfma_narrow(QT, wdata, n, k, x, XT, P.hl, m, y, yt, f, s);
   const hipError_t e = mfma_tile_launch<QT, XT>(P.cfg, P.hl, wdata, n, k, x, m, y, yt, f, sp, kts, ws, st, s);
   if (e != hipSuccess || sp == 1) return e;
   if (no) {

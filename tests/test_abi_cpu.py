@@ -236,32 +236,43 @@ def test_fused_stack_counts_prologue_launches(eb):
 def test_reduction_runs_next_prologue(eb, monkeypatch):
     """In a dependent layer chain the split-K reduction that writes the fp32
     stream h (O and down, + h) also normalises it for the next projection, so
-    those prologues cost no row-kernel launch; EB_STACK_FUSE_NORM=0 keeps them."""
-    d, f, m = 1024, 4096, 50   # the action-expert layer shape
-    H, A, Q, GU = 0x20000000, 0x21000000, 0x22000000, 0x23000000
-    ops, base = [], 0x10000000
-    for _ in range(2):
-        for n, k, x, y, pro, epi, res, yt in ((3 * d, d, H, Q, 1, 0, None, eb.EB_BF16),
-                                              (d, d, A, H, 0, 1, H, eb.EB_F32),
-                                              (2 * f, d, H, GU, 1, 2, None, eb.EB_BF16),
-                                              (d, f, GU, H, 0, 1, H, eb.EB_F32)):
-            w = eb.eb_qweights(eb.EB_Q8_0, 0, n, k, base)
-            base += (eb.lib.eb_qweights_bytes(eb.EB_Q8_0, n, k) + 4095) // 4096 * 4096
-            ops.append(eb.eb_qlinear_op(w, x, y, m, eb.EB_BF16, yt, pro, epi, G if pro else None,
-                                        res, 1e-5, 0))
-    arr = (eb.eb_qlinear_op * len(ops))(*ops)
-    # 8 projections, each split along k (product + reduction), and 4 prologues
+    those prologues cost no row-kernel launch; EB_STACK_FUSE_NORM=0 keeps them.
+    At m <= 64 the projections with k <= 2048 are one launch of the narrow
+    kernel (whole k per workgroup, no reduction), so only the prologue after
+    a split down projection (k = 4096) is fused."""
+    d, f = 1024, 4096   # the action-expert layer shape
+
+    def chain(m, stream16=False):
+        H, A, Q, GU = 0x20000000, 0x21000000, 0x22000000, 0x23000000
+        ops, base = [], 0x10000000
+        for _ in range(2):
+            for n, k, x, y, pro, epi, res, yt in ((3 * d, d, H, Q, 1, 0, None, eb.EB_BF16),
+                                                  (d, d, A, H, 0, 1, H, eb.EB_F32),
+                                                  (2 * f, d, H, GU, 1, 2, None, eb.EB_BF16),
+                                                  (d, f, GU, H, 0, 1, H, eb.EB_F32)):
+                w = eb.eb_qweights(eb.EB_Q8_0, 0, n, k, base)
+                base += (eb.lib.eb_qweights_bytes(eb.EB_Q8_0, n, k) + 4095) // 4096 * 4096
+                if stream16 and epi == 1:
+                    yt = eb.EB_BF16
+                ops.append(eb.eb_qlinear_op(w, x, y, m, eb.EB_BF16, yt, pro, epi,
+                                            G if pro else None, res, 1e-5, 0))
+        return (eb.eb_qlinear_op * len(ops))(*ops)
+
+    # m = 50: 6 narrow launches, 2 split down projections with their
+    # reductions and 4 prologue row kernels; fused, the second layer's first
+    # prologue runs in the first layer's down reduction
     monkeypatch.setenv("EB_STACK_FUSE_NORM", "0")
-    assert eb.lib.eb_qlinear_stack_launches(arr, len(ops)) == 16 + 4
-    # every prologue but the first follows the reduction of O or down
+    assert eb.lib.eb_qlinear_stack_launches(chain(50), 8) == 8 + 2 + 4
     monkeypatch.delenv("EB_STACK_FUSE_NORM")
-    assert eb.lib.eb_qlinear_stack_launches(arr, len(ops)) == 16 + 1
+    assert eb.lib.eb_qlinear_stack_launches(chain(50), 8) == 8 + 2 + 3
+    # m = 100: split projections; every prologue after a split O or down costs nothing
+    monkeypatch.setenv("EB_STACK_FUSE_NORM", "0")
+    unfused = eb.lib.eb_qlinear_stack_launches(chain(100), 8)
+    monkeypatch.delenv("EB_STACK_FUSE_NORM")
+    fused = eb.lib.eb_qlinear_stack_launches(chain(100), 8)
+    assert 8 + 4 < fused < unfused, (fused, unfused)
     # a 16-bit stream (no fp32 h to reduce into) keeps the row kernels
-    ops16 = [eb.eb_qlinear_op(o.w, o.x, o.y, o.m, o.x_type,
-                              eb.EB_BF16 if o.epilogue == 1 else o.y_type, o.prologue, o.epilogue,
-                              o.norm_weight, o.residual, o.norm_eps, 0) for o in ops]
-    arr16 = (eb.eb_qlinear_op * len(ops16))(*ops16)
-    assert eb.lib.eb_qlinear_stack_launches(arr16, len(ops16)) == 16 + 4
+    assert eb.lib.eb_qlinear_stack_launches(chain(100, stream16=True), 8) == unfused
 
 
 def test_qlinear_m0_is_noop(eb):
@@ -409,11 +420,16 @@ def test_library_imports_no_allocator(eb):
 
 
 def test_stack_counts_split_k_reduction(eb):
-    # a long-k op at m = 50 is split (product + ordered reduction); a large
-    # prefill op fills the GPU unsplit
-    split = [_op(eb, 1 * GB, 8 * GB, 9 * GB, k=4096, n=1024, m=50, qtype=eb.EB_Q8_0,
-                 xt=eb.EB_BF16)]
-    assert _launches(eb, split) == 2
+    # a long-k op at m = 100 or 50 is split (product + ordered reduction); at
+    # m = 50 and k <= 2048 the narrow kernel takes the whole of k in one
+    # launch; a large prefill op fills the GPU unsplit
+    for m in (100, 50):
+        split = [_op(eb, 1 * GB, 8 * GB, 9 * GB, k=4096, n=1024, m=m, qtype=eb.EB_Q8_0,
+                     xt=eb.EB_BF16)]
+        assert _launches(eb, split) == 2, m
+    narrow = [_op(eb, 1 * GB, 8 * GB, 9 * GB, k=2048, n=1024, m=50, qtype=eb.EB_Q8_0,
+                  xt=eb.EB_BF16)]
+    assert _launches(eb, narrow) == 1
     whole = [_op(eb, 1 * GB, 8 * GB, 9 * GB, k=3072, n=9216, m=4096, qtype=eb.EB_Q4_0,
                  xt=eb.EB_BF16)]
     assert _launches(eb, whole) == 1
@@ -425,13 +441,17 @@ def test_workspace_sizes(eb):
     q = eb.lib.eb_qlinear_workspace_bytes
     gemv = eb.eb_qlinear_op(_w(eb, k=4096, n=4096), 8 * GB, 9 * GB, 1, eb.EB_F16, eb.EB_F32)
     assert q(ctypes.byref(gemv), eb.EB_PATH_AUTO) == 0
-    plain = eb.eb_qlinear_op(_w(eb, k=4096, n=1024, data=1 * GB), 8 * GB, 9 * GB, 50, eb.EB_BF16,
+    plain = eb.eb_qlinear_op(_w(eb, k=4096, n=1024, data=1 * GB), 8 * GB, 9 * GB, 100, eb.EB_BF16,
                              eb.EB_F32)
     partial = q(ctypes.byref(plain), eb.EB_PATH_AUTO)
     assert partial > 0 and partial % 256 == 0  # split along k: fp32 partials
-    normed = eb.eb_qlinear_op(_w(eb, k=4096, n=1024, data=1 * GB), 8 * GB, 9 * GB, 50, eb.EB_BF16,
+    normed = eb.eb_qlinear_op(_w(eb, k=4096, n=1024, data=1 * GB), 8 * GB, 9 * GB, 100, eb.EB_BF16,
                               eb.EB_F32, eb.EB_PRO_RMSNORM, 0, G, None, 1e-5, 0)
-    assert q(ctypes.byref(normed), eb.EB_PATH_AUTO) == partial + 50 * 4096 * 2
+    assert q(ctypes.byref(normed), eb.EB_PATH_AUTO) == partial + 100 * 4096 * 2
+    # m <= 64, k <= 2048: the narrow kernel needs no partial sums
+    small = eb.eb_qlinear_op(_w(eb, k=2048, n=1024, data=1 * GB), 8 * GB, 9 * GB, 50, eb.EB_BF16,
+                             eb.EB_F32)
+    assert q(ctypes.byref(small), eb.EB_PATH_AUTO) == 0
     bad = eb.eb_qlinear_op(_w(eb, k=33), X, Y, 4, eb.EB_F16, eb.EB_F32)
     assert q(ctypes.byref(bad), eb.EB_PATH_AUTO) == 0
     # a fused run of small-m ops needs its table (and nothing else)

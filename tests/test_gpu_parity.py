@@ -128,6 +128,25 @@ def test_qlinear_mfma_parity(eb, oracle, qtype, xdtype, n, k):
     assert_parity(y, y_ref, bound, TOL_BF16, "mfma bf16 out")
 
 
+@pytest.mark.parametrize("qtype,xdtype", [("q8_0", torch.bfloat16), ("q4_0", torch.float16)])
+def test_narrow_kernel_edges(eb, oracle, qtype, xdtype):
+    """Lone small-m MFMA projections at the edges of the narrow kernel: every
+    count of 16-row blocks of m (1, 2, 4) and the m just past each, a ragged
+    last group of 16 weight rows, k at its limit (2048 = 64 blocks over 8
+    waves) and one block past it (the tiled kernel with a split of k), and an
+    uneven share of k between the waves (k = 11 blocks)."""
+    n = 1000 + 3
+    for k in (352, 2048, 2080):
+        w, x = _case(3000 + k, n, k, 64, xdtype)
+        qw = eb.quantize(w.to(DEV), qtype)
+        _, y_ref, bound = oracle_reference(oracle, qtype, w.numpy(), x)
+        for m in (1, 16, 17, 32, 33, 63, 64):
+            y = eb.qlinear(qw, x[:m].to(DEV), path="mfma")
+            assert_parity(y, y_ref[:m], bound[:m], TOL_F32, f"narrow m={m} k={k}")
+        y = eb.qlinear(qw, x[:40].to(DEV), out_dtype=torch.bfloat16, path="mfma")
+        assert_parity(y, y_ref[:40], bound[:40], TOL_BF16, f"narrow bf16 out k={k}")
+
+
 @pytest.mark.parametrize("qtype,xdtype", [("q8_0", torch.bfloat16), ("q4_0", torch.float16),
                                           ("q4_0", torch.bfloat16)])
 def test_every_mfma_tile_and_split(eb, oracle, qtype, xdtype):
