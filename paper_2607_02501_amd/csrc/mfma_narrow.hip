@@ -34,7 +34,6 @@ __device__ inline f32x4_t mfma16(const uint4 a, const uint4 b, f32x4_t c) {
                                                 __builtin_bit_cast(f16x8_t, b), c, 0, 0, 0);
 }
 
-constexpr int kNT = 16;     // weight rows per workgroup
 constexpr int kWaves = 8;   // waves per workgroup, splitting k
 constexpr int kAhead = 4;   // blocks loaded ahead of their MFMAs
 
@@ -68,23 +67,34 @@ __device__ inline void deq8(uint2 q, bool hi, float d, uint4 &wh, uint4 &wl) {
 }
 
 // MB: 16-row blocks of m (m <= 16 MB).  YT: EB_F32, or EB_BF16 for either
-// 16-bit output type (the op's type decides).
+// 16-bit output type (the op's type decides).  Measured on 50-row chains,
+// more weight rows per workgroup (32 or 64, the waves split between row
+// groups and slices of k) were slower: a workgroup's time grows with the
+// blocks each wave walks, at about 1.2 us per block, since every workgroup
+// also reads all of x through its compute unit.
 template <int QT, int XT, int YT, int MB, bool HL>
 __global__ void __launch_bounds__(kWaves * 64)
     mm_narrow_kernel(const uint8_t *__restrict__ wdata, int64_t n, int64_t k, int64_t d_off,
                      int64_t ds, const uint16_t *__restrict__ x, int m, void *__restrict__ y, int yt,
                      Fuse f) {
   static_assert(!HL || XT == EB_BF16, "hi/lo pairs are for bfloat16 activations");
+  constexpr int KS = kWaves;                        // slices of k
+  constexpr int NT = 16;                            // weight rows per workgroup
+  constexpr int PAIRS = MB * 64 * 2;                // output pairs per workgroup
+  constexpr int PPT = (PAIRS + kWaves * 64 - 1) / (kWaves * 64);
   constexpr int QSB = (QT == EB_Q8_0) ? 32 : 16;  // code bytes per block
-  __shared__ f32x4_t red[kWaves][MB][64];
+  __shared__ f32x4_t red[KS][MB][64];
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  // consecutive workgroups start on different slices, so that they do not
+  // all read the same activations at once
+  const int slice = (wave + (int)(blockIdx.x % KS)) % KS;
   const int r16 = lane & 15, g4 = lane >> 4;
-  const int64_t n0 = (int64_t)blockIdx.x * kNT;
-  const int rows_n = (int)min((int64_t)kNT, n - n0);
+  const int64_t n0 = (int64_t)blockIdx.x * NT;
+  const int rows_n = (int)min((int64_t)NT, n - n0);
   const int nb = (int)(k / kQK);
-  const int b0 = (int)((int64_t)nb * wave / kWaves), b1 = (int)((int64_t)nb * (wave + 1) / kWaves);
+  const int b0 = (int)((int64_t)nb * slice / KS), b1 = (int)((int64_t)nb * (slice + 1) / KS);
 
   // Raw buffer descriptors over this workgroup's rows (rows past n read
   // zeros) and over x's m rows (rows past m read zeros).
@@ -93,41 +103,77 @@ __global__ void __launch_bounds__(kWaves * 64)
   const auto dr = rsrc(wdata + d_off + n0 * drow, (uint32_t)rows_n * drow);
   const uint32_t xrow = (uint32_t)k * 2;
   const auto xr = rsrc(x, (uint32_t)m * xrow);
-  // lane parts of the offsets: Q8_0 codes 8 g4 .. + 7 of the block, Q4_0 the
-  // bytes 8 (g4 & 1) .. + 7 (nibble g4 >> 1)
-  const uint32_t qlane = (uint32_t)r16 * qrow + (QT == EB_Q8_0 ? 8u * g4 : 8u * (g4 & 1));
-  const uint32_t dlane = (uint32_t)r16 * drow;
+  // lane parts of the offsets: row r16 of the workgroup; Q8_0 codes 8 g4 ..
+  // + 7 of the block, Q4_0 the bytes 8 (g4 & 1) .. + 7 (nibble g4 >> 1)
+  const uint32_t wr = (uint32_t)r16;
+  const uint32_t qlane = wr * qrow + (QT == EB_Q8_0 ? 8u * g4 : 8u * (g4 & 1));
+  const uint32_t dlane = wr * drow;
   const uint32_t xlane = (uint32_t)r16 * xrow + 16u * g4;
   const bool nib_hi = (g4 >> 1) != 0;
+
+  // The residuals of this thread's outputs are loaded first, so that their
+  // latency passes under the product's.  Every load below is issued
+  // unconditionally (an offset past the end of its buffer reads zero without
+  // touching memory), so that each wait counts only the loads it needs.
+  constexpr uint32_t kPast = 0x80000000u;  // past every descriptor here
+  const int t = threadIdx.x;
+  float res[PPT][2];
+  if (f.epi == EB_EPI_ADD) {
+    constexpr uint32_t es = (YT == EB_F32) ? 4 : 2;
+    const auto rr = rsrc(f.r, (uint32_t)(m * n) * es);
+#pragma unroll
+    for (int i = 0; i < PPT; ++i) {
+      const int e = t + i * kWaves * 64;
+      const int mb = e / 128, l = (e % 128) / 2, p = e % 2;
+      const int col = 16 * mb + (l & 15), nl = 4 * (l >> 4) + 2 * p;
+      const uint32_t o = (uint32_t)((int64_t)col * n + n0 + nl) * es;
+      const bool ok0 = e < PAIRS && col < m && nl < rows_n, ok1 = ok0 && nl + 1 < rows_n;
+      if constexpr (YT == EB_F32) {
+        res[i][0] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rr, (int)(ok0 ? o : kPast), 0, 0));
+        res[i][1] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rr, (int)(ok1 ? o + 4 : kPast), 0, 0));
+      } else {
+        res[i][0] = from_y16(__builtin_amdgcn_raw_buffer_load_b16(rr, (int)(ok0 ? o : kPast), 0, 0), yt);
+        res[i][1] = from_y16(__builtin_amdgcn_raw_buffer_load_b16(rr, (int)(ok1 ? o + 2 : kPast), 0, 0), yt);
+      }
+    }
+  }
 
   struct Blk {
     uint2 q;
     uint16_t d;
     uint4 xb[MB];
   };
-  auto load = [&](Blk &B, int b) __attribute__((always_inline)) {
-    const uint32_t qo = qlane + (uint32_t)b * QSB;
-    const auto v = __builtin_amdgcn_raw_buffer_load_b64(qr, (int)qo, 0, 0);
+  // block j of this wave's slice; past the slice, zeros (code 0 with scale 0
+  // and activations 0 add exactly nothing to the accumulators)
+  const int nbw = b1 - b0;
+  auto load = [&](Blk &B, int j) __attribute__((always_inline)) {
+    const bool ok = j < nbw;
+    const uint32_t b = (uint32_t)(b0 + j);
+    const auto v = __builtin_amdgcn_raw_buffer_load_b64(qr, (int)(ok ? qlane + b * QSB : kPast), 0, 0);
     B.q = make_uint2(v[0], v[1]);
-    B.d = __builtin_amdgcn_raw_buffer_load_b16(dr, (int)(dlane + 2u * b), 0, 0);
+    B.d = __builtin_amdgcn_raw_buffer_load_b16(dr, (int)(ok ? dlane + 2u * b : kPast), 0, 0);
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb)
-      B.xb[mb] = bload(xr, xlane + (uint32_t)mb * 16u * xrow + (uint32_t)b * 64u);
+      B.xb[mb] = bload(xr, ok ? xlane + (uint32_t)mb * 16u * xrow + b * 64u : kPast);
   };
 
   f32x4_t acc[MB];
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb) acc[mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
+  // issued block by block, each one's loads together, so that the wait
+  // before a block's MFMAs leaves the later blocks' loads in flight
   Blk S0, S1, S2, S3;
-  int b = b0;
-  if (b0 + 0 < b1) load(S0, b0 + 0);
-  if (b0 + 1 < b1) load(S1, b0 + 1);
-  if (b0 + 2 < b1) load(S2, b0 + 2);
-  if (b0 + 3 < b1) load(S3, b0 + 3);
+  load(S0, 0);
+  __builtin_amdgcn_sched_barrier(0);
+  load(S1, 1);
+  __builtin_amdgcn_sched_barrier(0);
+  load(S2, 2);
+  __builtin_amdgcn_sched_barrier(0);
+  load(S3, 3);
+  __builtin_amdgcn_sched_barrier(0);
   // one block: its MFMAs, then its registers take the block kAhead further
-  auto step = [&](Blk &B) __attribute__((always_inline)) -> bool {
-    if (b >= b1) return false;
+  auto step = [&](Blk &B, int j) __attribute__((always_inline)) {
     uint4 wh, wl;
     deq8<QT, XT, HL>(B.q, nib_hi, (float)__builtin_bit_cast(_Float16, B.d), wh, wl);
 #pragma unroll
@@ -137,46 +183,57 @@ __global__ void __launch_bounds__(kWaves * 64)
       for (int mb = 0; mb < MB; ++mb) acc[mb] = mfma16<XT>(wl, B.xb[mb], acc[mb]);
     }
     __builtin_amdgcn_sched_barrier(0);
-    if (b + kAhead < b1) load(B, b + kAhead);
-    ++b;
-    return true;
+    load(B, j + kAhead);
+    __builtin_amdgcn_sched_barrier(0);
   };
-  while (step(S0) && step(S1) && step(S2) && step(S3)) {
+  static_assert(kAhead == 4, "four register sets");
+  for (int j = 0; j < nbw; j += 4) {
+    step(S0, j);
+    step(S1, j + 1);
+    step(S2, j + 2);
+    step(S3, j + 3);
   }
 
-  // partial tiles of the waves, added in wave order
+  // partial tiles of the slices, added in slice order
 #pragma unroll
-  for (int mb = 0; mb < MB; ++mb) red[wave][mb][lane] = acc[mb];
+  for (int mb = 0; mb < MB; ++mb) red[slice][mb][lane] = acc[mb];
   __syncthreads();
-  // thread t: output pair (rows 2 p, 2 p + 1 of the tile) of one column:
-  // flat index e = t over (mb, lane, pair), pair p in 0..1 of the lane's 4 rows
-  const int t = threadIdx.x;
-  if (t >= MB * 64 * 2) return;
-  const int mb = t / 128, rest = t % 128, l = rest / 2, p = rest % 2;
-  float v0 = 0.f, v1 = 0.f;
+  // element e of this thread: output pair (rows 2 p, 2 p + 1 of the lane's 4
+  // rows) of one column; e runs over (mb, lane, pair)
 #pragma unroll
-  for (int w = 0; w < kWaves; ++w) {
-    const f32x4_t a = red[w][mb][l];
-    v0 += p ? a[2] : a[0];
-    v1 += p ? a[3] : a[1];
+  for (int i = 0; i < PPT; ++i) {
+    const int e = t + i * kWaves * 64;
+    if (e >= PAIRS) break;
+    const int mb = e / 128, l = (e % 128) / 2, p = e % 2;
+    float v0 = 0.f, v1 = 0.f;
+#pragma unroll
+    for (int w = 0; w < KS; ++w) {
+      const f32x4_t a = red[w][mb][l];
+      v0 += p ? a[2] : a[0];
+      v1 += p ? a[3] : a[1];
+    }
+    const int col = 16 * mb + (l & 15);               // row of x / y
+    const int nl = 4 * (l >> 4) + 2 * p;              // first of the two rows
+    if (col >= m || nl >= rows_n) continue;
+    if (f.epi == EB_EPI_GLU) {  // n even: the pair (gate, up) is complete
+      store_y(y, (int64_t)col * (n / 2) + (n0 + nl) / 2, silu_mul(v0, v1), yt);
+      continue;
+    }
+    const int64_t o = (int64_t)col * n + n0 + nl;
+    if (f.epi == EB_EPI_ADD) {  // the residual shares the output's type
+      v0 += res[i][0];
+      v1 += res[i][1];
+    }
+    store_y(y, o, v0, yt);
+    if (nl + 1 < rows_n) store_y(y, o + 1, v1, yt);
   }
-  const int col = 16 * mb + (l & 15);         // row of x / y
-  const int nl = 4 * (l >> 4) + 2 * p;         // first of the two tile rows
-  if (col >= m || nl >= rows_n) return;
-  if (f.epi == EB_EPI_GLU) {  // n even: the pair (gate, up) is complete
-    store_y(y, (int64_t)col * (n / 2) + (n0 + nl) / 2, silu_mul(v0, v1), yt);
-    return;
-  }
-  const int64_t o = (int64_t)col * n + n0 + nl;
-  put_y(y, o, v0, yt, f);
-  if (nl + 1 < rows_n) put_y(y, o + 1, v1, yt, f);
 }
 
 template <int QT, int XT, int YT, bool HL>
 hipError_t launch_mb(const void *wdata, int64_t n, int64_t k, const void *x, int64_t m, void *y,
                      int32_t yt, const Fuse &f, hipStream_t s) {
   const Layout L = layout_of(QT, n, k);
-  const unsigned grid = (unsigned)((n + kNT - 1) / kNT);
+  const unsigned grid = (unsigned)((n + 15) / 16);
   const auto *xp = static_cast<const uint16_t *>(x);
   const auto *wp = static_cast<const uint8_t *>(wdata);
   if (m <= 16)
@@ -210,9 +267,10 @@ bool narrow_fits(int64_t m, int64_t n, int64_t k) {
   // costs more than it saves: measured on the action-expert chain, k = 1024
   // projections take 8-10 us instead of about 16 us (tiled kernel split along
   // k plus its reduction), but the k = 4096 down projection 22 us instead of
-  // 16.  Every byte span of a workgroup stays within 32-bit buffer offsets.
-  return m >= 1 && m <= kNarrowMaxM && k <= kNarrowMaxK && (int64_t)m * k * 2 <= 0x7fffffffLL &&
-         (int64_t)kNT * (k / kQK) * 34 <= 0x7fffffffLL && (n + kNT - 1) / kNT <= 0x7fffffffLL;
+  // 16.  Offsets in x, a workgroup's weights and y stay below 2^31 (an
+  // offset of 2^31 reads zero).
+  return m >= 1 && m <= kNarrowMaxM && k <= kNarrowMaxK && (int64_t)m * k * 2 < 0x7fff0000LL &&
+         (int64_t)64 * (k / kQK) * 34 < 0x7fff0000LL && (int64_t)m * n * 4 < 0x7fff0000LL;
 }
 
 hipError_t launch_mfma_narrow(int32_t type, const void *wdata, int64_t n, int64_t k, const void *x,
