@@ -27,6 +27,23 @@
  *   Dequant: w_hat = q * d16 (Q8_0) or (nibble - 8) * d16 (Q4_0), exact in
  *   binary64.
  *
+ *   Q6_S super-block (210 bytes, 256 weights = 16 sub-blocks of 16): the
+ *   6-bit configuration of the same evaluation; the paper names no format, so
+ *   this one is defined here (a two-level "super-block" scale):
+ *     m_j = the signed element of largest magnitude of sub-block j (first
+ *           index on ties, starting from +0.0);  s_j = fl32(m_j / -32)
+ *     amax = max_j |s_j|;  d32 = fl32(amax / 127);  d16 = binary16_RNE(d32)
+ *     sc_j = clamp(round_half_away_from_zero(s_j / d16), -127, 127)
+ *            (0 for every j when d16 == 0)
+ *     e_j  = d16 * sc_j   (exact: at most 11 + 7 significant bits)
+ *     q_i  = clamp(floor(x_i / e_j + 1/2), -32, 31)   (0 when e_j == 0)
+ *     u_i  = q_i + 32 in 0..63
+ *   Bytes: d16, then sc_0..sc_15 as int8, then 8 chunks of 24 bytes, chunk c
+ *   holding elements 32c .. 32c + 31 (local index i): byte i (0..15) =
+ *   (u_i & 15) | (u_{i+16} & 15) << 4, byte 16 + t (t = 0..7) =
+ *   (u_t >> 4) | (u_{t+8} >> 4) << 2 | (u_{t+16} >> 4) << 4 | (u_{t+24} >> 4) << 6.
+ *   Dequant: w_hat_i = (u_i - 32) * d16 * sc_{i/16}, exact in binary64.
+ *
  * Readings taken where the format description is silent (each is listed with
  * its reason in the design notes of the repository):
  *   - codes are rounded against the *stored* binary16 scale d16, so that every
@@ -35,7 +52,8 @@
  *   - ties: Q8_0 rounds half away from zero, Q4_0 rounds half up;
  *   - x / d16 is evaluated in binary64: x has 24 significant bits and d16 at
  *     most 11, so the binary64 quotient can neither create nor destroy a tie
- *     and every rounding decision equals the one on the exact quotient.
+ *     and every rounding decision equals the one on the exact quotient; the
+ *     same holds for s_j / d16 and x_i / e_j of Q6_S (e_j: at most 18 bits).
  *
  * Matmul: every product and sum in binary64, in plain k order, one output at
  * a time.  Alongside y it returns bound[m][n] = sum_k |x[m][k]| * |w_hat[n][k]|,
@@ -61,11 +79,14 @@
 
 #define ORACLE_Q8_0 1
 #define ORACLE_Q4_0 2
+#define ORACLE_Q6_S 3
 
 #define ORACLE_X_F16 1
 #define ORACLE_X_BF16 2
 
 #define QK 32
+#define QK6 256 /* weights per Q6_S super-block */
+#define QS6 16  /* weights per Q6_S sub-block */
 
 /* ---------------------------------------------------------------------- */
 /* binary16 / bfloat16 encode and decode, written from the IEEE 754 formats */
@@ -196,9 +217,69 @@ static void quantize_block_q4_0(const float *x, uint8_t *blk) {
   for (int i = 0; i < QK / 2; ++i) blk[2 + i] = (uint8_t)(nib[i] | (nib[i + QK / 2] << 4));
 }
 
+static void quantize_block_q6_s(const float *x, uint8_t *blk) {
+  float s[QK6 / QS6];
+  float amax = 0.0f;
+  for (int j = 0; j < QK6 / QS6; ++j) {
+    float mag = 0.0f, m = 0.0f;
+    for (int i = 0; i < QS6; ++i) {
+      float a = fabsf(x[j * QS6 + i]);
+      if (a > mag) {
+        mag = a;
+        m = x[j * QS6 + i];
+      }
+    }
+    s[j] = m / -32.0f;
+    if (fabsf(s[j]) > amax) amax = fabsf(s[j]);
+  }
+  float d32 = amax / 127.0f;
+  uint16_t d16 = oracle_float_to_half_rne(d32);
+  double d = oracle_half_to_double(d16);
+  put_d16(blk, d16);
+  int sc[QK6 / QS6];
+  for (int j = 0; j < QK6 / QS6; ++j) {
+    sc[j] = 0;
+    if (d != 0.0) {
+      double t = round((double)s[j] / d); /* half away from zero */
+      if (t > 127.0) t = 127.0;
+      if (t < -127.0) t = -127.0;
+      sc[j] = (int)t;
+    }
+    blk[2 + j] = (uint8_t)(int8_t)sc[j];
+  }
+  int u[QK6];
+  for (int i = 0; i < QK6; ++i) {
+    double e = d * (double)sc[i / QS6]; /* exact */
+    int q = 0;
+    if (e != 0.0) {
+      double t = floor((double)x[i] / e + 0.5); /* round half up */
+      if (t > 31.0) t = 31.0;
+      if (t < -32.0) t = -32.0;
+      q = (int)t;
+    }
+    u[i] = q + 32;
+  }
+  for (int c = 0; c < QK6 / 32; ++c) {
+    uint8_t *ch = blk + 2 + QK6 / QS6 + 24 * c;
+    const int *uc = u + 32 * c;
+    for (int i = 0; i < 16; ++i) ch[i] = (uint8_t)((uc[i] & 15) | (uc[i + 16] & 15) << 4);
+    for (int t = 0; t < 8; ++t)
+      ch[16 + t] = (uint8_t)((uc[t] >> 4) | (uc[t + 8] >> 4) << 2 | (uc[t + 16] >> 4) << 4 |
+                             (uc[t + 24] >> 4) << 6);
+  }
+}
+
 int64_t oracle_block_bytes(int qtype) {
   if (qtype == ORACLE_Q8_0) return 2 + QK;
   if (qtype == ORACLE_Q4_0) return 2 + QK / 2;
+  if (qtype == ORACLE_Q6_S) return 2 + QK6 / QS6 + QK6 * 6 / 8;
+  return -1;
+}
+
+/* Weights per block: 32, or 256 for the Q6_S super-block. */
+int64_t oracle_block_elems(int qtype) {
+  if (qtype == ORACLE_Q8_0 || qtype == ORACLE_Q4_0) return QK;
+  if (qtype == ORACLE_Q6_S) return QK6;
   return -1;
 }
 
@@ -212,25 +293,28 @@ typedef struct {
 
 static void *run_qjob(void *arg) {
   qjob_t *J = (qjob_t *)arg;
-  int64_t bb = oracle_block_bytes(J->qtype);
-  int64_t nb = J->k / QK;
+  int64_t bb = oracle_block_bytes(J->qtype), be = oracle_block_elems(J->qtype);
+  int64_t nb = J->k / be;
   for (int64_t r = J->begin; r < J->end; ++r)
     for (int64_t b = 0; b < nb; ++b) {
-      const float *src = J->w + r * J->k + b * QK;
+      const float *src = J->w + r * J->k + b * be;
       uint8_t *dst = J->out + (r * nb + b) * bb;
       if (J->qtype == ORACLE_Q8_0)
         quantize_block_q8_0(src, dst);
-      else
+      else if (J->qtype == ORACLE_Q4_0)
         quantize_block_q4_0(src, dst);
+      else
+        quantize_block_q6_s(src, dst);
     }
   return NULL;
 }
 
-/* w: fp32 [n][k] row-major; out: n * (k/32) canonical blocks, row by row.
- * Threads (nthreads <= 1: the calling thread) only split the rows. */
+/* w: fp32 [n][k] row-major; out: n * (k/E) canonical blocks (E weights per
+ * block), row by row.  Threads (nthreads <= 1: the calling thread) only split
+ * the rows. */
 int oracle_quantize(int qtype, const float *w, int64_t n, int64_t k, uint8_t *out, int nthreads) {
-  int64_t bb = oracle_block_bytes(qtype);
-  if (bb < 0 || n < 0 || k < 0 || k % QK != 0 || (!w && n * k) || (!out && n * k))
+  int64_t bb = oracle_block_bytes(qtype), be = oracle_block_elems(qtype);
+  if (bb < 0 || n < 0 || k < 0 || k % be != 0 || (!w && n * k) || (!out && n * k))
     return ORACLE_EINVAL;
   if (nthreads < 1) nthreads = 1;
   if (nthreads > n) nthreads = n > 0 ? (int)n : 1;
@@ -272,9 +356,27 @@ static double code_at(int qtype, const uint8_t *blk, int j) {
   return (double)(nibble - 8);
 }
 
-/* One row of w_hat (k values) from the row's nb = k/32 blocks. */
+/* Code u_i (0..63) of element i of a Q6_S super-block. */
+static int q6_code(const uint8_t *blk, int i) {
+  const uint8_t *ch = blk + 2 + QK6 / QS6 + 24 * (i / 32);
+  int l = i % 32;
+  int lo = (l < 16) ? (ch[l] & 15) : (ch[l - 16] >> 4);
+  int hi = (ch[16 + l % 8] >> (2 * (l / 8))) & 3;
+  return lo | hi << 4;
+}
+
+/* One row of w_hat (k values) from the row's k/E blocks. */
 static void dequant_row(int qtype, const uint8_t *row_blocks, int64_t k, double *dst) {
   int64_t bb = oracle_block_bytes(qtype);
+  if (qtype == ORACLE_Q6_S) {
+    for (int64_t b = 0; b < k / QK6; ++b) {
+      const uint8_t *blk = row_blocks + b * bb;
+      double d = oracle_half_to_double(get_d16(blk));
+      for (int i = 0; i < QK6; ++i)
+        dst[b * QK6 + i] = (double)(q6_code(blk, i) - 32) * (d * (double)(int8_t)blk[2 + i / QS6]);
+    }
+    return;
+  }
   for (int64_t b = 0; b < k / QK; ++b) {
     const uint8_t *blk = row_blocks + b * bb;
     double d = oracle_half_to_double(get_d16(blk));
@@ -283,9 +385,9 @@ static void dequant_row(int qtype, const uint8_t *row_blocks, int64_t k, double 
 }
 
 int oracle_dequant(int qtype, const uint8_t *blocks, int64_t n, int64_t k, double *w_hat) {
-  int64_t bb = oracle_block_bytes(qtype);
-  if (bb < 0 || n < 0 || k < 0 || k % QK != 0) return ORACLE_EINVAL;
-  for (int64_t r = 0; r < n; ++r) dequant_row(qtype, blocks + r * (k / QK) * bb, k, w_hat + r * k);
+  int64_t bb = oracle_block_bytes(qtype), be = oracle_block_elems(qtype);
+  if (bb < 0 || n < 0 || k < 0 || k % be != 0) return ORACLE_EINVAL;
+  for (int64_t r = 0; r < n; ++r) dequant_row(qtype, blocks + r * (k / be) * bb, k, w_hat + r * k);
   return ORACLE_OK;
 }
 
@@ -307,12 +409,12 @@ typedef struct {
 
 static void *run_job(void *arg) {
   job_t *J = (job_t *)arg;
-  int64_t bb = oracle_block_bytes(J->qtype);
+  int64_t bb = oracle_block_bytes(J->qtype), be = oracle_block_elems(J->qtype);
   double *wrow = (double *)malloc(sizeof(double) * (size_t)(J->k ? J->k : 1));
   if (!wrow) return (void *)1;
   for (int64_t c = J->begin; c < J->end; ++c) {
     int64_t n = J->cols[c];
-    dequant_row(J->qtype, J->blocks + n * (J->k / QK) * bb, J->k, wrow);
+    dequant_row(J->qtype, J->blocks + n * (J->k / be) * bb, J->k, wrow);
     for (int64_t i = 0; i < J->m; ++i) {
       const double *xr = J->xd + i * J->k;
       double s = 0.0, b = 0.0;
@@ -337,7 +439,8 @@ static void *run_job(void *arg) {
 int oracle_qlinear(int qtype, const uint8_t *blocks, int64_t n, int64_t k, const uint16_t *x,
                    int xdtype, int64_t m, const int64_t *cols, int64_t ncols, double *y,
                    double *bound, int nthreads) {
-  if (oracle_block_bytes(qtype) < 0 || k <= 0 || k % QK != 0 || n <= 0 || m < 0 || ncols < 0)
+  if (oracle_block_bytes(qtype) < 0 || k <= 0 || k % oracle_block_elems(qtype) != 0 || n <= 0 ||
+      m < 0 || ncols < 0)
     return ORACLE_EINVAL;
   if (xdtype != ORACLE_X_F16 && xdtype != ORACLE_X_BF16) return ORACLE_EINVAL;
   for (int64_t c = 0; c < ncols; ++c)

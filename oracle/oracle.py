@@ -7,7 +7,9 @@ own shared object from ``oracle.c`` with gcc.
 
 Every function follows the definition in the header of ``oracle.c``: the
 Q8_0 / Q4_0 block formats (32 weights per block along k, one binary16 scale)
-that realise the paper's 8-bit and 4-bit configurations (section 4, Table 3),
+and the Q6_S super-block format (256 weights, 16 int8 sub-block scales under
+one binary16 scale, 6-bit codes) that realise the paper's 8-, 4- and 6-bit
+configurations (section 4, Table 3),
 and the binary64 linear layer y = x . w_hat^T, plus the decoder-layer steps
 fused around it (section 3.2, operator fusion): RMS normalisation before a
 projection, the SiLU-gated product of a gate/up pair and the residual addition
@@ -23,9 +25,11 @@ import numpy as np
 
 Q8_0 = 1
 Q4_0 = 2
+Q6_S = 3
 X_F16 = 1
 X_BF16 = 2
 QK = 32
+BLOCK_ELEMS = {Q8_0: 32, Q4_0: 32, Q6_S: 256}
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "oracle.c")
@@ -57,6 +61,8 @@ class Oracle:
         L.oracle_float_to_half_rne.argtypes = [ctypes.c_float]
         L.oracle_block_bytes.restype = ctypes.c_int64
         L.oracle_block_bytes.argtypes = [ctypes.c_int]
+        L.oracle_block_elems.restype = ctypes.c_int64
+        L.oracle_block_elems.argtypes = [ctypes.c_int]
         L.oracle_quantize.restype = ctypes.c_int
         L.oracle_quantize.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_int64,
                                       ctypes.c_int64, ctypes.c_void_p, ctypes.c_int]
@@ -93,11 +99,12 @@ class Oracle:
 
     # -- quantize / dequantize -----------------------------------------------
     def quantize(self, qtype: int, w: np.ndarray, nthreads: int = 1) -> np.ndarray:
-        """fp32 W[n, k] -> canonical blocks, uint8 [n, k/32, block_bytes]."""
+        """fp32 W[n, k] -> canonical blocks, uint8 [n, k/E, block_bytes], E =
+        BLOCK_ELEMS[qtype] weights per block."""
         w = np.ascontiguousarray(w, dtype=np.float32)
         n, k = w.shape
         bb = self.block_bytes(qtype)
-        out = np.zeros((n, k // QK, bb), dtype=np.uint8)
+        out = np.zeros((n, k // BLOCK_ELEMS[qtype], bb), dtype=np.uint8)
         rc = self.lib.oracle_quantize(qtype, w.ctypes.data, n, k, out.ctypes.data, int(nthreads))
         if rc != 0:
             raise ValueError("oracle_quantize rejected the arguments")
@@ -105,7 +112,7 @@ class Oracle:
 
     def dequant(self, qtype: int, blocks: np.ndarray, n: int, k: int) -> np.ndarray:
         blocks = np.ascontiguousarray(blocks, dtype=np.uint8)
-        assert blocks.size == n * (k // QK) * self.block_bytes(qtype)
+        assert blocks.size == n * (k // BLOCK_ELEMS[qtype]) * self.block_bytes(qtype)
         out = np.empty((n, k), dtype=np.float64)
         rc = self.lib.oracle_dequant(qtype, blocks.ctypes.data, n, k, out.ctypes.data)
         if rc != 0:
@@ -119,7 +126,7 @@ class Oracle:
         Returns (y, bound), float64 [m, len(cols)] (all n columns when cols is None).
         """
         blocks = np.ascontiguousarray(blocks, dtype=np.uint8)
-        assert blocks.size == n * (k // QK) * self.block_bytes(qtype)
+        assert blocks.size == n * (k // BLOCK_ELEMS[qtype]) * self.block_bytes(qtype)
         x_bits = np.ascontiguousarray(x_bits, dtype=np.uint16)
         if x_bits.ndim == 1:
             x_bits = x_bits.reshape(1, -1)
