@@ -11,6 +11,7 @@ paper_2607_02501_amd/workloads.py):
 
   q8_0_m1_2048              one Q8_0 2048x2048 decode linear (128 distinct copies per pass)
   q4_0_decode_7b            batch-1 decode through a 32-layer 7B-class Q4_0 stack
+  q6_s_decode_7b            the same decode stack in the 6-bit Q6_S format
   q8_0_vlm_prefill_816      VLM-backbone prefill, m = 816, 18 layers of d = 2048
   q8_0_action_expert_50x10  action-expert denoising, m = 50, 18 layers x 10 steps
   q4_0_video_wam_4096       video world-action backbone, m = 4096, 28 layers of d = 3072
@@ -62,7 +63,8 @@ MAX_HOST_THREADS = 16
 ALL_CONFIGS = [("q8_0_m1_2048", False), ("q4_0_video_wam_4096", False),
                ("q8_0_vlm_prefill_816", False), ("q8_0_vlm_prefill_816", True),
                ("q8_0_action_expert_50x10", False), ("q8_0_action_expert_50x10", True),
-               ("q4_0_decode_7b", False), ("q4_0_decode_7b", True)]
+               ("q4_0_decode_7b", False), ("q4_0_decode_7b", True),
+               ("q6_s_decode_7b", False), ("q6_s_decode_7b", True)]
 HEADLINE = ("q4_0_decode_7b", True)
 
 
@@ -97,7 +99,7 @@ def parse():
 
 
 def weight_bytes(qtype, n, k):
-    return n * (k // 32) * (34 if qtype == "q8_0" else 18)
+    return n * (k // {"q8_0": 32, "q4_0": 32, "q6_s": 256}[qtype]) * {"q8_0": 34, "q4_0": 18, "q6_s": 210}[qtype]
 
 
 def op_bytes(qtype, m, n, k):
@@ -326,7 +328,7 @@ def cpu_baseline(args, wl, W, dev, mfma_bound, seconds):
     orc = O.get()
     cores = min(O.available_cores(), MAX_HOST_THREADS)
     rows = min(args.cpu_rows or (wl.m if wl.m <= 8 else 8), wl.m)
-    qt = O.Q8_0 if wl.qtype == "q8_0" else O.Q4_0
+    qt = {"q8_0": O.Q8_0, "q4_0": O.Q4_0, "q6_s": O.Q6_S}[wl.qtype]
     xt = O.X_F16 if wl.x_dtype == torch.float16 else O.X_BF16
     cache, cache_bytes = [], 0
     secs, nbytes, flops, ops, layers_seen = 0.0, 0, 0, 0, 0
@@ -382,7 +384,7 @@ def cpu_baseline_chain(args, wl, W, dev, mfma_bound, seconds):
     orc = O.get()
     cores = min(O.available_cores(), MAX_HOST_THREADS)
     rows = min(args.cpu_rows or (wl.m if wl.m <= 8 else 8), wl.m)
-    qt = O.Q8_0 if wl.qtype == "q8_0" else O.Q4_0
+    qt = {"q8_0": O.Q8_0, "q4_0": O.Q4_0, "q6_s": O.Q6_S}[wl.qtype]
     xt = O.X_F16 if wl.x_dtype == torch.float16 else O.X_BF16
     (_, d, n_qkv), _, (_, _, n_gu), (_, f, _) = wl.projections
     h = W.normal((wl.m, d), W.seed_of(wl.wid, 4095, 15, 3), dev)[:rows].cpu().numpy().astype(np.float64)

@@ -20,10 +20,23 @@
  *   When d16 == 0 every code is 0.  Codes are rounded against the stored
  *   binary16 scale, exactly (the rounding decision equals the one on the exact
  *   quotient).
+ *   EB_Q6_S (the 6-bit configuration; the paper names no format, this one is
+ *            defined here): super-blocks of 256 weights in 16 sub-blocks of 16.
+ *            m_j = signed element of largest |w| of sub-block j (first index
+ *            wins), s_j = fl32(m_j / -32); d16 = binary16_RNE(fl32(max_j |s_j|
+ *            / 127)); sc_j = clamp(round_half_away(s_j / d16), -127, 127)
+ *            (0 when d16 == 0); e_j = d16 * sc_j;
+ *            q_i = clamp(floor(w_i / e_j + 1/2), -32, 31) (0 when e_j == 0),
+ *            stored as u_i = q_i + 32; w_hat = q * e_j.  k % 256 == 0.
  *
  * Canonical byte layout (array of blocks, row by row, k/32 blocks per row):
  *   Q8_0 block, 34 bytes: d16 little-endian, then q_0..q_31 as int8.
  *   Q4_0 block, 18 bytes: d16, then 16 bytes, byte i = (c_i + 8) | (c_{i+16} + 8) << 4.
+ *   Q6_S super-block, 210 bytes (k/256 per row): d16, sc_0..sc_15 (int8),
+ *     then 8 chunks of 24 bytes, chunk c holding weights 32c .. 32c + 31
+ *     (local index i): byte i (0..15) = (u_i & 15) | (u_{i+16} & 15) << 4,
+ *     byte 16 + t (t = 0..7) = (u_t >> 4) | (u_{t+8} >> 4) << 2 |
+ *     (u_{t+16} >> 4) << 4 | (u_{t+24} >> 4) << 6.
  *
  * Device layout ("planar", what eb_quantize_* write and eb_qlinear reads),
  * inside one buffer of eb_qweights_bytes(type, n, k) bytes:
@@ -33,6 +46,10 @@
  *   d plane at byte offset d_off = round_up(n * (k/32) * QB, 256): row r, block
  *     b at binary16 index r * DS + b, DS = round_up(k/32, 8); entries b >= k/32
  *     are zero.
+ *   Q6_S: qs plane of 24-byte chunks (QB = 24 per 32 weights, the chunk bytes
+ *     above); int8 sub-scale plane at sc_off = round_up(n * (k/32) * 24, 256),
+ *     row r at byte r * (k/16); d plane at round_up(sc_off + n * (k/16), 256),
+ *     row stride DS = round_up(k/256, 8) binary16 entries.
  *   It holds the canonical bytes, rearranged; eb_qweights_to_canonical /
  *   eb_qweights_from_canonical convert in either direction.
  *
@@ -54,7 +71,8 @@
  *     block (the binary16 scale must not overflow).
  *   - Outputs must not overlap inputs (one exception: the residual of a
  *     residual-adding epilogue may be the output itself, see below).
- *   - Sizes: 1 <= n <= 2^31 - 1, 32 <= k <= 2^24 with k % 32 == 0,
+ *   - Sizes: 1 <= n <= 2^31 - 1, 32 <= k <= 2^24 with k % 32 == 0 (k % 256
+ *     == 0 for Q6_S),
  *     0 <= m <= 2^24 (m == 0 is a no-op).
  *   - Thread-compatible: concurrent calls must use different output buffers.
  */
@@ -80,6 +98,7 @@ typedef int32_t eb_status;
 /* quantization formats */
 #define EB_Q8_0 1
 #define EB_Q4_0 2
+#define EB_Q6_S 3
 
 /* element types */
 #define EB_F32 0
@@ -88,7 +107,7 @@ typedef int32_t eb_status;
 
 /* kernel paths for eb_qlinear_ex */
 #define EB_PATH_AUTO 0 /* pick by m, qtype and shape (measured crossover) */
-#define EB_PATH_GEMV 1 /* bandwidth-bound GEMV, requires m <= 8 and m' * k <= 65536, m' = m rounded up to 1, 2, 4 or 8 */
+#define EB_PATH_GEMV 1 /* bandwidth-bound GEMV, requires m <= 8 and m' * k <= 65536, m' = m rounded up to 1, 2, 4 or 8; not for Q6_S */
 #define EB_PATH_MFMA 2 /* LDS-tiled dequantize-to-16-bit + MFMA, any m */
 
 /* A quantized weight matrix W[n][k] in the planar device layout above.
@@ -109,7 +128,9 @@ typedef struct {
   int64_t d_offset;      /* start of the binary16 scale plane */
   int64_t d_stride;      /* scale-plane row stride in binary16 elements (DS) */
   int64_t total_bytes;   /* == eb_qweights_bytes */
-  int64_t canonical_bytes; /* n * (k/32) * (2 + QB), size of the canonical form */
+  int64_t canonical_bytes; /* size of the canonical form: n * (k/32) * (2 + QB), Q6_S n * (k/256) * 210 */
+  int64_t sc_offset;     /* Q6_S: start of the int8 sub-scale plane (0 otherwise) */
+  int64_t sc_stride;     /* Q6_S: its row stride in bytes, k/16 (0 otherwise) */
 } eb_layout;
 
 /* Steps of a decoder layer fused around one projection (paper section 3.2,
@@ -182,6 +203,14 @@ eb_status eb_quantize_q8_0(const float *w, int64_t n, int64_t k, void *out, hipS
 
 /* Same as eb_quantize_q8_0 for the Q4_0 format. */
 eb_status eb_quantize_q4_0(const float *w, int64_t n, int64_t k, void *out, hipStream_t stream);
+
+/* Same as eb_quantize_q8_0 for the Q6_S format (k % 256 == 0, else
+ * EB_ERR_INVALID).  Q6_S ops run on the matrix cores at every m (one kernel:
+ * 16 weight rows and up to 64 rows of x per workgroup, the whole of k;
+ * EB_PATH_GEMV returns EB_ERR_UNSUPPORTED) and never join a fused stack
+ * launch.  Accuracy as the MFMA path: bfloat16 activations take w_hat as
+ * hi/lo pairs at every m (2e-3); binary16 activations round w_hat once. */
+eb_status eb_quantize_q6_s(const float *w, int64_t n, int64_t k, void *out, hipStream_t stream);
 
 /* Write the canonical array-of-blocks bytes of *w into `dst` (device,
  * eb_layout.canonical_bytes bytes, no alignment requirement). */

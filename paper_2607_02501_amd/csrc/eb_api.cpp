@@ -45,11 +45,20 @@ constexpr int64_t kMaxM = int64_t(1) << 24;
 
 bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
-bool valid_type(int32_t t) { return t == EB_Q8_0 || t == EB_Q4_0; }
+bool valid_type(int32_t t) { return t == EB_Q8_0 || t == EB_Q4_0 || t == EB_Q6_S; }
 bool known_dtype(int32_t t) { return t == EB_F32 || t == EB_F16 || t == EB_BF16; }
 
-bool valid_nk(int64_t n, int64_t k) {
-  return n >= 1 && n <= kMaxN && k >= kQK && k <= kMaxK && k % kQK == 0;
+// k: a multiple of the format's block (32 weights, 256 for Q6_S)
+bool valid_k(int32_t type, int64_t k) {
+  return k >= 0 && k <= kMaxK && k % block_elems(type) == 0;
+}
+
+bool valid_nk(int32_t type, int64_t n, int64_t k) {
+  return n >= 1 && n <= kMaxN && k >= kQK && valid_k(type, k);
+}
+
+size_t canonical_bytes(int32_t type, int64_t n, int64_t k) {
+  return (size_t)n * (size_t)(k / block_elems(type)) * (size_t)canonical_block_bytes(type);
 }
 
 bool overlaps(const void *a, size_t an, const void *b, size_t bn) {
@@ -66,7 +75,7 @@ bool gemv_fits(int64_t m, int64_t k) {
 }
 
 eb_status check_weights(const eb_qweights *w) {
-  if (!w || !w->data || !valid_type(w->type) || w->reserved != 0 || !valid_nk(w->n, w->k))
+  if (!w || !w->data || !valid_type(w->type) || w->reserved != 0 || !valid_nk(w->type, w->n, w->k))
     return EB_ERR_INVALID;
   if (!aligned(w->data, 256)) return EB_ERR_ALIGN;
   return EB_OK;
@@ -132,6 +141,8 @@ eb_status check_op(const eb_qlinear_op &o, int32_t path) {
   if (o.epilogue == EB_EPI_ADD && o.residual != o.y && overlaps(o.y, yb, o.residual, yb))
     return EB_ERR_INVALID;
   if (path == EB_PATH_GEMV && !gemv_fits(m, o.w.k)) return EB_ERR_UNSUPPORTED;
+  if (o.w.type == EB_Q6_S && (path == EB_PATH_GEMV || !q6_fits(m, o.w.n, o.w.k)))
+    return EB_ERR_UNSUPPORTED;
   return EB_OK;
 }
 
@@ -140,10 +151,10 @@ eb_status check_op(const eb_qlinear_op &o, int32_t path) {
 // shapes): the GEMV wins at m = 1 everywhere and at m = 2..4 unless the matrix
 // has few rows (n = 1024 loses); from m = 5 the MFMA path wins or loses by at
 // most 20%, so it is taken for every m >= 5.
+// Q6_S has one kernel for every m, on the matrix cores.
 int32_t pick_path(int32_t type, int32_t xt, int64_t m, int64_t n, int64_t k) {
-  (void)type;
   (void)xt;
-  if (!gemv_fits(m, k)) return EB_PATH_MFMA;
+  if (type == EB_Q6_S || !gemv_fits(m, k)) return EB_PATH_MFMA;
   if (m == 1) return EB_PATH_GEMV;
   return (m <= 4 && n >= 2048) ? EB_PATH_GEMV : EB_PATH_MFMA;
 }
@@ -235,7 +246,7 @@ eb_status check_workspace(const eb_qlinear_op *ops, int32_t n_ops, const void *w
 
 eb_status quantize_common(int32_t type, const float *w, int64_t n, int64_t k, void *out,
                           hipStream_t s) {
-  if (n < 0 || n > kMaxN || k < 0 || k > kMaxK || k % kQK != 0) return EB_ERR_INVALID;
+  if (n < 0 || n > kMaxN || !valid_k(type, k)) return EB_ERR_INVALID;
   if (n == 0 || k == 0) return EB_OK;
   if (!w || !out) return EB_ERR_INVALID;
   if (!aligned(w, 16) || !aligned(out, 256)) return EB_ERR_ALIGN;
@@ -366,7 +377,7 @@ bool env_off(const char *name) {
 }
 
 bool fusable(const eb_qlinear_op &o) {
-  return o.m == 1 && gemv_fits(1, o.w.k) && m1_fusable(o.w.type, o.m, o.w.k, o.epilogue);
+  return o.w.type != EB_Q6_S && o.m == 1 && gemv_fits(1, o.w.k) && m1_fusable(o.w.type, o.m, o.w.k, o.epilogue);
 }
 
 // MFMA ops that may join a fused launch.  The fused kernel addresses tiles of
@@ -384,12 +395,12 @@ int64_t mm_max_m() {
 // MFMA ops with more rows than a fused small-m launch takes, which may share a
 // grouped launch (EB_STACK_GROUP=0 turns that off).
 bool gm_fusable(const eb_qlinear_op &o) {
-  return o.m > mm_max_m() && !env_off("EB_STACK_GROUP") &&
+  return o.w.type != EB_Q6_S && o.m > mm_max_m() && !env_off("EB_STACK_GROUP") &&
          pick_path(o.w.type, o.x_type, o.m, o.w.n, o.w.k) == EB_PATH_MFMA;
 }
 
 bool mm_fusable(const eb_qlinear_op &o) {
-  return o.m >= 1 && o.m <= mm_max_m() && o.w.k < kMMaxK &&
+  return o.w.type != EB_Q6_S && o.m >= 1 && o.m <= mm_max_m() && o.w.k < kMMaxK &&
          (o.m + 256) * o.w.n * (int64_t)dsize(o.y_type) < (int64_t(1) << 31) &&
          pick_path(o.w.type, o.x_type, o.m, o.w.n, o.w.k) == EB_PATH_MFMA;
 }
@@ -896,20 +907,21 @@ const char *eb_status_str(eb_status s) {
 }
 
 size_t eb_qweights_bytes(int32_t type, int64_t n, int64_t k) {
-  if (!valid_type(type) || n < 0 || n > kMaxN || k < 0 || k > kMaxK || k % kQK != 0) return 0;
+  if (!valid_type(type) || n < 0 || n > kMaxN || !valid_k(type, k)) return 0;
   return (size_t)layout_of(type, n, k).total;
 }
 
 eb_status eb_qweights_layout(int32_t type, int64_t n, int64_t k, eb_layout *out) {
-  if (!out || !valid_type(type) || n < 0 || n > kMaxN || k < 0 || k > kMaxK || k % kQK != 0)
-    return EB_ERR_INVALID;
+  if (!out || !valid_type(type) || n < 0 || n > kMaxN || !valid_k(type, k)) return EB_ERR_INVALID;
   const Layout L = layout_of(type, n, k);
   out->qs_offset = 0;
   out->qs_row_bytes = L.qs_row;
   out->d_offset = L.d_off;
   out->d_stride = L.ds;
   out->total_bytes = L.total;
-  out->canonical_bytes = n * L.nb * (2 + qs_bytes_per_block(type));
+  out->canonical_bytes = (int64_t)canonical_bytes(type, n, k);
+  out->sc_offset = L.sc_off;
+  out->sc_stride = L.ss;
   return EB_OK;
 }
 
@@ -921,11 +933,15 @@ eb_status eb_quantize_q4_0(const float *w, int64_t n, int64_t k, void *out, hipS
   return quantize_common(EB_Q4_0, w, n, k, out, stream);
 }
 
+eb_status eb_quantize_q6_s(const float *w, int64_t n, int64_t k, void *out, hipStream_t stream) {
+  return quantize_common(EB_Q6_S, w, n, k, out, stream);
+}
+
 eb_status eb_qweights_to_canonical(const eb_qweights *w, void *dst, hipStream_t stream) {
   eb_status st = check_weights(w);
   if (st != EB_OK) return st;
   if (!dst) return EB_ERR_INVALID;
-  const size_t cb = (size_t)w->n * (w->k / kQK) * (2 + qs_bytes_per_block(w->type));
+  const size_t cb = canonical_bytes(w->type, w->n, w->k);
   if (overlaps(dst, cb, w->data, eb_qweights_bytes(w->type, w->n, w->k))) return EB_ERR_INVALID;
   return launch_to_canonical(w->type, w->data, w->n, w->k, dst, stream) == hipSuccess ? EB_OK
                                                                                        : EB_ERR_HIP;
@@ -933,9 +949,9 @@ eb_status eb_qweights_to_canonical(const eb_qweights *w, void *dst, hipStream_t 
 
 eb_status eb_qweights_from_canonical(int32_t type, const void *src, int64_t n, int64_t k,
                                      void *out, hipStream_t stream) {
-  if (!valid_type(type) || !valid_nk(n, k) || !src || !out) return EB_ERR_INVALID;
+  if (!valid_type(type) || !valid_nk(type, n, k) || !src || !out) return EB_ERR_INVALID;
   if (!aligned(out, 256)) return EB_ERR_ALIGN;
-  const size_t cb = (size_t)n * (k / kQK) * (2 + qs_bytes_per_block(type));
+  const size_t cb = canonical_bytes(type, n, k);
   if (overlaps(src, cb, out, eb_qweights_bytes(type, n, k))) return EB_ERR_INVALID;
   return launch_from_canonical(type, src, n, k, out, stream) == hipSuccess ? EB_OK : EB_ERR_HIP;
 }
@@ -991,7 +1007,7 @@ eb_status eb_qlinear(const eb_qweights *w, const void *x, int32_t x_type, int64_
 }
 
 int32_t eb_qlinear_auto_path(int32_t type, int32_t x_type, int64_t m, int64_t n, int64_t k) {
-  if (!valid_type(type) || !valid_nk(n, k) || m < 1 || m > kMaxM) return EB_ERR_INVALID;
+  if (!valid_type(type) || !valid_nk(type, n, k) || m < 1 || m > kMaxM) return EB_ERR_INVALID;
   return pick_path(type, x_type, m, n, k);
 }
 

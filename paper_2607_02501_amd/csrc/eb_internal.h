@@ -13,27 +13,45 @@
 
 namespace eb {
 
-constexpr int kQK = 32;  // weights per block
+constexpr int kQK = 32;    // weights per block (Q6_S: per 24-byte code chunk)
+constexpr int kQK6 = 256;  // weights per Q6_S super-block
 
-__host__ __device__ inline int64_t qs_bytes_per_block(int32_t type) { return type == EB_Q8_0 ? 32 : 16; }
+__host__ __device__ inline int64_t qs_bytes_per_block(int32_t type) {
+  return type == EB_Q8_0 ? 32 : (type == EB_Q4_0 ? 16 : 24);
+}
 __host__ __device__ inline int64_t round_up(int64_t v, int64_t a) { return (v + a - 1) / a * a; }
 
 struct Layout {
-  int64_t nb;        // blocks per row
-  int64_t qs_row;    // bytes per qs row
-  int64_t d_off;     // byte offset of the scale plane
-  int64_t ds;        // scale-plane row stride (elements)
-  int64_t total;     // total bytes
+  int64_t nb;          // blocks (Q6_S: 32-weight code chunks) per row
+  int64_t qs_row;      // bytes per qs row
+  int64_t d_off;       // byte offset of the binary16 scale plane
+  int64_t ds;          // scale-plane row stride (elements)
+  int64_t total;       // total bytes
+  int64_t sc_off = 0;  // Q6_S: byte offset of the int8 sub-block scale plane
+  int64_t ss = 0;      // Q6_S: its row stride (bytes, k / 16)
 };
 
 inline Layout layout_of(int32_t type, int64_t n, int64_t k) {
   Layout L;
   L.nb = k / kQK;
   L.qs_row = L.nb * qs_bytes_per_block(type);
-  L.d_off = round_up(n * L.qs_row, 256);
-  L.ds = round_up(L.nb, 8);
+  if (type == EB_Q6_S) {
+    L.sc_off = round_up(n * L.qs_row, 256);
+    L.ss = k / 16;
+    L.d_off = round_up(L.sc_off + n * L.ss, 256);
+    L.ds = round_up(k / kQK6, 8);
+  } else {
+    L.d_off = round_up(n * L.qs_row, 256);
+    L.ds = round_up(L.nb, 8);
+  }
   L.total = round_up(L.d_off + n * L.ds * 2, 256);
   return L;
+}
+
+// weights per canonical block and bytes per canonical block
+inline int64_t block_elems(int32_t type) { return type == EB_Q6_S ? kQK6 : kQK; }
+inline int64_t canonical_block_bytes(int32_t type) {
+  return type == EB_Q6_S ? 2 + 16 + 192 : 2 + qs_bytes_per_block(type);
 }
 
 // Fused steps of one op (EB_PRO_*, EB_EPI_*) as the kernels take them.  The
@@ -116,6 +134,7 @@ hipError_t launch_gemv_m1_multi(int32_t type, int32_t xt, int ns, const M1Op *de
 // (partial sums, summed in order by a second kernel).
 struct MfmaPlan {
   int cfg = 0;
+  bool q6 = false;        // Q6_S weights: the Q6_S kernel (any m, no split)
   bool hl = false;        // bfloat16 activations at m <= 128: hi/lo weight tiles
   bool narrow = false;    // m <= kNarrowMaxM: the one-launch narrow kernel (no tiles, no split)
   int splits = 1;
@@ -153,6 +172,12 @@ bool narrow_fits(int64_t m, int64_t n, int64_t k);
 hipError_t launch_mfma_narrow(int32_t type, const void *wdata, int64_t n, int64_t k, const void *x,
                               int32_t xt, bool hl, int64_t m, void *y, int32_t yt, const Fuse &f,
                               hipStream_t s);
+// Q6_S weights on the matrix cores, any m, one launch (mfma_q6.hip): 16
+// weight rows and up to 64 rows of x per workgroup, k split over its waves.
+// bfloat16 activations take w_hat as hi/lo pairs at every m.
+bool q6_fits(int64_t m, int64_t n, int64_t k);
+hipError_t launch_mfma_q6(const void *wdata, int64_t n, int64_t k, const void *x, int32_t xt,
+                          int64_t m, void *y, int32_t yt, const Fuse &f, hipStream_t s);
 // Whether a workgroup's byte spans of a bm x bn tile fit 32-bit buffer offsets.
 bool mfma_fits_offsets(int32_t type, int64_t n, int64_t k, int bm, int bn);
 int mfma_tile_count();

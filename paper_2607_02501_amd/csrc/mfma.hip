@@ -148,6 +148,12 @@ MfmaPlan plan_mfma(int32_t type, int32_t xt, int64_t m, int64_t n, int64_t k, si
   }
   MfmaPlan best;
   best.hl = hl;
+  if (type == EB_Q6_S) {  // one kernel for every m
+    best.q6 = true;
+    best.hl = xt == EB_BF16;
+    best.kts = (int)nk;
+    return best;
+  }
   // a lone small-m projection: one launch of the narrow kernel, whole k per
   // workgroup (measured on the action-expert chain: the tiled kernel split
   // along k plus its reduction took about 16 us per projection)
@@ -278,6 +284,10 @@ hipError_t launch_q(const void *wdata, int64_t n, int64_t k, const void *x, int6
 hipError_t launch_mfma(int32_t type, const void *wdata, int64_t n, int64_t k, const void *x,
                        int32_t xt, int64_t m, void *y, int32_t yt, const Fuse &f,
                        const MfmaPlan &plan, float *ws, hipStream_t s, const NormOut *no) {
+  if (type == EB_Q6_S) {
+    if (no) return hipErrorInvalidValue;  // no split, so no reduction to fuse into
+    return launch_mfma_q6(wdata, n, k, x, xt, m, y, yt, f, s);
+  }
   if (type == EB_Q4_0) {
     if (xt == EB_F16) return launch_q<EB_Q4_0, EB_F16>(wdata, n, k, x, m, y, yt, f, plan, ws, s, no);
     return launch_q<EB_Q4_0, EB_BF16>(wdata, n, k, x, m, y, yt, f, plan, ws, s, no);

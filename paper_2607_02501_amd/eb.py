@@ -26,6 +26,7 @@ EB_ERR_HIP = -4
 
 EB_Q8_0 = 1
 EB_Q4_0 = 2
+EB_Q6_S = 3
 EB_F32 = 0
 EB_F16 = 1
 EB_BF16 = 2
@@ -38,7 +39,10 @@ EB_EPI_NONE = 0
 EB_EPI_ADD = 1
 EB_EPI_GLU = 2
 
-QTYPES = {"q8_0": EB_Q8_0, "q4_0": EB_Q4_0}
+QTYPES = {"q8_0": EB_Q8_0, "q4_0": EB_Q4_0, "q6_s": EB_Q6_S}
+# weights and canonical bytes per block of each format
+BLOCK_ELEMS = {"q8_0": 32, "q4_0": 32, "q6_s": 256}
+BLOCK_BYTES = {"q8_0": 34, "q4_0": 18, "q6_s": 210}
 DTYPES = {torch.float32: EB_F32, torch.float16: EB_F16, torch.bfloat16: EB_BF16}
 PATHS = {"auto": EB_PATH_AUTO, "gemv": EB_PATH_GEMV, "mfma": EB_PATH_MFMA}
 PROLOGUES = {None: EB_PRO_NONE, "none": EB_PRO_NONE, "rmsnorm": EB_PRO_RMSNORM}
@@ -53,7 +57,8 @@ class eb_qweights(ctypes.Structure):
 class eb_layout(ctypes.Structure):
     _fields_ = [("qs_offset", ctypes.c_int64), ("qs_row_bytes", ctypes.c_int64),
                 ("d_offset", ctypes.c_int64), ("d_stride", ctypes.c_int64),
-                ("total_bytes", ctypes.c_int64), ("canonical_bytes", ctypes.c_int64)]
+                ("total_bytes", ctypes.c_int64), ("canonical_bytes", ctypes.c_int64),
+                ("sc_offset", ctypes.c_int64), ("sc_stride", ctypes.c_int64)]
 
 
 class eb_qlinear_op(ctypes.Structure):
@@ -79,7 +84,7 @@ lib.eb_qweights_bytes.restype = ctypes.c_size_t
 lib.eb_qweights_bytes.argtypes = [_i32, _i64, _i64]
 lib.eb_qweights_layout.restype = _i32
 lib.eb_qweights_layout.argtypes = [_i32, _i64, _i64, ctypes.POINTER(eb_layout)]
-for _name in ("eb_quantize_q8_0", "eb_quantize_q4_0"):
+for _name in ("eb_quantize_q8_0", "eb_quantize_q4_0", "eb_quantize_q6_s"):
     getattr(lib, _name).restype = _i32
     getattr(lib, _name).argtypes = [_vp, _i64, _i64, _vp, _vp]
 lib.eb_qweights_to_canonical.restype = _i32
@@ -177,15 +182,17 @@ def quantize(w: torch.Tensor, qtype: str, out: QWeights | None = None) -> QWeigh
     w = w.contiguous()
     n, k = w.shape
     out = out or empty_qweights(qtype, n, k, w.device)
-    fn = lib.eb_quantize_q8_0 if qtype == "q8_0" else lib.eb_quantize_q4_0
+    fn = {"q8_0": lib.eb_quantize_q8_0, "q4_0": lib.eb_quantize_q4_0,
+          "q6_s": lib.eb_quantize_q6_s}[qtype]
     _check(fn(w.data_ptr(), n, k, out.buf.data_ptr(), _stream(w.device)), fn.__name__)
     return out
 
 
 def to_canonical(qw: QWeights) -> torch.Tensor:
-    """Canonical array-of-blocks bytes (device uint8 tensor [n, k/32, block_bytes])."""
-    bb = 34 if qw.qtype == "q8_0" else 18
-    dst = torch.empty((qw.n, qw.k // 32, bb), dtype=torch.uint8, device=qw.device)
+    """Canonical array-of-blocks bytes (device uint8 tensor [n, k/E, block_bytes],
+    E = BLOCK_ELEMS[qtype])."""
+    dst = torch.empty((qw.n, qw.k // BLOCK_ELEMS[qw.qtype], BLOCK_BYTES[qw.qtype]),
+                      dtype=torch.uint8, device=qw.device)
     c = qw.c
     _check(lib.eb_qweights_to_canonical(ctypes.byref(c), dst.data_ptr(), _stream(qw.device)),
            "eb_qweights_to_canonical")

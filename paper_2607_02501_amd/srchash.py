@@ -13,6 +13,8 @@ _FILES = {
              "mfma_q4_0_bf16.hip", "mfma_q4_0_f16.hip", "mfma_common.h", "norm.hip") + _COMMON,
     # fused small-m MFMA kernels (m <= 128)
     "mm": ("mfma_lds2.hip", "mfma_multi.hip", "mfma_common.h", "mm_common.h", "norm.hip") + _COMMON,
+    # the Q6_S kernel (every m)
+    "q6": ("mfma_q6.hip", "mfma_common.h", "norm.hip") + _COMMON,
 }
 
 
@@ -20,6 +22,10 @@ def family(symbol: str) -> str:
     """Kernel family of a kernel symbol (as the profiler names it)."""
     if symbol.startswith("gemv"):
         return "gemv"
+    if symbol.startswith("mm_q6"):
+        return "q6"
+    if symbol.startswith("mm_narrow"):
+        return "mfma"
     if symbol.startswith("mm_"):
         return "mm"
     return "mfma"

@@ -21,6 +21,7 @@ import torch
 
 Q8_0 = "q8_0"
 Q4_0 = "q4_0"
+Q6_S = "q6_s"
 
 
 @dataclass(frozen=True)
@@ -50,6 +51,10 @@ WORKLOADS = {
     "q4_0_decode_7b": Workload("q4_0_decode_7b", Q4_0, torch.float16, 1, 32, 1,
                                (("qkv", 4096, 12288), ("o", 4096, 4096),
                                 ("gate_up", 4096, 22016), ("down", 11008, 4096)), wid=1),
+    # the same decoder in the 6-bit format (Q6_S super-blocks)
+    "q6_s_decode_7b": Workload("q6_s_decode_7b", Q6_S, torch.float16, 1, 32, 1,
+                               (("qkv", 4096, 12288), ("o", 4096, 4096),
+                                ("gate_up", 4096, 22016), ("down", 11008, 4096)), wid=5),
     # VLM backbone prefill: 3 camera views x 256 patch tokens + 48 text tokens
     "q8_0_vlm_prefill_816": Workload("q8_0_vlm_prefill_816", Q8_0, torch.bfloat16, 816, 18, 1,
                                      (("qkv", 2048, 2560), ("o", 2048, 2048),

@@ -4,7 +4,7 @@ import torch
 
 from oracle import oracle as O
 
-QT = {"q8_0": O.Q8_0, "q4_0": O.Q4_0}
+QT = {"q8_0": O.Q8_0, "q4_0": O.Q4_0, "q6_s": O.Q6_S}
 XT = {torch.float16: O.X_F16, torch.bfloat16: O.X_BF16}
 
 # Error bound of the method: fp32 accumulation of 16-bit inputs, normalised by

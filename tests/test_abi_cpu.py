@@ -31,7 +31,8 @@ def declared_functions():
 
 def test_header_declares_the_boundary():
     names = declared_functions()
-    for required in ("eb_quantize_q8_0", "eb_quantize_q4_0", "eb_qlinear", "eb_qlinear_stack"):
+    for required in ("eb_quantize_q8_0", "eb_quantize_q4_0", "eb_quantize_q6_s", "eb_qlinear",
+                     "eb_qlinear_stack"):
         assert required in names
 
 
@@ -65,9 +66,59 @@ def test_layout(eb, qtype, qb, n, k):
     assert eb.qweights_bytes(qtype, n, k) == L.total_bytes
 
 
+@pytest.mark.parametrize("n,k", [(1, 256), (7, 768), (4096, 4096), (4096, 11008), (3, 2304)])
+def test_layout_q6(eb, n, k):
+    """Q6_S planar layout: 24-byte code chunks per 32 weights, the int8
+    sub-scale plane (k/16 bytes per row), the binary16 scale plane
+    (round_up(k/256, 8) entries per row), each 256-byte aligned."""
+    if k % 256:
+        assert eb.lib.eb_qweights_bytes(eb.EB_Q6_S, n, k) == 0
+        return
+    L = eb.layout("q6_s", n, k)
+    nb = k // 32
+    assert L.qs_offset == 0 and L.qs_row_bytes == nb * 24
+    assert L.sc_offset % 256 == 0 and 0 <= L.sc_offset - n * nb * 24 < 256
+    assert L.sc_stride == k // 16
+    assert L.d_offset % 256 == 0 and 0 <= L.d_offset - (L.sc_offset + n * k // 16) < 256
+    assert L.d_stride % 8 == 0 and k // 256 <= L.d_stride < k // 256 + 8
+    assert L.total_bytes % 256 == 0 and 0 <= L.total_bytes - (L.d_offset + 2 * n * L.d_stride) < 256
+    assert L.canonical_bytes == n * (k // 256) * 210
+    assert eb.qweights_bytes("q6_s", n, k) == L.total_bytes
+    # Q8_0 / Q4_0 layouts have no sub-scale plane
+    assert eb.layout("q8_0", n, k).sc_offset == 0 and eb.layout("q4_0", n, k).sc_stride == 0
+
+
+def test_q6_validation(eb):
+    L = eb.lib
+    assert L.eb_quantize_q6_s(0x200000, 4, 128, 0x100000, None) == -1   # k % 256
+    assert L.eb_quantize_q6_s(0x200000, 4, 256, 0x100080, None) == -2   # out misaligned
+    assert L.eb_quantize_q6_s(None, 0, 256, None, None) == 0            # empty: no-op
+    assert L.eb_qweights_from_canonical(eb.EB_Q6_S, 0x200000, 4, 288, 0x100000, None) == -1
+    w = _w(eb, eb.EB_Q6_S, n=64, k=512)
+    # every m runs on the matrix cores; the GEMV path is refused
+    for m in (1, 4, 50, 300):
+        assert L.eb_qlinear_auto_path(eb.EB_Q6_S, eb.EB_BF16, m, 64, 512) == eb.EB_PATH_MFMA
+    assert L.eb_qlinear_ex(ctypes.byref(w), X, eb.EB_F16, 1, Y, eb.EB_F32, eb.EB_PATH_GEMV,
+                           None) == eb.EB_ERR_UNSUPPORTED
+    bad = _w(eb, eb.EB_Q6_S, n=64, k=288)
+    assert L.eb_qlinear(ctypes.byref(bad), X, eb.EB_F16, 1, Y, eb.EB_F32, None) == -1
+    # no split along k: no workspace, except for a prologue's normalised rows
+    op = eb.eb_qlinear_op(_w(eb, eb.EB_Q6_S, n=1024, k=4096, data=1 * GB), 8 * GB, 9 * GB, 50,
+                          eb.EB_BF16, eb.EB_F32)
+    assert L.eb_qlinear_workspace_bytes(ctypes.byref(op), eb.EB_PATH_AUTO) == 0
+    normed = eb.eb_qlinear_op(_w(eb, eb.EB_Q6_S, n=1024, k=4096, data=1 * GB), 8 * GB, 9 * GB, 50,
+                              eb.EB_BF16, eb.EB_F32, eb.EB_PRO_RMSNORM, 0, G, None, 1e-5, 0)
+    assert L.eb_qlinear_workspace_bytes(ctypes.byref(normed), eb.EB_PATH_AUTO) == 50 * 4096 * 2
+    # in a stack every Q6_S op is a launch of its own (plus its prologue's row kernel)
+    ops = [_op(eb, 1 * GB + i * (64 << 20), 8 * GB + i * (1 << 20), 9 * GB + i * (1 << 20),
+               k=1024, n=2048, m=1, qtype=eb.EB_Q6_S, xt=eb.EB_F16) for i in range(4)]
+    assert _launches(eb, ops) == 4
+
+
 def test_bytes_rejects_bad_sizes(eb):
     assert eb.lib.eb_qweights_bytes(eb.EB_Q8_0, 4, 33) == 0
-    assert eb.lib.eb_qweights_bytes(3, 4, 32) == 0
+    assert eb.lib.eb_qweights_bytes(4, 4, 32) == 0
+    assert eb.lib.eb_qweights_bytes(eb.EB_Q6_S, 4, 32) == 0
     assert eb.lib.eb_qweights_bytes(eb.EB_Q4_0, -1, 32) == 0
     assert eb.lib.eb_qweights_layout(eb.EB_Q4_0, 4, 32, None) == eb.EB_ERR_INVALID
 
