@@ -107,7 +107,7 @@ typedef int32_t eb_status;
 
 /* kernel paths for eb_qlinear_ex */
 #define EB_PATH_AUTO 0 /* pick by m, qtype and shape (measured crossover) */
-#define EB_PATH_GEMV 1 /* bandwidth-bound GEMV, requires m <= 8 and m' * k <= 65536, m' = m rounded up to 1, 2, 4 or 8; not for Q6_S */
+#define EB_PATH_GEMV 1 /* bandwidth-bound GEMV, requires m <= 8 and m' * k <= 65536, m' = m rounded up to 1, 2, 4 or 8 */
 #define EB_PATH_MFMA 2 /* LDS-tiled dequantize-to-16-bit + MFMA, any m */
 
 /* A quantized weight matrix W[n][k] in the planar device layout above.
@@ -205,11 +205,11 @@ eb_status eb_quantize_q8_0(const float *w, int64_t n, int64_t k, void *out, hipS
 eb_status eb_quantize_q4_0(const float *w, int64_t n, int64_t k, void *out, hipStream_t stream);
 
 /* Same as eb_quantize_q8_0 for the Q6_S format (k % 256 == 0, else
- * EB_ERR_INVALID).  Q6_S ops run on the matrix cores at every m (one kernel:
- * 16 weight rows and up to 64 rows of x per workgroup, the whole of k;
- * EB_PATH_GEMV returns EB_ERR_UNSUPPORTED) and never join a fused stack
- * launch.  Accuracy as the MFMA path: bfloat16 activations take w_hat as
- * hi/lo pairs at every m (2e-3); binary16 activations round w_hat once. */
+ * EB_ERR_INVALID).  Q6_S ops have a GEMV of their own (m <= 8, fp32 products
+ * of the codes; EB_PATH_AUTO takes it up to m = 4) and one matrix-core kernel
+ * for every m (16 weight rows and up to 64 rows of x per workgroup, the whole
+ * of k; bfloat16 activations take w_hat as hi/lo pairs, binary16 ones round
+ * it once), both within the 2e-3 bound; they never join a fused stack launch. */
 eb_status eb_quantize_q6_s(const float *w, int64_t n, int64_t k, void *out, hipStream_t stream);
 
 /* Write the canonical array-of-blocks bytes of *w into `dst` (device,

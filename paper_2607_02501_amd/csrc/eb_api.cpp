@@ -141,7 +141,9 @@ eb_status check_op(const eb_qlinear_op &o, int32_t path) {
   if (o.epilogue == EB_EPI_ADD && o.residual != o.y && overlaps(o.y, yb, o.residual, yb))
     return EB_ERR_INVALID;
   if (path == EB_PATH_GEMV && !gemv_fits(m, o.w.k)) return EB_ERR_UNSUPPORTED;
-  if (o.w.type == EB_Q6_S && (path == EB_PATH_GEMV || !q6_fits(m, o.w.n, o.w.k)))
+  if (o.w.type == EB_Q6_S && path == EB_PATH_GEMV && !gemv_q6_fits(m, o.w.n, o.w.k))
+    return EB_ERR_UNSUPPORTED;
+  if (o.w.type == EB_Q6_S && path != EB_PATH_GEMV && !q6_fits(m, o.w.n, o.w.k))
     return EB_ERR_UNSUPPORTED;
   return EB_OK;
 }
@@ -151,10 +153,11 @@ eb_status check_op(const eb_qlinear_op &o, int32_t path) {
 // shapes): the GEMV wins at m = 1 everywhere and at m = 2..4 unless the matrix
 // has few rows (n = 1024 loses); from m = 5 the MFMA path wins or loses by at
 // most 20%, so it is taken for every m >= 5.
-// Q6_S has one kernel for every m, on the matrix cores.
+// Q6_S: its GEMV up to m = 4, its matrix-core kernel beyond.
 int32_t pick_path(int32_t type, int32_t xt, int64_t m, int64_t n, int64_t k) {
   (void)xt;
-  if (type == EB_Q6_S || !gemv_fits(m, k)) return EB_PATH_MFMA;
+  if (type == EB_Q6_S) return m <= 4 && gemv_q6_fits(m, n, k) ? EB_PATH_GEMV : EB_PATH_MFMA;
+  if (!gemv_fits(m, k)) return EB_PATH_MFMA;
   if (m == 1) return EB_PATH_GEMV;
   return (m <= 4 && n >= 2048) ? EB_PATH_GEMV : EB_PATH_MFMA;
 }

@@ -172,6 +172,11 @@ bool narrow_fits(int64_t m, int64_t n, int64_t k);
 hipError_t launch_mfma_narrow(int32_t type, const void *wdata, int64_t n, int64_t k, const void *x,
                               int32_t xt, bool hl, int64_t m, void *y, int32_t yt, const Fuse &f,
                               hipStream_t s);
+// Q6_S weights, m <= 8 (gemv_q6.hip): a wave per pair of weight rows, lanes
+// over 32-weight chunks, fp32 products of the 6-bit codes and x staged in LDS.
+bool gemv_q6_fits(int64_t m, int64_t n, int64_t k);
+hipError_t launch_gemv_q6(const void *wdata, int64_t n, int64_t k, const void *x, int32_t xt,
+                          int64_t m, void *y, int32_t yt, const Fuse &f, hipStream_t s);
 // Q6_S weights on the matrix cores, any m, one launch (mfma_q6.hip): 16
 // weight rows and up to 64 rows of x per workgroup, k split over its waves.
 // bfloat16 activations take w_hat as hi/lo pairs at every m.

@@ -955,6 +955,7 @@ hipError_t launch_gemv_m1_multi(int32_t type, int32_t xt, int ns, const M1Op *de
 
 hipError_t launch_gemv(int32_t type, const void *wdata, int64_t n, int64_t k, const void *x,
                        int32_t xt, int64_t m, void *y, int32_t yt, const Fuse &f, hipStream_t s) {
+  if (type == EB_Q6_S) return launch_gemv_q6(wdata, n, k, x, xt, m, y, yt, f, s);
   if (type == EB_Q4_0) {
     if (xt == EB_F16) return launch_m<EB_Q4_0, EB_F16>(wdata, n, k, x, m, y, yt, f, s);
     return launch_m<EB_Q4_0, EB_BF16>(wdata, n, k, x, m, y, yt, f, s);

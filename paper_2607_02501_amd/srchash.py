@@ -15,11 +15,14 @@ _FILES = {
     "mm": ("mfma_lds2.hip", "mfma_multi.hip", "mfma_common.h", "mm_common.h", "norm.hip") + _COMMON,
     # the Q6_S kernel (every m)
     "q6": ("mfma_q6.hip", "mfma_common.h", "norm.hip") + _COMMON,
+    "gemv_q6": ("gemv_q6.hip",) + _COMMON,
 }
 
 
 def family(symbol: str) -> str:
     """Kernel family of a kernel symbol (as the profiler names it)."""
+    if symbol.startswith("gemv_q6"):
+        return "gemv_q6"
     if symbol.startswith("gemv"):
         return "gemv"
     if symbol.startswith("mm_q6"):

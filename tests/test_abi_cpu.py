@@ -95,14 +95,16 @@ def test_q6_validation(eb):
     assert L.eb_quantize_q6_s(None, 0, 256, None, None) == 0            # empty: no-op
     assert L.eb_qweights_from_canonical(eb.EB_Q6_S, 0x200000, 4, 288, 0x100000, None) == -1
     w = _w(eb, eb.EB_Q6_S, n=64, k=512)
-    # every m runs on the matrix cores; the GEMV path is refused
-    for m in (1, 4, 50, 300):
-        assert L.eb_qlinear_auto_path(eb.EB_Q6_S, eb.EB_BF16, m, 64, 512) == eb.EB_PATH_MFMA
-    assert L.eb_qlinear_ex(ctypes.byref(w), X, eb.EB_F16, 1, Y, eb.EB_F32, eb.EB_PATH_GEMV,
+    # its GEMV up to m = 4, the matrix cores beyond; the GEMV takes m <= 8
+    for m, path in ((1, eb.EB_PATH_GEMV), (4, eb.EB_PATH_GEMV), (5, eb.EB_PATH_MFMA),
+                    (50, eb.EB_PATH_MFMA), (300, eb.EB_PATH_MFMA)):
+        assert L.eb_qlinear_auto_path(eb.EB_Q6_S, eb.EB_BF16, m, 64, 512) == path, m
+    assert L.eb_qlinear_ex(ctypes.byref(w), X, eb.EB_F16, 9, Y, eb.EB_F32, eb.EB_PATH_GEMV,
                            None) == eb.EB_ERR_UNSUPPORTED
     bad = _w(eb, eb.EB_Q6_S, n=64, k=288)
     assert L.eb_qlinear(ctypes.byref(bad), X, eb.EB_F16, 1, Y, eb.EB_F32, None) == -1
     # no split along k: no workspace, except for a prologue's normalised rows
+    # on the matrix-core path (the GEMV normalises while it stages x)
     op = eb.eb_qlinear_op(_w(eb, eb.EB_Q6_S, n=1024, k=4096, data=1 * GB), 8 * GB, 9 * GB, 50,
                           eb.EB_BF16, eb.EB_F32)
     assert L.eb_qlinear_workspace_bytes(ctypes.byref(op), eb.EB_PATH_AUTO) == 0
