@@ -84,6 +84,10 @@ def parse():
     ap.add_argument("--workload", default=None, help="measure this workload only")
     ap.add_argument("--chain", action="store_true",
                     help="with --workload: the dependent decoder-layer chain")
+    ap.add_argument("--multirate", action="store_true",
+                    help="measure only the multi-rate control tick (VLM backbone + action expert)")
+    ap.add_argument("--no-multirate", action="store_true",
+                    help="leave the multi-rate control tick out of the full run")
     ap.add_argument("--cpu-rows", type=int, default=None, help="activation rows in the oracle sample")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="oracle time the headline CPU baseline sample is sized to")
@@ -555,12 +559,70 @@ def run_workload(args, name, chain, cpu_seconds, eb, W, torch, dev):
     return out
 
 
+def run_multirate(args, eb, W, torch, dev):
+    """Control ticks of a VLM-backboned policy with a flow-matching action
+    expert (include/eb_multirate.h): the backbone module is the dependent
+    816-row prefill chain (18 layers, d = 2048), refreshed every R ticks; the
+    expert module is one denoising step of the 50-row action-expert chain
+    (18 layers, d = 1024), run 10 times every tick.  Reports ms per tick
+    averaged over whole refresh cycles for R = 1, 2, 4, and the refresh and
+    reuse ticks of R = 4 separately."""
+    import dataclasses
+
+    wb = W.WORKLOADS["q8_0_vlm_prefill_816"]
+    we = dataclasses.replace(W.WORKLOADS["q8_0_action_expert_50x10"], steps=1)
+    mods_ops = []
+    for wl in (wb, we):
+        qws = {(layer, p): eb.quantize(W.weights(wl, layer, p, dev), wl.qtype)
+               for layer in range(wl.layers) for p in range(len(wl.projections))}
+        entries, _, _ = chain_entries(wl, W, qws, dev, torch)
+        mods_ops.append((eb.make_ops(entries), entries, qws))
+    b_ops, e_ops = mods_ops[0][0], mods_ops[1][0]
+    out = {"unit": "ms/tick", "expert_steps_per_tick": 10,
+           "modules": {"backbone": "q8_0_vlm_prefill_816 chain (period R)",
+                       "expert": "q8_0_action_expert_50x10 chain, one step (10 per tick)"}}
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    cycles = max(1, args.steps // 10)
+    for R in (1, 2, 4):
+        mods = eb.make_modules([(b_ops, R, 0, 1), (e_ops, 1, 0, 10)])
+        for t in range(R):          # warm-up cycle: plans built, graphs captured
+            eb.multirate_tick(mods, t, dev)
+        torch.cuda.synchronize()
+        a.record()
+        for c in range(cycles):
+            for t in range(R):
+                eb.multirate_tick(mods, t, dev)
+        b.record()
+        torch.cuda.synchronize()
+        out[f"R{R}"] = round(a.elapsed_time(b) / (cycles * R), 4)
+        if R == 4:
+            per = []
+            for t in range(2):
+                torch.cuda.synchronize()
+                a.record()
+                for _ in range(cycles):
+                    eb.multirate_tick(mods, t, dev)
+                b.record()
+                torch.cuda.synchronize()
+                per.append(a.elapsed_time(b) / cycles)
+            out["refresh_tick_ms"], out["reuse_tick_ms"] = round(per[0], 4), round(per[1], 4)
+        log(f"[bench] multi-rate tick, backbone every {R} ticks: {out[f'R{R}']:.4f} ms/tick")
+        del mods
+    # without reuse the backbone would run before every denoising step
+    out["no_reuse_estimate_ms"] = round(10 * (out["refresh_tick_ms"] - out["reuse_tick_ms"])
+                                        + out["reuse_tick_ms"], 4)
+    eb.stack_cache_clear()
+    del mods_ops
+    torch.cuda.empty_cache()
+    return out
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}, WORLD_SIZE {world}): "
-              "this build has no multi-GPU path; run with --gpus 1.", file=sys.stderr)
+              "there is no multi-GPU path; run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
     import torch
@@ -598,6 +660,9 @@ def main():
         r = run_workload(args, args.workload, args.chain, args.cpu_seconds, eb, W, torch, dev)
         print(json.dumps({**common, **r}), flush=True)
         return
+    if args.multirate:
+        print(json.dumps({**common, "multirate": run_multirate(args, eb, W, torch, dev)}), flush=True)
+        return
 
     results = {}
     for name, chain in ALL_CONFIGS:
@@ -605,6 +670,8 @@ def main():
         secs = args.cpu_seconds if head else args.cpu_seconds_other
         results[name + ("_chain" if chain else "")] = run_workload(args, name, chain, secs, eb, W,
                                                                     torch, dev)
+    if not args.no_multirate:
+        results["multirate_vla_tick"] = run_multirate(args, eb, W, torch, dev)
     head = results.pop(HEADLINE[0] + "_chain")
     if head["cpu_baseline"] is not None:
         head["cpu_baseline"]["single_thread"] = cpu_single_thread(W, dev)

@@ -113,6 +113,19 @@ lib.eb_qlinear_tuned.restype = _i32
 lib.eb_qlinear_tuned.argtypes = [ctypes.POINTER(eb_qlinear_op), _i32, _i32, _vp, ctypes.c_size_t, _vp]
 lib.eb_qlinear_stack_launches.restype = _i32
 lib.eb_qlinear_stack_launches.argtypes = [ctypes.POINTER(eb_qlinear_op), _i32]
+
+
+class eb_module(ctypes.Structure):
+    _fields_ = [("ops", ctypes.POINTER(eb_qlinear_op)), ("n_ops", _i32), ("period", _i32),
+                ("phase", _i32), ("repeats", _i32)]
+
+
+lib.eb_multirate_workspace_bytes.restype = ctypes.c_size_t
+lib.eb_multirate_workspace_bytes.argtypes = [ctypes.POINTER(eb_module), _i32]
+lib.eb_multirate_tick.restype = _i32
+lib.eb_multirate_tick.argtypes = [ctypes.POINTER(eb_module), _i32, _i64, _vp, ctypes.c_size_t, _vp]
+lib.eb_multirate_launches.restype = _i32
+lib.eb_multirate_launches.argtypes = [ctypes.POINTER(eb_module), _i32, _i64]
 lib.eb_stack_cache_clear.restype = _i32
 lib.eb_stack_cache_clear.argtypes = []
 lib.eb_mfma_tile_count.restype = _i32
@@ -349,3 +362,35 @@ def stack_cache_clear() -> None:
 
 def mfma_tile_count() -> int:
     return int(lib.eb_mfma_tile_count())
+
+
+def make_modules(specs) -> ctypes.Array:
+    """specs: iterable of (ops array from make_ops, period, phase, repeats).
+    The op arrays are kept on the result (the modules point into them)."""
+    specs = list(specs)
+    arr = (eb_module * len(specs))()
+    for i, (ops, period, phase, repeats) in enumerate(specs):
+        arr[i] = eb_module(ctypes.cast(ops, ctypes.POINTER(eb_qlinear_op)), len(ops), period, phase,
+                           repeats)
+    arr._eb_ops = [s[0] for s in specs]
+    return arr
+
+
+def multirate_tick(mods: ctypes.Array, tick: int, device=None) -> None:
+    """eb_multirate_tick with a workspace that belongs to this module array."""
+    nbytes = int(lib.eb_multirate_workspace_bytes(mods, len(mods)))
+    ws = getattr(mods, "_eb_workspace", None)
+    if nbytes and (ws is None or ws.numel() < nbytes):
+        ws = torch.empty(nbytes, dtype=torch.uint8,
+                         device=device if device is not None else torch.device("cuda"))
+        mods._eb_workspace = ws
+    dev = ws.device if ws is not None else torch.device("cuda")
+    _check(lib.eb_multirate_tick(mods, len(mods), tick, ws.data_ptr() if nbytes else None, nbytes,
+                                 _stream(dev)), "eb_multirate_tick")
+
+
+def multirate_launches(mods: ctypes.Array, tick: int) -> int:
+    n = lib.eb_multirate_launches(mods, len(mods), tick)
+    if n < 0:
+        raise EBError(n, "eb_multirate_launches")
+    return n

@@ -24,7 +24,8 @@ def eb():
 
 
 def declared_functions():
-    text = open(HEADER).read()
+    text = "".join(open(os.path.join(ROOT, "include", h)).read()
+                   for h in sorted(os.listdir(os.path.join(ROOT, "include"))) if h.endswith(".h"))
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"\b(eb_[a-z0-9_]+)\s*\(", text)))
 
@@ -455,7 +456,9 @@ def test_no_process_wide_setters_in_the_abi():
     choice is a per-call argument of the tuning header)."""
     names = declared_functions()
     assert not [n for n in names if "force" in n or n.startswith("eb_set")], names
-    assert "eb_qlinear_tuned" not in names  # tuning entry points live in eb_tuning.h
+    # tuning entry points live in eb_tuning.h, not in the public eb.h
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    assert "eb_qlinear_tuned" not in text
 
 
 def test_library_imports_no_allocator(eb):
@@ -586,3 +589,38 @@ def test_stack_groups_independent_large_m_mfma_ops(eb, monkeypatch):
     assert _launches(eb, full) == 3
     monkeypatch.setenv("EB_STACK_SPLIT_TAIL", "0")
     assert _launches(eb, full) == 1
+
+
+def test_multirate_policy_and_counts(eb):
+    """Control ticks (include/eb_multirate.h): a module runs on ticks t with
+    t % period == phase, `repeats` times; the tick's launches are the due
+    modules' stack launches; each module gets its own workspace slice."""
+    backbone = [_op(eb, 1 * GB + i * (64 << 20), 8 * GB + i * (1 << 20), 9 * GB + i * (1 << 20),
+                    k=1024, n=2048, m=100, qtype=eb.EB_Q8_0, xt=eb.EB_BF16) for i in range(2)]
+    expert = [_op(eb, 2 * GB + i * (64 << 20), 10 * GB + i * (1 << 20), 11 * GB + i * (1 << 20),
+                  k=1024, n=1024, m=1, qtype=eb.EB_Q4_0) for i in range(3)]
+    b_ops = (eb.eb_qlinear_op * 2)(*backbone)
+    e_ops = (eb.eb_qlinear_op * 3)(*expert)
+    lb, le = _launches(eb, backbone), _launches(eb, expert)
+    mods = eb.make_modules([(b_ops, 4, 1, 1), (e_ops, 1, 0, 10)])
+    for t in range(8):
+        assert eb.multirate_launches(mods, t) == (lb if t % 4 == 1 else 0) + 10 * le, t
+    ws = eb.lib.eb_multirate_workspace_bytes(mods, 2)
+    sb = eb.lib.eb_qlinear_stack_workspace_bytes(b_ops, 2)
+    se = eb.lib.eb_qlinear_stack_workspace_bytes(e_ops, 3)
+    assert ws == (sb + 255) // 256 * 256 + (se + 255) // 256 * 256
+    # bad policies, ticks and workspaces are refused before anything runs
+    L = eb.lib
+    for period, phase, repeats in ((0, 0, 1), (2, 2, 1), (2, -1, 1), (1, 0, 0)):
+        bad = eb.make_modules([(e_ops, period, phase, repeats)])
+        assert L.eb_multirate_launches(bad, 1, 0) == eb.EB_ERR_INVALID
+        assert L.eb_multirate_workspace_bytes(bad, 1) == 0
+        assert L.eb_multirate_tick(bad, 1, 0, None, 0, None) == eb.EB_ERR_INVALID
+    assert L.eb_multirate_launches(mods, 2, -1) == eb.EB_ERR_INVALID
+    assert L.eb_multirate_tick(None, 1, 0, None, 0, None) == eb.EB_ERR_INVALID
+    assert L.eb_multirate_tick(mods, 0, 0, None, 0, None) == eb.EB_ERR_INVALID
+    if ws:
+        assert L.eb_multirate_tick(mods, 2, 0, None, 0, None) == eb.EB_ERR_INVALID
+        assert L.eb_multirate_tick(mods, 2, 0, 12 * GB, ws - 1, None) == eb.EB_ERR_INVALID
+        assert L.eb_multirate_tick(mods, 2, 0, 12 * GB + 16, ws, None) == eb.EB_ERR_ALIGN
+
