@@ -61,6 +61,12 @@
  * normalised.  Threads (pthreads) only split the set of outputs; each output
  * is still one sequential binary64 loop.
  *
+ * Low-precision prefill variant (section 3.2, backend-specific dispatch):
+ * the activations quantized per 32-element block to int8 with a binary32
+ * scale (s = fl32(max|x| / 127), codes rounded half away from zero against
+ * s), each block's product an exact integer sum of code products scaled by
+ * s * d16, and the bound of the activation-quantization error.
+ *
  * Layer steps on either side of the product (section 3.2, operator fusion),
  * each in binary64: rounding to binary16 / bfloat16 (nearest, ties to even),
  * RMS normalisation h * gamma / sqrt(eps + mean h^2) and the SiLU-gated
@@ -571,5 +577,100 @@ int oracle_rmsnorm(const float *h, const float *gamma, double eps, int64_t m, in
 int oracle_silu_mul(const double *g, const double *u, int64_t count, double *out) {
   if (count < 0) return ORACLE_EINVAL;
   for (int64_t i = 0; i < count; ++i) out[i] = g[i] / (1.0 + exp(-g[i])) * u[i];
+  return ORACLE_OK;
+}
+
+/* ---------------------------------------------------------------------- */
+/* Low-precision prefill variant (section 3.2, backend-specific dispatch:  */
+/* the large-m projections on the integer matrix cores).  The activations  */
+/* are quantized per 32-element block along k to int8 with a binary32      */
+/* scale; each block's product is a sum of integer code products, scaled  */
+/* by the activation block scale and the weight block scale.               */
+/* ---------------------------------------------------------------------- */
+
+/* Per row i and block b of x[m][k] (binary16 or bfloat16 words):
+ *   a = max_j |x_ij|,  s_ib = fl32(a / 127)  (0 when a == 0),
+ *   xq_ij = clamp(round_half_away_from_zero(x_ij / s_ib), -127, 127)
+ *           (0 when s_ib == 0),
+ * the quotient in binary64 (x has at most 11 significant bits and s 24, so
+ * it decides every rounding as the exact quotient would).  xq: int8 [m][k];
+ * s: binary32 [m][k/32]. */
+int oracle_quantize_x8(const uint16_t *x, int xdtype, int64_t m, int64_t k, int8_t *xq, float *s) {
+  if (m < 0 || k <= 0 || k % QK != 0) return ORACLE_EINVAL;
+  if (xdtype != ORACLE_X_F16 && xdtype != ORACLE_X_BF16) return ORACLE_EINVAL;
+  for (int64_t i = 0; i < m; ++i)
+    for (int64_t b = 0; b < k / QK; ++b) {
+      double v[QK];
+      float a = 0.0f;
+      for (int j = 0; j < QK; ++j) {
+        uint16_t w = x[i * k + b * QK + j];
+        v[j] = xdtype == ORACLE_X_F16 ? oracle_half_to_double(w) : oracle_bf16_to_double(w);
+        float av = (float)fabs(v[j]); /* exact: a 16-bit value fits binary32 */
+        if (av > a) a = av;
+      }
+      float sc = a / 127.0f;
+      s[i * (k / QK) + b] = sc;
+      for (int j = 0; j < QK; ++j) {
+        int q = 0;
+        if (sc != 0.0f) {
+          double t = round(v[j] / (double)sc); /* half away from zero */
+          if (t > 127.0) t = 127.0;
+          if (t < -127.0) t = -127.0;
+          q = (int)t;
+        }
+        xq[i * k + b * QK + j] = (int8_t)q;
+      }
+    }
+  return ORACLE_OK;
+}
+
+/* Integer code of weight j of a Q8_0 / Q4_0 block. */
+static int int_code(int qtype, const uint8_t *blk, int j) {
+  if (qtype == ORACLE_Q8_0) return (int8_t)blk[2 + j];
+  int byte = blk[2 + (j % (QK / 2))];
+  return ((j < QK / 2) ? (byte & 0x0f) : (byte >> 4)) - 8;
+}
+
+/* y[i][c] = sum_b s_ib * d_nb * P_inb, P_inb = sum_{j in block b} xq_ij * q_nj
+ * (an exact integer), n = cols[c], the outer sum in binary64 in block order;
+ * bound[i][c] = sum_j |s_ib xq_ij| |w_hat_nj| (the scale of an fp32
+ * implementation's rounding error); qerr[i][c] = sum_b (s_ib / 2) sum_{j in b}
+ * |w_hat_nj|, which bounds |y - x . w_hat| for the 16-bit x the codes came
+ * from (every |x_ij - s_ib xq_ij| <= s_ib / 2).  Q8_0 and Q4_0 weights. */
+int oracle_qlinear_x8(int qtype, const uint8_t *blocks, int64_t n, int64_t k, const int8_t *xq,
+                      const float *s, int64_t m, const int64_t *cols, int64_t ncols, double *y,
+                      double *bound, double *qerr) {
+  if ((qtype != ORACLE_Q8_0 && qtype != ORACLE_Q4_0) || k <= 0 || k % QK != 0 || n <= 0 || m < 0 ||
+      ncols < 0)
+    return ORACLE_EINVAL;
+  for (int64_t c = 0; c < ncols; ++c)
+    if (cols[c] < 0 || cols[c] >= n) return ORACLE_EINVAL;
+  const int64_t nb = k / QK, bb = oracle_block_bytes(qtype);
+  for (int64_t c = 0; c < ncols; ++c) {
+    const uint8_t *row = blocks + cols[c] * nb * bb;
+    for (int64_t i = 0; i < m; ++i) {
+      double acc = 0.0, bd = 0.0, qe = 0.0;
+      for (int64_t b = 0; b < nb; ++b) {
+        const uint8_t *blk = row + b * bb;
+        const double d = oracle_half_to_double(get_d16(blk));
+        const double sb = (double)s[i * nb + b];
+        long long p = 0;
+        double wsum = 0.0, xw = 0.0;
+        for (int j = 0; j < QK; ++j) {
+          const int q = int_code(qtype, blk, j);
+          const int xv = xq[i * k + b * QK + j];
+          p += (long long)xv * q;
+          wsum += fabs((double)q * d);
+          xw += fabs((double)xv) * fabs((double)q * d);
+        }
+        acc += sb * d * (double)p;
+        bd += sb * xw;
+        qe += sb / 2.0 * wsum;
+      }
+      y[i * ncols + c] = acc;
+      bound[i * ncols + c] = bd;
+      qerr[i * ncols + c] = qe;
+    }
+  }
   return ORACLE_OK;
 }

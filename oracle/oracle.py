@@ -80,6 +80,14 @@ class Oracle:
         L.oracle_rmsnorm.restype = ctypes.c_int
         L.oracle_rmsnorm.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_double,
                                      ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p]
+        L.oracle_quantize_x8.restype = ctypes.c_int
+        L.oracle_quantize_x8.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int64,
+                                         ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]
+        L.oracle_qlinear_x8.restype = ctypes.c_int
+        L.oracle_qlinear_x8.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_int64,
+                                        ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
+                                        ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64,
+                                        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
         L.oracle_silu_mul.restype = ctypes.c_int
         L.oracle_silu_mul.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
                                       ctypes.c_void_p]
@@ -142,6 +150,39 @@ class Oracle:
             raise ValueError("oracle_qlinear rejected the arguments")
         return y, bound
 
+
+    # -- low-precision prefill variant: int8 activation blocks --------------
+    def quantize_x8(self, x_bits: np.ndarray, xdtype: int):
+        """uint16 [m, k] activation words -> (int8 codes [m, k], binary32 scales [m, k/32])."""
+        x_bits = np.ascontiguousarray(x_bits, dtype=np.uint16)
+        if x_bits.ndim == 1:
+            x_bits = x_bits.reshape(1, -1)
+        m, k = x_bits.shape
+        xq = np.zeros((m, k), dtype=np.int8)
+        s = np.zeros((m, k // QK), dtype=np.float32)
+        if self.lib.oracle_quantize_x8(x_bits.ctypes.data, xdtype, m, k, xq.ctypes.data,
+                                       s.ctypes.data) != 0:
+            raise ValueError("oracle_quantize_x8 rejected the arguments")
+        return xq, s
+
+    def qlinear_x8(self, qtype: int, blocks: np.ndarray, n: int, k: int, xq: np.ndarray,
+                   s: np.ndarray, cols=None):
+        """The int8-activation product.  Returns (y, bound, qerr), float64
+        [m, len(cols)]: y = sum_b s d (integer block dot), bound = sum |x~||w_hat|
+        with x~ = s xq, qerr = the activation-quantization error bound."""
+        blocks = np.ascontiguousarray(blocks, dtype=np.uint8)
+        assert blocks.size == n * (k // QK) * self.block_bytes(qtype)
+        xq = np.ascontiguousarray(xq, dtype=np.int8)
+        s = np.ascontiguousarray(s, dtype=np.float32)
+        m = xq.shape[0]
+        assert xq.shape == (m, k) and s.shape == (m, k // QK)
+        cols = np.arange(n, dtype=np.int64) if cols is None else np.ascontiguousarray(cols, dtype=np.int64)
+        y = np.zeros((m, cols.size)); bound = np.zeros((m, cols.size)); qerr = np.zeros((m, cols.size))
+        if self.lib.oracle_qlinear_x8(qtype, blocks.ctypes.data, n, k, xq.ctypes.data, s.ctypes.data,
+                                      m, cols.ctypes.data, cols.size, y.ctypes.data,
+                                      bound.ctypes.data, qerr.ctypes.data) != 0:
+            raise ValueError("oracle_qlinear_x8 rejected the arguments")
+        return y, bound, qerr
 
     # -- the steps around the linear layer in a decoder layer ---------------
     def round_x16(self, v: np.ndarray, xdtype: int) -> np.ndarray:
