@@ -56,6 +56,7 @@ METRIC = ("qlinear HBM GB/s (M=1) and MFMA TFLOP/s (M≥512) vs MI355X peak; "
           "ms/backbone pass")
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 PEAK_MFMA_16BIT_TFLOPS = 2500.0  # MI355X dense bf16 / fp16 matrix
+PEAK_MFMA_INT8_TOPS = 5000.0     # MI355X dense int8 matrix
 RIDGE_FLOP_PER_BYTE = PEAK_MFMA_16BIT_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)  # 312.5
 MAX_HOST_THREADS = 16
 
@@ -86,6 +87,10 @@ def parse():
                     help="with --workload: the dependent decoder-layer chain")
     ap.add_argument("--multirate", action="store_true",
                     help="measure only the multi-rate control tick (VLM backbone + action expert)")
+    ap.add_argument("--int8", action="store_true",
+                    help="with --workload: the int8-activation prefill path, op by op")
+    ap.add_argument("--no-int8", action="store_true",
+                    help="leave the int8 prefill measurements out of the full run")
     ap.add_argument("--no-multirate", action="store_true",
                     help="leave the multi-rate control tick out of the full run")
     ap.add_argument("--cpu-rows", type=int, default=None, help="activation rows in the oracle sample")
@@ -559,6 +564,59 @@ def run_workload(args, name, chain, cpu_seconds, eb, W, torch, dev):
     return out
 
 
+def run_int8(args, name, eb, W, torch, dev):
+    """The int8-activation prefill path (EB_PATH_MFMA_I8) over every projection
+    of an independent large-m workload, one eb_qlinear_fused_ws call per op in
+    layer order (each op: the activation-quantization launch, then the int8
+    product launch), timed with HIP events on the launch stream.  TOP/s
+    against the dense int8 peak; ms per pass."""
+    import ctypes
+
+    wl = W.WORKLOADS[name]
+    qws = {(layer, p): eb.quantize(W.weights(wl, layer, p, dev), wl.qtype)
+           for layer in range(wl.layers) for p in range(len(wl.projections))}
+    entries, meta, _ = independent_entries(wl, W, qws, dev, torch)
+    ops = eb.make_ops(entries)
+    need = max(int(eb.lib.eb_qlinear_workspace_bytes(ctypes.byref(ops[i]), eb.EB_PATH_MFMA_I8))
+               for i in range(len(ops)))
+    ws = torch.empty(need, dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream().cuda_stream
+    fn, wp = eb.lib.eb_qlinear_fused_ws, ws.data_ptr()
+    refs = [ctypes.byref(ops[i]) for i in range(len(ops))]
+
+    def one_pass():
+        for r in refs:
+            st = fn(r, eb.EB_PATH_MFMA_I8, wp, need, stream)
+            if st != 0:
+                raise SystemExit(f"eb_qlinear_fused_ws (int8 path) failed: {st}")
+
+    for _ in range(max(1, args.warmup // 5)):
+        one_pass()
+    torch.cuda.synchronize()
+    steps = max(1, args.steps // 5)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(steps):
+        one_pass()
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / steps
+    flops = sum(2 * m * n * k for (_, _, m, n, k) in meta)
+    tops = flops / (ms * 1e-3) / 1e12
+    log(f"[bench] {name} int8 path: {ms:.4f} ms/pass, {tops:.1f} TOP/s")
+    del entries, ops, qws, ws
+    torch.cuda.empty_cache()
+    return {"ms_per_step": round(ms, 5), "value": round(tops, 2), "unit": "TOP/s", "steps": steps,
+            "launches_per_pass": 2 * len(meta),
+            "dtype": f"{wl.qtype} weight codes x int8 activation blocks, i32 block products, f32 accumulate",
+            "config": {"workload": name + "_int8", "m": wl.m, "layers": wl.layers,
+                       "ops_per_pass": len(meta), "flops_per_pass": flops,
+                       "graph_replay": False, "dependent_chain": False},
+            "roofline": {"bound": "mfma", "achieved": round(tops, 2), "peak": PEAK_MFMA_INT8_TOPS,
+                         "unit": "TOP/s", "frac": round(tops / PEAK_MFMA_INT8_TOPS, 4),
+                         "note": "whole pass incl. the activation-quantization launches"}}
+
+
 def run_multirate(args, eb, W, torch, dev):
     """Control ticks of a VLM-backboned policy with a flow-matching action
     expert (include/eb_multirate.h): the backbone module is the dependent
@@ -656,6 +714,9 @@ def main():
     common = {"metric": METRIC, "n_gpus": 1, "higher_is_better": True, "scaling": "weak",
               "vs_baseline": None,
               "data": "synthetic (seeded N(0,0.02) weights, N(0,1) activations and stream)"}
+    if args.workload and args.int8:
+        print(json.dumps({**common, **run_int8(args, args.workload, eb, W, torch, dev)}), flush=True)
+        return
     if args.workload:
         r = run_workload(args, args.workload, args.chain, args.cpu_seconds, eb, W, torch, dev)
         print(json.dumps({**common, **r}), flush=True)
@@ -670,6 +731,9 @@ def main():
         secs = args.cpu_seconds if head else args.cpu_seconds_other
         results[name + ("_chain" if chain else "")] = run_workload(args, name, chain, secs, eb, W,
                                                                     torch, dev)
+    if not args.no_int8:
+        for name in ("q4_0_video_wam_4096", "q8_0_vlm_prefill_816"):
+            results[name + "_int8"] = run_int8(args, name, eb, W, torch, dev)
     if not args.no_multirate:
         results["multirate_vla_tick"] = run_multirate(args, eb, W, torch, dev)
     head = results.pop(HEADLINE[0] + "_chain")

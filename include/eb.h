@@ -109,6 +109,16 @@ typedef int32_t eb_status;
 #define EB_PATH_AUTO 0 /* pick by m, qtype and shape (measured crossover) */
 #define EB_PATH_GEMV 1 /* bandwidth-bound GEMV, requires m <= 8 and m' * k <= 65536, m' = m rounded up to 1, 2, 4 or 8 */
 #define EB_PATH_MFMA 2 /* LDS-tiled dequantize-to-16-bit + MFMA, any m */
+/* Low-precision prefill variant (section 3.2, backend-specific dispatch), Q8_0 /
+ * Q4_0, opt-in only (EB_PATH_AUTO never takes it): x is quantized per
+ * 32-element block along k to int8 (s = fl32(max|x| / 127), codes rounded half
+ * away from zero against s, into the workspace: eb_qlinear_workspace_bytes),
+ * the weight codes go to the int8 matrix cores as they are and each block's
+ * exact integer product is scaled by s * d16 in fp32.  Accuracy: within 2e-3
+ * of that method's exact value, normalised by sum |s xq||w_hat|; it differs
+ * from the 16-bit product by at most sum_b (s_b / 2) sum_{k in b} |w_hat|.
+ * No normalisation prologue (EB_ERR_UNSUPPORTED); epilogues as usual. */
+#define EB_PATH_MFMA_I8 3
 
 /* A quantized weight matrix W[n][k] in the planar device layout above.
  * `data` is a device pointer, 256-byte aligned, eb_qweights_bytes(type, n, k)

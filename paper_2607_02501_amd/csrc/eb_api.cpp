@@ -117,7 +117,8 @@ eb_status check_op(const eb_qlinear_op &o, int32_t path) {
   const int64_t m = o.m;
   if (m < 0 || m > kMaxM) return EB_ERR_INVALID;
   if (!known_dtype(o.x_type) || !known_dtype(o.y_type)) return EB_ERR_INVALID;
-  if (path != EB_PATH_AUTO && path != EB_PATH_GEMV && path != EB_PATH_MFMA) return EB_ERR_INVALID;
+  if (path != EB_PATH_AUTO && path != EB_PATH_GEMV && path != EB_PATH_MFMA && path != EB_PATH_MFMA_I8)
+    return EB_ERR_INVALID;
   if (o.prologue != EB_PRO_NONE && o.prologue != EB_PRO_RMSNORM) return EB_ERR_INVALID;
   if (o.epilogue != EB_EPI_NONE && o.epilogue != EB_EPI_ADD && o.epilogue != EB_EPI_GLU)
     return EB_ERR_INVALID;
@@ -141,9 +142,12 @@ eb_status check_op(const eb_qlinear_op &o, int32_t path) {
   if (o.epilogue == EB_EPI_ADD && o.residual != o.y && overlaps(o.y, yb, o.residual, yb))
     return EB_ERR_INVALID;
   if (path == EB_PATH_GEMV && !gemv_fits(m, o.w.k)) return EB_ERR_UNSUPPORTED;
+  if (path == EB_PATH_MFMA_I8 && (o.w.type == EB_Q6_S || o.prologue != EB_PRO_NONE ||
+                                  !i8_fits(m, o.w.n, o.w.k)))
+    return EB_ERR_UNSUPPORTED;
   if (o.w.type == EB_Q6_S && path == EB_PATH_GEMV && !gemv_q6_fits(m, o.w.n, o.w.k))
     return EB_ERR_UNSUPPORTED;
-  if (o.w.type == EB_Q6_S && path != EB_PATH_GEMV && !q6_fits(m, o.w.n, o.w.k))
+  if (o.w.type == EB_Q6_S && path == EB_PATH_MFMA && !q6_fits(m, o.w.n, o.w.k))
     return EB_ERR_UNSUPPORTED;
   return EB_OK;
 }
@@ -220,6 +224,10 @@ eb_status launch_op(const eb_qlinear_op &o, int32_t path, uint8_t *ws, size_t ws
   hipError_t e;
   if (path == EB_PATH_GEMV) {
     e = launch_gemv(o.w.type, o.w.data, o.w.n, o.w.k, o.x, o.x_type, o.m, o.y, o.y_type, fuse_of(o), s);
+  } else if (path == EB_PATH_MFMA_I8) {
+    if (!ws || wsb < i8_workspace_bytes(o.m, o.w.k)) return EB_ERR_UNSUPPORTED;
+    e = launch_mfma_i8(o.w.type, o.w.data, o.w.n, o.w.k, o.x, o.x_type, o.m, o.y, o.y_type, fuse_of(o),
+                       ws, s);
   } else {
     const OpScratch sc = op_scratch(o, ws ? wsb : 0, force_cfg, force_splits);
     if (sc.xb && (!ws || wsb < sc.xb)) return EB_ERR_UNSUPPORTED;
@@ -976,6 +984,7 @@ size_t eb_qlinear_workspace_bytes(const eb_qlinear_op *op, int32_t path) {
   if (!op || check_op(*op, path) != EB_OK || op->m == 0) return 0;
   if (path == EB_PATH_AUTO) path = pick_path(op->w.type, op->x_type, op->m, op->w.n, op->w.k);
   if (path == EB_PATH_GEMV) return 0;
+  if (path == EB_PATH_MFMA_I8) return i8_workspace_bytes(op->m, op->w.k);
   return op_scratch(*op, kMaxSplitWorkspace + xhat_bytes(*op)).total;
 }
 
@@ -997,6 +1006,8 @@ eb_status eb_qlinear_fused_static(const eb_qlinear_op *op, int32_t path, hipStre
   const int32_t p =
       path == EB_PATH_AUTO ? pick_path(op->w.type, op->x_type, op->m, op->w.n, op->w.k) : path;
   if (p == EB_PATH_MFMA && xhat_bytes(*op) > kStaticScratchBytes) return EB_ERR_UNSUPPORTED;
+  if (p == EB_PATH_MFMA_I8 && i8_workspace_bytes(op->m, op->w.k) > kStaticScratchBytes)
+    return EB_ERR_UNSUPPORTED;
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return EB_ERR_HIP;
   uint8_t *ws = static_scratch(dev);

@@ -183,6 +183,15 @@ hipError_t launch_gemv_q6(const void *wdata, int64_t n, int64_t k, const void *x
 bool q6_fits(int64_t m, int64_t n, int64_t k);
 hipError_t launch_mfma_q6(const void *wdata, int64_t n, int64_t k, const void *x, int32_t xt,
                           int64_t m, void *y, int32_t yt, const Fuse &f, hipStream_t s);
+// Low-precision prefill variant (mfma_i8.hip, Q8_0 / Q4_0): x quantized per
+// 32-element block to int8 into the workspace (i8_workspace_bytes: the codes,
+// then the block scales), then the int8 matrix-core product with per-block
+// scaling.
+size_t i8_workspace_bytes(int64_t m, int64_t k);
+bool i8_fits(int64_t m, int64_t n, int64_t k);
+hipError_t launch_mfma_i8(int32_t type, const void *wdata, int64_t n, int64_t k, const void *x,
+                          int32_t xt, int64_t m, void *y, int32_t yt, const Fuse &f, void *ws,
+                          hipStream_t s);
 // Whether a workgroup's byte spans of a bm x bn tile fit 32-bit buffer offsets.
 bool mfma_fits_offsets(int32_t type, int64_t n, int64_t k, int bm, int bn);
 int mfma_tile_count();

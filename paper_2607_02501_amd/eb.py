@@ -33,6 +33,7 @@ EB_BF16 = 2
 EB_PATH_AUTO = 0
 EB_PATH_GEMV = 1
 EB_PATH_MFMA = 2
+EB_PATH_MFMA_I8 = 3
 EB_PRO_NONE = 0
 EB_PRO_RMSNORM = 1
 EB_EPI_NONE = 0
@@ -44,7 +45,7 @@ QTYPES = {"q8_0": EB_Q8_0, "q4_0": EB_Q4_0, "q6_s": EB_Q6_S}
 BLOCK_ELEMS = {"q8_0": 32, "q4_0": 32, "q6_s": 256}
 BLOCK_BYTES = {"q8_0": 34, "q4_0": 18, "q6_s": 210}
 DTYPES = {torch.float32: EB_F32, torch.float16: EB_F16, torch.bfloat16: EB_BF16}
-PATHS = {"auto": EB_PATH_AUTO, "gemv": EB_PATH_GEMV, "mfma": EB_PATH_MFMA}
+PATHS = {"auto": EB_PATH_AUTO, "gemv": EB_PATH_GEMV, "mfma": EB_PATH_MFMA, "mfma_i8": EB_PATH_MFMA_I8}
 PROLOGUES = {None: EB_PRO_NONE, "none": EB_PRO_NONE, "rmsnorm": EB_PRO_RMSNORM}
 EPILOGUES = {None: EB_EPI_NONE, "none": EB_EPI_NONE, "add": EB_EPI_ADD, "glu": EB_EPI_GLU}
 

@@ -16,6 +16,7 @@ _FILES = {
     # the Q6_S kernel (every m)
     "q6": ("mfma_q6.hip", "mfma_common.h", "norm.hip") + _COMMON,
     "gemv_q6": ("gemv_q6.hip",) + _COMMON,
+    "i8": ("mfma_i8.hip", "mfma_common.h") + _COMMON,
 }
 
 
@@ -25,6 +26,8 @@ def family(symbol: str) -> str:
         return "gemv_q6"
     if symbol.startswith("gemv"):
         return "gemv"
+    if symbol.startswith("mm_i8") or symbol.startswith("quantize_x8"):
+        return "i8"
     if symbol.startswith("mm_q6"):
         return "q6"
     if symbol.startswith("mm_narrow"):

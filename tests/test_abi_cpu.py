@@ -624,3 +624,30 @@ def test_multirate_policy_and_counts(eb):
         assert L.eb_multirate_tick(mods, 2, 0, 12 * GB, ws - 1, None) == eb.EB_ERR_INVALID
         assert L.eb_multirate_tick(mods, 2, 0, 12 * GB + 16, ws, None) == eb.EB_ERR_ALIGN
 
+
+def test_int8_path_validation(eb):
+    """The int8-activation prefill path: Q8_0 / Q4_0 only, no prologue, a
+    workspace for the codes (m * k bytes, 256-aligned) and block scales
+    (k/32 * round_up(m, 4) floats); never chosen by the automatic path."""
+    L = eb.lib
+    q = L.eb_qlinear_workspace_bytes
+    for m in (1, 37, 816):
+        op = eb.eb_qlinear_op(_w(eb, eb.EB_Q8_0, n=2048, k=4096, data=1 * GB), 8 * GB, 9 * GB, m,
+                              eb.EB_BF16, eb.EB_F32)
+        expect = (m * 4096 + 255) // 256 * 256 + (128 * ((m + 3) // 4 * 4) * 4 + 255) // 256 * 256
+        assert q(ctypes.byref(op), eb.EB_PATH_MFMA_I8) == expect, m
+        assert L.eb_qlinear_auto_path(eb.EB_Q8_0, eb.EB_BF16, m, 2048, 4096) != eb.EB_PATH_MFMA_I8
+        # no workspace: refused before anything runs
+        assert L.eb_qlinear_fused_ws(ctypes.byref(op), eb.EB_PATH_MFMA_I8, None, 0, None) == \
+            eb.EB_ERR_UNSUPPORTED
+    q6 = eb.eb_qlinear_op(_w(eb, eb.EB_Q6_S, n=2048, k=4096, data=1 * GB), 8 * GB, 9 * GB, 100,
+                          eb.EB_BF16, eb.EB_F32)
+    assert L.eb_qlinear_fused_ws(ctypes.byref(q6), eb.EB_PATH_MFMA_I8, None, 0, None) == \
+        eb.EB_ERR_UNSUPPORTED
+    normed = eb.eb_qlinear_op(_w(eb, eb.EB_Q4_0, n=2048, k=4096, data=1 * GB), 8 * GB, 9 * GB, 100,
+                              eb.EB_BF16, eb.EB_F32, eb.EB_PRO_RMSNORM, 0, G, None, 1e-5, 0)
+    assert L.eb_qlinear_fused_ws(ctypes.byref(normed), eb.EB_PATH_MFMA_I8, None, 0, None) == \
+        eb.EB_ERR_UNSUPPORTED
+    assert L.eb_qlinear_ex(ctypes.byref(_w(eb)), X, eb.EB_F16, 4, Y, eb.EB_F32, 4, None) == \
+        eb.EB_ERR_INVALID   # unknown path
+
