@@ -83,12 +83,6 @@ __global__ void __launch_bounds__(kThreads)
   finish_row<XT>(ss, red, h + row * k, g, eps, k, out + row * (k / 2));
 }
 
-// Split-K reduction of a projection with n outputs per row whose fp32 output
-// row h is the next projection's input under a normalisation prologue: row
-// `row` of y = the partials summed in split order (+ the residual), as the
-// plain reduction computes each element, then the row is normalised into
-// `out` for the next projection.  One workgroup per row; every thread reads
-// back only the y elements it wrote itself.
 // Sum of the partials of flat element o (float4 at o) in split order, plus
 // the residual.
 __device__ inline float4 reduce4(const float *__restrict__ ws, int splits, int64_t ws_stride,
@@ -145,6 +139,12 @@ __global__ void __launch_bounds__(kThreads)
   }
 }
 
+// Split-K reduction of a projection with n outputs per row whose fp32 output
+// row h is the next projection's input under a normalisation prologue: row
+// `row` of y = the partials summed in split order (+ the residual), as the
+// plain reduction computes each element, then the row is normalised into
+// `out` for the next projection.  One workgroup per row; every thread reads
+// back only the y elements it wrote itself.
 template <int XT>
 __global__ void __launch_bounds__(kThreads)
     reduce_rmsnorm_kernel(const float *__restrict__ ws, int splits, int64_t ws_stride, int64_t n,
