@@ -136,7 +136,7 @@ struct MfmaPlan {
   int cfg = 0;
   bool q6 = false;        // Q6_S weights: the Q6_S kernel (any m, no split)
   bool hl = false;        // bfloat16 activations at m <= 128: hi/lo weight tiles
-  bool narrow = false;    // m <= kNarrowMaxM: the one-launch narrow kernel (no tiles, no split)
+  bool narrow = false;    // m <= kNarrowMaxM: the narrow kernel (splits > 1: plus the reduction)
   int splits = 1;
   int kts = 0;            // K-tiles of 64 per split
   int64_t ws_stride = 0;  // floats between the partial outputs of two splits
@@ -166,12 +166,16 @@ hipError_t mfma_tile_launch(int cfg, bool hl, const void *wdata, int64_t n, int6
 // Lone small-m projections (m <= kNarrowMaxM) in one launch: 16 weight rows
 // and the whole of k per workgroup, k split over its waves and the partial
 // tiles added through LDS (mfma_narrow.hip).  hl: bfloat16 hi/lo pairs.
+// When the 16-row workgroups do not fill the GPU, k is split (narrow_splits)
+// and each split writes fp32 partial sums for the ordered reduction.
 constexpr int64_t kNarrowMaxM = 64;
-constexpr int64_t kNarrowMaxK = 2048;
-bool narrow_fits(int64_t m, int64_t n, int64_t k);
+constexpr int64_t kNarrowMaxK = 2048;  // k per split
+constexpr int kNarrowMaxSplits = 8;
+bool narrow_fits(int64_t m, int64_t n, int64_t k, int splits);
+int narrow_splits(int64_t n, int64_t k, int cus);
 hipError_t launch_mfma_narrow(int32_t type, const void *wdata, int64_t n, int64_t k, const void *x,
                               int32_t xt, bool hl, int64_t m, void *y, int32_t yt, const Fuse &f,
-                              hipStream_t s);
+                              int splits, float *ws, int64_t ws_stride, hipStream_t s);
 // Q6_S weights, m <= 8 (gemv_q6.hip): a wave per pair of weight rows, lanes
 // over 32-weight chunks, fp32 products of the 6-bit codes and x staged in LDS.
 bool gemv_q6_fits(int64_t m, int64_t n, int64_t k);

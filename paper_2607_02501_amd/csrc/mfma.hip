@@ -154,13 +154,22 @@ MfmaPlan plan_mfma(int32_t type, int32_t xt, int64_t m, int64_t n, int64_t k, si
     best.kts = (int)nk;
     return best;
   }
-  // a lone small-m projection: one launch of the narrow kernel, whole k per
-  // workgroup (measured on the action-expert chain: the tiled kernel split
-  // along k plus its reduction took about 16 us per projection)
-  if (fc < 0 && fs <= 0 && narrow_fits(m, n, k)) {
-    best.narrow = true;
-    best.kts = (int)nk;
-    return best;
+  // a lone small-m projection: the narrow kernel (16 weight rows per
+  // workgroup), k split only when its workgroups do not fill the GPU
+  // (measured on the action-expert chain: the tiled kernel split along k
+  // plus its reduction took about 16 us per projection)
+  if (fc < 0 && fs <= 0 && m <= kNarrowMaxM) {
+    int sp = narrow_splits(n, k, cus);
+    const int64_t stride = (m * n + 63) / 64 * 64;
+    if (sp > 1 && (size_t)(stride * sp * 4) > max_ws) sp = 1;
+    if (narrow_fits(m, n, k, sp)) {
+      best.narrow = true;
+      best.splits = sp;
+      best.kts = (int)nk;
+      best.ws_stride = sp > 1 ? stride : 0;
+      best.ws_bytes = sp > 1 ? (size_t)(stride * sp * 4) : 0;
+      return best;
+    }
   }
   double best_t = 0;
   bool have = false;
@@ -264,8 +273,9 @@ hipError_t launch_q(const void *wdata, int64_t n, int64_t k, const void *x, int6
   const int sp = ws ? P.splits : 1;
   const int kts = ws ? P.kts : (int)((k + kBK - 1) / kBK);
   const int64_t st = P.ws_stride;
-  if (P.narrow) return launch_mfma_narrow(QT, wdata, n, k, x, XT, P.hl, m, y, yt, f, s);
-  const hipError_t e = mfma_tile_launch<QT, XT>(P.cfg, P.hl, wdata, n, k, x, m, y, yt, f, sp, kts, ws, st, s);
+  const hipError_t e =
+      P.narrow ? launch_mfma_narrow(QT, wdata, n, k, x, XT, P.hl, m, y, yt, f, sp, ws, st, s)
+               : mfma_tile_launch<QT, XT>(P.cfg, P.hl, wdata, n, k, x, m, y, yt, f, sp, kts, ws, st, s);
   if (e != hipSuccess || sp == 1) return e;
   if (no) {
     if (yt != EB_F32 || f.epi == EB_EPI_GLU) return hipErrorInvalidValue;

@@ -16,6 +16,9 @@
 // ahead of their MFMAs.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+#include <cstdlib>
+
 #include "eb_internal.h"
 #include "epilogue.h"
 #include "mfma_common.h"
@@ -76,7 +79,7 @@ template <int QT, int XT, int YT, int MB, bool HL>
 __global__ void __launch_bounds__(kWaves * 64)
     mm_narrow_kernel(const uint8_t *__restrict__ wdata, int64_t n, int64_t k, int64_t d_off,
                      int64_t ds, const uint16_t *__restrict__ x, int m, void *__restrict__ y, int yt,
-                     Fuse f) {
+                     Fuse f, int splits, float *__restrict__ ws, int64_t ws_stride) {
   static_assert(!HL || XT == EB_BF16, "hi/lo pairs are for bfloat16 activations");
   constexpr int KS = kWaves;                        // slices of k
   constexpr int NT = 16;                            // weight rows per workgroup
@@ -93,8 +96,13 @@ __global__ void __launch_bounds__(kWaves * 64)
   const int r16 = lane & 15, g4 = lane >> 4;
   const int64_t n0 = (int64_t)blockIdx.x * NT;
   const int rows_n = (int)min((int64_t)NT, n - n0);
+  // split blockIdx.y of `splits` takes blocks [sb0, sb1) of k; its waves
+  // split that range further
   const int nb = (int)(k / kQK);
-  const int b0 = (int)((int64_t)nb * slice / KS), b1 = (int)((int64_t)nb * (slice + 1) / KS);
+  const int sp = (int)blockIdx.y;
+  const int sb0 = (int)((int64_t)nb * sp / splits), sb1 = (int)((int64_t)nb * (sp + 1) / splits);
+  const int b0 = sb0 + (int)((int64_t)(sb1 - sb0) * slice / KS);
+  const int b1 = sb0 + (int)((int64_t)(sb1 - sb0) * (slice + 1) / KS);
 
   // Raw buffer descriptors over this workgroup's rows (rows past n read
   // zeros) and over x's m rows (rows past m read zeros).
@@ -118,7 +126,7 @@ __global__ void __launch_bounds__(kWaves * 64)
   constexpr uint32_t kPast = 0x80000000u;  // past every descriptor here
   const int t = threadIdx.x;
   float res[PPT][2];
-  if (f.epi == EB_EPI_ADD) {
+  if (f.epi == EB_EPI_ADD && !ws) {  // (a split's reduction adds the residual)
     constexpr uint32_t es = (YT == EB_F32) ? 4 : 2;
     const auto rr = rsrc(f.r, (uint32_t)(m * n) * es);
 #pragma unroll
@@ -215,6 +223,12 @@ __global__ void __launch_bounds__(kWaves * 64)
     const int col = 16 * mb + (l & 15);               // row of x / y
     const int nl = 4 * (l >> 4) + 2 * p;              // first of the two rows
     if (col >= m || nl >= rows_n) continue;
+    if (ws) {  // a split of k: the raw partial sums, for the ordered reduction
+      float *w = ws + (int64_t)sp * ws_stride + (int64_t)col * n + n0 + nl;
+      w[0] = v0;
+      if (nl + 1 < rows_n) w[1] = v1;
+      continue;
+    }
     if (f.epi == EB_EPI_GLU) {  // n even: the pair (gate, up) is complete
       store_y(y, (int64_t)col * (n / 2) + (n0 + nl) / 2, silu_mul(v0, v1), yt);
       continue;
@@ -229,56 +243,82 @@ __global__ void __launch_bounds__(kWaves * 64)
   }
 }
 
+struct Split {
+  int splits;
+  float *ws;
+  int64_t stride;
+};
+
 template <int QT, int XT, int YT, bool HL>
 hipError_t launch_mb(const void *wdata, int64_t n, int64_t k, const void *x, int64_t m, void *y,
-                     int32_t yt, const Fuse &f, hipStream_t s) {
+                     int32_t yt, const Fuse &f, const Split &sp, hipStream_t s) {
   const Layout L = layout_of(QT, n, k);
-  const unsigned grid = (unsigned)((n + 15) / 16);
+  const dim3 grid((unsigned)((n + 15) / 16), (unsigned)sp.splits);
   const auto *xp = static_cast<const uint16_t *>(x);
   const auto *wp = static_cast<const uint8_t *>(wdata);
   if (m <= 16)
-    mm_narrow_kernel<QT, XT, YT, 1, HL><<<grid, kWaves * 64, 0, s>>>(wp, n, k, L.d_off, L.ds, xp, (int)m, y, yt, f);
+    mm_narrow_kernel<QT, XT, YT, 1, HL><<<grid, kWaves * 64, 0, s>>>(wp, n, k, L.d_off, L.ds, xp, (int)m, y, yt, f, sp.splits, sp.ws, sp.stride);
   else if (m <= 32)
-    mm_narrow_kernel<QT, XT, YT, 2, HL><<<grid, kWaves * 64, 0, s>>>(wp, n, k, L.d_off, L.ds, xp, (int)m, y, yt, f);
+    mm_narrow_kernel<QT, XT, YT, 2, HL><<<grid, kWaves * 64, 0, s>>>(wp, n, k, L.d_off, L.ds, xp, (int)m, y, yt, f, sp.splits, sp.ws, sp.stride);
   else
-    mm_narrow_kernel<QT, XT, YT, 4, HL><<<grid, kWaves * 64, 0, s>>>(wp, n, k, L.d_off, L.ds, xp, (int)m, y, yt, f);
+    mm_narrow_kernel<QT, XT, YT, 4, HL><<<grid, kWaves * 64, 0, s>>>(wp, n, k, L.d_off, L.ds, xp, (int)m, y, yt, f, sp.splits, sp.ws, sp.stride);
   return hipGetLastError();
 }
 
 template <int QT, int XT, bool HL>
 hipError_t launch_y(const void *wdata, int64_t n, int64_t k, const void *x, int64_t m, void *y,
-                    int32_t yt, const Fuse &f, hipStream_t s) {
-  if (yt == EB_F32) return launch_mb<QT, XT, EB_F32, HL>(wdata, n, k, x, m, y, yt, f, s);
-  return launch_mb<QT, XT, EB_BF16, HL>(wdata, n, k, x, m, y, yt, f, s);
+                    int32_t yt, const Fuse &f, const Split &sp, hipStream_t s) {
+  if (yt == EB_F32) return launch_mb<QT, XT, EB_F32, HL>(wdata, n, k, x, m, y, yt, f, sp, s);
+  return launch_mb<QT, XT, EB_BF16, HL>(wdata, n, k, x, m, y, yt, f, sp, s);
 }
 
 template <int QT>
 hipError_t launch_x(int32_t xt, bool hl, const void *wdata, int64_t n, int64_t k, const void *x,
-                    int64_t m, void *y, int32_t yt, const Fuse &f, hipStream_t s) {
-  if (xt == EB_F16) return launch_y<QT, EB_F16, false>(wdata, n, k, x, m, y, yt, f, s);
-  if (hl) return launch_y<QT, EB_BF16, true>(wdata, n, k, x, m, y, yt, f, s);
-  return launch_y<QT, EB_BF16, false>(wdata, n, k, x, m, y, yt, f, s);
+                    int64_t m, void *y, int32_t yt, const Fuse &f, const Split &sp, hipStream_t s) {
+  if (xt == EB_F16) return launch_y<QT, EB_F16, false>(wdata, n, k, x, m, y, yt, f, sp, s);
+  if (hl) return launch_y<QT, EB_BF16, true>(wdata, n, k, x, m, y, yt, f, sp, s);
+  return launch_y<QT, EB_BF16, false>(wdata, n, k, x, m, y, yt, f, sp, s);
 }
 
 }  // namespace
 
-bool narrow_fits(int64_t m, int64_t n, int64_t k) {
-  // Every workgroup reads all of x (up to 64 rows of k), which for long k
-  // costs more than it saves: measured on the action-expert chain, k = 1024
-  // projections take 8-10 us instead of about 16 us (tiled kernel split along
-  // k plus its reduction), but the k = 4096 down projection 22 us instead of
-  // 16.  Offsets in x, a workgroup's weights and y stay below 2^31 (an
-  // offset of 2^31 reads zero).
-  return m >= 1 && m <= kNarrowMaxM && k <= kNarrowMaxK && (int64_t)m * k * 2 < 0x7fff0000LL &&
-         (int64_t)64 * (k / kQK) * 34 < 0x7fff0000LL && (int64_t)m * n * 4 < 0x7fff0000LL;
+bool narrow_fits(int64_t m, int64_t n, int64_t k, int splits) {
+  // Every workgroup reads all of x for its share of k (up to 64 rows), which
+  // for a long share costs more than it saves: measured on the action-expert
+  // chain, k = 1024 projections take 8-10 us instead of about 16 us (tiled
+  // kernel split along k plus its reduction), but an unsplit k = 4096 down
+  // projection 22 us instead of 16.  Offsets in x, a workgroup's weights and
+  // y stay below 2^31 (an offset of 2^31 reads zero).
+  return m >= 1 && m <= kNarrowMaxM && splits >= 1 && splits <= kNarrowMaxSplits &&
+         (splits == 1 || k / kQK >= (int64_t)splits * 8) && k / splits <= kNarrowMaxK &&
+         (int64_t)m * k * 2 < 0x7fff0000LL && (int64_t)64 * (k / kQK) * 34 < 0x7fff0000LL &&
+         (int64_t)m * n * 4 < 0x7fff0000LL;
+}
+
+// Splits of k for a lone small-m projection: when its 16-row workgroups do not
+// fill the GPU, k is split so that they do (about one workgroup per CU), each
+// split writing partial sums for the ordered reduction -- a narrow launch's
+// time follows the activation bytes each workgroup reads through its CU.
+int narrow_splits(int64_t n, int64_t k, int cus) {
+  static const int env = [] {
+    const char *e = std::getenv("EB_NARROW_SPLITS");
+    return e ? std::atoi(e) : 0;
+  }();
+  const int64_t wgs = (n + 15) / 16, nb = k / kQK;
+  int sp = env > 0 ? env : (int)std::max<int64_t>(1, cus / std::max<int64_t>(1, wgs));
+  sp = (int)std::min<int64_t>({(int64_t)sp, (int64_t)kNarrowMaxSplits, nb / 8});
+  if (k / std::max(sp, 1) > kNarrowMaxK)  // shares of at most kNarrowMaxK
+    sp = (int)std::min<int64_t>(kNarrowMaxSplits, (k + kNarrowMaxK - 1) / kNarrowMaxK);
+  return std::max(sp, 1);
 }
 
 hipError_t launch_mfma_narrow(int32_t type, const void *wdata, int64_t n, int64_t k, const void *x,
                               int32_t xt, bool hl, int64_t m, void *y, int32_t yt, const Fuse &f,
-                              hipStream_t s) {
-  if (!narrow_fits(m, n, k)) return hipErrorInvalidValue;
-  if (type == EB_Q4_0) return launch_x<EB_Q4_0>(xt, hl, wdata, n, k, x, m, y, yt, f, s);
-  return launch_x<EB_Q8_0>(xt, hl, wdata, n, k, x, m, y, yt, f, s);
+                              int splits, float *ws, int64_t ws_stride, hipStream_t s) {
+  if (!narrow_fits(m, n, k, splits) || (splits > 1 && !ws)) return hipErrorInvalidValue;
+  const Split sp{splits, splits > 1 ? ws : nullptr, ws_stride};
+  if (type == EB_Q4_0) return launch_x<EB_Q4_0>(xt, hl, wdata, n, k, x, m, y, yt, f, sp, s);
+  return launch_x<EB_Q8_0>(xt, hl, wdata, n, k, x, m, y, yt, f, sp, s);
 }
 
 }  // namespace eb

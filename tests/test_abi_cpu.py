@@ -291,9 +291,9 @@ def test_reduction_runs_next_prologue(eb, monkeypatch):
     """In a dependent layer chain the split-K reduction that writes the fp32
     stream h (O and down, + h) also normalises it for the next projection, so
     those prologues cost no row-kernel launch; EB_STACK_FUSE_NORM=0 keeps them.
-    At m <= 64 the projections with k <= 2048 are one launch of the narrow
-    kernel (whole k per workgroup, no reduction), so only the prologue after
-    a split down projection (k = 4096) is fused."""
+    At m <= 64 the projections run on the narrow kernel; those whose 16-row
+    workgroups would not fill the GPU (O and down: 1024 rows) split k and are
+    reduced, and those reductions normalise for the next projection."""
     d, f = 1024, 4096   # the action-expert layer shape
 
     def chain(m, stream16=False):
@@ -312,13 +312,14 @@ def test_reduction_runs_next_prologue(eb, monkeypatch):
                                             G if pro else None, res, 1e-5, 0))
         return (eb.eb_qlinear_op * len(ops))(*ops)
 
-    # m = 50: 6 narrow launches, 2 split down projections with their
-    # reductions and 4 prologue row kernels; fused, the second layer's first
-    # prologue runs in the first layer's down reduction
+    # m = 50: 8 narrow launches, 4 reductions (O and down split k: 64
+    # workgroups of 16 rows would leave most CUs idle) and 4 prologue row
+    # kernels; fused, every prologue after a split O or down runs in its
+    # reduction, leaving the first layer's QKV prologue
     monkeypatch.setenv("EB_STACK_FUSE_NORM", "0")
-    assert eb.lib.eb_qlinear_stack_launches(chain(50), 8) == 8 + 2 + 4
+    assert eb.lib.eb_qlinear_stack_launches(chain(50), 8) == 8 + 4 + 4
     monkeypatch.delenv("EB_STACK_FUSE_NORM")
-    assert eb.lib.eb_qlinear_stack_launches(chain(50), 8) == 8 + 2 + 3
+    assert eb.lib.eb_qlinear_stack_launches(chain(50), 8) == 8 + 4 + 1
     # m = 100: split projections; every prologue after a split O or down costs nothing
     monkeypatch.setenv("EB_STACK_FUSE_NORM", "0")
     unfused = eb.lib.eb_qlinear_stack_launches(chain(100), 8)
@@ -476,14 +477,15 @@ def test_library_imports_no_allocator(eb):
 
 
 def test_stack_counts_split_k_reduction(eb):
-    # a long-k op at m = 100 or 50 is split (product + ordered reduction); at
-    # m = 50 and k <= 2048 the narrow kernel takes the whole of k in one
-    # launch; a large prefill op fills the GPU unsplit
+    # a long-k op at m = 100 or 50 is split (product + ordered reduction);
+    # at m = 50 the narrow kernel takes the whole of k in one launch when its
+    # 16-row workgroups fill the GPU (n = 4096: 256 of them); a large prefill
+    # op fills the GPU unsplit
     for m in (100, 50):
         split = [_op(eb, 1 * GB, 8 * GB, 9 * GB, k=4096, n=1024, m=m, qtype=eb.EB_Q8_0,
                      xt=eb.EB_BF16)]
         assert _launches(eb, split) == 2, m
-    narrow = [_op(eb, 1 * GB, 8 * GB, 9 * GB, k=2048, n=1024, m=50, qtype=eb.EB_Q8_0,
+    narrow = [_op(eb, 1 * GB, 8 * GB, 9 * GB, k=2048, n=4096, m=50, qtype=eb.EB_Q8_0,
                   xt=eb.EB_BF16)]
     assert _launches(eb, narrow) == 1
     whole = [_op(eb, 1 * GB, 8 * GB, 9 * GB, k=3072, n=9216, m=4096, qtype=eb.EB_Q4_0,
@@ -504,8 +506,8 @@ def test_workspace_sizes(eb):
     normed = eb.eb_qlinear_op(_w(eb, k=4096, n=1024, data=1 * GB), 8 * GB, 9 * GB, 100, eb.EB_BF16,
                               eb.EB_F32, eb.EB_PRO_RMSNORM, 0, G, None, 1e-5, 0)
     assert q(ctypes.byref(normed), eb.EB_PATH_AUTO) == partial + 100 * 4096 * 2
-    # m <= 64, k <= 2048: the narrow kernel needs no partial sums
-    small = eb.eb_qlinear_op(_w(eb, k=2048, n=1024, data=1 * GB), 8 * GB, 9 * GB, 50, eb.EB_BF16,
+    # m <= 64, k <= 2048, n = 4096: the narrow kernel needs no partial sums
+    small = eb.eb_qlinear_op(_w(eb, k=2048, n=4096, data=1 * GB), 8 * GB, 9 * GB, 50, eb.EB_BF16,
                              eb.EB_F32)
     assert q(ctypes.byref(small), eb.EB_PATH_AUTO) == 0
     bad = eb.eb_qlinear_op(_w(eb, k=33), X, Y, 4, eb.EB_F16, eb.EB_F32)

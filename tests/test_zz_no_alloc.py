@@ -45,9 +45,10 @@ def _op(eb, qw, h, g, r, y, epi):
 def test_static_scratch_matches_workspace_entry(eb, qtype, epi):
     stream = torch.cuda.current_stream().cuda_stream
     # m = 100, k = 4096 -> n = 1024: split along k on the MFMA path (partial
-    # sums after the normalised activations); then m = 20, k = 1024 (one
-    # narrow launch: normalised activations only)
-    for i, (m, n, k) in enumerate(((100, 1024, 4096), (20, 512, 1024))):
+    # sums after the normalised activations); then m = 20, k = 1024 -> n =
+    # 4096 (one narrow launch whose workgroups fill the GPU: normalised
+    # activations only)
+    for i, (m, n, k) in enumerate(((100, 1024, 4096), (20, 4096, 1024))):
         print(f"[no-alloc] {qtype} {epi} call {i}: m={m} n={n} k={k}", flush=True)
         qw, h, g, r, n_out = _case(eb, 7000 + 10 * i, m, n, k, qtype, epi)
         y_ws = torch.full((m, n_out), float("nan"), device=DEV)
