@@ -388,7 +388,7 @@ bool env_off(const char *name) {
 }
 
 bool fusable(const eb_qlinear_op &o) {
-  return o.w.type != EB_Q6_S && o.m == 1 && gemv_fits(1, o.w.k) && m1_fusable(o.w.type, o.m, o.w.k, o.epilogue);
+  return o.m == 1 && gemv_fits(1, o.w.k) && m1_fusable(o.w.type, o.m, o.w.k, o.epilogue);
 }
 
 // MFMA ops that may join a fused launch.  The fused kernel addresses tiles of

@@ -110,9 +110,10 @@ struct M1Op {
   int64_t n;
   int64_t d_off;      // scale-plane offset
   int64_t ds;         // scale-plane row stride (elements)
-  int64_t unit_begin; // work units (16-byte code units) before this matrix
+  int64_t sc_off;     // Q6_S: sub-scale plane offset (unused otherwise)
+  int64_t unit_begin; // work units before this matrix
   int32_t k;
-  int32_t ku;         // 16-byte code units per row
+  int32_t ku;         // work units per row: 16-byte code units (Q6_S: 64-weight units)
   int32_t yt;
   int32_t pad;
   Fuse f;
@@ -179,6 +180,15 @@ hipError_t launch_mfma_narrow(int32_t type, const void *wdata, int64_t n, int64_
 // Q6_S weights, m <= 8 (gemv_q6.hip): a wave per pair of weight rows, lanes
 // over 32-weight chunks, fp32 products of the 6-bit codes and x staged in LDS.
 bool gemv_q6_fits(int64_t m, int64_t n, int64_t k);
+// m == 1 Q6_S kernel (k up to 16384) and its fused multi-matrix launch, the
+// counterparts of m1_slots / m1_fusable / m1_fill / launch_gemv_m1_multi
+int q6_m1_slots(int64_t k);
+bool q6_m1_fits(int64_t k);
+bool q6_m1_fusable(int64_t k, int32_t epi);
+int64_t q6_m1_fill(const void *wdata, int64_t n, int64_t k, const void *x, void *y, int32_t yt,
+                   const Fuse &f, int64_t unit_begin, M1Op *o);
+hipError_t launch_gemv_q6_multi(int32_t xt, int ns, const M1Op *dev_ops, int nops, int64_t units,
+                                int64_t rows, hipStream_t s);
 hipError_t launch_gemv_q6(const void *wdata, int64_t n, int64_t k, const void *x, int32_t xt,
                           int64_t m, void *y, int32_t yt, const Fuse &f, hipStream_t s);
 // Q6_S weights on the matrix cores, any m, one launch (mfma_q6.hip): 16

@@ -2,10 +2,29 @@
 // the bandwidth-bound decode case of the 6-bit configuration (paper section
 // 4, Table 3; section 3.2, latency-first batch-1 execution).
 //
-// A wave owns a pair of weight rows (so a gate/up pair's product is formed in
-// the wave) and its lanes walk the rows' 24-byte code chunks (32 weights
-// each) in lane order: one wave load covers 64 consecutive chunks of a row,
-// 1536 contiguous bytes, read as three 8-byte loads per lane.  A chunk
+// m == 1 (the decode step): a 64-weight unit is two consecutive 24-byte code
+// chunks, 48 bytes at offset 48 u of the row, the four sub-block scales of
+// those chunks (one 4-byte word) and their super-block's d16.  Lane l of a
+// wave owns units l, l + 64, ... of the wave's rows.  A wave reads the 3 KiB
+// of codes of 64 units with three fully coalesced 16-byte loads per lane (1
+// KiB contiguous per instruction; a lane's own 48 bytes, read directly, would
+// make each instruction touch 3 KiB in 16-byte pieces, which measured 25%
+// slower) and hands each lane its unit through a wave-private 3 KiB LDS
+// buffer.  The codes are decoded in
+// registers into binary16 pairs (low nibble and the two top bits placed into
+// the mantissa of 1024, or one nibble higher into 1024 + 16 u; one packed
+// subtraction leaves u - 32 or 16 (u - 32) exactly) and multiplied with
+// v_dot2_f32_f16 against x, staged once per workgroup into LDS in the
+// decoder's pair order; each 16-weight sub-block sum is then scaled by
+// e_j = d16 sc_j (exact in fp32).  bfloat16 x takes bfloat16 128 as the magic
+// value (128 + u = c + 160) and removes 160 * (sum of the sub-block's x),
+// precomputed in binary64 at staging.  One launch per matrix, or one
+// persistent launch for a run of independent matrices.
+//
+// m = 2 .. 8: a wave owns a pair of weight rows (so a gate/up pair's product
+// is formed in the wave) and its lanes walk the rows' 24-byte code chunks (32
+// weights each) in lane order: one wave load covers 64 consecutive chunks of a
+// row, 1536 contiguous bytes, read as three 8-byte loads per lane.  A chunk
 // decodes to u = low nibble | top bits << 4, and the lane accumulates
 // (u - 32) x in fp32 per 16-weight sub-block (every product exact: 6-bit code
 // times 16-bit activation), then e_j times that sum (e_j = d16 sc_j, exact in
@@ -16,6 +35,7 @@
 
 #include "eb_internal.h"
 #include "epilogue.h"
+#include "gemv_common.h"
 
 namespace eb {
 namespace {
@@ -172,6 +192,443 @@ __global__ void __launch_bounds__(kThreads)
   }
 }
 
+// ---------------------------------------------------------------------------
+// m == 1
+// ---------------------------------------------------------------------------
+
+constexpr int kU6 = 64;         // weights per unit (two code chunks)
+constexpr int kU6Bytes = 48;    // code bytes per unit
+constexpr int kU6Parts = 8;     // 16-byte x parts per unit (4 per chunk)
+constexpr int kQ6M1MaxSlots = 4;  // units per lane: k <= 64 * 64 * 4
+
+// Rows per wave of the fused launch by slot count (no spills at 4 waves per
+// SIMD); the one-matrix launch adds its rows in the same order, so both agree
+// bitwise (reduce_rows gives a row the same association for every R).
+__host__ __device__ constexpr int q6_multi_rows(int ns) { return ns <= 2 ? 2 : 1; }
+
+// Sub-block sums of one 32-weight chunk: sa over weights 0..15, sb over
+// 16..31.  L: the 16 low-nibble bytes (byte t: weight t in bits 0..3, weight
+// t + 16 in bits 4..7); H: the 8 top-bit bytes (byte t: top bits of weights
+// t, t + 8, t + 16, t + 24 at bit 0, 2, 4, 6).  Word i of L covers weights
+// 4i .. 4i + 3 and 4i + 16 .. 4i + 19, whose top bits sit in top-bit word
+// i & 1 at shift 2 (i >> 1) and 2 (i >> 1) + 4.  x part i holds the x pairs
+// (4i, 4i+2) (4i+1, 4i+3) (4i+16, 4i+18) (4i+17, 4i+19).
+template <int XT>
+__device__ inline void chunk_dot6(const uint32_t (&L)[4], uint32_t H0, uint32_t H1, const uint4 *xf,
+                                  float offa, float offb, float &sa, float &sb) {
+  float lo = 0.f, hi = 0.f;
+  if constexpr (XT == EB_F16) {
+    const uint32_t magic = vconst(0x64006400u);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t h = (i & 1) ? H1 : H0;
+      // top bits of the even / odd bytes' weights moved to bits 4..5 (and,
+      // for the weights 16 further on, 8..9) of the 16-bit lanes
+      const uint32_t te = (i < 2) ? h << 4 : h << 2, to = (i < 2) ? h >> 4 : h >> 6;
+      const uint32_t v = L[i], v8 = L[i] >> 8;
+      // 1024 + u - 1056 = u - 32;  1024 + 16 u - 1536 = 16 (u - 32)
+      lo = dot2h(sub_h2(and_or(te, 0x00300030u, and_or(v, 0x000F000Fu, magic)), (_Float16)1056.0f),
+                 xf[i].x, lo);
+      lo = dot2h(sub_h2(and_or(to, 0x00300030u, and_or(v8, 0x000F000Fu, magic)), (_Float16)1056.0f),
+                 xf[i].y, lo);
+      hi = dot2h(sub_h2(and_or(te, 0x03000300u, and_or(v, 0x00F000F0u, magic)), (_Float16)1536.0f),
+                 xf[i].z, hi);
+      hi = dot2h(sub_h2(and_or(to, 0x03000300u, and_or(v8, 0x00F000F0u, magic)), (_Float16)1536.0f),
+                 xf[i].w, hi);
+    }
+    (void)offa;
+    (void)offb;
+    sa = lo;
+    sb = hi * 0.0625f;  // exact
+  } else {
+    const uint32_t magic = vconst(0x43004300u);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t h = (i & 1) ? H1 : H0;
+      const int s = 2 * (i >> 1);
+      const uint32_t v = L[i];
+      // every code at bits 0..5: bfloat16 128 + u
+      lo = dot2bf(and_or(h << (4 - s), 0x00300030u, and_or(v, 0x000F000Fu, magic)), xf[i].x, lo);
+      lo = dot2bf(and_or(h >> (4 + s), 0x00300030u, and_or(v >> 8, 0x000F000Fu, magic)), xf[i].y, lo);
+      hi = dot2bf(and_or(h >> s, 0x00300030u, and_or(v >> 4, 0x000F000Fu, magic)), xf[i].z, hi);
+      hi = dot2bf(and_or(h >> (8 + s), 0x00300030u, and_or(v >> 12, 0x000F000Fu, magic)), xf[i].w, hi);
+    }
+    sa = lo - offa;
+    sb = hi - offb;
+  }
+}
+
+// Stage x (one row) into LDS for q6_rows: part p of unit u at xs[p * P + u]
+// (p = 4 h + i: chunk h of the unit, word i), and with bfloat16 x the four
+// sub-block offsets 160 * sum x of unit u at xoff[4 u .. 4 u + 3].  One thread
+// per part; with the normalisation prologue x is the fp32 stream h, each
+// thread's first two parts' h values stay in registers between the sum of
+// squares and the normalisation, and the sum is reduced over the wave by
+// exchanges and over the waves in order through `red` (one float per wave).
+template <int XT>
+__device__ __attribute__((always_inline)) inline void stage_x6(
+    const void *__restrict__ xv, int64_t k, int ku, uint4 *xs, float *xoff, int P, bool norm,
+    const float *__restrict__ gamma, float eps, float *red) {
+  const int nch = ku * kU6Parts, T = (int)blockDim.x, tid = (int)threadIdx.x;
+  auto first = [](int c, int &u, int &p, int &e0) __attribute__((always_inline)) {
+    u = c >> 3;
+    p = c & 7;
+    e0 = u * kU6 + (p >> 2) * 32 + 4 * (p & 3);  // e1 = e0 + 16
+  };
+  // pairs (a0,a2) (a1,a3) (b0,b2) (b1,b3), and the offsets' partial sums
+  auto put = [&](int c, int u, int p, const uint32_t (&ra)[2], const uint32_t (&rb)[2])
+      __attribute__((always_inline)) {
+    xs[p * P + u] = make_uint4((ra[0] & 0xffffu) | (ra[1] << 16), (ra[0] >> 16) | (ra[1] & 0xffff0000u),
+                               (rb[0] & 0xffffu) | (rb[1] << 16), (rb[0] >> 16) | (rb[1] & 0xffff0000u));
+    if constexpr (XT == EB_BF16) {
+      double sa = 0.0, sb = 0.0;
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        sa += x_to_f64<XT>(ra[j] & 0xffffu) + x_to_f64<XT>(ra[j] >> 16);
+        sb += x_to_f64<XT>(rb[j] & 0xffffu) + x_to_f64<XT>(rb[j] >> 16);
+      }
+      // the four parts of a chunk are four consecutive lanes
+      sa += __shfl_xor(sa, 1);
+      sb += __shfl_xor(sb, 1);
+      sa += __shfl_xor(sa, 2);
+      sb += __shfl_xor(sb, 2);
+      if ((c & 3) == 0) {
+        xoff[4 * u + 2 * (p >> 2)] = (float)(160.0 * sa);
+        xoff[4 * u + 2 * (p >> 2) + 1] = (float)(160.0 * sb);
+      }
+    }
+  };
+  if (!norm) {
+    const uint16_t *x = static_cast<const uint16_t *>(xv);
+    for (int c = tid; c < nch; c += T) {
+      int u, p, e0;
+      first(c, u, p, e0);
+      const uint2 a = *reinterpret_cast<const uint2 *>(x + e0);
+      const uint2 b = *reinterpret_cast<const uint2 *>(x + e0 + 16);
+      const uint32_t ra[2] = {a.x, a.y}, rb[2] = {b.x, b.y};
+      put(c, u, p, ra, rb);
+    }
+    return;
+  }
+  const float *h = static_cast<const float *>(xv);
+  float4 ha[2], hb[2];
+  float ss = 0.f;
+  auto sq = [](float acc, float4 v) __attribute__((always_inline)) {
+    acc = __builtin_fmaf(v.x, v.x, acc);
+    acc = __builtin_fmaf(v.y, v.y, acc);
+    acc = __builtin_fmaf(v.z, v.z, acc);
+    return __builtin_fmaf(v.w, v.w, acc);
+  };
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int c = tid + j * T;
+    if (c < nch) {
+      int u, p, e0;
+      first(c, u, p, e0);
+      ha[j] = *reinterpret_cast<const float4 *>(h + e0);
+      hb[j] = *reinterpret_cast<const float4 *>(h + e0 + 16);
+      ss = sq(sq(ss, ha[j]), hb[j]);
+    }
+  }
+  for (int c = tid + 2 * T; c < nch; c += T) {
+    int u, p, e0;
+    first(c, u, p, e0);
+    ss = sq(sq(ss, *reinterpret_cast<const float4 *>(h + e0)), *reinterpret_cast<const float4 *>(h + e0 + 16));
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) ss += __shfl_xor(ss, o);
+  if ((tid & 63) == 0) red[tid >> 6] = ss;
+  __syncthreads();
+  float tot = 0.f;
+  for (int w = 0; w < (T >> 6); ++w) tot += red[w];
+  const float r = 1.0f / __builtin_sqrtf(tot / (float)k + eps);
+  auto normed = [&](float4 v, const float *g, uint32_t (&o)[2]) __attribute__((always_inline)) {
+    const float4 gg = *reinterpret_cast<const float4 *>(g);
+    o[0] = pack_x16<XT>(v.x * gg.x * r, v.y * gg.y * r);
+    o[1] = pack_x16<XT>(v.z * gg.z * r, v.w * gg.w * r);
+  };
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int c = tid + j * T;
+    if (c < nch) {
+      int u, p, e0;
+      first(c, u, p, e0);
+      uint32_t ra[2], rb[2];
+      normed(ha[j], gamma + e0, ra);
+      normed(hb[j], gamma + e0 + 16, rb);
+      put(c, u, p, ra, rb);
+    }
+  }
+  for (int c = tid + 2 * T; c < nch; c += T) {
+    int u, p, e0;
+    first(c, u, p, e0);
+    uint32_t ra[2], rb[2];
+    normed(*reinterpret_cast<const float4 *>(h + e0), gamma + e0, ra);
+    normed(*reinterpret_cast<const float4 *>(h + e0 + 16), gamma + e0 + 16, rb);
+    put(c, u, p, ra, rb);
+  }
+}
+
+// LDS of q6_rows: 8 x part rows of P entries, the bfloat16 offsets (4 P
+// floats), a 3 KiB code buffer per wave and one float per wave for the
+// normalisation's reduction.
+constexpr int kU6WaveBuf = 64 * kU6Bytes / 16;  // uint4 entries per wave
+__host__ __device__ constexpr size_t q6_m1_lds(int ns, int waves) {
+  return (size_t)kU6Parts * (64 * ns + 1) * 16 + (size_t)4 * (64 * ns + 1) * 4 +
+         (size_t)waves * kU6WaveBuf * 16 + (size_t)waves * 4;
+}
+
+// Rows g*R .. g*R+R-1 for groups g = g0, g0 + gstride, ... < g_end of one
+// matrix, m == 1.  Called by every thread of the workgroup (it stages x into
+// LDS and synchronises once); waves whose first group is past g_end only help
+// with the staging.  PD register sets of weights: the group being computed
+// and the next PD - 1, whose loads are in flight meanwhile.
+template <int XT, int NS, int R, int PD>
+__device__ __attribute__((always_inline)) inline void q6_rows(
+    const uint8_t *__restrict__ wdata, int64_t n, int64_t k, int64_t sc_off, int64_t d_off,
+    int64_t ds, const void *__restrict__ x, void *__restrict__ y, int yt, const Fuse &f, int64_t g,
+    int64_t g_end, int64_t gstride, uint4 *smem) {
+  // entry 64 * NS of every part row (and its offsets) is zero and stands in
+  // for units past the end of the row
+  constexpr int P = 64 * NS + 1;
+  const int ku = (int)(k / kU6);  // 64 * (NS - 1) < ku <= 64 * NS
+  uint4 *xs = smem;
+  float *xoff = reinterpret_cast<float *>(smem + kU6Parts * P);
+  uint4 *cbuf = reinterpret_cast<uint4 *>(xoff + 4 * P);  // [waves][192]
+  float *red = reinterpret_cast<float *>(cbuf + (blockDim.x >> 6) * kU6WaveBuf);
+  const int lane = threadIdx.x & 63;
+  uint4 *wbuf = cbuf + (threadIdx.x >> 6) * kU6WaveBuf;
+  const uint32_t q_row = (uint32_t)ku * kU6Bytes, s_row = (uint32_t)(k / 16), d_row = (uint32_t)(ds * 2);
+  const uint8_t *__restrict__ sbase = wdata + sc_off;
+  const uint8_t *__restrict__ dbase = wdata + d_off;
+
+  // per-lane byte offsets inside a row: the lane's 16-byte pieces of slot s's
+  // 3 KiB of codes (loads past the row's end return zeros), and its unit's
+  // scales; units past the end of the row (last slot only) read the row's
+  // last unit's scales and meet zero x
+  uint32_t qoff[NS], soff[NS], doff[NS], xidx[NS];
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+    const int u = lane + 64 * s;
+    const int uc = min(u, ku - 1);
+    qoff[s] = (uint32_t)(64 * s * kU6Bytes + 16 * lane);
+    soff[s] = (uint32_t)uc * 4u;
+    doff[s] = (uint32_t)(uc >> 2) * 2u;
+    xidx[s] = u < ku ? (uint32_t)u : 64u * NS;
+  }
+
+  static_assert(PD >= 1 && PD <= 2, "1 or 2 weight register sets");
+  struct WSet {
+    uint4 a[NS][R], b[NS][R], c[NS][R];
+    uint32_t sc[NS][R];
+    uint16_t dh[NS][R];
+  };
+  WSet A, B;
+  auto load_group = [&](WSet &S, int64_t grp) __attribute__((always_inline)) {
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      int64_t row = grp * R + r;
+      row = row < n ? row : n - 1;  // tail rows are computed but not stored
+      const auto rq = rsrc(wdata + row * q_row, q_row);
+      const auto rs = rsrc(sbase + row * s_row, s_row);
+      const auto rd = rsrc(dbase + row * d_row, d_row);
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+        const auto va = __builtin_amdgcn_raw_buffer_load_b128(rq, (int)qoff[s], 0, kNT);
+        const auto vb = __builtin_amdgcn_raw_buffer_load_b128(rq, (int)qoff[s] + 1024, 0, kNT);
+        const auto vc = __builtin_amdgcn_raw_buffer_load_b128(rq, (int)qoff[s] + 2048, 0, kNT);
+        S.a[s][r] = make_uint4(va[0], va[1], va[2], va[3]);
+        S.b[s][r] = make_uint4(vb[0], vb[1], vb[2], vb[3]);
+        S.c[s][r] = make_uint4(vc[0], vc[1], vc[2], vc[3]);
+        S.sc[s][r] = __builtin_amdgcn_raw_buffer_load_b32(rs, (int)soff[s], 0, kNT);
+        S.dh[s][r] = __builtin_amdgcn_raw_buffer_load_b16(rd, (int)doff[s], 0, kNT);
+      }
+    }
+  };
+  if (g < g_end) load_group(A, g);
+  if (PD >= 2 && g + gstride < g_end) load_group(B, g + gstride);
+  stage_x6<XT>(x, k, ku, xs, xoff, P, f.pro == EB_PRO_RMSNORM, f.gamma, f.eps, red);
+  if (threadIdx.x < kU6Parts) xs[threadIdx.x * P + 64 * NS] = make_uint4(0, 0, 0, 0);
+  if (threadIdx.x < 4) xoff[4 * 64 * NS + threadIdx.x] = 0.f;
+  __syncthreads();
+
+  auto step = [&](WSet &S) __attribute__((always_inline)) -> bool {
+    if (g >= g_end) return false;
+    float acc[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) acc[r] = 0.f;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      uint4 xf[kU6Parts];
+#pragma unroll
+      for (int p = 0; p < kU6Parts; ++p) xf[p] = xs[p * P + xidx[s]];
+      float4 xo = make_float4(0.f, 0.f, 0.f, 0.f);
+      if constexpr (XT == EB_BF16) xo = reinterpret_cast<const float4 *>(xoff)[xidx[s]];
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        const float d = (float)__builtin_bit_cast(_Float16, S.dh[s][r]);
+        const uint32_t sc = S.sc[s][r];
+        // pieces l, l + 64, l + 128 of the wave's 3 KiB in, the lane's own
+        // unit (pieces 3 l .. 3 l + 2) out; a wave's LDS operations complete
+        // in order, so the reads see the writes and the next writes follow
+        // the reads
+        wbuf[lane] = S.a[s][r];
+        wbuf[lane + 64] = S.b[s][r];
+        wbuf[lane + 128] = S.c[s][r];
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        const uint4 qa = wbuf[3 * lane], qb = wbuf[3 * lane + 1], qc = wbuf[3 * lane + 2];
+        __builtin_amdgcn_wave_barrier();
+        const uint32_t L0[4] = {qa.x, qa.y, qa.z, qa.w}, L1[4] = {qb.z, qb.w, qc.x, qc.y};
+        float s0, s1, s2, s3;
+        chunk_dot6<XT>(L0, qb.x, qb.y, xf, xo.x, xo.y, s0, s1);
+        chunk_dot6<XT>(L1, qc.z, qc.w, xf + 4, xo.z, xo.w, s2, s3);
+        // e_j = d16 sc_j: a 11-bit by 8-bit product, exact in fp32
+        acc[r] = __builtin_fmaf(d * (float)(int8_t)(sc & 0xffu), s0, acc[r]);
+        acc[r] = __builtin_fmaf(d * (float)(int8_t)((sc >> 8) & 0xffu), s1, acc[r]);
+        acc[r] = __builtin_fmaf(d * (float)(int8_t)((sc >> 16) & 0xffu), s2, acc[r]);
+        acc[r] = __builtin_fmaf(d * (float)(int8_t)(sc >> 24), s3, acc[r]);
+      }
+    }
+    int rr;
+    bool writer;
+    const float tot = reduce_rows<R>(acc, lane, rr, writer);
+    const int64_t row = g * R + rr;
+    if constexpr (R >= 2) {
+      if (f.epi == EB_EPI_GLU) {
+        // the up row (odd) of a pair is held R/2 ... lanes away, see reduce_rows
+        const float up = __shfl_xor(tot, R == 8 ? 8 : (R == 4 ? 16 : 32));
+        if (writer && (rr & 1) == 0 && row < n) store_y(y, row / 2, silu_mul(tot, up), yt);
+      } else if (writer && row < n) {
+        put_y(y, row, tot, yt, f);
+      }
+    } else {
+      if (writer && row < n) put_y(y, row, tot, yt, f);
+    }
+    g += gstride;
+    __builtin_amdgcn_sched_barrier(0);
+    if (g + (PD - 1) * gstride < g_end) load_group(S, g + (PD - 1) * gstride);
+    return true;
+  };
+  if constexpr (PD == 2) {
+    while (step(A) && step(B)) {
+    }
+  } else {
+    while (step(A)) {
+    }
+  }
+}
+
+// One matrix per launch: one workgroup per CU (x is staged, and normalised,
+// once per CU) of 16 waves, or 8 where a wave's weights and x parts would not
+// fit the registers of four waves per SIMD without spilling (measured: up to
+// 3 slots, 4 slot-rows).
+__host__ __device__ constexpr int q6_m1_waves(int ns, int r) { return ns <= 3 && ns * r <= 4 ? 16 : 8; }
+
+template <int XT, int NS, int R, int WG>
+__global__ void __launch_bounds__(64 * WG) __attribute__((amdgpu_waves_per_eu(WG / 4)))
+    gemv_q6_m1_kernel(const uint8_t *__restrict__ wdata, int64_t n, int64_t k, int64_t sc_off,
+                      int64_t d_off, int64_t ds, const void *__restrict__ x, void *__restrict__ y,
+                      int yt, Fuse f) {
+  extern __shared__ uint4 smem[];
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  // a second register set of weights in flight where it fits
+  constexpr int PD = NS == 1 ? 2 : 1;
+  q6_rows<XT, NS, R, PD>(wdata, n, k, sc_off, d_off, ds, x, y, yt, f, (int64_t)blockIdx.x * WG + wave,
+                         (n + R - 1) / R, (int64_t)gridDim.x * WG, smem);
+}
+
+// Several independent matrices (m == 1, same activation type, same slot count
+// NS) in one persistent launch: the launch's units (rows weighted by their
+// length) are cut into gridDim.x equal shares, each converted to whole R-row
+// groups of the matrices it covers (neighbours round a shared boundary the
+// same way, so every row is computed once).
+constexpr int kQ6MultiWaves = 4;
+
+template <int XT, int NS>
+__global__ void __launch_bounds__(64 * kQ6MultiWaves) __attribute__((amdgpu_waves_per_eu(NS <= 1 ? 4 : 3)))
+    gemv_q6_m1_multi_kernel(const M1Op *__restrict__ ops, int nops, int64_t units) {
+  constexpr int R = q6_multi_rows(NS);
+  extern __shared__ uint4 smem[];
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int64_t G = gridDim.x;
+  const int64_t u0 = units * (int64_t)blockIdx.x / G, u1 = units * ((int64_t)blockIdx.x + 1) / G;
+  int lo = 0, hi = nops - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) / 2;
+    if (ops[mid].unit_begin <= u0) lo = mid; else hi = mid - 1;
+  }
+  for (int op = lo; op < nops && ops[op].unit_begin < u1; ++op) {
+    const M1Op o = ops[op];
+    auto row_at = [&](int64_t u) {
+      int64_t r = (u - o.unit_begin) / o.ku;
+      r = r < 0 ? 0 : (r > o.n ? o.n : r);
+      return r == o.n ? r : r / R * R;
+    };
+    const int64_t r0 = row_at(u0), r1 = row_at(u1);
+    if (r0 >= r1) continue;  // uniform across the workgroup
+    q6_rows<XT, NS, R, 1>(o.w, o.n, o.k, o.sc_off, o.d_off, o.ds, o.x, o.y, o.yt, o.f, r0 / R + wave,
+                          (r1 + R - 1) / R, kQ6MultiWaves, smem);
+    __syncthreads();  // the next matrix restages LDS
+  }
+}
+
+template <int XT, int NS>
+hipError_t launch_m1_ns(const void *wdata, int64_t n, int64_t k, const void *x, void *y, int32_t yt,
+                        const Fuse &f, hipStream_t s) {
+  const Layout L = layout_of(EB_Q6_S, n, k);
+  const int r = f.epi == EB_EPI_GLU ? 2 : 1;  // the gate/up product needs both rows in one wave
+  const int wg = r == 2 ? q6_m1_waves(NS, 2) : q6_m1_waves(NS, 1);
+  const int64_t groups = (n + r - 1) / r;
+  int64_t grid = (groups + wg - 1) / wg;
+  const int64_t cap = (int64_t)device_cu_count();
+  if (grid > cap) grid = cap;
+  const size_t lds = q6_m1_lds(NS, wg);
+  auto kern = r == 2 ? gemv_q6_m1_kernel<XT, NS, 2, q6_m1_waves(NS, 2)>
+                     : gemv_q6_m1_kernel<XT, NS, 1, q6_m1_waves(NS, 1)>;
+  if (lds > 64 * 1024) {
+    hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  kern<<<(unsigned)grid, 64 * wg, lds, s>>>((const uint8_t *)wdata, n, k, L.sc_off, L.d_off, L.ds, x,
+                                           y, yt, f);
+  return hipGetLastError();
+}
+
+template <int XT>
+hipError_t launch_m1(const void *wdata, int64_t n, int64_t k, const void *x, void *y, int32_t yt,
+                     const Fuse &f, hipStream_t s) {
+  switch (q6_m1_slots(k)) {
+    case 1: return launch_m1_ns<XT, 1>(wdata, n, k, x, y, yt, f, s);
+    case 2: return launch_m1_ns<XT, 2>(wdata, n, k, x, y, yt, f, s);
+    case 3: return launch_m1_ns<XT, 3>(wdata, n, k, x, y, yt, f, s);
+    default: return launch_m1_ns<XT, 4>(wdata, n, k, x, y, yt, f, s);
+  }
+}
+
+template <int XT, int NS>
+hipError_t launch_multi_t(const M1Op *ops, int nops, int64_t units, int64_t rows, hipStream_t s) {
+  int64_t grid = (int64_t)device_cu_count() * 4;
+  const int64_t groups = rows / (kQ6MultiWaves * q6_multi_rows(NS));  // keep every wave busy
+  if (grid > groups) grid = groups > 0 ? groups : 1;
+  gemv_q6_m1_multi_kernel<XT, NS><<<(unsigned)grid, 64 * kQ6MultiWaves, q6_m1_lds(NS, kQ6MultiWaves), s>>>(
+      ops, nops, units);
+  return hipGetLastError();
+}
+
+template <int XT>
+hipError_t launch_multi(const M1Op *ops, int nops, int64_t units, int64_t rows, int ns, hipStream_t s) {
+  switch (ns) {
+    case 1: return launch_multi_t<XT, 1>(ops, nops, units, rows, s);
+    case 2: return launch_multi_t<XT, 2>(ops, nops, units, rows, s);
+    case 3: return launch_multi_t<XT, 3>(ops, nops, units, rows, s);
+    case 4: return launch_multi_t<XT, 4>(ops, nops, units, rows, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
 template <int MT>
 hipError_t launch_mt(const void *wdata, int64_t n, int64_t k, const void *x, int32_t xt, int64_t m,
                      void *y, int32_t yt, const Fuse &f, hipStream_t s) {
@@ -192,6 +649,38 @@ hipError_t launch_mt(const void *wdata, int64_t n, int64_t k, const void *x, int
 
 }  // namespace
 
+int q6_m1_slots(int64_t k) { return (int)((k / kU6 + 63) / 64); }
+
+bool q6_m1_fits(int64_t k) { return k > 0 && k % kQK6 == 0 && q6_m1_slots(k) <= kQ6M1MaxSlots; }
+
+bool q6_m1_fusable(int64_t k, int32_t epi) {
+  return q6_m1_fits(k) && (epi != EB_EPI_GLU || q6_multi_rows(q6_m1_slots(k)) >= 2);
+}
+
+int64_t q6_m1_fill(const void *wdata, int64_t n, int64_t k, const void *x, void *y, int32_t yt,
+                   const Fuse &f, int64_t unit_begin, M1Op *o) {
+  const Layout L = layout_of(EB_Q6_S, n, k);
+  o->w = (const uint8_t *)wdata;
+  o->x = x;
+  o->y = y;
+  o->f = f;
+  o->n = n;
+  o->d_off = L.d_off;
+  o->ds = L.ds;
+  o->sc_off = L.sc_off;
+  o->unit_begin = unit_begin;
+  o->k = (int32_t)k;
+  o->ku = (int32_t)(k / kU6);
+  o->yt = yt;
+  return n * (k / kU6);
+}
+
+hipError_t launch_gemv_q6_multi(int32_t xt, int ns, const M1Op *dev_ops, int nops, int64_t units,
+                                int64_t rows, hipStream_t s) {
+  if (xt == EB_F16) return launch_multi<EB_F16>(dev_ops, nops, units, rows, ns, s);
+  return launch_multi<EB_BF16>(dev_ops, nops, units, rows, ns, s);
+}
+
 bool gemv_q6_fits(int64_t m, int64_t n, int64_t k) {
   const int64_t mt = m <= 1 ? 1 : (m <= 2 ? 2 : (m <= 4 ? 4 : 8));
   return m >= 1 && m <= kGemvMaxM && mt * k <= kGemvMaxMK && k % kQK6 == 0 &&
@@ -201,6 +690,10 @@ bool gemv_q6_fits(int64_t m, int64_t n, int64_t k) {
 hipError_t launch_gemv_q6(const void *wdata, int64_t n, int64_t k, const void *x, int32_t xt,
                           int64_t m, void *y, int32_t yt, const Fuse &f, hipStream_t s) {
   if (!gemv_q6_fits(m, n, k)) return hipErrorInvalidValue;
+  if (m == 1 && q6_m1_fits(k)) {
+    if (xt == EB_F16) return launch_m1<EB_F16>(wdata, n, k, x, y, yt, f, s);
+    return launch_m1<EB_BF16>(wdata, n, k, x, y, yt, f, s);
+  }
   if (m <= 1) return launch_mt<1>(wdata, n, k, x, xt, m, y, yt, f, s);
   if (m <= 2) return launch_mt<2>(wdata, n, k, x, xt, m, y, yt, f, s);
   if (m <= 4) return launch_mt<4>(wdata, n, k, x, xt, m, y, yt, f, s);

@@ -112,10 +112,17 @@ def test_q6_validation(eb):
     normed = eb.eb_qlinear_op(_w(eb, eb.EB_Q6_S, n=1024, k=4096, data=1 * GB), 8 * GB, 9 * GB, 50,
                               eb.EB_BF16, eb.EB_F32, eb.EB_PRO_RMSNORM, 0, G, None, 1e-5, 0)
     assert L.eb_qlinear_workspace_bytes(ctypes.byref(normed), eb.EB_PATH_AUTO) == 50 * 4096 * 2
-    # in a stack every Q6_S op is a launch of its own (plus its prologue's row kernel)
-    ops = [_op(eb, 1 * GB + i * (64 << 20), 8 * GB + i * (1 << 20), 9 * GB + i * (1 << 20),
-               k=1024, n=2048, m=1, qtype=eb.EB_Q6_S, xt=eb.EB_F16) for i in range(4)]
-    assert _launches(eb, ops) == 4
+    # in a stack independent m == 1 Q6_S ops share one fused GEMV launch (k up
+    # to 16384); with more rows, or longer rows, every op is a launch of its own
+    def q6ops(m, k):
+        return [_op(eb, 1 * GB + i * (64 << 20), 8 * GB + i * (1 << 20), 9 * GB + i * (1 << 20),
+                    k=k, n=2048, m=m, qtype=eb.EB_Q6_S, xt=eb.EB_F16) for i in range(4)]
+    assert _launches(eb, q6ops(1, 1024)) == 1
+    assert _launches(eb, q6ops(1, 16384)) == 1
+    assert _launches(eb, q6ops(2, 1024)) == 4
+    assert _launches(eb, q6ops(1, 16640)) == 4
+    # one fused launch per slot count (64-weight units per lane: k = 4096 -> 1, 11008 -> 3)
+    assert _launches(eb, q6ops(1, 4096)[:2] + q6ops(1, 11008)[2:]) == 2
 
 
 def test_bytes_rejects_bad_sizes(eb):

@@ -186,3 +186,72 @@ def test_q6_stack_matches_single_calls(eb, monkeypatch):
         run(h, qkv, act, True)
         assert torch.equal(qkv, ref_qkv) and torch.equal(act, ref_act) and torch.equal(h, ref_h), mode
     eb.stack_cache_clear()
+
+
+# m == 1: units of 64 weights, one per lane per slot; k from one slot to four,
+# each with a ragged last slot (units past the row's end meet zero x) and full
+M1_KS = [256, 4096, 4352, 8192, 11008, 12544, 16384]
+
+
+@pytest.mark.parametrize("xdtype", [torch.float16, torch.bfloat16])
+@pytest.mark.parametrize("k", M1_KS)
+def test_q6_m1_every_slot_count(eb, oracle, xdtype, k):
+    n = 77
+    w = W.normal((n, k), 1300 + k, "cpu", W.WEIGHT_STD)
+    qw = eb.quantize(w.to(DEV), "q6_s")
+    for kind, x in (("normal", W.normal((1, k), 1301 + k, "cpu")),
+                    ("outlier", W.outlier_rows(1, k, 1302 + k)),
+                    ("onehot", W.onehot_rows(1, k, 1303 + k))):
+        x = x.to(xdtype)
+        _, y_ref, bound = oracle_reference(oracle, "q6_s", w.numpy(), x)
+        y = eb.qlinear(qw, x.to(DEV))
+        assert_parity(y, y_ref, bound, TOL_F32, f"q6 m=1 k={k} {kind}")
+
+
+@pytest.mark.parametrize("pro,epi", FUSIONS)
+@pytest.mark.parametrize("k", [4352, 11008])
+def test_q6_m1_fused_steps_long_rows(eb, oracle, pro, epi, k):
+    """The fused steps at two and three slots per lane (the gate/up product
+    takes two rows per wave, which at three slots runs 8-wave workgroups)."""
+    for xdtype, ydtype in ((torch.float16, torch.float32), (torch.bfloat16, torch.bfloat16)):
+        c = Case(eb, 1400 + k, "q6_s", 130, k, 1, xdtype, pro, epi, ydtype)
+        y = c.run(eb)
+        torch.cuda.synchronize()
+        y_ref, scale = c.reference(oracle)
+        assert_fused(y, y_ref, scale, f"q6_m1_{pro}_{epi} k={k} {xdtype}")
+
+
+@pytest.mark.parametrize("xdtype", [torch.float16, torch.bfloat16])
+def test_q6_m1_fused_launch_matches_single_calls(eb, oracle, xdtype, monkeypatch):
+    """Independent m == 1 projections of several slot counts (k = 1024, 4096,
+    4352, 11008) with every fused step share fused launches in a stack:
+    bitwise equal to single calls, and each within the oracle's bar."""
+    shapes = [(3 * 512, 4096, "rmsnorm", None), (4096, 4096, None, "add"), (2 * 600, 4352, "rmsnorm", "glu"),
+              (4096, 11008, None, "add"), (1030, 1024, None, None), (96, 11008, "rmsnorm", None)]
+    cases = [Case(eb, 1500 + i, "q6_s", n, k, 1, xdtype, pro, epi, torch.float32)
+             for i, (n, k, pro, epi) in enumerate(shapes)]
+    singles = [c.run(eb) for c in cases]
+    torch.cuda.synchronize()
+    for c, y in zip(cases, singles):
+        y_ref, scale = c.reference(oracle)
+        assert_fused(y, y_ref, scale, f"q6_m1 fused {c.n}x{c.k} {c.pro} {c.epi}")
+    outs = [torch.empty_like(y) for y in singles]
+    specs = []
+    for c, o in zip(cases, outs):
+        kw = dict(x_dtype=c.xdtype, epilogue=c.epi)
+        if c.pro:
+            kw.update(prologue="rmsnorm", norm_weight=c.gd, eps=1e-5)
+        if c.epi == "add":
+            kw.update(residual=c.rd)
+        specs.append((c.qw, c.xd, o, kw))
+    ops = eb.make_ops(specs)
+    assert eb.stack_launches(ops) == 3   # slot counts 1, 2 and 3
+    for mode in ("1", "1", "0"):
+        monkeypatch.setenv("EB_STACK_GRAPH", mode)
+        for o in outs:
+            o.fill_(float("nan"))
+        eb.qlinear_stack(ops)
+        torch.cuda.synchronize()
+        for y, o in zip(singles, outs):
+            assert torch.equal(y, o), mode
+    eb.stack_cache_clear()
