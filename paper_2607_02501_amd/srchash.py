@@ -7,7 +7,7 @@ _CSRC = os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc")
 _COMMON = ("epilogue.h", "eb_internal.h", "eb_api.cpp")
 _FILES = {
     # GEMV kernels (m <= 8)
-    "gemv": ("gemv.hip",) + _COMMON,
+    "gemv": ("gemv.hip", "gemv_common.h") + _COMMON,
     # tile kernel of the MFMA path (single ops, split-K, grouped launches)
     "mfma": ("mfma.hip", "mfma_tile.h", "mfma_narrow.hip", "mfma_q8_0_bf16.hip", "mfma_q8_0_f16.hip",
              "mfma_q4_0_bf16.hip", "mfma_q4_0_f16.hip", "mfma_common.h", "norm.hip") + _COMMON,
@@ -15,7 +15,7 @@ _FILES = {
     "mm": ("mfma_lds2.hip", "mfma_multi.hip", "mfma_common.h", "mm_common.h", "norm.hip") + _COMMON,
     # the Q6_S kernel (every m)
     "q6": ("mfma_q6.hip", "mfma_common.h", "norm.hip") + _COMMON,
-    "gemv_q6": ("gemv_q6.hip",) + _COMMON,
+    "gemv_q6": ("gemv_q6.hip", "gemv_common.h") + _COMMON,
     "i8": ("mfma_i8.hip", "mfma_common.h") + _COMMON,
 }
 
