@@ -13,6 +13,7 @@ paper_2607_02501_amd/workloads.py):
   q4_0_decode_7b            batch-1 decode through a 32-layer 7B-class Q4_0 stack
   q6_s_decode_7b            the same decode stack in the 6-bit Q6_S format
   q8_0_vlm_prefill_816      VLM-backbone prefill, m = 816, 18 layers of d = 2048
+  q6_s_vlm_prefill_816      the same prefill in the 6-bit Q6_S format
   q8_0_action_expert_50x10  action-expert denoising, m = 50, 18 layers x 10 steps
   q4_0_video_wam_4096       video world-action backbone, m = 4096, 28 layers of d = 3072
 
@@ -65,7 +66,7 @@ ALL_CONFIGS = [("q8_0_m1_2048", False), ("q4_0_video_wam_4096", False),
                ("q8_0_vlm_prefill_816", False), ("q8_0_vlm_prefill_816", True),
                ("q8_0_action_expert_50x10", False), ("q8_0_action_expert_50x10", True),
                ("q4_0_decode_7b", False), ("q4_0_decode_7b", True),
-               ("q6_s_decode_7b", False), ("q6_s_decode_7b", True)]
+               ("q6_s_decode_7b", False), ("q6_s_decode_7b", True), ("q6_s_vlm_prefill_816", False)]
 HEADLINE = ("q4_0_decode_7b", True)
 
 

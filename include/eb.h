@@ -215,11 +215,13 @@ eb_status eb_quantize_q8_0(const float *w, int64_t n, int64_t k, void *out, hipS
 eb_status eb_quantize_q4_0(const float *w, int64_t n, int64_t k, void *out, hipStream_t stream);
 
 /* Same as eb_quantize_q8_0 for the Q6_S format (k % 256 == 0, else
- * EB_ERR_INVALID).  Q6_S ops have a GEMV of their own (m <= 8, fp32 products
- * of the codes; EB_PATH_AUTO takes it up to m = 4) and one matrix-core kernel
- * for every m (16 weight rows and up to 64 rows of x per workgroup, the whole
- * of k; bfloat16 activations take w_hat as hi/lo pairs, binary16 ones round
- * it once), both within the 2e-3 bound; they never join a fused stack launch. */
+ * EB_ERR_INVALID).  Q6_S ops have GEMVs of their own (m <= 8; EB_PATH_AUTO
+ * takes them up to m = 4; independent m == 1 ops share fused stack launches),
+ * a matrix-core kernel of their own up to m = 128 (16 weight rows and up to 64
+ * rows of x per workgroup, the whole of k; bfloat16 activations take w_hat as
+ * hi/lo pairs, binary16 ones round it once), and the tile kernel of the other
+ * formats beyond (k may be split); the accuracy of each path is as stated for
+ * eb_qlinear.  They never join fused or grouped matrix-core stack launches. */
 eb_status eb_quantize_q6_s(const float *w, int64_t n, int64_t k, void *out, hipStream_t stream);
 
 /* Write the canonical array-of-blocks bytes of *w into `dst` (device,

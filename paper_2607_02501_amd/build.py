@@ -23,7 +23,7 @@ LIB = os.path.join(PKG, "libeb.so")
 
 ARCH = "gfx950"
 SOURCES = ["eb_api.cpp", "eb_multirate.cpp", "quantize.hip", "gemv.hip", "norm.hip", "mfma.hip", "mfma_q8_0_bf16.hip",
-           "mfma_q8_0_f16.hip", "mfma_q4_0_bf16.hip", "mfma_q4_0_f16.hip", "mfma_multi.hip",
+           "mfma_q8_0_f16.hip", "mfma_q4_0_bf16.hip", "mfma_q4_0_f16.hip", "mfma_q6_s_bf16.hip", "mfma_q6_s_f16.hip", "mfma_multi.hip",
            "mfma_lds2.hip", "mfma_narrow.hip", "mfma_q6.hip", "gemv_q6.hip", "mfma_i8.hip"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-I", INCLUDE, "-I", CSRC,
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

@@ -404,9 +404,10 @@ int64_t mm_max_m() {
 }
 
 // MFMA ops with more rows than a fused small-m launch takes, which may share a
-// grouped launch (EB_STACK_GROUP=0 turns that off).
+// grouped launch (EB_STACK_GROUP=0 turns that off); Q6_S ops only where they
+// take the tile kernel (m > 128).
 bool gm_fusable(const eb_qlinear_op &o) {
-  return o.w.type != EB_Q6_S && o.m > mm_max_m() && !env_off("EB_STACK_GROUP") &&
+  return (o.w.type != EB_Q6_S || o.m > 128) && o.m > mm_max_m() && !env_off("EB_STACK_GROUP") &&
          pick_path(o.w.type, o.x_type, o.m, o.w.n, o.w.k) == EB_PATH_MFMA;
 }
 
@@ -500,6 +501,7 @@ eb_status build_plan(const eb_qlinear_op *ops, int32_t n_ops, uint8_t *wsbase, P
       e.k = o.w.k;
       e.d_off = L.d_off;
       e.ds = L.ds;
+      e.sc_off = L.sc_off;
       e.m = o.m;
       e.yt = o.y_type;
       e.pad = o.reserved == kRelX;

@@ -220,6 +220,7 @@ struct GOp {
   const uint16_t *x;  // activations [m][k]
   void *y;            // outputs [m][n]
   int64_t n, k, d_off, ds, m;
+  int64_t sc_off;     // Q6_S sub-scale plane (not grouped; 0 otherwise)
   int32_t yt, pad;
   Fuse f;
 };

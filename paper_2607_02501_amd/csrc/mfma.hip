@@ -25,7 +25,7 @@ bool mfma_fits_offsets(int32_t type, int64_t n, int64_t k, int bm, int bn) {
   const int64_t qsb = qs_bytes_per_block(type);
   const int64_t lim = 0xffffffffLL;
   return (int64_t)bm * k * 2 <= lim && (int64_t)bn * (k / kQK) * qsb <= lim &&
-         (int64_t)bn * L.ds * 2 <= lim;
+         (int64_t)bn * L.ds * 2 <= lim && (int64_t)bn * L.ss <= lim;
 }
 
 namespace {
@@ -82,6 +82,7 @@ __global__ void __launch_bounds__(256)
 // dequantization per flop of the 256-row tiles; with Q4_0 only half of its
 // threads have a 32-weight chunk to dequantize per K-tile, which made it
 // slower than 256 x 256 there (measured), so it is planned for Q8_0 only.
+// Q6_S (two 32-weight chunks per row per K-tile, like Q4_0) takes Q4_0's set.
 struct Cfg {
   int bm, bn, wm, wn, per_cu;
   double rate;
@@ -93,6 +94,9 @@ constexpr Cfg kCfgs[] = {
     {256, 256, 2, 4, 1, 977, 3}, {256, 256, 2, 2, 1, 835, 3}, {512, 128, 4, 2, 1, 1035, 1},
 };
 bool planned_for(const Cfg &g, int32_t type) { return g.formats & (type == EB_Q8_0 ? 1 : 2); }
+
+// canonical weight bytes per 32 weights
+double bytes_per_32(int32_t type) { return type == EB_Q8_0 ? 34.0 : (type == EB_Q6_S ? 26.25 : 18.0); }
 constexpr int kNumCfgs = sizeof(kCfgs) / sizeof(kCfgs[0]);
 
 // Tile configurations that also come with hi/lo weight tiles (bfloat16
@@ -121,7 +125,7 @@ double estimate(int32_t type, const Cfg &g, int64_t m, int64_t n, int64_t k, int
     const int64_t w = std::min<int64_t>(g.per_cu, (std::min(left, slots) + cus - 1) / cus);
     t += w * wg_flops / (cu_rate * std::sqrt((double)w / g.per_cu)) + 1e-6;
   }
-  const double wbytes = (double)n * k * (type == EB_Q8_0 ? 34.0 : 18.0) / 32.0;
+  const double wbytes = (double)n * k * bytes_per_32(type) / 32.0;
   t = std::max(t, wbytes / 5e12);
   if (splits > 1) t += (2.0 * splits + 1.0) * (double)m * n * 4 / 4e12 + 3e-6;
   return t;
@@ -148,7 +152,9 @@ MfmaPlan plan_mfma(int32_t type, int32_t xt, int64_t m, int64_t n, int64_t k, si
   }
   MfmaPlan best;
   best.hl = hl;
-  if (type == EB_Q6_S) {  // one kernel for every m
+  // Q6_S: its own kernel up to 128 rows (hi/lo weights for bfloat16 x), the
+  // tile kernel beyond (measured at 816 and 4096 rows: 10x faster)
+  if (type == EB_Q6_S && (m <= kHLMaxM || !mfma_fits_offsets(type, n, k, 64, 128))) {
     best.q6 = true;
     best.hl = xt == EB_BF16;
     best.kts = (int)nk;
@@ -184,9 +190,7 @@ MfmaPlan plan_mfma(int32_t type, int32_t xt, int64_t m, int64_t n, int64_t k, si
       if (!per_cu) continue;
       g.per_cu = per_cu;
     }
-    const bool fits = type == EB_Q4_0 ? mfma_fits_offsets(EB_Q4_0, n, k, g.bm, g.bn)
-                                      : mfma_fits_offsets(EB_Q8_0, n, k, g.bm, g.bn);
-    if (!fits) continue;
+    if (!mfma_fits_offsets(type, n, k, g.bm, g.bn)) continue;
     for (int sp = 1; sp <= 16; ++sp) {
       if (sp > 1 && max_ws == 0) break;
       if (fs > 0 && sp != fs) continue;
@@ -229,8 +233,7 @@ int plan_grouped(int32_t type, const std::vector<GOp> &ops, std::vector<int2> &o
     bool fits = true;
     double work = 0, longest = 0;
     for (const GOp &o : ops) {
-      fits = fits && (type == EB_Q4_0 ? mfma_fits_offsets(EB_Q4_0, o.n, o.k, g.bm, g.bn)
-                                      : mfma_fits_offsets(EB_Q8_0, o.n, o.k, g.bm, g.bn));
+      fits = fits && mfma_fits_offsets(type, o.n, o.k, g.bm, g.bn);
       const double nk = (double)((o.k + kBK - 1) / kBK);
       work += (double)(((o.m + g.bm - 1) / g.bm) * ((o.n + g.bn - 1) / g.bn)) * nk;
       longest = std::max(longest, nk);
@@ -295,8 +298,12 @@ hipError_t launch_mfma(int32_t type, const void *wdata, int64_t n, int64_t k, co
                        int32_t xt, int64_t m, void *y, int32_t yt, const Fuse &f,
                        const MfmaPlan &plan, float *ws, hipStream_t s, const NormOut *no) {
   if (type == EB_Q6_S) {
-    if (no) return hipErrorInvalidValue;  // no split, so no reduction to fuse into
-    return launch_mfma_q6(wdata, n, k, x, xt, m, y, yt, f, s);
+    if (plan.q6) {
+      if (no) return hipErrorInvalidValue;  // no split, so no reduction to fuse into
+      return launch_mfma_q6(wdata, n, k, x, xt, m, y, yt, f, s);
+    }
+    if (xt == EB_F16) return launch_q<EB_Q6_S, EB_F16>(wdata, n, k, x, m, y, yt, f, plan, ws, s, no);
+    return launch_q<EB_Q6_S, EB_BF16>(wdata, n, k, x, m, y, yt, f, plan, ws, s, no);
   }
   if (type == EB_Q4_0) {
     if (xt == EB_F16) return launch_q<EB_Q4_0, EB_F16>(wdata, n, k, x, m, y, yt, f, plan, ws, s, no);
@@ -308,6 +315,10 @@ hipError_t launch_mfma(int32_t type, const void *wdata, int64_t n, int64_t k, co
 
 hipError_t launch_mfma_grouped(int32_t type, int32_t xt, int cfg, const GOp *ops, const int2 *order,
                                 int64_t entries, hipStream_t s) {
+  if (type == EB_Q6_S) {
+    if (xt == EB_F16) return mfma_tile_launch_grouped<EB_Q6_S, EB_F16>(cfg, ops, order, entries, s);
+    return mfma_tile_launch_grouped<EB_Q6_S, EB_BF16>(cfg, ops, order, entries, s);
+  }
   if (type == EB_Q4_0) {
     if (xt == EB_F16) return mfma_tile_launch_grouped<EB_Q4_0, EB_F16>(cfg, ops, order, entries, s);
     return mfma_tile_launch_grouped<EB_Q4_0, EB_BF16>(cfg, ops, order, entries, s);

@@ -11,7 +11,6 @@
 namespace eb {
 namespace {
 
-
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
@@ -43,7 +42,8 @@ __device__ inline f32x16_t mfma32(const uint4 a, const uint4 b, f32x16_t c) {
 
 template <int QT>
 struct WTile {
-  // 16-byte weight chunks per row per K-tile: Q8_0 four half-blocks, Q4_0 two blocks
+  // weight chunks per row per K-tile: Q8_0 four 16-byte half-blocks, Q4_0 two
+  // 16-byte blocks, Q6_S two 24-byte code chunks (one 48-byte unit of 64 weights)
   static constexpr int kChunksPerRow = (QT == EB_Q8_0) ? 4 : 2;
   static constexpr int kElemsPerChunk = (QT == EB_Q8_0) ? 16 : 32;
 };
@@ -60,6 +60,7 @@ template <int QT>
 struct Deq {
   static constexpr int kVecs = (QT == EB_Q8_0) ? 2 : 4;
 };
+
 
 // two codes in bytes b0, b1 of v -> 16-bit halves 0x64bb of the result
 __device__ inline uint32_t under_1024(uint32_t v, uint32_t sel) {
@@ -124,6 +125,43 @@ __device__ inline void dequant_chunk(const uint4 q, float d, uint4 (&v)[Deq<QT>:
     v[2] = make_uint4(hi[0], hi[1], hi[2], hi[3]);
     v[3] = make_uint4(hi[4], hi[5], hi[6], hi[7]);
   }
+}
+
+// Q6_S: one 24-byte chunk of 32 weights -> 4 vectors, in k order.  The
+// chunk's 16 low-nibble bytes L (byte t: weight t in bits 0..3, weight t + 16
+// in bits 4..7) and 8 top-bit bytes H (byte t: the top bits of weights t,
+// t + 8, t + 16, t + 24 at bits 0, 2, 4, 6) are merged into bytes u = 0..63,
+// four per word, placed under binary16 1024 by one byte permute per two
+// codes, and
+//   fma(1024 + u, e, -1056 e) = (u - 32) e,   e = d16 sc_j
+// is exact (e has at most 18 significant bits, 1056 e and the result at most
+// 24); one rounding to the 16-bit activation type.  Weights 0..15 of the
+// chunk use sub-scale sc0, 16..31 sc1.
+template <int XT>
+__device__ inline void dequant_chunk_q6(const uint4 l16, const uint2 h8, uint32_t sc2, float d,
+                                        uint4 (&v)[4]) {
+  const uint32_t L[4] = {l16.x, l16.y, l16.z, l16.w};
+  const uint32_t H[2] = {h8.x, h8.y};
+  const float e0 = d * (float)(int8_t)(sc2 & 0xffu), e1 = d * (float)(int8_t)((sc2 >> 8) & 0xffu);
+  const float c0 = -1056.0f * e0, c1 = -1056.0f * e1;
+  constexpr uint32_t kSelLo = 0x04010400u, kSelHi = 0x04030402u;
+  uint32_t lo[8], hi[8];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    // word j: weights 4j .. 4j + 3 (low nibbles) and 4j + 16 .. (high), their
+    // top bits in top-bit word j & 1 at shift 2 (j >> 1) and 2 (j >> 1) + 4
+    const uint32_t t = H[j & 1] >> (2 * (j >> 1));
+    const uint32_t ul = (L[j] & 0x0f0f0f0fu) | ((t & 0x03030303u) << 4);
+    const uint32_t uh = ((L[j] >> 4) & 0x0f0f0f0fu) | ((t & 0x30303030u));
+    lo[2 * j] = deq_pair<XT>(under_1024(ul, kSelLo), e0, c0);
+    lo[2 * j + 1] = deq_pair<XT>(under_1024(ul, kSelHi), e0, c0);
+    hi[2 * j] = deq_pair<XT>(under_1024(uh, kSelLo), e1, c1);
+    hi[2 * j + 1] = deq_pair<XT>(under_1024(uh, kSelHi), e1, c1);
+  }
+  v[0] = make_uint4(lo[0], lo[1], lo[2], lo[3]);
+  v[1] = make_uint4(lo[4], lo[5], lo[6], lo[7]);
+  v[2] = make_uint4(hi[0], hi[1], hi[2], hi[3]);
+  v[3] = make_uint4(hi[4], hi[5], hi[6], hi[7]);
 }
 
 // dequant_chunk for bfloat16 activations, as hi/lo pairs (split2_bf16):

@@ -66,13 +66,13 @@ __device__ inline uint8_t *lds_array() {
 template <int QT, int XT, int BM, int BN, int WM, int WN, bool G = false, bool HL = false>
 __global__ void __launch_bounds__(WM *WN * 64)
     mfma_kernel(const uint8_t *__restrict__ wdata_, int64_t n_, int64_t k_, int64_t d_off_,
-                int64_t ds_, const uint16_t *__restrict__ x_, int64_t m_, void *__restrict__ y_,
+                int64_t ds_, int64_t sc_off_, const uint16_t *__restrict__ x_, int64_t m_, void *__restrict__ y_,
                 int yt_, Fuse f_, int kts_, float *__restrict__ ws, int64_t ws_stride,
                 const GOp *__restrict__ gops, const int2 *__restrict__ gorder) {
   const uint8_t *wdata = wdata_;
   const uint16_t *x = x_;
   void *y = y_;
-  int64_t n = n_, k = k_, d_off = d_off_, ds = ds_, m = m_;
+  int64_t n = n_, k = k_, d_off = d_off_, ds = ds_, sc_off = sc_off_, m = m_;
   int yt = yt_, kts = kts_;
   Fuse f = f_;
   int64_t gtile = 0;
@@ -87,6 +87,7 @@ __global__ void __launch_bounds__(WM *WN * 64)
     k = o.k;
     d_off = o.d_off;
     ds = o.ds;
+    sc_off = o.sc_off;
     m = o.m;
     yt = o.yt;
     f = o.f;
@@ -102,15 +103,17 @@ __global__ void __launch_bounds__(WM *WN * 64)
   constexpr int WCH = BN * WCPR;                   // weight chunks per K-tile
   constexpr int BCH = (WCH + T - 1) / T;           // per thread (the last may be partial)
   constexpr int KSTEPS = kBK / 16;
-  constexpr int QSB = (QT == EB_Q8_0) ? 32 : 16;   // code bytes per block
+  constexpr bool Q6 = QT == EB_Q6_S;
+  constexpr int QSB = (QT == EB_Q8_0) ? 32 : (Q6 ? 24 : 16);  // code bytes per 32 weights
   constexpr int NV = Deq<QT>::kVecs;               // 16-byte vectors per dequantized chunk
   constexpr int ABYTES = BM * kBK * 2, BBYTES = BN * kBK * 2;
   static_assert(!HL || XT == EB_BF16, "hi/lo weight tiles are for bfloat16 activations");
+  static_assert(!HL || !Q6, "Q6_S takes this kernel only without hi/lo tiles (m > 128)");
   constexpr int BW = (HL ? 4 : 2) * BBYTES;         // the two weight buffers (hi and lo parts)
   constexpr int NRD = FM + FN * (HL ? 2 : 1);       // LDS fragment reads per k-step
   constexpr int NMF = FM * FN * (HL ? 2 : 1);       // MFMAs per k-step
   // vector-memory operations one thread issues per K-tile
-  constexpr int NX = ADMA, NW = 2 * BCH;
+  constexpr int NX = ADMA, NW = (Q6 ? 4 : 2) * BCH;  // Q6_S: codes, top bits, d16, sub-scales
   static_assert(ADMA >= 1 && ADMA * 8 * WAVES == BM, "x tile must split into 8-row copies");
   static_assert(TM % 32 == 0 && TN % 32 == 0, "wave sub-tile must be whole fragments");
   static_assert(2 * NW + NX <= 63, "vmcnt range");
@@ -161,10 +164,16 @@ __global__ void __launch_bounds__(WM *WN * 64)
   const int nk = (int)min((int64_t)kts, (k + kBK - 1) / kBK - kt0);
   const uint8_t *const xbase = reinterpret_cast<const uint8_t *>(x) + m0 * k * 2 + kt0 * (kBK * 2);
   const uint8_t *const qbase = wdata + n0 * nb * QSB + kt0 * (2 * QSB);
-  const uint8_t *const dbase = wdata + d_off + n0 * ds * 2 + kt0 * 4;
+  // scales: Q8_0 / Q4_0 two binary16 scales per row per K-tile; Q6_S one d16
+  // per four K-tiles (found by K-tile index, not by a linear advance) and
+  // four int8 sub-scales per row per K-tile in the sub-scale plane
+  const uint8_t *const dbase = wdata + d_off + n0 * ds * 2 + (Q6 ? 0 : kt0 * 4);
+  const int64_t srow = k / 16;
+  const uint8_t *const sbase = wdata + sc_off + n0 * srow + kt0 * 4;
   const uint32_t xrec = (uint32_t)(rows_m * k * 2 - kt0 * (kBK * 2));
   const uint32_t qrec = (uint32_t)(rows_n * nb * QSB - kt0 * (2 * QSB));
-  const uint32_t drec = (uint32_t)(rows_n * ds * 2 - kt0 * 4);
+  const uint32_t drec = (uint32_t)(rows_n * ds * 2 - (Q6 ? 0 : kt0 * 4));
+  const uint32_t srec = Q6 ? (uint32_t)(rows_n * srow - kt0 * 4) : 0u;
 
   // x copy: wave `wave`, copy i moves tile rows 8 (i WAVES + wave) .. +7; lane
   // j fills LDS chunk position j % 8 of row j / 8, i.e. logical chunk
@@ -179,14 +188,23 @@ __global__ void __launch_bounds__(WM *WN * 64)
   // indices past the tile (only when T does not divide it) are moved past the
   // buffers too and their stores are skipped.  Chunk c of a row covers logical
   // 16-byte positions NV c .. NV c + NV - 1; since NV c is a multiple of NV the
-  // stored position of part q is (NV c ^ swz(r)) ^ q, so wl ^ (16 q).
-  uint32_t qo[BCH], dof[BCH], wl[BCH];
+  // stored position of part q is (NV c ^ swz(r)) ^ q, so wl ^ (16 q).  A Q6_S
+  // chunk c (bytes 24 c .. 24 c + 23 of the row's 48-byte unit) is read as its
+  // 16 code bytes and its 8 top-bit bytes (8-byte aligned loads), with its two
+  // sub-scales.
+  uint32_t qo[BCH], dof[BCH], wl[BCH], so[Q6 ? BCH : 1];
 #pragma unroll
   for (int i = 0; i < BCH; ++i) {
     const int idx = min(tid + i * T, WCH), r = idx / WCPR, c = idx % WCPR;
     const int blk = (QT == EB_Q8_0) ? (c >> 1) : c;
-    qo[i] = (uint32_t)((r * nb + blk) * QSB + ((QT == EB_Q8_0) ? (c & 1) * 16 : 0));
-    dof[i] = (uint32_t)((r * ds + blk) * 2);
+    if constexpr (Q6) {
+      qo[i] = (uint32_t)(r * nb * QSB + 24 * c);
+      dof[i] = (uint32_t)(r * ds * 2);
+      so[i] = (uint32_t)(r * srow + 2 * c);
+    } else {
+      qo[i] = (uint32_t)((r * nb + blk) * QSB + ((QT == EB_Q8_0) ? (c & 1) * 16 : 0));
+      dof[i] = (uint32_t)((r * ds + blk) * 2);
+    }
     wl[i] = (uint32_t)(r * (kBK * 2) + (((NV * c) ^ swz(r)) << 4));
   }
 
@@ -203,24 +221,38 @@ __global__ void __launch_bounds__(WM *WN * 64)
   // reads a zero scale from the scale-plane padding, so its weights are zeros.
   struct Raw {
     uint4 b[BCH];
+    uint2 h[Q6 ? BCH : 1];      // Q6_S: the chunk's 8 top-bit bytes
     uint16_t d[BCH];
+    uint16_t sc[Q6 ? BCH : 1];  // Q6_S: the chunk's two int8 sub-scales
   };
   Raw S0, S1, S2;
   auto load_w = [&](Raw &S, int kt) __attribute__((always_inline)) {
-    const uint32_t qadv = (uint32_t)kt * (2 * QSB), dadv = (uint32_t)kt * 4;
+    const uint32_t qadv = (uint32_t)kt * (2 * QSB);
+    const uint32_t dadv = Q6 ? (uint32_t)((kt0 + kt) >> 2) * 2 : (uint32_t)kt * 4;
     const auto qr = rsrc(qbase + qadv, qrec - qadv);
     const auto dr = rsrc(dbase + dadv, drec - dadv);
 #pragma unroll
     for (int i = 0; i < BCH; ++i) {
       S.b[i] = bload(qr, qo[i]);
+      if constexpr (Q6) {
+        const auto t = __builtin_amdgcn_raw_buffer_load_b64(qr, (int)qo[i] + 16, 0, 0);
+        S.h[i] = make_uint2(t[0], t[1]);
+      }
       S.d[i] = __builtin_amdgcn_raw_buffer_load_b16(dr, (int)dof[i], 0, 0);
+    }
+    if constexpr (Q6) {
+      const auto sr = rsrc(sbase + (uint32_t)kt * 4, srec - (uint32_t)kt * 4);
+#pragma unroll
+      for (int i = 0; i < BCH; ++i) S.sc[i] = __builtin_amdgcn_raw_buffer_load_b16(sr, (int)so[i], 0, 0);
     }
   };
   auto store_w = [&](const Raw &S, uint8_t *sB, int i) __attribute__((always_inline)) {
     if (WCH % T != 0 && i == BCH - 1 && tid + i * T >= WCH) return;
     uint4 v[NV];
     const float d = (float)__builtin_bit_cast(_Float16, S.d[i]);
-    if constexpr (HL) {
+    if constexpr (Q6) {
+      dequant_chunk_q6<XT>(S.b[i], S.h[i], S.sc[i], d, v);
+    } else if constexpr (HL) {
       uint4 vl[NV];
       dequant_chunk_hl<QT>(S.b[i], d, v, vl);
 #pragma unroll
@@ -312,7 +344,7 @@ __global__ void __launch_bounds__(WM *WN * 64)
     // spread evenly between the MFMAs instead of in bursts (measured: 2.5%
     // faster on the video projections; for Q8_0 the same spreading was 1-4%
     // slower, so its VALU work is left to the compiler).
-    constexpr int kVpm = (BCH * (HL ? 160 : 80) + KSTEPS * NMF - 1) / (KSTEPS * NMF);
+    constexpr int kVpm = (BCH * (HL ? 160 : (Q6 ? 100 : 80)) + KSTEPS * NMF - 1) / (KSTEPS * NMF);
     __builtin_amdgcn_sched_group_barrier(0x100, NRD, 0);
     __builtin_amdgcn_sched_group_barrier(0x020, NW, 0);
 #pragma unroll
@@ -321,7 +353,7 @@ __global__ void __launch_bounds__(WM *WN * 64)
 #pragma unroll
       for (int j = 0; j < NMF; ++j) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        if constexpr (QT == EB_Q4_0) __builtin_amdgcn_sched_group_barrier(0x002, kVpm, 0);
+        if constexpr (QT != EB_Q8_0) __builtin_amdgcn_sched_group_barrier(0x002, kVpm, 0);
       }
     }
   };
@@ -460,7 +492,7 @@ hipError_t launch_t(const void *wdata, int64_t n, int64_t k, const void *x, int6
   if (tiles * splits > 0x7fffffff) return hipErrorInvalidValue;
   if (!mfma_fits_offsets(QT, n, k, BM, BN)) return hipErrorInvalidValue;
   mfma_kernel<QT, XT, BM, BN, WM, WN, false, HL><<<(unsigned)(tiles * splits), WM * WN * 64, 0, s>>>(
-      (const uint8_t *)wdata, n, k, L.d_off, L.ds, (const uint16_t *)x, m, y, yt, f, kts,
+      (const uint8_t *)wdata, n, k, L.d_off, L.ds, L.sc_off, (const uint16_t *)x, m, y, yt, f, kts,
       splits > 1 ? ws : nullptr, ws_stride, nullptr, nullptr);
   return hipGetLastError();
 }
@@ -469,7 +501,7 @@ template <int QT, int XT, int BM, int BN, int WM, int WN>
 hipError_t launch_g(const GOp *ops, const int2 *order, int64_t entries, hipStream_t s) {
   if (entries <= 0 || entries > 0x7fffffff) return hipErrorInvalidValue;
   mfma_kernel<QT, XT, BM, BN, WM, WN, true><<<(unsigned)entries, WM * WN * 64, 0, s>>>(
-      nullptr, 0, 0, 0, 0, nullptr, 0, nullptr, 0, Fuse{}, 0, nullptr, 0, ops, order);
+      nullptr, 0, 0, 0, 0, 0, nullptr, 0, nullptr, 0, Fuse{}, 0, nullptr, 0, ops, order);
   return hipGetLastError();
 }
 
@@ -479,7 +511,7 @@ template <int QT, int XT>
 hipError_t mfma_tile_launch(int cfg, bool hl, const void *wdata, int64_t n, int64_t k, const void *x,
                             int64_t m, void *y, int32_t yt, const Fuse &f, int sp, int kts,
                             float *ws, int64_t st, hipStream_t s) {
-  if constexpr (XT == EB_BF16) {
+  if constexpr (XT == EB_BF16 && QT != EB_Q6_S) {
     if (hl) {  // the configurations with hi/lo weight tiles
       if (cfg == 0) return launch_t<QT, XT, 64, 128, 2, 2, true>(wdata, n, k, x, m, y, yt, f, sp, kts, ws, st, s);
       if (cfg == 1) return launch_t<QT, XT, 128, 128, 2, 2, true>(wdata, n, k, x, m, y, yt, f, sp, kts, ws, st, s);

@@ -10,7 +10,8 @@ _FILES = {
     "gemv": ("gemv.hip", "gemv_common.h") + _COMMON,
     # tile kernel of the MFMA path (single ops, split-K, grouped launches)
     "mfma": ("mfma.hip", "mfma_tile.h", "mfma_narrow.hip", "mfma_q8_0_bf16.hip", "mfma_q8_0_f16.hip",
-             "mfma_q4_0_bf16.hip", "mfma_q4_0_f16.hip", "mfma_common.h", "norm.hip") + _COMMON,
+             "mfma_q4_0_bf16.hip", "mfma_q4_0_f16.hip", "mfma_q6_s_bf16.hip", "mfma_q6_s_f16.hip",
+             "mfma_common.h", "norm.hip") + _COMMON,
     # fused small-m MFMA kernels (m <= 128)
     "mm": ("mfma_lds2.hip", "mfma_multi.hip", "mfma_common.h", "mm_common.h", "norm.hip") + _COMMON,
     # the Q6_S kernel (every m)

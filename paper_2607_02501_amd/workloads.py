@@ -59,6 +59,10 @@ WORKLOADS = {
     "q8_0_vlm_prefill_816": Workload("q8_0_vlm_prefill_816", Q8_0, torch.bfloat16, 816, 18, 1,
                                      (("qkv", 2048, 2560), ("o", 2048, 2048),
                                       ("gate_up", 2048, 32768), ("down", 16384, 2048)), wid=2),
+    # the same prefill in the 6-bit format
+    "q6_s_vlm_prefill_816": Workload("q6_s_vlm_prefill_816", Q6_S, torch.bfloat16, 816, 18, 1,
+                                     (("qkv", 2048, 2560), ("o", 2048, 2048),
+                                      ("gate_up", 2048, 32768), ("down", 16384, 2048)), wid=6),
     # flow-matching action expert: 50 action tokens, 10 denoising steps, same weights each step
     "q8_0_action_expert_50x10": Workload("q8_0_action_expert_50x10", Q8_0, torch.bfloat16, 50, 18,
                                          10, (("qkv", 1024, 2048), ("o", 1024, 1024),

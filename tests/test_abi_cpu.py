@@ -123,6 +123,20 @@ def test_q6_validation(eb):
     assert _launches(eb, q6ops(1, 16640)) == 4
     # one fused launch per slot count (64-weight units per lane: k = 4096 -> 1, 11008 -> 3)
     assert _launches(eb, q6ops(1, 4096)[:2] + q6ops(1, 11008)[2:]) == 2
+    # beyond 128 rows the tile kernel of the other formats: a lone op may split
+    # k (many tiles: unsplit), independent ops share one grouped launch
+    op = eb.eb_qlinear_op(_w(eb, eb.EB_Q6_S, n=4096, k=4096, data=1 * GB), 8 * GB, 9 * GB, 4096,
+                          eb.EB_BF16, eb.EB_F32)
+    assert L.eb_qlinear_workspace_bytes(ctypes.byref(op), eb.EB_PATH_AUTO) == 0
+    for m, n, k in ((129, 4096, 4096), (816, 2048, 2048), (4096, 4096, 4096)):
+        ops = [_op(eb, 1 * GB + i * (64 << 20), 8 * GB + i * (64 << 20), 12 * GB + i * (128 << 20),
+                   k=k, n=n, m=m, qtype=eb.EB_Q6_S, xt=eb.EB_BF16) for i in range(3)]
+        assert _launches(eb, ops) == 1, (m, n, k)
+        assert _launches(eb, ops[:1]) in (1, 2), (m, n, k)   # the op alone, split or not
+    # up to 128 rows its own kernel, one launch per op
+    assert _launches(eb, [_op(eb, 1 * GB + i * (64 << 20), 8 * GB + i * (64 << 20),
+                              12 * GB + i * (128 << 20), k=2048, n=2048, m=128, qtype=eb.EB_Q6_S,
+                              xt=eb.EB_BF16) for i in range(3)]) == 3
 
 
 def test_bytes_rejects_bad_sizes(eb):
