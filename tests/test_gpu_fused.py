@@ -210,7 +210,11 @@ def _chain_reference(orc, L, qtype, xdtype, h0):
                                                 ("q8_0", torch.bfloat16, 40, 2048, 1024),
                                                 ("q8_0", torch.bfloat16, 100, 1024, 4096),
                                                 ("q4_0", torch.bfloat16, 100, 3072, 1024),
-                                                ("q8_0", torch.bfloat16, 72, 5120, 1024)])
+                                                ("q8_0", torch.bfloat16, 72, 5120, 1024),
+                                                ("q6_s", torch.float16, 1, 512, 768),
+                                                ("q6_s", torch.bfloat16, 50, 512, 768),
+                                                ("q6_s", torch.bfloat16, 300, 512, 768),
+                                                ("q6_s", torch.float16, 200, 1024, 2048)])
 def test_decoder_layer_chain(eb, oracle, qtype, xdtype, m, d, f, monkeypatch):
     """The four projections of a layer as one stack: results equal the ops run
     one by one through eb_qlinear_fused, bit for bit (with and without the

@@ -157,12 +157,12 @@ FUSIONS = [("rmsnorm", None), (None, "add"), (None, "glu"), ("rmsnorm", "glu"), 
                                            (torch.bfloat16, torch.bfloat16)])
 def test_q6_fused_steps(eb, oracle, pro, epi, xdtype, ydtype):
     n, k = 198, 1280
-    for m in (1, 20, 150):
+    for m, splits in ((1, 0), (20, 0), (150, 0), (150, 3)):
         c = Case(eb, 1200 + m, "q6_s", n, k, m, xdtype, pro, epi, ydtype)
-        y = c.run(eb)
+        y = c.run(eb, splits=splits)   # 150 rows: the tile kernel, k split 3 ways in the second run
         torch.cuda.synchronize()
         y_ref, scale = c.reference(oracle)
-        assert_fused(y, y_ref, scale, f"q6_fused_{pro}_{epi} m={m}")
+        assert_fused(y, y_ref, scale, f"q6_fused_{pro}_{epi} m={m} splits={splits}")
 
 
 def test_q6_zero_weights_and_determinism(eb):
