@@ -1,5 +1,7 @@
 // mfma_q6.hip -- linear layers on Q6_S weights (the 6-bit configuration of
-// paper section 4, Table 3) on the matrix cores, for every m, in one launch.
+// paper section 4, Table 3) on the matrix cores, in one launch: the path for
+// m <= 128 (and for any m the tile kernel cannot address); larger m takes the
+// tile kernel of the other formats (mfma_tile.h).
 //
 // Q6_S: super-blocks of 256 weights along k, 16 int8 sub-block scales sc_j
 // under one binary16 scale d16, 6-bit codes u (w_hat = (u - 32) d16 sc_j).

@@ -10,10 +10,10 @@
 // tokens (paper section 2.1 / Table 1 model families; section 3.2
 // "operator fusion, backend-specific dispatch").
 //
-// y[m][n] = sum_k x[m][k] * w_hat[n][k], w_hat = code * d16 rounded once to
-// the activation type (bfloat16 or binary16), or, for bfloat16 activations on
-// the small tiles (m <= 128), carried as a hi/lo pair of bfloat16 values;
-// fp32 accumulation.
+// y[m][n] = sum_k x[m][k] * w_hat[n][k], w_hat = code * d16 (Q6_S: (u - 32)
+// d16 sc_j) rounded once to the activation type (bfloat16 or binary16), or,
+// for bfloat16 activations on the small tiles (m <= 128; Q8_0 and Q4_0),
+// carried as a hi/lo pair of bfloat16 values; fp32 accumulation.
 //
 // A workgroup of WM x WN waves computes a BM x BN tile of y; each wave owns a
 // (BM/WM) x (BN/WN) sub-tile of fp32 accumulators.  Per K-tile of 64:
