@@ -307,6 +307,10 @@ int narrow_splits(int64_t n, int64_t k, int cus) {
   const int64_t wgs = (n + 15) / 16, nb = k / kQK;
   int sp = env > 0 ? env : (int)std::max<int64_t>(1, cus / std::max<int64_t>(1, wgs));
   sp = (int)std::min<int64_t>({(int64_t)sp, (int64_t)kNarrowMaxSplits, nb / 8});
+  // a split of 2 saves each wave half its blocks (about 1.2 us each) but adds
+  // the reduction launch: on the 50-row chains the 2048-wide QKV projection
+  // (4 blocks per wave) ran faster unsplit
+  if (env <= 0 && sp == 2) sp = 1;
   if (k / std::max(sp, 1) > kNarrowMaxK)  // shares of at most kNarrowMaxK
     sp = (int)std::min<int64_t>(kNarrowMaxSplits, (k + kNarrowMaxK - 1) / kNarrowMaxK);
   return std::max(sp, 1);
