@@ -244,8 +244,8 @@ def scratch(device, nbytes: int):
 
 def _run_op(op: eb_qlinear_op, path: int, device, tile=None, splits=0) -> None:
     nbytes = int(lib.eb_qlinear_workspace_bytes(ctypes.byref(op), path if tile is None else EB_PATH_MFMA))
-    if tile is not None and nbytes:
-        nbytes += 64 << 20  # room for any forced split
+    if tile is not None:
+        nbytes += 64 << 20  # room for any forced split (also where the automatic plan needs none)
     ws = scratch(device, nbytes)
     wp, wb = (ws.data_ptr(), ws.numel()) if ws is not None else (None, 0)
     if tile is None:
