@@ -280,3 +280,57 @@ def test_q6_m1_fused_launch_matches_single_calls(eb, oracle, xdtype, monkeypatch
         for y, o in zip(singles, outs):
             assert torch.equal(y, o), mode
     eb.stack_cache_clear()
+
+
+def _extreme_q6_weights(n, k, seed):
+    """N(0, 0.02) rows whose super-blocks are rescaled: every third to
+    max |w| = 60000, every fifth to about 1e-6 (a binary16-subnormal or zero
+    super-scale), and inside every other super-block one sub-block 100x
+    smaller than the rest (sub-scales far below the super-scale)."""
+    w = W.normal((n, k), seed, "cpu", W.WEIGHT_STD).view(n, k // 256, 256)
+    amax = w.abs().amax(dim=2, keepdim=True).clamp_min(1e-30)
+    ns = k // 256
+    big = torch.zeros(ns, dtype=torch.bool)
+    big[0::3] = True
+    tiny = torch.zeros(ns, dtype=torch.bool)
+    tiny[1::5] = True
+    w = torch.where(big.view(1, ns, 1), w / amax * 60000.0, w)
+    w = torch.where(tiny.view(1, ns, 1), w / amax * 1e-6, w)
+    w[:, 0::2, 32:48] *= 0.01
+    return w.reshape(n, k).contiguous()
+
+
+@pytest.mark.parametrize("xdtype", [torch.float16, torch.bfloat16])
+def test_q6_extreme_scales_every_path(eb, oracle, xdtype, monkeypatch):
+    """Super-blocks with max |w| from 1e-6 to 60000 in one row and sub-blocks
+    far below their super-scale, on every Q6_S path: the m = 1 GEMV (lone and
+    in a fused launch), the m <= 8 GEMV, the Q6_S matrix-core kernel and the
+    tile kernel (binary16 x: w_hat rounded to binary16 adds 2^-25 sum_k |x|;
+    bfloat16 x: the tile bound)."""
+    monkeypatch.delenv("EB_STACK_FUSE", raising=False)
+    n, k = 200, 2560
+    w = _extreme_q6_weights(n, k, 2000 + (xdtype == torch.bfloat16))
+    x = W.normal((300, k), 2010, "cpu").to(xdtype)
+    qw = eb.quantize(w.to(DEV), "q6_s")
+    _, y_ref, bound = oracle_reference(oracle, "q6_s", w.numpy(), x)
+    xd = x.to(DEV)
+    sum_abs_x = x.double().abs().sum(dim=1, keepdim=True).numpy()
+    f16 = xdtype == torch.float16
+    for m in (1, 4):
+        y = eb.qlinear(qw, xd[:m], path="gemv")
+        assert_parity(y, y_ref[:m], bound[:m], TOL_F32, f"q6_scale_gemv m={m}")
+    for m in (50, 300):
+        y = eb.qlinear(qw, xd[:m], path="mfma")
+        tol = TOL_TILE_BF16 if (m > 128 and not f16) else TOL_F32
+        assert_parity(y, y_ref[:m], bound[:m], tol, f"q6_scale_mfma m={m}",
+                      slack=2.0 ** -25 * sum_abs_x[:m] if f16 else None)
+    # two independent m = 1 ops in one fused launch
+    ya = torch.full((1, n), float("nan"), device=DEV)
+    yb = torch.full((1, n), float("nan"), device=DEV)
+    ops = eb.make_ops([(qw, xd[:1], ya), (qw, xd[1:2], yb)])
+    assert eb.stack_launches(ops) == 1
+    eb.qlinear_stack(ops)
+    torch.cuda.synchronize()
+    assert_parity(ya, y_ref[:1], bound[:1], TOL_F32, "q6_scale_fused m=1")
+    assert_parity(yb, y_ref[1:2], bound[1:2], TOL_F32, "q6_scale_fused m=1 (op 2)")
+    eb.stack_cache_clear()
