@@ -575,14 +575,19 @@ __device__ __attribute__((always_inline)) inline void m1_rows(const uint8_t *__r
     S.dh[s][r] = __builtin_amdgcn_raw_buffer_load_b16(G.d[r], (int)(last ? dlast : dbase_l),
                                                       last ? 0 : (int)dstep * s, kNT);
   };
-  // items in the order step consumes them (slot-major)
+  // items in the order step consumes them (slot-major), kept in that order
+  // (left to the scheduler, the scales would follow all the codes and the
+  // first item's wait would be a wait for the whole group)
   auto load_group = [&](WSet &S, int64_t grp) __attribute__((always_inline)) {
     GRes G;
     group_res(grp, G);
 #pragma unroll
     for (int s = 0; s < NS; ++s)
 #pragma unroll
-      for (int r = 0; r < R; ++r) load_item(S, G, s, r);
+      for (int r = 0; r < R; ++r) {
+        load_item(S, G, s, r);
+        __builtin_amdgcn_sched_barrier(0);
+      }
   };
   // Binary16 activations: their loads are issued first, then the weight
   // loads of the first group, which stay in flight while x is staged

@@ -261,20 +261,62 @@ __device__ inline void chunk_dot6(const uint32_t (&L)[4], uint32_t H0, uint32_t 
 // Stage x (one row) into LDS for q6_rows: part p of unit u at xs[p * P + u]
 // (p = 4 h + i: chunk h of the unit, word i), and with bfloat16 x the four
 // sub-block offsets 160 * sum x of unit u at xoff[4 u .. 4 u + 3].  One thread
-// per part; with the normalisation prologue x is the fp32 stream h, each
-// thread's first two parts' h values stay in registers between the sum of
-// squares and the normalisation, and the sum is reduced over the wave by
-// exchanges and over the waves in order through `red` (one float per wave).
-template <int XT>
-__device__ __attribute__((always_inline)) inline void stage_x6(
-    const void *__restrict__ xv, int64_t k, int ku, uint4 *xs, float *xoff, int P, bool norm,
-    const float *__restrict__ gamma, float eps, float *red) {
+// per part; with the normalisation prologue x is the fp32 stream h, the
+// thread's first part's h values stay in registers between the sum of squares
+// and the normalisation, and the sum is reduced over the wave by exchanges and
+// over the waves in order through `red` (one float per wave).
+//
+// Two phases: x6_issue loads the thread's first part (h and gamma), or the
+// raw 16-bit values of its first two, into registers, and x6_finish stages
+// them with the rest.  The caller issues its first weight loads in between:
+// vector-memory loads complete in issue order, so waiting for activations
+// loaded after the weights would wait for all of those weights.
+struct X6Regs {
+  // normalisation prologue: h[e0..e0+3], h[e0+16..e0+19] and gamma there,
+  // for the thread's first part; otherwise the raw 8-byte halves of its first
+  // two parts (a = {part 0 at e0, part 1 at e0}, b likewise at e0 + 16)
+  uint4 a, b, ga, gb;
+};
+
+__device__ __attribute__((always_inline)) inline void x6_part(int c, int &u, int &p, int &e0) {
+  u = c >> 3;
+  p = c & 7;
+  e0 = u * kU6 + (p >> 2) * 32 + 4 * (p & 3);  // e1 = e0 + 16
+}
+
+__device__ __attribute__((always_inline)) inline void x6_issue(const void *__restrict__ xv, int ku, bool norm,
+                                                               const float *__restrict__ gamma, X6Regs &R) {
   const int nch = ku * kU6Parts, T = (int)blockDim.x, tid = (int)threadIdx.x;
-  auto first = [](int c, int &u, int &p, int &e0) __attribute__((always_inline)) {
-    u = c >> 3;
-    p = c & 7;
-    e0 = u * kU6 + (p >> 2) * 32 + 4 * (p & 3);  // e1 = e0 + 16
-  };
+  int u, p, e0;
+  if (norm) {
+    if (tid < nch) {
+      x6_part(tid, u, p, e0);
+      const float *h = static_cast<const float *>(xv);
+      R.a = *reinterpret_cast<const uint4 *>(h + e0);
+      R.b = *reinterpret_cast<const uint4 *>(h + e0 + 16);
+      R.ga = *reinterpret_cast<const uint4 *>(gamma + e0);
+      R.gb = *reinterpret_cast<const uint4 *>(gamma + e0 + 16);
+    }
+  } else {
+    const uint16_t *x = static_cast<const uint16_t *>(xv);
+    if (tid < nch) {
+      x6_part(tid, u, p, e0);
+      const uint2 ra = *reinterpret_cast<const uint2 *>(x + e0), rb = *reinterpret_cast<const uint2 *>(x + e0 + 16);
+      R.a.x = ra.x, R.a.y = ra.y, R.b.x = rb.x, R.b.y = rb.y;
+    }
+    if (tid + T < nch) {
+      x6_part(tid + T, u, p, e0);
+      const uint2 ra = *reinterpret_cast<const uint2 *>(x + e0), rb = *reinterpret_cast<const uint2 *>(x + e0 + 16);
+      R.a.z = ra.x, R.a.w = ra.y, R.b.z = rb.x, R.b.w = rb.y;
+    }
+  }
+}
+
+template <int XT>
+__device__ __attribute__((always_inline)) inline void x6_finish(
+    const void *__restrict__ xv, int64_t k, int ku, uint4 *xs, float *xoff, int P, bool norm,
+    const float *__restrict__ gamma, float eps, float *red, const X6Regs &R) {
+  const int nch = ku * kU6Parts, T = (int)blockDim.x, tid = (int)threadIdx.x;
   // pairs (a0,a2) (a1,a3) (b0,b2) (b1,b3), and the offsets' partial sums
   auto put = [&](int c, int u, int p, const uint32_t (&ra)[2], const uint32_t (&rb)[2])
       __attribute__((always_inline)) {
@@ -298,11 +340,28 @@ __device__ __attribute__((always_inline)) inline void stage_x6(
       }
     }
   };
+  auto f4 = [](uint4 v) __attribute__((always_inline)) {
+    return make_float4(__builtin_bit_cast(float, v.x), __builtin_bit_cast(float, v.y),
+                       __builtin_bit_cast(float, v.z), __builtin_bit_cast(float, v.w));
+  };
+  // The offsets' exchanges stay within the four consecutive lanes of a
+  // chunk's parts, which are all in or all out of each phase below (nch is a
+  // multiple of 8, T of 64).
   if (!norm) {
     const uint16_t *x = static_cast<const uint16_t *>(xv);
-    for (int c = tid; c < nch; c += T) {
-      int u, p, e0;
-      first(c, u, p, e0);
+    int u, p, e0;
+    if (tid < nch) {
+      x6_part(tid, u, p, e0);
+      const uint32_t ra[2] = {R.a.x, R.a.y}, rb[2] = {R.b.x, R.b.y};
+      put(tid, u, p, ra, rb);
+    }
+    if (tid + T < nch) {
+      x6_part(tid + T, u, p, e0);
+      const uint32_t ra[2] = {R.a.z, R.a.w}, rb[2] = {R.b.z, R.b.w};
+      put(tid + T, u, p, ra, rb);
+    }
+    for (int c = tid + 2 * T; c < nch; c += T) {
+      x6_part(c, u, p, e0);
       const uint2 a = *reinterpret_cast<const uint2 *>(x + e0);
       const uint2 b = *reinterpret_cast<const uint2 *>(x + e0 + 16);
       const uint32_t ra[2] = {a.x, a.y}, rb[2] = {b.x, b.y};
@@ -311,7 +370,6 @@ __device__ __attribute__((always_inline)) inline void stage_x6(
     return;
   }
   const float *h = static_cast<const float *>(xv);
-  float4 ha[2], hb[2];
   float ss = 0.f;
   auto sq = [](float acc, float4 v) __attribute__((always_inline)) {
     acc = __builtin_fmaf(v.x, v.x, acc);
@@ -319,20 +377,10 @@ __device__ __attribute__((always_inline)) inline void stage_x6(
     acc = __builtin_fmaf(v.z, v.z, acc);
     return __builtin_fmaf(v.w, v.w, acc);
   };
-#pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int c = tid + j * T;
-    if (c < nch) {
-      int u, p, e0;
-      first(c, u, p, e0);
-      ha[j] = *reinterpret_cast<const float4 *>(h + e0);
-      hb[j] = *reinterpret_cast<const float4 *>(h + e0 + 16);
-      ss = sq(sq(ss, ha[j]), hb[j]);
-    }
-  }
-  for (int c = tid + 2 * T; c < nch; c += T) {
+  if (tid < nch) ss = sq(sq(ss, f4(R.a)), f4(R.b));
+  for (int c = tid + T; c < nch; c += T) {
     int u, p, e0;
-    first(c, u, p, e0);
+    x6_part(c, u, p, e0);
     ss = sq(sq(ss, *reinterpret_cast<const float4 *>(h + e0)), *reinterpret_cast<const float4 *>(h + e0 + 16));
   }
 #pragma unroll
@@ -342,29 +390,24 @@ __device__ __attribute__((always_inline)) inline void stage_x6(
   float tot = 0.f;
   for (int w = 0; w < (T >> 6); ++w) tot += red[w];
   const float r = 1.0f / __builtin_sqrtf(tot / (float)k + eps);
-  auto normed = [&](float4 v, const float *g, uint32_t (&o)[2]) __attribute__((always_inline)) {
-    const float4 gg = *reinterpret_cast<const float4 *>(g);
+  auto normed = [&](float4 v, float4 gg, uint32_t (&o)[2]) __attribute__((always_inline)) {
     o[0] = pack_x16<XT>(v.x * gg.x * r, v.y * gg.y * r);
     o[1] = pack_x16<XT>(v.z * gg.z * r, v.w * gg.w * r);
   };
-#pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int c = tid + j * T;
-    if (c < nch) {
-      int u, p, e0;
-      first(c, u, p, e0);
-      uint32_t ra[2], rb[2];
-      normed(ha[j], gamma + e0, ra);
-      normed(hb[j], gamma + e0 + 16, rb);
-      put(c, u, p, ra, rb);
-    }
-  }
-  for (int c = tid + 2 * T; c < nch; c += T) {
+  if (tid < nch) {
     int u, p, e0;
-    first(c, u, p, e0);
+    x6_part(tid, u, p, e0);
     uint32_t ra[2], rb[2];
-    normed(*reinterpret_cast<const float4 *>(h + e0), gamma + e0, ra);
-    normed(*reinterpret_cast<const float4 *>(h + e0 + 16), gamma + e0 + 16, rb);
+    normed(f4(R.a), f4(R.ga), ra);
+    normed(f4(R.b), f4(R.gb), rb);
+    put(tid, u, p, ra, rb);
+  }
+  for (int c = tid + T; c < nch; c += T) {
+    int u, p, e0;
+    x6_part(c, u, p, e0);
+    uint32_t ra[2], rb[2];
+    normed(*reinterpret_cast<const float4 *>(h + e0), *reinterpret_cast<const float4 *>(gamma + e0), ra);
+    normed(*reinterpret_cast<const float4 *>(h + e0 + 16), *reinterpret_cast<const float4 *>(gamma + e0 + 16), rb);
     put(c, u, p, ra, rb);
   }
 }
@@ -381,9 +424,8 @@ __host__ __device__ constexpr size_t q6_m1_lds(int ns, int waves) {
 // Rows g*R .. g*R+R-1 for groups g = g0, g0 + gstride, ... < g_end of one
 // matrix, m == 1.  Called by every thread of the workgroup (it stages x into
 // LDS and synchronises once); waves whose first group is past g_end only help
-// with the staging.  PD register sets of weights: the group being computed
-// and the next PD - 1, whose loads are in flight meanwhile.
-template <int XT, int NS, int R, int PD>
+// with the staging.
+template <int XT, int NS, int R>
 __device__ __attribute__((always_inline)) inline void q6_rows(
     const uint8_t *__restrict__ wdata, int64_t n, int64_t k, int64_t sc_off, int64_t d_off,
     int64_t ds, const void *__restrict__ x, void *__restrict__ y, int yt, const Fuse &f, int64_t g,
@@ -402,68 +444,98 @@ __device__ __attribute__((always_inline)) inline void q6_rows(
   const uint8_t *__restrict__ sbase = wdata + sc_off;
   const uint8_t *__restrict__ dbase = wdata + d_off;
 
-  // per-lane byte offsets inside a row: the lane's 16-byte pieces of slot s's
-  // 3 KiB of codes (loads past the row's end return zeros), and its unit's
-  // scales; units past the end of the row (last slot only) read the row's
-  // last unit's scales and meet zero x
-  uint32_t qoff[NS], soff[NS], doff[NS], xidx[NS];
-#pragma unroll
-  for (int s = 0; s < NS; ++s) {
-    const int u = lane + 64 * s;
-    const int uc = min(u, ku - 1);
-    qoff[s] = (uint32_t)(64 * s * kU6Bytes + 16 * lane);
-    soff[s] = (uint32_t)uc * 4u;
-    doff[s] = (uint32_t)(uc >> 2) * 2u;
-    xidx[s] = u < ku ? (uint32_t)u : 64u * NS;
-  }
+  // Per-lane byte offsets inside a row: the lane's 16-byte pieces of slot
+  // s's 3 KiB of codes at 3072 s + 16 lane (+ 1024, + 2048; loads past the
+  // row's end return zeros), and its unit's scales.  Only the last slot can
+  // pass the end of the row (ku > 64 (NS - 1)): its units read the row's
+  // last unit's scales and meet zero x.  The other slots' offsets are the
+  // lane's base plus a constant.
+  const int ul = lane + 64 * (NS - 1), ulc = min(ul, ku - 1);
+  const uint32_t slast = (uint32_t)ulc * 4u, dlast = (uint32_t)(ulc >> 2) * 2u;
+  const uint32_t xlast = ul < ku ? (uint32_t)ul : 64u * NS;
+  const uint32_t qbase = 16u * lane, sbase_l = 4u * lane, dbase_l = (uint32_t)(lane >> 2) * 2u;
 
-  static_assert(PD >= 1 && PD <= 2, "1 or 2 weight register sets");
+  // One register set of weights, NS R items (slot s of row r: 48 code bytes,
+  // 4 sub-scales and the super-block scale of the lane's unit).  Each item is
+  // reloaded with the same item of the wave's next group right after it has
+  // been used, so a wave keeps one group of reads in flight without pauses
+  // while it decodes.  A group past g_end gets zero-sized buffer ranges (its
+  // loads return zeros without a memory access), so every load is issued on
+  // every path: a load issued on only some paths makes the compiler's
+  // counter wait for an earlier load a wait for everything.
   struct WSet {
     uint4 a[NS][R], b[NS][R], c[NS][R];
     uint32_t sc[NS][R];
     uint16_t dh[NS][R];
   };
-  WSet A, B;
-  auto load_group = [&](WSet &S, int64_t grp) __attribute__((always_inline)) {
+  WSet A;
+  struct GRes {
+    __amdgpu_buffer_rsrc_t q[R], s[R], d[R];
+  };
+  auto group_res = [&](int64_t grp, GRes &G) __attribute__((always_inline)) {
+    const bool live = grp < g_end;
 #pragma unroll
     for (int r = 0; r < R; ++r) {
       int64_t row = grp * R + r;
       row = row < n ? row : n - 1;  // tail rows are computed but not stored
-      const auto rq = rsrc(wdata + row * q_row, q_row);
-      const auto rs = rsrc(sbase + row * s_row, s_row);
-      const auto rd = rsrc(dbase + row * d_row, d_row);
-#pragma unroll
-      for (int s = 0; s < NS; ++s) {
-        const auto va = __builtin_amdgcn_raw_buffer_load_b128(rq, (int)qoff[s], 0, kNT);
-        const auto vb = __builtin_amdgcn_raw_buffer_load_b128(rq, (int)qoff[s] + 1024, 0, kNT);
-        const auto vc = __builtin_amdgcn_raw_buffer_load_b128(rq, (int)qoff[s] + 2048, 0, kNT);
-        S.a[s][r] = make_uint4(va[0], va[1], va[2], va[3]);
-        S.b[s][r] = make_uint4(vb[0], vb[1], vb[2], vb[3]);
-        S.c[s][r] = make_uint4(vc[0], vc[1], vc[2], vc[3]);
-        S.sc[s][r] = __builtin_amdgcn_raw_buffer_load_b32(rs, (int)soff[s], 0, kNT);
-        S.dh[s][r] = __builtin_amdgcn_raw_buffer_load_b16(rd, (int)doff[s], 0, kNT);
-      }
+      G.q[r] = rsrc(wdata + row * q_row, live ? q_row : 0u);
+      G.s[r] = rsrc(sbase + row * s_row, live ? s_row : 0u);
+      G.d[r] = rsrc(dbase + row * d_row, live ? d_row : 0u);
     }
   };
-  if (g < g_end) load_group(A, g);
-  if (PD >= 2 && g + gstride < g_end) load_group(B, g + gstride);
-  stage_x6<XT>(x, k, ku, xs, xoff, P, f.pro == EB_PRO_RMSNORM, f.gamma, f.eps, red);
+  auto load_item = [&](WSet &S, const GRes &G, int s, int r) __attribute__((always_inline)) {
+    const bool last = s == NS - 1;
+    const auto va = __builtin_amdgcn_raw_buffer_load_b128(G.q[r], (int)qbase, 3072 * s, kNT);
+    const auto vb = __builtin_amdgcn_raw_buffer_load_b128(G.q[r], (int)qbase, 3072 * s + 1024, kNT);
+    const auto vc = __builtin_amdgcn_raw_buffer_load_b128(G.q[r], (int)qbase, 3072 * s + 2048, kNT);
+    S.a[s][r] = make_uint4(va[0], va[1], va[2], va[3]);
+    S.b[s][r] = make_uint4(vb[0], vb[1], vb[2], vb[3]);
+    S.c[s][r] = make_uint4(vc[0], vc[1], vc[2], vc[3]);
+    S.sc[s][r] = __builtin_amdgcn_raw_buffer_load_b32(G.s[r], (int)(last ? slast : sbase_l), last ? 0 : 256 * s, kNT);
+    S.dh[s][r] = __builtin_amdgcn_raw_buffer_load_b16(G.d[r], (int)(last ? dlast : dbase_l), last ? 0 : 32 * s, kNT);
+  };
+  // x's loads first, then the first group's weights, which stay in flight
+  // while x is staged (and, with the prologue, normalised)
+  const bool norm = f.pro == EB_PRO_RMSNORM;
+  X6Regs xr;
+  x6_issue(x, ku, norm, f.gamma, xr);
+  __builtin_amdgcn_sched_barrier(0);
+  {
+    // in the order step consumes them, kept in that order (left to the
+    // scheduler, the scales would follow all the codes and the first item's
+    // wait would be a wait for the whole group)
+    GRes G;
+    group_res(g, G);
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        load_item(A, G, s, r);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  x6_finish<XT>(x, k, ku, xs, xoff, P, norm, f.gamma, f.eps, red, xr);
   if (threadIdx.x < kU6Parts) xs[threadIdx.x * P + 64 * NS] = make_uint4(0, 0, 0, 0);
   if (threadIdx.x < 4) xoff[4 * 64 * NS + threadIdx.x] = 0.f;
   __syncthreads();
 
-  auto step = [&](WSet &S) __attribute__((always_inline)) -> bool {
-    if (g >= g_end) return false;
+  // one group (g < g_end), computed from set S, whose items are reloaded
+  // with the next group's as they are used
+  auto step = [&](WSet &S) __attribute__((always_inline)) {
+    GRes G;
+    group_res(g + gstride, G);
     float acc[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) acc[r] = 0.f;
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
+      const uint32_t xi = s == NS - 1 ? xlast : (uint32_t)lane + 64u * s;
       uint4 xf[kU6Parts];
 #pragma unroll
-      for (int p = 0; p < kU6Parts; ++p) xf[p] = xs[p * P + xidx[s]];
+      for (int p = 0; p < kU6Parts; ++p) xf[p] = xs[p * P + xi];
       float4 xo = make_float4(0.f, 0.f, 0.f, 0.f);
-      if constexpr (XT == EB_BF16) xo = reinterpret_cast<const float4 *>(xoff)[xidx[s]];
+      if constexpr (XT == EB_BF16) xo = reinterpret_cast<const float4 *>(xoff)[xi];
 #pragma unroll
       for (int r = 0; r < R; ++r) {
         const float d = (float)__builtin_bit_cast(_Float16, S.dh[s][r]);
@@ -489,6 +561,8 @@ __device__ __attribute__((always_inline)) inline void q6_rows(
         acc[r] = __builtin_fmaf(d * (float)(int8_t)((sc >> 8) & 0xffu), s1, acc[r]);
         acc[r] = __builtin_fmaf(d * (float)(int8_t)((sc >> 16) & 0xffu), s2, acc[r]);
         acc[r] = __builtin_fmaf(d * (float)(int8_t)(sc >> 24), s3, acc[r]);
+        __builtin_amdgcn_sched_barrier(0);
+        load_item(S, G, s, r);
       }
     }
     int rr;
@@ -507,17 +581,9 @@ __device__ __attribute__((always_inline)) inline void q6_rows(
       if (writer && row < n) put_y(y, row, tot, yt, f);
     }
     g += gstride;
-    __builtin_amdgcn_sched_barrier(0);
-    if (g + (PD - 1) * gstride < g_end) load_group(S, g + (PD - 1) * gstride);
-    return true;
   };
-  if constexpr (PD == 2) {
-    while (step(A) && step(B)) {
-    }
-  } else {
-    while (step(A)) {
-    }
-  }
+  const int64_t cnt = g < g_end ? (g_end - g + gstride - 1) / gstride : 0;
+  for (int64_t i = 0; i < cnt; ++i) step(A);
 }
 
 // One matrix per launch: one workgroup per CU (x is staged, and normalised,
@@ -533,9 +599,7 @@ __global__ void __launch_bounds__(64 * WG) __attribute__((amdgpu_waves_per_eu(WG
                       int yt, Fuse f) {
   extern __shared__ uint4 smem[];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  // a second register set of weights in flight where it fits
-  constexpr int PD = NS == 1 ? 2 : 1;
-  q6_rows<XT, NS, R, PD>(wdata, n, k, sc_off, d_off, ds, x, y, yt, f, (int64_t)blockIdx.x * WG + wave,
+  q6_rows<XT, NS, R>(wdata, n, k, sc_off, d_off, ds, x, y, yt, f, (int64_t)blockIdx.x * WG + wave,
                          (n + R - 1) / R, (int64_t)gridDim.x * WG, smem);
 }
 
@@ -568,7 +632,7 @@ __global__ void __launch_bounds__(64 * kQ6MultiWaves) __attribute__((amdgpu_wave
     };
     const int64_t r0 = row_at(u0), r1 = row_at(u1);
     if (r0 >= r1) continue;  // uniform across the workgroup
-    q6_rows<XT, NS, R, 1>(o.w, o.n, o.k, o.sc_off, o.d_off, o.ds, o.x, o.y, o.yt, o.f, r0 / R + wave,
+    q6_rows<XT, NS, R>(o.w, o.n, o.k, o.sc_off, o.d_off, o.ds, o.x, o.y, o.yt, o.f, r0 / R + wave,
                           (r1 + R - 1) / R, kQ6MultiWaves, smem);
     __syncthreads();  // the next matrix restages LDS
   }
