@@ -500,11 +500,25 @@ __global__ void __launch_bounds__(64 * kWaves)
 // instructions.
 // ---------------------------------------------------------------------------
 
+// Items in flight per wave for a group of `items` items: the largest divisor
+// of it up to `cap` (so that an item's register set is a compile-time
+// function of its index).  Lone launches cap it at 4: measured on the decode
+// chain's projections (1, 2, 4 and 6 items per group), 0.993 ms per pass
+// against 1.003 (cap 3), 1.002 (cap 2) and 1.017 (no cap; the 6-item down
+// projection 11% slower).  The fused multi-matrix kernel, whose workgroups
+// run many groups each, does not cap it (2% faster on its 6-slot matrices).
+constexpr int kM1Ring = 4;
+__host__ __device__ constexpr int m1_ring(int items, int cap) {
+  int d = items < cap ? items : cap;
+  while (items % d) --d;
+  return d;
+}
+
 // Rows g*R .. g*R+R-1 for groups g = g0, g0 + gstride, ... < g_end of one
 // matrix, m == 1.  Called by every thread of the workgroup (it stages x into
 // LDS and synchronises once); waves whose first group is past g_end only help
 // with the staging.
-template <int QT, int XT, int NS, int R>
+template <int QT, int XT, int NS, int R, int RING>
 __device__ __attribute__((always_inline)) inline void m1_rows(const uint8_t *__restrict__ wdata, int64_t n, int64_t k,
                                int64_t d_off, int64_t ds, const void *__restrict__ x,
                                void *__restrict__ y, int yt, const Fuse &f, int64_t g, int64_t g_end,
@@ -535,19 +549,21 @@ __device__ __attribute__((always_inline)) inline void m1_rows(const uint8_t *__r
   // slot s < NS - 1: code bytes at qbase + 1024 s, scale at dbase_l + dstep s
   constexpr uint32_t dstep = (QT == EB_Q4_0) ? 128u : 64u;
 
-  // One register set of weights, NS R items (slot s of row r: the lane's 16
-  // code bytes and their scale).  Each item is reloaded with the same item of
-  // the wave's next group right after it has been used, so a wave keeps one
-  // group of reads (NS R KiB) in flight without pauses while it decodes.
-  // Measured on the 32-layer decode chain: 1.02 ms per pass, against 1.16 ms
-  // with two sets reloaded this way and 1.14 ms with two sets reloaded after
-  // their group: with more reads queued, a set completes only when nearly
-  // all of them have arrived, and its decoding no longer overlaps the loads.
-  struct WSet {
-    uint4 q[NS][R];
-    uint16_t dh[NS][R];
+  // A ring of D register sets for the NS R items of a group (item i = slot
+  // s of row r, i = s R + r: the lane's 16 code bytes and their scale).
+  // Item i lives in set i % D; right after it has been used, its set is
+  // reloaded with item i + D, of this group or of the wave's next one.  A
+  // wave thus keeps D items (D KiB) of reads in flight without pauses while
+  // it decodes.  (Measured on the 32-layer decode chain: with two groups'
+  // items in flight instead of one, 1.16 against 1.02 ms per pass; with more
+  // reads queued, an item completes only when nearly all of them have
+  // arrived, and the decoding no longer overlaps the loads.)
+  constexpr int I = NS * R, D = m1_ring(I, RING);
+  struct Item {
+    uint4 q;
+    uint16_t dh;
   };
-  WSet A;
+  Item ring[D];
   // A group past g_end gets zero-sized buffer ranges: its loads return zeros
   // without a memory access.  Every load is therefore issued on every path:
   // a load issued on only some paths makes the compiler's counter wait for
@@ -566,28 +582,14 @@ __device__ __attribute__((always_inline)) inline void m1_rows(const uint8_t *__r
       G.d[r] = rsrc(dbase + row * d_row, live ? d_row : 0u);
     }
   };
-  // one item: slot s of row r (the lane's 16 code bytes and their scale)
-  auto load_item = [&](WSet &S, const GRes &G, int s, int r) __attribute__((always_inline)) {
+  auto load_item = [&](Item &it, const GRes &G, int i) __attribute__((always_inline)) {
+    const int s = i / R, r = i % R;
     const bool last = s == NS - 1;
     const auto v = __builtin_amdgcn_raw_buffer_load_b128(G.q[r], (int)(last ? qlast : qbase),
                                                          last ? 0 : 1024 * s, kNT);
-    S.q[s][r] = make_uint4(v[0], v[1], v[2], v[3]);
-    S.dh[s][r] = __builtin_amdgcn_raw_buffer_load_b16(G.d[r], (int)(last ? dlast : dbase_l),
-                                                      last ? 0 : (int)dstep * s, kNT);
-  };
-  // items in the order step consumes them (slot-major), kept in that order
-  // (left to the scheduler, the scales would follow all the codes and the
-  // first item's wait would be a wait for the whole group)
-  auto load_group = [&](WSet &S, int64_t grp) __attribute__((always_inline)) {
-    GRes G;
-    group_res(grp, G);
-#pragma unroll
-    for (int s = 0; s < NS; ++s)
-#pragma unroll
-      for (int r = 0; r < R; ++r) {
-        load_item(S, G, s, r);
-        __builtin_amdgcn_sched_barrier(0);
-      }
+    it.q = make_uint4(v[0], v[1], v[2], v[3]);
+    it.dh = __builtin_amdgcn_raw_buffer_load_b16(G.d[r], (int)(last ? dlast : dbase_l),
+                                                 last ? 0 : (int)dstep * s, kNT);
   };
   // Binary16 activations: their loads are issued first, then the weight
   // loads of the first group, which stay in flight while x is staged
@@ -597,8 +599,17 @@ __device__ __attribute__((always_inline)) inline void m1_rows(const uint8_t *__r
   X1Regs xr;
   if constexpr (XT == EB_F16) x1_issue<QT>(x, ku, norm, f.gamma, xr);
   __builtin_amdgcn_sched_barrier(0);
-  load_group(A, g);
-  __builtin_amdgcn_sched_barrier(0);
+  {
+    // kept in item order (left to the scheduler, the scales would follow all
+    // the codes and the first item's wait would be a wait for all of them)
+    GRes G;
+    group_res(g, G);
+#pragma unroll
+    for (int i = 0; i < D; ++i) {
+      load_item(ring[i], G, i);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
   if constexpr (XT == EB_F16) {
     x1_finish<QT>(x, k, ku, xs, P, norm, f.gamma, f.eps, xoff, xr);
   } else {
@@ -610,11 +621,11 @@ __device__ __attribute__((always_inline)) inline void m1_rows(const uint8_t *__r
   if (XT != EB_F16 && threadIdx.x == 0) xoff[64 * NS] = 0.f;
   __syncthreads();
 
-  // one group (g < g_end), computed from set S, whose items are reloaded
-  // with the next group's as they are used
-  auto step = [&](WSet &S) __attribute__((always_inline)) {
-    GRes G;
-    group_res(g + gstride, G);
+  // one group (g < g_end)
+  auto step = [&]() __attribute__((always_inline)) {
+    GRes Gc, Gn;
+    if constexpr (D < I) group_res(g, Gc);
+    group_res(g + gstride, Gn);
     float acc[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) acc[r] = 0.f;
@@ -628,10 +639,15 @@ __device__ __attribute__((always_inline)) inline void m1_rows(const uint8_t *__r
       const float xo = XT == EB_F16 ? 0.f : xoff[xi];
 #pragma unroll
       for (int r = 0; r < R; ++r) {
-        acc[r] = __builtin_fmaf((float)__builtin_bit_cast(_Float16, S.dh[s][r]),
-                                unit_dot<QT, XT>(S.q[s][r], xf, xo), acc[r]);
+        const int i = s * R + r;
+        Item &it = ring[i % D];
+        acc[r] = __builtin_fmaf((float)__builtin_bit_cast(_Float16, it.dh), unit_dot<QT, XT>(it.q, xf, xo),
+                                acc[r]);
         __builtin_amdgcn_sched_barrier(0);
-        load_item(S, G, s, r);
+        if (i + D < I)
+          load_item(it, Gc, i + D);
+        else
+          load_item(it, Gn, i + D - I);
       }
     }
     int rr;
@@ -656,7 +672,7 @@ __device__ __attribute__((always_inline)) inline void m1_rows(const uint8_t *__r
     g += gstride;
   };
   const int64_t cnt = g < g_end ? (g_end - g + gstride - 1) / gstride : 0;
-  for (int64_t i = 0; i < cnt; ++i) step(A);
+  for (int64_t i = 0; i < cnt; ++i) step();
 }
 
 // One matrix per launch.  WPE: minimum waves per SIMD the register allocation
@@ -673,7 +689,7 @@ __global__ void __launch_bounds__(64 * WG) __attribute__((amdgpu_waves_per_eu(WP
                    int64_t ds, const void *__restrict__ x, void *__restrict__ y, int yt, Fuse f) {
   extern __shared__ uint4 smem[];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
-  m1_rows<QT, XT, NS, R>(wdata, n, k, d_off, ds, x, y, yt, f,
+  m1_rows<QT, XT, NS, R, kM1Ring>(wdata, n, k, d_off, ds, x, y, yt, f,
                                                 (int64_t)blockIdx.x * WG + wave, (n + R - 1) / R,
                                                 (int64_t)gridDim.x * WG, smem);
 }
@@ -716,7 +732,7 @@ __global__ void __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_e
     };
     const int64_t r0 = row_at(u0), r1 = row_at(u1);
     if (r0 >= r1) continue;  // uniform across the workgroup
-    m1_rows<QT, XT, NS, R>(o.w, o.n, o.k, o.d_off, o.ds, o.x, o.y, o.yt, o.f, r0 / R + wave,
+    m1_rows<QT, XT, NS, R, NS * R>(o.w, o.n, o.k, o.d_off, o.ds, o.x, o.y, o.yt, o.f, r0 / R + wave,
                               (r1 + R - 1) / R, kWaves, smem);
     __syncthreads();  // the next matrix restages LDS
   }

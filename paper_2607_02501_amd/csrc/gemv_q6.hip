@@ -425,7 +425,16 @@ __host__ __device__ constexpr size_t q6_m1_lds(int ns, int waves) {
 // matrix, m == 1.  Called by every thread of the workgroup (it stages x into
 // LDS and synchronises once); waves whose first group is past g_end only help
 // with the staging.
-template <int XT, int NS, int R>
+// Items in flight per wave for a group of `items` items: the largest divisor
+// of it up to `cap`.
+__host__ __device__ constexpr int q6_ring(int items, int cap) {
+  int d = items < cap ? items : cap;
+  while (items % d) --d;
+  return d;
+}
+constexpr int kQ6Ring = 1;
+
+template <int XT, int NS, int R, int RING>
 __device__ __attribute__((always_inline)) inline void q6_rows(
     const uint8_t *__restrict__ wdata, int64_t n, int64_t k, int64_t sc_off, int64_t d_off,
     int64_t ds, const void *__restrict__ x, void *__restrict__ y, int yt, const Fuse &f, int64_t g,
@@ -455,20 +464,23 @@ __device__ __attribute__((always_inline)) inline void q6_rows(
   const uint32_t xlast = ul < ku ? (uint32_t)ul : 64u * NS;
   const uint32_t qbase = 16u * lane, sbase_l = 4u * lane, dbase_l = (uint32_t)(lane >> 2) * 2u;
 
-  // One register set of weights, NS R items (slot s of row r: 48 code bytes,
-  // 4 sub-scales and the super-block scale of the lane's unit).  Each item is
-  // reloaded with the same item of the wave's next group right after it has
-  // been used, so a wave keeps one group of reads in flight without pauses
-  // while it decodes.  A group past g_end gets zero-sized buffer ranges (its
-  // loads return zeros without a memory access), so every load is issued on
-  // every path: a load issued on only some paths makes the compiler's
-  // counter wait for an earlier load a wait for everything.
-  struct WSet {
-    uint4 a[NS][R], b[NS][R], c[NS][R];
-    uint32_t sc[NS][R];
-    uint16_t dh[NS][R];
+  // A ring of D register sets for the NS R items of a group (item i = slot
+  // s of row r, i = s R + r: 48 code bytes, 4 sub-scales and the super-block
+  // scale of the lane's unit; 3 KiB per wave).  Item i lives in set i % D;
+  // right after it has been used, its set is reloaded with item i + D, of
+  // this group or of the wave's next one, so a wave keeps D items of reads in
+  // flight without pauses while it decodes.  A group past g_end gets
+  // zero-sized buffer ranges (its loads return zeros without a memory
+  // access), so every load is issued on every path: a load issued on only
+  // some paths makes the compiler's counter wait for an earlier load a wait
+  // for everything.
+  constexpr int I = NS * R, D = q6_ring(I, RING);
+  struct Item {
+    uint4 a, b, c;
+    uint32_t sc;
+    uint16_t dh;
   };
-  WSet A;
+  Item ring[D];
   struct GRes {
     __amdgpu_buffer_rsrc_t q[R], s[R], d[R];
   };
@@ -483,16 +495,17 @@ __device__ __attribute__((always_inline)) inline void q6_rows(
       G.d[r] = rsrc(dbase + row * d_row, live ? d_row : 0u);
     }
   };
-  auto load_item = [&](WSet &S, const GRes &G, int s, int r) __attribute__((always_inline)) {
+  auto load_item = [&](Item &it, const GRes &G, int i) __attribute__((always_inline)) {
+    const int s = i / R, r = i % R;
     const bool last = s == NS - 1;
     const auto va = __builtin_amdgcn_raw_buffer_load_b128(G.q[r], (int)qbase, 3072 * s, kNT);
     const auto vb = __builtin_amdgcn_raw_buffer_load_b128(G.q[r], (int)qbase, 3072 * s + 1024, kNT);
     const auto vc = __builtin_amdgcn_raw_buffer_load_b128(G.q[r], (int)qbase, 3072 * s + 2048, kNT);
-    S.a[s][r] = make_uint4(va[0], va[1], va[2], va[3]);
-    S.b[s][r] = make_uint4(vb[0], vb[1], vb[2], vb[3]);
-    S.c[s][r] = make_uint4(vc[0], vc[1], vc[2], vc[3]);
-    S.sc[s][r] = __builtin_amdgcn_raw_buffer_load_b32(G.s[r], (int)(last ? slast : sbase_l), last ? 0 : 256 * s, kNT);
-    S.dh[s][r] = __builtin_amdgcn_raw_buffer_load_b16(G.d[r], (int)(last ? dlast : dbase_l), last ? 0 : 32 * s, kNT);
+    it.a = make_uint4(va[0], va[1], va[2], va[3]);
+    it.b = make_uint4(vb[0], vb[1], vb[2], vb[3]);
+    it.c = make_uint4(vc[0], vc[1], vc[2], vc[3]);
+    it.sc = __builtin_amdgcn_raw_buffer_load_b32(G.s[r], (int)(last ? slast : sbase_l), last ? 0 : 256 * s, kNT);
+    it.dh = __builtin_amdgcn_raw_buffer_load_b16(G.d[r], (int)(last ? dlast : dbase_l), last ? 0 : 32 * s, kNT);
   };
   // x's loads first, then the first group's weights, which stay in flight
   // while x is staged (and, with the prologue, normalised)
@@ -507,12 +520,10 @@ __device__ __attribute__((always_inline)) inline void q6_rows(
     GRes G;
     group_res(g, G);
 #pragma unroll
-    for (int s = 0; s < NS; ++s)
-#pragma unroll
-      for (int r = 0; r < R; ++r) {
-        load_item(A, G, s, r);
-        __builtin_amdgcn_sched_barrier(0);
-      }
+    for (int i = 0; i < D; ++i) {
+      load_item(ring[i], G, i);
+      __builtin_amdgcn_sched_barrier(0);
+    }
   }
   __builtin_amdgcn_sched_barrier(0);
   x6_finish<XT>(x, k, ku, xs, xoff, P, norm, f.gamma, f.eps, red, xr);
@@ -520,11 +531,11 @@ __device__ __attribute__((always_inline)) inline void q6_rows(
   if (threadIdx.x < 4) xoff[4 * 64 * NS + threadIdx.x] = 0.f;
   __syncthreads();
 
-  // one group (g < g_end), computed from set S, whose items are reloaded
-  // with the next group's as they are used
-  auto step = [&](WSet &S) __attribute__((always_inline)) {
-    GRes G;
-    group_res(g + gstride, G);
+  // one group (g < g_end)
+  auto step = [&]() __attribute__((always_inline)) {
+    GRes Gc, Gn;
+    if constexpr (D < I) group_res(g, Gc);
+    group_res(g + gstride, Gn);
     float acc[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) acc[r] = 0.f;
@@ -538,15 +549,17 @@ __device__ __attribute__((always_inline)) inline void q6_rows(
       if constexpr (XT == EB_BF16) xo = reinterpret_cast<const float4 *>(xoff)[xi];
 #pragma unroll
       for (int r = 0; r < R; ++r) {
-        const float d = (float)__builtin_bit_cast(_Float16, S.dh[s][r]);
-        const uint32_t sc = S.sc[s][r];
+        const int i = s * R + r;
+        Item &it = ring[i % D];
+        const float d = (float)__builtin_bit_cast(_Float16, it.dh);
+        const uint32_t sc = it.sc;
         // pieces l, l + 64, l + 128 of the wave's 3 KiB in, the lane's own
         // unit (pieces 3 l .. 3 l + 2) out; a wave's LDS operations complete
         // in order, so the reads see the writes and the next writes follow
         // the reads
-        wbuf[lane] = S.a[s][r];
-        wbuf[lane + 64] = S.b[s][r];
-        wbuf[lane + 128] = S.c[s][r];
+        wbuf[lane] = it.a;
+        wbuf[lane + 64] = it.b;
+        wbuf[lane + 128] = it.c;
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
@@ -562,7 +575,10 @@ __device__ __attribute__((always_inline)) inline void q6_rows(
         acc[r] = __builtin_fmaf(d * (float)(int8_t)((sc >> 16) & 0xffu), s2, acc[r]);
         acc[r] = __builtin_fmaf(d * (float)(int8_t)(sc >> 24), s3, acc[r]);
         __builtin_amdgcn_sched_barrier(0);
-        load_item(S, G, s, r);
+        if (i + D < I)
+          load_item(it, Gc, i + D);
+        else
+          load_item(it, Gn, i + D - I);
       }
     }
     int rr;
@@ -583,7 +599,7 @@ __device__ __attribute__((always_inline)) inline void q6_rows(
     g += gstride;
   };
   const int64_t cnt = g < g_end ? (g_end - g + gstride - 1) / gstride : 0;
-  for (int64_t i = 0; i < cnt; ++i) step(A);
+  for (int64_t i = 0; i < cnt; ++i) step();
 }
 
 // One matrix per launch: one workgroup per CU (x is staged, and normalised,
@@ -599,7 +615,7 @@ __global__ void __launch_bounds__(64 * WG) __attribute__((amdgpu_waves_per_eu(WG
                       int yt, Fuse f) {
   extern __shared__ uint4 smem[];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  q6_rows<XT, NS, R>(wdata, n, k, sc_off, d_off, ds, x, y, yt, f, (int64_t)blockIdx.x * WG + wave,
+  q6_rows<XT, NS, R, kQ6Ring>(wdata, n, k, sc_off, d_off, ds, x, y, yt, f, (int64_t)blockIdx.x * WG + wave,
                          (n + R - 1) / R, (int64_t)gridDim.x * WG, smem);
 }
 
@@ -632,7 +648,7 @@ __global__ void __launch_bounds__(64 * kQ6MultiWaves) __attribute__((amdgpu_wave
     };
     const int64_t r0 = row_at(u0), r1 = row_at(u1);
     if (r0 >= r1) continue;  // uniform across the workgroup
-    q6_rows<XT, NS, R>(o.w, o.n, o.k, o.sc_off, o.d_off, o.ds, o.x, o.y, o.yt, o.f, r0 / R + wave,
+    q6_rows<XT, NS, R, NS * R>(o.w, o.n, o.k, o.sc_off, o.d_off, o.ds, o.x, o.y, o.yt, o.f, r0 / R + wave,
                           (r1 + R - 1) / R, kQ6MultiWaves, smem);
     __syncthreads();  // the next matrix restages LDS
   }
