@@ -479,6 +479,18 @@ __global__ void __launch_bounds__(64 * kWaves)
 #pragma unroll
       for (int s = 0; s < RS; ++s) {
         const int64_t r = it * kRowsPerItem + s * kRowsPerSet + rsub;
+        if (f.epi == EB_EPI_ADD) {  // the row's residuals read together
+          // offsets from the item's first row (the same in every lane)
+          const int64_t b0 = it * kRowsPerItem;
+          uint32_t rel[MT];
+          bool ok[MT];
+#pragma unroll
+          for (int mm = 0; mm < MT; ++mm) {
+            rel[mm] = (uint32_t)mm * (uint32_t)n + (uint32_t)(r - b0);
+            ok[mm] = mm < m && r < n;
+          }
+          if (put_y_add(y, f.r, b0, (int64_t)(m - 1) * n + kRowsPerItem, rel, ok, acc[s], yt)) continue;
+        }
         if (r >= n) continue;
 #pragma unroll
         for (int mm = 0; mm < MT; ++mm) {

@@ -182,6 +182,20 @@ __global__ void __launch_bounds__(kThreads)
 #pragma unroll
       for (int o = 32; o >= 1; o >>= 1) acc[rr][mm] += __shfl_xor(acc[rr][mm], o);
   if (lane != 0) return;
+  if (f.epi == EB_EPI_ADD) {  // the residuals read together
+    uint32_t rel[2 * MT];
+    bool ok[2 * MT];
+    float v[2 * MT];
+#pragma unroll
+    for (int mm = 0; mm < MT; ++mm)
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        rel[2 * mm + t] = (uint32_t)mm * (uint32_t)n + t;
+        ok[2 * mm + t] = mm < m && (t == 0 || two);
+        v[2 * mm + t] = acc[t][mm];
+      }
+    if (put_y_add(y, f.r, r0, (int64_t)(m - 1) * n + 2, rel, ok, v, yt)) return;
+  }
   for (int mm = 0; mm < MT && mm < m; ++mm) {
     if (f.epi == EB_EPI_GLU) {  // n even: rows r0, r0 + 1 are a gate/up pair
       store_y(y, (int64_t)mm * (n / 2) + pair, silu_mul(acc[0][mm], acc[1][mm]), yt);

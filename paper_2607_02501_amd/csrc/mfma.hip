@@ -70,8 +70,16 @@ __global__ void __launch_bounds__(256)
   }
   if (f.epi == EB_EPI_GLU) {
     for (int t = 0; t + 1 < e; t += 2) store_y(y, (i + t) / 2, silu_mul(a[t], a[t + 1]), yt);
+  } else if (f.epi == EB_EPI_ADD) {  // the residuals read together
+    // offsets from the workgroup's first element (the same in every lane)
+    const int64_t b0 = (int64_t)blockIdx.x * 1024;
+    const int64_t span = count - b0 < 1024 ? count - b0 : 1024;
+    const uint32_t t0 = (uint32_t)(i - b0);
+    const uint32_t rel[4] = {t0, t0 + 1, t0 + 2, t0 + 3};
+    const bool ok[4] = {true, e > 1, e > 2, e > 3};
+    put_y_add(y, f.r, b0, span, rel, ok, a, yt);
   } else {
-    for (int t = 0; t < e; ++t) put_y(y, i + t, a[t], yt, f);
+    for (int t = 0; t < e; ++t) store_y(y, i + t, a[t], yt);
   }
 }
 

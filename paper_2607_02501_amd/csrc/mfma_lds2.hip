@@ -251,6 +251,44 @@ __global__ void __launch_bounds__(WAVES * 64)
       const uint32_t row = (uint32_t)m0 + i * 32 + (lane & 31);
 #pragma unroll
       for (int j = 0; j < FN; ++j) {
+        // the fragment's 16 residuals read before any output is written (an
+        // output reads only its own residual; one group after the other,
+        // each read would wait behind the previous write)
+        float res[4][4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) res[q][e] = 0.f;
+        if (add) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int cl = wave * 32 * FN + j * 32 + 8 * q + 4 * (int)wh;
+            const uint32_t base = (row * n + (uint32_t)n0 + cl) * YSZ;
+            if (packed) {
+              const uint32_t off = cl < rn ? base : 0x80000000u;
+              if constexpr (YT == EB_F32) {
+                const u32x4_t r = __builtin_amdgcn_raw_buffer_load_b128(rr, (int)off, 0, 0);
+                // element values: this compiler turns __builtin_bit_cast of a
+                // vector element into element 0 of the vector (one dword loaded)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) res[q][e] = __uint_as_float((uint32_t)r[e]);
+              } else {
+                const u32x2_t r = __builtin_amdgcn_raw_buffer_load_b64(rr, (int)off, 0, 0);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) res[q][e] = from_y16((uint16_t)(r[e >> 1] >> (16 * (e & 1))), yt);
+              }
+            } else {
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                const uint32_t off = cl + e < rn ? base + e * YSZ : 0x80000000u;
+                if constexpr (YT == EB_F32)
+                  res[q][e] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rr, (int)off, 0, 0));
+                else
+                  res[q][e] = from_y16(__builtin_amdgcn_raw_buffer_load_b16(rr, (int)off, 0, 0), yt);
+              }
+            }
+          }
+        }
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           const int cl = wave * 32 * FN + j * 32 + 8 * q + 4 * (int)wh;
@@ -289,11 +327,8 @@ __global__ void __launch_bounds__(WAVES * 64)
             const uint32_t off = cl < rn ? base : 0x80000000u;
             if constexpr (YT == EB_F32) {
               if (add) {
-                const u32x4_t r = __builtin_amdgcn_raw_buffer_load_b128(rr, (int)off, 0, 0);
-                // convert element values: this compiler turns __builtin_bit_cast of a
-                // vector element into element 0 of the vector (one dword loaded)
 #pragma unroll
-                for (int e = 0; e < 4; ++e) v[e] += __uint_as_float((uint32_t)r[e]);
+                for (int e = 0; e < 4; ++e) v[e] += res[q][e];
               }
               u32x4_t w;
 #pragma unroll
@@ -301,10 +336,8 @@ __global__ void __launch_bounds__(WAVES * 64)
               __builtin_amdgcn_raw_buffer_store_b128(w, yr, (int)off, 0, 0);
             } else {
               if (add) {
-                const u32x2_t r = __builtin_amdgcn_raw_buffer_load_b64(rr, (int)off, 0, 0);
 #pragma unroll
-                for (int e = 0; e < 4; ++e)
-                  v[e] += from_y16((uint16_t)(r[e >> 1] >> (16 * (e & 1))), yt);
+                for (int e = 0; e < 4; ++e) v[e] += res[q][e];
               }
               u32x2_t w;
 #pragma unroll
@@ -316,14 +349,11 @@ __global__ void __launch_bounds__(WAVES * 64)
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
               const uint32_t off = cl + e < rn ? base + e * YSZ : 0x80000000u;
-              if constexpr (YT == EB_F32) {
-                if (add)
-                  v[e] += __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rr, (int)off, 0, 0));
+              if (add) v[e] += res[q][e];
+              if constexpr (YT == EB_F32)
                 __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v[e]), yr, (int)off, 0, 0);
-              } else {
-                if (add) v[e] += from_y16(__builtin_amdgcn_raw_buffer_load_b16(rr, (int)off, 0, 0), yt);
+              else
                 __builtin_amdgcn_raw_buffer_store_b16(to_y16(v[e], yt), yr, (int)off, 0, 0);
-              }
             }
           }
         }

@@ -220,6 +220,22 @@ __global__ void __launch_bounds__(256)
         const uint32_t col = glu ? ((uint32_t)n0 + cl) / 2 : (uint32_t)n0 + cl;
         const bool keep = cl < rn && (!glu || (cl & 1) == 0);
         const uint32_t base = keep ? (row0 * nout + col) * YSZ : 0x80000000u;
+        // the 16 residuals read before any output is written (an output
+        // reads only its own residual; element by element, each read would
+        // wait behind the previous write)
+        float res[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) res[r] = 0.f;
+        if (add) {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const uint32_t off = base + (uint32_t)(8 * (r >> 2) + (r & 3)) * nout * YSZ;
+            if constexpr (YT == EB_F32)
+              res[r] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rr, (int)off, 0, 0));
+            else
+              res[r] = from_y16(__builtin_amdgcn_raw_buffer_load_b16(rr, (int)off, 0, 0), yt);
+          }
+        }
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const uint32_t off = base + (uint32_t)(8 * (r >> 2) + (r & 3)) * nout * YSZ;
@@ -229,10 +245,7 @@ __global__ void __launch_bounds__(256)
                 float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, true));
             v = silu_mul(v, u);
           } else if (add) {
-            if constexpr (YT == EB_F32)
-              v += __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rr, (int)off, 0, 0));
-            else
-              v += from_y16(__builtin_amdgcn_raw_buffer_load_b16(rr, (int)off, 0, 0), yt);
+            v += res[r];
           }
           if constexpr (YT == EB_F32)
             __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), yr, (int)off, 0, 0);

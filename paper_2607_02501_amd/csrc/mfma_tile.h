@@ -469,6 +469,22 @@ __global__ void __launch_bounds__(WM *WN * 64)
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
       const int cl = wn * TN + j * 32 + (lane & 31);
+      // the fragment's 16 residuals read together (where the registers allow:
+      // not with 256 accumulators per lane)
+      if (FM * FN <= 8 && !ws && f.epi == EB_EPI_ADD) {
+        uint32_t rel[16];
+        bool ok[16];
+        float v[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int rl = wm * TM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+          rel[r] = (uint32_t)rl * (uint32_t)n + (uint32_t)cl;
+          ok[r] = cl < rows_n && rl < rows_m;
+          v[r] = acc[i][j][r];
+        }
+        // elements m0 n + n0 + rel, within the tile's rows_m rows of n
+        if (put_y_add(y, f.r, m0 * n + n0, (int64_t)rows_m * n, rel, ok, v, yt)) continue;
+      }
       if (cl >= rows_n) continue;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {

@@ -103,10 +103,12 @@ FUSIONS = [("rmsnorm", None), (None, "add"), (None, "glu"), ("rmsnorm", "glu"), 
     ("q4_0", torch.bfloat16, torch.float16)])
 def test_fused_single_calls(eb, oracle, pro, epi, qtype, xdtype, ydtype):
     """m = 1 (one-row GEMV kernel), m = 3 (general GEMV kernel), m = 20 and
-    m = 150 (tiled MFMA kernel, the latter with a split of k forced), on a
-    ragged shape: n = 198 (99 gate/up pairs), k = 1184 (37 blocks)."""
+    m = 150 (tiled MFMA kernel, with its own epilogue and with a split of k
+    forced, whose reduction applies the epilogue), on a ragged shape: n = 198
+    (99 gate/up pairs), k = 1184 (37 blocks)."""
     n, k = 198, 1184
-    for m, path, splits in ((1, "gemv", 0), (3, "gemv", 0), (20, "mfma", 0), (150, "mfma", 4)):
+    for m, path, splits in ((1, "gemv", 0), (3, "gemv", 0), (20, "mfma", 0), (150, "mfma", 1),
+                            (150, "mfma", 4)):
         c = Case(eb, 1000 + m, qtype, n, k, m, xdtype, pro, epi, ydtype)
         y = c.run(eb, path, splits=splits)
         torch.cuda.synchronize()
@@ -125,15 +127,18 @@ def test_glu_on_long_rows_uses_paired_rows(eb, oracle):
 
 
 def test_residual_in_place(eb, oracle):
-    """residual == y: the residual stream is updated in place, on both paths."""
-    for m, path in ((1, "gemv"), (40, "mfma")):
-        c = Case(eb, 1200 + m, "q8_0", 256, 512, m, torch.bfloat16, None, "add", torch.float32)
+    """residual == y: the residual stream is updated in place, on both paths
+    (m = 150: the tile kernel's own epilogue, and with a split of k its
+    reduction's)."""
+    for m, path, splits in ((1, "gemv", 0), (3, "gemv", 0), (40, "mfma", 0), (150, "mfma", 1),
+                            (150, "mfma", 3)):
+        c = Case(eb, 1200 + m + splits, "q8_0", 256, 512, m, torch.bfloat16, None, "add", torch.float32)
         h = c.rd.clone()
         eb.qlinear_fused(c.qw, c.xd, out_dtype=torch.float32, epilogue="add", residual=h, out=h,
-                         path=path)
+                         path=path, splits=splits)
         torch.cuda.synchronize()
         y_ref, scale = c.reference(oracle)
-        assert_fused(h, y_ref, scale, f"fused_inplace m={m} {path}")
+        assert_fused(h, y_ref, scale, f"fused_inplace m={m} {path} splits={splits}")
 
 
 def test_zero_stream_and_zero_weights(eb):
