@@ -106,8 +106,8 @@ Fuse fuse_of(const eb_qlinear_op &o) {
   f.gamma = o.prologue == EB_PRO_RMSNORM ? o.norm_weight : nullptr;
   f.r = o.epilogue == EB_EPI_ADD ? o.residual : nullptr;
   f.eps = o.norm_eps;
-  f.pro = (int16_t)o.prologue;
-  f.epi = (int16_t)o.epilogue;
+  f.pro = o.prologue;
+  f.epi = o.epilogue;
   return f;
 }
 

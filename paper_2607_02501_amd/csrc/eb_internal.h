@@ -60,11 +60,17 @@ inline int64_t canonical_block_bytes(int32_t type) {
 // kernels read activations normalised beforehand by launch_rmsnorm and only
 // apply the epilogue.  `r` is the residual of EB_EPI_ADD ([m][n] of the
 // output type, possibly the output itself).
+// pro and epi are whole dwords: kernels that read an op's Fuse from a
+// table in device memory then get them by scalar loads, whereas a 16-bit
+// field takes a vector load, whose wait also waits for every vector load
+// issued before it (the next tile's prefetch in the persistent kernels; no
+// measurable change on the action-expert and VLM passes, which run few tiles
+// per workgroup).
 struct Fuse {
   const float *gamma;
   const void *r;
   float eps;
-  int16_t pro, epi;
+  int32_t pro, epi;
 };
 
 // ---- launchers (each returns hipSuccess or the launch error) ----
