@@ -526,15 +526,28 @@ __host__ __device__ constexpr int m1_ring(int items, int cap) {
   return d;
 }
 
-// Rows g*R .. g*R+R-1 for groups g = g0, g0 + gstride, ... < g_end of one
-// matrix, m == 1.  Called by every thread of the workgroup (it stages x into
-// LDS and synchronises once); waves whose first group is past g_end only help
-// with the staging.
+// Rows g*R .. g*R+R-1 for the wave's groups g in [gbase, g_end) of one
+// matrix, m == 1: gbase + vb, + gstride, ... in the whole rounds of gstride
+// groups, and gbase + (whole rounds) gstride + vw in the last, partial one
+// (vb and vw number the gstride waves; callers that pass vb == vw walk
+// gbase + vb + i gstride).  Called by every thread of the workgroup (it stages
+// x into LDS and synchronises once); waves without a group only help with the
+// staging.
 template <int QT, int XT, int NS, int R, int RING>
 __device__ __attribute__((always_inline)) inline void m1_rows(const uint8_t *__restrict__ wdata, int64_t n, int64_t k,
                                int64_t d_off, int64_t ds, const void *__restrict__ x,
-                               void *__restrict__ y, int yt, const Fuse &f, int64_t g, int64_t g_end,
-                               int64_t gstride, uint4 *smem) {
+                               void *__restrict__ y, int yt, const Fuse &f, int64_t gbase, int64_t vb,
+                               int64_t vw, int64_t g_end, int64_t gstride, uint4 *smem) {
+  // The wave's groups: gbase + vb + i gstride in the whole rounds i < full,
+  // then, in the last, partial round, gbase + full gstride + vw (a numbering
+  // that spreads that round's groups over the compute units; past the end:
+  // g_end, a dead group).
+  const int64_t full = (g_end - gbase) / gstride, rem = g_end - gbase - full * gstride;
+  const int64_t cnt = full + (vw < rem ? 1 : 0);
+  auto grp = [&](int64_t i) __attribute__((always_inline)) {
+    return i < full ? gbase + vb + i * gstride : (i == full && vw < rem ? gbase + full * gstride + vw : g_end);
+  };
+  int64_t g = grp(0), gnext = g_end;
   constexpr int CH = Unit<QT>::kChunks;
   // LDS: CH chunk rows of P entries; entry 64 * NS of every row is zero and
   // stands in for units past the end of the row.  P is a compile-time
@@ -637,7 +650,7 @@ __device__ __attribute__((always_inline)) inline void m1_rows(const uint8_t *__r
   auto step = [&]() __attribute__((always_inline)) {
     GRes Gc, Gn;
     if constexpr (D < I) group_res(g, Gc);
-    group_res(g + gstride, Gn);
+    group_res(gnext, Gn);
     float acc[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) acc[r] = 0.f;
@@ -681,10 +694,12 @@ __device__ __attribute__((always_inline)) inline void m1_rows(const uint8_t *__r
     } else {
       if (writer && row < n) put_y(y, row, tot, yt, f);
     }
-    g += gstride;
   };
-  const int64_t cnt = g < g_end ? (g_end - g + gstride - 1) / gstride : 0;
-  for (int64_t i = 0; i < cnt; ++i) step();
+  for (int64_t i = 0; i < cnt; ++i) {
+    g = grp(i);
+    gnext = grp(i + 1);
+    step();
+  }
 }
 
 // One matrix per launch.  WPE: minimum waves per SIMD the register allocation
@@ -701,9 +716,14 @@ __global__ void __launch_bounds__(64 * WG) __attribute__((amdgpu_waves_per_eu(WP
                    int64_t ds, const void *__restrict__ x, void *__restrict__ y, int yt, Fuse f) {
   extern __shared__ uint4 smem[];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
-  m1_rows<QT, XT, NS, R, kM1Ring>(wdata, n, k, d_off, ds, x, y, yt, f,
-                                                (int64_t)blockIdx.x * WG + wave, (n + R - 1) / R,
-                                                (int64_t)gridDim.x * WG, smem);
+  // Group numbering: the whole rounds block-major (a compute unit's waves
+  // take neighbouring rows), the last, partial round wave-major, so that its
+  // groups spread over every compute unit instead of filling the first ones
+  // (the decode layer's 11008 gate/up pairs over 4096 waves: 43-44 groups per
+  // CU instead of 48 on 176 CUs and 32 on the rest).
+  m1_rows<QT, XT, NS, R, kM1Ring>(wdata, n, k, d_off, ds, x, y, yt, f, 0,
+                                  (int64_t)blockIdx.x * WG + wave, (int64_t)wave * gridDim.x + blockIdx.x,
+                                  (n + R - 1) / R, (int64_t)gridDim.x * WG, smem);
 }
 
 // Rows per wave for the fused multi-matrix kernel, by slot count (no spills
@@ -744,7 +764,7 @@ __global__ void __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_e
     };
     const int64_t r0 = row_at(u0), r1 = row_at(u1);
     if (r0 >= r1) continue;  // uniform across the workgroup
-    m1_rows<QT, XT, NS, R, NS * R>(o.w, o.n, o.k, o.d_off, o.ds, o.x, o.y, o.yt, o.f, r0 / R + wave,
+    m1_rows<QT, XT, NS, R, NS * R>(o.w, o.n, o.k, o.d_off, o.ds, o.x, o.y, o.yt, o.f, r0 / R, wave, wave,
                               (r1 + R - 1) / R, kWaves, smem);
     __syncthreads();  // the next matrix restages LDS
   }
