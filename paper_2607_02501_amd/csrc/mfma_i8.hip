@@ -245,20 +245,7 @@ __global__ void __launch_bounds__(256)
   for (int j = 0; j < 2; ++j) {
     const int cl = 64 * wn + 32 * j + r;
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      if (f.epi == EB_EPI_ADD) {  // the fragment's 16 residuals read together
-        uint32_t rel[16];
-        bool ok[16];
-        float v[16];
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int rl = 64 * wm + 32 * i + 8 * (e >> 2) + 4 * h + (e & 3);
-          rel[e] = (uint32_t)rl * (uint32_t)n + (uint32_t)cl;
-          ok[e] = rl < rows_m && cl < rows_n;
-          v[e] = acc[i][j][e];
-        }
-        if (put_y_add(y, f.r, m0 * n + n0, (int64_t)rows_m * n, rel, ok, v, yt)) continue;
-      }
+    for (int i = 0; i < 2; ++i)
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         const int rl = 64 * wm + 32 * i + 8 * (e >> 2) + 4 * h + (e & 3);
@@ -271,7 +258,6 @@ __global__ void __launch_bounds__(256)
         }
         if (rl < rows_m && cl < rows_n) put_y(y, (m0 + rl) * n + n0 + cl, v, yt, f);
       }
-    }
   }
 }
 
