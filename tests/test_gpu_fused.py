@@ -126,6 +126,23 @@ def test_glu_on_long_rows_uses_paired_rows(eb, oracle):
     assert_fused(y, y_ref, scale, "fused_glu_long m=1")
 
 
+@pytest.mark.parametrize("qtype", ["q4_0", "q8_0", "q6_s"])
+@pytest.mark.parametrize("pro,epi", [(None, None), ("rmsnorm", "glu"), (None, "add")])
+def test_m1_lone_launch_partial_last_round(eb, oracle, qtype, pro, epi):
+    """Lone m = 1 launches with more row groups than waves (one 16-wave
+    workgroup per compute unit, 4096 waves on 256 CUs): 9426 rows are two
+    whole rounds of one-row groups and a partial third, or one whole round of
+    gate/up pairs and a partial second; the partial round's groups are
+    numbered differently from the whole rounds'.  k = 256: one unit slot per
+    lane."""
+    n, k = 9426, 256
+    c = Case(eb, 1300, qtype, n, k, 1, torch.float16, pro, epi, torch.float32)
+    y = c.run(eb, "gemv")
+    torch.cuda.synchronize()
+    y_ref, scale = c.reference(oracle)
+    assert_fused(y, y_ref, scale, f"m1_lone_rounds {qtype} {pro} {epi}")
+
+
 def test_residual_in_place(eb, oracle):
     """residual == y: the residual stream is updated in place, on both paths
     (m = 150: the tile kernel's own epilogue, and with a split of k its
