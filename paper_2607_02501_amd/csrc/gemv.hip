@@ -728,8 +728,9 @@ __global__ void __launch_bounds__(64 * WG) __attribute__((amdgpu_waves_per_eu(WP
 
 // Rows per wave for the fused multi-matrix kernel, by slot count (no spills
 // at 4 waves per SIMD).
-// (The one-matrix kernel uses the same rows per wave by default, so a fused
-// stack and single calls add in the same order and agree bitwise.)
+// (A row gets the same bits whatever the rows per wave: reduce_rows adds a
+// one-row wave's sums in the two-row order, so a fused stack and single calls,
+// one row per wave outside the gate/up pairs, agree bitwise.)
 __host__ __device__ constexpr int m1_multi_rows(int ns) { return ns <= 4 ? 2 : 1; }
 
 // Several independent matrices (m == 1, same formats, same slot count NS) in
