@@ -28,8 +28,9 @@ namespace {
 //    to one of two LDS stages at the end of the next step.  Steps without a
 //    scale load issue the same loads with an empty range (no memory access),
 //    so every step has the same number of vector-memory ops in flight.
-// One 256-thread workgroup per CU; wave w owns columns 64w..64w+63 of the
-// 64 x 256 tile and dequantizes its codes straight into MFMA registers, with
+// One workgroup of WAVES waves per CU (launched with 8); wave w owns the
+// 256 / WAVES columns from (256 / WAVES) w of the 64 x 256 tile and
+// dequantizes its codes straight into MFMA registers, with
 // the k order of mm_breg_kernel applied to each 64-wide half of the step.
 // The weights are the MFMA A operand, so y leaves in 4-column packed stores.
 // Chunk (16 B) swizzles keep the 16-lane phases of every LDS read on distinct
@@ -226,8 +227,9 @@ __global__ void __launch_bounds__(WAVES * 64)
   };
   zero_acc();
 
-  // lane (l, reg r) of sub-tile (i, j) holds y[m0 + 32 i + l % 32][n0 + 64 wave +
-  // 32 j + 8 (r / 4) + 4 (l / 32) + r % 4]; see mm_ldsw_kernel for the bounds.
+  // lane (l, reg r) of sub-tile (i, j) holds y[m0 + 32 i + l % 32][n0 + 32 FN wave
+  // + 32 j + 8 (r / 4) + 4 (l / 32) + r % 4]; rows past the op's m read zero x
+  // (x rows past the buffer) and columns past its n are not stored.
   //
   // Fused steps: the residual of EB_EPI_ADD is read with the same packed
   // accesses as the stores; with EB_EPI_GLU the four columns of a packed
