@@ -532,8 +532,10 @@ __host__ __device__ constexpr int m1_ring(int items, int cap) {
 // (vb and vw number the gstride waves; callers that pass vb == vw walk
 // gbase + vb + i gstride).  Called by every thread of the workgroup (it stages
 // x into LDS and synchronises once); waves without a group only help with the
-// staging.
-template <int QT, int XT, int NS, int R, int RING>
+// staging.  PRE (residual-adding ops with fp32 output, EB_EPI_ADD): the
+// residual of each lane's row is loaded before the group's weights, so the
+// epilogue does not wait a memory round trip for it after the reduction.
+template <int QT, int XT, int NS, int R, int RING, bool PRE = false>
 __device__ __attribute__((always_inline)) inline void m1_rows(const uint8_t *__restrict__ wdata, int64_t n, int64_t k,
                                int64_t d_off, int64_t ds, const void *__restrict__ x,
                                void *__restrict__ y, int yt, const Fuse &f, int64_t gbase, int64_t vb,
@@ -624,6 +626,24 @@ __device__ __attribute__((always_inline)) inline void m1_rows(const uint8_t *__r
   X1Regs xr;
   if constexpr (XT == EB_F16) x1_issue<QT>(x, ku, norm, f.gamma, xr);
   __builtin_amdgcn_sched_barrier(0);
+  // PRE: the fp32 residual of the row this lane's reduction ends in, for
+  // group grp (a group past g_end reads zero without a memory access).  The
+  // first group's is loaded before its weights, the next group's right after
+  // this group's output: either way it is older than every load issued while
+  // its group is decoded, so waiting for it never waits for those.
+  const uint32_t res_off = 4u * (uint32_t)reduce_row<R>(lane);
+  auto res_load = [&](int64_t grp) __attribute__((always_inline)) -> float {
+    const bool live = grp < g_end;
+    const int64_t r0 = live ? grp * R : 0;
+    const uint32_t bytes = live ? 4u * (uint32_t)min((int64_t)R, n - r0) : 0u;
+    const auto rs = rsrc(static_cast<const float *>(f.r) + r0, bytes);
+    return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, (int)res_off, 0, 0));
+  };
+  float res_cur = 0.f;
+  if constexpr (PRE) {
+    res_cur = res_load(g);
+    __builtin_amdgcn_sched_barrier(0);
+  }
   {
     // kept in item order (left to the scheduler, the scales would follow all
     // the codes and the first item's wait would be a wait for all of them)
@@ -679,10 +699,13 @@ __device__ __attribute__((always_inline)) inline void m1_rows(const uint8_t *__r
     bool writer;
     const float tot = reduce_rows<R>(acc, lane, rr, writer);
     const int64_t row = g * R + rr;
-    // (the add epilogue's wait for its residual also waits for the reloads
-    // just issued; a lone launch gives the decoder layer's residual-adding
-    // projections one group per wave, so those are zero-sized)
-    if constexpr (R >= 2) {
+    // (without PRE, the add epilogue's wait for its residual also waits for
+    // the reloads just issued)
+    if constexpr (PRE) {
+      // put_y's arithmetic: the fp32 sum, then the fp32 store
+      if (writer && row < n) store_y(y, row, tot + res_cur, EB_F32);
+      res_cur = res_load(gnext);
+    } else if constexpr (R >= 2) {
       if (f.epi == EB_EPI_GLU) {
         // the up row (odd) of a pair is held R/2 ... lanes away: 8 (R = 8),
         // 16 (R = 4) or 32 (R = 2) lanes, see reduce_rows
@@ -710,7 +733,7 @@ __device__ __attribute__((always_inline)) inline void m1_rows(const uint8_t *__r
 // waves per workgroup and one workgroup per CU it is done once per CU instead
 // of four times, and the 256 workgroups re-read the shared activations from
 // the L2 a quarter as often.
-template <int QT, int XT, int NS, int R, int WPE, int WG>
+template <int QT, int XT, int NS, int R, int WPE, int WG, bool PRE>
 __global__ void __launch_bounds__(64 * WG) __attribute__((amdgpu_waves_per_eu(WPE)))
     gemv_m1_kernel(const uint8_t *__restrict__ wdata, int64_t n, int64_t k, int64_t d_off,
                    int64_t ds, const void *__restrict__ x, void *__restrict__ y, int yt, Fuse f) {
@@ -721,7 +744,7 @@ __global__ void __launch_bounds__(64 * WG) __attribute__((amdgpu_waves_per_eu(WP
   // groups spread over every compute unit instead of filling the first ones
   // (the decode layer's 11008 gate/up pairs over 4096 waves: 43-44 groups per
   // CU instead of 48 on 176 CUs and 32 on the rest).
-  m1_rows<QT, XT, NS, R, kM1Ring>(wdata, n, k, d_off, ds, x, y, yt, f, 0,
+  m1_rows<QT, XT, NS, R, kM1Ring, PRE>(wdata, n, k, d_off, ds, x, y, yt, f, 0,
                                   (int64_t)blockIdx.x * WG + wave, (int64_t)wave * gridDim.x + blockIdx.x,
                                   (n + R - 1) / R, (int64_t)gridDim.x * WG, smem);
 }
@@ -772,7 +795,7 @@ __global__ void __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_e
 }
 
 // ---------------------------------------------------------------------------
-template <int QT, int XT, int NS, int R, int WPE, int WG>
+template <int QT, int XT, int NS, int R, int WPE, int WG, bool PRE = false>
 hipError_t launch_m1_t(const void *wdata, int64_t n, int64_t k, const void *x, void *y, int32_t yt,
                        const Fuse &f, hipStream_t s, int wg_per_cu) {
   const Layout L = layout_of(QT, n, k);
@@ -781,7 +804,7 @@ hipError_t launch_m1_t(const void *wdata, int64_t n, int64_t k, const void *x, v
   int64_t grid = (groups + WG - 1) / WG;
   const int64_t cap = (int64_t)device_cu_count() * wg_per_cu;
   if (grid > cap) grid = cap;
-  gemv_m1_kernel<QT, XT, NS, R, WPE, WG><<<(unsigned)grid, 64 * WG, lds, s>>>(
+  gemv_m1_kernel<QT, XT, NS, R, WPE, WG, PRE><<<(unsigned)grid, 64 * WG, lds, s>>>(
       (const uint8_t *)wdata, n, k, L.d_off, L.ds, x, y, yt, f);
   return hipGetLastError();
 }
@@ -813,6 +836,11 @@ hipError_t launch_m1_ns(const void *wdata, int64_t n, int64_t k, const void *x, 
   // rows of a pair in one wave
   M1Shape v = m1_shape(NS);
   if (f.epi == EB_EPI_GLU && v.r < 2) v.r = 2;
+  // residual-adding ops with fp32 output (the decoder layer's O and down
+  // projections on the residual stream) in the default shape preload their
+  // residuals
+  if (f.epi == EB_EPI_ADD && yt == EB_F32 && v.r == 1 && v.wpe == 4 && v.waves == 16)
+    return launch_m1_t<QT, XT, NS, 1, 4, 16, true>(wdata, n, k, x, y, yt, f, s, v.wg);
 #define EB_M1(R_, W_, G_)                                                                  \
   if (v.r == R_ && v.wpe == W_ && v.waves == G_)                                          \
     return launch_m1_t<QT, XT, NS, R_, W_, G_>(wdata, n, k, x, y, yt, f, s, v.wg);

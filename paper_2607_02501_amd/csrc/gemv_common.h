@@ -90,8 +90,18 @@ __device__ inline float half8(float a, float b, int lane) {
   return keep + dpp<0x128>(send);  // row_ror:8
 }
 
+// The row whose total reduce_rows<R> returns in `lane`.
+template <int R>
+__device__ inline int reduce_row(int lane) {
+  if constexpr (R == 8) return ((lane >> 3) & 1) + 2 * ((lane >> 4) & 1) + 4 * (lane >> 5);
+  if constexpr (R == 4) return ((lane >> 4) & 1) + 2 * (lane >> 5);
+  if constexpr (R == 2) return lane >> 5;
+  return 0;
+}
+
 // Reduce v[0..R) over the 64 lanes.  Returns the total of row `row` (a
-// function of the lane) in every lane; `writer` marks one lane per row.
+// function of the lane, reduce_row<R>) in every lane; `writer` marks one lane
+// per row.
 template <int R>
 __device__ inline float reduce_rows(const float (&v)[R], int lane, int &row, bool &writer) {
   if constexpr (R == 8) {
@@ -99,19 +109,19 @@ __device__ inline float reduce_rows(const float (&v)[R], int lane, int &row, boo
           a3 = swap32(v[3], v[7]);
     float b0 = swap16(a0, a2), b1 = swap16(a1, a3);
     float c = red8(half8(b0, b1, lane));
-    row = ((lane >> 3) & 1) + 2 * ((lane >> 4) & 1) + 4 * (lane >> 5);
+    row = reduce_row<R>(lane);
     writer = (lane & 7) == 0;
     return c;
   } else if constexpr (R == 4) {
     float a0 = swap32(v[0], v[2]), a1 = swap32(v[1], v[3]);
     float b = red16(swap16(a0, a1));
-    row = ((lane >> 4) & 1) + 2 * (lane >> 5);
+    row = reduce_row<R>(lane);
     writer = (lane & 15) == 0;
     return b;
   } else if constexpr (R == 2) {
     float a = red16(swap32(v[0], v[1]));
     a = swap16(a, a);
-    row = lane >> 5;
+    row = reduce_row<R>(lane);
     writer = (lane & 31) == 0;
     return a;
   } else {
@@ -120,7 +130,7 @@ __device__ inline float reduce_rows(const float (&v)[R], int lane, int &row, boo
     // the same bits for a row
     float a = red16(swap32(v[0], v[0]));
     a = swap16(a, a);
-    row = 0;
+    row = reduce_row<R>(lane);
     writer = lane == 0;
     return a;
   }
