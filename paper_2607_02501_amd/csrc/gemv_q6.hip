@@ -451,7 +451,9 @@ __host__ __device__ constexpr int q6_ring(int items, int cap) {
 }
 constexpr int kQ6Ring = 1;
 
-template <int XT, int NS, int R, int RING>
+// PRE (residual-adding ops with fp32 output): each lane's row residual is
+// loaded before the group's weights, as in m1_rows.
+template <int XT, int NS, int R, int RING, bool PRE = false>
 __device__ __attribute__((always_inline)) inline void q6_rows(
     const uint8_t *__restrict__ wdata, int64_t n, int64_t k, int64_t sc_off, int64_t d_off,
     int64_t ds, const void *__restrict__ x, void *__restrict__ y, int yt, const Fuse &f, int64_t gbase,
@@ -540,6 +542,22 @@ __device__ __attribute__((always_inline)) inline void q6_rows(
   X6Regs xr;
   x6_issue(x, ku, norm, f.gamma, xr);
   __builtin_amdgcn_sched_barrier(0);
+  // PRE: the first group's residual before its weights, each next group's
+  // right after this group's output (older than every load issued while its
+  // group is decoded); a group past g_end reads zero without a memory access
+  const uint32_t res_off = 4u * (uint32_t)reduce_row<R>(lane);
+  auto res_load = [&](int64_t grp) __attribute__((always_inline)) -> float {
+    const bool live = grp < g_end;
+    const int64_t r0 = live ? grp * R : 0;
+    const uint32_t bytes = live ? 4u * (uint32_t)min((int64_t)R, n - r0) : 0u;
+    const auto rs = rsrc(static_cast<const float *>(f.r) + r0, bytes);
+    return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, (int)res_off, 0, 0));
+  };
+  float res_cur = 0.f;
+  if constexpr (PRE) {
+    res_cur = res_load(g);
+    __builtin_amdgcn_sched_barrier(0);
+  }
   {
     // in the order step consumes them, kept in that order (left to the
     // scheduler, the scales would follow all the codes and the first item's
@@ -612,7 +630,11 @@ __device__ __attribute__((always_inline)) inline void q6_rows(
     bool writer;
     const float tot = reduce_rows<R>(acc, lane, rr, writer);
     const int64_t row = g * R + rr;
-    if constexpr (R >= 2) {
+    if constexpr (PRE) {
+      // put_y's arithmetic: the fp32 sum, then the fp32 store
+      if (writer && row < n) store_y(y, row, tot + res_cur, EB_F32);
+      res_cur = res_load(gnext);
+    } else if constexpr (R >= 2) {
       if (f.epi == EB_EPI_GLU) {
         // the up row (odd) of a pair is held R/2 ... lanes away, see reduce_rows
         const float up = __shfl_xor(tot, R == 8 ? 8 : (R == 4 ? 16 : 32));
@@ -637,7 +659,7 @@ __device__ __attribute__((always_inline)) inline void q6_rows(
 // 3 slots, 4 slot-rows).
 __host__ __device__ constexpr int q6_m1_waves(int ns, int r) { return ns <= 3 && ns * r <= 4 ? 16 : 8; }
 
-template <int XT, int NS, int R, int WG>
+template <int XT, int NS, int R, int WG, bool PRE>
 __global__ void __launch_bounds__(64 * WG) __attribute__((amdgpu_waves_per_eu(WG / 4)))
     gemv_q6_m1_kernel(const uint8_t *__restrict__ wdata, int64_t n, int64_t k, int64_t sc_off,
                       int64_t d_off, int64_t ds, const void *__restrict__ x, void *__restrict__ y,
@@ -645,7 +667,7 @@ __global__ void __launch_bounds__(64 * WG) __attribute__((amdgpu_waves_per_eu(WG
   extern __shared__ uint4 smem[];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   // group numbering as in gemv_m1_kernel
-  q6_rows<XT, NS, R, kQ6Ring>(wdata, n, k, sc_off, d_off, ds, x, y, yt, f, 0,
+  q6_rows<XT, NS, R, kQ6Ring, PRE>(wdata, n, k, sc_off, d_off, ds, x, y, yt, f, 0,
                               (int64_t)blockIdx.x * WG + wave, (int64_t)wave * gridDim.x + blockIdx.x,
                               (n + R - 1) / R, (int64_t)gridDim.x * WG, smem);
 }
@@ -696,8 +718,11 @@ hipError_t launch_m1_ns(const void *wdata, int64_t n, int64_t k, const void *x, 
   const int64_t cap = (int64_t)device_cu_count();
   if (grid > cap) grid = cap;
   const size_t lds = q6_m1_lds(NS, wg);
-  auto kern = r == 2 ? gemv_q6_m1_kernel<XT, NS, 2, q6_m1_waves(NS, 2)>
-                     : gemv_q6_m1_kernel<XT, NS, 1, q6_m1_waves(NS, 1)>;
+  // residual-adding ops with fp32 output preload their residuals
+  const bool pre = f.epi == EB_EPI_ADD && yt == EB_F32;
+  auto kern = r == 2 ? gemv_q6_m1_kernel<XT, NS, 2, q6_m1_waves(NS, 2), false>
+                     : (pre ? gemv_q6_m1_kernel<XT, NS, 1, q6_m1_waves(NS, 1), true>
+                            : gemv_q6_m1_kernel<XT, NS, 1, q6_m1_waves(NS, 1), false>);
   if (lds > 64 * 1024) {
     hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
                                        (int)lds);
