@@ -517,7 +517,8 @@ __global__ void __launch_bounds__(64 * kWaves)
 // function of its index).  Lone launches cap it at 4: measured on the decode
 // chain's projections (1, 2, 4 and 6 items per group), 0.993 ms per pass
 // against 1.003 (cap 3), 1.002 (cap 2) and 1.017 (no cap; the 6-item down
-// projection 11% slower).  The fused multi-matrix kernel, whose workgroups
+// projection 11% slower, and still 6% slower with the first group split
+// around the staging of x).  The fused multi-matrix kernel, whose workgroups
 // run many groups each, does not cap it (2% faster on its 6-slot matrices).
 constexpr int kM1Ring = 4;
 __host__ __device__ constexpr int m1_ring(int items, int cap) {
