@@ -143,6 +143,30 @@ def test_m1_lone_launch_partial_last_round(eb, oracle, qtype, pro, epi):
     assert_fused(y, y_ref, scale, f"m1_lone_rounds {qtype} {pro} {epi}")
 
 
+@pytest.mark.parametrize("qtype,k,pro,epi", [
+    ("q4_0", 4096, "rmsnorm", "glu"),   # 2 slots x 2 rows: 4 items in flight
+    ("q4_0", 8192, None, None),         # 4 slots: 4 items
+    ("q4_0", 8192, None, "add"),
+    ("q4_0", 11008, None, "add"),       # 6 slots: 3 items
+    ("q4_0", 16384, "rmsnorm", None),   # 8 slots: 4 items
+    ("q8_0", 2048, "rmsnorm", "glu"),   # 2 slots x 2 rows
+    ("q8_0", 4096, None, "add"),        # 4 slots
+    ("q8_0", 8192, None, None),         # 8 slots
+])
+def test_m1_lone_launch_item_rings(eb, oracle, qtype, k, pro, epi):
+    """Lone m = 1 launches whose waves keep 3 or 4 items (1 KiB each) in flight
+    (part of the first group requested before x is staged, the rest after),
+    with more row groups than waves (4096 on 256 CUs), so that waves run the
+    group loop more than once; residual-adding ops with fp32 output read each
+    row's residual ahead of its weights."""
+    n = 9000 if epi == "glu" else 4200
+    c = Case(eb, 1400 + k // 32, qtype, n, k, 1, torch.float16, pro, epi, torch.float32)
+    y = c.run(eb, "gemv")
+    torch.cuda.synchronize()
+    y_ref, scale = c.reference(oracle)
+    assert_fused(y, y_ref, scale, f"m1_rings {qtype} k={k} {pro} {epi}")
+
+
 def test_residual_in_place(eb, oracle):
     """residual == y: the residual stream is updated in place, on both paths
     (m = 150: the tile kernel's own epilogue, and with a split of k its
