@@ -153,17 +153,21 @@ eb_status check_op(const eb_qlinear_op &o, int32_t path) {
 }
 
 // Path choice from the measured GEMV / MFMA crossover on MI355X (single ops
-// replayed from a graph, Q4_0 and Q8_0 at the decode / prefill / action-expert
-// shapes): the GEMV wins at m = 1 everywhere and at m = 2..4 unless the matrix
-// has few rows (n = 1024 loses); from m = 5 the MFMA path wins or loses by at
-// most 20%, so it is taken for every m >= 5.
+// without a workspace, replayed from a graph; Q4_0 and Q8_0 at the decode /
+// prefill / action-expert shapes): the GEMV wins at m = 1 everywhere; at
+// m = 2..4 when the matrix has 4096 rows or more (with 1024 or 2048 the
+// matrix cores win by 20-55%); at m = 5..8 where, in addition, the narrow
+// matrix-core kernel does not apply (k > 2048: the unsplit tile kernel loses
+// by 5-30%; the narrow kernel wins by 15-50%, or ties within 2%).
 // Q6_S: its GEMV up to m = 4, its matrix-core kernel beyond.
 int32_t pick_path(int32_t type, int32_t xt, int64_t m, int64_t n, int64_t k) {
   (void)xt;
   if (type == EB_Q6_S) return m <= 4 && gemv_q6_fits(m, n, k) ? EB_PATH_GEMV : EB_PATH_MFMA;
   if (!gemv_fits(m, k)) return EB_PATH_MFMA;
   if (m == 1) return EB_PATH_GEMV;
-  return (m <= 4 && n >= 2048) ? EB_PATH_GEMV : EB_PATH_MFMA;
+  if (n < 4096) return EB_PATH_MFMA;
+  if (m <= 4) return EB_PATH_GEMV;
+  return narrow_fits(m, n, k, 1) ? EB_PATH_MFMA : EB_PATH_GEMV;
 }
 
 // Bytes of normalised activations an op on the MFMA path needs (256-aligned).

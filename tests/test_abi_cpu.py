@@ -389,11 +389,17 @@ def test_auto_path(eb):
     assert f(eb.EB_Q8_0, eb.EB_BF16, 816, 2560, 2048) == eb.EB_PATH_MFMA
     assert f(eb.EB_Q8_0, eb.EB_BF16, 50, 2048, 1024) == eb.EB_PATH_MFMA
     assert f(eb.EB_Q8_0, eb.EB_F16, 1, 4096, 1 << 20) == eb.EB_PATH_MFMA  # x too large for LDS
-    # measured crossover: GEMV for m = 2..4 unless n is small, MFMA from m = 5
+    # measured crossover: GEMV for m = 2..4 when n >= 4096, for m = 5..8 when
+    # also k is past the narrow matrix-core kernel (k > 2048)
     assert f(eb.EB_Q4_0, eb.EB_F16, 4, 4096, 4096) == eb.EB_PATH_GEMV
     assert f(eb.EB_Q8_0, eb.EB_BF16, 4, 1024, 4096) == eb.EB_PATH_MFMA
-    assert f(eb.EB_Q4_0, eb.EB_F16, 5, 4096, 4096) == eb.EB_PATH_MFMA
-    assert f(eb.EB_Q4_0, eb.EB_F16, 8, 4096, 4096) == eb.EB_PATH_MFMA
+    assert f(eb.EB_Q8_0, eb.EB_BF16, 3, 2048, 2048) == eb.EB_PATH_MFMA
+    assert f(eb.EB_Q8_0, eb.EB_BF16, 2, 8192, 1024) == eb.EB_PATH_GEMV
+    assert f(eb.EB_Q4_0, eb.EB_F16, 5, 4096, 4096) == eb.EB_PATH_GEMV
+    assert f(eb.EB_Q4_0, eb.EB_F16, 8, 12288, 4096) == eb.EB_PATH_GEMV
+    assert f(eb.EB_Q8_0, eb.EB_BF16, 6, 8192, 1024) == eb.EB_PATH_MFMA
+    assert f(eb.EB_Q8_0, eb.EB_BF16, 8, 32768, 2048) == eb.EB_PATH_MFMA
+    assert f(eb.EB_Q4_0, eb.EB_F16, 5, 4096, 16384) == eb.EB_PATH_MFMA  # x too large for the GEMV
     assert f(eb.EB_Q8_0, eb.EB_F16, 0, 64, 64) == eb.EB_ERR_INVALID
 
 
